@@ -1,0 +1,337 @@
+/*
+ * oracle.c -- plain, slow CPU reference for the SparseSpec-L decode hot path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library.  The product path never
+ * calls it, and it shares no code with the HIP library.
+ *
+ * Everything is computed in double precision straight from the definitions in
+ * "A Sparse Glimpse of the Whole: Train-Free Self-Speculative Decoding":
+ *
+ *   verify   Sec. 3.1 (full verification as one dense attention pass that
+ *            materializes the attention weights) and Sec. 3.2 Eq. 3 (per-head
+ *            importance = attention mass received from the last W queries);
+ *   select   Sec. 3.2 Eq. 4 (sink + top-K_mid of the remaining span + recent);
+ *   draft    Sec. 3.2 Eq. 5 (attention over the gathered K/V rows);
+ *   control  Sec. 3.3 Eq. 6 (entropy EMAs), Eq. 7 (soft acceptance
+ *            probability), Eq. 8 (speculation length maximizing expected
+ *            tokens per unit cost).
+ *
+ * Readings of points the paper leaves open (all documented with the tests):
+ *   - scores are kept per KV head and summed over the query heads sharing it;
+ *   - the window is the last min(W, q) rows of the verify block, rejected
+ *     drafts included;
+ *   - the verify block is causal, bottom-right aligned: row j of q rows sees
+ *     keys 0 .. T-q+j;
+ *   - positions are 0-based; sink = [0, min(K_sink,T)), recent =
+ *     [max(T-K_recent, sink end), T), the middle span is what lies between;
+ *   - top-K ties go to the lower position; output is sorted ascending.
+ *
+ * Inputs are bf16 bit patterns (uint16) widened exactly to double.
+ * Layouts:
+ *   q       [batch][max_q][Hq][d]      verify queries
+ *   k, v    [batch][Hkv][max_ctx][d]   dense cache, head-major
+ *   out     [batch][max_q][Hq][d]      double
+ *   scores  [batch][Hkv][max_ctx]      double
+ *   idx     [batch][Hkv][budget]       int32
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+static double widen_bf16(uint16_t h)
+{
+    uint32_t u = ((uint32_t)h) << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+int oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+void oracle_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
+/*
+ * Verification attention with importance-score emission.
+ *
+ * For sequence b with T = ctx_len[b] cached tokens (the q = q_len[b] verify
+ * tokens included), verify row j (0 <= j < q) sits at position p = T - q + j.
+ * For query head h and its KV head c = h / (Hq/Hkv):
+ *     x_i = sm_scale * <q[b,j,h], k[b,c,i]>          for 0 <= i <= p
+ *     P_i = exp(x_i - max x) / sum_t exp(x_t - max x)
+ *     out[b,j,h] = sum_i P_i v[b,c,i]
+ *     scores[b,c,i] += P_i   when j is among the last min(W, q) rows.
+ * Entries of scores beyond T are left untouched; entries below T start at 0.
+ *
+ * units: optional list of (b * Hkv + c) to compute (NULL: all); lets tests
+ * evaluate a sample of a large workload.  Returns 0, or -1 on bad arguments.
+ */
+int oracle_verify(int batch, int n_q_heads, int n_kv_heads, int head_dim,
+                  int max_ctx, int max_q,
+                  const int32_t *ctx_len, const int32_t *q_len,
+                  const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                  double sm_scale, int window,
+                  const int32_t *units, int n_units,
+                  double *out, double *scores)
+{
+    if (batch < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads != 0 || head_dim < 1 ||
+        window < 1)
+        return -1;
+    for (int b = 0; b < batch; ++b)
+        if (q_len[b] < 1 || q_len[b] > max_q || ctx_len[b] < q_len[b] || ctx_len[b] > max_ctx)
+            return -1;
+    const int g = n_q_heads / n_kv_heads;
+    const int d = head_dim;
+    const int total = units ? n_units : batch * n_kv_heads;
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int u = 0; u < total; ++u) {
+        const int unit = units ? units[u] : u;
+        const int b = unit / n_kv_heads;
+        const int c = unit % n_kv_heads;
+        const int T = ctx_len[b];
+        const int nq = q_len[b];
+        const int w = window < nq ? window : nq;
+        double *S = scores + ((size_t)b * n_kv_heads + c) * max_ctx;
+        const uint16_t *kc = k + ((size_t)b * n_kv_heads + c) * max_ctx * d;
+        const uint16_t *vc = v + ((size_t)b * n_kv_heads + c) * max_ctx * d;
+        double *x = (double *)malloc(sizeof(double) * (size_t)T);
+        double *qrow = (double *)malloc(sizeof(double) * (size_t)d);
+        for (int i = 0; i < T; ++i) S[i] = 0.0;
+
+        for (int j = 0; j < nq; ++j) {
+            const int p = T - nq + j;               /* last visible key */
+            const int in_window = (j >= nq - w);
+            for (int hh = 0; hh < g; ++hh) {
+                const int h = c * g + hh;
+                const uint16_t *qs = q + (((size_t)b * max_q + j) * n_q_heads + h) * d;
+                for (int e = 0; e < d; ++e) qrow[e] = widen_bf16(qs[e]);
+
+                double m = -INFINITY;
+                for (int i = 0; i <= p; ++i) {
+                    double dot = 0.0;
+                    for (int e = 0; e < d; ++e) dot += qrow[e] * widen_bf16(kc[(size_t)i * d + e]);
+                    x[i] = sm_scale * dot;
+                    if (x[i] > m) m = x[i];
+                }
+                double L = 0.0;
+                for (int i = 0; i <= p; ++i) {
+                    x[i] = exp(x[i] - m);
+                    L += x[i];
+                }
+                double *o = out + (((size_t)b * max_q + j) * n_q_heads + h) * d;
+                for (int e = 0; e < d; ++e) o[e] = 0.0;
+                for (int i = 0; i <= p; ++i) {
+                    const double P = x[i] / L;
+                    for (int e = 0; e < d; ++e) o[e] += P * widen_bf16(vc[(size_t)i * d + e]);
+                    if (in_window) S[i] += P;
+                }
+            }
+        }
+        free(x);
+        free(qrow);
+    }
+    return 0;
+}
+
+/* Candidate for the top-K ranking: higher score first, lower position on ties. */
+typedef struct { double s; int32_t i; } cand_t;
+
+static int cand_cmp(const void *pa, const void *pb)
+{
+    const cand_t *a = (const cand_t *)pa, *b = (const cand_t *)pb;
+    if (a->s > b->s) return -1;
+    if (a->s < b->s) return 1;
+    return (a->i > b->i) - (a->i < b->i);
+}
+
+/* Number of indices Eq. 4 yields for T positions (same for every head). */
+int oracle_index_count(int T, int k_sink, int k_recent, int budget)
+{
+    const int k_mid = budget - k_sink - k_recent;
+    const int s_end = k_sink < T ? k_sink : T;
+    const int r_start = (T - k_recent) > s_end ? (T - k_recent) : s_end;
+    const int n_mid = r_start - s_end;
+    return s_end + (k_mid < n_mid ? k_mid : n_mid) + (T - r_start);
+}
+
+/*
+ * Recallable index construction (Eq. 4).  For each (b, c) with T = ctx_len[b]:
+ *   sink    = [0, min(K_sink, T))
+ *   recent  = [max(T - K_recent, end of sink), T)
+ *   mid     = the positions in between
+ *   TopK    = the min(K_mid, |mid|) mid positions of highest score,
+ *             K_mid = budget - K_sink - K_recent
+ * idx[b,c,:] = sink U TopK U recent in ascending order; n_idx[b] = its size.
+ * Slots of idx past n_idx[b] are not written.  Returns 0 or -1.
+ */
+int oracle_select(int batch, int n_kv_heads, int max_ctx, const int32_t *ctx_len,
+                  const double *scores, int k_sink, int k_recent, int budget,
+                  int32_t *idx, int32_t *n_idx)
+{
+    if (batch < 1 || n_kv_heads < 1 || k_sink < 0 || k_recent < 0 || budget < 1 ||
+        k_sink + k_recent > budget)
+        return -1;
+    for (int b = 0; b < batch; ++b)
+        if (ctx_len[b] < 1 || ctx_len[b] > max_ctx) return -1;
+    const int k_mid = budget - k_sink - k_recent;
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int u = 0; u < batch * n_kv_heads; ++u) {
+        const int b = u / n_kv_heads, c = u % n_kv_heads;
+        const int T = ctx_len[b];
+        const double *S = scores + ((size_t)b * n_kv_heads + c) * max_ctx;
+        const int s_end = k_sink < T ? k_sink : T;
+        const int r_start = (T - k_recent) > s_end ? (T - k_recent) : s_end;
+        const int n_mid = r_start - s_end;
+        const int take = k_mid < n_mid ? k_mid : n_mid;
+
+        char *keep = (char *)calloc((size_t)T, 1);
+        cand_t *cands = (cand_t *)malloc(sizeof(cand_t) * (size_t)(n_mid > 0 ? n_mid : 1));
+        for (int t = 0; t < n_mid; ++t) {
+            cands[t].s = S[s_end + t];
+            cands[t].i = s_end + t;
+        }
+        qsort(cands, (size_t)n_mid, sizeof(cand_t), cand_cmp);
+        for (int t = 0; t < take; ++t) keep[cands[t].i] = 1;
+        for (int i = 0; i < s_end; ++i) keep[i] = 1;
+        for (int i = r_start; i < T; ++i) keep[i] = 1;
+
+        int32_t *out = idx + ((size_t)b * n_kv_heads + c) * budget;
+        int n = 0;
+        for (int i = 0; i < T; ++i)
+            if (keep[i]) out[n++] = i;
+        if (c == 0) n_idx[b] = n;
+        free(keep);
+        free(cands);
+    }
+    return 0;
+}
+
+/*
+ * Draft attention over the gathered rows (Eq. 5): for sequence b, query head
+ * h, KV head c = h / g, with the n = n_idx[b] indices I = idx[b,c,0..n):
+ *     x_t = sm_scale * <q_draft[b,h], k[b,c,I_t]>,  P = softmax(x),
+ *     out[b,h] = sum_t P_t v[b,c,I_t].
+ * Layouts: q_draft / out [batch][Hq][d].  Returns 0 or -1.
+ */
+int oracle_draft(int batch, int n_q_heads, int n_kv_heads, int head_dim, int max_ctx,
+                 int budget, const int32_t *n_idx, const uint16_t *q_draft,
+                 const uint16_t *k, const uint16_t *v, const int32_t *idx,
+                 double sm_scale, double *out)
+{
+    if (batch < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads != 0 || head_dim < 1)
+        return -1;
+    for (int b = 0; b < batch; ++b)
+        if (n_idx[b] < 1 || n_idx[b] > budget) return -1;
+    const int g = n_q_heads / n_kv_heads;
+    const int d = head_dim;
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int bh = 0; bh < batch * n_q_heads; ++bh) {
+        const int b = bh / n_q_heads, h = bh % n_q_heads, c = h / g;
+        const int n = n_idx[b];
+        const int32_t *I = idx + ((size_t)b * n_kv_heads + c) * budget;
+        const uint16_t *kc = k + ((size_t)b * n_kv_heads + c) * max_ctx * d;
+        const uint16_t *vc = v + ((size_t)b * n_kv_heads + c) * max_ctx * d;
+        const uint16_t *qs = q_draft + ((size_t)b * n_q_heads + h) * d;
+        double *x = (double *)malloc(sizeof(double) * (size_t)n);
+        double m = -INFINITY;
+        for (int t = 0; t < n; ++t) {
+            double dot = 0.0;
+            for (int e = 0; e < d; ++e)
+                dot += widen_bf16(qs[e]) * widen_bf16(kc[(size_t)I[t] * d + e]);
+            x[t] = sm_scale * dot;
+            if (x[t] > m) m = x[t];
+        }
+        double L = 0.0;
+        for (int t = 0; t < n; ++t) {
+            x[t] = exp(x[t] - m);
+            L += x[t];
+        }
+        double *o = out + ((size_t)b * n_q_heads + h) * d;
+        for (int e = 0; e < d; ++e) o[e] = 0.0;
+        for (int t = 0; t < n; ++t) {
+            const double P = x[t] / L;
+            for (int e = 0; e < d; ++e) o[e] += P * widen_bf16(vc[(size_t)I[t] * d + e]);
+        }
+        free(x);
+    }
+    return 0;
+}
+
+/* ---------------------------------------------------------------------------
+ * Adaptive speculation length (Sec. 3.3).
+ * ------------------------------------------------------------------------- */
+
+/* Eq. 6: one exponential-moving-average step of a class-mean entropy. */
+double oracle_ema(double prev, double observed, double beta)
+{
+    return beta * prev + (1.0 - beta) * observed;
+}
+
+/* Eq. 7, as printed: softmax over the negative L1 distances to the centers. */
+double oracle_accept_prob(double H, double h_acc, double h_rej)
+{
+    const double ea = exp(-fabs(H - h_acc));
+    const double er = exp(-fabs(H - h_rej));
+    return ea / (ea + er);
+}
+
+/* Expected number of accepted drafts among the first k: sum_m prod_{i<=m} p_i. */
+double oracle_expected_accepted(const double *p, int k)
+{
+    double sum = 0.0;
+    for (int m = 1; m <= k; ++m) {
+        double prod = 1.0;
+        for (int i = 0; i < m; ++i) prod *= p[i];
+        sum += prod;
+    }
+    return sum;
+}
+
+/* The Eq. 8 objective: expected tokens per step over the step's cost. */
+double oracle_step_efficiency(const double *p, int k, double c_draft, double c_verify)
+{
+    return (1.0 + oracle_expected_accepted(p, k)) / ((double)k * c_draft + c_verify);
+}
+
+/*
+ * Eq. 8: k* = argmax over candidates k (with k <= n, so that p_1..p_k are
+ * known) of the objective.  Equal objectives resolve to the smaller k.
+ * Returns -1 if no candidate qualifies.
+ */
+int oracle_choose_k(const double *p, int n, const int32_t *cands, int n_cands,
+                    double c_draft, double c_verify)
+{
+    int best = -1;
+    double best_val = 0.0;
+    for (int t = 0; t < n_cands; ++t) {
+        const int k = cands[t];
+        if (k < 0 || k > n) continue;
+        const double val = oracle_step_efficiency(p, k, c_draft, c_verify);
+        if (best < 0 || val > best_val || (val == best_val && k < best)) {
+            best = k;
+            best_val = val;
+        }
+    }
+    return best;
+}

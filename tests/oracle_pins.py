@@ -1,0 +1,443 @@
+"""Pins that tie the CPU oracle to facts outside itself.
+
+Each ``pin_*`` function takes a loaded oracle library and raises
+``AssertionError`` when the oracle disagrees with:
+
+* a library routine computing the same definition independently
+  (``torch.nn.functional.scaled_dot_product_attention`` in fp64, whose GQA
+  convention is query head h -> KV head h // (Hq/Hkv); ``numpy.lexsort``);
+* a closed form (K = 0 gives uniform attention, V = 1 gives O = 1, constant
+  acceptance probability gives a geometric series, ...);
+* an invariant (probability rows sum to one, so the Eq. 3 scores of one KV
+  head sum to min(W, q) * group; index sets are sorted, unique, contain
+  sink and recent);
+* brute force on tiny inputs (every subset of the middle span).
+
+``test_oracle_pins.py`` runs them on the real oracle (all must pass) and
+``test_oracle_mutants.py`` on copies of the oracle with a planted mistake
+(at least one must fail for each mistake).
+"""
+from __future__ import annotations
+
+import itertools
+import math
+
+import numpy as np
+import torch
+import torch.nn.functional as F
+
+import oracle
+from paper_2607_27735_amd.workloads import generate, f32_to_bf16_bits
+
+
+def _bf16_to_t64(bits: np.ndarray) -> torch.Tensor:
+    """Library widening of bf16 bit patterns to float64 (torch's own bf16 type)."""
+    t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16).copy())
+    return t.view(torch.bfloat16).to(torch.float64)
+
+
+def _tiny(seed, *, hq=8, hkv=2, d=128, ctx=(40,), ql=(5,), B=16, window=16,
+          k_sink=4, k_recent=8):
+    return generate(seed, name="tiny", batch=len(ctx), n_q_heads=hq, n_kv_heads=hkv,
+                    ctx_len=list(ctx), q_len=list(ql), head_dim=d, budget=B,
+                    window=window, k_sink=k_sink, k_recent=k_recent)
+
+
+def _sdpa_verify(w, q_bits=None, k_bits=None, v_bits=None):
+    """Verify output from torch SDPA with an explicit bottom-right causal mask."""
+    q = _bf16_to_t64(w.q if q_bits is None else q_bits)
+    k = _bf16_to_t64(w.k if k_bits is None else k_bits)
+    v = _bf16_to_t64(w.v if v_bits is None else v_bits)
+    out = torch.zeros(q.shape, dtype=torch.float64)
+    for b in range(w.batch):
+        T, nq = int(w.ctx_len[b]), int(w.q_len[b])
+        qb = q[b, :nq].permute(1, 0, 2).unsqueeze(0)           # [1, Hq, nq, d]
+        kb = k[b, :, :T].unsqueeze(0)                            # [1, Hkv, T, d]
+        vb = v[b, :, :T].unsqueeze(0)
+        pos = torch.arange(T)
+        rows = torch.arange(nq) + (T - nq)
+        mask = pos[None, :] <= rows[:, None]
+        o = F.scaled_dot_product_attention(qb, kb, vb, attn_mask=mask, scale=w.sm_scale,
+                                           enable_gqa=True)
+        out[b, :nq] = o[0].permute(1, 0, 2)
+    return out.numpy()
+
+
+def _softmax_scores(w, q_bits=None, k_bits=None):
+    """Eq. 3 scores from torch.softmax weights (per KV head, summed over the group)."""
+    q = _bf16_to_t64(w.q if q_bits is None else q_bits)
+    k = _bf16_to_t64(w.k if k_bits is None else k_bits)
+    g = w.group
+    S = np.zeros((w.batch, w.n_kv_heads, w.max_ctx))
+    for b in range(w.batch):
+        T, nq = int(w.ctx_len[b]), int(w.q_len[b])
+        wn = min(w.window, nq)
+        for c in range(w.n_kv_heads):
+            qb = q[b, nq - wn:nq, c * g:(c + 1) * g, :]          # [wn, g, d]
+            logits = torch.einsum("jhd,td->jht", qb, k[b, c, :T]) * w.sm_scale
+            pos = torch.arange(T)
+            rows = torch.arange(nq - wn, nq) + (T - nq)
+            mask = pos[None, None, :] <= rows[:, None, None]
+            P = torch.softmax(logits.masked_fill(~mask, -math.inf), dim=-1)
+            S[b, c, :T] = P.sum(dim=(0, 1)).numpy()
+    return S
+
+
+# ---------------------------------------------------------------------------
+# verify: output O
+# ---------------------------------------------------------------------------
+
+def pin_verify_matches_sdpa(lib):
+    for seed, kw in [(11, {}), (12, dict(hq=4, hkv=4, ctx=(33, 20), ql=(3, 7))),
+                     (13, dict(hq=6, hkv=2, d=16, ctx=(9,), ql=(9,))),
+                     (14, dict(hq=8, hkv=1, d=32, ctx=(64, 17, 5), ql=(4, 1, 2)))]:
+        w = _tiny(seed, **kw)
+        out, _ = oracle.verify(w, lib=lib)
+        ref = _sdpa_verify(w)
+        err = np.abs(out - ref).max()
+        assert err < 1e-12, f"verify O vs SDPA (seed {seed}): {err}"
+
+
+def pin_verify_value_one(lib):
+    """V = 1 makes every output exactly 1: the probabilities of a row sum to one."""
+    w = _tiny(21, ctx=(50, 31), ql=(6, 2))
+    v = np.full_like(w.v, f32_to_bf16_bits(np.float32(1.0)))
+    out, _ = oracle.verify(w, v=v, lib=lib)
+    for b in range(w.batch):
+        nq = int(w.q_len[b])
+        assert np.abs(out[b, :nq] - 1.0).max() < 1e-12
+        assert np.all(out[b, nq:] == 0.0)
+
+
+def pin_verify_zero_keys_closed_form(lib):
+    """K = 0 makes attention uniform over the visible prefix: row j of q (position
+    p = T - q + j) outputs the mean of V rows 0..p, and the Eq. 3 score of key i
+    is group * sum over window rows with p >= i of 1 / (p + 1)."""
+    w = _tiny(22, ctx=(37, 12), ql=(5, 4), window=3)
+    k0 = np.zeros_like(w.k)
+    out, S = oracle.verify(w, k=k0, lib=lib)
+    V = _bf16_to_t64(w.v).numpy()
+    g = w.group
+    for b in range(w.batch):
+        T, nq = int(w.ctx_len[b]), int(w.q_len[b])
+        for j in range(nq):
+            p = T - nq + j
+            for h in range(w.n_q_heads):
+                ref = V[b, h // g, :p + 1].mean(axis=0)
+                assert np.abs(out[b, j, h] - ref).max() < 1e-12
+        wn = min(w.window, nq)
+        for i in range(T):
+            ref = g * sum(1.0 / (T - nq + j + 1) for j in range(nq - wn, nq) if T - nq + j >= i)
+            for c in range(w.n_kv_heads):
+                assert abs(S[b, c, i] - ref) < 1e-12, (b, c, i, S[b, c, i], ref)
+
+
+def pin_verify_planted_key(lib):
+    """A key aligned with every query at huge scale takes all the attention:
+    O equals that V row and its score equals min(W, q) * group."""
+    w = _tiny(23, hq=4, hkv=2, ctx=(30,), ql=(4,))
+    q = _bf16_to_t64(w.q).numpy()
+    k = _bf16_to_t64(w.k).numpy().copy()
+    i_star = 7
+    for c in range(w.n_kv_heads):
+        direction = q[0, :4, 2 * c:2 * c + 2].reshape(-1, w.head_dim).sum(axis=0)
+        k[0, c, i_star] = 200.0 * direction / np.linalg.norm(direction)
+    kb = f32_to_bf16_bits(k.astype(np.float32))
+    out, S = oracle.verify(w, k=kb, lib=lib)
+    V = _bf16_to_t64(w.v).numpy()
+    for j in range(4):
+        for h in range(4):
+            assert np.abs(out[0, j, h] - V[0, h // 2, i_star]).max() < 1e-6
+    for c in range(2):
+        assert abs(S[0, c, i_star] - 4 * 2) < 1e-6
+        assert S[0, c, :30].sum() - S[0, c, i_star] < 1e-6
+
+
+# ---------------------------------------------------------------------------
+# verify: scores S (Eq. 3)
+# ---------------------------------------------------------------------------
+
+def pin_scores_match_softmax(lib):
+    for seed, kw in [(31, {}), (32, dict(ctx=(45, 23), ql=(7, 3), window=4)),
+                     (33, dict(hq=12, hkv=3, d=16, ctx=(18,), ql=(18,), window=16))]:
+        w = _tiny(seed, **kw)
+        _, S = oracle.verify(w, lib=lib)
+        ref = _softmax_scores(w)
+        err = np.abs(S - ref).max()
+        assert err < 1e-12, f"scores vs torch.softmax (seed {seed}): {err}"
+
+
+def pin_scores_total_mass(lib):
+    """Each window row's probabilities sum to 1, so a KV head's scores sum to
+    min(W, q) * group; every score lies in [0, min(W, q) * group]."""
+    for window in (16, 2, 1):
+        w = _tiny(41, hq=8, hkv=2, ctx=(60, 25, 9), ql=(6, 3, 9), window=window)
+        _, S = oracle.verify(w, lib=lib)
+        for b in range(w.batch):
+            T, nq = int(w.ctx_len[b]), int(w.q_len[b])
+            wn = min(window, nq)
+            for c in range(w.n_kv_heads):
+                assert abs(S[b, c, :T].sum() - wn * w.group) < 1e-11
+                assert S[b, c, :T].min() >= 0.0
+                assert S[b, c, :T].max() <= wn * w.group + 1e-12
+                assert np.all(S[b, c, T:] == 0.0)
+
+
+def pin_scores_permutation(lib):
+    """Keys visible to every verify row are exchangeable: permuting them permutes
+    their scores and leaves the outputs unchanged."""
+    w = _tiny(42, ctx=(40,), ql=(5,))
+    T, nq = 40, 5
+    perm = np.random.default_rng(0).permutation(T - nq + 1)
+    k = w.k.copy(); v = w.v.copy()
+    k[0, :, :T - nq + 1] = w.k[0][:, perm]
+    v[0, :, :T - nq + 1] = w.v[0][:, perm]
+    out0, S0 = oracle.verify(w, lib=lib)
+    out1, S1 = oracle.verify(w, k=k, v=v, lib=lib)
+    assert np.abs(out0 - out1).max() < 1e-12
+    assert np.abs(S1[0, :, :T - nq + 1] - S0[0][:, perm]).max() < 1e-12
+    assert np.abs(S1[0, :, T - nq + 1:T] - S0[0, :, T - nq + 1:T]).max() < 1e-12
+
+
+# ---------------------------------------------------------------------------
+# select (Eq. 4)
+# ---------------------------------------------------------------------------
+
+def _spans(T, ks, kr):
+    s_end = min(ks, T)
+    r_start = max(T - kr, s_end)
+    return s_end, r_start
+
+
+def _select_lexsort(scores_row, T, ks, kr, B):
+    s_end, r_start = _spans(T, ks, kr)
+    mid = np.arange(s_end, r_start)
+    take = min(B - ks - kr, len(mid))
+    order = np.lexsort((mid, -scores_row[mid]))       # primary -score, then position
+    chosen = set(mid[order[:take]].tolist())
+    keep = sorted(set(range(s_end)) | chosen | set(range(r_start, T)))
+    return np.array(keep, dtype=np.int32)
+
+
+def _check_index_properties(row, n, S, T, ks, kr, B):
+    sel = row[:n]
+    assert np.all(np.diff(sel) > 0), "not strictly ascending"
+    assert sel.min() >= 0 and sel.max() < T
+    s_end, r_start = _spans(T, ks, kr)
+    sset = set(sel.tolist())
+    assert set(range(s_end)) <= sset and set(range(r_start, T)) <= sset
+    mid_sel = [i for i in sel if s_end <= i < r_start]
+    mid_out = [i for i in range(s_end, r_start) if i not in sset]
+    assert len(mid_sel) == min(B - ks - kr, r_start - s_end)
+    for a in mid_sel:          # defining property of TopK with the tie rule
+        for b in mid_out:
+            assert S[a] > S[b] or (S[a] == S[b] and a < b), (a, b)
+
+
+def pin_select_lexsort(lib):
+    rng = np.random.default_rng(51)
+    for T, ks, kr, B in [(40, 4, 8, 16), (200, 4, 32, 64), (37, 0, 5, 12), (64, 3, 0, 10),
+                         (500, 4, 32, 100)]:
+        batch, hkv = 2, 3
+        S = np.zeros((batch, hkv, T + 3))
+        S[:, :, :T] = rng.random((batch, hkv, T))
+        S[0, 1, 10:20] = 0.25                       # ties across the boundary
+        w = _tiny(0, hq=3, hkv=3, d=8, ctx=(T, T), ql=(1, 1), B=B, k_sink=ks, k_recent=kr)
+        idx, n_idx = oracle.select(w, S, ctx_len=np.array([T, T]), lib=lib)
+        for b in range(batch):
+            for c in range(hkv):
+                ref = _select_lexsort(S[b, c], T, ks, kr, B)
+                assert n_idx[b] == len(ref)
+                assert np.array_equal(idx[b, c, :n_idx[b]], ref), (T, b, c)
+                _check_index_properties(idx[b, c], n_idx[b], S[b, c], T, ks, kr, B)
+                assert np.all(idx[b, c, n_idx[b]:] == -1), "wrote past n_idx"
+
+
+def pin_select_bruteforce_subsets(lib):
+    """Tiny spans: among all subsets of the middle span of size K_mid, the chosen
+    one has the largest score sum, and among equal sums the smallest sorted
+    positions (integer-valued scores make ties exact)."""
+    rng = np.random.default_rng(52)
+    for trial in range(30):
+        T = int(rng.integers(6, 13)); ks, kr = 1, 2; kmid = int(rng.integers(1, 5)); B = ks + kr + kmid
+        S = np.zeros((1, 1, T))
+        S[0, 0] = rng.integers(0, 4, size=T).astype(np.float64)
+        w = _tiny(0, hq=1, hkv=1, d=8, ctx=(T,), ql=(1,), B=B, k_sink=ks, k_recent=kr)
+        idx, n_idx = oracle.select(w, S, lib=lib)
+        s_end, r_start = _spans(T, ks, kr)
+        mid = list(range(s_end, r_start))
+        take = min(kmid, len(mid))
+        best = max(itertools.combinations(mid, take),
+                   key=lambda sub: (sum(S[0, 0, i] for i in sub), [-i for i in sub]))
+        ref = sorted(set(range(s_end)) | set(best) | set(range(r_start, T)))
+        assert list(idx[0, 0, :n_idx[0]]) == ref, (S[0, 0], ref, idx[0, 0, :n_idx[0]])
+
+
+def pin_select_special_cases(lib):
+    rng = np.random.default_rng(53)
+    T = 50
+    S = np.zeros((1, 1, T)); S[0, 0] = rng.random(T)
+    w = _tiny(0, hq=1, hkv=1, d=8, ctx=(T,), ql=(1,))
+    # budget >= T: every position
+    idx, n = oracle.select(w, S, k_sink=4, k_recent=8, budget=T, lib=lib)
+    assert n[0] == T and np.array_equal(idx[0, 0, :T], np.arange(T))
+    idx, n = oracle.select(w, S, k_sink=4, k_recent=8, budget=T + 17, lib=lib)
+    assert n[0] == T and np.array_equal(idx[0, 0, :T], np.arange(T))
+    # K_mid = 0: sink and recent only
+    idx, n = oracle.select(w, S, k_sink=4, k_recent=8, budget=12, lib=lib)
+    assert list(idx[0, 0, :n[0]]) == list(range(4)) + list(range(T - 8, T))
+    # all scores equal: the lowest K_mid middle positions
+    S1 = np.ones((1, 1, T))
+    idx, n = oracle.select(w, S1, k_sink=4, k_recent=8, budget=20, lib=lib)
+    assert list(idx[0, 0, :n[0]]) == list(range(12)) + list(range(T - 8, T))
+    # T shorter than the sink
+    idx, n = oracle.select(w, S, ctx_len=np.array([3]), k_sink=4, k_recent=8, budget=20,
+                           lib=lib)
+    assert list(idx[0, 0, :n[0]]) == [0, 1, 2]
+    # recent overlapping the sink
+    idx, n = oracle.select(w, S, ctx_len=np.array([10]), k_sink=4, k_recent=8, budget=13,
+                           lib=lib)
+    assert list(idx[0, 0, :n[0]]) == list(range(10))
+    # index counts
+    for T_, ks, kr, B in [(50, 4, 8, 20), (3, 4, 8, 20), (10, 4, 8, 13), (4096, 4, 32, 256),
+                          (32768, 4, 32, 2048)]:
+        cnt = oracle.index_count(T_, ks, kr, B, lib=lib)
+        s_end, r_start = _spans(T_, ks, kr)
+        assert cnt == s_end + min(B - ks - kr, r_start - s_end) + (T_ - r_start)
+    assert oracle.index_count(32768, 4, 32, 2048, lib=lib) == 2048
+    assert oracle.index_count(100, 4, 32, 2048, lib=lib) == 100
+
+
+# ---------------------------------------------------------------------------
+# draft (Eq. 5)
+# ---------------------------------------------------------------------------
+
+def pin_draft_matches_sdpa(lib):
+    rng = np.random.default_rng(61)
+    w = _tiny(62, hq=8, hkv=2, ctx=(70, 33), ql=(1, 1), B=24)
+    idx = np.zeros((2, 2, 24), dtype=np.int32)
+    n_idx = np.array([24, 19], dtype=np.int32)
+    for b in range(2):
+        for c in range(2):
+            idx[b, c, :n_idx[b]] = np.sort(rng.choice(int(w.ctx_len[b]), n_idx[b], replace=False))
+    out = oracle.draft(w, idx, n_idx, lib=lib)
+    q = _bf16_to_t64(w.q_draft); k = _bf16_to_t64(w.k); v = _bf16_to_t64(w.v)
+    for b in range(2):
+        n = int(n_idx[b])
+        for h in range(8):
+            c = h // 4
+            I = torch.from_numpy(idx[b, c, :n].astype(np.int64))
+            o = F.scaled_dot_product_attention(q[b, h][None, None, None], k[b, c, I][None, None],
+                                               v[b, c, I][None, None], scale=w.sm_scale)
+            assert (out[b, h] - o[0, 0, 0].numpy()).__abs__().max() < 1e-12
+
+
+def pin_draft_full_equals_dense(lib):
+    """With every position selected, draft attention is dense attention: it equals
+    verify with a single query row (no causal restriction then applies)."""
+    w = _tiny(63, hq=8, hkv=2, ctx=(45,), ql=(1,), B=45)
+    T = 45
+    idx = np.arange(T, dtype=np.int32)[None, None, :].repeat(2, axis=1)
+    n_idx = np.array([T], dtype=np.int32)
+    qv = w.q.copy()
+    qv[0, 0] = w.q_draft[0]
+    out_d = oracle.draft(w, idx, n_idx, lib=lib)
+    out_v, _ = oracle.verify(w, q=qv, lib=lib)
+    assert np.abs(out_d[0] - out_v[0, 0]).max() < 1e-12
+    ref = _sdpa_verify(w, q_bits=qv)
+    assert np.abs(out_d[0] - ref[0, 0]).max() < 1e-12
+
+
+def pin_draft_permutation(lib):
+    rng = np.random.default_rng(64)
+    w = _tiny(65, hq=4, hkv=2, ctx=(60,), ql=(1,), B=20)
+    idx = np.zeros((1, 2, 20), dtype=np.int32)
+    for c in range(2):
+        idx[0, c] = rng.choice(60, 20, replace=False)
+    n_idx = np.array([20], dtype=np.int32)
+    o1 = oracle.draft(w, idx, n_idx, lib=lib)
+    o2 = oracle.draft(w, idx[:, :, ::-1].copy(), n_idx, lib=lib)
+    assert np.abs(o1 - o2).max() < 1e-12
+    # V = 1 gives 1
+    v1 = np.full_like(w.v, f32_to_bf16_bits(np.float32(1.0)))
+    o3 = oracle.draft(w, idx, n_idx, v=v1, lib=lib)
+    assert np.abs(o3 - 1.0).max() < 1e-12
+
+
+# ---------------------------------------------------------------------------
+# controller (Eq. 6-8)
+# ---------------------------------------------------------------------------
+
+def pin_controller_closed_forms(lib):
+    # Eq. 6: n identical observations from m0: m_n = beta^n m0 + (1 - beta^n) H
+    m, beta, H = 2.0, 0.9, 0.5
+    for n in range(1, 8):
+        m = oracle.ema(m, H, beta, lib=lib)
+        assert abs(m - (beta ** n * 2.0 + (1 - beta ** n) * H)) < 1e-12
+    # Eq. 7: equal distances -> 1/2; at the accepted center -> logistic of the gap
+    assert abs(oracle.accept_prob(1.0, 0.5, 1.5, lib=lib) - 0.5) < 1e-15
+    for gap in (0.1, 1.0, 3.0):
+        p = oracle.accept_prob(0.7, 0.7, 0.7 + gap, lib=lib)
+        assert abs(p - 1.0 / (1.0 + math.exp(-gap))) < 1e-12
+        p = oracle.accept_prob(0.7 + gap, 0.7, 0.7 + gap, lib=lib)
+        assert abs(p - 1.0 / (1.0 + math.exp(gap))) < 1e-12
+    # far beyond both centers the distances differ by the gap: p = 1/(1+e^{gap})
+    assert abs(oracle.accept_prob(10.0, 0.5, 1.5, lib=lib) - 1.0 / (1.0 + math.e)) < 1e-12
+    assert oracle.accept_prob(0.0, 0.5, 1.5, lib=lib) > 0.5
+    # constant p: geometric series p (1 - p^k) / (1 - p)
+    for pc in (0.3, 0.5, 0.9):
+        for k in range(0, 9):
+            e = oracle.expected_accepted([pc] * max(k, 1), k, lib=lib)
+            assert abs(e - pc * (1 - pc ** k) / (1 - pc)) < 1e-12
+    # p = 1/2: objective (2 - 2^-k) / (k Cd + Cv)
+    for k in range(1, 10):
+        v = oracle.step_efficiency([0.5] * k, k, 0.3, 2.0, lib=lib)
+        assert abs(v - (2 - 2.0 ** -k) / (k * 0.3 + 2.0)) < 1e-12
+    # p = 1: Eq. 1 with alpha = 1 (times 1/Cv): (k + 1) / (k gamma + 1)
+    for k in range(1, 10):
+        v = oracle.step_efficiency([1.0] * k, k, 0.25, 1.0, lib=lib)
+        assert abs(v - (k + 1) / (k * 0.25 + 1)) < 1e-12
+    # non-uniform prefix product
+    p = [0.9, 0.5, 0.2]
+    assert abs(oracle.expected_accepted(p, 3, lib=lib) - (0.9 + 0.45 + 0.09)) < 1e-12
+    assert abs(oracle.expected_accepted(p, 2, lib=lib) - (0.9 + 0.45)) < 1e-12
+
+
+def pin_controller_argmax(lib):
+    cands = list(range(1, 21))
+    # free drafting with positive acceptance: the longest candidate wins
+    assert oracle.choose_k([0.4] * 20, cands, 0.0, 1.0, lib=lib) == 20
+    # near-zero acceptance: the shortest candidate wins
+    assert oracle.choose_k([1e-9] * 20, cands, 0.1, 1.0, lib=lib) == 1
+    # only candidates k <= n are considered
+    assert oracle.choose_k([0.99] * 5, cands, 0.01, 1.0, lib=lib) == 5
+    assert oracle.choose_k([0.9] * 3, [4, 8], 0.0, 1.0, lib=lib) == -1
+    # exact tie (p = 0 beyond the first token, free drafting): the smaller k
+    assert oracle.choose_k([0.5, 0.0, 0.0, 0.0], [1, 2, 3, 4], 0.0, 1.0, lib=lib) == 1
+    # efficiency inversion: with constant p, extending k pays while the tail
+    # acceptance p^k exceeds the marginal cost; compare with enumeration
+    rng = np.random.default_rng(71)
+    for _ in range(50):
+        n = int(rng.integers(1, 21))
+        p = rng.random(n)
+        cd, cv = float(rng.random() * 0.5), 1.0 + float(rng.random())
+        vals = []
+        for k in cands:
+            if k <= n:
+                e = sum(float(np.prod(p[:m])) for m in range(1, k + 1))
+                vals.append(((1 + e) / (k * cd + cv), -k))
+        best = -max(vals)[1]
+        assert oracle.choose_k(list(p), cands, cd, cv, lib=lib) == best
+    # lower entropy -> larger accepted probability -> longer k (feedback direction)
+    h_acc, h_rej = 0.5, 2.5
+    p_lo = [oracle.accept_prob(0.4, h_acc, h_rej, lib=lib)] * 20
+    p_hi = [oracle.accept_prob(2.4, h_acc, h_rej, lib=lib)] * 20
+    assert oracle.choose_k(p_lo, cands, 0.05, 1.0, lib=lib) > \
+        oracle.choose_k(p_hi, cands, 0.05, 1.0, lib=lib)
+
+
+ALL_PINS = [pin_verify_matches_sdpa, pin_verify_value_one, pin_verify_zero_keys_closed_form,
+            pin_verify_planted_key, pin_scores_match_softmax, pin_scores_total_mass,
+            pin_scores_permutation, pin_select_lexsort, pin_select_bruteforce_subsets,
+            pin_select_special_cases, pin_draft_matches_sdpa, pin_draft_full_equals_dense,
+            pin_draft_permutation, pin_controller_closed_forms, pin_controller_argmax]

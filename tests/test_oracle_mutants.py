@@ -1,0 +1,89 @@
+"""The pins are strong enough: plant one plausible mistake at a time in a copy
+of the oracle's C source, build it, and require that at least one pin fails.
+
+Planted mistakes stay on the CPU, in temporary copies of the oracle.
+"""
+import os
+import subprocess
+import sys
+
+import pytest
+
+import oracle
+from oracle_pins import ALL_PINS
+
+_SRC = os.path.join(os.path.dirname(oracle.__file__), "oracle.c")
+
+# (name, text in oracle.c, replacement)
+MUTANTS = [
+    ("drop_softmax_scale", "x[i] = sm_scale * dot;", "x[i] = dot;"),
+    ("gqa_head_interleaved", "const int h = c * g + hh;", "const int h = hh * n_kv_heads + c;"),
+    ("causal_off_by_one", "const int p = T - nq + j;", "const int p = T - nq + j - 1;"),
+    ("causal_dropped", "const int p = T - nq + j;", "const int p = T - 1;"),
+    ("window_off_by_one", "(j >= nq - w)", "(j > nq - w)"),
+    ("scores_unnormalized", "if (in_window) S[i] += P;", "if (in_window) S[i] += x[i];"),
+    ("scores_first_rows", "(j >= nq - w)", "(j < w)"),
+    ("max_not_subtracted_twice", "x[i] = exp(x[i] - m);\n                    L += x[i];",
+     "x[i] = exp(x[i] - m);\n                    L += 1.0;"),
+    ("tie_to_higher_position", "return (a->i > b->i) - (a->i < b->i);",
+     "return (a->i < b->i) - (a->i > b->i);"),
+    ("ascending_scores", "if (a->s > b->s) return -1;\n    if (a->s < b->s) return 1;",
+     "if (a->s < b->s) return -1;\n    if (a->s > b->s) return 1;"),
+    ("recent_off_by_one", "const int r_start = (T - k_recent) > s_end ? (T - k_recent) : s_end;\n"
+     "        const int n_mid", "const int r_start = (T - k_recent + 1) > s_end ? "
+     "(T - k_recent + 1) : s_end;\n        const int n_mid"),
+    ("sink_not_kept", "for (int i = 0; i < s_end; ++i) keep[i] = 1;", ""),
+    ("kmid_ignores_sink", "const int k_mid = budget - k_sink - k_recent;\n\n#pragma omp parallel for"
+     " schedule(dynamic, 1)\n    for (int u = 0; u < batch * n_kv_heads; ++u) {",
+     "const int k_mid = budget - k_recent;\n\n#pragma omp parallel for schedule(dynamic, 1)\n"
+     "    for (int u = 0; u < batch * n_kv_heads; ++u) {"),
+    ("draft_head_modulo", "const int b = bh / n_q_heads, h = bh % n_q_heads, c = h / g;",
+     "const int b = bh / n_q_heads, h = bh % n_q_heads, c = h % n_kv_heads;"),
+    ("draft_drops_last_index", "for (int t = 0; t < n; ++t) {\n            double dot",
+     "for (int t = 0; t < n - 1; ++t) {\n            double dot"),
+    ("ema_weights_swapped", "return beta * prev + (1.0 - beta) * observed;",
+     "return beta * observed + (1.0 - beta) * prev;"),
+    ("accept_prob_inverted", "return ea / (ea + er);", "return er / (ea + er);"),
+    ("expected_drops_last_term", "for (int m = 1; m <= k; ++m) {", "for (int m = 1; m < k; ++m) {"),
+    ("expected_sum_not_product", "for (int i = 0; i < m; ++i) prod *= p[i];",
+     "for (int i = 0; i < m; ++i) prod = p[i];"),
+    ("objective_no_correction_token", "return (1.0 + oracle_expected_accepted(p, k))",
+     "return (oracle_expected_accepted(p, k))"),
+    ("argmax_ties_to_larger", "(val == best_val && k < best)", "(val == best_val && k > best)"),
+    ("argmax_allows_unknown_k", "if (k < 0 || k > n) continue;", "if (k < 0) continue;"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(name, old, new, tmp_path):
+    src = open(_SRC).read()
+    assert src.count(old) >= 1, f"mutation anchor for {name} not found in oracle.c"
+    mutated = src.replace(old, new, 1)
+    csrc = tmp_path / "oracle_mutant.c"
+    csrc.write_text(mutated)
+    so = tmp_path / "liboracle_mutant.so"
+    subprocess.run(["gcc", "-O1", "-fopenmp", "-fPIC", "-shared", "-std=c11", str(csrc),
+                    "-o", str(so), "-lm"], check=True)
+    # The pins run in a child process: a planted out-of-bounds write may abort it,
+    # which also counts as the mistake being caught.
+    code = (
+        "import sys, oracle\n"
+        "from oracle_pins import ALL_PINS\n"
+        f"lib = oracle.load({str(so)!r})\n"
+        "caught = []\n"
+        "for pin in ALL_PINS:\n"
+        "    try:\n"
+        "        pin(lib)\n"
+        "    except (AssertionError, ValueError, IndexError):\n"
+        "        caught.append(pin.__name__)\n"
+        "print('CAUGHT', ' '.join(caught))\n"
+        "sys.exit(0 if caught else 3)\n")
+    env = dict(os.environ)
+    here = os.path.dirname(os.path.abspath(__file__))
+    env["PYTHONPATH"] = os.pathsep.join([os.path.dirname(here), here, env.get("PYTHONPATH", "")])
+    env["OMP_NUM_THREADS"] = "2"
+    r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True,
+                       timeout=300)
+    assert r.returncode != 3, f"no pin catches the planted mistake {name}:\n{r.stdout}{r.stderr}"
+    if r.returncode == 0:
+        assert "CAUGHT" in r.stdout
