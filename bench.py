@@ -1,0 +1,233 @@
+#!/usr/bin/env python3
+"""Benchmark of one SparseSpec-L decode-step hot path (one layer) on one GPU.
+
+A step is verify attention with score emission, top-B selection and one draft
+attention step, each one call of the C ABI, over the Llama-3-8B-shaped
+32K-context workload (batch 1, 32 query / 8 KV heads, head_dim 128, k = 6,
+B = 2048, four planted heavy-hitter keys per KV head).  Inputs are seeded and
+synthetic and already resident in HBM when timing starts.
+
+Every step reads a different copy of the KV cache (enough copies that each
+step's cache was last touched more than 512 MiB earlier), so the 256 MB
+Infinity Cache cannot serve it and the numbers are HBM numbers.
+
+Prints one JSON line: µs per step (lower is better), per-call times from HIP
+events on the launch stream, the verify call against the HBM roofline, and the
+CPU oracle timed on the host's cores on the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+METRIC = "µs per verify+select+draft step and HBM GB/s (% of peak) at 32K ctx, 1 GPU"
+HBM_PEAK_GBPS = 8000.0
+
+
+def algorithmic_bytes(w, out_bytes: int):
+    """Bytes each call must move at least once (see the design notes)."""
+    hkv, hq, d = w.n_kv_heads, w.n_q_heads, w.head_dim
+    T = [int(t) for t in w.ctx_len]
+    q = [int(x) for x in w.q_len]
+    from paper_2607_27735_amd.binding import index_count
+    n = [index_count(t, w.k_sink, w.k_recent, w.budget) for t in T]
+    verify = sum(hkv * t * d * 2 * 2 + hkv * t * 4 for t in T) + \
+        sum(qb * hq * d * 2 + qb * hq * d * out_bytes for qb in q)
+    select = sum(hkv * t * 4 + hkv * nb * 4 for t, nb in zip(T, n)) + 4 * w.batch
+    draft = sum(hkv * nb * (d * 2 * 2 + 4) for nb in n) + w.batch * hq * d * (2 + out_bytes)
+    return {"verify": verify, "select": select, "draft": draft}, n
+
+
+def cpu_baseline(w, seconds: float):
+    import numpy as np
+    import oracle
+    threads = min(len(os.sched_getaffinity(0)), 16)
+    oracle.set_num_threads(threads)
+    times = []
+    t_start = time.perf_counter()
+    while True:
+        t0 = time.perf_counter()
+        _, s = oracle.verify(w)
+        idx, n_idx = oracle.select(w, s)
+        oracle.draft(w, np.maximum(idx, 0), n_idx)
+        times.append(time.perf_counter() - t0)
+        if time.perf_counter() - t_start >= seconds or len(times) >= 200:
+            break
+    units = w.batch * w.n_kv_heads
+    return {"value": statistics.median(times) * 1e6, "unit": "us/step",
+            "cores": min(threads, units), "kind": "oracle",
+            "sample": f"the full workload step (verify over all {units} KV-head units, select, "
+                      f"draft), repeated {len(times)} times; median; fp64 C, OpenMP over "
+                      f"units with {threads} threads available"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", type=int, default=2, help="named workload 1..5 (default 2)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--mode", choices=["eager", "graph"], default="graph")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (the hot path runs on one GPU; see the design "
+              f"notes for how it would shard); --gpus {args.gpus} is not supported",
+              file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+    from paper_2607_27735_amd import binding as B
+    from paper_2607_27735_amd.workloads import make_config, CONFIGS
+
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        return 1
+    B.load()
+    w = make_config(args.workload)
+    dev = torch.device("cuda:0")
+
+    def up(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16).copy()).view(
+            torch.bfloat16).to(dev)
+
+    q, qd = up(w.q), up(w.q_draft)
+    k0, v0 = up(w.k), up(w.v)
+    kv_bytes = k0.numel() * 2 * 2
+    n_copies = max(2, math.ceil((512 << 20) / kv_bytes) + 1)
+    kvs = [(k0, v0)] + [(k0.clone(), v0.clone()) for _ in range(n_copies - 1)]
+    params = B.make_params(w.sm_scale, window=w.window, k_sink=w.k_sink, k_recent=w.k_recent,
+                           budget=w.budget, out_fp32=False)
+    out = torch.empty(q.shape, dtype=torch.bfloat16, device=dev)
+    scores = torch.zeros((w.batch, w.n_kv_heads, w.max_ctx), dtype=torch.float32, device=dev)
+    idx = torch.zeros((w.batch, w.n_kv_heads, w.budget), dtype=torch.int32, device=dev)
+    n_idx = torch.zeros(w.batch, dtype=torch.int32, device=dev)
+    dout = torch.empty(qd.shape, dtype=torch.bfloat16, device=dev)
+
+    stream = torch.cuda.current_stream()
+    steps = [B.PreparedStep(q, k, v, qd, w.ctx_len, w.q_len, params, out, scores, idx, n_idx,
+                            dout, stream=stream) for (k, v) in kvs]
+    for i in range(args.warmup):
+        steps[i % n_copies].step()
+    torch.cuda.synchronize()
+
+    calls = ("verify", "select", "draft")
+    graphs = None
+    if args.mode == "graph":
+        # One graph per call and KV copy: launches replay without host
+        # marshalling, and events between replays time each call.
+        graphs = []
+        cap = torch.cuda.Stream()
+        cap.wait_stream(stream)
+        for (k, v) in kvs:
+            with torch.cuda.stream(cap):
+                st = B.PreparedStep(q, k, v, qd, w.ctx_len, w.q_len, params, out, scores, idx,
+                                    n_idx, dout, stream=cap)
+            gs = []
+            for name in calls:
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=cap):
+                    getattr(st, name)()
+                gs.append(g)
+            graphs.append(gs)
+        stream.wait_stream(cap)
+        for i in range(args.warmup):
+            for g in graphs[i % n_copies]:
+                g.replay()
+        torch.cuda.synchronize()
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        e = ev[i]
+        if graphs is not None:
+            gs = graphs[i % n_copies]
+            e[0].record(stream)
+            gs[0].replay()
+            e[1].record(stream)
+            gs[1].replay()
+            e[2].record(stream)
+            gs[2].replay()
+            e[3].record(stream)
+        else:
+            st = steps[i % n_copies]
+            e[0].record(stream)
+            st.verify()
+            e[1].record(stream)
+            st.select()
+            e[2].record(stream)
+            st.draft()
+            e[3].record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+
+    per = {c: [ev[i][j].elapsed_time(ev[i][j + 1]) * 1e3 for i in range(args.steps)]
+           for j, c in enumerate(calls)}
+    step_us = [ev[i][0].elapsed_time(ev[i][3]) * 1e3 for i in range(args.steps)]
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    nbytes, n_list = algorithmic_bytes(w, out_bytes=2)
+    kernels = {}
+    for c in calls:
+        avg = statistics.fmean(per[c])
+        kernels[c] = {"avg_us": round(avg, 3), "median_us": round(statistics.median(per[c]), 3),
+                      "p10_us": round(float(np.percentile(per[c], 10)), 3),
+                      "p90_us": round(float(np.percentile(per[c], 90)), 3),
+                      "alg_bytes": nbytes[c],
+                      "gbps": round(nbytes[c] / (avg * 1e-6) / 1e9, 1),
+                      "hbm_frac": round(nbytes[c] / (avg * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)}
+    v_avg = kernels["verify"]["avg_us"]
+    step_total = sum(nbytes.values())
+    result = {
+        "metric": METRIC,
+        "value": round(ms_per_step * 1e3, 3),
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: batch {w.batch}, {w.n_q_heads} query / "
+                               f"{w.n_kv_heads} KV heads, head_dim {w.head_dim}, context "
+                               f"{list(map(int, w.ctx_len))}, k+1 = {list(map(int, w.q_len))}, "
+                               f"B = {w.budget}, K_sink {w.k_sink}, K_recent {w.k_recent}, "
+                               f"W {w.window}",
+                   "batch": w.batch, "n_q_heads": w.n_q_heads, "n_kv_heads": w.n_kv_heads,
+                   "head_dim": w.head_dim, "ctx_len": list(map(int, w.ctx_len)),
+                   "q_len": list(map(int, w.q_len)), "budget": w.budget,
+                   "launch": args.mode, "kv_copies_rotated": n_copies},
+        "gpu_step_us_median": round(statistics.median(step_us), 3),
+        "step_alg_bytes": step_total,
+        "step_hbm_gbps": round(step_total / (ms_per_step * 1e-3) / 1e9, 1),
+        "roofline": {"bound": "hbm", "kernel": "ssl_verify_attn (verify_stats + verify_main + "
+                                               "verify_combine)",
+                     "achieved": round(nbytes["verify"] / (v_avg * 1e-6) / 1e9, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(nbytes["verify"] / (v_avg * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+                     "traffic": None, "bytes_per_launch": nbytes["verify"],
+                     "avg_launch_us": v_avg},
+        "kernels": kernels,
+    }
+    # sanity: score mass of every KV head equals min(W, q) * group
+    s = scores.double().sum(dim=2).cpu().numpy()
+    want = np.array([min(w.window, int(x)) * w.group for x in w.q_len])[:, None]
+    result["score_mass_max_rel_err"] = float(np.abs(s - want).max() / want.max())
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

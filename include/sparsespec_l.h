@@ -1,0 +1,210 @@
+/*
+ * sparsespec_l.h -- C ABI of the MI355X (gfx950) hot path of SparseSpec-L's
+ * self-speculative decode step ("A Sparse Glimpse of the Whole: Train-Free
+ * Self-Speculative Decoding").
+ *
+ * One decode iteration of the method (Sec. 3.1) drafts tokens with attention
+ * over a sparse, recallable view of the KV cache and verifies them with one
+ * dense attention pass whose attention weights are recycled into per-head
+ * importance scores.  For one layer this library provides:
+ *
+ *   ssl_verify_attn   dense verify attention of the k+1 verify rows over the
+ *                     whole cache, emitting the Eq. 3 importance scores in the
+ *                     same call (Sec. 3.1, Sec. 3.2 Eq. 3);
+ *   ssl_select_topb   the Eq. 4 index set: sink, top-K_mid of the middle span
+ *                     by score, recent (Sec. 3.2);
+ *   ssl_draft_attn    draft-step attention over the K/V rows the index set
+ *                     names, gathered on the fly (Sec. 3.2 Eq. 5);
+ *   ssl_ctrl_*        the host-side adaptive speculation-length controller
+ *                     (Sec. 3.3 Eq. 6-8); scalar, never touches the GPU.
+ *
+ * Conventions shared by every GPU entry point
+ * -------------------------------------------
+ *  - Tensors are caller-owned device buffers.  Element types: bf16 for q, k,
+ *    v and q_draft; fp32 for scores; int32 for indices; outputs bf16 or fp32
+ *    (ssl_params.out_fp32).
+ *  - Layouts (row-major, innermost last; head_dim must be 128):
+ *      q        [batch][max_q][n_q_heads][128]   verify rows of each sequence
+ *      k, v     [batch][n_kv_heads][max_ctx][128] dense cache, head-major
+ *      out      [batch][max_q][n_q_heads][128]   verify output
+ *      scores   [batch][n_kv_heads][max_ctx]     Eq. 3 importance
+ *      idx      [batch][n_kv_heads][budget]      Eq. 4 index sets
+ *      n_idx    [batch]
+ *      q_draft  [batch][n_q_heads][128], draft out the same
+ *  - ctx_len[b] counts the cached tokens of sequence b *including* its
+ *    q_len[b] verify rows, which occupy positions ctx_len-q_len .. ctx_len-1.
+ *    Verify row j attends to keys 0 .. ctx_len-q_len+j (causal, bottom-right
+ *    aligned).  Query head h reads KV head h / (n_q_heads / n_kv_heads).
+ *  - Scores are kept per KV head: the attention probability a key receives,
+ *    summed over the query heads sharing that KV head and over the last
+ *    min(window, q_len) verify rows.  Rows of each sequence therefore sum to
+ *    min(window, q_len) * (n_q_heads / n_kv_heads).
+ *  - Host arrays (ctx_len, q_len, n_idx_host) are read during the call only.
+ *  - The workspace is caller-allocated device memory of at least the size the
+ *    matching *_workspace function reports; its contents need no
+ *    initialization and are scratch after the call returns.
+ *  - Calls are asynchronous on `stream`; the library allocates nothing, keeps
+ *    no global state and never synchronizes.  Two calls that share a
+ *    workspace must be ordered on one stream.
+ *  - Every argument check happens on the host before any HIP call, so a
+ *    rejected call has no effect on the device.  Device-side data (scores,
+ *    idx) is not validated: index values outside [0, max_ctx) are clamped
+ *    (results are then meaningless but memory stays in bounds).
+ *  - Limits: head_dim 128; 1 <= batch <= 64; q_len * group <= 64;
+ *    max_q <= 64; n_q_heads / n_kv_heads <= 16 for the draft call.
+ */
+#ifndef SPARSESPEC_L_H
+#define SPARSESPEC_L_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes: every entry point returns one; no exception crosses the ABI. */
+enum {
+    SSL_OK = 0,
+    SSL_ERR_NULL = -1,        /* a required pointer is NULL */
+    SSL_ERR_SHAPE = -2,       /* inconsistent sizes (see each call) */
+    SSL_ERR_UNSUPPORTED = -3, /* valid request outside this build's limits */
+    SSL_ERR_BUDGET = -4,      /* budget < 1, k_sink/k_recent < 0 or k_sink + k_recent > budget */
+    SSL_ERR_ALIGN = -5,       /* device pointer not 16-byte (tensors) / 4-byte (int, fp32) aligned */
+    SSL_ERR_WORKSPACE = -6,   /* workspace NULL or smaller than required */
+    SSL_ERR_HIP = -7          /* a HIP launch failed (hipGetLastError after the launches) */
+};
+
+typedef struct {
+    int32_t batch;       /* sequences */
+    int32_t n_q_heads;   /* query heads; a multiple of n_kv_heads */
+    int32_t n_kv_heads;  /* KV heads */
+    int32_t head_dim;    /* must be 128 */
+    int32_t max_ctx;     /* token capacity of each (sequence, KV head) cache row */
+    int32_t max_q;       /* verify-row capacity of q and out per sequence */
+} ssl_shape;
+
+typedef struct {
+    float sm_scale;      /* logit scale, usually 1/sqrt(head_dim) */
+    int32_t window;      /* W of Eq. 3 (the paper uses 16); >= 1 */
+    int32_t k_sink;      /* K_sink of Eq. 4; >= 0 */
+    int32_t k_recent;    /* K_recent of Eq. 4; >= 0 */
+    int32_t budget;      /* K_total = K_sink + K_mid + K_recent of Eq. 4 */
+    int32_t out_fp32;    /* 1: outputs are fp32, 0: bf16 (round to nearest even) */
+} ssl_params;
+
+/* Human-readable text of a status code (static storage). */
+const char *ssl_status_string(int status);
+
+/* Number of indices Eq. 4 yields for T positions:
+ * min(k_sink,T) + min(K_mid, |middle span|) + |recent span|, where the recent
+ * span is [max(T - k_recent, min(k_sink, T)), T).  Equals T when T <= budget.
+ * Returns SSL_ERR_BUDGET / SSL_ERR_SHAPE (T < 1) on bad arguments. */
+int32_t ssl_index_count(int32_t T, int32_t k_sink, int32_t k_recent, int32_t budget);
+
+/*
+ * Verify attention with importance scores (Sec. 3.1; Sec. 3.2 Eq. 3).
+ *
+ * For each sequence b, verify row j < q_len[b], query head h (KV head c):
+ *   out[b,j,h]  = softmax_i(sm_scale * q[b,j,h].k[b,c,i]) . v[b,c,i],
+ *                 over keys i <= ctx_len[b] - q_len[b] + j;
+ *   scores[b,c,i] = sum over the last min(window, q_len[b]) rows j and the
+ *                 query heads of c of those probabilities, 0 <= i < ctx_len[b].
+ * Probabilities are computed in fp32 from bf16 inputs with fp32 accumulation;
+ * the value product uses the probabilities rounded to bf16.
+ * Writes out rows j < q_len[b] and scores entries i < ctx_len[b] only.
+ * Errors: SSL_ERR_SHAPE if n_q_heads % n_kv_heads, q_len < 1,
+ * q_len > ctx_len, ctx_len > max_ctx, q_len > max_q or max_q > 64;
+ * SSL_ERR_UNSUPPORTED if head_dim != 128, batch > 64 or q_len * group > 64.
+ */
+int ssl_verify_workspace(const ssl_shape *shape, const ssl_params *params,
+                         const int32_t *ctx_len_host, const int32_t *q_len_host,
+                         size_t *bytes_out);
+int ssl_verify_attn(const ssl_shape *shape, const ssl_params *params,
+                    const int32_t *ctx_len_host, const int32_t *q_len_host,
+                    const void *q, const void *k_cache, const void *v_cache,
+                    void *out, float *scores,
+                    void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Recallable index construction (Sec. 3.2 Eq. 4).
+ *
+ * For each (b, c) with T = ctx_len_host[b] (the committed length; scores
+ * entries 0..T-1 are read):
+ *   sink    [0, min(k_sink, T))
+ *   recent  [max(T - k_recent, min(k_sink, T)), T)
+ *   TopK    the min(K_mid, |middle|) middle positions of highest score,
+ *           K_mid = budget - k_sink - k_recent; equal scores go to the lower
+ *           position.  Scores must be non-negative and finite (as verify
+ *           writes them); comparison is exact on their fp32 values.
+ * idx[b,c,0..n) receives sink U TopK U recent in ascending order and
+ * n_idx[b] = n = ssl_index_count(T, ...); slots past n are not written.
+ * Errors: SSL_ERR_BUDGET; SSL_ERR_SHAPE if ctx_len < 1 or > max_ctx.
+ */
+int ssl_select_workspace(const ssl_shape *shape, const ssl_params *params,
+                         const int32_t *ctx_len_host, size_t *bytes_out);
+int ssl_select_topb(const ssl_shape *shape, const ssl_params *params,
+                    const int32_t *ctx_len_host, const float *scores,
+                    int32_t *idx, int32_t *n_idx,
+                    void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Draft attention over the gathered sparse view (Sec. 3.2 Eq. 5).
+ *
+ * For each b and query head h (KV head c), with n = n_idx_host[b] and
+ * I = idx[b,c,0..n):
+ *   out[b,h] = softmax_t(sm_scale * q_draft[b,h].k[b,c,I_t]) . v[b,c,I_t].
+ * K/V rows are read in place from the dense cache (never copied).  Same
+ * arithmetic as verify.  Errors: SSL_ERR_SHAPE if n < 1 or n > budget;
+ * SSL_ERR_UNSUPPORTED if the group exceeds 16.
+ */
+int ssl_draft_workspace(const ssl_shape *shape, const ssl_params *params,
+                        const int32_t *n_idx_host, size_t *bytes_out);
+int ssl_draft_attn(const ssl_shape *shape, const ssl_params *params,
+                   const int32_t *n_idx_host, const void *q_draft,
+                   const void *k_cache, const void *v_cache, const int32_t *idx,
+                   void *out, void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Adaptive speculation length (Sec. 3.3), host only.
+ *
+ * State: the class-mean entropies of accepted and rejected drafts, tracked by
+ * exponential moving averages with coefficient beta (Eq. 6).  Each class mean
+ * starts at its first observation.  Entropies are in nats.
+ */
+typedef struct ssl_ctrl ssl_ctrl;
+
+/* k_cands: the candidate set (values >= 0, copied); k_default is returned by
+ * ssl_ctrl_choose_k until both classes have been observed.  NULL on bad
+ * arguments (beta outside [0,1], n_cands < 1 or > 256, a negative candidate). */
+ssl_ctrl *ssl_ctrl_create(double beta, const int32_t *k_cands, int32_t n_cands,
+                          int32_t k_default);
+void ssl_ctrl_destroy(ssl_ctrl *ctrl);
+
+/* Eq. 6 update after one verification: H[0..n_drafted) are the draft
+ * entropies in drafting order, the first n_accepted were accepted.  The
+ * accepted class observes the mean of H[0..n_accepted), the rejected class
+ * the mean of the rest; a class with no tokens is not updated. */
+int ssl_ctrl_observe(ssl_ctrl *ctrl, const double *H, int32_t n_drafted, int32_t n_accepted);
+
+/* Eq. 7: soft acceptance probability of a draft with entropy H (0.5 while a
+ * class is still unobserved). */
+double ssl_ctrl_accept_prob(const ssl_ctrl *ctrl, double H);
+
+/* Eq. 8 over the first n draft entropies: the candidate k <= n maximizing
+ * (1 + sum_{m<=k} prod_{i<=m} p_i) / (k*c_draft + c_verify), ties to the
+ * smaller k.  Returns k_default before both classes are observed, and
+ * SSL_ERR_SHAPE if no candidate is <= n. */
+int32_t ssl_ctrl_choose_k(const ssl_ctrl *ctrl, const double *H, int32_t n,
+                          double c_draft, double c_verify);
+
+/* State access: out[0..4) = {h_acc, h_rej, seen_acc, seen_rej}. */
+int ssl_ctrl_get_state(const ssl_ctrl *ctrl, double *out4);
+int ssl_ctrl_set_state(ssl_ctrl *ctrl, const double *in4);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPARSESPEC_L_H */

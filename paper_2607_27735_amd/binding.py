@@ -1,0 +1,386 @@
+"""Python binding of the C-ABI library (argument marshalling only).
+
+Each function takes torch tensors, checks their dtype/device/shape against
+the layout the C ABI documents, and passes raw device pointers and the current
+HIP stream through ctypes.  Every step of the computation runs in the HIP
+kernels of ``libsparsespec_l.so``; there is no fallback: if the library is
+missing, or a tensor is not on a GPU, the call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsparsespec_l.so")
+
+SSL_OK = 0
+SSL_ERR_NULL = -1
+SSL_ERR_SHAPE = -2
+SSL_ERR_UNSUPPORTED = -3
+SSL_ERR_BUDGET = -4
+SSL_ERR_ALIGN = -5
+SSL_ERR_WORKSPACE = -6
+SSL_ERR_HIP = -7
+
+EXPORTED = [
+    "ssl_status_string", "ssl_index_count",
+    "ssl_verify_workspace", "ssl_verify_attn",
+    "ssl_select_workspace", "ssl_select_topb",
+    "ssl_draft_workspace", "ssl_draft_attn",
+    "ssl_ctrl_create", "ssl_ctrl_destroy", "ssl_ctrl_observe", "ssl_ctrl_accept_prob",
+    "ssl_ctrl_choose_k", "ssl_ctrl_get_state", "ssl_ctrl_set_state",
+]
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("max_ctx", ctypes.c_int32), ("max_q", ctypes.c_int32)]
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("sm_scale", ctypes.c_float), ("window", ctypes.c_int32),
+                ("k_sink", ctypes.c_int32), ("k_recent", ctypes.c_int32),
+                ("budget", ctypes.c_int32), ("out_fp32", ctypes.c_int32)]
+
+
+class SSLError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} (status {status})")
+
+
+_lib = None
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_f64p = ctypes.POINTER(ctypes.c_double)
+_vp = ctypes.c_void_p
+_sz = ctypes.c_size_t
+_szp = ctypes.POINTER(ctypes.c_size_t)
+
+
+def load(path: Optional[str] = None):
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"{p} not found: build it with `python -m paper_2607_27735_amd.build`")
+    lib = ctypes.CDLL(p)
+    sp, pp = ctypes.POINTER(Shape), ctypes.POINTER(Params)
+    lib.ssl_status_string.argtypes = [ctypes.c_int]
+    lib.ssl_status_string.restype = ctypes.c_char_p
+    lib.ssl_index_count.argtypes = [ctypes.c_int32] * 4
+    lib.ssl_index_count.restype = ctypes.c_int32
+    lib.ssl_verify_workspace.argtypes = [sp, pp, _i32p, _i32p, _szp]
+    lib.ssl_verify_attn.argtypes = [sp, pp, _i32p, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+    lib.ssl_select_workspace.argtypes = [sp, pp, _i32p, _szp]
+    lib.ssl_select_topb.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _sz, _vp]
+    lib.ssl_draft_workspace.argtypes = [sp, pp, _i32p, _szp]
+    lib.ssl_draft_attn.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+    for f in ("ssl_verify_workspace", "ssl_verify_attn", "ssl_select_workspace",
+              "ssl_select_topb", "ssl_draft_workspace", "ssl_draft_attn"):
+        getattr(lib, f).restype = ctypes.c_int
+    lib.ssl_ctrl_create.argtypes = [ctypes.c_double, _i32p, ctypes.c_int32, ctypes.c_int32]
+    lib.ssl_ctrl_create.restype = _vp
+    lib.ssl_ctrl_destroy.argtypes = [_vp]
+    lib.ssl_ctrl_destroy.restype = None
+    lib.ssl_ctrl_observe.argtypes = [_vp, _f64p, ctypes.c_int32, ctypes.c_int32]
+    lib.ssl_ctrl_observe.restype = ctypes.c_int
+    lib.ssl_ctrl_accept_prob.argtypes = [_vp, ctypes.c_double]
+    lib.ssl_ctrl_accept_prob.restype = ctypes.c_double
+    lib.ssl_ctrl_choose_k.argtypes = [_vp, _f64p, ctypes.c_int32, ctypes.c_double, ctypes.c_double]
+    lib.ssl_ctrl_choose_k.restype = ctypes.c_int32
+    lib.ssl_ctrl_get_state.argtypes = [_vp, _f64p]
+    lib.ssl_ctrl_get_state.restype = ctypes.c_int
+    lib.ssl_ctrl_set_state.argtypes = [_vp, _f64p]
+    lib.ssl_ctrl_set_state.restype = ctypes.c_int
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load().ssl_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != SSL_OK:
+        raise SSLError(status, where)
+
+
+def _host_i32(x) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(x, dtype=np.int32).reshape(-1))
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _need_gpu(*ts: torch.Tensor) -> None:
+    for t in ts:
+        if not t.is_cuda:
+            raise RuntimeError("the HIP path needs GPU tensors; there is no CPU fallback")
+        if not t.is_contiguous():
+            raise RuntimeError("tensors must be contiguous")
+
+
+def make_params(sm_scale: float, window: int = 16, k_sink: int = 4, k_recent: int = 32,
+                budget: int = 2048, out_fp32: bool = False) -> Params:
+    return Params(float(sm_scale), int(window), int(k_sink), int(k_recent), int(budget),
+                  1 if out_fp32 else 0)
+
+
+def index_count(T: int, k_sink: int, k_recent: int, budget: int) -> int:
+    return int(load().ssl_index_count(T, k_sink, k_recent, budget))
+
+
+# ---------------------------------------------------------------------------
+# verify
+# ---------------------------------------------------------------------------
+
+def verify_shape(q: torch.Tensor, k: torch.Tensor) -> Shape:
+    batch, max_q, hq, d = q.shape
+    b2, hkv, max_ctx, d2 = k.shape
+    return Shape(batch, hq, hkv, d, max_ctx, max_q)
+
+
+def verify_workspace_bytes(shape: Shape, params: Params, ctx_len, q_len) -> int:
+    ctx, ql = _host_i32(ctx_len), _host_i32(q_len)
+    n = ctypes.c_size_t(0)
+    _check(load().ssl_verify_workspace(ctypes.byref(shape), ctypes.byref(params),
+                                       ctx.ctypes.data_as(_i32p), ql.ctypes.data_as(_i32p),
+                                       ctypes.byref(n)), "ssl_verify_workspace")
+    return int(n.value)
+
+
+def verify_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, ctx_len, q_len,
+                params: Params, out: Optional[torch.Tensor] = None,
+                scores: Optional[torch.Tensor] = None,
+                workspace: Optional[torch.Tensor] = None, stream=None
+                ) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Verify attention + Eq. 3 scores.  q [B, max_q, Hq, 128] bf16, k/v
+    [B, Hkv, max_ctx, 128] bf16; returns (out, scores)."""
+    _need_gpu(q, k, v)
+    if q.dtype != torch.bfloat16 or k.dtype != torch.bfloat16 or v.dtype != torch.bfloat16:
+        raise TypeError("q, k, v must be bfloat16")
+    if k.shape != v.shape or q.shape[0] != k.shape[0] or q.shape[3] != k.shape[3]:
+        raise ValueError("q/k/v shapes disagree")
+    shape = verify_shape(q, k)
+    ctx, ql = _host_i32(ctx_len), _host_i32(q_len)
+    if len(ctx) != shape.batch or len(ql) != shape.batch:
+        raise ValueError("ctx_len / q_len need one entry per sequence")
+    odt = torch.float32 if params.out_fp32 else torch.bfloat16
+    if out is None:
+        out = torch.zeros(q.shape, dtype=odt, device=q.device)
+    if scores is None:
+        scores = torch.zeros((shape.batch, shape.n_kv_heads, shape.max_ctx), dtype=torch.float32,
+                             device=q.device)
+    _need_gpu(out, scores)
+    if out.dtype != odt or scores.dtype != torch.float32:
+        raise TypeError("out dtype must match params.out_fp32; scores must be float32")
+    if out.shape != q.shape or scores.shape != (shape.batch, shape.n_kv_heads, shape.max_ctx):
+        raise ValueError("out/scores shape")
+    need = verify_workspace_bytes(shape, params, ctx, ql)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    _check(load().ssl_verify_attn(ctypes.byref(shape), ctypes.byref(params),
+                                  ctx.ctypes.data_as(_i32p), ql.ctypes.data_as(_i32p),
+                                  _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(scores),
+                                  _ptr(workspace), workspace.numel(), _stream(stream)),
+           "ssl_verify_attn")
+    return out, scores
+
+
+# ---------------------------------------------------------------------------
+# select
+# ---------------------------------------------------------------------------
+
+def select_topb(scores: torch.Tensor, ctx_len, params: Params, n_q_heads: Optional[int] = None,
+                idx: Optional[torch.Tensor] = None, n_idx: Optional[torch.Tensor] = None,
+                stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Eq. 4 index sets from scores [B, Hkv, max_ctx] fp32; returns (idx, n_idx)
+    with idx [B, Hkv, budget] int32 (slots past n_idx[b] untouched)."""
+    _need_gpu(scores)
+    if scores.dtype != torch.float32:
+        raise TypeError("scores must be float32")
+    batch, hkv, max_ctx = scores.shape
+    shape = Shape(batch, n_q_heads or hkv, hkv, 128, max_ctx, 1)
+    ctx = _host_i32(ctx_len)
+    if idx is None:
+        idx = torch.full((batch, hkv, params.budget), -1, dtype=torch.int32, device=scores.device)
+    if n_idx is None:
+        n_idx = torch.zeros(batch, dtype=torch.int32, device=scores.device)
+    _need_gpu(idx, n_idx)
+    if idx.shape != (batch, hkv, params.budget) or idx.dtype != torch.int32:
+        raise ValueError("idx must be int32 [batch, n_kv_heads, budget]")
+    n = ctypes.c_size_t(0)
+    _check(load().ssl_select_workspace(ctypes.byref(shape), ctypes.byref(params),
+                                       ctx.ctypes.data_as(_i32p), ctypes.byref(n)),
+           "ssl_select_workspace")
+    _check(load().ssl_select_topb(ctypes.byref(shape), ctypes.byref(params),
+                                  ctx.ctypes.data_as(_i32p), _ptr(scores), _ptr(idx),
+                                  _ptr(n_idx), None, 0, _stream(stream)), "ssl_select_topb")
+    return idx, n_idx
+
+
+# ---------------------------------------------------------------------------
+# draft
+# ---------------------------------------------------------------------------
+
+def draft_workspace_bytes(shape: Shape, params: Params, n_idx_host) -> int:
+    n_idx = _host_i32(n_idx_host)
+    n = ctypes.c_size_t(0)
+    _check(load().ssl_draft_workspace(ctypes.byref(shape), ctypes.byref(params),
+                                      n_idx.ctypes.data_as(_i32p), ctypes.byref(n)),
+           "ssl_draft_workspace")
+    return int(n.value)
+
+
+def draft_attn(q_draft: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: torch.Tensor,
+               n_idx_host, params: Params, out: Optional[torch.Tensor] = None,
+               workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Eq. 5 draft attention.  q_draft [B, Hq, 128] bf16; idx [B, Hkv, budget]
+    int32; n_idx_host: per-sequence index counts on the host."""
+    _need_gpu(q_draft, k, v, idx)
+    if q_draft.dtype != torch.bfloat16 or k.dtype != torch.bfloat16 or v.dtype != torch.bfloat16:
+        raise TypeError("q_draft, k, v must be bfloat16")
+    if idx.dtype != torch.int32:
+        raise TypeError("idx must be int32")
+    batch, hq, d = q_draft.shape
+    _, hkv, max_ctx, _ = k.shape
+    shape = Shape(batch, hq, hkv, d, max_ctx, 1)
+    if idx.shape != (batch, hkv, params.budget):
+        raise ValueError("idx must be [batch, n_kv_heads, budget]")
+    n_idx = _host_i32(n_idx_host)
+    odt = torch.float32 if params.out_fp32 else torch.bfloat16
+    if out is None:
+        out = torch.zeros(q_draft.shape, dtype=odt, device=q_draft.device)
+    _need_gpu(out)
+    need = draft_workspace_bytes(shape, params, n_idx)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q_draft.device)
+    _check(load().ssl_draft_attn(ctypes.byref(shape), ctypes.byref(params),
+                                 n_idx.ctypes.data_as(_i32p), _ptr(q_draft), _ptr(k), _ptr(v),
+                                 _ptr(idx), _ptr(out), _ptr(workspace), workspace.numel(),
+                                 _stream(stream)), "ssl_draft_attn")
+    return out
+
+
+# ---------------------------------------------------------------------------
+# controller
+# ---------------------------------------------------------------------------
+
+class Controller:
+    """Eq. 6-8 speculation-length controller (host C code)."""
+
+    def __init__(self, beta: float = 0.9, candidates: Sequence[int] = tuple(range(1, 21)),
+                 k_default: int = 4):
+        c = _host_i32(list(candidates))
+        self._lib = load()
+        self._h = self._lib.ssl_ctrl_create(float(beta), c.ctypes.data_as(_i32p), len(c),
+                                            int(k_default))
+        if not self._h:
+            raise ValueError("invalid controller arguments")
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h:
+            self._lib.ssl_ctrl_destroy(h)
+            self._h = None
+
+    def observe(self, entropies: Sequence[float], n_accepted: int) -> None:
+        H = np.ascontiguousarray(np.asarray(entropies, dtype=np.float64).reshape(-1))
+        _check(self._lib.ssl_ctrl_observe(self._h, H.ctypes.data_as(_f64p), len(H),
+                                          int(n_accepted)), "ssl_ctrl_observe")
+
+    def accept_prob(self, H: float) -> float:
+        return float(self._lib.ssl_ctrl_accept_prob(self._h, float(H)))
+
+    def choose_k(self, entropies: Sequence[float], c_draft: float, c_verify: float) -> int:
+        H = np.ascontiguousarray(np.asarray(entropies, dtype=np.float64).reshape(-1))
+        if len(H) == 0:
+            H = np.zeros(1)
+            n = 0
+        else:
+            n = len(H)
+        k = int(self._lib.ssl_ctrl_choose_k(self._h, H.ctypes.data_as(_f64p), n, float(c_draft),
+                                            float(c_verify)))
+        if k < 0:
+            raise SSLError(k, "ssl_ctrl_choose_k")
+        return k
+
+    def state(self) -> Tuple[float, float, bool, bool]:
+        s = np.zeros(4)
+        _check(self._lib.ssl_ctrl_get_state(self._h, s.ctypes.data_as(_f64p)), "ssl_ctrl_get_state")
+        return float(s[0]), float(s[1]), bool(s[2]), bool(s[3])
+
+    def set_state(self, h_acc: float, h_rej: float, seen_acc: bool, seen_rej: bool) -> None:
+        s = np.array([h_acc, h_rej, float(seen_acc), float(seen_rej)], dtype=np.float64)
+        _check(self._lib.ssl_ctrl_set_state(self._h, s.ctypes.data_as(_f64p)), "ssl_ctrl_set_state")
+
+
+# ---------------------------------------------------------------------------
+# Prepared step: marshalling done once, each call is a single C-ABI call.
+# ---------------------------------------------------------------------------
+
+class PreparedStep:
+    """One verify + select + draft step over fixed device buffers.
+
+    All argument structures are built once, so each ``verify()`` /
+    ``select()`` / ``draft()`` is one ctypes call into the library on the
+    stream given (default: torch's current stream at construction).
+    """
+
+    def __init__(self, q, k, v, q_draft, ctx_len, q_len, params: Params, out, scores, idx, n_idx,
+                 draft_out, stream=None):
+        self._lib = load()
+        _need_gpu(q, k, v, q_draft, out, scores, idx, n_idx, draft_out)
+        self.shape = verify_shape(q, k)
+        self.params = params
+        self.ctx = _host_i32(ctx_len)
+        self.ql = _host_i32(q_len)
+        self.n_idx_host = np.array([index_count(int(t), params.k_sink, params.k_recent,
+                                                params.budget) for t in self.ctx], dtype=np.int32)
+        self.dshape = Shape(self.shape.batch, self.shape.n_q_heads, self.shape.n_kv_heads,
+                            self.shape.head_dim, self.shape.max_ctx, 1)
+        vws = verify_workspace_bytes(self.shape, params, self.ctx, self.ql)
+        dws = draft_workspace_bytes(self.dshape, params, self.n_idx_host)
+        self.vws = torch.empty(max(vws, 1), dtype=torch.uint8, device=q.device)
+        self.dws = torch.empty(max(dws, 1), dtype=torch.uint8, device=q.device)
+        self.tensors = (q, k, v, q_draft, out, scores, idx, n_idx, draft_out)
+        self.stream = _stream(stream)
+        sp, pp = ctypes.byref(self.shape), ctypes.byref(params)
+        cp, qp = self.ctx.ctypes.data_as(_i32p), self.ql.ctypes.data_as(_i32p)
+        self._v = (sp, pp, cp, qp, q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                   scores.data_ptr(), self.vws.data_ptr(), self.vws.numel(), self.stream)
+        self._s = (sp, pp, cp, scores.data_ptr(), idx.data_ptr(), n_idx.data_ptr(), None, 0,
+                   self.stream)
+        self._d = (ctypes.byref(self.dshape), pp, self.n_idx_host.ctypes.data_as(_i32p),
+                   q_draft.data_ptr(), k.data_ptr(), v.data_ptr(), idx.data_ptr(),
+                   draft_out.data_ptr(), self.dws.data_ptr(), self.dws.numel(), self.stream)
+
+    def verify(self) -> None:
+        _check(self._lib.ssl_verify_attn(*self._v), "ssl_verify_attn")
+
+    def select(self) -> None:
+        _check(self._lib.ssl_select_topb(*self._s), "ssl_select_topb")
+
+    def draft(self) -> None:
+        _check(self._lib.ssl_draft_attn(*self._d), "ssl_draft_attn")
+
+    def step(self) -> None:
+        self.verify()
+        self.select()
+        self.draft()

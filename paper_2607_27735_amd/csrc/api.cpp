@@ -1,0 +1,302 @@
+// api.cpp -- the C ABI: argument validation, work decomposition, launches.
+//
+// Every check runs on the host before the first HIP call, so a rejected call
+// leaves the device untouched and is testable without a GPU.
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "../../include/sparsespec_l.h"
+#include "launch.h"
+
+using namespace ssl;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int kVerifyRowCap = 64;
+constexpr int kDraftRowCap = 16;
+constexpr int kDraftChunk = 64;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int check_shape(const ssl_shape* s) {
+    if (!s) return SSL_ERR_NULL;
+    if (s->batch < 1 || s->n_q_heads < 1 || s->n_kv_heads < 1 || s->max_ctx < 1 || s->max_q < 1)
+        return SSL_ERR_SHAPE;
+    if (s->n_q_heads % s->n_kv_heads != 0) return SSL_ERR_SHAPE;
+    if (s->head_dim != 128) return SSL_ERR_UNSUPPORTED;
+    if (s->batch > kTableBatch) return SSL_ERR_UNSUPPORTED;
+    return SSL_OK;
+}
+
+int check_budget(const ssl_params* p) {
+    if (!p) return SSL_ERR_NULL;
+    if (p->budget < 1 || p->k_sink < 0 || p->k_recent < 0) return SSL_ERR_BUDGET;
+    if ((int64_t)p->k_sink + p->k_recent > p->budget) return SSL_ERR_BUDGET;
+    return SSL_OK;
+}
+
+// Verify work decomposition: items are (sequence, KV head, key chunk).
+struct VerifyPlan {
+    int chunk, n_items, n_rows, row_tiles;
+    size_t ml_off, o_off, bytes;
+    SeqTable seq;
+};
+
+int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, const int32_t* ql,
+                VerifyPlan* plan) {
+    int rc = check_shape(s);
+    if (rc) return rc;
+    if (!p) return SSL_ERR_NULL;
+    if (!ctx || !ql) return SSL_ERR_NULL;
+    if (s->max_q > 64) return SSL_ERR_SHAPE;
+    if (p->window < 1 || !(p->sm_scale > 0.f) || !isfinite(p->sm_scale)) return SSL_ERR_SHAPE;
+    const int g = s->n_q_heads / s->n_kv_heads;
+    int64_t total_keys = 0;
+    int max_rows = 0;
+    for (int b = 0; b < s->batch; ++b) {
+        if (ql[b] < 1 || ql[b] > ctx[b] || ctx[b] > s->max_ctx || ql[b] > s->max_q)
+            return SSL_ERR_SHAPE;
+        max_rows = std::max(max_rows, ql[b] * g);
+        total_keys += (int64_t)ctx[b] * s->n_kv_heads;
+    }
+    if (max_rows > kVerifyRowCap) return SSL_ERR_UNSUPPORTED;
+
+    // Chunk: a power of two in [128, 2048] giving about one item per CU.
+    int chunk = 128;
+    while (chunk < 2048 && (int64_t)chunk * 256 < total_keys) chunk *= 2;
+    memset(&plan->seq, 0, sizeof plan->seq);
+    plan->seq.n_seq = s->batch;
+    int64_t items = 0, rows = 0;
+    for (int b = 0; b < s->batch; ++b) {
+        plan->seq.item_start[b] = (int32_t)items;
+        plan->seq.row_start[b] = (int32_t)rows;
+        plan->seq.ctx[b] = ctx[b];
+        plan->seq.qlen[b] = ql[b];
+        items += (int64_t)s->n_kv_heads * ((ctx[b] + chunk - 1) / chunk);
+        rows += (int64_t)s->n_kv_heads * ql[b] * g;
+    }
+    if (items > (1 << 30) || rows > (1 << 30)) return SSL_ERR_UNSUPPORTED;
+    plan->seq.item_start[s->batch] = (int32_t)items;
+    plan->seq.row_start[s->batch] = (int32_t)rows;
+    plan->chunk = chunk;
+    plan->n_items = (int)items;
+    plan->n_rows = (int)rows;
+    plan->row_tiles = (max_rows + 15) / 16;
+    plan->ml_off = 0;
+    plan->o_off = align_up((size_t)items * kVerifyRowCap * sizeof(float) * 2);
+    plan->bytes = plan->o_off + align_up((size_t)items * kVerifyRowCap * 128 * sizeof(float));
+    return SSL_OK;
+}
+
+struct DraftPlan {
+    int chunk, n_items, n_rows;
+    size_t ml_off, o_off, bytes;
+    SeqTable seq;
+};
+
+int plan_draft(const ssl_shape* s, const ssl_params* p, const int32_t* n_idx, DraftPlan* plan) {
+    int rc = check_shape(s);
+    if (rc) return rc;
+    rc = check_budget(p);
+    if (rc) return rc;
+    if (!n_idx) return SSL_ERR_NULL;
+    if (!(p->sm_scale > 0.f) || !isfinite(p->sm_scale)) return SSL_ERR_SHAPE;
+    const int g = s->n_q_heads / s->n_kv_heads;
+    if (g > kDraftRowCap) return SSL_ERR_UNSUPPORTED;
+    memset(&plan->seq, 0, sizeof plan->seq);
+    plan->seq.n_seq = s->batch;
+    const int chunk = kDraftChunk;
+    int64_t items = 0;
+    for (int b = 0; b < s->batch; ++b) {
+        if (n_idx[b] < 1 || n_idx[b] > p->budget) return SSL_ERR_SHAPE;
+        plan->seq.item_start[b] = (int32_t)items;
+        plan->seq.ctx[b] = n_idx[b];
+        items += (int64_t)s->n_kv_heads * ((n_idx[b] + chunk - 1) / chunk);
+    }
+    if (items > (1 << 30)) return SSL_ERR_UNSUPPORTED;
+    plan->seq.item_start[s->batch] = (int32_t)items;
+    plan->chunk = chunk;
+    plan->n_items = (int)items;
+    plan->n_rows = s->batch * s->n_q_heads;
+    plan->ml_off = 0;
+    plan->o_off = align_up((size_t)items * kDraftRowCap * sizeof(float) * 2);
+    plan->bytes = plan->o_off + align_up((size_t)items * kDraftRowCap * 128 * sizeof(float));
+    return SSL_OK;
+}
+
+int check_select(const ssl_shape* s, const ssl_params* p, const int32_t* ctx) {
+    int rc = check_shape(s);
+    if (rc) return rc;
+    rc = check_budget(p);
+    if (rc) return rc;
+    if (!ctx) return SSL_ERR_NULL;
+    for (int b = 0; b < s->batch; ++b)
+        if (ctx[b] < 1 || ctx[b] > s->max_ctx) return SSL_ERR_SHAPE;
+    return SSL_OK;
+}
+
+int check_workspace(const void* ws, size_t have, size_t need) {
+    if (need == 0) return SSL_OK;
+    if (!ws || have < need) return SSL_ERR_WORKSPACE;
+    if (!aligned(ws, 16)) return SSL_ERR_ALIGN;
+    return SSL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ssl_status_string(int status) {
+    switch (status) {
+        case SSL_OK: return "ok";
+        case SSL_ERR_NULL: return "a required pointer is NULL";
+        case SSL_ERR_SHAPE: return "inconsistent shape, length or parameter";
+        case SSL_ERR_UNSUPPORTED: return "request outside the supported limits";
+        case SSL_ERR_BUDGET: return "invalid budget: need budget >= 1, k_sink, k_recent >= 0, k_sink + k_recent <= budget";
+        case SSL_ERR_ALIGN: return "device pointer is not suitably aligned";
+        case SSL_ERR_WORKSPACE: return "workspace missing or too small";
+        case SSL_ERR_HIP: return "HIP kernel launch failed";
+        default: return "unknown status";
+    }
+}
+
+int32_t ssl_index_count(int32_t T, int32_t k_sink, int32_t k_recent, int32_t budget) {
+    if (budget < 1 || k_sink < 0 || k_recent < 0 || (int64_t)k_sink + k_recent > budget)
+        return SSL_ERR_BUDGET;
+    if (T < 1) return SSL_ERR_SHAPE;
+    const int32_t k_mid = budget - k_sink - k_recent;
+    const int32_t s_end = std::min(k_sink, T);
+    const int32_t r_start = std::max(T - k_recent, s_end);
+    return s_end + std::min(k_mid, r_start - s_end) + (T - r_start);
+}
+
+int ssl_verify_workspace(const ssl_shape* shape, const ssl_params* params,
+                         const int32_t* ctx_len_host, const int32_t* q_len_host, size_t* bytes_out) {
+    if (!bytes_out) return SSL_ERR_NULL;
+    VerifyPlan plan;
+    const int rc = plan_verify(shape, params, ctx_len_host, q_len_host, &plan);
+    if (rc) return rc;
+    *bytes_out = plan.bytes;
+    return SSL_OK;
+}
+
+int ssl_verify_attn(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
+                    const int32_t* q_len_host, const void* q, const void* k_cache,
+                    const void* v_cache, void* out, float* scores, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream) {
+    VerifyPlan plan;
+    int rc = plan_verify(shape, params, ctx_len_host, q_len_host, &plan);
+    if (rc) return rc;
+    if (!q || !k_cache || !v_cache || !out || !scores) return SSL_ERR_NULL;
+    if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16) ||
+        !aligned(scores, 4))
+        return SSL_ERR_ALIGN;
+    rc = check_workspace(workspace, workspace_bytes, plan.bytes);
+    if (rc) return rc;
+
+    VerifyArgs a;
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k_cache);
+    a.v = static_cast<const uint16_t*>(v_cache);
+    a.part_ml = reinterpret_cast<float2*>(static_cast<char*>(workspace) + plan.ml_off);
+    a.part_o = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.o_off);
+    a.scores = scores;
+    a.out = out;
+    a.n_q_heads = shape->n_q_heads;
+    a.n_kv_heads = shape->n_kv_heads;
+    a.group = shape->n_q_heads / shape->n_kv_heads;
+    a.max_ctx = shape->max_ctx;
+    a.max_q = shape->max_q;
+    a.window = params->window;
+    a.chunk = plan.chunk;
+    a.out_fp32 = params->out_fp32 ? 1 : 0;
+    a.scale_log2 = params->sm_scale * 1.4426950408889634f;
+    a.seq = plan.seq;
+    return launch_verify(a, plan.n_items, plan.n_rows, plan.row_tiles, stream) == hipSuccess
+               ? SSL_OK
+               : SSL_ERR_HIP;
+}
+
+int ssl_select_workspace(const ssl_shape* shape, const ssl_params* params,
+                         const int32_t* ctx_len_host, size_t* bytes_out) {
+    if (!bytes_out) return SSL_ERR_NULL;
+    const int rc = check_select(shape, params, ctx_len_host);
+    if (rc) return rc;
+    *bytes_out = 0;
+    return SSL_OK;
+}
+
+int ssl_select_topb(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
+                    const float* scores, int32_t* idx, int32_t* n_idx, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream) {
+    int rc = check_select(shape, params, ctx_len_host);
+    if (rc) return rc;
+    if (!scores || !idx || !n_idx) return SSL_ERR_NULL;
+    if (!aligned(scores, 4) || !aligned(idx, 4) || !aligned(n_idx, 4)) return SSL_ERR_ALIGN;
+    rc = check_workspace(workspace, workspace_bytes, 0);
+    if (rc) return rc;
+    SelectArgs a;
+    memset(&a, 0, sizeof a);
+    a.scores = scores;
+    a.idx = idx;
+    a.n_idx = n_idx;
+    a.n_kv_heads = shape->n_kv_heads;
+    a.max_ctx = shape->max_ctx;
+    a.k_sink = params->k_sink;
+    a.k_recent = params->k_recent;
+    a.budget = params->budget;
+    a.batch = shape->batch;
+    for (int b = 0; b < shape->batch; ++b) a.ctx[b] = ctx_len_host[b];
+    return launch_select(a, shape->batch * shape->n_kv_heads, stream) == hipSuccess ? SSL_OK
+                                                                                   : SSL_ERR_HIP;
+}
+
+int ssl_draft_workspace(const ssl_shape* shape, const ssl_params* params,
+                        const int32_t* n_idx_host, size_t* bytes_out) {
+    if (!bytes_out) return SSL_ERR_NULL;
+    DraftPlan plan;
+    const int rc = plan_draft(shape, params, n_idx_host, &plan);
+    if (rc) return rc;
+    *bytes_out = plan.bytes;
+    return SSL_OK;
+}
+
+int ssl_draft_attn(const ssl_shape* shape, const ssl_params* params, const int32_t* n_idx_host,
+                   const void* q_draft, const void* k_cache, const void* v_cache,
+                   const int32_t* idx, void* out, void* workspace, size_t workspace_bytes,
+                   hipStream_t stream) {
+    DraftPlan plan;
+    int rc = plan_draft(shape, params, n_idx_host, &plan);
+    if (rc) return rc;
+    if (!q_draft || !k_cache || !v_cache || !idx || !out) return SSL_ERR_NULL;
+    if (!aligned(q_draft, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) ||
+        !aligned(out, 16) || !aligned(idx, 4))
+        return SSL_ERR_ALIGN;
+    rc = check_workspace(workspace, workspace_bytes, plan.bytes);
+    if (rc) return rc;
+    DraftArgs a;
+    a.q = static_cast<const uint16_t*>(q_draft);
+    a.k = static_cast<const uint16_t*>(k_cache);
+    a.v = static_cast<const uint16_t*>(v_cache);
+    a.idx = idx;
+    a.part_ml = reinterpret_cast<float2*>(static_cast<char*>(workspace) + plan.ml_off);
+    a.part_o = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.o_off);
+    a.out = out;
+    a.n_q_heads = shape->n_q_heads;
+    a.n_kv_heads = shape->n_kv_heads;
+    a.group = shape->n_q_heads / shape->n_kv_heads;
+    a.max_ctx = shape->max_ctx;
+    a.budget = params->budget;
+    a.chunk = plan.chunk;
+    a.out_fp32 = params->out_fp32 ? 1 : 0;
+    a.scale_log2 = params->sm_scale * 1.4426950408889634f;
+    a.seq = plan.seq;
+    return launch_draft(a, plan.n_items, plan.n_rows, stream) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
+}
+
+}  // extern "C"

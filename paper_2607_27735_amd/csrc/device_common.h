@@ -1,0 +1,86 @@
+// device_common.h -- CDNA4 (gfx950) building blocks shared by the kernels.
+//
+// Wave64 throughout.  Matrix products use the gfx950 bf16 MFMA
+// v_mfma_f32_16x16x32_bf16: A is 16(M) x 32(K), B is 32(K) x 16(N), fp32
+// 16x16 accumulator.  Lane l supplies A row (l & 15) and B column (l & 15),
+// each as 8 consecutive K elements starting at 8 * (l >> 4); it receives
+// accumulator column (l & 15), rows 4 * (l >> 4) + 0..3.  Because a lane's
+// 8 K elements only need to agree between A and B, the kernels are free to
+// map K slots to keys or to head-dim elements in whatever order makes their
+// global loads contiguous.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ssl {
+
+constexpr int kHeadDim = 128;
+constexpr int kWave = 64;
+constexpr int kMaxBatch = 64;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// Two fp32 values -> packed bf16 pair (round to nearest even), lo in bits 0-15.
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+    f32x2 v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __builtin_bit_cast(float, w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __builtin_bit_cast(float, w & 0xffff0000u); }
+
+// Low halves of x and y packed as (x.lo, y.lo); high halves as (x.hi, y.hi).
+__device__ __forceinline__ uint32_t perm_lo(uint32_t x, uint32_t y) {
+    return __builtin_amdgcn_perm(y, x, 0x05040100u);
+}
+__device__ __forceinline__ uint32_t perm_hi(uint32_t x, uint32_t y) {
+    return __builtin_amdgcn_perm(y, x, 0x07060302u);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+// Row rotation inside each 16-lane DPP row.
+template <int N>
+__device__ __forceinline__ float row_ror(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+        0, __builtin_bit_cast(int, x), 0x120 + N, 0xf, 0xf, false));
+}
+
+// Sum over the 16 lanes of a DPP row; every lane of the row gets the total.
+__device__ __forceinline__ float row16_sum(float x) {
+    x += row_ror<8>(x);
+    x += row_ror<4>(x);
+    x += row_ror<2>(x);
+    x += row_ror<1>(x);
+    return x;
+}
+
+__device__ __forceinline__ float shfl_xor_f(float x, int mask) {
+    return __shfl_xor(x, mask, kWave);
+}
+
+// Merge of two online-softmax summaries in the log2 domain: (M, L) absorbs
+// (m, l), where L = sum 2^(y - M).  Empty summaries carry M = -inf, L = 0.
+__device__ __forceinline__ void ml_merge(float& M, float& L, float m, float l) {
+    const float Mn = fmaxf(M, m);
+    if (Mn == -INFINITY) return;
+    L = L * fast_exp2(M - Mn) + l * fast_exp2(m - Mn);
+    M = Mn;
+}
+
+__device__ __forceinline__ u32x4 ld_u32x4(const uint16_t* p) {
+    return *reinterpret_cast<const u32x4*>(p);
+}
+
+}  // namespace ssl

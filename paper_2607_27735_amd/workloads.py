@@ -5,9 +5,11 @@ method's arithmetic (no attention, no scores, no selection), so both the HIP
 path and the CPU oracle may consume what it produces.
 
 Every tensor is drawn in fp32 from ``numpy.random.default_rng(seed)`` (PCG64)
-in a fixed order -- context lengths, speculation lengths, verify queries, K, V,
-draft queries, then the structure draws -- the structure is applied in fp32,
-and the result is rounded to bfloat16 (round to nearest, ties to even).
+in a fixed order -- context lengths, speculation lengths, the structure draws
+(planted positions, rank permutations), verify queries, K and V (one
+(sequence, KV head) slice after another, ``max_ctx`` rows each), draft
+queries -- the structure is applied to K in fp32, and every value is rounded
+to bfloat16 (round to nearest, ties to even).
 Tensors are returned as ``uint16`` bf16 bit patterns:
 
 * ``q``        ``[batch][max_q][n_q_heads][head_dim]``: the k+1 verify rows of
@@ -33,6 +35,14 @@ from typing import Dict, Optional, Sequence
 
 import numpy as np
 
+try:
+    # Large fresh arrays are faulted in far faster without numpy's huge-page
+    # advice on some hosts; the values drawn are unaffected.
+    from numpy._core.multiarray import _set_madvise_hugepage
+    _set_madvise_hugepage(False)
+except Exception:  # pragma: no cover - older/newer numpy layouts
+    pass
+
 HEAD_DIM = 128
 DEFAULT_WINDOW = 16        # Sec. 3.2: aggregation window W
 DEFAULT_K_SINK = 4         # reading: the paper gives no value
@@ -40,11 +50,15 @@ DEFAULT_K_RECENT = 32      # reading: the paper gives no value
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
-    """Round fp32 values to bf16 (nearest, ties to even); returns uint16 bits."""
-    x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-    return u.astype(np.uint16)
+    """Round fp32 values to bf16 (nearest, ties to even); returns uint16 bits.
+
+    Uses torch's CPU conversion (same rounding as the integer recipe
+    ``(u + 0x7FFF + ((u >> 16) & 1)) >> 16`` on the fp32 bit pattern ``u``,
+    which the tests check) because it is much faster on large arrays.
+    """
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return t.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
 
 
 def bf16_bits_to_f32(h: np.ndarray) -> np.ndarray:
@@ -127,60 +141,67 @@ def generate(seed: int, *, name: str, batch: int, n_q_heads: int, n_kv_heads: in
     if max_q is None:
         max_q = int(ql.max())
     hq, hkv, d = n_q_heads, n_kv_heads, head_dim
+    g = hq // hkv
+    sm_scale = 1.0 / math.sqrt(d)
+
+    # Structure draws come first so that K can be drawn, shaped and rounded one
+    # (sequence, KV head) slice at a time.
+    structure: Dict[str, object] = {}
+    heavy = None
+    if heavy_hitters > 0:
+        # Planted high-norm key rows at seeded distinct positions of the span
+        # that top-B selection ranks (after the sink, before the recent tail).
+        heavy = np.zeros((batch, hkv, heavy_hitters), dtype=np.int64)
+        for b in range(batch):
+            lo, hi = k_sink, int(ctx[b]) - k_recent
+            for c in range(hkv):
+                heavy[b, c] = np.sort(rng.choice(hi - lo, size=heavy_hitters, replace=False) + lo)
+        structure["heavy_positions"] = heavy
+    ranks = None
+    if zipf_s is not None:
+        # Power-law attention profile: a seeded random rank per position.
+        ranks = np.zeros((batch, hkv, max_ctx), dtype=np.int64)
+        for b in range(batch):
+            for c in range(hkv):
+                ranks[b, c, :ctx[b]] = rng.permutation(int(ctx[b])) + 1
+        structure["zipf_ranks"] = ranks
+        structure["zipf_s"] = zipf_s
 
     q = _normal(rng, (batch, max_q, hq, d))
     for b in range(batch):
         q[b, ql[b]:] = 0.0
     q_bits = f32_to_bf16_bits(q)
     del q
+    qf = bf16_bits_to_f32(q_bits)
 
-    k = _normal(rng, (batch, hkv, max_ctx, d))
-    v = _normal(rng, (batch, hkv, max_ctx, d))
-    qd = _normal(rng, (batch, hq, d))
-
-    structure: Dict[str, object] = {}
-    sm_scale = 1.0 / math.sqrt(d)
-    if heavy_hitters > 0:
-        # Planted high-norm key rows at seeded distinct positions of the span
-        # that top-B selection ranks (after the sink, before the recent tail).
-        pos = np.zeros((batch, hkv, heavy_hitters), dtype=np.int64)
-        for b in range(batch):
-            lo, hi = k_sink, int(ctx[b]) - k_recent
-            for c in range(hkv):
-                p = rng.choice(hi - lo, size=heavy_hitters, replace=False) + lo
-                pos[b, c] = np.sort(p)
-                k[b, c, pos[b, c]] *= np.float32(heavy_scale)
-        structure["heavy_positions"] = pos
-    if zipf_s is not None:
-        # Power-law attention profile: per KV head, a seeded random rank per
-        # position and a key shift along the mean verify-query direction so
-        # that the logit of that mean query moves by -s*ln(rank).
-        qf = bf16_bits_to_f32(q_bits)
-        g = hq // hkv
-        ranks = np.zeros((batch, hkv, max_ctx), dtype=np.int64)
-        for b in range(batch):
-            T = int(ctx[b])
-            for c in range(hkv):
+    k_bits = np.empty((batch, hkv, max_ctx, d), dtype=np.uint16)
+    v_bits = np.empty((batch, hkv, max_ctx, d), dtype=np.uint16)
+    buf = np.empty((max_ctx, d), dtype=np.float32)
+    for b in range(batch):
+        T = int(ctx[b])
+        for c in range(hkv):
+            rng.standard_normal(out=buf, dtype=np.float32)
+            if heavy is not None:
+                buf[heavy[b, c]] *= np.float32(heavy_scale)
+            if ranks is not None:
+                # shift keys along the mean verify-query direction u so that the
+                # logit of that mean query moves by -s * ln(rank)
                 rows = qf[b, :ql[b], c * g:(c + 1) * g, :].reshape(-1, d).astype(np.float64)
                 qbar = rows.mean(axis=0)
                 nrm = float(np.linalg.norm(qbar))
                 u = qbar / nrm
-                r = rng.permutation(T) + 1
-                ranks[b, c, :T] = r
-                bias = -zipf_s * np.log(r.astype(np.float64))
+                bias = -zipf_s * np.log(ranks[b, c, :T].astype(np.float64))
                 shift = (bias / (sm_scale * nrm))[:, None] * u[None, :]
-                k[b, c, :T] = (k[b, c, :T].astype(np.float64) + shift).astype(np.float32)
-        structure["zipf_ranks"] = ranks
-        structure["zipf_s"] = zipf_s
-
+                buf[:T] = (buf[:T].astype(np.float64) + shift).astype(np.float32)
+            buf[T:] = 0.0
+            k_bits[b, c] = f32_to_bf16_bits(buf)
     for b in range(batch):
-        k[b, :, ctx[b]:] = 0.0
-        v[b, :, ctx[b]:] = 0.0
-    k_bits = f32_to_bf16_bits(k)
-    del k
-    v_bits = f32_to_bf16_bits(v)
-    del v
-    qd_bits = f32_to_bf16_bits(qd)
+        T = int(ctx[b])
+        for c in range(hkv):
+            rng.standard_normal(out=buf, dtype=np.float32)
+            buf[T:] = 0.0
+            v_bits[b, c] = f32_to_bf16_bits(buf)
+    qd_bits = f32_to_bf16_bits(_normal(rng, (batch, hq, d)))
 
     return Workload(name=name, batch=batch, n_q_heads=hq, n_kv_heads=hkv, head_dim=d,
                     max_ctx=int(max_ctx), max_q=int(max_q), ctx_len=ctx, q_len=ql,
