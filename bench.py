@@ -74,7 +74,7 @@ def main() -> int:
     ap.add_argument("--workload", type=int, default=2, help="named workload 1..5 (default 2)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=["eager", "graph"], default="graph")
+    ap.add_argument("--mode", choices=["eager", "graph"], default="eager")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the hot path runs on one GPU; see the design "
@@ -110,6 +110,12 @@ def main() -> int:
     idx = torch.zeros((w.batch, w.n_kv_heads, w.budget), dtype=torch.int32, device=dev)
     n_idx = torch.zeros(w.batch, dtype=torch.int32, device=dev)
     dout = torch.empty(qd.shape, dtype=torch.bfloat16, device=dev)
+
+    vshape = B.Shape(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.max_ctx, w.max_q)
+    schedule, vchunk, vitems = B.verify_plan(vshape, params, w.ctx_len, w.q_len)
+    sched_name = "one-sweep" if schedule == B.VERIFY_ONE_SWEEP else "two-sweep"
+    verify_kernels = ("zero_u32_kernel + verify_fused_kernel" if schedule == B.VERIFY_ONE_SWEEP
+                      else "verify_stats_kernel + verify_main_kernel + verify_combine_kernel")
 
     stream = torch.cuda.current_stream()
     steps = [B.PreparedStep(q, k, v, qd, w.ctx_len, w.q_len, params, out, scores, idx, n_idx,
@@ -206,12 +212,13 @@ def main() -> int:
                    "batch": w.batch, "n_q_heads": w.n_q_heads, "n_kv_heads": w.n_kv_heads,
                    "head_dim": w.head_dim, "ctx_len": list(map(int, w.ctx_len)),
                    "q_len": list(map(int, w.q_len)), "budget": w.budget,
-                   "launch": args.mode, "kv_copies_rotated": n_copies},
+                   "launch": args.mode, "kv_copies_rotated": n_copies,
+                   "verify_schedule": sched_name, "verify_chunk": vchunk,
+                   "verify_items": vitems},
         "gpu_step_us_median": round(statistics.median(step_us), 3),
         "step_alg_bytes": step_total,
         "step_hbm_gbps": round(step_total / (ms_per_step * 1e-3) / 1e9, 1),
-        "roofline": {"bound": "hbm", "kernel": "ssl_verify_attn (verify_stats + verify_main + "
-                                               "verify_combine)",
+        "roofline": {"bound": "hbm", "kernel": f"ssl_verify_attn ({verify_kernels})",
                      "achieved": round(nbytes["verify"] / (v_avg * 1e-6) / 1e9, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(nbytes["verify"] / (v_avg * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),

@@ -92,7 +92,19 @@ typedef struct {
     int32_t k_recent;    /* K_recent of Eq. 4; >= 0 */
     int32_t budget;      /* K_total = K_sink + K_mid + K_recent of Eq. 4 */
     int32_t out_fp32;    /* 1: outputs are fp32, 0: bf16 (round to nearest even) */
+    int32_t verify_mode; /* SSL_VERIFY_AUTO, SSL_VERIFY_TWO_SWEEP or SSL_VERIFY_ONE_SWEEP */
 } ssl_params;
+
+/* How ssl_verify_attn schedules its work (results agree to rounding):
+ *  AUTO       currently the two-sweep schedule (the faster one on MI355X:
+ *             the one-sweep schedule pays for a cooperative launch and a
+ *             cross-workgroup barrier);
+ *  TWO_SWEEP  a K-only pass for the row statistics, then a K+V pass;
+ *  ONE_SWEEP  a single K+V pass; SSL_ERR_UNSUPPORTED when it does not fit
+ *             (at most 128 (sequence, KV head) pairs and 256 work items; an
+ *             item holds at most 2176 / 1024 / 640 / 384 keys for up to
+ *             16 / 32 / 48 / 64 verify rows per KV head). */
+enum { SSL_VERIFY_AUTO = 0, SSL_VERIFY_TWO_SWEEP = 1, SSL_VERIFY_ONE_SWEEP = 2 };
 
 /* Human-readable text of a status code (static storage). */
 const char *ssl_status_string(int status);
@@ -115,12 +127,22 @@ int32_t ssl_index_count(int32_t T, int32_t k_sink, int32_t k_recent, int32_t bud
  * the value product uses the probabilities rounded to bf16.
  * Writes out rows j < q_len[b] and scores entries i < ctx_len[b] only.
  * Errors: SSL_ERR_SHAPE if n_q_heads % n_kv_heads, q_len < 1,
- * q_len > ctx_len, ctx_len > max_ctx, q_len > max_q or max_q > 64;
- * SSL_ERR_UNSUPPORTED if head_dim != 128, batch > 64 or q_len * group > 64.
+ * q_len > ctx_len, ctx_len > max_ctx, q_len > max_q, max_q > 64, window < 1,
+ * sm_scale not positive and finite, or verify_mode unknown;
+ * SSL_ERR_UNSUPPORTED if head_dim != 128, batch > 64, q_len * group > 64, or
+ * a one-sweep request that does not fit.  The workspace size covers both
+ * schedules.
  */
 int ssl_verify_workspace(const ssl_shape *shape, const ssl_params *params,
                          const int32_t *ctx_len_host, const int32_t *q_len_host,
                          size_t *bytes_out);
+/* The schedule ssl_verify_attn would use for these arguments: *schedule_out
+ * = SSL_VERIFY_ONE_SWEEP or SSL_VERIFY_TWO_SWEEP (one sweep still falls back
+ * to two if the device refuses the co-resident launch), *chunk_out = keys per
+ * work item, *items_out = work items (each one workgroup).  Host only. */
+int ssl_verify_plan(const ssl_shape *shape, const ssl_params *params,
+                    const int32_t *ctx_len_host, const int32_t *q_len_host,
+                    int32_t *schedule_out, int32_t *chunk_out, int32_t *items_out);
 int ssl_verify_attn(const ssl_shape *shape, const ssl_params *params,
                     const int32_t *ctx_len_host, const int32_t *q_len_host,
                     const void *q, const void *k_cache, const void *v_cache,

@@ -27,9 +27,13 @@ SSL_ERR_ALIGN = -5
 SSL_ERR_WORKSPACE = -6
 SSL_ERR_HIP = -7
 
+VERIFY_AUTO = 0
+VERIFY_TWO_SWEEP = 1
+VERIFY_ONE_SWEEP = 2
+
 EXPORTED = [
     "ssl_status_string", "ssl_index_count",
-    "ssl_verify_workspace", "ssl_verify_attn",
+    "ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn",
     "ssl_select_workspace", "ssl_select_topb",
     "ssl_draft_workspace", "ssl_draft_attn",
     "ssl_ctrl_create", "ssl_ctrl_destroy", "ssl_ctrl_observe", "ssl_ctrl_accept_prob",
@@ -46,7 +50,8 @@ class Shape(ctypes.Structure):
 class Params(ctypes.Structure):
     _fields_ = [("sm_scale", ctypes.c_float), ("window", ctypes.c_int32),
                 ("k_sink", ctypes.c_int32), ("k_recent", ctypes.c_int32),
-                ("budget", ctypes.c_int32), ("out_fp32", ctypes.c_int32)]
+                ("budget", ctypes.c_int32), ("out_fp32", ctypes.c_int32),
+                ("verify_mode", ctypes.c_int32)]
 
 
 class SSLError(RuntimeError):
@@ -79,11 +84,12 @@ def load(path: Optional[str] = None):
     lib.ssl_index_count.restype = ctypes.c_int32
     lib.ssl_verify_workspace.argtypes = [sp, pp, _i32p, _i32p, _szp]
     lib.ssl_verify_attn.argtypes = [sp, pp, _i32p, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+    lib.ssl_verify_plan.argtypes = [sp, pp, _i32p, _i32p, _i32p, _i32p, _i32p]
     lib.ssl_select_workspace.argtypes = [sp, pp, _i32p, _szp]
     lib.ssl_select_topb.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _sz, _vp]
     lib.ssl_draft_workspace.argtypes = [sp, pp, _i32p, _szp]
     lib.ssl_draft_attn.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
-    for f in ("ssl_verify_workspace", "ssl_verify_attn", "ssl_select_workspace",
+    for f in ("ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn", "ssl_select_workspace",
               "ssl_select_topb", "ssl_draft_workspace", "ssl_draft_attn"):
         getattr(lib, f).restype = ctypes.c_int
     lib.ssl_ctrl_create.argtypes = [ctypes.c_double, _i32p, ctypes.c_int32, ctypes.c_int32]
@@ -137,9 +143,9 @@ def _need_gpu(*ts: torch.Tensor) -> None:
 
 
 def make_params(sm_scale: float, window: int = 16, k_sink: int = 4, k_recent: int = 32,
-                budget: int = 2048, out_fp32: bool = False) -> Params:
+                budget: int = 2048, out_fp32: bool = False, verify_mode: int = VERIFY_AUTO) -> Params:
     return Params(float(sm_scale), int(window), int(k_sink), int(k_recent), int(budget),
-                  1 if out_fp32 else 0)
+                  1 if out_fp32 else 0, int(verify_mode))
 
 
 def index_count(T: int, k_sink: int, k_recent: int, budget: int) -> int:
@@ -163,6 +169,17 @@ def verify_workspace_bytes(shape: Shape, params: Params, ctx_len, q_len) -> int:
                                        ctx.ctypes.data_as(_i32p), ql.ctypes.data_as(_i32p),
                                        ctypes.byref(n)), "ssl_verify_workspace")
     return int(n.value)
+
+
+def verify_plan(shape: Shape, params: Params, ctx_len, q_len) -> Tuple[int, int, int]:
+    """(schedule, keys per item, items) that verify_attn would use."""
+    ctx, ql = _host_i32(ctx_len), _host_i32(q_len)
+    sch, ch, it = ctypes.c_int32(0), ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(load().ssl_verify_plan(ctypes.byref(shape), ctypes.byref(params),
+                                  ctx.ctypes.data_as(_i32p), ql.ctypes.data_as(_i32p),
+                                  ctypes.byref(sch), ctypes.byref(ch), ctypes.byref(it)),
+           "ssl_verify_plan")
+    return int(sch.value), int(ch.value), int(it.value)
 
 
 def verify_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, ctx_len, q_len,

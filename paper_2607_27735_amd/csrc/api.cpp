@@ -40,11 +40,19 @@ int check_budget(const ssl_params* p) {
     return SSL_OK;
 }
 
-// Verify work decomposition: items are (sequence, KV head, key chunk).
+// Verify work decomposition.  Two-sweep items are (sequence, KV head, key
+// chunk); the one-sweep schedule uses the same kind of items ("slots"), all
+// resident at once.  The workspace holds per-item row statistics and partial
+// outputs for whichever schedule needs more, plus the arrival counters.
+constexpr int kFusedMaxSlots = 256;
+
 struct VerifyPlan {
     int chunk, n_items, n_rows, row_tiles;
-    size_t ml_off, o_off, bytes;
+    bool fused_ok;
+    int fused_chunk, fused_slots, n_units;
+    size_t ml_off, o_off, arrive_off, bytes;
     SeqTable seq;
+    FusedTable ft;
 };
 
 int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, const int32_t* ql,
@@ -55,6 +63,8 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
     if (!ctx || !ql) return SSL_ERR_NULL;
     if (s->max_q > 64) return SSL_ERR_SHAPE;
     if (p->window < 1 || !(p->sm_scale > 0.f) || !isfinite(p->sm_scale)) return SSL_ERR_SHAPE;
+    if (p->verify_mode < SSL_VERIFY_AUTO || p->verify_mode > SSL_VERIFY_ONE_SWEEP)
+        return SSL_ERR_SHAPE;
     const int g = s->n_q_heads / s->n_kv_heads;
     int64_t total_keys = 0;
     int max_rows = 0;
@@ -65,8 +75,9 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
         total_keys += (int64_t)ctx[b] * s->n_kv_heads;
     }
     if (max_rows > kVerifyRowCap) return SSL_ERR_UNSUPPORTED;
+    plan->row_tiles = (max_rows + 15) / 16;
 
-    // Chunk: a power of two in [128, 2048] giving about one item per CU.
+    // Two-sweep chunk: a power of two in [128, 2048] giving about one item per CU.
     int chunk = 128;
     while (chunk < 2048 && (int64_t)chunk * 256 < total_keys) chunk *= 2;
     memset(&plan->seq, 0, sizeof plan->seq);
@@ -86,10 +97,48 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
     plan->chunk = chunk;
     plan->n_items = (int)items;
     plan->n_rows = (int)rows;
-    plan->row_tiles = (max_rows + 15) / 16;
+
+    // One-sweep: the smallest multiple of 128 keys that keeps every slot
+    // resident (one workgroup per CU), if it fits the LDS logit stash.
+    const int64_t units = (int64_t)s->batch * s->n_kv_heads;
+    plan->n_units = (int)units;
+    plan->fused_ok = false;
+    plan->fused_slots = 0;
+    plan->fused_chunk = 0;
+    const int cap = fused_max_chunk(plan->row_tiles);
+    if (units <= kFusedMaxUnits && cap >= 128) {
+        for (int fc = 128; fc <= cap; fc += 128) {
+            int64_t slots = 0;
+            for (int b = 0; b < s->batch; ++b)
+                slots += (int64_t)s->n_kv_heads * ((ctx[b] + fc - 1) / fc);
+            if (slots <= kFusedMaxSlots) {
+                plan->fused_ok = true;
+                plan->fused_chunk = fc;
+                plan->fused_slots = (int)slots;
+                break;
+            }
+        }
+    }
+    if (p->verify_mode == SSL_VERIFY_ONE_SWEEP && !plan->fused_ok) return SSL_ERR_UNSUPPORTED;
+    if (plan->fused_ok) {
+        memset(&plan->ft, 0, sizeof plan->ft);
+        plan->ft.n_units = (int)units;
+        plan->ft.chunk = plan->fused_chunk;
+        int slot = 0;
+        for (int b = 0; b < s->batch; ++b)
+            for (int c = 0; c < s->n_kv_heads; ++c) {
+                const int u = b * s->n_kv_heads + c;
+                plan->ft.unit[u] = u;
+                plan->ft.slot_start[u] = slot;
+                slot += (ctx[b] + plan->fused_chunk - 1) / plan->fused_chunk;
+            }
+        plan->ft.slot_start[units] = slot;
+    }
+    const size_t slots_max = (size_t)std::max(plan->n_items, plan->fused_slots);
     plan->ml_off = 0;
-    plan->o_off = align_up((size_t)items * kVerifyRowCap * sizeof(float) * 2);
-    plan->bytes = plan->o_off + align_up((size_t)items * kVerifyRowCap * 128 * sizeof(float));
+    plan->o_off = align_up(slots_max * kVerifyRowCap * sizeof(float) * 2);
+    plan->arrive_off = plan->o_off + align_up(slots_max * kVerifyRowCap * 128 * sizeof(float));
+    plan->bytes = plan->arrive_off + align_up((size_t)kFusedMaxUnits * sizeof(uint32_t));
     return SSL_OK;
 }
 
@@ -185,6 +234,20 @@ int ssl_verify_workspace(const ssl_shape* shape, const ssl_params* params,
     return SSL_OK;
 }
 
+int ssl_verify_plan(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
+                    const int32_t* q_len_host, int32_t* schedule_out, int32_t* chunk_out,
+                    int32_t* items_out) {
+    if (!schedule_out || !chunk_out || !items_out) return SSL_ERR_NULL;
+    VerifyPlan plan;
+    const int rc = plan_verify(shape, params, ctx_len_host, q_len_host, &plan);
+    if (rc) return rc;
+    const bool one = plan.fused_ok && params->verify_mode == SSL_VERIFY_ONE_SWEEP;
+    *schedule_out = one ? SSL_VERIFY_ONE_SWEEP : SSL_VERIFY_TWO_SWEEP;
+    *chunk_out = one ? plan.fused_chunk : plan.chunk;
+    *items_out = one ? plan.fused_slots : plan.n_items;
+    return SSL_OK;
+}
+
 int ssl_verify_attn(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
                     const int32_t* q_len_host, const void* q, const void* k_cache,
                     const void* v_cache, void* out, float* scores, void* workspace,
@@ -217,6 +280,16 @@ int ssl_verify_attn(const ssl_shape* shape, const ssl_params* params, const int3
     a.out_fp32 = params->out_fp32 ? 1 : 0;
     a.scale_log2 = params->sm_scale * 1.4426950408889634f;
     a.seq = plan.seq;
+    if (plan.fused_ok && params->verify_mode == SSL_VERIFY_ONE_SWEEP) {
+        FusedArgs fa;
+        fa.v = a;
+        fa.arrive = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + plan.arrive_off);
+        fa.ft = plan.ft;
+        const hipError_t e = launch_verify_fused(fa, plan.fused_slots, plan.row_tiles, stream);
+        if (e == hipSuccess) return SSL_OK;
+        (void)hipGetLastError();   // the refused cooperative launch ran nothing
+        if (params->verify_mode == SSL_VERIFY_ONE_SWEEP) return SSL_ERR_HIP;
+    }
     return launch_verify(a, plan.n_items, plan.n_rows, plan.row_tiles, stream) == hipSuccess
                ? SSL_OK
                : SSL_ERR_HIP;

@@ -48,24 +48,21 @@ struct Gathered {
     u32x4 v[8];
 };
 
-__device__ __forceinline__ int cache_row(const int32_t* ib, int pos, int last, int max_ctx) {
-    const int r = ib[min(pos, last)];
-    return min(max(r, 0), max_ctx - 1);
-}
-
-__device__ __forceinline__ void gather_tile(const DraftArgs& a, const int32_t* ib, int pos0, int last,
-                                            const uint16_t* kbase, const uint16_t* vbase, int m16,
-                                            int G, Gathered& t) {
+// Gathers the K and V rows of the 32-key tile starting at chunk position p0.
+// Lane l of the wave holds the cache row of chunk position l in `my_row`;
+// the rows each lane needs are fetched from their owners by lane shuffles.
+__device__ __forceinline__ void gather_tile(int my_row, int p0, const uint16_t* kbase,
+                                            const uint16_t* vbase, int m16, int G, Gathered& t) {
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-        const int row = cache_row(ib, pos0 + 16 * h + a_row_key(m16), last, a.max_ctx);
+        const int row = __shfl(my_row, p0 + 16 * h + a_row_key(m16), kWave);
         const uint16_t* p = kbase + (size_t)row * kHeadDim + 8 * G;
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) t.k[h][kb] = ld_u32x4(p + 32 * kb);
     }
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-        const int row = cache_row(ib, pos0 + 16 * (e >> 2) + G + 4 * (e & 3), last, a.max_ctx);
+        const int row = __shfl(my_row, p0 + 16 * (e >> 2) + G + 4 * (e & 3), kWave);
         t.v[e] = ld_u32x4(vbase + (size_t)row * kHeadDim + 8 * m16);
     }
 }
@@ -148,20 +145,15 @@ __global__ __launch_bounds__(kWave) void draft_kernel(DraftArgs a) {
 #pragma unroll
     for (int jd = 0; jd < 8; ++jd) oacc[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int ntile = (it.key_end - it.key_begin + kTile - 1) / kTile;
+    // One chunk is two 32-key tiles: lane l loads the cache row of chunk
+    // position l once, then every K/V row of both tiles is requested at once.
+    const int my_row = min(max(ib[min(it.key_begin + lane, last)], 0), a.max_ctx - 1);
     Gathered ta, tb;
-    int tt = 0;
-    gather_tile(a, ib, it.key_begin, last, kbase, vbase, m16, G, ta);
-    for (;;) {
-        int tn = tt + 1 < ntile ? tt + 1 : tt;
-        gather_tile(a, ib, it.key_begin + tn * kTile, last, kbase, vbase, m16, G, tb);
-        draft_tile(a, qop, ta, it.key_begin + tt * kTile, it.key_end, G, M, L, oacc);
-        if (++tt >= ntile) break;
-        tn = tt + 1 < ntile ? tt + 1 : tt;
-        gather_tile(a, ib, it.key_begin + tn * kTile, last, kbase, vbase, m16, G, ta);
-        draft_tile(a, qop, tb, it.key_begin + tt * kTile, it.key_end, G, M, L, oacc);
-        if (++tt >= ntile) break;
-    }
+    gather_tile(my_row, 0, kbase, vbase, m16, G, ta);
+    gather_tile(my_row, kTile, kbase, vbase, m16, G, tb);
+    draft_tile(a, qop, ta, it.key_begin, it.key_end, G, M, L, oacc);
+    if (it.key_begin + kTile < it.key_end)
+        draft_tile(a, qop, tb, it.key_begin + kTile, it.key_end, G, M, L, oacc);
     L += shfl_xor_f(L, 16);
     L += shfl_xor_f(L, 32);
 
@@ -176,7 +168,13 @@ __global__ __launch_bounds__(kWave) void draft_kernel(DraftArgs a) {
     }
 }
 
-__global__ __launch_bounds__(kHeadDim) void draft_combine_kernel(DraftArgs a) {
+// Combine of one query head's partials.  256 threads: thread t handles
+// head-dim quad t % 32 for the items t / 32, t / 32 + 8, ..., merging them
+// online; the eight partial states are then merged in a fixed order.
+constexpr int kCombineThreads = 256;
+constexpr int kCombineGroups = kCombineThreads / 32;
+
+__global__ __launch_bounds__(kCombineThreads) void draft_combine_kernel(DraftArgs a) {
     const SeqTable& st = a.seq;
     const int bh = blockIdx.x;
     const int b = bh / a.n_q_heads;
@@ -185,29 +183,68 @@ __global__ __launch_bounds__(kHeadDim) void draft_combine_kernel(DraftArgs a) {
     const int row = h - c * a.group;
     const int nchunk = (st.ctx[b] + a.chunk - 1) / a.chunk;
     const int item0 = st.item_start[b] + c * nchunk;
-    float M = -INFINITY;
-    for (int s = 0; s < nchunk; ++s) M = fmaxf(M, a.part_ml[(size_t)(item0 + s) * kRowCap + row].x);
-    float L = 0.f, acc = 0.f;
-    const int d = threadIdx.x;
-    for (int s = 0; s < nchunk; ++s) {
-        const float2 ml = a.part_ml[(size_t)(item0 + s) * kRowCap + row];
-        const float w = fast_exp2(ml.x - M);
-        L += ml.y * w;
-        acc += a.part_o[((size_t)(item0 + s) * kRowCap + row) * kHeadDim + d] * w;
+    const int d4 = threadIdx.x & 31, sg = threadIdx.x >> 5;
+    const f32x4* po = reinterpret_cast<const f32x4*>(a.part_o);
+    float M = -INFINITY, L = 0.f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s0 = sg; s0 < nchunk; s0 += 8 * kCombineGroups) {
+        float2 ml[8];
+        f32x4 o[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int s = s0 + u * kCombineGroups;
+            const bool ok = s < nchunk;
+            const size_t slot = (size_t)(item0 + (ok ? s : 0)) * kRowCap + row;
+            ml[u] = ok ? a.part_ml[slot] : make_float2(-INFINITY, 0.f);
+            o[u] = ok ? po[slot * (kHeadDim / 4) + d4] : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        float Mn = M;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) Mn = fmaxf(Mn, ml[u].x);
+        const float alpha = fast_exp2(M - Mn);   // M = -inf at first: 0
+        L *= alpha;
+        acc *= alpha;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const float wgt = fast_exp2(ml[u].x - Mn);   // empty slots: 0
+            L += ml[u].y * wgt;
+            acc += o[u] * wgt;
+        }
+        M = Mn;
     }
-    const float o = acc / L;
-    const size_t oi = ((size_t)b * a.n_q_heads + h) * kHeadDim + d;
-    if (a.out_fp32)
-        reinterpret_cast<float*>(a.out)[oi] = o;
-    else
-        reinterpret_cast<__bf16*>(a.out)[oi] = (__bf16)o;
+    __shared__ f32x4 racc[kCombineGroups][32];
+    __shared__ float2 rml[kCombineGroups][32];
+    racc[sg][d4] = acc;
+    rml[sg][d4] = make_float2(M, L);
+    __syncthreads();
+    if (sg != 0) return;
+    float Mx = -INFINITY;
+#pragma unroll
+    for (int gq = 0; gq < kCombineGroups; ++gq) Mx = fmaxf(Mx, rml[gq][d4].x);
+    float Lx = 0.f;
+    f32x4 ox = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int gq = 0; gq < kCombineGroups; ++gq) {
+        const float2 m = rml[gq][d4];
+        const float wgt = m.x == -INFINITY ? 0.f : fast_exp2(m.x - Mx);
+        Lx += m.y * wgt;
+        ox += racc[gq][d4] * wgt;
+    }
+    ox *= 1.0f / Lx;
+    const size_t base = ((size_t)b * a.n_q_heads + h) * kHeadDim + 4 * d4;
+    if (a.out_fp32) {
+        *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out) + base) = ox;
+    } else {
+        uint2 pk = make_uint2(pack_bf16(ox[0], ox[1]), pack_bf16(ox[2], ox[3]));
+        *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + base) = pk;
+    }
 }
 
 }  // namespace
 
 hipError_t launch_draft(const DraftArgs& a, int n_items, int n_rows_total, hipStream_t stream) {
     hipLaunchKernelGGL(draft_kernel, dim3(n_items), dim3(kWave), 0, stream, a);
-    hipLaunchKernelGGL(draft_combine_kernel, dim3(n_rows_total), dim3(kHeadDim), 0, stream, a);
+    hipLaunchKernelGGL(draft_combine_kernel, dim3(n_rows_total), dim3(kCombineThreads), 0, stream, a);
     return hipGetLastError();
 }
 

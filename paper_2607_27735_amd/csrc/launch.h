@@ -55,9 +55,34 @@ struct DraftArgs {
     SeqTable seq;           // ctx[] holds n_idx per sequence
 };
 
+// Single-sweep verify: every work item of the launch is resident at once
+// (cooperative launch), items of KV-head unit u are slots
+// [slot_start[u], slot_start[u + 1]), each covering `chunk` keys.
+constexpr int kFusedMaxUnits = 128;
+
+struct FusedTable {
+    int32_t n_units;
+    int32_t chunk;
+    int32_t unit[kFusedMaxUnits];            // b * n_kv_heads + c
+    int32_t slot_start[kFusedMaxUnits + 1];
+};
+
+struct FusedArgs {
+    VerifyArgs v;           // part_ml / part_o are indexed by slot
+    uint32_t* arrive;       // [n_units] arrival counters, zero at launch
+    FusedTable ft;
+};
+
 // Launchers return hipSuccess or the error of the launch.
 hipError_t launch_verify(const VerifyArgs& a, int n_items, int n_rows_total, int row_tiles,
                          hipStream_t stream);
+// Zeroes the arrival counters, then launches the single-sweep kernel as a
+// cooperative grid of n_slots workgroups.  Returns the launch error (for
+// instance when the grid cannot be co-resident; nothing has run then except
+// the counter fill).
+hipError_t launch_verify_fused(const FusedArgs& a, int n_slots, int row_tiles, hipStream_t stream);
+// Largest key chunk the single-sweep kernel can hold in LDS for row_tiles.
+int fused_max_chunk(int row_tiles);
 hipError_t launch_select(const SelectArgs& a, int n_units, hipStream_t stream);
 hipError_t launch_draft(const DraftArgs& a, int n_items, int n_rows_total, hipStream_t stream);
 

@@ -23,21 +23,12 @@
 // all query heads of a KV head, 12..64 rows, form a genuine 16-row-tiled
 // contraction); P.V runs on the MFMA as O^T = V^T P^T so that every row's
 // softmax state and output stay in the lane that owns the row.
-#include "device_common.h"
-#include "launch.h"
+#include "verify_common.h"
 
 namespace ssl {
 namespace {
 
-constexpr int kThreads = 256;  // 4 waves
-constexpr int kWaves = 4;
-constexpr int kTile = 32;      // keys per wave step
-constexpr int kRowCap = 64;    // rows per item slot in the workspace
-
-// Tile-local key assigned to A row m of a 16-key half tile.  The accumulator
-// rows lane group G receives are 4G + i, which then hold keys G + 4i: the same
-// keys lane group G loads as full 256-byte rows for the V^T operand.
-__device__ __forceinline__ int a_row_key(int m) { return (m >> 2) + 4 * (m & 3); }
+using namespace vc;
 
 struct Item {
     int b, c, s, nchunk, T, nq, key_begin, key_end, unit, item0;
@@ -59,81 +50,6 @@ __device__ __forceinline__ Item decode_item(const SeqTable& st, int item, int n_
     it.unit = b * n_kv + it.c;
     it.item0 = st.item_start[b] + it.c * it.nchunk;
     return it;
-}
-
-// The verify rows a lane owns: row rt*16 + (lane & 15) of each row tile.
-template <int NRT>
-struct Rows {
-    int plim[NRT];      // last key the row may see; -1 for padding rows
-    bool inwin[NRT];    // row contributes to the scores
-    u32x4 q[NRT][4];    // B operand (Q^T): row's head-dim slice per 32-wide k-block
-};
-
-template <int NRT>
-__device__ __forceinline__ void load_rows(const VerifyArgs& a, const Item& it, int m16, int G,
-                                          Rows<NRT>& r) {
-    const int g = a.group;
-    const int R = it.nq * g;
-    const int wn = min(a.window, it.nq);
-#pragma unroll
-    for (int rt = 0; rt < NRT; ++rt) {
-        const int row = rt * 16 + m16;
-        if (row < R) {
-            const int j = row / g;
-            const int hh = row - j * g;
-            r.plim[rt] = it.T - it.nq + j;
-            r.inwin[rt] = j >= it.nq - wn;
-            const uint16_t* qp = a.q + (((size_t)it.b * a.max_q + j) * a.n_q_heads + it.c * g + hh) *
-                                           kHeadDim + 8 * G;
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb) r.q[rt][kb] = ld_u32x4(qp + 32 * kb);
-        } else {
-            r.plim[rt] = -1;
-            r.inwin[rt] = false;
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb) r.q[rt][kb] = u32x4{0u, 0u, 0u, 0u};
-        }
-    }
-}
-
-// K operand of a 32-key tile: lane (m16, G) holds key a_row_key(m16) (+16 for
-// the second half) and head-dim elements 32kb + 8G .. +8 of k-block kb.
-__device__ __forceinline__ void load_k(const uint16_t* kbase, int key0, int T, int m16, int G,
-                                       u32x4 (&kr)[2][4]) {
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-        const int key = min(key0 + 16 * t + a_row_key(m16), T - 1);
-        const uint16_t* p = kbase + (size_t)key * kHeadDim + 8 * G;
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) kr[t][kb] = ld_u32x4(p + 32 * kb);
-    }
-}
-
-// V rows of a 32-key tile: slot e = 4t + i is key 16t + G + 4i, and lane
-// (m16, G) holds its head-dim elements 8*m16 .. +8; one load instruction
-// covers four whole consecutive rows.
-__device__ __forceinline__ void load_v(const uint16_t* vbase, int key0, int T, int m16, int G,
-                                       u32x4 (&vr)[8]) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        const int key = min(key0 + 16 * (e >> 2) + G + 4 * (e & 3), T - 1);
-        vr[e] = ld_u32x4(vbase + (size_t)key * kHeadDim + 8 * m16);
-    }
-}
-
-// Logits^T tile: acc[t][rt][i] = q(row rt*16+m16) . k(key 16t + G + 4i).
-template <int NRT>
-__device__ __forceinline__ void qk_tile(const u32x4 (&kr)[2][4], const Rows<NRT>& r,
-                                        f32x4 (&acc)[2][NRT]) {
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int rt = 0; rt < NRT; ++rt) {
-            f32x4 s = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb) s = mfma_bf16(kr[t][kb], r.q[rt][kb], s);
-            acc[t][rt] = s;
-        }
 }
 
 // ---------------------------------------------------------------------------
@@ -173,7 +89,7 @@ __global__ __launch_bounds__(kThreads) void verify_stats_kernel(VerifyArgs a) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int m16 = lane & 15, G = lane >> 4;
     Rows<NRT> r;
-    load_rows<NRT>(a, it, m16, G, r);
+    load_rows<NRT>(a, it.b, it.c, it.T, it.nq, m16, G, r);
     const uint16_t* kbase = a.k + (size_t)it.unit * a.max_ctx * kHeadDim;
 
     float M[NRT], L[NRT];
@@ -181,23 +97,12 @@ __global__ __launch_bounds__(kThreads) void verify_stats_kernel(VerifyArgs a) {
     for (int rt = 0; rt < NRT; ++rt) { M[rt] = -INFINITY; L[rt] = 0.f; }
 
     const int ntile = (it.key_end - it.key_begin + kTile - 1) / kTile;
-    int tt = wave;
-    if (tt < ntile) {
-        u32x4 ka[2][4], kb_[2][4];
-        load_k(kbase, it.key_begin + tt * kTile, it.T, m16, G, ka);
-        for (;;) {
-            int tn = tt + kWaves < ntile ? tt + kWaves : tt;
-            load_k(kbase, it.key_begin + tn * kTile, it.T, m16, G, kb_);
-            stats_tile<NRT>(a, r, ka, it.key_begin + tt * kTile, G, M, L);
-            tt += kWaves;
-            if (tt >= ntile) break;
-            tn = tt + kWaves < ntile ? tt + kWaves : tt;
-            load_k(kbase, it.key_begin + tn * kTile, it.T, m16, G, ka);
-            stats_tile<NRT>(a, r, kb_, it.key_begin + tt * kTile, G, M, L);
-            tt += kWaves;
-            if (tt >= ntile) break;
-        }
-    }
+    tile_pipeline<4, KTile>(
+        wave, ntile, kWaves,
+        [&](KTile& b, int t) { load_k(kbase, it.key_begin + t * kTile, it.T, m16, G, b.k); },
+        [&](const KTile& b, int t) {
+            stats_tile<NRT>(a, r, b.k, it.key_begin + t * kTile, G, M, L);
+        });
     // Merge the four lane groups (they saw disjoint keys of the same rows).
 #pragma unroll
     for (int rt = 0; rt < NRT; ++rt) {
@@ -289,35 +194,51 @@ __global__ __launch_bounds__(kThreads) void verify_main_kernel(VerifyArgs a) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int m16 = lane & 15, G = lane >> 4;
 
-    // Row log-sum-exp from every item of this (sequence, KV head): lane group
-    // G merges items G, G+4, ... and the groups are merged by shuffles.
-    float lse[NRT];
-    {
-        float M[NRT], L[NRT];
-#pragma unroll
-        for (int rt = 0; rt < NRT; ++rt) { M[rt] = -INFINITY; L[rt] = 0.f; }
-        for (int s2 = G; s2 < it.nchunk; s2 += 4) {
-            const float2* pm = a.part_ml + (size_t)(it.item0 + s2) * kRowCap + m16;
-#pragma unroll
-            for (int rt = 0; rt < NRT; ++rt) {
-                const float2 ml = pm[rt * 16];
-                ml_merge(M[rt], L[rt], ml.x, ml.y);
-            }
-        }
-#pragma unroll
-        for (int rt = 0; rt < NRT; ++rt) {
-            ml_merge(M[rt], L[rt], shfl_xor_f(M[rt], 16), shfl_xor_f(L[rt], 16));
-            ml_merge(M[rt], L[rt], shfl_xor_f(M[rt], 32), shfl_xor_f(L[rt], 32));
-            lse[rt] = L[rt] > 0.f ? M[rt] + fast_log2(L[rt]) : INFINITY;
-        }
-    }
-
     Rows<NRT> r;
-    load_rows<NRT>(a, it, m16, G, r);
+    load_rows<NRT>(a, it.b, it.c, it.T, it.nq, m16, G, r);
     const size_t cache_off = (size_t)it.unit * a.max_ctx * kHeadDim;
     const uint16_t* kbase = a.k + cache_off;
     const uint16_t* vbase = a.v + cache_off;
     float* srow = a.scores + (size_t)it.unit * a.max_ctx;
+    const int ntile = (it.key_end - it.key_begin + kTile - 1) / kTile;
+
+    // Row log-sum-exp from the statistics of every item of this (sequence, KV
+    // head): thread t merges row t % 64 over the items t / 64, t / 64 + 4, ...
+    // (all of its loads in flight together), then the four partial states of
+    // each row are merged in a fixed order.
+    __shared__ float2 lse_part[kWaves][kRowCap];
+    __shared__ float lse_row[kRowCap];
+    {
+        const int R = it.nq * a.group;
+        const int rr = threadIdx.x & (kRowCap - 1), ph = threadIdx.x >> 6;
+        float M = -INFINITY, L = 0.f;
+        if (rr < R) {
+            for (int s0 = ph; s0 < it.nchunk; s0 += 8 * kWaves) {
+                float2 v[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int s2 = s0 + u * kWaves;
+                    v[u] = s2 < it.nchunk ? a.part_ml[(size_t)(it.item0 + s2) * kRowCap + rr]
+                                          : make_float2(-INFINITY, 0.f);
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u) ml_merge(M, L, v[u].x, v[u].y);
+            }
+        }
+        lse_part[ph][rr] = make_float2(M, L);
+        __syncthreads();
+        if (threadIdx.x < kRowCap) {
+            float Mx = -INFINITY, Lx = 0.f;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w)
+                ml_merge(Mx, Lx, lse_part[w][threadIdx.x].x, lse_part[w][threadIdx.x].y);
+            lse_row[threadIdx.x] = Lx > 0.f ? Mx + fast_log2(Lx) : INFINITY;
+        }
+        __syncthreads();
+    }
+    float lse[NRT];
+#pragma unroll
+    for (int rt = 0; rt < NRT; ++rt) lse[rt] = lse_row[rt * 16 + m16];
 
     f32x4 oacc[8][NRT];
 #pragma unroll
@@ -325,29 +246,16 @@ __global__ __launch_bounds__(kThreads) void verify_main_kernel(VerifyArgs a) {
 #pragma unroll
         for (int rt = 0; rt < NRT; ++rt) oacc[jd][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int ntile = (it.key_end - it.key_begin + kTile - 1) / kTile;
-    int tt = wave;
-    if (tt < ntile) {
-        u32x4 ka[2][4], kb_[2][4], va[8], vb[8];
-        load_k(kbase, it.key_begin + tt * kTile, it.T, m16, G, ka);
-        load_v(vbase, it.key_begin + tt * kTile, it.T, m16, G, va);
-        for (;;) {
-            int tn = tt + kWaves < ntile ? tt + kWaves : tt;
-            load_k(kbase, it.key_begin + tn * kTile, it.T, m16, G, kb_);
-            load_v(vbase, it.key_begin + tn * kTile, it.T, m16, G, vb);
-            main_tile<NRT>(a, r, lse, ka, va, it.key_begin + tt * kTile, it.key_end, srow, m16, G,
-                           oacc);
-            tt += kWaves;
-            if (tt >= ntile) break;
-            tn = tt + kWaves < ntile ? tt + kWaves : tt;
-            load_k(kbase, it.key_begin + tn * kTile, it.T, m16, G, ka);
-            load_v(vbase, it.key_begin + tn * kTile, it.T, m16, G, va);
-            main_tile<NRT>(a, r, lse, kb_, vb, it.key_begin + tt * kTile, it.key_end, srow, m16, G,
-                           oacc);
-            tt += kWaves;
-            if (tt >= ntile) break;
-        }
-    }
+    tile_pipeline<(NRT <= 2 ? 3 : 2), KVTile>(
+        wave, ntile, kWaves,
+        [&](KVTile& b, int t) {
+            load_k(kbase, it.key_begin + t * kTile, it.T, m16, G, b.k);
+            load_v(vbase, it.key_begin + t * kTile, it.T, m16, G, b.v);
+        },
+        [&](const KVTile& b, int t) {
+            main_tile<NRT>(a, r, lse, b.k, b.v, it.key_begin + t * kTile, it.key_end, srow, m16,
+                           G, oacc);
+        });
 
     // Sum the four waves' partial outputs in LDS (fixed order), then write the
     // item's rows.  oacc[jd][rt][i] is row rt*16+m16, head-dim 32G + 8i + jd.
@@ -380,8 +288,14 @@ __global__ __launch_bounds__(kThreads) void verify_main_kernel(VerifyArgs a) {
 
 // ---------------------------------------------------------------------------
 // Combine: out row = sum over the items of its (sequence, KV head).
+// 256 threads per row: thread t sums head-dim quad t % 32 over the items
+// t / 32, t / 32 + 8, ... with all its loads in flight at once; the eight
+// partial sums are then added in a fixed order.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kHeadDim) void verify_combine_kernel(VerifyArgs a) {
+constexpr int kCombineThreads = 256;
+constexpr int kCombineGroups = kCombineThreads / 32;
+
+__global__ __launch_bounds__(kCombineThreads) void verify_combine_kernel(VerifyArgs a) {
     const SeqTable& st = a.seq;
     const int gr = blockIdx.x;
     int b = 0;
@@ -392,17 +306,36 @@ __global__ __launch_bounds__(kHeadDim) void verify_combine_kernel(VerifyArgs a) 
     const int row = local - c * R;
     const int nchunk = (st.ctx[b] + a.chunk - 1) / a.chunk;
     const int item0 = st.item_start[b] + c * nchunk;
-    const int d = threadIdx.x;
-    float acc = 0.f;
-    for (int s = 0; s < nchunk; ++s)
-        acc += a.part_o[((size_t)(item0 + s) * kRowCap + row) * kHeadDim + d];
+    const int d4 = threadIdx.x & 31, sg = threadIdx.x >> 5;
+    const f32x4* po = reinterpret_cast<const f32x4*>(a.part_o);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s0 = sg; s0 < nchunk; s0 += 8 * kCombineGroups) {
+        f32x4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int s = s0 + u * kCombineGroups;
+            v[u] = s < nchunk ? po[((size_t)(item0 + s) * kRowCap + row) * (kHeadDim / 4) + d4]
+                              : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc += v[u];
+    }
+    __shared__ f32x4 red[kCombineGroups][32];
+    red[sg][d4] = acc;
+    __syncthreads();
+    if (sg != 0) return;
+    f32x4 o = red[0][d4];
+#pragma unroll
+    for (int gq = 1; gq < kCombineGroups; ++gq) o += red[gq][d4];
     const int j = row / a.group;
     const int h = c * a.group + (row - j * a.group);
-    const size_t o = (((size_t)b * a.max_q + j) * a.n_q_heads + h) * kHeadDim + d;
-    if (a.out_fp32)
-        reinterpret_cast<float*>(a.out)[o] = acc;
-    else
-        reinterpret_cast<__bf16*>(a.out)[o] = (__bf16)acc;
+    const size_t base = (((size_t)b * a.max_q + j) * a.n_q_heads + h) * kHeadDim + 4 * d4;
+    if (a.out_fp32) {
+        *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out) + base) = o;
+    } else {
+        uint2 pk = make_uint2(pack_bf16(o[0], o[1]), pack_bf16(o[2], o[3]));
+        *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + base) = pk;
+    }
 }
 
 template <int NRT>
@@ -410,7 +343,7 @@ hipError_t launch_verify_nrt(const VerifyArgs& a, int n_items, int n_rows_total,
                              hipStream_t stream) {
     hipLaunchKernelGGL(verify_stats_kernel<NRT>, dim3(n_items), dim3(kThreads), 0, stream, a);
     hipLaunchKernelGGL(verify_main_kernel<NRT>, dim3(n_items), dim3(kThreads), 0, stream, a);
-    hipLaunchKernelGGL(verify_combine_kernel, dim3(n_rows_total), dim3(kHeadDim), 0, stream, a);
+    hipLaunchKernelGGL(verify_combine_kernel, dim3(n_rows_total), dim3(kCombineThreads), 0, stream, a);
     return hipGetLastError();
 }
 

@@ -1,0 +1,132 @@
+// verify_common.h -- building blocks shared by the verify kernels: the MFMA
+// operand layouts for K, V and the verify rows, and the register-ring tile
+// pipeline.  Internal to the library.
+#pragma once
+
+#include "device_common.h"
+#include "launch.h"
+
+namespace ssl {
+namespace vc {
+
+constexpr int kThreads = 256;  // 4 waves
+constexpr int kWaves = 4;
+constexpr int kTile = 32;      // keys per wave step
+constexpr int kRowCap = 64;    // rows per item slot in the workspace
+
+// Tile-local key assigned to A row m of a 16-key half tile.  The accumulator
+// rows lane group G receives are 4G + i, which then hold keys G + 4i: the same
+// keys lane group G loads as full 256-byte rows for the V^T operand.
+__device__ __forceinline__ int a_row_key(int m) { return (m >> 2) + 4 * (m & 3); }
+
+// The verify rows a lane owns: row rt*16 + (lane & 15) of each row tile.
+template <int NRT>
+struct Rows {
+    int plim[NRT];      // last key the row may see; -1 for padding rows
+    bool inwin[NRT];    // row contributes to the scores
+    u32x4 q[NRT][4];    // B operand (Q^T): row's head-dim slice per 32-wide k-block
+};
+
+template <int NRT>
+__device__ __forceinline__ void load_rows(const VerifyArgs& a, int b, int c, int T, int nq, int m16,
+                                          int G, Rows<NRT>& r) {
+    const int g = a.group;
+    const int R = nq * g;
+    const int wn = min(a.window, nq);
+#pragma unroll
+    for (int rt = 0; rt < NRT; ++rt) {
+        const int row = rt * 16 + m16;
+        if (row < R) {
+            const int j = row / g;
+            const int hh = row - j * g;
+            r.plim[rt] = T - nq + j;
+            r.inwin[rt] = j >= nq - wn;
+            const uint16_t* qp =
+                a.q + (((size_t)b * a.max_q + j) * a.n_q_heads + c * g + hh) * kHeadDim + 8 * G;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) r.q[rt][kb] = ld_u32x4(qp + 32 * kb);
+        } else {
+            r.plim[rt] = -1;
+            r.inwin[rt] = false;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) r.q[rt][kb] = u32x4{0u, 0u, 0u, 0u};
+        }
+    }
+}
+
+// K operand of a 32-key tile: lane (m16, G) holds key a_row_key(m16) (+16 for
+// the second half) and head-dim elements 32kb + 8G .. +8 of k-block kb.
+__device__ __forceinline__ void load_k(const uint16_t* kbase, int key0, int T, int m16, int G,
+                                       u32x4 (&kr)[2][4]) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+        const int key = min(key0 + 16 * t + a_row_key(m16), T - 1);
+        const uint16_t* p = kbase + (size_t)key * kHeadDim + 8 * G;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) kr[t][kb] = ld_u32x4(p + 32 * kb);
+    }
+}
+
+// V rows of a 32-key tile: slot e = 4t + i is key 16t + G + 4i, and lane
+// (m16, G) holds its head-dim elements 8*m16 .. +8; one load instruction
+// covers four whole consecutive rows.
+__device__ __forceinline__ void load_v(const uint16_t* vbase, int key0, int T, int m16, int G,
+                                       u32x4 (&vr)[8]) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const int key = min(key0 + 16 * (e >> 2) + G + 4 * (e & 3), T - 1);
+        vr[e] = ld_u32x4(vbase + (size_t)key * kHeadDim + 8 * m16);
+    }
+}
+
+// Logits^T tile: acc[t][rt][i] = q(row rt*16+m16) . k(key 16t + G + 4i).
+template <int NRT>
+__device__ __forceinline__ void qk_tile(const u32x4 (&kr)[2][4], const Rows<NRT>& r,
+                                        f32x4 (&acc)[2][NRT]) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int rt = 0; rt < NRT; ++rt) {
+            f32x4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) s = mfma_bf16(kr[t][kb], r.q[rt][kb], s);
+            acc[t][rt] = s;
+        }
+}
+
+// Runs compute(tile) over the wave's tiles first, first + step, ... < ntile
+// with a ring of NBUF register buffers: while one tile is computed, the loads
+// of the next NBUF - 1 tiles are in flight.  load(buf, tile) issues loads only.
+template <int NBUF, typename Buf, typename Load, typename Compute>
+__device__ __forceinline__ void tile_pipeline(int first, int ntile, int step, Load&& load,
+                                              Compute&& compute) {
+    Buf buf[NBUF];
+#pragma unroll
+    for (int p = 0; p < NBUF - 1; ++p) {
+        const int t = first + p * step;
+        if (t < ntile) load(buf[p], t);
+    }
+    int tt = first;
+    while (tt < ntile) {
+#pragma unroll
+        for (int p = 0; p < NBUF; ++p) {
+            if (tt < ntile) {
+                const int tn = tt + (NBUF - 1) * step;
+                if (tn < ntile) load(buf[(p + NBUF - 1) % NBUF], tn);
+                compute(buf[p], tt);
+            }
+            tt += step;
+        }
+    }
+}
+
+struct KTile {
+    u32x4 k[2][4];
+};
+struct KVTile {
+    u32x4 k[2][4];
+    u32x4 v[8];
+};
+
+}  // namespace vc
+}  // namespace ssl

@@ -5,9 +5,10 @@ Tolerances (bf16 inputs, fp32 accumulation):
 
 * outputs: the stated bar is max |O - O_ref| <= 1e-2.  A tighter per-element
   bound follows from the arithmetic: the only rounding larger than fp32's is
-  that of the probabilities to bf16 before the P.V product (relative 2^-9),
-  so |O - O_ref| <= 2^-9 * sum_i P_i |v_i| plus fp32 terms; the tests allow
-  3e-3 * sum_i P_i |v_i| + 1e-6, with sum_i P_i |v_i| from the oracle run on
+  that of the probabilities to bf16 before the P.V product (8 significant
+  bits, round to nearest: relative error at most 2^-8), so
+  |O - O_ref| <= 2^-8 * sum_i P_i |v_i| plus fp32 terms; the tests allow
+  4e-3 * sum_i P_i |v_i| + 1e-6, with sum_i P_i |v_i| from the oracle run on
   |V| (plus 2^-8 |O_ref| when outputs are bf16);
 * scores: |S - S_ref| <= 1e-3 * S_ref for every key with S_ref > 0;
 * index sets: bit-exact against the oracle's select run on the same fp32
@@ -30,11 +31,13 @@ def dev_bf16(bits: np.ndarray) -> torch.Tensor:
     return t.view(torch.bfloat16).cuda()
 
 
-def params_of(w, out_fp32=True, budget=None, k_sink=None, k_recent=None, window=None):
+def params_of(w, out_fp32=True, budget=None, k_sink=None, k_recent=None, window=None,
+              mode=B.VERIFY_AUTO):
     return B.make_params(w.sm_scale, window=w.window if window is None else window,
                          k_sink=w.k_sink if k_sink is None else k_sink,
                          k_recent=w.k_recent if k_recent is None else k_recent,
-                         budget=w.budget if budget is None else budget, out_fp32=out_fp32)
+                         budget=w.budget if budget is None else budget, out_fp32=out_fp32,
+                         verify_mode=mode)
 
 
 class Dev:
@@ -48,9 +51,10 @@ class Dev:
         self.qd = dev_bf16(w.q_draft)
 
 
-def gpu_verify(d: Dev, out_fp32=True, scores_fill=-1.0, out_fill=-7.0, window=None):
+def gpu_verify(d: Dev, out_fp32=True, scores_fill=-1.0, out_fill=-7.0, window=None,
+               mode=B.VERIFY_AUTO):
     w = d.w
-    p = params_of(w, out_fp32=out_fp32, window=window)
+    p = params_of(w, out_fp32=out_fp32, window=window, mode=mode)
     odt = torch.float32 if out_fp32 else torch.bfloat16
     out = torch.full(d.q.shape, out_fill, dtype=odt, device="cuda")
     sc = torch.full((w.batch, w.n_kv_heads, w.max_ctx), scores_fill, dtype=torch.float32,
@@ -94,7 +98,7 @@ def check_outputs(o_gpu, o_ref, oabs_ref, rows_mask, out_fp32=True, what="O"):
     assert np.all(np.isfinite(o_gpu[sel])), f"{what}: non-finite outputs"
     maxabs = float(diff.max()) if diff.size else 0.0
     assert maxabs <= 1e-2, f"{what}: max |dO| = {maxabs:.3e} > 1e-2"
-    bound = 3e-3 * oabs_ref + 1e-6
+    bound = 4e-3 * oabs_ref + 1e-6
     if not out_fp32:
         bound = bound + 2.0 ** -8 * np.abs(o_ref)
     bad = (np.abs(o_gpu - o_ref) > bound) & sel

@@ -49,7 +49,7 @@ def _shape(**kw):
 
 def _params(**kw):
     d = dict(sm_scale=1 / math.sqrt(128), window=16, k_sink=4, k_recent=32, budget=256,
-             out_fp32=0)
+             out_fp32=0, verify_mode=0)
     d.update(kw)
     return B.Params(**d)
 
@@ -91,6 +91,15 @@ def test_verify_validation(lib):
     assert _verify(lib, params=_params(window=0)) == B.SSL_ERR_SHAPE
     assert _verify(lib, params=_params(sm_scale=0.0)) == B.SSL_ERR_SHAPE
     assert _verify(lib, params=_params(sm_scale=float("nan"))) == B.SSL_ERR_SHAPE
+    assert _verify(lib, params=_params(verify_mode=3)) == B.SSL_ERR_SHAPE
+    assert _verify(lib, params=_params(verify_mode=-1)) == B.SSL_ERR_SHAPE
+    # a one-sweep request that cannot have every chunk resident at once
+    big = _shape(max_ctx=1 << 20)
+    assert _verify(lib, shape=big, ctx=(1 << 20,), params=_params(verify_mode=2)) == \
+        B.SSL_ERR_UNSUPPORTED
+    many = _shape(batch=20, n_q_heads=64, n_kv_heads=8)
+    assert _verify(lib, shape=many, ctx=(128,) * 20, ql=(2,) * 20,
+                   params=_params(verify_mode=2)) == B.SSL_ERR_UNSUPPORTED
     for name in ("q", "k", "v", "out", "scores"):
         assert _verify(lib, **{name: None}) == B.SSL_ERR_NULL, name
         assert _verify(lib, **{name: FAKE_ODD}) == B.SSL_ERR_ALIGN, name
@@ -197,3 +206,26 @@ def test_binding_refuses_cpu_tensors(lib):
     k = torch.zeros(1, 2, 64, 128, dtype=torch.bfloat16)
     with pytest.raises(RuntimeError, match="no CPU fallback"):
         B.verify_attn(q, k, k, [64], [2], B.make_params(0.1))
+
+
+def test_verify_plan_schedules(lib):
+    """Schedules of the named workloads: AUTO runs two sweeps; one sweep fits at
+    4K and 32K only."""
+    from paper_2607_27735_amd.workloads import CONFIGS
+    fits = {1: True, 2: True, 3: False, 4: False, 5: False}
+    for n, cfg in CONFIGS.items():
+        batch = cfg["batch"]
+        ctx = cfg.get("ctx_len") or [cfg["ctx_range"][1]] * batch
+        ql = cfg.get("q_len") or [cfg["k_range"][1] + 1] * batch
+        shape = B.Shape(batch, cfg["n_q_heads"], cfg["n_kv_heads"], 128,
+                        cfg.get("max_ctx") or max(ctx), max(ql))
+        sch, chunk, items = B.verify_plan(shape, B.make_params(1 / math.sqrt(128)), ctx, ql)
+        assert sch == B.VERIFY_TWO_SWEEP, n
+        assert chunk % 128 == 0 and items >= 1
+        one = B.make_params(1 / math.sqrt(128), verify_mode=B.VERIFY_ONE_SWEEP)
+        if fits[n]:
+            sch, chunk, items = B.verify_plan(shape, one, ctx, ql)
+            assert sch == B.VERIFY_ONE_SWEEP and items <= 256 and chunk % 128 == 0
+        else:
+            with pytest.raises(B.SSLError):
+                B.verify_plan(shape, one, ctx, ql)
