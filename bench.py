@@ -75,6 +75,7 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--mode", choices=["eager", "graph"], default="eager")
+    ap.add_argument("--verify-mode", choices=["auto", "two-sweep", "one-sweep"], default="auto")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the hot path runs on one GPU; see the design "
@@ -103,8 +104,10 @@ def main() -> int:
     kv_bytes = k0.numel() * 2 * 2
     n_copies = max(2, math.ceil((512 << 20) / kv_bytes) + 1)
     kvs = [(k0, v0)] + [(k0.clone(), v0.clone()) for _ in range(n_copies - 1)]
+    vmode = {"auto": B.VERIFY_AUTO, "two-sweep": B.VERIFY_TWO_SWEEP,
+             "one-sweep": B.VERIFY_ONE_SWEEP}[args.verify_mode]
     params = B.make_params(w.sm_scale, window=w.window, k_sink=w.k_sink, k_recent=w.k_recent,
-                           budget=w.budget, out_fp32=False)
+                           budget=w.budget, out_fp32=False, verify_mode=vmode)
     out = torch.empty(q.shape, dtype=torch.bfloat16, device=dev)
     scores = torch.zeros((w.batch, w.n_kv_heads, w.max_ctx), dtype=torch.float32, device=dev)
     idx = torch.zeros((w.batch, w.n_kv_heads, w.budget), dtype=torch.int32, device=dev)
@@ -114,7 +117,7 @@ def main() -> int:
     vshape = B.Shape(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.max_ctx, w.max_q)
     schedule, vchunk, vitems = B.verify_plan(vshape, params, w.ctx_len, w.q_len)
     sched_name = "one-sweep" if schedule == B.VERIFY_ONE_SWEEP else "two-sweep"
-    verify_kernels = ("zero_u32_kernel + verify_fused_kernel" if schedule == B.VERIFY_ONE_SWEEP
+    verify_kernels = ("verify_fused_kernel + verify_combine_kernel" if schedule == B.VERIFY_ONE_SWEEP
                       else "verify_stats_kernel + verify_main_kernel + verify_combine_kernel")
 
     stream = torch.cuda.current_stream()

@@ -96,14 +96,13 @@ typedef struct {
 } ssl_params;
 
 /* How ssl_verify_attn schedules its work (results agree to rounding):
- *  AUTO       currently the two-sweep schedule (the faster one on MI355X:
- *             the one-sweep schedule pays for a cooperative launch and a
- *             cross-workgroup barrier);
+ *  AUTO       the one-sweep schedule where it fits, else the two-sweep one;
  *  TWO_SWEEP  a K-only pass for the row statistics, then a K+V pass;
- *  ONE_SWEEP  a single K+V pass; SSL_ERR_UNSUPPORTED when it does not fit
- *             (at most 128 (sequence, KV head) pairs and 256 work items; an
- *             item holds at most 2176 / 1024 / 640 / 384 keys for up to
- *             16 / 32 / 48 / 64 verify rows per KV head). */
+ *  ONE_SWEEP  a single K+V pass whose chunks of one (sequence, KV head)
+ *             exchange row statistics while resident together;
+ *             SSL_ERR_UNSUPPORTED when it does not fit: a (sequence, KV head)
+ *             may span at most 128 chunks of at most 2176 / 1024 / 640 / 384
+ *             keys for up to 16 / 32 / 48 / 64 verify rows per KV head. */
 enum { SSL_VERIFY_AUTO = 0, SSL_VERIFY_TWO_SWEEP = 1, SSL_VERIFY_ONE_SWEEP = 2 };
 
 /* Human-readable text of a status code (static storage). */
@@ -162,7 +161,15 @@ int ssl_verify_attn(const ssl_shape *shape, const ssl_params *params,
  *           writes them); comparison is exact on their fp32 values.
  * idx[b,c,0..n) receives sink U TopK U recent in ascending order and
  * n_idx[b] = n = ssl_index_count(T, ...); slots past n are not written.
- * Errors: SSL_ERR_BUDGET; SSL_ERR_SHAPE if ctx_len < 1 or > max_ctx.
+ *
+ * Workspace: ssl_select_workspace gives its size for these context lengths
+ * (about 17 bytes per position of the longest context, per (b, c)); device
+ * memory, 16-byte aligned, owned by the caller, no initial contents needed.
+ * A call uses it until the call's work on `stream` ends; calls that overlap
+ * in time must not share one workspace.
+ * Errors: SSL_ERR_BUDGET; SSL_ERR_SHAPE if ctx_len < 1 or > max_ctx;
+ * SSL_ERR_UNSUPPORTED if the longest context exceeds 2^21 positions;
+ * SSL_ERR_WORKSPACE if the workspace is missing or too small.
  */
 int ssl_select_workspace(const ssl_shape *shape, const ssl_params *params,
                          const int32_t *ctx_len_host, size_t *bytes_out);

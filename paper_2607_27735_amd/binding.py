@@ -242,14 +242,22 @@ def select_topb(scores: torch.Tensor, ctx_len, params: Params, n_q_heads: Option
     _need_gpu(idx, n_idx)
     if idx.shape != (batch, hkv, params.budget) or idx.dtype != torch.int32:
         raise ValueError("idx must be int32 [batch, n_kv_heads, budget]")
+    ws = torch.empty(max(select_workspace_bytes(shape, params, ctx), 1), dtype=torch.uint8,
+                     device=scores.device)
+    _check(load().ssl_select_topb(ctypes.byref(shape), ctypes.byref(params),
+                                  ctx.ctypes.data_as(_i32p), _ptr(scores), _ptr(idx),
+                                  _ptr(n_idx), _ptr(ws), ws.numel(), _stream(stream)),
+           "ssl_select_topb")
+    return idx, n_idx
+
+
+def select_workspace_bytes(shape: Shape, params: Params, ctx_len) -> int:
+    ctx = _host_i32(ctx_len)
     n = ctypes.c_size_t(0)
     _check(load().ssl_select_workspace(ctypes.byref(shape), ctypes.byref(params),
                                        ctx.ctypes.data_as(_i32p), ctypes.byref(n)),
            "ssl_select_workspace")
-    _check(load().ssl_select_topb(ctypes.byref(shape), ctypes.byref(params),
-                                  ctx.ctypes.data_as(_i32p), _ptr(scores), _ptr(idx),
-                                  _ptr(n_idx), None, 0, _stream(stream)), "ssl_select_topb")
-    return idx, n_idx
+    return int(n.value)
 
 
 # ---------------------------------------------------------------------------
@@ -373,8 +381,10 @@ class PreparedStep:
         self.dshape = Shape(self.shape.batch, self.shape.n_q_heads, self.shape.n_kv_heads,
                             self.shape.head_dim, self.shape.max_ctx, 1)
         vws = verify_workspace_bytes(self.shape, params, self.ctx, self.ql)
+        sws = select_workspace_bytes(self.shape, params, self.ctx)
         dws = draft_workspace_bytes(self.dshape, params, self.n_idx_host)
         self.vws = torch.empty(max(vws, 1), dtype=torch.uint8, device=q.device)
+        self.sws = torch.empty(max(sws, 1), dtype=torch.uint8, device=q.device)
         self.dws = torch.empty(max(dws, 1), dtype=torch.uint8, device=q.device)
         self.tensors = (q, k, v, q_draft, out, scores, idx, n_idx, draft_out)
         self.stream = _stream(stream)
@@ -382,8 +392,8 @@ class PreparedStep:
         cp, qp = self.ctx.ctypes.data_as(_i32p), self.ql.ctypes.data_as(_i32p)
         self._v = (sp, pp, cp, qp, q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                    scores.data_ptr(), self.vws.data_ptr(), self.vws.numel(), self.stream)
-        self._s = (sp, pp, cp, scores.data_ptr(), idx.data_ptr(), n_idx.data_ptr(), None, 0,
-                   self.stream)
+        self._s = (sp, pp, cp, scores.data_ptr(), idx.data_ptr(), n_idx.data_ptr(),
+                   self.sws.data_ptr(), self.sws.numel(), self.stream)
         self._d = (ctypes.byref(self.dshape), pp, self.n_idx_host.ctypes.data_as(_i32p),
                    q_draft.data_ptr(), k.data_ptr(), v.data_ptr(), idx.data_ptr(),
                    draft_out.data_ptr(), self.dws.data_ptr(), self.dws.numel(), self.stream)

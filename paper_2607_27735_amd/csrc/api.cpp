@@ -4,8 +4,11 @@
 // leaves the device untouched and is testable without a GPU.
 #include <math.h>
 #include <string.h>
+#include <unistd.h>
 
 #include <algorithm>
+#include <atomic>
+#include <chrono>
 
 #include "../../include/sparsespec_l.h"
 #include "launch.h"
@@ -43,16 +46,33 @@ int check_budget(const ssl_params* p) {
 // Verify work decomposition.  Two-sweep items are (sequence, KV head, key
 // chunk); the one-sweep schedule uses the same kind of items ("slots"), all
 // resident at once.  The workspace holds per-item row statistics and partial
-// outputs for whichever schedule needs more, plus the arrival counters.
-constexpr int kFusedMaxSlots = 256;
+// outputs for whichever schedule needs more, plus the one-sweep tags.
+constexpr int kFusedMaxSlotsPerUnit = 128;
+
+// One-sweep publication tags: a process-wide sequence whose start mixes the
+// clock and the process id, so that tags differ between calls and, with
+// overwhelming probability, from whatever a workspace held before.
+uint64_t next_call_tag() {
+    static std::atomic<uint64_t> seq{[] {
+        uint64_t x = (uint64_t)std::chrono::steady_clock::now().time_since_epoch().count();
+        x ^= (uint64_t)getpid() << 32;
+        x ^= x >> 33;   // splitmix64 finaliser
+        x *= 0xff51afd7ed558ccdull;
+        x ^= x >> 33;
+        x *= 0xc4ceb9fe1a85ec53ull;
+        x ^= x >> 33;
+        return x;
+    }()};
+    return seq.fetch_add(1, std::memory_order_relaxed) + 1;
+}
 
 struct VerifyPlan {
     int chunk, n_items, n_rows, row_tiles;
     bool fused_ok;
-    int fused_chunk, fused_slots, n_units;
-    size_t ml_off, o_off, arrive_off, bytes;
+    int fused_chunk, fused_slots;
+    size_t ml_off, o_off, tag_off, bytes;
     SeqTable seq;
-    FusedTable ft;
+    SeqTable fseq;   // the one-sweep slots as items
 };
 
 int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, const int32_t* ql,
@@ -98,47 +118,41 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
     plan->n_items = (int)items;
     plan->n_rows = (int)rows;
 
-    // One-sweep: the smallest multiple of 128 keys that keeps every slot
-    // resident (one workgroup per CU), if it fits the LDS logit stash.
-    const int64_t units = (int64_t)s->batch * s->n_kv_heads;
-    plan->n_units = (int)units;
+    // One-sweep: chunks (multiples of 128 keys, at most what the LDS logit
+    // stash holds) of about one slot per CU over the whole call, but never
+    // more than kFusedMaxSlotsPerUnit slots per (sequence, KV head), all of
+    // which must be resident together.
     plan->fused_ok = false;
     plan->fused_slots = 0;
     plan->fused_chunk = 0;
     const int cap = fused_max_chunk(plan->row_tiles);
-    if (units <= kFusedMaxUnits && cap >= 128) {
-        for (int fc = 128; fc <= cap; fc += 128) {
-            int64_t slots = 0;
-            for (int b = 0; b < s->batch; ++b)
-                slots += (int64_t)s->n_kv_heads * ((ctx[b] + fc - 1) / fc);
-            if (slots <= kFusedMaxSlots) {
-                plan->fused_ok = true;
-                plan->fused_chunk = fc;
-                plan->fused_slots = (int)slots;
-                break;
-            }
+    int max_ctx = 0;
+    for (int b = 0; b < s->batch; ++b) max_ctx = std::max(max_ctx, ctx[b]);
+    const int64_t per_unit_min = ((int64_t)max_ctx + kFusedMaxSlotsPerUnit - 1) / kFusedMaxSlotsPerUnit;
+    const int64_t spread = (total_keys + 255) / 256;
+    int64_t fc = std::max(per_unit_min, spread);
+    fc = std::max<int64_t>(128, (fc + 127) / 128 * 128);
+    if (fc > cap) fc = cap / 128 * 128;
+    if (fc >= 128 && ((int64_t)max_ctx + fc - 1) / fc <= kFusedMaxSlotsPerUnit) {
+        int64_t slots = 0;
+        plan->fseq = plan->seq;
+        for (int b = 0; b < s->batch; ++b) {
+            plan->fseq.item_start[b] = (int32_t)slots;
+            slots += (int64_t)s->n_kv_heads * ((ctx[b] + fc - 1) / fc);
+        }
+        if (slots <= (1 << 30)) {
+            plan->fseq.item_start[s->batch] = (int32_t)slots;
+            plan->fused_ok = true;
+            plan->fused_chunk = (int)fc;
+            plan->fused_slots = (int)slots;
         }
     }
     if (p->verify_mode == SSL_VERIFY_ONE_SWEEP && !plan->fused_ok) return SSL_ERR_UNSUPPORTED;
-    if (plan->fused_ok) {
-        memset(&plan->ft, 0, sizeof plan->ft);
-        plan->ft.n_units = (int)units;
-        plan->ft.chunk = plan->fused_chunk;
-        int slot = 0;
-        for (int b = 0; b < s->batch; ++b)
-            for (int c = 0; c < s->n_kv_heads; ++c) {
-                const int u = b * s->n_kv_heads + c;
-                plan->ft.unit[u] = u;
-                plan->ft.slot_start[u] = slot;
-                slot += (ctx[b] + plan->fused_chunk - 1) / plan->fused_chunk;
-            }
-        plan->ft.slot_start[units] = slot;
-    }
     const size_t slots_max = (size_t)std::max(plan->n_items, plan->fused_slots);
     plan->ml_off = 0;
     plan->o_off = align_up(slots_max * kVerifyRowCap * sizeof(float) * 2);
-    plan->arrive_off = plan->o_off + align_up(slots_max * kVerifyRowCap * 128 * sizeof(float));
-    plan->bytes = plan->arrive_off + align_up((size_t)kFusedMaxUnits * sizeof(uint32_t));
+    plan->tag_off = plan->o_off + align_up(slots_max * kVerifyRowCap * 128 * sizeof(float));
+    plan->bytes = plan->tag_off + align_up((size_t)plan->fused_slots * sizeof(uint64_t));
     return SSL_OK;
 }
 
@@ -186,6 +200,31 @@ int check_select(const ssl_shape* s, const ssl_params* p, const int32_t* ctx) {
     if (!ctx) return SSL_ERR_NULL;
     for (int b = 0; b < s->batch; ++b)
         if (ctx[b] < 1 || ctx[b] > s->max_ctx) return SSL_ERR_SHAPE;
+    return SSL_OK;
+}
+
+// Select workspace: per-partition histograms, candidate segments and the
+// position bitmask of every unit, sized for the longest context of the call.
+struct SelectPlan {
+    int part, parts;
+    size_t hist_off, coarse_off, cnt_off, thr_off, mask_off, seg_off, bytes;
+};
+
+int plan_select(const ssl_shape* s, const int32_t* ctx, SelectPlan* plan) {
+    int max_t = 0;
+    for (int b = 0; b < s->batch; ++b) max_t = ctx[b] > max_t ? ctx[b] : max_t;
+    plan->part = ssl::select_part_len(max_t);
+    plan->parts = (max_t + plan->part - 1) / plan->part;
+    if (plan->parts > ssl::kMaxSelectParts) return SSL_ERR_UNSUPPORTED;
+    const size_t slots = (size_t)s->batch * s->n_kv_heads * plan->parts;
+    const size_t units = (size_t)s->batch * s->n_kv_heads;
+    plan->hist_off = 0;
+    plan->coarse_off = plan->hist_off + align_up(slots * 2048 * sizeof(uint32_t));
+    plan->cnt_off = plan->coarse_off + align_up(slots * 64 * sizeof(uint32_t));
+    plan->thr_off = plan->cnt_off + align_up(slots * sizeof(uint32_t));
+    plan->mask_off = plan->thr_off + align_up(units * 2 * sizeof(uint32_t));
+    plan->seg_off = plan->mask_off + align_up(slots * (plan->part / 32) * sizeof(uint32_t));
+    plan->bytes = plan->seg_off + align_up(slots * plan->part * 2 * sizeof(uint32_t));
     return SSL_OK;
 }
 
@@ -241,7 +280,7 @@ int ssl_verify_plan(const ssl_shape* shape, const ssl_params* params, const int3
     VerifyPlan plan;
     const int rc = plan_verify(shape, params, ctx_len_host, q_len_host, &plan);
     if (rc) return rc;
-    const bool one = plan.fused_ok && params->verify_mode == SSL_VERIFY_ONE_SWEEP;
+    const bool one = plan.fused_ok && params->verify_mode != SSL_VERIFY_TWO_SWEEP;
     *schedule_out = one ? SSL_VERIFY_ONE_SWEEP : SSL_VERIFY_TWO_SWEEP;
     *chunk_out = one ? plan.fused_chunk : plan.chunk;
     *items_out = one ? plan.fused_slots : plan.n_items;
@@ -280,15 +319,17 @@ int ssl_verify_attn(const ssl_shape* shape, const ssl_params* params, const int3
     a.out_fp32 = params->out_fp32 ? 1 : 0;
     a.scale_log2 = params->sm_scale * 1.4426950408889634f;
     a.seq = plan.seq;
-    if (plan.fused_ok && params->verify_mode == SSL_VERIFY_ONE_SWEEP) {
+    if (plan.fused_ok && params->verify_mode != SSL_VERIFY_TWO_SWEEP) {
         FusedArgs fa;
         fa.v = a;
-        fa.arrive = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + plan.arrive_off);
-        fa.ft = plan.ft;
-        const hipError_t e = launch_verify_fused(fa, plan.fused_slots, plan.row_tiles, stream);
-        if (e == hipSuccess) return SSL_OK;
-        (void)hipGetLastError();   // the refused cooperative launch ran nothing
-        if (params->verify_mode == SSL_VERIFY_ONE_SWEEP) return SSL_ERR_HIP;
+        fa.v.chunk = plan.fused_chunk;
+        fa.v.seq = plan.fseq;
+        fa.tag = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + plan.tag_off);
+        fa.call_tag = next_call_tag();
+        return launch_verify_fused(fa, plan.fused_slots, plan.n_rows, plan.row_tiles, stream) ==
+                       hipSuccess
+                   ? SSL_OK
+                   : SSL_ERR_HIP;
     }
     return launch_verify(a, plan.n_items, plan.n_rows, plan.row_tiles, stream) == hipSuccess
                ? SSL_OK
@@ -298,9 +339,12 @@ int ssl_verify_attn(const ssl_shape* shape, const ssl_params* params, const int3
 int ssl_select_workspace(const ssl_shape* shape, const ssl_params* params,
                          const int32_t* ctx_len_host, size_t* bytes_out) {
     if (!bytes_out) return SSL_ERR_NULL;
-    const int rc = check_select(shape, params, ctx_len_host);
+    int rc = check_select(shape, params, ctx_len_host);
     if (rc) return rc;
-    *bytes_out = 0;
+    SelectPlan plan;
+    rc = plan_select(shape, ctx_len_host, &plan);
+    if (rc) return rc;
+    *bytes_out = plan.bytes;
     return SSL_OK;
 }
 
@@ -311,13 +355,25 @@ int ssl_select_topb(const ssl_shape* shape, const ssl_params* params, const int3
     if (rc) return rc;
     if (!scores || !idx || !n_idx) return SSL_ERR_NULL;
     if (!aligned(scores, 4) || !aligned(idx, 4) || !aligned(n_idx, 4)) return SSL_ERR_ALIGN;
-    rc = check_workspace(workspace, workspace_bytes, 0);
+    SelectPlan plan;
+    rc = plan_select(shape, ctx_len_host, &plan);
     if (rc) return rc;
+    rc = check_workspace(workspace, workspace_bytes, plan.bytes);
+    if (rc) return rc;
+    char* ws = static_cast<char*>(workspace);
     SelectArgs a;
     memset(&a, 0, sizeof a);
     a.scores = scores;
     a.idx = idx;
     a.n_idx = n_idx;
+    a.hist = reinterpret_cast<uint32_t*>(ws + plan.hist_off);
+    a.coarse = reinterpret_cast<uint32_t*>(ws + plan.coarse_off);
+    a.cnt = reinterpret_cast<uint32_t*>(ws + plan.cnt_off);
+    a.thr = reinterpret_cast<uint32_t*>(ws + plan.thr_off);
+    a.mask = reinterpret_cast<uint32_t*>(ws + plan.mask_off);
+    a.seg = reinterpret_cast<uint2*>(ws + plan.seg_off);
+    a.part = plan.part;
+    a.parts = plan.parts;
     a.n_kv_heads = shape->n_kv_heads;
     a.max_ctx = shape->max_ctx;
     a.k_sink = params->k_sink;

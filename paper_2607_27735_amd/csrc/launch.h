@@ -34,11 +34,25 @@ struct VerifyArgs {
     SeqTable seq;
 };
 
+// Select splits each (sequence, KV head) unit into partitions of `part`
+// positions (a multiple of 1024, at most kSelectMaxRounds * 1024); `parts` is
+// the partition stride of the workspace arrays (partitions of the longest
+// sequence), at most kSelectMaxParts.
+constexpr int kSelectMaxRounds = 8;
+constexpr int kSelectTargetParts = 32;
+constexpr int kMaxSelectParts = 256;
+
 struct SelectArgs {
     const float* scores;
     int32_t* idx;
     int32_t* n_idx;
-    int32_t n_kv_heads, max_ctx, k_sink, k_recent, budget, batch;
+    uint32_t* hist;     // [units][parts][2048] top-12-bit histogram of each partition
+    uint32_t* coarse;   // [units][parts][64]   the same in bins of 32
+    uint32_t* cnt;      // [units][parts]       candidates of each partition
+    uint32_t* thr;      // [units][2]           threshold bin d1 and the count needed from it
+    uint32_t* mask;     // [units][parts * part / 32] position bitmask
+    uint2* seg;         // [units][parts][part] candidate (score bits, position)
+    int32_t n_kv_heads, max_ctx, k_sink, k_recent, budget, batch, part, parts;
     int32_t ctx[kTableBatch];
 };
 
@@ -55,34 +69,29 @@ struct DraftArgs {
     SeqTable seq;           // ctx[] holds n_idx per sequence
 };
 
-// Single-sweep verify: every work item of the launch is resident at once
-// (cooperative launch), items of KV-head unit u are slots
-// [slot_start[u], slot_start[u + 1]), each covering `chunk` keys.
-constexpr int kFusedMaxUnits = 128;
-
-struct FusedTable {
-    int32_t n_units;
-    int32_t chunk;
-    int32_t unit[kFusedMaxUnits];            // b * n_kv_heads + c
-    int32_t slot_start[kFusedMaxUnits + 1];
-};
-
+// Single-sweep verify: the slots (items of v.seq / v.chunk) of one KV-head
+// unit must be resident at once.
 struct FusedArgs {
-    VerifyArgs v;           // part_ml / part_o are indexed by slot
-    uint32_t* arrive;       // [n_units] arrival counters, zero at launch
-    FusedTable ft;
+    VerifyArgs v;           // part_ml / part_o indexed by slot
+    uint64_t* tag;          // [n_slots] publication tags (no initialisation needed)
+    uint64_t call_tag;      // this call's tag: unique within the process
 };
 
 // Launchers return hipSuccess or the error of the launch.
 hipError_t launch_verify(const VerifyArgs& a, int n_items, int n_rows_total, int row_tiles,
                          hipStream_t stream);
-// Zeroes the arrival counters, then launches the single-sweep kernel as a
-// cooperative grid of n_slots workgroups.  Returns the launch error (for
-// instance when the grid cannot be co-resident; nothing has run then except
-// the counter fill).
-hipError_t launch_verify_fused(const FusedArgs& a, int n_slots, int row_tiles, hipStream_t stream);
+// Launches the single-sweep kernel over n_slots workgroups, then the combine
+// kernel over n_rows_total rows.  Returns the first launch error.
+hipError_t launch_verify_fused(const FusedArgs& a, int n_slots, int n_rows_total, int row_tiles,
+                               hipStream_t stream);
+// The combine kernel alone: out[row] = sum of the row's normalised partials.
+hipError_t launch_verify_combine(const VerifyArgs& a, int n_rows_total, hipStream_t stream);
 // Largest key chunk the single-sweep kernel can hold in LDS for row_tiles.
 int fused_max_chunk(int row_tiles);
+// Partition length for the longest context max_t: the smallest multiple of
+// 1024 (in powers of two, at most kSelectMaxRounds * 1024) that keeps a unit at
+// <= kSelectTargetParts partitions.
+int select_part_len(int max_t);
 hipError_t launch_select(const SelectArgs& a, int n_units, hipStream_t stream);
 hipError_t launch_draft(const DraftArgs& a, int n_items, int n_rows_total, hipStream_t stream);
 

@@ -1,93 +1,72 @@
-// select.hip -- Eq. 4 recallable index sets by radix select.
+// select.hip -- Eq. 4 recallable index sets by a split radix select.
 //
-// One 1024-thread workgroup per (sequence, KV head).  Scores are non-negative
-// fp32, so their bit patterns order like their values.  Wave w owns the
-// contiguous positions [w*span, (w+1)*span) and lane l the positions
-// w*span + l + 64j; for contexts up to 64K each lane keeps its scores in
-// registers, so the data is read from memory once.
+// Scores are non-negative fp32, so their bit patterns order like their
+// values.  Each (sequence, KV head) unit is cut into partitions of `part`
+// positions, one 256-thread workgroup per partition, so that a handful of
+// units still spreads over the whole chip.  Three kernels; the kernel
+// boundaries are the only synchronisation between workgroups.
 //
-// 1. Pass 1 histograms the top 12 bits of the middle scores (LDS) and finds
-//    the bin d1 holding the K_mid-th largest score.
-// 2. One sweep over the scores marks, in an LDS bitmask of positions, the
-//    sink, the recent span and every middle position whose top bits exceed
-//    d1 (a 64-lane ballot is exactly two bitmask words), and appends the
-//    positions inside bin d1 to an LDS candidate list.
-// 3. Passes 2 and 3 (10 + 10 bits) run over the candidates only and give the
-//    exact threshold tau and `need`, the number of entries equal to tau that
-//    still fit; candidates above tau are marked, and ties are marked lowest
-//    position first, so the set is unique.
-// 4. The set is emitted in ascending order from the bitmask with one block
-//    scan of per-thread popcounts.
-//
-// If bin d1 holds more candidates than the LDS list (massive ties), or the
-// context exceeds the bitmask, the same three radix passes run over all
-// middle scores and the set is emitted by an ordered two-pass ballot
-// compaction instead.
+// hist:   each partition histograms the top 12 bits of its middle scores
+//         (2048 fine bins, plus 64 coarse bins of 32) into its own slot of
+//         the workspace: no atomics on global memory, nothing to clear.
+// mark:   every partition sums the coarse and then the fine slot histograms
+//         of its unit and finds the bin d1 holding the K_mid-th largest middle
+//         score.  It writes its words of the unit's position bitmask (sink,
+//         recent, middle positions above bin d1) and appends its bin-d1
+//         positions, in position order, to its own candidate segment.
+// finish: one workgroup per unit runs two 10-bit radix passes over the
+//         candidates for the exact threshold tau and `need`, the number of
+//         entries equal to tau that still fit; it marks the candidates above
+//         tau and the first `need` ties (lowest positions) and emits the set
+//         in ascending order by a block scan of per-thread popcounts.
 #include "device_common.h"
 #include "launch.h"
 
 namespace ssl {
 namespace {
 
-constexpr int kSelThreads = 1024;
+constexpr int kSelThreads = 256;
 constexpr int kSelWaves = kSelThreads / kWave;
-constexpr int kRegPerLane = 64;           // register-resident scores per lane (T <= 65536)
-constexpr int kCandCap = 4096;            // LDS candidate list
-constexpr int kSegCap = kCandCap / kSelWaves;   // per-wave segment of the list
-constexpr int kMaskWords = 8192;          // LDS position bitmask: T <= 262144
-constexpr uint32_t kNone = 0xffffffffu;   // "not a middle position" marker
+constexpr int kRound = 4 * kSelThreads;      // positions per round: 4 per thread
+constexpr int kTailCand = 8192;              // candidates the finish kernel caches in LDS
+constexpr int kTailWords = 4096;             // bitmask words per emission chunk
+constexpr uint32_t kNone = 0xffffffffu;      // "not a middle position" marker
 
-__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
-    return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
-                                     __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+__device__ __forceinline__ uint32_t bin12(uint32_t k) { return (k >> 20) & 2047u; }
+
+struct Geom {
+    int T, s_end, r_start, take, parts;
+    bool all_mid, simple;
+};
+
+__device__ __forceinline__ Geom geom_of(const SelectArgs& a, int b) {
+    Geom g;
+    g.T = a.ctx[b];
+    g.s_end = min(a.k_sink, g.T);
+    g.r_start = max(g.T - a.k_recent, g.s_end);
+    const int n_mid = g.r_start - g.s_end;
+    g.take = min(a.budget - a.k_sink - a.k_recent, n_mid);
+    g.all_mid = g.take == n_mid;
+    g.simple = g.all_mid || g.take == 0;   // no radix select needed
+    g.parts = (g.T + a.part - 1) / a.part;
+    return g;
 }
 
-__device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
-
-// Block-wide search of a histogram read from its top bin down: finds the bin
-// where the running count from the top first reaches `remaining` and the count
-// strictly above it, and publishes both through LDS.
-template <int NBINS>
-__device__ __forceinline__ void find_digit(const uint32_t* hist, int remaining, uint32_t* sh_digit,
-                                           int32_t* sh_above, uint32_t* wave_tot) {
-    constexpr int PER = NBINS >= kSelThreads ? NBINS / kSelThreads : 1;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    // Thread t covers bins NBINS-1-PER*t .. NBINS-PER*(t+1) (descending).
-    uint32_t h[PER];
-    uint32_t sum = 0u;
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-        const int bin = NBINS - 1 - PER * tid - q;
-        h[q] = bin >= 0 ? hist[bin] : 0u;
-        sum += h[q];
-    }
-    uint32_t incl = sum;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t v = __shfl_up((int)incl, off, kWave);
-        if (lane >= off) incl += v;
-    }
-    if (lane == 63) wave_tot[wave] = incl;
-    __syncthreads();
-    uint32_t before = 0u;
-    for (int w = 0; w < wave; ++w) before += wave_tot[w];
-    uint32_t above = before + incl - sum;
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-        const int bin = NBINS - 1 - PER * tid - q;
-        if (bin >= 0 && (int)above < remaining && remaining <= (int)(above + h[q])) {
-            *sh_digit = (uint32_t)bin;
-            *sh_above = (int32_t)above;
-        }
-        above += h[q];
-    }
-    __syncthreads();
+// Score bits of position i if it is a middle position, kNone otherwise.  The
+// load is clamped into [0, T) so that it is unconditional.
+__device__ __forceinline__ uint32_t key_of(const float* S, const Geom& g, int i) {
+    const uint32_t v = __builtin_bit_cast(uint32_t, S[min(i, g.T - 1)]);
+    return (i >= g.s_end && i < g.r_start) ? v : kNone;
 }
 
-// Exclusive prefix sum of one value per thread over the block; *total gets
-// the sum.  Uses wave_tot as scratch.
-__device__ __forceinline__ int block_exclusive_scan(int v, uint32_t* wave_tot, int* total) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+__device__ __forceinline__ bool is_edge(const Geom& g, int i) {
+    return i < g.T && (i < g.s_end || i >= g.r_start);
+}
+
+// Exclusive prefix sum of one value per thread over the workgroup; *total gets
+// the sum.  wave_tot is LDS scratch of kSelWaves words.
+__device__ __forceinline__ int block_scan(int v, int* wave_tot, int* total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     int incl = v;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
@@ -95,284 +74,417 @@ __device__ __forceinline__ int block_exclusive_scan(int v, uint32_t* wave_tot, i
         if (lane >= off) incl += u;
     }
     __syncthreads();
-    if (lane == 63) wave_tot[wave] = (uint32_t)incl;
+    if (lane == 63) wave_tot[wave] = incl;
     __syncthreads();
     int before = 0, all = 0;
+#pragma unroll
     for (int w = 0; w < kSelWaves; ++w) {
-        const int t = (int)wave_tot[w];
-        if (w < wave) before += t;
+        const int t = wave_tot[w];
+        before += w < wave ? t : 0;
         all += t;
     }
     *total = all;
     return before + incl - v;
 }
 
-// NJ > 0: every lane keeps exactly NJ scores in registers (T <= 1024 * NJ);
-// NJ == 0: scores are re-read from memory in each sweep.
-template <int NJ>
-__global__ __launch_bounds__(kSelThreads) void select_kernel(SelectArgs a) {
-    constexpr bool REG = NJ > 0;
-    const int unit = blockIdx.x;
-    const int b = unit / a.n_kv_heads;
-    const int c = unit - b * a.n_kv_heads;
-    const int T = a.ctx[b];
-    const float* S = a.scores + (size_t)unit * a.max_ctx;
-    int32_t* out = a.idx + (size_t)unit * a.budget;
+// In a histogram of NBINS bins read from the top bin down, finds the bin where
+// the running count first reaches `remaining` (1 <= remaining <= the total)
+// and the count strictly above that bin; the result goes to sh[0] (bin) and
+// sh[1] (count above).
+template <int NBINS>
+__device__ __forceinline__ void find_digit(const uint32_t* h, int remaining, int* sh,
+                                           int* wave_tot) {
+    constexpr int PER = NBINS / kSelThreads;
+    const int tid = threadIdx.x;
+    int c[PER];
+    int sum = 0;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        c[q] = (int)h[NBINS - 1 - PER * tid - q];
+        sum += c[q];
+    }
+    int total;
+    int above = block_scan(sum, wave_tot, &total);
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        if (above < remaining && remaining <= above + c[q]) {
+            sh[0] = NBINS - 1 - PER * tid - q;
+            sh[1] = above;
+        }
+        above += c[q];
+    }
+    __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// Kernel 1: per-partition histograms.  grid = (parts, units).
+// ---------------------------------------------------------------------------
+template <int NR>
+__global__ __launch_bounds__(kSelThreads) void select_hist_kernel(SelectArgs a) {
+    const int p = blockIdx.x, u = blockIdx.y;
+    const int b = u / a.n_kv_heads;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-
-    const int s_end = min(a.k_sink, T);
-    const int r_start = max(T - a.k_recent, s_end);
-    const int n_mid = r_start - s_end;
-    const int k_mid = a.budget - a.k_sink - a.k_recent;
-    const int take = min(k_mid, n_mid);
-    const bool all_mid = take == n_mid;
-
-    const int span = REG ? NJ * kWave
-                         : ((T + kSelWaves - 1) / kSelWaves + kWave - 1) / kWave * kWave;
-    const int lo = wave * span;
-    const int hi = min(lo + span, T);
-    const int nj = span / kWave;
+    const Geom g = geom_of(a, b);
+    if (p >= g.parts || g.simple) return;
+    const float* S = a.scores + (size_t)u * a.max_ctx;
 
     __shared__ uint32_t hist[2048];
-    __shared__ uint32_t mask[kMaskWords];
-    __shared__ uint32_t cand_key[kCandCap];
-    __shared__ int32_t cand_pos[kCandCap];
-    __shared__ uint32_t wave_tot[kSelWaves];
-    __shared__ uint32_t sh_digit;
-    __shared__ int32_t sh_above;
-    __shared__ int32_t seg_count[kSelWaves];
-    __shared__ int32_t sh_overflow;
-    __shared__ int32_t w_nontie[kSelWaves], w_ties[kSelWaves];
-
-    // Key of the element at (wave, lane, j): its score bits if it is a middle
-    // position, kNone otherwise (sink, recent, beyond T).
-    // The load itself is unconditional (clamped to a valid position) so that
-    // all of a lane's loads issue back to back.
-    uint32_t vals[REG ? NJ : 1];
-    auto load_key = [&](int j) -> uint32_t {
-        const int i = lo + kWave * j + lane;
-        const uint32_t v = __builtin_bit_cast(uint32_t, S[min(i, T - 1)]);
-        return (i < hi && i >= s_end && i < r_start) ? v : kNone;
-    };
-    if (REG) {
+    uint32_t keys[4 * NR];
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) vals[j] = load_key(j);
-    }
-    // Applies f(j, key) to every element of this lane in j order.
-    auto for_each = [&](auto&& f) {
-        if (REG) {
+    for (int r = 0; r < NR; ++r)
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) f(j, vals[j]);
-        } else {
-            for (int j = 0; j < nj; ++j) f(j, load_key(j));
-        }
-    };
+        for (int e = 0; e < 4; ++e)
+            keys[4 * r + e] = key_of(S, g, p * a.part + r * kRound + wave * 256 + e * 64 + lane);
+    for (int x = tid; x < 2048; x += kSelThreads) hist[x] = 0u;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 4 * NR; ++j)
+        if (keys[j] != kNone) atomicAdd(&hist[bin12(keys[j])], 1u);
+    __syncthreads();
 
-    const bool use_mask = T <= kMaskWords * 32;
-    uint32_t tau = kNone;   // nothing from the middle span unless selection runs
-    int need = 0;
+    const size_t up = (size_t)u * a.parts + p;
+    uint4* dst = reinterpret_cast<uint4*>(a.hist + up * 2048);
+    const uint4* src = reinterpret_cast<const uint4*>(hist);
+    dst[tid] = src[tid];
+    dst[tid + kSelThreads] = src[tid + kSelThreads];
+    // coarse bin t>>2 = fine bins [32*(t>>2), +32): 4 threads of 8 bins each
+    uint32_t s = 0u;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) s += hist[8 * tid + q];
+    s += (uint32_t)__shfl_xor((int)s, 1, kWave);
+    s += (uint32_t)__shfl_xor((int)s, 2, kWave);
+    if ((tid & 3) == 0) a.coarse[up * 64 + (tid >> 2)] = s;
+}
+
+// ---------------------------------------------------------------------------
+// Kernel 2: threshold bin, bitmask words and candidate segments.
+// grid = (parts, units).
+// ---------------------------------------------------------------------------
+template <int NR>
+__global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) {
+    const int p = blockIdx.x, u = blockIdx.y;
+    const int b = u / a.n_kv_heads;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const Geom g = geom_of(a, b);
+    if (p >= g.parts) return;
+    const float* S = a.scores + (size_t)u * a.max_ctx;
+    const size_t up0 = (size_t)u * a.parts;   // first slot of this unit
+    uint32_t* mask = a.mask + (size_t)u * (a.parts * (a.part / 32));
+
+    __shared__ uint32_t red[256];
+    __shared__ int wave_tot[kSelWaves];
+    __shared__ int sh[4];
+
+    // Issue the score loads first; the threshold search below hides them.
+    uint32_t keys[4 * NR];
+#pragma unroll
+    for (int r = 0; r < NR; ++r)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            keys[4 * r + e] = key_of(S, g, p * a.part + r * kRound + wave * 256 + e * 64 + lane);
+
+    // ---- bin d1 and the count still needed from it ------------------------
     uint32_t d1 = 0u;
-    const bool simple = all_mid || take == 0;   // no radix select needed
-    bool fast = use_mask;                       // candidate list + bitmask path
-
-    if (!simple) {
-        // Pass 1: bits 31..20 (the sign bit is 0: 11 significant bits).
-        for (int x = tid; x < 2048; x += kSelThreads) hist[x] = 0u;
-        __syncthreads();
-        for_each([&](int, uint32_t k) {
-            atomicAdd(&hist[(k >> 20) & 2047u], k != kNone ? 1u : 0u);
-        });
-        __syncthreads();
-        find_digit<2048>(hist, take, &sh_digit, &sh_above, wave_tot);
-        d1 = sh_digit;
-        need = take - sh_above;               // entries still needed from bin d1
-        fast = fast && hist[d1] <= (uint32_t)kCandCap;
-        __syncthreads();
-    }
-
-    if (use_mask && (fast || simple)) {
-        // ---- bitmask path -------------------------------------------------
-        // sink, recent, and middle positions above bin d1 (or every middle
-        // position when all fit); 64 consecutive positions are two words.
-        // Candidates (bin d1) go to this wave's segment of the list.
-        int run = 0;
-        for_each([&](int j, uint32_t k) {
-            const int i = lo + kWave * j + lane;
-            const bool valid = i < hi;
-            const bool edge = valid && (i < s_end || i >= r_start);
-            const bool mid = k != kNone;
-            const uint32_t dg = (k >> 20) & 2047u;
-            const bool def = edge || (mid && (simple ? all_mid : dg > d1));
-            const bool cand = !simple && mid && dg == d1;
-            const uint64_t m = ballot(def);
-            const int w0 = (lo + kWave * j) >> 5;
-            if (lane < 2 && w0 + lane < kMaskWords)
-                mask[w0 + lane] = lane == 0 ? (uint32_t)m : (uint32_t)(m >> 32);
-            const uint64_t cm = ballot(cand);
-            const int slot = run + (int)lanes_below(cm);
-            if (cand && slot < kSegCap) {
-                cand_key[wave * kSegCap + slot] = k;
-                cand_pos[wave * kSegCap + slot] = i;
-            }
-            run += __builtin_popcountll(cm);
-        });
-        if (tid == 0) sh_overflow = 0;
-        __syncthreads();
-        if (lane == 0) {
-            seg_count[wave] = min(run, kSegCap);
-            if (run > kSegCap) sh_overflow = 1;
-        }
-        __syncthreads();
-        fast = !simple && !sh_overflow;
-    }
-    if (use_mask && (fast || simple)) {
-        if (!simple) {
-            // candidate x lives at segment x / kSegCap, offset x % kSegCap
-            auto cand_ok = [&](int x) { return (x % kSegCap) < seg_count[x / kSegCap]; };
-            const int nc = kCandCap;
-            // passes 2 and 3 over the candidates (all share the top 12 bits)
-            uint32_t prefix = d1 << 20;
+    int need = 0;
+    if (!g.simple) {
+        {   // coarse totals: thread t sums coarse bin t&63 over partitions q, q+4, ...
+            const int cb = tid & 63, q = tid >> 6;
+            uint32_t s = 0u;
+            for (int p0 = q; p0 < g.parts; p0 += 4 * 8) {
+                uint32_t v[8];
 #pragma unroll
-            for (int pass = 0; pass < 2; ++pass) {
-                const int shift = pass == 0 ? 10 : 0;
-                const uint32_t pmask = pass == 0 ? 0xfff00000u : 0xfffffc00u;
-                hist[tid] = 0u;
-                __syncthreads();
-                for (int x = tid; x < nc; x += kSelThreads) {
-                    const uint32_t k = cand_key[x];
-                    if (cand_ok(x) && (k & pmask) == prefix) atomicAdd(&hist[(k >> shift) & 1023u], 1u);
+                for (int j = 0; j < 8; ++j) {
+                    const int pp = p0 + 4 * j;
+                    v[j] = pp < g.parts ? a.coarse[(up0 + pp) * 64 + cb] : 0u;
                 }
-                __syncthreads();
-                find_digit<1024>(hist, need, &sh_digit, &sh_above, wave_tot);
-                prefix |= sh_digit << shift;
-                need -= sh_above;
-                __syncthreads();
+#pragma unroll
+                for (int j = 0; j < 8; ++j) s += v[j];
             }
-            tau = prefix;
-            const int n_ties = (int)hist[tau & 1023u];
-            __syncthreads();
-            // mark candidates above tau, and the `need` lowest-position ties
-            for (int x = tid; x < nc; x += kSelThreads) {
-                if (!cand_ok(x)) continue;
-                const uint32_t k = cand_key[x];
-                bool sel = k > tau;
-                if (k == tau) {
-                    if (need >= n_ties) {
-                        sel = true;
-                    } else {
-                        const int p = cand_pos[x];
-                        int rank = 0;
-                        for (int y = 0; y < nc; ++y)
-                            rank += (cand_ok(y) && cand_key[y] == tau && cand_pos[y] < p);
-                        sel = rank < need;
-                    }
-                }
-                if (sel) {
-                    const int p = cand_pos[x];
-                    atomicOr(&mask[p >> 5], 1u << (p & 31));
-                }
-            }
-            __syncthreads();
+            red[q * 64 + cb] = s;
         }
-        // ---- ordered emission from the bitmask ------------------------------
-        const int n_words = (T + 31) >> 5;
-        const int wpt = (n_words + kSelThreads - 1) / kSelThreads;
-        const int w_lo = min(tid * wpt, n_words), w_hi = min(w_lo + wpt, n_words);
-        int cnt = 0;
-        for (int w = w_lo; w < w_hi; ++w) cnt += __builtin_popcount(mask[w]);
-        int total = 0;
-        int pos = block_exclusive_scan(cnt, wave_tot, &total);
-        for (int w = w_lo; w < w_hi; ++w) {
-            uint32_t m = mask[w];
-            while (m) {
-                const int bit = __builtin_ctz(m);
-                m &= m - 1u;
-                if (pos < a.budget) out[pos] = w * 32 + bit;
-                ++pos;
+        __syncthreads();
+        if (wave == 0) {
+            const int cb = 63 - lane;   // descending
+            const int tot = (int)(red[cb] + red[64 + cb] + red[128 + cb] + red[192 + cb]);
+            int incl = tot;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const int v = __shfl_up(incl, off, kWave);
+                if (lane >= off) incl += v;
+            }
+            const int above = incl - tot;
+            if (above < g.take && g.take <= incl) {
+                sh[0] = cb;
+                sh[1] = above;
             }
         }
-        if (c == 0 && tid == 0) a.n_idx[b] = total;
-        return;
+        __syncthreads();
+        const int dc = sh[0] & 63, above_c = sh[1];   // (mask: malformed scores stay in bounds)
+        {   // fine totals of coarse bin dc: thread t sums fine bin t&31 over partitions q, q+8, ...
+            const int fb = tid & 31, q = tid >> 5;
+            uint32_t s = 0u;
+            for (int p0 = q; p0 < g.parts; p0 += 8 * 4) {
+                uint32_t v[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int pp = p0 + 8 * j;
+                    v[j] = pp < g.parts ? a.hist[(up0 + pp) * 2048 + dc * 32 + fb] : 0u;
+                }
+#pragma unroll
+                for (int j = 0; j < 4; ++j) s += v[j];
+            }
+            red[q * 32 + fb] = s;
+        }
+        __syncthreads();
+        if (wave == 0) {
+            const int fb = 31 - (lane & 31);
+            int tot = 0;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) tot += (int)red[q * 32 + fb];
+            tot = lane < 32 ? tot : 0;
+            int incl = tot;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const int v = __shfl_up(incl, off, kWave);
+                if (lane >= off) incl += v;
+            }
+            const int above = above_c + incl - tot;
+            if (lane < 32 && above < g.take && g.take <= above + tot) {
+                sh[2] = dc * 32 + fb;
+                sh[3] = g.take - above;
+            }
+        }
+        __syncthreads();
+        d1 = (uint32_t)sh[2];
+        need = sh[3];
     }
 
-    // ---- general path: radix over all middle scores, ordered compaction ----
-    if (!simple) {
-        uint32_t prefix = d1 << 20;
+    // ---- bitmask words and bin-d1 candidates of this partition -------------
+    const uint64_t lt = (1ull << lane) - 1ull;
+    uint2* seg = a.seg + (up0 + p) * a.part;
+    int run = 0;   // candidates of this partition so far (uniform)
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        const int base = p * a.part + r * kRound + wave * 256;
+        uint64_t defb[4], candb[4];
+        int n_w = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int i = base + e * 64 + lane;
+            const uint32_t k = keys[4 * r + e];
+            const bool mid = k != kNone;
+            const uint32_t dg = bin12(k);
+            const bool def = is_edge(g, i) || (mid && (g.simple ? g.all_mid : dg > d1));
+            const bool cand = !g.simple && mid && dg == d1;
+            defb[e] = __ballot(def);
+            candb[e] = __ballot(cand);
+            n_w += __builtin_popcountll(candb[e]);
+        }
+        if (lane < 8) {
+            const uint64_t m = lane < 2 ? defb[0] : lane < 4 ? defb[1] : lane < 6 ? defb[2] : defb[3];
+            mask[base / 32 + lane] = (lane & 1) ? (uint32_t)(m >> 32) : (uint32_t)m;
+        }
+        if (!g.simple) {
+            int round_total;
+            int slot = run + block_scan(lane == 0 ? n_w : 0, wave_tot, &round_total);
+            slot = __shfl(slot, 0, kWave);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if ((candb[e] >> lane) & 1ull)
+                    seg[slot + __builtin_popcountll(candb[e] & lt)] =
+                        make_uint2(keys[4 * r + e], (uint32_t)(base + e * 64 + lane));
+                slot += __builtin_popcountll(candb[e]);
+            }
+            run += round_total;
+        }
+    }
+    if (tid == 0) {
+        a.cnt[up0 + p] = (uint32_t)run;
+        if (p == 0) {
+            a.thr[2 * u] = d1;
+            a.thr[2 * u + 1] = (uint32_t)need;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Kernel 3: exact threshold, ties and ordered emission.  grid = units.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kSelThreads) void select_finish_kernel(SelectArgs a) {
+    const int u = blockIdx.x;
+    const int b = u / a.n_kv_heads;
+    const int c_head = u - b * a.n_kv_heads;
+    const int tid = threadIdx.x;
+    const Geom g = geom_of(a, b);
+    const size_t up0 = (size_t)u * a.parts;
+    const uint32_t* mask = a.mask + (size_t)u * (a.parts * (a.part / 32));
+
+    __shared__ int wave_tot[kSelWaves];
+    __shared__ int sh[2];
+    __shared__ uint32_t h1024[1024];
+    __shared__ int offs[kMaxSelectParts + 1];
+    __shared__ uint2 cand_lds[kTailCand];
+    __shared__ uint32_t lmask[kTailWords];
+
+    // The first bitmask chunk is loaded up front (all loads in flight at once)
+    // and parked in LDS once the candidate offsets are known.
+    constexpr int kWordsPerThread = kTailWords / kSelThreads;
+    const int n_words = (g.T + 31) >> 5;
+    uint32_t mw[kWordsPerThread];
+#pragma unroll
+    for (int j = 0; j < kWordsPerThread; ++j) {
+        const int x = tid + j * kSelThreads;
+        mw[j] = x < n_words ? mask[x] : 0u;
+    }
+
+    // Candidate offsets: partition pp owns [offs[pp], offs[pp+1]) of the
+    // concatenated list, which is in position order.
+    {
+        const int per = (g.parts + kSelThreads - 1) / kSelThreads;
+        const int q0 = min(g.parts, tid * per), q1 = min(g.parts, q0 + per);
+        int s = 0;
+        for (int q = q0; q < q1; ++q) s += (int)a.cnt[up0 + q];
+        int nc_all;
+        int o = block_scan(s, wave_tot, &nc_all);
+        for (int q = q0; q < q1; ++q) {
+            offs[q] = o;
+            o += (int)a.cnt[up0 + q];
+        }
+        if (tid == 0) offs[g.parts] = nc_all;
+        __syncthreads();
+    }
+    const int nc = g.simple ? 0 : offs[g.parts];
+    const bool cached = nc <= kTailCand;
+    auto cand_global = [&](int x) -> uint2 {
+        int lo = 0, hi = g.parts - 1;   // last partition whose offset is <= x
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (offs[mid] <= x) lo = mid; else hi = mid - 1;
+        }
+        return a.seg[(up0 + lo) * a.part + (x - offs[lo])];
+    };
+    auto cand = [&](int x) -> uint2 { return cached ? cand_lds[x] : cand_global(x); };
+
+    uint32_t tau = 0u;
+    int need = 0;
+    if (!g.simple) {
+        need = (int)a.thr[2 * u + 1];
+        if (cached) {
+            constexpr int U = 8;   // loads in flight per thread
+            for (int x0 = tid; x0 < nc; x0 += U * kSelThreads) {
+                uint2 v[U];
+#pragma unroll
+                for (int j = 0; j < U; ++j) {
+                    const int x = x0 + j * kSelThreads;
+                    v[j] = x < nc ? cand_global(x) : make_uint2(0u, 0u);
+                }
+#pragma unroll
+                for (int j = 0; j < U; ++j) {
+                    const int x = x0 + j * kSelThreads;
+                    if (x < nc) cand_lds[x] = v[j];
+                }
+            }
+            __syncthreads();
+        }
+        uint32_t prefix = a.thr[2 * u] << 20;
 #pragma unroll
         for (int pass = 0; pass < 2; ++pass) {
             const int shift = pass == 0 ? 10 : 0;
             const uint32_t pmask = pass == 0 ? 0xfff00000u : 0xfffffc00u;
-            hist[tid] = 0u;
+            for (int x = tid; x < 1024; x += kSelThreads) h1024[x] = 0u;
             __syncthreads();
-            for_each([&](int, uint32_t k) {
-                if (k != kNone && (k & pmask) == prefix) atomicAdd(&hist[(k >> shift) & 1023u], 1u);
-            });
+            for (int x = tid; x < nc; x += kSelThreads) {
+                const uint32_t k = cand(x).x;
+                if ((k & pmask) == prefix) atomicAdd(&h1024[(k >> shift) & 1023u], 1u);
+            }
             __syncthreads();
-            find_digit<1024>(hist, need, &sh_digit, &sh_above, wave_tot);
-            prefix |= sh_digit << shift;
-            need -= sh_above;
+            find_digit<1024>(h1024, need, sh, wave_tot);
+            prefix |= (uint32_t)sh[0] << shift;
+            need -= sh[1];
             __syncthreads();
         }
         tau = prefix;
     }
-    auto classify = [&](int j, uint32_t k, bool& edge, bool& gt, bool& tie) {
-        const int i = lo + kWave * j + lane;
-        edge = i < hi && (i < s_end || i >= r_start);
-        const bool mid = k != kNone;
-        gt = mid && (all_mid || (take > 0 && k > tau));
-        tie = mid && !all_mid && take > 0 && k == tau;
-    };
-    int nontie = 0, ties = 0;
-    for_each([&](int j, uint32_t k) {
-        bool edge, gt, tie;
-        classify(j, k, edge, gt, tie);
-        nontie += __builtin_popcountll(ballot(edge || gt));
-        ties += __builtin_popcountll(ballot(tie));
-    });
-    if (lane == 0) { w_nontie[wave] = nontie; w_ties[wave] = ties; }
-    __syncthreads();
-    int out_base = 0, tie_base = 0;
-    for (int w = 0; w < wave; ++w) {
-        out_base += w_nontie[w] + min(max(need - tie_base, 0), w_ties[w]);
-        tie_base += w_ties[w];
+    // Ties: thread t ranks the contiguous slice [x0, x1) of the list.
+    const int per = (nc + kSelThreads - 1) / kSelThreads;
+    const int x0 = min(nc, tid * per), x1 = min(nc, x0 + per);
+    int tie_base = 0;
+    if (!g.simple) {
+        int nt = 0;
+        for (int x = x0; x < x1; ++x) nt += cand(x).x == tau;
+        int tie_total;
+        tie_base = block_scan(nt, wave_tot, &tie_total);
     }
-    int tie_run = 0, out_run = 0;
-    for_each([&](int j, uint32_t k) {
-        bool edge, gt, tie;
-        classify(j, k, edge, gt, tie);
-        const uint64_t tmask = ballot(tie);
-        const bool take_tie = tie && (tie_base + tie_run + (int)lanes_below(tmask)) < need;
-        const bool sel = edge || gt || take_tie;
-        const uint64_t smask = ballot(sel);
-        const int pos = out_base + out_run + (int)lanes_below(smask);
-        if (sel && pos < a.budget) out[pos] = lo + kWave * j + lane;
-        tie_run += __builtin_popcountll(tmask);
-        out_run += __builtin_popcountll(smask);
-    });
-    if (c == 0 && tid == 0) {
-        int total = 0, tb = 0;
-        for (int w = 0; w < kSelWaves; ++w) {
-            total += w_nontie[w] + min(max(need - tb, 0), w_ties[w]);
-            tb += w_ties[w];
+    int32_t* out = a.idx + (size_t)u * a.budget;
+    int emitted = 0;
+    for (int cw = 0; cw < n_words; cw += kTailWords) {
+        const int nw = min(kTailWords, n_words - cw);
+        if (cw == 0) {
+#pragma unroll
+            for (int j = 0; j < kWordsPerThread; ++j) lmask[tid + j * kSelThreads] = mw[j];
+        } else {
+            for (int x = tid; x < nw; x += kSelThreads) lmask[x] = mask[cw + x];
         }
-        a.n_idx[b] = total;
+        __syncthreads();
+        if (!g.simple) {
+            int rank = tie_base;
+            for (int x = x0; x < x1; ++x) {
+                const uint2 kp = cand(x);
+                bool sel = kp.x > tau;
+                if (kp.x == tau) {
+                    sel = rank < need;
+                    ++rank;
+                }
+                const int w = (int)(kp.y >> 5) - cw;
+                if (sel && w >= 0 && w < nw) atomicOr(&lmask[w], 1u << (kp.y & 31u));
+            }
+            __syncthreads();
+        }
+        const int wpt = (nw + kSelThreads - 1) / kSelThreads;
+        const int w0 = min(nw, tid * wpt), w1 = min(nw, w0 + wpt);
+        int cnt = 0;
+        for (int w = w0; w < w1; ++w) cnt += __builtin_popcount(lmask[w]);
+        int chunk_total;
+        int pos = emitted + block_scan(cnt, wave_tot, &chunk_total);
+        for (int w = w0; w < w1; ++w) {
+            uint32_t m = lmask[w];
+            while (m) {
+                const int bit = __builtin_ctz(m);
+                m &= m - 1u;
+                if (pos < a.budget) out[pos] = (cw + w) * 32 + bit;
+                ++pos;
+            }
+        }
+        emitted += chunk_total;
+        __syncthreads();
     }
+    if (c_head == 0 && tid == 0) a.n_idx[b] = emitted;
+}
+
+template <int NR>
+void launch_nr(const SelectArgs& a, int n_units, hipStream_t stream) {
+    const dim3 grid(a.parts, n_units), block(kSelThreads);
+    hipLaunchKernelGGL(select_hist_kernel<NR>, grid, block, 0, stream, a);
+    hipLaunchKernelGGL(select_mark_kernel<NR>, grid, block, 0, stream, a);
+    hipLaunchKernelGGL(select_finish_kernel, dim3(n_units), block, 0, stream, a);
 }
 
 }  // namespace
 
+int select_part_len(int max_t) {
+    int nr = 1;
+    while (nr < kSelectMaxRounds && (long long)nr * kRound * kSelectTargetParts < max_t) nr <<= 1;
+    return nr * kRound;
+}
+
 hipError_t launch_select(const SelectArgs& a, int n_units, hipStream_t stream) {
-    int max_t = 0;
-    for (int b = 0; b < a.batch; ++b) max_t = max(max_t, a.ctx[b]);
-    const dim3 grid(n_units), block(kSelThreads);
-    if (max_t <= kSelThreads * 16)
-        hipLaunchKernelGGL(select_kernel<16>, grid, block, 0, stream, a);
-    else if (max_t <= kSelThreads * 32)
-        hipLaunchKernelGGL(select_kernel<32>, grid, block, 0, stream, a);
-    else if (max_t <= kSelThreads * kRegPerLane)
-        hipLaunchKernelGGL(select_kernel<kRegPerLane>, grid, block, 0, stream, a);
-    else
-        hipLaunchKernelGGL(select_kernel<0>, grid, block, 0, stream, a);
+    switch (a.part / kRound) {
+        case 1: launch_nr<1>(a, n_units, stream); break;
+        case 2: launch_nr<2>(a, n_units, stream); break;
+        case 4: launch_nr<4>(a, n_units, stream); break;
+        case 8: launch_nr<8>(a, n_units, stream); break;
+        default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 

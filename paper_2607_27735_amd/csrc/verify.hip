@@ -30,27 +30,6 @@ namespace {
 
 using namespace vc;
 
-struct Item {
-    int b, c, s, nchunk, T, nq, key_begin, key_end, unit, item0;
-};
-
-__device__ __forceinline__ Item decode_item(const SeqTable& st, int item, int n_kv, int chunk) {
-    Item it;
-    int b = 0;
-    while (b + 1 < st.n_seq && item >= st.item_start[b + 1]) ++b;
-    it.b = b;
-    it.T = st.ctx[b];
-    it.nq = st.qlen[b];
-    it.nchunk = (it.T + chunk - 1) / chunk;
-    const int local = item - st.item_start[b];
-    it.c = local / it.nchunk;
-    it.s = local - it.c * it.nchunk;
-    it.key_begin = it.s * chunk;
-    it.key_end = min(it.key_begin + chunk, it.T);
-    it.unit = b * n_kv + it.c;
-    it.item0 = st.item_start[b] + it.c * it.nchunk;
-    return it;
-}
 
 // ---------------------------------------------------------------------------
 // Sweep 1: per-item row statistics from K only.
@@ -348,6 +327,12 @@ hipError_t launch_verify_nrt(const VerifyArgs& a, int n_items, int n_rows_total,
 }
 
 }  // namespace
+
+hipError_t launch_verify_combine(const VerifyArgs& a, int n_rows_total, hipStream_t stream) {
+    hipLaunchKernelGGL(verify_combine_kernel, dim3(n_rows_total), dim3(kCombineThreads), 0, stream,
+                       a);
+    return hipGetLastError();
+}
 
 hipError_t launch_verify(const VerifyArgs& a, int n_items, int n_rows_total, int row_tiles,
                          hipStream_t stream) {

@@ -128,5 +128,29 @@ struct KVTile {
     u32x4 v[8];
 };
 
+// A work item: (sequence b, KV head c, key chunk s) of a launch whose items
+// are numbered sequence by sequence, head by head, chunk by chunk.
+struct Item {
+    int b, c, s, nchunk, T, nq, key_begin, key_end, unit, item0;
+};
+
+__device__ __forceinline__ Item decode_item(const SeqTable& st, int item, int n_kv, int chunk) {
+    Item it;
+    int b = 0;
+    while (b + 1 < st.n_seq && item >= st.item_start[b + 1]) ++b;
+    it.b = b;
+    it.T = st.ctx[b];
+    it.nq = st.qlen[b];
+    it.nchunk = (it.T + chunk - 1) / chunk;
+    const int local = item - st.item_start[b];
+    it.c = local / it.nchunk;
+    it.s = local - it.c * it.nchunk;
+    it.key_begin = it.s * chunk;
+    it.key_end = min(it.key_begin + chunk, it.T);
+    it.unit = b * n_kv + it.c;
+    it.item0 = st.item_start[b] + it.c * it.nchunk;
+    return it;
+}
+
 }  // namespace vc
 }  // namespace ssl

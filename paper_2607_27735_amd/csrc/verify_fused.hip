@@ -1,22 +1,33 @@
 // verify_fused.hip -- single-sweep verify attention with fused Eq. 3 scores.
 //
 // The Eq. 3 score of a key needs the final normalizer of every verify row,
-// which no split of the context knows while it streams.  When every work item
-// of the call fits on the GPU at once, one sweep suffices:
+// which no split of the context knows while it streams.  When every chunk of
+// a (sequence, KV head) can be resident at once, one sweep suffices:
 //
 //   1. each workgroup streams its chunk of K and V once, runs an online
 //      softmax per verify row (P.V on the MFMA, as in the two-sweep kernel)
 //      and keeps the scaled logits of its chunk in LDS;
-//   2. it publishes its partial output and (running max, sum) per row, then
-//      waits at a per-(sequence, KV head) arrival counter until every chunk of
-//      that head has published (agent-scope release/acquire);
+//   2. it publishes its (running max, sum) per row and then a 64-bit call tag
+//      for its chunk, and waits until every chunk of its head shows the tag;
 //   3. from the merged (max, sum) of all chunks it forms the exact
 //      probabilities of its own keys from the LDS logits and writes their
-//      scores, and it combines one share of the head's output rows.
+//      scores, and writes its partial output already scaled to the exact
+//      normalizer, so that the two-sweep combine kernel only has to add the
+//      partials of each row.
 //
-// The launch is cooperative, so all workgroups are co-resident and the wait
-// always ends; it is additionally bounded, so a broken invariant cannot hang
-// the GPU (the results would then be wrong, never a fault).
+// Publication avoids agent-scope fences, which write back a whole L2 per wave
+// on this multi-XCD part: the few published words are written and read with
+// device-coherent (agent-scope relaxed atomic) stores and loads, and every
+// wave waits for its stores to complete before the tag is written.  The tags
+// need no initialisation: the host draws a fresh 64-bit tag for every call
+// from a process-wide sequence with a clock-seeded start, so a stale or
+// uninitialised word matches only by a 2^-64 accident.
+//
+// The wait ends: workgroups are dispatched in index order and the chunks of
+// one head are consecutive, so when the lowest unfinished head waits, every
+// workgroup ahead of its chunks has finished and its chunks (at most a few
+// per XCD) are resident.  The wait is also bounded, so a broken invariant
+// cannot hang the GPU (the results would then be wrong, never a fault).
 #include "verify_common.h"
 
 namespace ssl {
@@ -26,7 +37,6 @@ using namespace vc;
 
 constexpr int kStashPad = 4;          // floats of padding per stashed row
 constexpr int kSpinLimit = 1 << 22;   // bounded wait (far above any real wait)
-constexpr int kCombGroups = kThreads / 32;
 
 template <int NRT>
 constexpr int static_lds_bytes() {
@@ -35,11 +45,36 @@ constexpr int static_lds_bytes() {
            + kRowCap * 8                    // row_ml
            + kRowCap * 4                    // row_lse
            + kWaves * kRowCap * 8           // lse_part
-           + kCombGroups * 32 * 16          // comb
+           + kRowCap * 4                    // row_mw
            + 64;
 }
 
 __device__ __forceinline__ float safe_max(float m) { return m == -INFINITY ? 0.f : m; }
+
+// Device-coherent 32-bit store and load (agent scope, relaxed).
+__device__ __forceinline__ void st_dev(float* p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev(const float* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 ld_dev2(const float2* p) {
+    const float* f = reinterpret_cast<const float*>(p);
+    return make_float2(ld_dev(f), ld_dev(f + 1));
+}
+__device__ __forceinline__ void st_dev64(uint64_t* p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t ld_dev64(const uint64_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Waits until every store this wave issued has completed (vmcnt = 0); the
+// signal fences keep the compiler from moving memory accesses across it.
+__device__ __forceinline__ void wait_stores_done() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
 
 // One 32-key tile: logits to the LDS stash, online softmax, P.V.
 template <int NRT>
@@ -102,27 +137,22 @@ __device__ __forceinline__ void fused_tile(const VerifyArgs& a, const Rows<NRT>&
 template <int NRT>
 __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     const VerifyArgs& a = fa.v;
-    const FusedTable& ft = fa.ft;
-    extern __shared__ float stash[];            // [NRT*16][chunk + pad]
+    extern __shared__ __attribute__((aligned(16))) float stash[];   // [NRT*16][chunk + pad]
     __shared__ f32x4 red[NRT * 16][kHeadDim / 4];
     __shared__ float2 wml[kWaves][NRT * 16];
     __shared__ float2 row_ml[kRowCap];
     __shared__ float row_lse[kRowCap];
     __shared__ float2 lse_part[kWaves][kRowCap];
-    __shared__ f32x4 comb[kCombGroups][32];
+    __shared__ float row_mw[kRowCap];
 
     const int slot = blockIdx.x;
-    int u = 0;
-    while (u + 1 < ft.n_units && slot >= ft.slot_start[u + 1]) ++u;
-    const int unit = ft.unit[u];
-    const int b = unit / a.n_kv_heads, c = unit - b * a.n_kv_heads;
-    const int slot0 = ft.slot_start[u];
-    const int nchunk = ft.slot_start[u + 1] - slot0;
-    const int s = slot - slot0;
-    const int T = a.seq.ctx[b], nq = a.seq.qlen[b];
+    const Item it = decode_item(a.seq, slot, a.n_kv_heads, a.chunk);
+    const int unit = it.unit, b = it.b, c = it.c;
+    const int slot0 = it.item0, nchunk = it.nchunk;
+    const int T = it.T, nq = it.nq;
     const int R = nq * a.group;
-    const int chunk = ft.chunk;
-    const int key_begin = s * chunk, key_end = min(key_begin + chunk, T);
+    const int chunk = a.chunk;
+    const int key_begin = it.key_begin, key_end = it.key_end;
     const int stride = chunk + kStashPad;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int m16 = lane & 15, G = lane >> 4;
@@ -163,6 +193,19 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         if (G == 0) wml[wave][rt * 16 + m16] = make_float2(M[rt], L[rt]);
     }
     __syncthreads();
+    // Publish the row statistics first: their write-through latency overlaps
+    // the reduction of the partial outputs below.
+    if (tid < R) {
+        float Mw = -INFINITY, Lw = 0.f;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) Mw = fmaxf(Mw, wml[w][tid].x);
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) Lw += wml[w][tid].y * fast_exp2(wml[w][tid].x - safe_max(Mw));
+        float* pm = reinterpret_cast<float*>(a.part_ml + (size_t)slot * kRowCap + tid);
+        st_dev(pm, Mw);
+        st_dev(pm + 1, Lw);
+        row_mw[tid] = Mw;
+    }
     // rescale every wave's output to the workgroup's row maximum, then add
     // the waves in a fixed order
 #pragma unroll
@@ -195,30 +238,22 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         }
         __syncthreads();
     }
-    f32x4* po = reinterpret_cast<f32x4*>(a.part_o + (size_t)slot * kRowCap * kHeadDim);
-    for (int x = tid; x < R * (kHeadDim / 4); x += kThreads) po[x] = red[x >> 5][x & 31];
-    if (tid < R) {
-        float Mw = -INFINITY, Lw = 0.f;
-#pragma unroll
-        for (int w = 0; w < kWaves; ++w) Mw = fmaxf(Mw, wml[w][tid].x);
-#pragma unroll
-        for (int w = 0; w < kWaves; ++w) Lw += wml[w][tid].y * fast_exp2(wml[w][tid].x - safe_max(Mw));
-        a.part_ml[(size_t)slot * kRowCap + tid] = make_float2(Mw, Lw);
-    }
 
-    // ---- arrival barrier of this (sequence, KV head) -----------------------
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    // ---- wait for every chunk of this (sequence, KV head) -------------------
+    wait_stores_done();
     __syncthreads();
-    if (tid == 0) {
-        __hip_atomic_fetch_add(&fa.arrive[u], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (tid == 0) st_dev64(fa.tag + slot, fa.call_tag);
+    if (wave == 0) {
         int spins = 0;
-        while (__hip_atomic_load(&fa.arrive[u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <
-                   (uint32_t)nchunk &&
-               ++spins < kSpinLimit)
-            __builtin_amdgcn_s_sleep(1);
+        bool all_in;
+        do {
+            bool in = true;
+            for (int s2 = lane; s2 < nchunk; s2 += kWave) in &= ld_dev64(fa.tag + slot0 + s2) == fa.call_tag;
+            all_in = __all(in);
+            if (!all_in) __builtin_amdgcn_s_sleep(1);
+        } while (!all_in && ++spins < kSpinLimit);
     }
     __syncthreads();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
     // ---- 3a. exact row statistics over every chunk of the head -------------
     {
@@ -230,7 +265,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
 #pragma unroll
                 for (int uu = 0; uu < 8; ++uu) {
                     const int s2 = s0 + uu * kWaves;
-                    v[uu] = s2 < nchunk ? a.part_ml[(size_t)(slot0 + s2) * kRowCap + rr]
+                    v[uu] = s2 < nchunk ? ld_dev2(a.part_ml + (size_t)(slot0 + s2) * kRowCap + rr)
                                         : make_float2(-INFINITY, 0.f);
                 }
 #pragma unroll
@@ -254,72 +289,46 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         const int wn = min(a.window, nq);
         const int r0 = (nq - wn) * a.group;   // first window row
         float* srow = a.scores + (size_t)unit * a.max_ctx;
-        for (int kl = tid; kl < key_end - key_begin; kl += kThreads) {
-            float sc = 0.f;
-            for (int row = r0; row < R; ++row) sc += fast_exp2(stash[row * stride + kl] - row_lse[row]);
-            srow[key_begin + kl] = sc;
+        // four consecutive keys per thread (one 16-byte LDS read per row); the
+        // stash row stride and the chunk are multiples of 4 floats
+        const int nk = key_end - key_begin;
+        for (int k4 = 4 * tid; k4 < nk; k4 += 4 * kThreads) {
+            f32x4 sc = {0.f, 0.f, 0.f, 0.f};
+            for (int row = r0; row < R; ++row) {
+                const f32x4 y = *reinterpret_cast<const f32x4*>(stash + row * stride + k4);
+                const float l = row_lse[row];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) sc[i] += fast_exp2(y[i] - l);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (k4 + i < nk) srow[key_begin + k4 + i] = sc[i];
         }
     }
 
-    // ---- 3c. combine this item's share of the head's output rows ------------
-    const int d4 = tid & 31, sg = tid >> 5;
-    const f32x4* pall = reinterpret_cast<const f32x4*>(a.part_o);
-    for (int row = s; row < R; row += nchunk) {
-        const float Mr = safe_max(row_ml[row].x);
-        const float inv = 1.0f / row_ml[row].y;
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        for (int s0 = sg; s0 < nchunk; s0 += 8 * kCombGroups) {
-            f32x4 v[8];
-            float wgt[8];
-#pragma unroll
-            for (int uu = 0; uu < 8; ++uu) {
-                const int s2 = s0 + uu * kCombGroups;
-                const bool ok = s2 < nchunk;
-                const size_t sl = (size_t)(slot0 + (ok ? s2 : 0)) * kRowCap + row;
-                v[uu] = ok ? pall[sl * (kHeadDim / 4) + d4] : f32x4{0.f, 0.f, 0.f, 0.f};
-                wgt[uu] = ok ? fast_exp2(a.part_ml[sl].x - Mr) : 0.f;
-            }
-#pragma unroll
-            for (int uu = 0; uu < 8; ++uu) acc += v[uu] * wgt[uu];
+    // ---- 3c. this chunk's output, scaled to the exact normalizer ------------
+    // (the combine kernel adds the partials of each row)
+    {
+        const float* redf = reinterpret_cast<const float*>(&red[0][0]);
+        float* po = a.part_o + (size_t)slot * kRowCap * kHeadDim;
+        for (int x = tid; x < R * kHeadDim; x += kThreads) {
+            const int row = x >> 7;
+            po[x] = redf[x] * fast_exp2(safe_max(row_mw[row]) - row_lse[row]);
         }
-        comb[sg][d4] = acc;
-        __syncthreads();
-        if (sg == 0) {
-            f32x4 o = comb[0][d4];
-#pragma unroll
-            for (int gq = 1; gq < kCombGroups; ++gq) o += comb[gq][d4];
-            o *= inv;
-            const int j = row / a.group;
-            const int h = c * a.group + (row - j * a.group);
-            const size_t base = (((size_t)b * a.max_q + j) * a.n_q_heads + h) * kHeadDim + 4 * d4;
-            if (a.out_fp32) {
-                *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out) + base) = o;
-            } else {
-                uint2 pk = make_uint2(pack_bf16(o[0], o[1]), pack_bf16(o[2], o[3]));
-                *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + base) = pk;
-            }
-        }
-        __syncthreads();
     }
-}
-
-__global__ void zero_u32_kernel(uint32_t* p, int n) {
-    for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0u;
 }
 
 template <int NRT>
-hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, hipStream_t stream) {
-    const size_t dyn = (size_t)NRT * 16 * (a.ft.chunk + kStashPad) * sizeof(float);
+hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, int n_rows_total,
+                            hipStream_t stream) {
+    const size_t dyn = (size_t)NRT * 16 * (a.v.chunk + kStashPad) * sizeof(float);
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(verify_fused_kernel<NRT>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(zero_u32_kernel, dim3(1), dim3(256), 0, stream, a.arrive, a.ft.n_units);
+    hipLaunchKernelGGL(verify_fused_kernel<NRT>, dim3(n_slots), dim3(kThreads), dyn, stream, a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    FusedArgs local = a;
-    void* args[] = {&local};
-    return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(verify_fused_kernel<NRT>),
-                                      dim3(n_slots), dim3(kThreads), args, (unsigned)dyn, stream);
+    return launch_verify_combine(a.v, n_rows_total, stream);
 }
 
 }  // namespace
@@ -337,12 +346,13 @@ int fused_max_chunk(int row_tiles) {
     return (floats_per_row - kStashPad) / 128 * 128;
 }
 
-hipError_t launch_verify_fused(const FusedArgs& a, int n_slots, int row_tiles, hipStream_t stream) {
+hipError_t launch_verify_fused(const FusedArgs& a, int n_slots, int n_rows_total, int row_tiles,
+                               hipStream_t stream) {
     switch (row_tiles) {
-        case 1: return launch_fused_nrt<1>(a, n_slots, stream);
-        case 2: return launch_fused_nrt<2>(a, n_slots, stream);
-        case 3: return launch_fused_nrt<3>(a, n_slots, stream);
-        default: return launch_fused_nrt<4>(a, n_slots, stream);
+        case 1: return launch_fused_nrt<1>(a, n_slots, n_rows_total, stream);
+        case 2: return launch_fused_nrt<2>(a, n_slots, n_rows_total, stream);
+        case 3: return launch_fused_nrt<3>(a, n_slots, n_rows_total, stream);
+        default: return launch_fused_nrt<4>(a, n_slots, n_rows_total, stream);
     }
 }
 

@@ -93,12 +93,13 @@ def test_verify_validation(lib):
     assert _verify(lib, params=_params(sm_scale=float("nan"))) == B.SSL_ERR_SHAPE
     assert _verify(lib, params=_params(verify_mode=3)) == B.SSL_ERR_SHAPE
     assert _verify(lib, params=_params(verify_mode=-1)) == B.SSL_ERR_SHAPE
-    # a one-sweep request that cannot have every chunk resident at once
+    # one-sweep requests whose (sequence, KV head) would need more than 128
+    # resident chunks: 2^20 keys, and 49153 keys at 64 rows (384-key chunks)
     big = _shape(max_ctx=1 << 20)
     assert _verify(lib, shape=big, ctx=(1 << 20,), params=_params(verify_mode=2)) == \
         B.SSL_ERR_UNSUPPORTED
-    many = _shape(batch=20, n_q_heads=64, n_kv_heads=8)
-    assert _verify(lib, shape=many, ctx=(128,) * 20, ql=(2,) * 20,
+    rows64 = _shape(n_q_heads=64, n_kv_heads=8, max_ctx=65536, max_q=8)
+    assert _verify(lib, shape=rows64, ctx=(128 * 384 + 1,), ql=(8,),
                    params=_params(verify_mode=2)) == B.SSL_ERR_UNSUPPORTED
     for name in ("q", "k", "v", "out", "scores"):
         assert _verify(lib, **{name: None}) == B.SSL_ERR_NULL, name
@@ -152,7 +153,14 @@ def test_select_validation(lib):
     ca, cp = _i32(4096)
     s, p = _shape(), _params()
     assert lib.ssl_select_workspace(ctypes.byref(s), ctypes.byref(p), cp, ctypes.byref(n)) == 0
-    assert n.value == 0
+    assert n.value > 0
+    assert _select(lib) == B.SSL_ERR_WORKSPACE          # a workspace is required
+    ca2, cp2 = _i32(1 << 21)
+    s2 = _shape(max_ctx=1 << 22)
+    assert lib.ssl_select_workspace(ctypes.byref(s2), ctypes.byref(p), cp2, ctypes.byref(n)) == 0
+    ca3, cp3 = _i32((1 << 21) + 1)                       # beyond 256 partitions of 8192
+    assert lib.ssl_select_workspace(ctypes.byref(s2), ctypes.byref(p), cp3,
+                                    ctypes.byref(n)) == B.SSL_ERR_UNSUPPORTED
 
 
 def _draft(lib, shape=None, params=None, nidx=(256,), q=FAKE, k=FAKE, v=FAKE, idx=FAKE, out=FAKE,
@@ -209,10 +217,11 @@ def test_binding_refuses_cpu_tensors(lib):
 
 
 def test_verify_plan_schedules(lib):
-    """Schedules of the named workloads: AUTO runs two sweeps; one sweep fits at
-    4K and 32K only."""
+    """Schedules of the named workloads: one sweep fits wherever a (sequence,
+    KV head) needs at most 128 chunks of what the LDS logit stash holds (all
+    but the 131K context), and AUTO takes it there; TWO_SWEEP always plans."""
     from paper_2607_27735_amd.workloads import CONFIGS
-    fits = {1: True, 2: True, 3: False, 4: False, 5: False}
+    fits = {1: True, 2: True, 3: True, 4: False, 5: True}
     for n, cfg in CONFIGS.items():
         batch = cfg["batch"]
         ctx = cfg.get("ctx_len") or [cfg["ctx_range"][1]] * batch
@@ -220,12 +229,17 @@ def test_verify_plan_schedules(lib):
         shape = B.Shape(batch, cfg["n_q_heads"], cfg["n_kv_heads"], 128,
                         cfg.get("max_ctx") or max(ctx), max(ql))
         sch, chunk, items = B.verify_plan(shape, B.make_params(1 / math.sqrt(128)), ctx, ql)
-        assert sch == B.VERIFY_TWO_SWEEP, n
+        assert sch == (B.VERIFY_ONE_SWEEP if fits[n] else B.VERIFY_TWO_SWEEP), n
         assert chunk % 128 == 0 and items >= 1
+        two = B.make_params(1 / math.sqrt(128), verify_mode=B.VERIFY_TWO_SWEEP)
+        sch, chunk, items = B.verify_plan(shape, two, ctx, ql)
+        assert sch == B.VERIFY_TWO_SWEEP and chunk >= 128
         one = B.make_params(1 / math.sqrt(128), verify_mode=B.VERIFY_ONE_SWEEP)
         if fits[n]:
             sch, chunk, items = B.verify_plan(shape, one, ctx, ql)
-            assert sch == B.VERIFY_ONE_SWEEP and items <= 256 and chunk % 128 == 0
+            assert sch == B.VERIFY_ONE_SWEEP and chunk % 128 == 0
+            assert all(-(-t // chunk) <= 128 for t in ctx)
+            assert items == sum(cfg["n_kv_heads"] * -(-t // chunk) for t in ctx)
         else:
             with pytest.raises(B.SSLError):
                 B.verify_plan(shape, one, ctx, ql)

@@ -175,6 +175,34 @@ def test_select_special_cases():
             assert np.array_equal(idx[b, :, :n_ref[b]], idx_ref[b, :, :n_ref[b]])
 
 
+def test_select_long_contexts():
+    """Contexts long enough that one (sequence, KV head) spans many partitions,
+    several rounds per partition and more than one emission chunk; with
+    quantised or equal scores the threshold bin holds far more candidates than
+    the finishing workgroup caches.  Bit-exact against the oracle."""
+    from types import SimpleNamespace
+    rng = np.random.default_rng(11)
+    for ctx in ([140001, 65537], [262144, 3], [40000, 33000]):
+        w = SimpleNamespace(batch=2, n_q_heads=4, n_kv_heads=2, max_ctx=max(ctx),
+                            ctx_len=np.array(ctx, dtype=np.int32), sm_scale=1.0, window=16,
+                            k_sink=4, k_recent=32, budget=4096)
+        shape = (w.batch, w.n_kv_heads, w.max_ctx)
+        cases = {
+            "lognormal": np.exp(rng.normal(-8.0, 1.0, shape)).astype(np.float32),
+            "quantized-ties": (rng.integers(0, 3, shape) / 2.0).astype(np.float32),
+            "all-equal": np.full(shape, 0.25, np.float32),
+        }
+        for label, s32 in cases.items():
+            for budget in (4096, 20000):
+                print(f"select long ctx={ctx} {label} budget={budget}", flush=True)
+                idx_ref, n_ref = oracle.select(w, s32.astype(np.float64), budget=budget)
+                idx, n_idx = gpu_select(w, s32, budget=budget)
+                assert np.array_equal(n_idx, n_ref), (ctx, label, budget)
+                for b in range(w.batch):
+                    assert np.array_equal(idx[b, :, :n_ref[b]], idx_ref[b, :, :n_ref[b]]), \
+                        (ctx, label, budget, b)
+
+
 def test_draft_full_budget_equals_dense():
     """Sparse attention with every position selected is dense attention: the
     draft kernel over idx = [0, T) equals the verify kernel with one row."""
