@@ -66,6 +66,18 @@ __device__ __forceinline__ float row16_sum(float x) {
     return x;
 }
 
+// Inclusive prefix sum over the 64 lanes of a wave: shifts within rows of 16
+// lanes, then the row broadcasts of lanes 15 and 31 (DPP, no LDS traffic).
+__device__ __forceinline__ int wave_incl_scan(int x) {
+    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);   // row_shr:1
+    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);   // row_shr:2
+    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);   // row_shr:4
+    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);   // row_shr:8
+    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);   // row_bcast:15 -> rows 1, 3
+    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);   // row_bcast:31 -> rows 2, 3
+    return x;
+}
+
 __device__ __forceinline__ float shfl_xor_f(float x, int mask) {
     return __shfl_xor(x, mask, kWave);
 }

@@ -59,20 +59,11 @@ __device__ __forceinline__ uint32_t key_of(const float* S, const Geom& g, int i)
     return (i >= g.s_end && i < g.r_start) ? v : kNone;
 }
 
-__device__ __forceinline__ bool is_edge(const Geom& g, int i) {
-    return i < g.T && (i < g.s_end || i >= g.r_start);
-}
-
 // Exclusive prefix sum of one value per thread over the workgroup; *total gets
 // the sum.  wave_tot is LDS scratch of kSelWaves words.
 __device__ __forceinline__ int block_scan(int v, int* wave_tot, int* total) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int incl = v;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const int u = __shfl_up(incl, off, kWave);
-        if (lane >= off) incl += u;
-    }
+    const int incl = wave_incl_scan(v);
     __syncthreads();
     if (lane == 63) wave_tot[wave] = incl;
     __syncthreads();
@@ -85,35 +76,6 @@ __device__ __forceinline__ int block_scan(int v, int* wave_tot, int* total) {
     }
     *total = all;
     return before + incl - v;
-}
-
-// In a histogram of NBINS bins read from the top bin down, finds the bin where
-// the running count first reaches `remaining` (1 <= remaining <= the total)
-// and the count strictly above that bin; the result goes to sh[0] (bin) and
-// sh[1] (count above).
-template <int NBINS>
-__device__ __forceinline__ void find_digit(const uint32_t* h, int remaining, int* sh,
-                                           int* wave_tot) {
-    constexpr int PER = NBINS / kSelThreads;
-    const int tid = threadIdx.x;
-    int c[PER];
-    int sum = 0;
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-        c[q] = (int)h[NBINS - 1 - PER * tid - q];
-        sum += c[q];
-    }
-    int total;
-    int above = block_scan(sum, wave_tot, &total);
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-        if (above < remaining && remaining <= above + c[q]) {
-            sh[0] = NBINS - 1 - PER * tid - q;
-            sh[1] = above;
-        }
-        above += c[q];
-    }
-    __syncthreads();
 }
 
 // ---------------------------------------------------------------------------
@@ -166,7 +128,7 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
     const int b = u / a.n_kv_heads;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const Geom g = geom_of(a, b);
-    if (p >= g.parts) return;
+    if (p >= g.parts || g.simple) return;   // the finish kernel emits ranges then
     const float* S = a.scores + (size_t)u * a.max_ctx;
     const size_t up0 = (size_t)u * a.parts;   // first slot of this unit
     uint32_t* mask = a.mask + (size_t)u * (a.parts * (a.part / 32));
@@ -186,7 +148,7 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
     // ---- bin d1 and the count still needed from it ------------------------
     uint32_t d1 = 0u;
     int need = 0;
-    if (!g.simple) {
+    {
         {   // coarse totals: thread t sums coarse bin t&63 over partitions q, q+4, ...
             const int cb = tid & 63, q = tid >> 6;
             uint32_t s = 0u;
@@ -206,12 +168,7 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
         if (wave == 0) {
             const int cb = 63 - lane;   // descending
             const int tot = (int)(red[cb] + red[64 + cb] + red[128 + cb] + red[192 + cb]);
-            int incl = tot;
-#pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const int v = __shfl_up(incl, off, kWave);
-                if (lane >= off) incl += v;
-            }
+            const int incl = wave_incl_scan(tot);
             const int above = incl - tot;
             if (above < g.take && g.take <= incl) {
                 sh[0] = cb;
@@ -242,12 +199,7 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
 #pragma unroll
             for (int q = 0; q < 8; ++q) tot += (int)red[q * 32 + fb];
             tot = lane < 32 ? tot : 0;
-            int incl = tot;
-#pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const int v = __shfl_up(incl, off, kWave);
-                if (lane >= off) incl += v;
-            }
+            const int incl = wave_incl_scan(tot);
             const int above = above_c + incl - tot;
             if (lane < 32 && above < g.take && g.take <= above + tot) {
                 sh[2] = dc * 32 + fb;
@@ -274,8 +226,8 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
             const uint32_t k = keys[4 * r + e];
             const bool mid = k != kNone;
             const uint32_t dg = bin12(k);
-            const bool def = is_edge(g, i) || (mid && (g.simple ? g.all_mid : dg > d1));
-            const bool cand = !g.simple && mid && dg == d1;
+            const bool def = mid && dg > d1;
+            const bool cand = mid && dg == d1;
             defb[e] = __ballot(def);
             candb[e] = __ballot(cand);
             n_w += __builtin_popcountll(candb[e]);
@@ -284,10 +236,10 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
             const uint64_t m = lane < 2 ? defb[0] : lane < 4 ? defb[1] : lane < 6 ? defb[2] : defb[3];
             mask[base / 32 + lane] = (lane & 1) ? (uint32_t)(m >> 32) : (uint32_t)m;
         }
-        if (!g.simple) {
+        {
             int round_total;
             int slot = run + block_scan(lane == 0 ? n_w : 0, wave_tot, &round_total);
-            slot = __shfl(slot, 0, kWave);
+            slot = __builtin_amdgcn_readlane(slot, 0);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 if ((candb[e] >> lane) & 1ull)
@@ -310,6 +262,54 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
 // ---------------------------------------------------------------------------
 // Kernel 3: exact threshold, ties and ordered emission.  grid = units.
 // ---------------------------------------------------------------------------
+
+struct Digit {
+    int bin, above, count;
+};
+
+// In a 1024-bin histogram read from the top bin down, finds the bin where the
+// running count first reaches `remaining` (1 <= remaining <= the total), the
+// count strictly above that bin and the bin's own count.  Every wave computes
+// it on its own (lane l holds bins 1008-16l .. 1023-16l), so no barrier is
+// needed after it.
+__device__ __forceinline__ Digit find_digit_wave(const uint32_t* h, int remaining) {
+    const int lane = threadIdx.x & 63;
+    const int lo = 1008 - 16 * lane;
+    uint32_t v[16];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint4 w = *reinterpret_cast<const uint4*>(h + lo + 4 * i);
+        v[4 * i] = w.x;
+        v[4 * i + 1] = w.y;
+        v[4 * i + 2] = w.z;
+        v[4 * i + 3] = w.w;
+    }
+    int sum = 0;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) sum += (int)v[q];
+    int above = wave_incl_scan(sum) - sum;
+    int bin = 0, ab = 0, cnt = 0;
+    bool found = false;
+#pragma unroll
+    for (int q = 15; q >= 0; --q) {
+        const int c = (int)v[q];
+        if (!found && above < remaining && remaining <= above + c) {
+            found = true;
+            bin = lo + q;
+            ab = above;
+            cnt = c;
+        }
+        above += c;
+    }
+    const uint64_t who = __ballot(found);
+    const int src = who ? __builtin_ctzll(who) : 0;
+    Digit d;
+    d.bin = __builtin_amdgcn_readlane(bin, src);
+    d.above = __builtin_amdgcn_readlane(ab, src);
+    d.count = __builtin_amdgcn_readlane(cnt, src);
+    return d;
+}
+
 __global__ __launch_bounds__(kSelThreads) void select_finish_kernel(SelectArgs a) {
     const int u = blockIdx.x;
     const int b = u / a.n_kv_heads;
@@ -319,15 +319,25 @@ __global__ __launch_bounds__(kSelThreads) void select_finish_kernel(SelectArgs a
     const size_t up0 = (size_t)u * a.parts;
     const uint32_t* mask = a.mask + (size_t)u * (a.parts * (a.part / 32));
 
+    if (g.simple) {
+        // sink, then every middle position or none, then recent: ranges
+        int32_t* out = a.idx + (size_t)u * a.budget;
+        const int n = g.all_mid ? g.T : g.s_end + (g.T - g.r_start);
+        for (int x = tid; x < n; x += kSelThreads)
+            if (x < a.budget) out[x] = (g.all_mid || x < g.s_end) ? x : g.r_start + (x - g.s_end);
+        if (c_head == 0 && tid == 0) a.n_idx[b] = n;
+        return;
+    }
+
     __shared__ int wave_tot[kSelWaves];
-    __shared__ int sh[2];
-    __shared__ uint32_t h1024[1024];
+    __shared__ __attribute__((aligned(16))) uint32_t h2[1024];   // read as uint4
+    __shared__ __attribute__((aligned(16))) uint32_t h3[1024];
     __shared__ int offs[kMaxSelectParts + 1];
     __shared__ uint2 cand_lds[kTailCand];
     __shared__ uint32_t lmask[kTailWords];
 
-    // The first bitmask chunk is loaded up front (all loads in flight at once)
-    // and parked in LDS once the candidate offsets are known.
+    // All first-round loads at once: the first bitmask chunk and the
+    // partition candidate counts.
     constexpr int kWordsPerThread = kTailWords / kSelThreads;
     const int n_words = (g.T + 31) >> 5;
     uint32_t mw[kWordsPerThread];
@@ -336,16 +346,22 @@ __global__ __launch_bounds__(kSelThreads) void select_finish_kernel(SelectArgs a
         const int x = tid + j * kSelThreads;
         mw[j] = x < n_words ? mask[x] : 0u;
     }
+    const int per_p = (g.parts + kSelThreads - 1) / kSelThreads;
+    const int q0 = min(g.parts, tid * per_p), q1 = min(g.parts, q0 + per_p);
+    int my_cnt = 0;
+    for (int q = q0; q < q1; ++q) my_cnt += (int)a.cnt[up0 + q];
+    for (int x = tid; x < 1024; x += kSelThreads) {
+        h2[x] = 0u;
+        h3[x] = 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < kWordsPerThread; ++j) lmask[tid + j * kSelThreads] = mw[j];
 
     // Candidate offsets: partition pp owns [offs[pp], offs[pp+1]) of the
     // concatenated list, which is in position order.
     {
-        const int per = (g.parts + kSelThreads - 1) / kSelThreads;
-        const int q0 = min(g.parts, tid * per), q1 = min(g.parts, q0 + per);
-        int s = 0;
-        for (int q = q0; q < q1; ++q) s += (int)a.cnt[up0 + q];
         int nc_all;
-        int o = block_scan(s, wave_tot, &nc_all);
+        int o = block_scan(my_cnt, wave_tot, &nc_all);
         for (int q = q0; q < q1; ++q) {
             offs[q] = o;
             o += (int)a.cnt[up0 + q];
@@ -353,80 +369,88 @@ __global__ __launch_bounds__(kSelThreads) void select_finish_kernel(SelectArgs a
         if (tid == 0) offs[g.parts] = nc_all;
         __syncthreads();
     }
-    const int nc = g.simple ? 0 : offs[g.parts];
+    const int nc = offs[g.parts];
     const bool cached = nc <= kTailCand;
     auto cand_global = [&](int x) -> uint2 {
-        int lo = 0, hi = g.parts - 1;   // last partition whose offset is <= x
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (offs[mid] <= x) lo = mid; else hi = mid - 1;
-        }
+        int lo = 0;   // last partition whose offset is <= x (fixed steps, unrolled)
+#pragma unroll
+        for (int step = kMaxSelectParts / 2; step >= 1; step >>= 1)
+            lo += (lo + step < g.parts && offs[lo + step] <= x) ? step : 0;
         return a.seg[(up0 + lo) * a.part + (x - offs[lo])];
     };
     auto cand = [&](int x) -> uint2 { return cached ? cand_lds[x] : cand_global(x); };
 
     uint32_t tau = 0u;
     int need = 0;
-    if (!g.simple) {
+    bool all_ties = true;   // every entry equal to tau is taken
+    {
         need = (int)a.thr[2 * u + 1];
-        if (cached) {
-            constexpr int U = 8;   // loads in flight per thread
-            for (int x0 = tid; x0 < nc; x0 += U * kSelThreads) {
-                uint2 v[U];
+        const uint32_t d1 = a.thr[2 * u];
+        // Pass 2 (bits 19..10) while gathering: every candidate is in bin d1.
+        constexpr int U = 8;   // loads in flight per thread
+        for (int x0 = tid; x0 < nc; x0 += U * kSelThreads) {
+            uint2 v[U];
 #pragma unroll
-                for (int j = 0; j < U; ++j) {
-                    const int x = x0 + j * kSelThreads;
-                    v[j] = x < nc ? cand_global(x) : make_uint2(0u, 0u);
-                }
+            for (int j = 0; j < U; ++j) {
+                const int x = x0 + j * kSelThreads;
+                v[j] = x < nc ? cand_global(x) : make_uint2(0u, 0u);
+            }
 #pragma unroll
-                for (int j = 0; j < U; ++j) {
-                    const int x = x0 + j * kSelThreads;
-                    if (x < nc) cand_lds[x] = v[j];
+            for (int j = 0; j < U; ++j) {
+                const int x = x0 + j * kSelThreads;
+                if (x < nc) {
+                    if (cached) cand_lds[x] = v[j];
+                    atomicAdd(&h2[(v[j].x >> 10) & 1023u], 1u);
                 }
             }
-            __syncthreads();
         }
-        uint32_t prefix = a.thr[2 * u] << 20;
-#pragma unroll
-        for (int pass = 0; pass < 2; ++pass) {
-            const int shift = pass == 0 ? 10 : 0;
-            const uint32_t pmask = pass == 0 ? 0xfff00000u : 0xfffffc00u;
-            for (int x = tid; x < 1024; x += kSelThreads) h1024[x] = 0u;
-            __syncthreads();
-            for (int x = tid; x < nc; x += kSelThreads) {
-                const uint32_t k = cand(x).x;
-                if ((k & pmask) == prefix) atomicAdd(&h1024[(k >> shift) & 1023u], 1u);
-            }
-            __syncthreads();
-            find_digit<1024>(h1024, need, sh, wave_tot);
-            prefix |= (uint32_t)sh[0] << shift;
-            need -= sh[1];
-            __syncthreads();
+        __syncthreads();
+        const Digit dg2 = find_digit_wave(h2, need);
+        need -= dg2.above;
+        const uint32_t prefix = (d1 << 20) | ((uint32_t)dg2.bin << 10);
+        // Pass 3 (bits 9..0) over the candidates with that 22-bit prefix.
+        for (int x = tid; x < nc; x += kSelThreads) {
+            const uint32_t k = cand(x).x;
+            if ((k & 0xfffffc00u) == prefix) atomicAdd(&h3[k & 1023u], 1u);
         }
-        tau = prefix;
+        __syncthreads();
+        const Digit dg3 = find_digit_wave(h3, need);
+        need -= dg3.above;
+        tau = prefix | (uint32_t)dg3.bin;
+        all_ties = need == dg3.count;
     }
-    // Ties: thread t ranks the contiguous slice [x0, x1) of the list.
+    // Mark the candidates above tau and the chosen ties.  Ties are ranked
+    // only when some of them stay out: thread t then takes the contiguous
+    // slice [x0, x1) of the (position-ordered) list.
     const int per = (nc + kSelThreads - 1) / kSelThreads;
     const int x0 = min(nc, tid * per), x1 = min(nc, x0 + per);
     int tie_base = 0;
-    if (!g.simple) {
+    if (!all_ties) {
         int nt = 0;
         for (int x = x0; x < x1; ++x) nt += cand(x).x == tau;
         int tie_total;
         tie_base = block_scan(nt, wave_tot, &tie_total);
     }
+    // Sink, then the middle selections in position order, then the recent
+    // span: the bitmask holds middle positions only.
     int32_t* out = a.idx + (size_t)u * a.budget;
-    int emitted = 0;
+    for (int x = tid; x < g.s_end; x += kSelThreads)
+        if (x < a.budget) out[x] = x;
+    int emitted = g.s_end;
     for (int cw = 0; cw < n_words; cw += kTailWords) {
         const int nw = min(kTailWords, n_words - cw);
-        if (cw == 0) {
-#pragma unroll
-            for (int j = 0; j < kWordsPerThread; ++j) lmask[tid + j * kSelThreads] = mw[j];
-        } else {
+        if (cw > 0) {
+            __syncthreads();
             for (int x = tid; x < nw; x += kSelThreads) lmask[x] = mask[cw + x];
+            __syncthreads();
         }
-        __syncthreads();
-        if (!g.simple) {
+        if (all_ties) {
+            for (int x = tid; x < nc; x += kSelThreads) {
+                const uint2 kp = cand(x);
+                const int w = (int)(kp.y >> 5) - cw;
+                if (kp.x >= tau && w >= 0 && w < nw) atomicOr(&lmask[w], 1u << (kp.y & 31u));
+            }
+        } else {
             int rank = tie_base;
             for (int x = x0; x < x1; ++x) {
                 const uint2 kp = cand(x);
@@ -438,27 +462,41 @@ __global__ __launch_bounds__(kSelThreads) void select_finish_kernel(SelectArgs a
                 const int w = (int)(kp.y >> 5) - cw;
                 if (sel && w >= 0 && w < nw) atomicOr(&lmask[w], 1u << (kp.y & 31u));
             }
-            __syncthreads();
         }
+        __syncthreads();
+        // thread t owns words [w0, w1); their set bits, four words at a time,
+        // lowest first, without a branch per bit
         const int wpt = (nw + kSelThreads - 1) / kSelThreads;
         const int w0 = min(nw, tid * wpt), w1 = min(nw, w0 + wpt);
         int cnt = 0;
         for (int w = w0; w < w1; ++w) cnt += __builtin_popcount(lmask[w]);
         int chunk_total;
         int pos = emitted + block_scan(cnt, wave_tot, &chunk_total);
-        for (int w = w0; w < w1; ++w) {
-            uint32_t m = lmask[w];
-            while (m) {
-                const int bit = __builtin_ctz(m);
-                m &= m - 1u;
-                if (pos < a.budget) out[pos] = (cw + w) * 32 + bit;
+        for (int w = w0; w < w1; w += 4) {
+            uint32_t m[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) m[i] = w + i < w1 ? lmask[w + i] : 0u;
+            uint64_t lo = (uint64_t)m[0] | ((uint64_t)m[1] << 32);
+            uint64_t hi = (uint64_t)m[2] | ((uint64_t)m[3] << 32);
+            const int n4 = __builtin_popcountll(lo) + __builtin_popcountll(hi);
+            const int base = (cw + w) * 32;
+            for (int k = 0; k < n4; ++k) {
+                const bool use_lo = lo != 0ull;
+                const uint64_t cur = use_lo ? lo : hi;
+                const int bit = __builtin_ctzll(cur) + (use_lo ? 0 : 64);
+                const uint64_t nxt = cur & (cur - 1ull);
+                lo = use_lo ? nxt : lo;
+                hi = use_lo ? hi : nxt;
+                if (pos < a.budget) out[pos] = base + bit;
                 ++pos;
             }
         }
         emitted += chunk_total;
-        __syncthreads();
     }
-    if (c_head == 0 && tid == 0) a.n_idx[b] = emitted;
+    const int n_recent = g.T - g.r_start;
+    for (int x = tid; x < n_recent; x += kSelThreads)
+        if (emitted + x < a.budget) out[emitted + x] = g.r_start + x;
+    if (c_head == 0 && tid == 0) a.n_idx[b] = emitted + n_recent;
 }
 
 template <int NR>

@@ -28,6 +28,8 @@
 // workgroup ahead of its chunks has finished and its chunks (at most a few
 // per XCD) are resident.  The wait is also bounded, so a broken invariant
 // cannot hang the GPU (the results would then be wrong, never a fault).
+#include <atomic>
+
 #include "verify_common.h"
 
 namespace ssl {
@@ -322,9 +324,21 @@ template <int NRT>
 hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, int n_rows_total,
                             hipStream_t stream) {
     const size_t dyn = (size_t)NRT * 16 * (a.v.chunk + kStashPad) * sizeof(float);
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(verify_fused_kernel<NRT>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
+    // The kernel's dynamic LDS limit is raised to the largest stash once per
+    // device (setting it twice is harmless, so a race between threads is too).
+    constexpr int kMaxDevices = 64;
+    static std::atomic<bool> raised[kMaxDevices];
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices || !raised[dev].load(std::memory_order_relaxed)) {
+        e = hipFuncSetAttribute(
+            reinterpret_cast<const void*>(verify_fused_kernel<NRT>),
+            hipFuncAttributeMaxDynamicSharedMemorySize,
+            (int)((size_t)NRT * 16 * (fused_max_chunk(NRT) + kStashPad) * sizeof(float)));
+        if (e != hipSuccess) return e;
+        if (dev >= 0 && dev < kMaxDevices) raised[dev].store(true, std::memory_order_relaxed);
+    }
     hipLaunchKernelGGL(verify_fused_kernel<NRT>, dim3(n_slots), dim3(kThreads), dyn, stream, a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
