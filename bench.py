@@ -43,6 +43,116 @@ def algorithmic_bytes(w, out_bytes: int):
     return {"verify": verify, "select": select, "draft": draft}, n
 
 
+REPO = os.path.dirname(os.path.abspath(__file__))
+TRAFFIC_FILE = os.path.join(REPO, "profiles", "verify_traffic_llama8b_T32K.txt")
+OUR_KERNELS = ("verify_fused_kernel", "verify_stats_kernel", "verify_main_kernel",
+               "verify_combine_kernel", "select_hist_kernel", "select_mark_kernel",
+               "select_finish_kernel", "draft_kernel", "draft_combine_kernel")
+VERIFY_KERNELS = ("verify_fused_kernel", "verify_stats_kernel", "verify_main_kernel",
+                  "verify_combine_kernel")
+
+
+def sources_sha256() -> str:
+    """Hash of the HIP/C++ sources and the ABI header, in a fixed order."""
+    import hashlib
+    h = hashlib.sha256()
+    dirs = [os.path.join(REPO, "paper_2607_27735_amd", "csrc"), os.path.join(REPO, "include")]
+    for d in dirs:
+        for name in sorted(os.listdir(d)):
+            if name.endswith((".hip", ".h", ".cpp")):
+                h.update(name.encode())
+                with open(os.path.join(d, name), "rb") as f:
+                    h.update(f.read())
+    return h.hexdigest()
+
+
+def kernel_short(name: str) -> str:
+    for k in OUR_KERNELS:
+        if k in name:
+            return k + ("<" + name.split("<", 1)[1].split(">", 1)[0] + ">" if "<" in name else "")
+    return name
+
+
+def summarize_trace(d: str, command: str) -> str:
+    """Markdown table of a rocprofv3 --kernel-trace --stats run."""
+    import csv
+    import glob
+    f = glob.glob(os.path.join(d, "**", "*kernel_stats.csv"), recursive=True)[0]
+    rows = [r for r in csv.DictReader(open(f)) if any(k in r["Name"] for k in OUR_KERNELS)]
+    out = [f"command: `{command}`", "",
+           "| kernel | calls | avg us | min us | max us |", "|---|---:|---:|---:|---:|"]
+    for r in sorted(rows, key=lambda r: -float(r["AverageNs"])):
+        out.append(f"| {kernel_short(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} "
+                   f"| {float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} |")
+    per_call = {}
+    for r in rows:
+        k = kernel_short(r["Name"]).split("<")[0]
+        call = "verify" if k.startswith("verify") else "select" if k.startswith("select") else "draft"
+        per_call[call] = per_call.get(call, 0.0) + float(r["AverageNs"]) / 1e3
+    out += ["", "sum of kernel averages per call: " +
+            ", ".join(f"{c} {v:.2f} us" for c, v in per_call.items())]
+    return "\n".join(out) + "\n"
+
+
+def summarize_traffic(fetch_dir: str, write_dir: str, copy_mib: int, command: str) -> str:
+    """HBM traffic per launch from two rocprofv3 --pmc runs (FETCH_SIZE, then
+    WRITE_SIZE, KiB per dispatch), each scaled by what the counter reads for
+    the plain device copy of copy_mib MiB that the same command ends with."""
+    import csv
+    import glob
+
+    def load(d, counter):
+        f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+        rows = [r for r in csv.DictReader(open(f)) if r["Counter_Name"] == counter]
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        copies = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
+        per = {}
+        for r in rows:
+            k = kernel_short(r["Kernel_Name"])
+            if k.split("<")[0] in OUR_KERNELS:
+                per.setdefault(k, []).append(float(r["Counter_Value"]))
+        return copies[-3:], {k: statistics.fmean(v) for k, v in per.items()}
+
+    copy_bytes = copy_mib << 20
+    cf, fetch = load(fetch_dir, "FETCH_SIZE")
+    cw, write = load(write_dir, "WRITE_SIZE")
+    f_fac = copy_bytes / (statistics.fmean(cf) * 1024.0)
+    w_fac = copy_bytes / (statistics.fmean(cw) * 1024.0)
+    lines = [f"# HBM traffic per launch, llama8b-T32K workload (rocprofv3 FETCH_SIZE / WRITE_SIZE)",
+             f"command = {command}",
+             f"sources_sha256 = {sources_sha256()}",
+             f"copy_bytes = {copy_bytes}",
+             f"copy_fetch_kib = {statistics.fmean(cf):.1f}",
+             f"copy_write_kib = {statistics.fmean(cw):.1f}",
+             f"fetch_factor = {f_fac:.4f}",
+             f"write_factor = {w_fac:.4f}"]
+    call_bytes = 0.0
+    for k in sorted(set(fetch) | set(write)):
+        fb = fetch.get(k, 0.0) * 1024.0 * f_fac
+        wb = write.get(k, 0.0) * 1024.0 * w_fac
+        lines.append(f"{k} = fetch {fb:.0f} write {wb:.0f} bytes per launch")
+        if k.split("<")[0] in VERIFY_KERNELS:
+            call_bytes += fb + wb
+    lines.append(f"verify_call_traffic_bytes = {call_bytes:.0f}")
+    return "\n".join(lines) + "\n"
+
+
+def measured_traffic():
+    """Traffic per verify call from the committed summary, if it was taken on
+    the current sources; else None."""
+    try:
+        kv = {}
+        for line in open(TRAFFIC_FILE):
+            if " = " in line and not line.startswith("#"):
+                k, v = line.split(" = ", 1)
+                kv[k.strip()] = v.strip()
+        if kv.get("sources_sha256") != sources_sha256():
+            return None
+        return float(kv["verify_call_traffic_bytes"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(w, seconds: float):
     import numpy as np
     import oracle
@@ -76,7 +186,21 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--mode", choices=["eager", "graph"], default="eager")
     ap.add_argument("--verify-mode", choices=["auto", "two-sweep", "one-sweep"], default="auto")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="end with three plain device copies of this size (counter calibration)")
+    ap.add_argument("--summarize-trace", metavar="DIR",
+                    help="print a summary of a rocprofv3 --kernel-trace --stats output and exit")
+    ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="print HBM traffic per launch from two rocprofv3 --pmc outputs and exit")
+    ap.add_argument("--command-text", default="", help="the profiling command, for summaries")
     args = ap.parse_args()
+    if args.summarize_trace:
+        sys.stdout.write(summarize_trace(args.summarize_trace, args.command_text))
+        return 0
+    if args.summarize_traffic:
+        sys.stdout.write(summarize_traffic(*args.summarize_traffic, args.copy_calibration_mib,
+                                           args.command_text))
+        return 0
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the hot path runs on one GPU; see the design "
               f"notes for how it would shard); --gpus {args.gpus} is not supported",
@@ -237,7 +361,9 @@ def main() -> int:
                      "achieved": round(nbytes["verify"] / (v_avg * 1e-6) / 1e9, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(nbytes["verify"] / (v_avg * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
-                     "traffic": None, "bytes_per_launch": nbytes["verify"],
+                     "traffic": (measured_traffic() if (args.workload == 2 and args.mode == "eager"
+                                                        and args.verify_mode == "auto") else None),
+                     "bytes_per_launch": nbytes["verify"],
                      "avg_launch_us": v_avg},
         "kernels": kernels,
     }
@@ -245,6 +371,14 @@ def main() -> int:
     s = scores.double().sum(dim=2).cpu().numpy()
     want = np.array([min(w.window, int(x)) * w.group for x in w.q_len])[:, None]
     result["score_mass_max_rel_err"] = float(np.abs(s - want).max() / want.max())
+    if args.copy_calibration_mib > 0:
+        # a plain device copy of known size, for scaling the traffic counters
+        src = torch.empty(args.copy_calibration_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(result), flush=True)
