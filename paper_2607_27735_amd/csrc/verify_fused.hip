@@ -4,16 +4,17 @@
 // which no split of the context knows while it streams.  When every chunk of
 // a (sequence, KV head) can be resident at once, one sweep suffices:
 //
-//   1. each workgroup streams its chunk of K and V once, runs an online
-//      softmax per verify row (P.V on the MFMA, as in the two-sweep kernel)
-//      and keeps the scaled logits of its chunk in LDS;
+//   1. each workgroup streams its chunk of K and V once and runs an online
+//      softmax per verify row (P.V on the MFMA, as in the two-sweep kernel);
+//      it keeps in LDS the probabilities of its keys relative to the running
+//      row maxima, and those maxima for every 32-key tile;
 //   2. it publishes its (running max, sum) per row and then a 64-bit call tag
 //      for its chunk, and waits until every chunk of its head shows the tag;
-//   3. from the merged (max, sum) of all chunks it forms the exact
-//      probabilities of its own keys from the LDS logits and writes their
-//      scores, and writes its partial output already scaled to the exact
-//      normalizer, so that the two-sweep combine kernel only has to add the
-//      partials of each row.
+//   3. from the merged (max, sum) of all chunks it forms one factor per tile
+//      and row, so that a stashed probability times its factor is the exact
+//      probability, and writes the scores of its keys; it also writes its
+//      partial output already scaled to the exact normalizer, so that the
+//      two-sweep combine kernel only has to add the partials of each row.
 //
 // Publication avoids agent-scope fences, which write back a whole L2 per wave
 // on this multi-XCD part: the few published words are written and read with
@@ -28,6 +29,7 @@
 // workgroup ahead of its chunks has finished and its chunks (at most a few
 // per XCD) are resident.  The wait is also bounded, so a broken invariant
 // cannot hang the GPU (the results would then be wrong, never a fault).
+#include <algorithm>
 #include <atomic>
 
 #include "verify_common.h"
@@ -38,16 +40,16 @@ namespace {
 using namespace vc;
 
 constexpr int kStashPad = 4;          // floats of padding per stashed row
+constexpr int kParkStride = kHeadDim + 4;                 // floats per parked output row
+constexpr int kParkFloats = kWaves * 16 * kParkStride;    // one row tile of every wave
 constexpr int kSpinLimit = 1 << 22;   // bounded wait (far above any real wait)
 
 template <int NRT>
 constexpr int static_lds_bytes() {
-    return NRT * 16 * kHeadDim * 4          // red
-           + kWaves * NRT * 16 * 8          // wml
+    return kWaves * NRT * 16 * 8            // wml
            + kRowCap * 8                    // row_ml
            + kRowCap * 4                    // row_lse
            + kWaves * kRowCap * 8           // lse_part
-           + kRowCap * 4                    // row_mw
            + 64;
 }
 
@@ -78,12 +80,14 @@ __device__ __forceinline__ void wait_stores_done() {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-// One 32-key tile: logits to the LDS stash, online softmax, P.V.
+// One 32-key tile: online softmax and P.V; the tile's probabilities relative
+// to the running row maxima go to the LDS stash, those maxima to mtile.
 template <int NRT>
 __device__ __forceinline__ void fused_tile(const VerifyArgs& a, const Rows<NRT>& r,
                                            const KVTile& tl, int key0, int kl0, float* stash,
-                                           int stride, int m16, int G, float (&M)[NRT],
-                                           float (&L)[NRT], f32x4 (&oacc)[8][NRT]) {
+                                           int stride, float* mtile, int m16, int G,
+                                           float (&M)[NRT], float (&L)[NRT],
+                                           f32x4 (&oacc)[8][NRT]) {
     f32x4 acc[2][NRT];
     qk_tile<NRT>(tl.k, r, acc);
     float p[2][NRT][4];
@@ -97,7 +101,6 @@ __device__ __forceinline__ void fused_tile(const VerifyArgs& a, const Rows<NRT>&
             const int t = e >> 2, i = e & 3;
             const int key = key0 + 16 * t + G + 4 * i;
             y[e] = key <= r.plim[rt] ? acc[t][rt][i] * a.scale_log2 : -INFINITY;
-            srow[16 * t + G + 4 * i] = y[e];
             mt = fmaxf(mt, y[e]);
         }
         mt = fmaxf(mt, shfl_xor_f(mt, 16));
@@ -109,7 +112,9 @@ __device__ __forceinline__ void fused_tile(const VerifyArgs& a, const Rows<NRT>&
         for (int e = 0; e < 8; ++e) {
             p[e >> 2][rt][e & 3] = fast_exp2(y[e] - Mn);
             sum += p[e >> 2][rt][e & 3];
+            srow[16 * (e >> 2) + G + 4 * (e & 3)] = p[e >> 2][rt][e & 3];
         }
+        if (G == 0) mtile[(kl0 / kTile) * (NRT * 16) + rt * 16 + m16] = Mn;
         L[rt] = L[rt] * alpha + sum;
         M[rt] = fmaxf(M[rt], mt);
 #pragma unroll
@@ -140,12 +145,10 @@ template <int NRT>
 __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     const VerifyArgs& a = fa.v;
     extern __shared__ __attribute__((aligned(16))) float stash[];   // [NRT*16][chunk + pad]
-    __shared__ f32x4 red[NRT * 16][kHeadDim / 4];
     __shared__ float2 wml[kWaves][NRT * 16];
     __shared__ float2 row_ml[kRowCap];
     __shared__ float row_lse[kRowCap];
     __shared__ float2 lse_part[kWaves][kRowCap];
-    __shared__ float row_mw[kRowCap];
 
     const int slot = blockIdx.x;
     const Item it = decode_item(a.seq, slot, a.n_kv_heads, a.chunk);
@@ -156,6 +159,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     const int chunk = a.chunk;
     const int key_begin = it.key_begin, key_end = it.key_end;
     const int stride = chunk + kStashPad;
+    float* mtile = stash + NRT * 16 * stride;   // [chunk / kTile][NRT*16] running row maxima
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int m16 = lane & 15, G = lane >> 4;
 
@@ -183,8 +187,8 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
             load_v(vbase, key_begin + t * kTile, T, m16, G, bf.v);
         },
         [&](const KVTile& bf, int t) {
-            fused_tile<NRT>(a, r, bf, key_begin + t * kTile, t * kTile, stash, stride, m16, G, M,
-                            L, oacc);
+            fused_tile<NRT>(a, r, bf, key_begin + t * kTile, t * kTile, stash, stride, mtile, m16,
+                            G, M, L, oacc);
         });
 
     // ---- 2. publish the item's partial output and row statistics ----------
@@ -195,8 +199,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         if (G == 0) wml[wave][rt * 16 + m16] = make_float2(M[rt], L[rt]);
     }
     __syncthreads();
-    // Publish the row statistics first: their write-through latency overlaps
-    // the reduction of the partial outputs below.
+    // the workgroup's row statistics, merged over its waves
     if (tid < R) {
         float Mw = -INFINITY, Lw = 0.f;
 #pragma unroll
@@ -206,39 +209,6 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         float* pm = reinterpret_cast<float*>(a.part_ml + (size_t)slot * kRowCap + tid);
         st_dev(pm, Mw);
         st_dev(pm + 1, Lw);
-        row_mw[tid] = Mw;
-    }
-    // rescale every wave's output to the workgroup's row maximum, then add
-    // the waves in a fixed order
-#pragma unroll
-    for (int rt = 0; rt < NRT; ++rt) {
-        float Mw = -INFINITY;
-#pragma unroll
-        for (int w = 0; w < kWaves; ++w) Mw = fmaxf(Mw, wml[w][rt * 16 + m16].x);
-        const float f = fast_exp2(M[rt] - safe_max(Mw));
-#pragma unroll
-        for (int jd = 0; jd < 8; ++jd) oacc[jd][rt] *= f;
-    }
-    for (int w = 0; w < kWaves; ++w) {
-        if (wave == w) {
-#pragma unroll
-            for (int rt = 0; rt < NRT; ++rt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int row = rt * 16 + m16;
-                    const int c4 = (32 * G + 8 * i) / 4;
-                    f32x4 w0 = {oacc[0][rt][i], oacc[1][rt][i], oacc[2][rt][i], oacc[3][rt][i]};
-                    f32x4 w1 = {oacc[4][rt][i], oacc[5][rt][i], oacc[6][rt][i], oacc[7][rt][i]};
-                    if (w == 0) {
-                        red[row][c4] = w0;
-                        red[row][c4 + 1] = w1;
-                    } else {
-                        red[row][c4] += w0;
-                        red[row][c4 + 1] += w1;
-                    }
-                }
-        }
-        __syncthreads();
     }
 
     // ---- wait for every chunk of this (sequence, KV head) -------------------
@@ -285,23 +255,37 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         row_lse[tid] = Lx > 0.f ? Mx + fast_log2(Lx) : INFINITY;
     }
     __syncthreads();
+    // tile factors: a stashed probability times its tile's factor is exact
+    const int nk = key_end - key_begin;
+    const int ntl = (nk + kTile - 1) / kTile;
+    for (int x = tid; x < ntl * NRT * 16; x += kThreads) {
+        const int row = x % (NRT * 16);
+        mtile[x] = row < R ? fast_exp2(mtile[x] - row_lse[row]) : 0.f;
+    }
+    __syncthreads();
 
-    // ---- 3b. scores of this chunk's keys from the stashed logits -----------
+    // ---- 3b. scores of this chunk's keys from the stashed probabilities ----
     {
         const int wn = min(a.window, nq);
         const int r0 = (nq - wn) * a.group;   // first window row
         float* srow = a.scores + (size_t)unit * a.max_ctx;
-        // four consecutive keys per thread (one 16-byte LDS read per row); the
-        // stash row stride and the chunk are multiples of 4 floats
-        const int nk = key_end - key_begin;
+        // four consecutive keys per thread (one 16-byte LDS read per row, four
+        // rows in flight); the stash row stride and the chunk are multiples of
+        // 4 floats, and 4 consecutive keys share one tile
         for (int k4 = 4 * tid; k4 < nk; k4 += 4 * kThreads) {
+            const float* ct = mtile + (k4 / kTile) * (NRT * 16);
             f32x4 sc = {0.f, 0.f, 0.f, 0.f};
-            for (int row = r0; row < R; ++row) {
-                const f32x4 y = *reinterpret_cast<const f32x4*>(stash + row * stride + k4);
-                const float l = row_lse[row];
+            int row = r0;
+            for (; row + 4 <= R; row += 4) {
+                f32x4 pr[4];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) sc[i] += fast_exp2(y[i] - l);
+                for (int j = 0; j < 4; ++j)
+                    pr[j] = *reinterpret_cast<const f32x4*>(stash + (row + j) * stride + k4);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) sc += pr[j] * ct[row + j];
             }
+            for (; row < R; ++row)
+                sc += *reinterpret_cast<const f32x4*>(stash + row * stride + k4) * ct[row];
 #pragma unroll
             for (int i = 0; i < 4; ++i)
                 if (k4 + i < nk) srow[key_begin + k4 + i] = sc[i];
@@ -309,13 +293,38 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     }
 
     // ---- 3c. this chunk's output, scaled to the exact normalizer ------------
-    // (the combine kernel adds the partials of each row)
+    // The stash is free now: per row tile, every wave parks its partial P.V,
+    // scaled from its own row maxima to the exact normalizers, in a slice of
+    // it, and all threads add the four slices (in wave order) and store the
+    // sum; the combine kernel then adds the chunks of each row.
     {
-        const float* redf = reinterpret_cast<const float*>(&red[0][0]);
+        constexpr int kSliceStride = kParkStride;
+        float* park = stash;                          // [kWaves][16][kParkStride]
         float* po = a.part_o + (size_t)slot * kRowCap * kHeadDim;
-        for (int x = tid; x < R * kHeadDim; x += kThreads) {
-            const int row = x >> 7;
-            po[x] = redf[x] * fast_exp2(safe_max(row_mw[row]) - row_lse[row]);
+#pragma unroll
+        for (int rt = 0; rt < NRT; ++rt) {
+            __syncthreads();
+            const int row = rt * 16 + m16;
+            const float f = fast_exp2(safe_max(M[rt]) - row_lse[row]);
+            float* dst = park + (wave * 16 + m16) * kSliceStride;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int c = 32 * G + 8 * i;
+                *reinterpret_cast<f32x4*>(dst + c) =
+                    f32x4{oacc[0][rt][i], oacc[1][rt][i], oacc[2][rt][i], oacc[3][rt][i]} * f;
+                *reinterpret_cast<f32x4*>(dst + c + 4) =
+                    f32x4{oacc[4][rt][i], oacc[5][rt][i], oacc[6][rt][i], oacc[7][rt][i]} * f;
+            }
+            __syncthreads();
+            const int rows_here = min(16, R - rt * 16);
+            for (int x = tid; x < rows_here * (kHeadDim / 4); x += kThreads) {
+                const int rr = x >> 5, c4 = x & 31;
+                f32x4 o = *reinterpret_cast<const f32x4*>(park + rr * kSliceStride + 4 * c4);
+#pragma unroll
+                for (int w = 1; w < kWaves; ++w)
+                    o += *reinterpret_cast<const f32x4*>(park + (w * 16 + rr) * kSliceStride + 4 * c4);
+                *reinterpret_cast<f32x4*>(po + (size_t)(rt * 16 + rr) * kHeadDim + 4 * c4) = o;
+            }
         }
     }
 }
@@ -323,7 +332,9 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
 template <int NRT>
 hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, int n_rows_total,
                             hipStream_t stream) {
-    const size_t dyn = (size_t)NRT * 16 * (a.v.chunk + kStashPad) * sizeof(float);
+    // the logit stash, later reused to park the waves' partial outputs
+    const size_t dyn = std::max((size_t)NRT * 16 * (a.v.chunk + kStashPad + a.v.chunk / kTile),
+                                (size_t)kParkFloats) * sizeof(float);
     // The kernel's dynamic LDS limit is raised to the largest stash once per
     // device (setting it twice is harmless, so a race between threads is too).
     constexpr int kMaxDevices = 64;
@@ -335,7 +346,9 @@ hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, int n_rows_total,
         e = hipFuncSetAttribute(
             reinterpret_cast<const void*>(verify_fused_kernel<NRT>),
             hipFuncAttributeMaxDynamicSharedMemorySize,
-            (int)((size_t)NRT * 16 * (fused_max_chunk(NRT) + kStashPad) * sizeof(float)));
+            (int)((size_t)NRT * 16 *
+                  (fused_max_chunk(NRT) + kStashPad + fused_max_chunk(NRT) / kTile) *
+                  sizeof(float)));
         if (e != hipSuccess) return e;
         if (dev >= 0 && dev < kMaxDevices) raised[dev].store(true, std::memory_order_relaxed);
     }
@@ -356,8 +369,9 @@ int fused_max_chunk(int row_tiles) {
         case 3: stat = static_lds_bytes<3>(); break;
         default: stat = static_lds_bytes<4>(); break;
     }
+    // per stash row: chunk probabilities, padding, chunk / kTile tile maxima
     const int floats_per_row = (kLds - stat - 1024) / (int)sizeof(float) / (16 * row_tiles);
-    return (floats_per_row - kStashPad) / 128 * 128;
+    return (floats_per_row - kStashPad) * kTile / (kTile + 1) / 128 * 128;
 }
 
 hipError_t launch_verify_fused(const FusedArgs& a, int n_slots, int n_rows_total, int row_tiles,
