@@ -78,6 +78,39 @@ __device__ __forceinline__ int wave_incl_scan(int x) {
     return x;
 }
 
+// Device-coherent accesses (agent scope, relaxed atomics): the stores write
+// through and the loads read past the per-XCD L2, so a few words published by
+// one workgroup reach another without an L2 writeback.  After
+// wait_stores_done() every store the wave issued has completed.
+__device__ __forceinline__ void st_dev(float* p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev(const float* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev32(uint32_t* p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t ld_dev32(const uint32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev64(uint64_t* p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t ld_dev64(const uint64_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 ld_dev2(const float2* p) {
+    const float* f = reinterpret_cast<const float*>(p);
+    return make_float2(ld_dev(f), ld_dev(f + 1));
+}
+// (the signal fences keep the compiler from moving memory accesses across it)
+__device__ __forceinline__ void wait_stores_done() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 __device__ __forceinline__ float shfl_xor_f(float x, int mask) {
     return __shfl_xor(x, mask, kWave);
 }

@@ -118,17 +118,277 @@ __global__ __launch_bounds__(kSelThreads) void select_hist_kernel(SelectArgs a) 
     if ((tid & 3) == 0) a.coarse[up * 64 + (tid >> 2)] = s;
 }
 
+struct Digit {
+    int bin, above, count;
+};
+
+// In a 1024-bin histogram read from the top bin down, finds the bin where the
+// running count first reaches `remaining` (1 <= remaining <= the total), the
+// count strictly above that bin and the bin's own count.  Every wave computes
+// it on its own (lane l holds bins 1008-16l .. 1023-16l), so no barrier is
+// needed after it.
+__device__ __forceinline__ Digit find_digit_wave(const uint32_t* h, int remaining) {
+    const int lane = threadIdx.x & 63;
+    const int lo = 1008 - 16 * lane;
+    uint32_t v[16];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint4 w = *reinterpret_cast<const uint4*>(h + lo + 4 * i);
+        v[4 * i] = w.x;
+        v[4 * i + 1] = w.y;
+        v[4 * i + 2] = w.z;
+        v[4 * i + 3] = w.w;
+    }
+    int sum = 0;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) sum += (int)v[q];
+    int above = wave_incl_scan(sum) - sum;
+    int bin = 0, ab = 0, cnt = 0;
+    bool found = false;
+#pragma unroll
+    for (int q = 15; q >= 0; --q) {
+        const int c = (int)v[q];
+        if (!found && above < remaining && remaining <= above + c) {
+            found = true;
+            bin = lo + q;
+            ab = above;
+            cnt = c;
+        }
+        above += c;
+    }
+    const uint64_t who = __ballot(found);
+    const int src = who ? __builtin_ctzll(who) : 0;
+    Digit d;
+    d.bin = __builtin_amdgcn_readlane(bin, src);
+    d.above = __builtin_amdgcn_readlane(ab, src);
+    d.count = __builtin_amdgcn_readlane(cnt, src);
+    return d;
+}
+
+// ---------------------------------------------------------------------------
+// The finish of one unit: exact threshold, ties and ordered emission.
+// DEV: the unit's bitmask, counts and candidates were published by other
+// workgroups of the running kernel, so they are read with device-coherent
+// loads; otherwise they come from an earlier kernel.
+// ---------------------------------------------------------------------------
+
+// Sink, then every middle position or none, then recent: ranges.
+__device__ __forceinline__ void emit_ranges(const SelectArgs& a, int u, const Geom& g) {
+    const int b = u / a.n_kv_heads;
+    const int tid = threadIdx.x;
+    int32_t* out = a.idx + (size_t)u * a.budget;
+    const int n = g.all_mid ? g.T : g.s_end + (g.T - g.r_start);
+    for (int x = tid; x < n; x += kSelThreads)
+        if (x < a.budget) out[x] = (g.all_mid || x < g.s_end) ? x : g.r_start + (x - g.s_end);
+    if (u - b * a.n_kv_heads == 0 && tid == 0) a.n_idx[b] = n;
+}
+
+template <bool DEV>
+__device__ void finish_unit(const SelectArgs& a, int u, const Geom& g, uint32_t d1, int need) {
+    const int b = u / a.n_kv_heads;
+    const int c_head = u - b * a.n_kv_heads;
+    const int tid = threadIdx.x;
+    const size_t up0 = (size_t)u * a.parts;
+    const uint32_t* mask = a.mask + (size_t)u * (a.parts * (a.part / 32));
+    auto ldw = [](const uint32_t* p) -> uint32_t { return DEV ? ld_dev32(p) : *p; };
+    auto ldc = [](const uint2* p) -> uint2 {
+        if (!DEV) return *p;
+        const uint64_t v = ld_dev64(reinterpret_cast<const uint64_t*>(p));
+        return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
+    };
+
+    __shared__ int wave_tot[kSelWaves];
+    __shared__ __attribute__((aligned(16))) uint32_t h2[1024];   // read as uint4
+    __shared__ __attribute__((aligned(16))) uint32_t h3[1024];
+    __shared__ int offs[kMaxSelectParts + 1];
+    __shared__ uint2 cand_lds[kTailCand];
+    __shared__ uint32_t lmask[kTailWords];
+
+    // All first-round loads at once: the first bitmask chunk and the
+    // partition candidate counts.
+    constexpr int kWordsPerThread = kTailWords / kSelThreads;
+    const int n_words = (g.T + 31) >> 5;
+    uint32_t mw[kWordsPerThread];
+#pragma unroll
+    for (int j = 0; j < kWordsPerThread; ++j) {
+        const int x = tid + j * kSelThreads;
+        mw[j] = x < n_words ? ldw(mask + x) : 0u;
+    }
+    const int per_p = (g.parts + kSelThreads - 1) / kSelThreads;
+    const int q0 = min(g.parts, tid * per_p), q1 = min(g.parts, q0 + per_p);
+    int my_cnt = 0;
+    for (int q = q0; q < q1; ++q) my_cnt += (int)ldw(a.cnt + up0 + q);
+    for (int x = tid; x < 1024; x += kSelThreads) {
+        h2[x] = 0u;
+        h3[x] = 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < kWordsPerThread; ++j) lmask[tid + j * kSelThreads] = mw[j];
+
+    // Candidate offsets: partition pp owns [offs[pp], offs[pp+1]) of the
+    // concatenated list, which is in position order.
+    {
+        int nc_all;
+        int o = block_scan(my_cnt, wave_tot, &nc_all);
+        for (int q = q0; q < q1; ++q) {
+            offs[q] = o;
+            o += (int)ldw(a.cnt + up0 + q);
+        }
+        if (tid == 0) offs[g.parts] = nc_all;
+        __syncthreads();
+    }
+    const int nc = offs[g.parts];
+    const bool cached = nc <= kTailCand;
+    auto cand_global = [&](int x) -> uint2 {
+        int lo = 0;   // last partition whose offset is <= x (fixed steps, unrolled)
+#pragma unroll
+        for (int step = kMaxSelectParts / 2; step >= 1; step >>= 1)
+            lo += (lo + step < g.parts && offs[lo + step] <= x) ? step : 0;
+        return ldc(a.seg + (up0 + lo) * a.part + (x - offs[lo]));
+    };
+    auto cand = [&](int x) -> uint2 { return cached ? cand_lds[x] : cand_global(x); };
+
+    uint32_t tau = 0u;
+    bool all_ties = true;   // every entry equal to tau is taken
+    {
+        // Pass 2 (bits 19..10) while gathering: every candidate is in bin d1.
+        constexpr int U = 8;   // loads in flight per thread
+        for (int x0 = tid; x0 < nc; x0 += U * kSelThreads) {
+            uint2 v[U];
+#pragma unroll
+            for (int j = 0; j < U; ++j) {
+                const int x = x0 + j * kSelThreads;
+                v[j] = x < nc ? cand_global(x) : make_uint2(0u, 0u);
+            }
+#pragma unroll
+            for (int j = 0; j < U; ++j) {
+                const int x = x0 + j * kSelThreads;
+                if (x < nc) {
+                    if (cached) cand_lds[x] = v[j];
+                    atomicAdd(&h2[(v[j].x >> 10) & 1023u], 1u);
+                }
+            }
+        }
+        __syncthreads();
+        const Digit dg2 = find_digit_wave(h2, need);
+        need -= dg2.above;
+        const uint32_t prefix = (d1 << 20) | ((uint32_t)dg2.bin << 10);
+        // Pass 3 (bits 9..0) over the candidates with that 22-bit prefix.
+        for (int x = tid; x < nc; x += kSelThreads) {
+            const uint32_t k = cand(x).x;
+            if ((k & 0xfffffc00u) == prefix) atomicAdd(&h3[k & 1023u], 1u);
+        }
+        __syncthreads();
+        const Digit dg3 = find_digit_wave(h3, need);
+        need -= dg3.above;
+        tau = prefix | (uint32_t)dg3.bin;
+        all_ties = need == dg3.count;
+    }
+    // Mark the candidates above tau and the chosen ties.  Ties are ranked
+    // only when some of them stay out: thread t then takes the contiguous
+    // slice [x0, x1) of the (position-ordered) list.
+    const int per = (nc + kSelThreads - 1) / kSelThreads;
+    const int x0 = min(nc, tid * per), x1 = min(nc, x0 + per);
+    int tie_base = 0;
+    if (!all_ties) {
+        int nt = 0;
+        for (int x = x0; x < x1; ++x) nt += cand(x).x == tau;
+        int tie_total;
+        tie_base = block_scan(nt, wave_tot, &tie_total);
+    }
+    // Sink, then the middle selections in position order, then the recent
+    // span: the bitmask holds middle positions only.
+    int32_t* out = a.idx + (size_t)u * a.budget;
+    for (int x = tid; x < g.s_end; x += kSelThreads)
+        if (x < a.budget) out[x] = x;
+    int emitted = g.s_end;
+    for (int cw = 0; cw < n_words; cw += kTailWords) {
+        const int nw = min(kTailWords, n_words - cw);
+        if (cw > 0) {
+            __syncthreads();
+            for (int x = tid; x < nw; x += kSelThreads) lmask[x] = ldw(mask + cw + x);
+            __syncthreads();
+        }
+        if (all_ties) {
+            for (int x = tid; x < nc; x += kSelThreads) {
+                const uint2 kp = cand(x);
+                const int w = (int)(kp.y >> 5) - cw;
+                if (kp.x >= tau && w >= 0 && w < nw) atomicOr(&lmask[w], 1u << (kp.y & 31u));
+            }
+        } else {
+            int rank = tie_base;
+            for (int x = x0; x < x1; ++x) {
+                const uint2 kp = cand(x);
+                bool sel = kp.x > tau;
+                if (kp.x == tau) {
+                    sel = rank < need;
+                    ++rank;
+                }
+                const int w = (int)(kp.y >> 5) - cw;
+                if (sel && w >= 0 && w < nw) atomicOr(&lmask[w], 1u << (kp.y & 31u));
+            }
+        }
+        __syncthreads();
+        // thread t owns words [w0, w1); their set bits, four words at a time,
+        // lowest first, without a branch per bit
+        const int wpt = (nw + kSelThreads - 1) / kSelThreads;
+        const int w0 = min(nw, tid * wpt), w1 = min(nw, w0 + wpt);
+        int cnt = 0;
+        for (int w = w0; w < w1; ++w) cnt += __builtin_popcount(lmask[w]);
+        int chunk_total;
+        int pos = emitted + block_scan(cnt, wave_tot, &chunk_total);
+        for (int w = w0; w < w1; w += 4) {
+            uint32_t m[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) m[i] = w + i < w1 ? lmask[w + i] : 0u;
+            uint64_t lo = (uint64_t)m[0] | ((uint64_t)m[1] << 32);
+            uint64_t hi = (uint64_t)m[2] | ((uint64_t)m[3] << 32);
+            const int n4 = __builtin_popcountll(lo) + __builtin_popcountll(hi);
+            const int base = (cw + w) * 32;
+            for (int k = 0; k < n4; ++k) {
+                const bool use_lo = lo != 0ull;
+                const uint64_t cur = use_lo ? lo : hi;
+                const int bit = __builtin_ctzll(cur) + (use_lo ? 0 : 64);
+                const uint64_t nxt = cur & (cur - 1ull);
+                lo = use_lo ? nxt : lo;
+                hi = use_lo ? hi : nxt;
+                if (pos < a.budget) out[pos] = base + bit;
+                ++pos;
+            }
+        }
+        emitted += chunk_total;
+    }
+    const int n_recent = g.T - g.r_start;
+    for (int x = tid; x < n_recent; x += kSelThreads)
+        if (emitted + x < a.budget) out[emitted + x] = g.r_start + x;
+    if (c_head == 0 && tid == 0) a.n_idx[b] = emitted + n_recent;
+}
+
+__global__ __launch_bounds__(kSelThreads) void select_finish_kernel(SelectArgs a) {
+    const int u = blockIdx.x;
+    const Geom g = geom_of(a, u / a.n_kv_heads);
+    if (g.simple) {
+        emit_ranges(a, u, g);
+        return;
+    }
+    finish_unit<false>(a, u, g, a.thr[2 * u], (int)a.thr[2 * u + 1]);
+}
+
 // ---------------------------------------------------------------------------
 // Kernel 2: threshold bin, bitmask words and candidate segments.
 // grid = (parts, units).
 // ---------------------------------------------------------------------------
-template <int NR>
+template <int NR, bool FUSE>
 __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) {
     const int p = blockIdx.x, u = blockIdx.y;
     const int b = u / a.n_kv_heads;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const Geom g = geom_of(a, b);
-    if (p >= g.parts || g.simple) return;   // the finish kernel emits ranges then
+    if (p >= g.parts) return;
+    if (g.simple) {   // ranges only: the finish kernel, or partition 0 here, emits them
+        if (FUSE && p == 0) emit_ranges(a, u, g);
+        return;
+    }
     const float* S = a.scores + (size_t)u * a.max_ctx;
     const size_t up0 = (size_t)u * a.parts;   // first slot of this unit
     uint32_t* mask = a.mask + (size_t)u * (a.parts * (a.part / 32));
@@ -234,7 +494,9 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
         }
         if (lane < 8) {
             const uint64_t m = lane < 2 ? defb[0] : lane < 4 ? defb[1] : lane < 6 ? defb[2] : defb[3];
-            mask[base / 32 + lane] = (lane & 1) ? (uint32_t)(m >> 32) : (uint32_t)m;
+            const uint32_t wd = (lane & 1) ? (uint32_t)(m >> 32) : (uint32_t)m;
+            if (FUSE) st_dev32(mask + base / 32 + lane, wd);
+            else mask[base / 32 + lane] = wd;
         }
         {
             int round_total;
@@ -242,269 +504,67 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
             slot = __builtin_amdgcn_readlane(slot, 0);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                if ((candb[e] >> lane) & 1ull)
-                    seg[slot + __builtin_popcountll(candb[e] & lt)] =
-                        make_uint2(keys[4 * r + e], (uint32_t)(base + e * 64 + lane));
+                if ((candb[e] >> lane) & 1ull) {
+                    uint2* dst = seg + slot + __builtin_popcountll(candb[e] & lt);
+                    const uint32_t pos = (uint32_t)(base + e * 64 + lane);
+                    if (FUSE)
+                        st_dev64(reinterpret_cast<uint64_t*>(dst),
+                                 (uint64_t)keys[4 * r + e] | ((uint64_t)pos << 32));
+                    else
+                        *dst = make_uint2(keys[4 * r + e], pos);
+                }
                 slot += __builtin_popcountll(candb[e]);
             }
             run += round_total;
         }
     }
-    if (tid == 0) {
-        a.cnt[up0 + p] = (uint32_t)run;
-        if (p == 0) {
-            a.thr[2 * u] = d1;
-            a.thr[2 * u + 1] = (uint32_t)need;
+    if (!FUSE) {
+        if (tid == 0) {
+            a.cnt[up0 + p] = (uint32_t)run;
+            if (p == 0) {
+                a.thr[2 * u] = d1;
+                a.thr[2 * u + 1] = (uint32_t)need;
+            }
         }
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Kernel 3: exact threshold, ties and ordered emission.  grid = units.
-// ---------------------------------------------------------------------------
-
-struct Digit {
-    int bin, above, count;
-};
-
-// In a 1024-bin histogram read from the top bin down, finds the bin where the
-// running count first reaches `remaining` (1 <= remaining <= the total), the
-// count strictly above that bin and the bin's own count.  Every wave computes
-// it on its own (lane l holds bins 1008-16l .. 1023-16l), so no barrier is
-// needed after it.
-__device__ __forceinline__ Digit find_digit_wave(const uint32_t* h, int remaining) {
-    const int lane = threadIdx.x & 63;
-    const int lo = 1008 - 16 * lane;
-    uint32_t v[16];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const uint4 w = *reinterpret_cast<const uint4*>(h + lo + 4 * i);
-        v[4 * i] = w.x;
-        v[4 * i + 1] = w.y;
-        v[4 * i + 2] = w.z;
-        v[4 * i + 3] = w.w;
-    }
-    int sum = 0;
-#pragma unroll
-    for (int q = 0; q < 16; ++q) sum += (int)v[q];
-    int above = wave_incl_scan(sum) - sum;
-    int bin = 0, ab = 0, cnt = 0;
-    bool found = false;
-#pragma unroll
-    for (int q = 15; q >= 0; --q) {
-        const int c = (int)v[q];
-        if (!found && above < remaining && remaining <= above + c) {
-            found = true;
-            bin = lo + q;
-            ab = above;
-            cnt = c;
-        }
-        above += c;
-    }
-    const uint64_t who = __ballot(found);
-    const int src = who ? __builtin_ctzll(who) : 0;
-    Digit d;
-    d.bin = __builtin_amdgcn_readlane(bin, src);
-    d.above = __builtin_amdgcn_readlane(ab, src);
-    d.count = __builtin_amdgcn_readlane(cnt, src);
-    return d;
-}
-
-__global__ __launch_bounds__(kSelThreads) void select_finish_kernel(SelectArgs a) {
-    const int u = blockIdx.x;
-    const int b = u / a.n_kv_heads;
-    const int c_head = u - b * a.n_kv_heads;
-    const int tid = threadIdx.x;
-    const Geom g = geom_of(a, b);
-    const size_t up0 = (size_t)u * a.parts;
-    const uint32_t* mask = a.mask + (size_t)u * (a.parts * (a.part / 32));
-
-    if (g.simple) {
-        // sink, then every middle position or none, then recent: ranges
-        int32_t* out = a.idx + (size_t)u * a.budget;
-        const int n = g.all_mid ? g.T : g.s_end + (g.T - g.r_start);
-        for (int x = tid; x < n; x += kSelThreads)
-            if (x < a.budget) out[x] = (g.all_mid || x < g.s_end) ? x : g.r_start + (x - g.s_end);
-        if (c_head == 0 && tid == 0) a.n_idx[b] = n;
         return;
     }
-
-    __shared__ int wave_tot[kSelWaves];
-    __shared__ __attribute__((aligned(16))) uint32_t h2[1024];   // read as uint4
-    __shared__ __attribute__((aligned(16))) uint32_t h3[1024];
-    __shared__ int offs[kMaxSelectParts + 1];
-    __shared__ uint2 cand_lds[kTailCand];
-    __shared__ uint32_t lmask[kTailWords];
-
-    // All first-round loads at once: the first bitmask chunk and the
-    // partition candidate counts.
-    constexpr int kWordsPerThread = kTailWords / kSelThreads;
-    const int n_words = (g.T + 31) >> 5;
-    uint32_t mw[kWordsPerThread];
-#pragma unroll
-    for (int j = 0; j < kWordsPerThread; ++j) {
-        const int x = tid + j * kSelThreads;
-        mw[j] = x < n_words ? mask[x] : 0u;
+    // Publish, then look once at the unit's tags: a workgroup that sees every
+    // partition's tag finishes the unit.  Each workgroup's data and tag are
+    // complete before it looks, so the last one to publish sees them all;
+    // two that both see them all write identical results.
+    if (tid == 0) st_dev32(a.cnt + up0 + p, (uint32_t)run);
+    wait_stores_done();
+    __syncthreads();
+    if (tid == 0) {
+        st_dev64(a.tag + up0 + p, a.call_tag);
+        wait_stores_done();
     }
-    const int per_p = (g.parts + kSelThreads - 1) / kSelThreads;
-    const int q0 = min(g.parts, tid * per_p), q1 = min(g.parts, q0 + per_p);
-    int my_cnt = 0;
-    for (int q = q0; q < q1; ++q) my_cnt += (int)a.cnt[up0 + q];
-    for (int x = tid; x < 1024; x += kSelThreads) {
-        h2[x] = 0u;
-        h3[x] = 0u;
+    __syncthreads();
+    if (wave == 0) {
+        bool in = true;
+        for (int q = lane; q < g.parts; q += kWave) in &= ld_dev64(a.tag + up0 + q) == a.call_tag;
+        const bool all_in = __all(in);
+        if (lane == 0) sh[0] = all_in;
     }
-#pragma unroll
-    for (int j = 0; j < kWordsPerThread; ++j) lmask[tid + j * kSelThreads] = mw[j];
-
-    // Candidate offsets: partition pp owns [offs[pp], offs[pp+1]) of the
-    // concatenated list, which is in position order.
-    {
-        int nc_all;
-        int o = block_scan(my_cnt, wave_tot, &nc_all);
-        for (int q = q0; q < q1; ++q) {
-            offs[q] = o;
-            o += (int)a.cnt[up0 + q];
-        }
-        if (tid == 0) offs[g.parts] = nc_all;
-        __syncthreads();
-    }
-    const int nc = offs[g.parts];
-    const bool cached = nc <= kTailCand;
-    auto cand_global = [&](int x) -> uint2 {
-        int lo = 0;   // last partition whose offset is <= x (fixed steps, unrolled)
-#pragma unroll
-        for (int step = kMaxSelectParts / 2; step >= 1; step >>= 1)
-            lo += (lo + step < g.parts && offs[lo + step] <= x) ? step : 0;
-        return a.seg[(up0 + lo) * a.part + (x - offs[lo])];
-    };
-    auto cand = [&](int x) -> uint2 { return cached ? cand_lds[x] : cand_global(x); };
-
-    uint32_t tau = 0u;
-    int need = 0;
-    bool all_ties = true;   // every entry equal to tau is taken
-    {
-        need = (int)a.thr[2 * u + 1];
-        const uint32_t d1 = a.thr[2 * u];
-        // Pass 2 (bits 19..10) while gathering: every candidate is in bin d1.
-        constexpr int U = 8;   // loads in flight per thread
-        for (int x0 = tid; x0 < nc; x0 += U * kSelThreads) {
-            uint2 v[U];
-#pragma unroll
-            for (int j = 0; j < U; ++j) {
-                const int x = x0 + j * kSelThreads;
-                v[j] = x < nc ? cand_global(x) : make_uint2(0u, 0u);
-            }
-#pragma unroll
-            for (int j = 0; j < U; ++j) {
-                const int x = x0 + j * kSelThreads;
-                if (x < nc) {
-                    if (cached) cand_lds[x] = v[j];
-                    atomicAdd(&h2[(v[j].x >> 10) & 1023u], 1u);
-                }
-            }
-        }
-        __syncthreads();
-        const Digit dg2 = find_digit_wave(h2, need);
-        need -= dg2.above;
-        const uint32_t prefix = (d1 << 20) | ((uint32_t)dg2.bin << 10);
-        // Pass 3 (bits 9..0) over the candidates with that 22-bit prefix.
-        for (int x = tid; x < nc; x += kSelThreads) {
-            const uint32_t k = cand(x).x;
-            if ((k & 0xfffffc00u) == prefix) atomicAdd(&h3[k & 1023u], 1u);
-        }
-        __syncthreads();
-        const Digit dg3 = find_digit_wave(h3, need);
-        need -= dg3.above;
-        tau = prefix | (uint32_t)dg3.bin;
-        all_ties = need == dg3.count;
-    }
-    // Mark the candidates above tau and the chosen ties.  Ties are ranked
-    // only when some of them stay out: thread t then takes the contiguous
-    // slice [x0, x1) of the (position-ordered) list.
-    const int per = (nc + kSelThreads - 1) / kSelThreads;
-    const int x0 = min(nc, tid * per), x1 = min(nc, x0 + per);
-    int tie_base = 0;
-    if (!all_ties) {
-        int nt = 0;
-        for (int x = x0; x < x1; ++x) nt += cand(x).x == tau;
-        int tie_total;
-        tie_base = block_scan(nt, wave_tot, &tie_total);
-    }
-    // Sink, then the middle selections in position order, then the recent
-    // span: the bitmask holds middle positions only.
-    int32_t* out = a.idx + (size_t)u * a.budget;
-    for (int x = tid; x < g.s_end; x += kSelThreads)
-        if (x < a.budget) out[x] = x;
-    int emitted = g.s_end;
-    for (int cw = 0; cw < n_words; cw += kTailWords) {
-        const int nw = min(kTailWords, n_words - cw);
-        if (cw > 0) {
-            __syncthreads();
-            for (int x = tid; x < nw; x += kSelThreads) lmask[x] = mask[cw + x];
-            __syncthreads();
-        }
-        if (all_ties) {
-            for (int x = tid; x < nc; x += kSelThreads) {
-                const uint2 kp = cand(x);
-                const int w = (int)(kp.y >> 5) - cw;
-                if (kp.x >= tau && w >= 0 && w < nw) atomicOr(&lmask[w], 1u << (kp.y & 31u));
-            }
-        } else {
-            int rank = tie_base;
-            for (int x = x0; x < x1; ++x) {
-                const uint2 kp = cand(x);
-                bool sel = kp.x > tau;
-                if (kp.x == tau) {
-                    sel = rank < need;
-                    ++rank;
-                }
-                const int w = (int)(kp.y >> 5) - cw;
-                if (sel && w >= 0 && w < nw) atomicOr(&lmask[w], 1u << (kp.y & 31u));
-            }
-        }
-        __syncthreads();
-        // thread t owns words [w0, w1); their set bits, four words at a time,
-        // lowest first, without a branch per bit
-        const int wpt = (nw + kSelThreads - 1) / kSelThreads;
-        const int w0 = min(nw, tid * wpt), w1 = min(nw, w0 + wpt);
-        int cnt = 0;
-        for (int w = w0; w < w1; ++w) cnt += __builtin_popcount(lmask[w]);
-        int chunk_total;
-        int pos = emitted + block_scan(cnt, wave_tot, &chunk_total);
-        for (int w = w0; w < w1; w += 4) {
-            uint32_t m[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) m[i] = w + i < w1 ? lmask[w + i] : 0u;
-            uint64_t lo = (uint64_t)m[0] | ((uint64_t)m[1] << 32);
-            uint64_t hi = (uint64_t)m[2] | ((uint64_t)m[3] << 32);
-            const int n4 = __builtin_popcountll(lo) + __builtin_popcountll(hi);
-            const int base = (cw + w) * 32;
-            for (int k = 0; k < n4; ++k) {
-                const bool use_lo = lo != 0ull;
-                const uint64_t cur = use_lo ? lo : hi;
-                const int bit = __builtin_ctzll(cur) + (use_lo ? 0 : 64);
-                const uint64_t nxt = cur & (cur - 1ull);
-                lo = use_lo ? nxt : lo;
-                hi = use_lo ? hi : nxt;
-                if (pos < a.budget) out[pos] = base + bit;
-                ++pos;
-            }
-        }
-        emitted += chunk_total;
-    }
-    const int n_recent = g.T - g.r_start;
-    for (int x = tid; x < n_recent; x += kSelThreads)
-        if (emitted + x < a.budget) out[emitted + x] = g.r_start + x;
-    if (c_head == 0 && tid == 0) a.n_idx[b] = emitted + n_recent;
+    __syncthreads();
+    if (sh[0]) finish_unit<true>(a, u, g, d1, need);
 }
+
+// Calls of at most kFuseMaxGroups partition workgroups finish inside the mark
+// kernel (its LDS then holds one workgroup per CU); larger ones use the
+// separate finish kernel.
+constexpr int kFuseMaxGroups = 256;
 
 template <int NR>
 void launch_nr(const SelectArgs& a, int n_units, hipStream_t stream) {
     const dim3 grid(a.parts, n_units), block(kSelThreads);
     hipLaunchKernelGGL(select_hist_kernel<NR>, grid, block, 0, stream, a);
-    hipLaunchKernelGGL(select_mark_kernel<NR>, grid, block, 0, stream, a);
-    hipLaunchKernelGGL(select_finish_kernel, dim3(n_units), block, 0, stream, a);
+    if ((long long)a.parts * n_units <= kFuseMaxGroups) {
+        hipLaunchKernelGGL(HIP_KERNEL_NAME(select_mark_kernel<NR, true>), grid, block, 0, stream, a);
+    } else {
+        hipLaunchKernelGGL(HIP_KERNEL_NAME(select_mark_kernel<NR, false>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL(select_finish_kernel, dim3(n_units), block, 0, stream, a);
+    }
 }
 
 }  // namespace

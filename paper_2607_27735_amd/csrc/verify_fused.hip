@@ -55,30 +55,6 @@ constexpr int static_lds_bytes() {
 
 __device__ __forceinline__ float safe_max(float m) { return m == -INFINITY ? 0.f : m; }
 
-// Device-coherent 32-bit store and load (agent scope, relaxed).
-__device__ __forceinline__ void st_dev(float* p, float v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float ld_dev(const float* p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float2 ld_dev2(const float2* p) {
-    const float* f = reinterpret_cast<const float*>(p);
-    return make_float2(ld_dev(f), ld_dev(f + 1));
-}
-__device__ __forceinline__ void st_dev64(uint64_t* p, uint64_t v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint64_t ld_dev64(const uint64_t* p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// Waits until every store this wave issued has completed (vmcnt = 0); the
-// signal fences keep the compiler from moving memory accesses across it.
-__device__ __forceinline__ void wait_stores_done() {
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    __builtin_amdgcn_s_waitcnt(0x0F70);
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-}
 
 // One 32-key tile: online softmax and P.V; the tile's probabilities relative
 // to the running row maxima go to the LDS stash, those maxima to mtile.

@@ -94,12 +94,12 @@ def test_verify_validation(lib):
     assert _verify(lib, params=_params(verify_mode=3)) == B.SSL_ERR_SHAPE
     assert _verify(lib, params=_params(verify_mode=-1)) == B.SSL_ERR_SHAPE
     # one-sweep requests whose (sequence, KV head) would need more than 128
-    # resident chunks: 2^20 keys, and 49153 keys at 64 rows (384-key chunks)
+    # resident chunks: 2^20 keys, and 65537 keys at 64 rows (512-key chunks)
     big = _shape(max_ctx=1 << 20)
     assert _verify(lib, shape=big, ctx=(1 << 20,), params=_params(verify_mode=2)) == \
         B.SSL_ERR_UNSUPPORTED
-    rows64 = _shape(n_q_heads=64, n_kv_heads=8, max_ctx=65536, max_q=8)
-    assert _verify(lib, shape=rows64, ctx=(128 * 384 + 1,), ql=(8,),
+    rows64 = _shape(n_q_heads=64, n_kv_heads=8, max_ctx=1 << 17, max_q=8)
+    assert _verify(lib, shape=rows64, ctx=(128 * 512 + 1,), ql=(8,),
                    params=_params(verify_mode=2)) == B.SSL_ERR_UNSUPPORTED
     for name in ("q", "k", "v", "out", "scores"):
         assert _verify(lib, **{name: None}) == B.SSL_ERR_NULL, name
