@@ -20,7 +20,7 @@ namespace {
 constexpr size_t kAlign = 256;
 constexpr int kVerifyRowCap = 64;
 constexpr int kDraftRowCap = 16;
-constexpr int kDraftChunk = 64;
+constexpr int kDraftChunk = 256;   // index entries per draft workgroup (4 waves)
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -158,7 +158,7 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
 
 struct DraftPlan {
     int chunk, n_items, n_rows;
-    size_t ml_off, o_off, bytes;
+    size_t ml_off, o_off, tag_off, bytes;
     SeqTable seq;
 };
 
@@ -188,7 +188,8 @@ int plan_draft(const ssl_shape* s, const ssl_params* p, const int32_t* n_idx, Dr
     plan->n_rows = s->batch * s->n_q_heads;
     plan->ml_off = 0;
     plan->o_off = align_up((size_t)items * kDraftRowCap * sizeof(float) * 2);
-    plan->bytes = plan->o_off + align_up((size_t)items * kDraftRowCap * 128 * sizeof(float));
+    plan->tag_off = plan->o_off + align_up((size_t)items * kDraftRowCap * 128 * sizeof(float));
+    plan->bytes = plan->tag_off + align_up((size_t)items * sizeof(uint64_t));
     return SSL_OK;
 }
 
@@ -418,6 +419,8 @@ int ssl_draft_attn(const ssl_shape* shape, const ssl_params* params, const int32
     a.idx = idx;
     a.part_ml = reinterpret_cast<float2*>(static_cast<char*>(workspace) + plan.ml_off);
     a.part_o = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.o_off);
+    a.tag = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + plan.tag_off);
+    a.call_tag = next_call_tag();
     a.out = out;
     a.n_q_heads = shape->n_q_heads;
     a.n_kv_heads = shape->n_kv_heads;
@@ -428,7 +431,7 @@ int ssl_draft_attn(const ssl_shape* shape, const ssl_params* params, const int32
     a.out_fp32 = params->out_fp32 ? 1 : 0;
     a.scale_log2 = params->sm_scale * 1.4426950408889634f;
     a.seq = plan.seq;
-    return launch_draft(a, plan.n_items, plan.n_rows, stream) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
+    return launch_draft(a, plan.n_items, stream) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
 }
 
 }  // extern "C"

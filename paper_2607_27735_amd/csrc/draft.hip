@@ -1,11 +1,15 @@
 // draft.hip -- draft-step attention over the gathered sparse view (Eq. 5).
 //
 // The gather is fused: K/V rows named by the index set are read in place from
-// the dense cache, never copied.  Work items are (sequence, KV head, chunk of
-// the index list), one wave each; the wave keeps an online softmax per query
-// head of the group (up to 16 heads = one MFMA row tile) and writes its
-// unnormalized partial output with the running (max, sum).  A combine kernel
-// merges the partials of each query head.
+// the dense cache, never copied.  A workgroup takes 256 consecutive entries of
+// one (sequence, KV head)'s index list, one wave per 64; each wave keeps an
+// online softmax per query head of the group (up to 16 heads = one MFMA row
+// tile).  The four waves are merged through LDS into one partial output with
+// its (max, sum) per head, which the workgroup publishes with device-coherent
+// stores before writing its 64-bit call tag; it then looks once at the tags
+// of its (sequence, KV head).  The workgroup that sees all of them -- the last
+// to publish always does -- merges the partials and writes the output (two
+// that both see them write identical results).
 //
 // The MFMA layouts are the verify kernel's: K.Q^T on the bf16 MFMA with the
 // keys as A rows, O^T = V^T P^T so a head's softmax state and output stay in
@@ -19,6 +23,10 @@ namespace {
 
 constexpr int kTile = 32;
 constexpr int kRowCap = 16;
+constexpr int kDraftWaves = 4;
+constexpr int kDraftThreads = kDraftWaves * kWave;
+constexpr int kWaveChunk = 2 * kTile;          // index entries per wave
+constexpr int kParkStride = kHeadDim + 4;      // floats per parked head row
 
 __device__ __forceinline__ int a_row_key(int m) { return (m >> 2) + 4 * (m & 3); }
 
@@ -119,132 +127,164 @@ __device__ __forceinline__ void draft_tile(const DraftArgs& a, const u32x4 (&qop
     }
 }
 
-__global__ __launch_bounds__(kWave) void draft_kernel(DraftArgs a) {
+__global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
     const DItem it = decode_ditem(a.seq, blockIdx.x, a.n_kv_heads, a.chunk);
-    const int lane = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int m16 = lane & 15, G = lane >> 4;
     const int g = a.group;
 
-    u32x4 qop[4];
-    if (m16 < g) {
-        const uint16_t* qp = a.q + ((size_t)it.b * a.n_q_heads + it.c * g + m16) * kHeadDim + 8 * G;
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) qop[kb] = ld_u32x4(qp + 32 * kb);
-    } else {
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) qop[kb] = u32x4{0u, 0u, 0u, 0u};
-    }
-    const size_t cache_off = (size_t)it.unit * a.max_ctx * kHeadDim;
-    const uint16_t* kbase = a.k + cache_off;
-    const uint16_t* vbase = a.v + cache_off;
-    const int32_t* ib = a.idx + (size_t)it.unit * a.budget;
-    const int last = it.n - 1;
+    __shared__ float2 wml[kDraftWaves][kRowCap];
+    __shared__ float2 gml[kRowCap];
+    __shared__ float park[kDraftWaves][kRowCap][kParkStride];
+    __shared__ int sh_all;
 
+    // ---- one wave: 64 entries of the index list ----------------------------
+    const int wbeg = it.key_begin + wave * kWaveChunk;
+    const int wend = min(wbeg + kWaveChunk, it.key_end);
     float M = -INFINITY, L = 0.f;
     f32x4 oacc[8];
 #pragma unroll
     for (int jd = 0; jd < 8; ++jd) oacc[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    // One chunk is two 32-key tiles: lane l loads the cache row of chunk
-    // position l once, then every K/V row of both tiles is requested at once.
-    const int my_row = min(max(ib[min(it.key_begin + lane, last)], 0), a.max_ctx - 1);
-    Gathered ta, tb;
-    gather_tile(my_row, 0, kbase, vbase, m16, G, ta);
-    gather_tile(my_row, kTile, kbase, vbase, m16, G, tb);
-    draft_tile(a, qop, ta, it.key_begin, it.key_end, G, M, L, oacc);
-    if (it.key_begin + kTile < it.key_end)
-        draft_tile(a, qop, tb, it.key_begin + kTile, it.key_end, G, M, L, oacc);
-    L += shfl_xor_f(L, 16);
-    L += shfl_xor_f(L, 32);
-
-    const size_t item = blockIdx.x;
-    if (G == 0) a.part_ml[item * kRowCap + m16] = make_float2(M, L);
-    f32x4* po = reinterpret_cast<f32x4*>(a.part_o + (item * kRowCap + m16) * kHeadDim);
+    if (wbeg < wend) {
+        u32x4 qop[4];
+        if (m16 < g) {
+            const uint16_t* qp =
+                a.q + ((size_t)it.b * a.n_q_heads + it.c * g + m16) * kHeadDim + 8 * G;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int c4 = (32 * G + 8 * i) / 4;
-        po[c4] = f32x4{oacc[0][i], oacc[1][i], oacc[2][i], oacc[3][i]};
-        po[c4 + 1] = f32x4{oacc[4][i], oacc[5][i], oacc[6][i], oacc[7][i]};
-    }
-}
-
-// Combine of one query head's partials.  256 threads: thread t handles
-// head-dim quad t % 32 for the items t / 32, t / 32 + 8, ..., merging them
-// online; the eight partial states are then merged in a fixed order.
-constexpr int kCombineThreads = 256;
-constexpr int kCombineGroups = kCombineThreads / 32;
-
-__global__ __launch_bounds__(kCombineThreads) void draft_combine_kernel(DraftArgs a) {
-    const SeqTable& st = a.seq;
-    const int bh = blockIdx.x;
-    const int b = bh / a.n_q_heads;
-    const int h = bh - b * a.n_q_heads;
-    const int c = h / a.group;
-    const int row = h - c * a.group;
-    const int nchunk = (st.ctx[b] + a.chunk - 1) / a.chunk;
-    const int item0 = st.item_start[b] + c * nchunk;
-    const int d4 = threadIdx.x & 31, sg = threadIdx.x >> 5;
-    const f32x4* po = reinterpret_cast<const f32x4*>(a.part_o);
-    float M = -INFINITY, L = 0.f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int s0 = sg; s0 < nchunk; s0 += 8 * kCombineGroups) {
-        float2 ml[8];
-        f32x4 o[8];
+            for (int kb = 0; kb < 4; ++kb) qop[kb] = ld_u32x4(qp + 32 * kb);
+        } else {
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int s = s0 + u * kCombineGroups;
-            const bool ok = s < nchunk;
-            const size_t slot = (size_t)(item0 + (ok ? s : 0)) * kRowCap + row;
-            ml[u] = ok ? a.part_ml[slot] : make_float2(-INFINITY, 0.f);
-            o[u] = ok ? po[slot * (kHeadDim / 4) + d4] : f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int kb = 0; kb < 4; ++kb) qop[kb] = u32x4{0u, 0u, 0u, 0u};
         }
-        float Mn = M;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) Mn = fmaxf(Mn, ml[u].x);
-        const float alpha = fast_exp2(M - Mn);   // M = -inf at first: 0
-        L *= alpha;
-        acc *= alpha;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const float wgt = fast_exp2(ml[u].x - Mn);   // empty slots: 0
-            L += ml[u].y * wgt;
-            acc += o[u] * wgt;
-        }
-        M = Mn;
+        const size_t cache_off = (size_t)it.unit * a.max_ctx * kHeadDim;
+        const uint16_t* kbase = a.k + cache_off;
+        const uint16_t* vbase = a.v + cache_off;
+        const int32_t* ib = a.idx + (size_t)it.unit * a.budget;
+        const int last = it.n - 1;
+        // Lane l loads the cache row of entry l once; every K/V row of both
+        // tiles is then requested at once.
+        const int my_row = min(max(ib[min(wbeg + lane, last)], 0), a.max_ctx - 1);
+        Gathered ta, tb;
+        gather_tile(my_row, 0, kbase, vbase, m16, G, ta);
+        gather_tile(my_row, kTile, kbase, vbase, m16, G, tb);
+        draft_tile(a, qop, ta, wbeg, wend, G, M, L, oacc);
+        if (wbeg + kTile < wend) draft_tile(a, qop, tb, wbeg + kTile, wend, G, M, L, oacc);
+        L += shfl_xor_f(L, 16);
+        L += shfl_xor_f(L, 32);
     }
-    __shared__ f32x4 racc[kCombineGroups][32];
-    __shared__ float2 rml[kCombineGroups][32];
-    racc[sg][d4] = acc;
-    rml[sg][d4] = make_float2(M, L);
+
+    // ---- merge the four waves (fixed order) --------------------------------
+    if (G == 0) wml[wave][m16] = make_float2(M, L);
     __syncthreads();
-    if (sg != 0) return;
-    float Mx = -INFINITY;
+    if (tid < kRowCap) {
+        float Mx = -INFINITY;
 #pragma unroll
-    for (int gq = 0; gq < kCombineGroups; ++gq) Mx = fmaxf(Mx, rml[gq][d4].x);
-    float Lx = 0.f;
-    f32x4 ox = {0.f, 0.f, 0.f, 0.f};
+        for (int w = 0; w < kDraftWaves; ++w) Mx = fmaxf(Mx, wml[w][tid].x);
+        float Lx = 0.f;
 #pragma unroll
-    for (int gq = 0; gq < kCombineGroups; ++gq) {
-        const float2 m = rml[gq][d4];
-        const float wgt = m.x == -INFINITY ? 0.f : fast_exp2(m.x - Mx);
-        Lx += m.y * wgt;
-        ox += racc[gq][d4] * wgt;
+        for (int w = 0; w < kDraftWaves; ++w)
+            Lx += wml[w][tid].x == -INFINITY ? 0.f : wml[w][tid].y * fast_exp2(wml[w][tid].x - Mx);
+        gml[tid] = make_float2(Mx, Lx);
     }
-    ox *= 1.0f / Lx;
-    const size_t base = ((size_t)b * a.n_q_heads + h) * kHeadDim + 4 * d4;
-    if (a.out_fp32) {
-        *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out) + base) = ox;
-    } else {
-        uint2 pk = make_uint2(pack_bf16(ox[0], ox[1]), pack_bf16(ox[2], ox[3]));
-        *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + base) = pk;
+    __syncthreads();
+    {
+        const float Mx = gml[m16].x;
+        const float f = M == -INFINITY ? 0.f : fast_exp2(M - Mx);
+        float* dst = &park[wave][m16][0];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int c = 32 * G + 8 * i;
+            *reinterpret_cast<f32x4*>(dst + c) =
+                f32x4{oacc[0][i], oacc[1][i], oacc[2][i], oacc[3][i]} * f;
+            *reinterpret_cast<f32x4*>(dst + c + 4) =
+                f32x4{oacc[4][i], oacc[5][i], oacc[6][i], oacc[7][i]} * f;
+        }
+    }
+    __syncthreads();
+
+    // ---- publish this workgroup's partial (g heads x 128, and (max, sum)) ----
+    const size_t wg = blockIdx.x;
+    for (int x = tid; x < g * (kHeadDim / 2); x += kDraftThreads) {
+        const int row = x / (kHeadDim / 2), c2 = x - row * (kHeadDim / 2);
+        float2 o = *reinterpret_cast<const float2*>(&park[0][row][2 * c2]);
+#pragma unroll
+        for (int w = 1; w < kDraftWaves; ++w) {
+            const float2 v = *reinterpret_cast<const float2*>(&park[w][row][2 * c2]);
+            o.x += v.x;
+            o.y += v.y;
+        }
+        st_dev64(reinterpret_cast<uint64_t*>(a.part_o + (wg * kRowCap + row) * kHeadDim) + c2,
+                 __builtin_bit_cast(uint64_t, o));
+    }
+    if (tid < g)
+        st_dev64(reinterpret_cast<uint64_t*>(a.part_ml + wg * kRowCap + tid),
+                 __builtin_bit_cast(uint64_t, gml[tid]));
+    wait_stores_done();
+    __syncthreads();
+    if (tid == 0) {
+        st_dev64(a.tag + wg, a.call_tag);
+        wait_stores_done();
+    }
+    __syncthreads();
+    if (wave == 0) {
+        bool in = true;
+        for (int j = lane; j < it.nchunk; j += kWave) in &= ld_dev64(a.tag + it.item0 + j) == a.call_tag;
+        const bool all_in = __all(in);
+        if (lane == 0) sh_all = all_in;
+    }
+    __syncthreads();
+    if (!sh_all) return;
+
+    // ---- the last to publish: merge the partials of every head ---------------
+    for (int x = tid; x < g * (kHeadDim / 4); x += kDraftThreads) {
+        const int row = x >> 5, d4 = x & 31;
+        float Mx = -INFINITY, Lx = 0.f;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int j0 = 0; j0 < it.nchunk; j0 += 8) {
+            float2 ml[8];
+            f32x4 o[8];
+#pragma unroll
+            for (int uu = 0; uu < 8; ++uu) {
+                const int j = j0 + uu;
+                const bool ok = j < it.nchunk;
+                const size_t slot = (size_t)(it.item0 + (ok ? j : 0)) * kRowCap + row;
+                const uint64_t mlw = ok ? ld_dev64(reinterpret_cast<const uint64_t*>(a.part_ml + slot)) : 0ull;
+                ml[uu] = ok ? __builtin_bit_cast(float2, mlw) : make_float2(-INFINITY, 0.f);
+                const uint64_t* po = reinterpret_cast<const uint64_t*>(a.part_o + slot * kHeadDim) + 2 * d4;
+                const uint64_t lo = ok ? ld_dev64(po) : 0ull, hi = ok ? ld_dev64(po + 1) : 0ull;
+                const float2 flo = __builtin_bit_cast(float2, lo), fhi = __builtin_bit_cast(float2, hi);
+                o[uu] = f32x4{flo.x, flo.y, fhi.x, fhi.y};
+            }
+            float Mn = Mx;
+#pragma unroll
+            for (int uu = 0; uu < 8; ++uu) Mn = fmaxf(Mn, ml[uu].x);
+            const float alpha = Mx == -INFINITY ? 0.f : fast_exp2(Mx - Mn);
+            Lx *= alpha;
+            acc *= alpha;
+#pragma unroll
+            for (int uu = 0; uu < 8; ++uu) {
+                const float wgt = ml[uu].x == -INFINITY ? 0.f : fast_exp2(ml[uu].x - Mn);
+                Lx += ml[uu].y * wgt;
+                acc += o[uu] * wgt;
+            }
+            Mx = Mn;
+        }
+        acc *= 1.0f / Lx;
+        const int h = it.c * g + row;
+        const size_t base = ((size_t)it.b * a.n_q_heads + h) * kHeadDim + 4 * d4;
+        if (a.out_fp32) {
+            *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out) + base) = acc;
+        } else {
+            uint2 pk = make_uint2(pack_bf16(acc[0], acc[1]), pack_bf16(acc[2], acc[3]));
+            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + base) = pk;
+        }
     }
 }
 
 }  // namespace
 
-hipError_t launch_draft(const DraftArgs& a, int n_items, int n_rows_total, hipStream_t stream) {
-    hipLaunchKernelGGL(draft_kernel, dim3(n_items), dim3(kWave), 0, stream, a);
-    hipLaunchKernelGGL(draft_combine_kernel, dim3(n_rows_total), dim3(kCombineThreads), 0, stream, a);
+hipError_t launch_draft(const DraftArgs& a, int n_items, hipStream_t stream) {
+    hipLaunchKernelGGL(draft_kernel, dim3(n_items), dim3(kDraftThreads), 0, stream, a);
     return hipGetLastError();
 }
 

@@ -63,8 +63,10 @@ struct DraftArgs {
     const uint16_t* k;
     const uint16_t* v;
     const int32_t* idx;     // [batch][n_kv][budget]
-    float2* part_ml;        // [n_items][16]
-    float* part_o;          // [n_items][16][128]
+    float2* part_ml;        // [n_items][16]       per-workgroup (max, sum) per head
+    float* part_o;          // [n_items][16][128]  per-workgroup partial outputs
+    uint64_t* tag;          // [n_items] publication tags (no initialisation needed)
+    uint64_t call_tag;      // this call's tag: unique within the process
     void* out;              // [batch][n_q][128]
     int32_t n_q_heads, n_kv_heads, group, max_ctx, budget, chunk, out_fp32;
     float scale_log2;
@@ -95,6 +97,7 @@ int fused_max_chunk(int row_tiles);
 // <= kSelectTargetParts partitions.
 int select_part_len(int max_t);
 hipError_t launch_select(const SelectArgs& a, int n_units, hipStream_t stream);
-hipError_t launch_draft(const DraftArgs& a, int n_items, int n_rows_total, hipStream_t stream);
+// One workgroup per `chunk` (256) index entries; no combine kernel.
+hipError_t launch_draft(const DraftArgs& a, int n_items, hipStream_t stream);
 
 }  // namespace ssl

@@ -182,8 +182,11 @@ def test_select_long_contexts():
     the finishing workgroup caches.  Bit-exact against the oracle."""
     from types import SimpleNamespace
     rng = np.random.default_rng(11)
-    for ctx in ([140001, 65537], [262144, 3], [40000, 33000]):
-        w = SimpleNamespace(batch=2, n_q_heads=4, n_kv_heads=2, max_ctx=max(ctx),
+    # the first three calls have at most 256 partitions in all and finish inside the
+    # mark kernel; the last (16 x 8 units of 20 partitions) uses the finish kernel
+    for batch, hkv, ctx in ((2, 2, [140001, 65537]), (2, 2, [262144, 3]), (2, 2, [40000, 33000]),
+                            (16, 8, [20000 - 37 * i for i in range(16)])):
+        w = SimpleNamespace(batch=batch, n_q_heads=hkv * 2, n_kv_heads=hkv, max_ctx=max(ctx),
                             ctx_len=np.array(ctx, dtype=np.int32), sm_scale=1.0, window=16,
                             k_sink=4, k_recent=32, budget=4096)
         shape = (w.batch, w.n_kv_heads, w.max_ctx)
