@@ -156,6 +156,14 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
     return SSL_OK;
 }
 
+// AUTO takes one sweep where it fits and a KV head has at most 32 verify rows;
+// with more rows the single-sweep kernel (one wave per SIMD, logits of every
+// row in LDS) is bound by its per-tile latency and two sweeps are faster.
+bool use_one_sweep(const VerifyPlan& plan, const ssl_params* p) {
+    if (!plan.fused_ok || p->verify_mode == SSL_VERIFY_TWO_SWEEP) return false;
+    return p->verify_mode == SSL_VERIFY_ONE_SWEEP || plan.row_tiles <= 2;
+}
+
 struct DraftPlan {
     int chunk, n_items, n_rows;
     size_t ml_off, o_off, tag_off, bytes;
@@ -282,7 +290,7 @@ int ssl_verify_plan(const ssl_shape* shape, const ssl_params* params, const int3
     VerifyPlan plan;
     const int rc = plan_verify(shape, params, ctx_len_host, q_len_host, &plan);
     if (rc) return rc;
-    const bool one = plan.fused_ok && params->verify_mode != SSL_VERIFY_TWO_SWEEP;
+    const bool one = use_one_sweep(plan, params);
     *schedule_out = one ? SSL_VERIFY_ONE_SWEEP : SSL_VERIFY_TWO_SWEEP;
     *chunk_out = one ? plan.fused_chunk : plan.chunk;
     *items_out = one ? plan.fused_slots : plan.n_items;
@@ -321,7 +329,7 @@ int ssl_verify_attn(const ssl_shape* shape, const ssl_params* params, const int3
     a.out_fp32 = params->out_fp32 ? 1 : 0;
     a.scale_log2 = params->sm_scale * 1.4426950408889634f;
     a.seq = plan.seq;
-    if (plan.fused_ok && params->verify_mode != SSL_VERIFY_TWO_SWEEP) {
+    if (use_one_sweep(plan, params)) {
         FusedArgs fa;
         fa.v = a;
         fa.v.chunk = plan.fused_chunk;

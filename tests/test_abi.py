@@ -219,9 +219,11 @@ def test_binding_refuses_cpu_tensors(lib):
 def test_verify_plan_schedules(lib):
     """Schedules of the named workloads: one sweep fits wherever a (sequence,
     KV head) needs at most 128 chunks of what the LDS logit stash holds (all
-    but the 131K context), and AUTO takes it there; TWO_SWEEP always plans."""
+    but the 131K context); AUTO takes it there when a KV head has at most 32
+    verify rows (not at 44 or 48); TWO_SWEEP always plans."""
     from paper_2607_27735_amd.workloads import CONFIGS
     fits = {1: True, 2: True, 3: True, 4: False, 5: True}
+    auto_one = {1: True, 2: True, 3: False, 4: False, 5: False}
     for n, cfg in CONFIGS.items():
         batch = cfg["batch"]
         ctx = cfg.get("ctx_len") or [cfg["ctx_range"][1]] * batch
@@ -229,7 +231,7 @@ def test_verify_plan_schedules(lib):
         shape = B.Shape(batch, cfg["n_q_heads"], cfg["n_kv_heads"], 128,
                         cfg.get("max_ctx") or max(ctx), max(ql))
         sch, chunk, items = B.verify_plan(shape, B.make_params(1 / math.sqrt(128)), ctx, ql)
-        assert sch == (B.VERIFY_ONE_SWEEP if fits[n] else B.VERIFY_TWO_SWEEP), n
+        assert sch == (B.VERIFY_ONE_SWEEP if auto_one[n] else B.VERIFY_TWO_SWEEP), n
         assert chunk % 128 == 0 and items >= 1
         two = B.make_params(1 / math.sqrt(128), verify_mode=B.VERIFY_TWO_SWEEP)
         sch, chunk, items = B.verify_plan(shape, two, ctx, ql)
