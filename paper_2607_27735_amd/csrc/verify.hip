@@ -182,12 +182,14 @@ __global__ __launch_bounds__(kThreads) void verify_main_kernel(VerifyArgs a) {
     const int ntile = (it.key_end - it.key_begin + kTile - 1) / kTile;
 
     // Row log-sum-exp from the statistics of every item of this (sequence, KV
-    // head): thread t merges row t % 64 over the items t / 64, t / 64 + 4, ...
-    // (all of its loads in flight together), then the four partial states of
-    // each row are merged in a fixed order.
+    // head), computed while the first K/V tiles are loading: thread t merges
+    // row t % 64 over the items t / 64, t / 64 + 4, ... (all of its loads in
+    // flight together), then the four partial states of each row are merged
+    // in a fixed order.
     __shared__ float2 lse_part[kWaves][kRowCap];
     __shared__ float lse_row[kRowCap];
-    {
+    float lse[NRT];
+    auto row_lse = [&] {
         const int R = it.nq * a.group;
         const int rr = threadIdx.x & (kRowCap - 1), ph = threadIdx.x >> 6;
         float M = -INFINITY, L = 0.f;
@@ -214,10 +216,9 @@ __global__ __launch_bounds__(kThreads) void verify_main_kernel(VerifyArgs a) {
             lse_row[threadIdx.x] = Lx > 0.f ? Mx + fast_log2(Lx) : INFINITY;
         }
         __syncthreads();
-    }
-    float lse[NRT];
 #pragma unroll
-    for (int rt = 0; rt < NRT; ++rt) lse[rt] = lse_row[rt * 16 + m16];
+        for (int rt = 0; rt < NRT; ++rt) lse[rt] = lse_row[rt * 16 + m16];
+    };
 
     f32x4 oacc[8][NRT];
 #pragma unroll
@@ -234,7 +235,8 @@ __global__ __launch_bounds__(kThreads) void verify_main_kernel(VerifyArgs a) {
         [&](const KVTile& b, int t) {
             main_tile<NRT>(a, r, lse, b.k, b.v, it.key_begin + t * kTile, it.key_end, srow, m16,
                            G, oacc);
-        });
+        },
+        row_lse);
 
     // Sum the four waves' partial outputs in LDS (fixed order), then write the
     // item's rows.  oacc[jd][rt][i] is row rt*16+m16, head-dim 32G + 8i + jd.

@@ -97,15 +97,17 @@ __device__ __forceinline__ void qk_tile(const u32x4 (&kr)[2][4], const Rows<NRT>
 // Runs compute(tile) over the wave's tiles first, first + step, ... < ntile
 // with a ring of NBUF register buffers: while one tile is computed, the loads
 // of the next NBUF - 1 tiles are in flight.  load(buf, tile) issues loads only.
-template <int NBUF, typename Buf, typename Load, typename Compute>
+template <int NBUF, typename Buf, typename Load, typename Compute, typename Pre>
 __device__ __forceinline__ void tile_pipeline(int first, int ntile, int step, Load&& load,
-                                              Compute&& compute) {
+                                              Compute&& compute, Pre&& pre) {
     Buf buf[NBUF];
 #pragma unroll
     for (int p = 0; p < NBUF - 1; ++p) {
         const int t = first + p * step;
         if (t < ntile) load(buf[p], t);
     }
+    // Every wave runs pre() once, with the first tiles' loads already in flight.
+    pre();
     int tt = first;
     while (tt < ntile) {
 #pragma unroll
@@ -118,6 +120,12 @@ __device__ __forceinline__ void tile_pipeline(int first, int ntile, int step, Lo
             tt += step;
         }
     }
+}
+
+template <int NBUF, typename Buf, typename Load, typename Compute>
+__device__ __forceinline__ void tile_pipeline(int first, int ntile, int step, Load&& load,
+                                              Compute&& compute) {
+    tile_pipeline<NBUF, Buf>(first, ntile, step, load, compute, [] {});
 }
 
 struct KTile {
