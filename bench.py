@@ -47,7 +47,7 @@ REPO = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(REPO, "profiles", "verify_traffic_llama8b_T32K.txt")
 OUR_KERNELS = ("verify_fused_kernel", "verify_stats_kernel", "verify_main_kernel",
                "verify_combine_kernel", "select_hist_kernel", "select_mark_kernel",
-               "select_finish_kernel", "draft_kernel", "draft_combine_kernel")
+               "select_finish_kernel", "select_fused_kernel", "draft_kernel", "draft_combine_kernel")
 VERIFY_KERNELS = ("verify_fused_kernel", "verify_stats_kernel", "verify_main_kernel",
                   "verify_combine_kernel")
 

@@ -166,10 +166,8 @@ __device__ __forceinline__ Digit find_digit_wave(const uint32_t* h, int remainin
 }
 
 // ---------------------------------------------------------------------------
-// The finish of one unit: exact threshold, ties and ordered emission.
-// DEV: the unit's bitmask, counts and candidates were published by other
-// workgroups of the running kernel, so they are read with device-coherent
-// loads; otherwise they come from an earlier kernel.
+// The finish of one unit (separate kernel): exact threshold, ties and ordered
+// emission from the bitmask, counts and candidates of the mark kernel.
 // ---------------------------------------------------------------------------
 
 // Sink, then every middle position or none, then recent: ranges.
@@ -183,19 +181,14 @@ __device__ __forceinline__ void emit_ranges(const SelectArgs& a, int u, const Ge
     if (u - b * a.n_kv_heads == 0 && tid == 0) a.n_idx[b] = n;
 }
 
-template <bool DEV>
 __device__ void finish_unit(const SelectArgs& a, int u, const Geom& g, uint32_t d1, int need) {
     const int b = u / a.n_kv_heads;
     const int c_head = u - b * a.n_kv_heads;
     const int tid = threadIdx.x;
     const size_t up0 = (size_t)u * a.parts;
     const uint32_t* mask = a.mask + (size_t)u * (a.parts * (a.part / 32));
-    auto ldw = [](const uint32_t* p) -> uint32_t { return DEV ? ld_dev32(p) : *p; };
-    auto ldc = [](const uint2* p) -> uint2 {
-        if (!DEV) return *p;
-        const uint64_t v = ld_dev64(reinterpret_cast<const uint64_t*>(p));
-        return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
-    };
+    auto ldw = [](const uint32_t* p) -> uint32_t { return *p; };
+    auto ldc = [](const uint2* p) -> uint2 { return *p; };
 
     __shared__ int wave_tot[kSelWaves];
     __shared__ __attribute__((aligned(16))) uint32_t h2[1024];   // read as uint4
@@ -371,24 +364,20 @@ __global__ __launch_bounds__(kSelThreads) void select_finish_kernel(SelectArgs a
         emit_ranges(a, u, g);
         return;
     }
-    finish_unit<false>(a, u, g, a.thr[2 * u], (int)a.thr[2 * u + 1]);
+    finish_unit(a, u, g, a.thr[2 * u], (int)a.thr[2 * u + 1]);
 }
 
 // ---------------------------------------------------------------------------
 // Kernel 2: threshold bin, bitmask words and candidate segments.
 // grid = (parts, units).
 // ---------------------------------------------------------------------------
-template <int NR, bool FUSE>
+template <int NR>
 __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) {
     const int p = blockIdx.x, u = blockIdx.y;
     const int b = u / a.n_kv_heads;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const Geom g = geom_of(a, b);
-    if (p >= g.parts) return;
-    if (g.simple) {   // ranges only: the finish kernel, or partition 0 here, emits them
-        if (FUSE && p == 0) emit_ranges(a, u, g);
-        return;
-    }
+    if (p >= g.parts || g.simple) return;   // the finish kernel emits ranges then
     const float* S = a.scores + (size_t)u * a.max_ctx;
     const size_t up0 = (size_t)u * a.parts;   // first slot of this unit
     uint32_t* mask = a.mask + (size_t)u * (a.parts * (a.part / 32));
@@ -494,9 +483,7 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
         }
         if (lane < 8) {
             const uint64_t m = lane < 2 ? defb[0] : lane < 4 ? defb[1] : lane < 6 ? defb[2] : defb[3];
-            const uint32_t wd = (lane & 1) ? (uint32_t)(m >> 32) : (uint32_t)m;
-            if (FUSE) st_dev32(mask + base / 32 + lane, wd);
-            else mask[base / 32 + lane] = wd;
+            mask[base / 32 + lane] = (lane & 1) ? (uint32_t)(m >> 32) : (uint32_t)m;
         }
         {
             int round_total;
@@ -504,65 +491,404 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
             slot = __builtin_amdgcn_readlane(slot, 0);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                if ((candb[e] >> lane) & 1ull) {
-                    uint2* dst = seg + slot + __builtin_popcountll(candb[e] & lt);
-                    const uint32_t pos = (uint32_t)(base + e * 64 + lane);
-                    if (FUSE)
-                        st_dev64(reinterpret_cast<uint64_t*>(dst),
-                                 (uint64_t)keys[4 * r + e] | ((uint64_t)pos << 32));
-                    else
-                        *dst = make_uint2(keys[4 * r + e], pos);
-                }
+                if ((candb[e] >> lane) & 1ull)
+                    seg[slot + __builtin_popcountll(candb[e] & lt)] =
+                        make_uint2(keys[4 * r + e], (uint32_t)(base + e * 64 + lane));
                 slot += __builtin_popcountll(candb[e]);
             }
             run += round_total;
         }
     }
-    if (!FUSE) {
-        if (tid == 0) {
-            a.cnt[up0 + p] = (uint32_t)run;
-            if (p == 0) {
-                a.thr[2 * u] = d1;
-                a.thr[2 * u + 1] = (uint32_t)need;
-            }
-        }
-        return;
-    }
-    // Publish, then look once at the unit's tags: a workgroup that sees every
-    // partition's tag finishes the unit.  Each workgroup's data and tag are
-    // complete before it looks, so the last one to publish sees them all;
-    // two that both see them all write identical results.
-    if (tid == 0) st_dev32(a.cnt + up0 + p, (uint32_t)run);
-    wait_stores_done();
-    __syncthreads();
     if (tid == 0) {
-        st_dev64(a.tag + up0 + p, a.call_tag);
-        wait_stores_done();
+        a.cnt[up0 + p] = (uint32_t)run;
+        if (p == 0) {
+            a.thr[2 * u] = d1;
+            a.thr[2 * u + 1] = (uint32_t)need;
+        }
     }
-    __syncthreads();
-    if (wave == 0) {
-        bool in = true;
-        for (int q = lane; q < g.parts; q += kWave) in &= ld_dev64(a.tag + up0 + q) == a.call_tag;
-        const bool all_in = __all(in);
-        if (lane == 0) sh[0] = all_in;
-    }
-    __syncthreads();
-    if (sh[0]) finish_unit<true>(a, u, g, d1, need);
 }
 
-// Calls of at most kFuseMaxGroups partition workgroups finish inside the mark
-// kernel (its LDS then holds one workgroup per CU); larger ones use the
-// separate finish kernel.
+// ---------------------------------------------------------------------------
+// One kernel for calls of at most kFuseMaxGroups partition workgroups.  The
+// partitions of one unit are resident together (workgroups are dispatched in
+// index order and a unit's partitions are consecutive, so when the lowest
+// unfinished unit waits, every workgroup ahead of its partitions has finished)
+// and exchange what they need through the workspace with device-coherent
+// stores and loads, each exchange closed by a 64-bit call tag:
+//   A. every partition publishes its nonzero histogram bins (bin, count); all
+//      of them add the unit's bins and find the bin d1 holding the K_mid-th
+//      largest middle score and `need`;
+//   B. every partition publishes its bin-d1 candidates (in position order),
+//      their count and its count of middle positions above d1;
+//   C. every partition gathers the unit's candidates and resolves tau by two
+//      10-bit radix passes (the same result in each), then the output offset
+//      of every partition and how many of its entries equal to tau it takes
+//      (ties go to the lowest positions, i.e. the first partitions);
+//   D. every partition emits its own selections at its offset; partition 0
+//      also emits the sink and recent ranges and n_idx.
+// Every wait is bounded: a broken invariant gives wrong indices, never a hang.
+// ---------------------------------------------------------------------------
+constexpr int kSpinLimit = 1 << 20;   // bounded wait (far above any real wait)
+
+// Wave 0 polls until tag[0], tag[stride], ... tag[(n-1)*stride] all equal
+// `want`; the caller synchronises the workgroup afterwards.
+__device__ __forceinline__ void wait_tags(const uint64_t* tag, int n, int stride, uint64_t want) {
+    if ((threadIdx.x >> 6) != 0) return;
+    const int lane = threadIdx.x & 63;
+    int spins = 0;
+    bool all_in;
+    do {
+        bool in = true;
+        for (int q = lane; q < n; q += kWave) in &= ld_dev64(tag + (size_t)q * stride) == want;
+        all_in = __all(in);
+        if (!all_in) __builtin_amdgcn_s_sleep(1);
+    } while (!all_in && ++spins < kSpinLimit);
+}
+
+// Publishes this workgroup's stores, then its tag.
+__device__ __forceinline__ void publish_tag(uint64_t* tag, uint64_t value) {
+    wait_stores_done();
+    __syncthreads();
+    if (threadIdx.x == 0) st_dev64(tag, value);
+}
+
+template <int NR>
+__global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a) {
+    const int p = blockIdx.x, u = blockIdx.y;
+    const int b = u / a.n_kv_heads;
+    const int c_head = u - b * a.n_kv_heads;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const Geom g = geom_of(a, b);
+    if (p >= g.parts) return;
+    if (g.simple) {
+        if (p == 0) emit_ranges(a, u, g);
+        return;
+    }
+    const float* S = a.scores + (size_t)u * a.max_ctx;
+    const size_t up0 = (size_t)u * a.parts;
+    const int P = g.parts;
+    constexpr int kTags = 4;                  // tag slots per partition
+    uint64_t* tag = a.tag + up0 * kTags;      // [P][kTags]
+    uint32_t* info = a.info + up0 * 4;        // [P][4]: candidates, above d1, histogram entries
+    const uint64_t want = a.call_tag;
+
+    __shared__ __attribute__((aligned(16))) uint32_t hist[2048];   // read as uint4
+    __shared__ __attribute__((aligned(16))) uint32_t h2[1024];
+    __shared__ __attribute__((aligned(16))) uint32_t h3[1024];
+    __shared__ int wave_tot[kSelWaves];
+    __shared__ int def_w[kSelWaves];
+    __shared__ int sh[4];
+    __shared__ uint32_t words[kSelectMaxRounds * kRound / 32];   // this partition's bitmask
+    __shared__ int offs[kMaxSelectParts + 1];
+    __shared__ uint32_t n_def[kMaxSelectParts], n_above[kMaxSelectParts], n_tie[kMaxSelectParts];
+    __shared__ uint2 cand_lds[kTailCand];
+    __shared__ uint16_t cand_p[kTailCand];
+
+    uint32_t keys[4 * NR];
+#pragma unroll
+    for (int r = 0; r < NR; ++r)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            keys[4 * r + e] = key_of(S, g, p * a.part + r * kRound + wave * 256 + e * 64 + lane);
+    for (int x = tid; x < 2048; x += kSelThreads) hist[x] = 0u;
+    for (int x = tid; x < 1024; x += kSelThreads) {
+        h2[x] = 0u;
+        h3[x] = 0u;
+    }
+    if (tid < kMaxSelectParts) {
+        n_above[tid] = 0u;
+        n_tie[tid] = 0u;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 4 * NR; ++j)
+        if (keys[j] != kNone) atomicAdd(&hist[bin12(keys[j])], 1u);
+    __syncthreads();
+
+    // ---- A. nonzero histogram bins -----------------------------------------
+    {
+        // thread t: bins 8t .. 8t+7
+        const uint4 h0 = *reinterpret_cast<const uint4*>(hist + 8 * tid);
+        const uint4 h1 = *reinterpret_cast<const uint4*>(hist + 8 * tid + 4);
+        const uint32_t hv[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
+        int nz = 0;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) nz += hv[q] != 0u;
+        int n_entries;
+        int slot = block_scan(nz, wave_tot, &n_entries);
+        uint32_t* dst = a.hist + (up0 + p) * 2048;
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+            if (hv[q] != 0u) st_dev32(dst + slot++, ((uint32_t)(8 * tid + q) << 16) | hv[q]);
+        if (tid == 0) st_dev32(info + (size_t)p * 4 + 2, (uint32_t)n_entries);
+    }
+    publish_tag(tag + (size_t)p * kTags + 0, want);
+    wait_tags(tag + 0, P, kTags, want);
+    __syncthreads();
+    for (int x = tid; x < 2048; x += kSelThreads) hist[x] = 0u;   // now the unit's histogram
+    __syncthreads();
+    {
+        // wave w adds partitions w, w+4, ...; eight partitions' entries in flight
+        for (int p0 = wave; p0 < P; p0 += 4 * 8) {
+            int n[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int pp = p0 + 4 * j;
+                n[j] = pp < P ? (int)ld_dev32(info + (size_t)pp * 4 + 2) : 0;
+            }
+            for (int e0 = 0; ; e0 += kWave) {
+                bool any = false;
+                uint32_t v[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int pp = p0 + 4 * j;
+                    const bool ok = e0 + lane < n[j];
+                    any |= e0 < n[j];
+                    v[j] = ok ? ld_dev32(a.hist + (up0 + pp) * 2048 + e0 + lane) : 0u;
+                }
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    if (v[j] != 0u) atomicAdd(&hist[(v[j] >> 16) & 2047u], v[j] & 0xffffu);
+                if (!__any(any)) break;
+            }
+        }
+    }
+    __syncthreads();
+    {
+        // thread t: bins 2047-8t down to 2040-8t
+        const uint4 h0 = *reinterpret_cast<const uint4*>(hist + 2040 - 8 * tid);
+        const uint4 h1 = *reinterpret_cast<const uint4*>(hist + 2044 - 8 * tid);
+        const uint32_t hv[8] = {h1.w, h1.z, h1.y, h1.x, h0.w, h0.z, h0.y, h0.x};   // descending
+        int sum = 0;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) sum += (int)hv[q];
+        int total;
+        int above = block_scan(sum, wave_tot, &total);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            if (above < g.take && g.take <= above + (int)hv[q]) {
+                sh[0] = 2047 - 8 * tid - q;
+                sh[1] = g.take - above;
+            }
+            above += (int)hv[q];
+        }
+    }
+    __syncthreads();
+    const uint32_t d1 = (uint32_t)sh[0] & 2047u;
+    int need = sh[1];
+
+    // ---- B. candidates, counts -----------------------------------------------
+    const uint64_t lt = (1ull << lane) - 1ull;
+    uint2* seg = a.seg + (up0 + p) * a.part;
+    int run = 0, my_def = 0;
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        const int base = p * a.part + r * kRound + wave * 256;
+        uint64_t defb[4], candb[4];
+        int n_w = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t k = keys[4 * r + e];
+            const bool mid = k != kNone;
+            const uint32_t dg = bin12(k);
+            defb[e] = __ballot(mid && dg > d1);
+            candb[e] = __ballot(mid && dg == d1);
+            n_w += __builtin_popcountll(candb[e]);
+            my_def += __builtin_popcountll(defb[e]);
+        }
+        if (lane < 8) {
+            const uint64_t m = lane < 2 ? defb[0] : lane < 4 ? defb[1] : lane < 6 ? defb[2] : defb[3];
+            words[(r * kRound + wave * 256) / 32 + lane] = (lane & 1) ? (uint32_t)(m >> 32) : (uint32_t)m;
+        }
+        int round_total;
+        int slot = run + block_scan(lane == 0 ? n_w : 0, wave_tot, &round_total);
+        slot = __builtin_amdgcn_readlane(slot, 0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            if ((candb[e] >> lane) & 1ull) {
+                const uint32_t pos = (uint32_t)(base + e * 64 + lane);
+                st_dev64(reinterpret_cast<uint64_t*>(seg + slot + __builtin_popcountll(candb[e] & lt)),
+                         (uint64_t)keys[4 * r + e] | ((uint64_t)pos << 32));
+            }
+            slot += __builtin_popcountll(candb[e]);
+        }
+        run += round_total;
+    }
+    // my_def is per wave (ballots are wave-uniform): add the waves
+    if (lane == 0) def_w[wave] = my_def;
+    __syncthreads();
+    if (tid == 0) {
+        int nd = 0;
+#pragma unroll
+        for (int w = 0; w < kSelWaves; ++w) nd += def_w[w];
+        st_dev32(info + (size_t)p * 4 + 0, (uint32_t)run);
+        st_dev32(info + (size_t)p * 4 + 1, (uint32_t)nd);
+    }
+    publish_tag(tag + (size_t)p * kTags + 1, want);
+    wait_tags(tag + 1, P, kTags, want);
+    __syncthreads();
+
+    // ---- C. every partition resolves tau ------------------------------------
+    const int my_cnt = tid < P ? (int)ld_dev32(info + (size_t)tid * 4 + 0) : 0;
+    if (tid < P) n_def[tid] = ld_dev32(info + (size_t)tid * 4 + 1);
+    int nc;
+    {
+        const int o = block_scan(my_cnt, wave_tot, &nc);
+        if (tid < P) offs[tid] = o;
+        if (tid == 0) offs[P] = nc;
+        __syncthreads();
+    }
+    const bool cached = nc <= kTailCand;
+    auto part_of = [&](int x) -> int {   // last partition whose offset is <= x
+        int lo = 0;
+#pragma unroll
+        for (int step = kMaxSelectParts / 2; step >= 1; step >>= 1)
+            lo += (lo + step < P && offs[lo + step] <= x) ? step : 0;
+        return lo;
+    };
+    auto load_cand = [&](int pp, int j) -> uint2 {
+        const uint64_t v = ld_dev64(reinterpret_cast<const uint64_t*>(a.seg + (up0 + pp) * a.part + j));
+        return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
+    };
+    auto cand = [&](int x) -> uint2 {
+        if (cached) return cand_lds[x];
+        const int pp = part_of(x);
+        return load_cand(pp, x - offs[pp]);
+    };
+    if (cached) {
+        // wave w copies partitions w, w+4, ...; eight partitions in flight
+        for (int p0 = wave; p0 < P; p0 += 4 * 8) {
+            for (int e0 = 0; ; e0 += kWave) {
+                bool any = false;
+                uint2 v[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int pp = p0 + 4 * j;
+                    const int n = pp < P ? offs[pp + 1] - offs[pp] : 0;
+                    any |= e0 < n;
+                    v[j] = e0 + lane < n ? load_cand(pp, e0 + lane) : make_uint2(0u, 0u);
+                }
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int pp = p0 + 4 * j;
+                    const int n = pp < P ? offs[pp + 1] - offs[pp] : 0;
+                    if (e0 + lane < n) {
+                        const int x = offs[pp] + e0 + lane;
+                        cand_lds[x] = v[j];
+                        cand_p[x] = (uint16_t)pp;
+                        atomicAdd(&h2[(v[j].x >> 10) & 1023u], 1u);
+                    }
+                }
+                if (!__any(any)) break;
+            }
+        }
+    } else {
+        for (int x = tid; x < nc; x += kSelThreads) atomicAdd(&h2[(cand(x).x >> 10) & 1023u], 1u);
+    }
+    __syncthreads();
+    const Digit dg2 = find_digit_wave(h2, need);
+    need -= dg2.above;
+    const uint32_t prefix = (d1 << 20) | ((uint32_t)dg2.bin << 10);
+    for (int x = tid; x < nc; x += kSelThreads) {
+        const uint32_t k = cand(x).x;
+        if ((k & 0xfffffc00u) == prefix) atomicAdd(&h3[k & 1023u], 1u);
+    }
+    __syncthreads();
+    const Digit dg3 = find_digit_wave(h3, need);
+    need -= dg3.above;                       // entries equal to tau to take
+    const uint32_t tau = prefix | (uint32_t)dg3.bin;
+    for (int x = tid; x < nc; x += kSelThreads) {
+        const uint32_t k = cand(x).x;
+        if (k >= tau) {
+            const int pp = cached ? (int)cand_p[x] : part_of(x);
+            atomicAdd(k > tau ? &n_above[pp] : &n_tie[pp], 1u);
+        }
+    }
+    __syncthreads();
+    // ties go to the first partitions; offsets follow the sink
+    const int nt = tid < P ? (int)n_tie[tid] : 0;
+    int tie_total;
+    const int tie_before = block_scan(nt, wave_tot, &tie_total);
+    const int take_t = min(max(need - tie_before, 0), nt);
+    const int out_t = tid < P ? (int)n_def[tid] + (int)n_above[tid] + take_t : 0;
+    int total_mid;
+    const int off_t = g.s_end + block_scan(out_t, wave_tot, &total_mid);
+    if (tid == p) {
+        sh[2] = off_t;
+        sh[3] = take_t;
+    }
+    __syncthreads();
+    const int offset = sh[2], take = sh[3];
+
+    // ---- D. this partition's selections at its offset ------------------------
+    int tie_base = 0;   // ties of this partition before the current round (uniform)
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        uint64_t selb[4], tieb[4];
+        int n_t = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t k = keys[4 * r + e];
+            const bool cd = k != kNone && bin12(k) == d1;
+            selb[e] = __ballot(cd && k > tau);
+            tieb[e] = __ballot(cd && k == tau);
+            n_t += __builtin_popcountll(tieb[e]);
+        }
+        int round_ties;
+        int rank = tie_base + block_scan(lane == 0 ? n_t : 0, wave_tot, &round_ties);
+        rank = __builtin_amdgcn_readlane(rank, 0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            // ties in position order: the first `take` of this partition's
+            const bool mine = (tieb[e] >> lane) & 1ull;
+            selb[e] |= __ballot(mine && rank + __builtin_popcountll(tieb[e] & lt) < take);
+            rank += __builtin_popcountll(tieb[e]);
+        }
+        if (lane < 8) {
+            const uint64_t m = lane < 2 ? selb[0] : lane < 4 ? selb[1] : lane < 6 ? selb[2] : selb[3];
+            words[(r * kRound + wave * 256) / 32 + lane] |= (lane & 1) ? (uint32_t)(m >> 32) : (uint32_t)m;
+        }
+        tie_base += round_ties;
+    }
+    __syncthreads();
+    int32_t* out = a.idx + (size_t)u * a.budget;
+    {
+        const int nw = a.part / 32;   // words of this partition (<= 256: one per thread)
+        uint32_t m = tid < nw ? words[tid] : 0u;
+        int total;
+        int pos = offset + block_scan(__builtin_popcount(m), wave_tot, &total);
+        const int wbase = p * a.part + 32 * tid;
+        while (m) {
+            const int bit = __builtin_ctz(m);
+            m &= m - 1u;
+            if (pos < a.budget) out[pos] = wbase + bit;
+            ++pos;
+        }
+    }
+    if (p == 0) {
+        // sink, recent and the count
+        for (int x = tid; x < g.s_end; x += kSelThreads)
+            if (x < a.budget) out[x] = x;
+        const int n_recent = g.T - g.r_start;
+        const int rbase = g.s_end + total_mid;
+        for (int x = tid; x < n_recent; x += kSelThreads)
+            if (rbase + x < a.budget) out[rbase + x] = g.r_start + x;
+        if (c_head == 0 && tid == 0) a.n_idx[b] = rbase + n_recent;
+    }
+}
+
+// Calls of at most kFuseMaxGroups partition workgroups run as one kernel;
+// larger ones as histogram, mark and finish kernels.
 constexpr int kFuseMaxGroups = 256;
 
 template <int NR>
 void launch_nr(const SelectArgs& a, int n_units, hipStream_t stream) {
     const dim3 grid(a.parts, n_units), block(kSelThreads);
-    hipLaunchKernelGGL(select_hist_kernel<NR>, grid, block, 0, stream, a);
     if ((long long)a.parts * n_units <= kFuseMaxGroups) {
-        hipLaunchKernelGGL(HIP_KERNEL_NAME(select_mark_kernel<NR, true>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL(select_fused_kernel<NR>, grid, block, 0, stream, a);
     } else {
-        hipLaunchKernelGGL(HIP_KERNEL_NAME(select_mark_kernel<NR, false>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL(select_hist_kernel<NR>, grid, block, 0, stream, a);
+        hipLaunchKernelGGL(select_mark_kernel<NR>, grid, block, 0, stream, a);
         hipLaunchKernelGGL(select_finish_kernel, dim3(n_units), block, 0, stream, a);
     }
 }
