@@ -124,44 +124,32 @@ struct Digit {
 
 // In a 1024-bin histogram read from the top bin down, finds the bin where the
 // running count first reaches `remaining` (1 <= remaining <= the total), the
-// count strictly above that bin and the bin's own count.  Every wave computes
-// it on its own (lane l holds bins 1008-16l .. 1023-16l), so no barrier is
-// needed after it.
-__device__ __forceinline__ Digit find_digit_wave(const uint32_t* h, int remaining) {
-    const int lane = threadIdx.x & 63;
-    const int lo = 1008 - 16 * lane;
-    uint32_t v[16];
+// count strictly above that bin and the bin's own count.  Thread t holds the
+// four bins 1020-4t .. 1023-4t (one conflict-free 16-byte LDS read); every
+// thread gets the result.  It synchronises the workgroup (sh: 3 ints of LDS).
+__device__ __forceinline__ Digit find_digit_block(const uint32_t* h, int remaining, int* sh,
+                                                  int* wave_tot) {
+    const int tid = threadIdx.x;
+    const uint4 w = *reinterpret_cast<const uint4*>(h + 1020 - 4 * tid);
+    const int c[4] = {(int)w.w, (int)w.z, (int)w.y, (int)w.x};   // descending bins
+    const int sum = c[0] + c[1] + c[2] + c[3];
+    int total;
+    int above = block_scan(sum, wave_tot, &total);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const uint4 w = *reinterpret_cast<const uint4*>(h + lo + 4 * i);
-        v[4 * i] = w.x;
-        v[4 * i + 1] = w.y;
-        v[4 * i + 2] = w.z;
-        v[4 * i + 3] = w.w;
-    }
-    int sum = 0;
-#pragma unroll
-    for (int q = 0; q < 16; ++q) sum += (int)v[q];
-    int above = wave_incl_scan(sum) - sum;
-    int bin = 0, ab = 0, cnt = 0;
-    bool found = false;
-#pragma unroll
-    for (int q = 15; q >= 0; --q) {
-        const int c = (int)v[q];
-        if (!found && above < remaining && remaining <= above + c) {
-            found = true;
-            bin = lo + q;
-            ab = above;
-            cnt = c;
+    for (int q = 0; q < 4; ++q) {
+        if (above < remaining && remaining <= above + c[q]) {
+            sh[0] = 1023 - 4 * tid - q;
+            sh[1] = above;
+            sh[2] = c[q];
         }
-        above += c;
+        above += c[q];
     }
-    const uint64_t who = __ballot(found);
-    const int src = who ? __builtin_ctzll(who) : 0;
+    __syncthreads();
     Digit d;
-    d.bin = __builtin_amdgcn_readlane(bin, src);
-    d.above = __builtin_amdgcn_readlane(ab, src);
-    d.count = __builtin_amdgcn_readlane(cnt, src);
+    d.bin = sh[0] & 1023;
+    d.above = sh[1];
+    d.count = sh[2];
+    __syncthreads();
     return d;
 }
 
@@ -190,6 +178,7 @@ __device__ void finish_unit(const SelectArgs& a, int u, const Geom& g, uint32_t 
     auto ldw = [](const uint32_t* p) -> uint32_t { return *p; };
     auto ldc = [](const uint2* p) -> uint2 { return *p; };
 
+    __shared__ int sh_d[3];
     __shared__ int wave_tot[kSelWaves];
     __shared__ __attribute__((aligned(16))) uint32_t h2[1024];   // read as uint4
     __shared__ __attribute__((aligned(16))) uint32_t h3[1024];
@@ -263,7 +252,7 @@ __device__ void finish_unit(const SelectArgs& a, int u, const Geom& g, uint32_t 
             }
         }
         __syncthreads();
-        const Digit dg2 = find_digit_wave(h2, need);
+        const Digit dg2 = find_digit_block(h2, need, sh_d, wave_tot);
         need -= dg2.above;
         const uint32_t prefix = (d1 << 20) | ((uint32_t)dg2.bin << 10);
         // Pass 3 (bits 9..0) over the candidates with that 22-bit prefix.
@@ -272,7 +261,7 @@ __device__ void finish_unit(const SelectArgs& a, int u, const Geom& g, uint32_t 
             if ((k & 0xfffffc00u) == prefix) atomicAdd(&h3[k & 1023u], 1u);
         }
         __syncthreads();
-        const Digit dg3 = find_digit_wave(h3, need);
+        const Digit dg3 = find_digit_block(h3, need, sh_d, wave_tot);
         need -= dg3.above;
         tau = prefix | (uint32_t)dg3.bin;
         all_ties = need == dg3.count;
@@ -578,6 +567,7 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
     __shared__ int wave_tot[kSelWaves];
     __shared__ int def_w[kSelWaves];
     __shared__ int sh[4];
+    __shared__ int sh_d[3];
     __shared__ uint32_t words[kSelectMaxRounds * kRound / 32];   // this partition's bitmask
     __shared__ int offs[kMaxSelectParts + 1];
     __shared__ uint32_t n_def[kMaxSelectParts], n_above[kMaxSelectParts], n_tie[kMaxSelectParts];
@@ -756,37 +746,43 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
         return load_cand(pp, x - offs[pp]);
     };
     if (cached) {
-        // wave w copies partitions w, w+4, ...; eight partitions in flight
+        // wave w copies partitions w, w+4, ...: the first 128 entries of eight
+        // partitions in flight at once, then any remainder
         for (int p0 = wave; p0 < P; p0 += 4 * 8) {
-            for (int e0 = 0; ; e0 += kWave) {
-                bool any = false;
-                uint2 v[8];
+            int n[8], o[8];
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const int pp = p0 + 4 * j;
-                    const int n = pp < P ? offs[pp + 1] - offs[pp] : 0;
-                    any |= e0 < n;
-                    v[j] = e0 + lane < n ? load_cand(pp, e0 + lane) : make_uint2(0u, 0u);
+            for (int j = 0; j < 8; ++j) {
+                const int pp = p0 + 4 * j;
+                o[j] = pp < P ? offs[pp] : 0;
+                n[j] = pp < P ? offs[pp + 1] - o[j] : 0;
+            }
+            for (int e0 = 0; ; e0 += 2 * kWave) {
+                bool more = false;
+                uint2 v[16];
+#pragma unroll
+                for (int j = 0; j < 16; ++j) {
+                    const int pp = p0 + 4 * (j & 7), e = e0 + (j >> 3) * kWave + lane;
+                    v[j] = e < n[j & 7] ? load_cand(pp, e) : make_uint2(0u, 0u);
                 }
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const int pp = p0 + 4 * j;
-                    const int n = pp < P ? offs[pp + 1] - offs[pp] : 0;
-                    if (e0 + lane < n) {
-                        const int x = offs[pp] + e0 + lane;
+                for (int j = 0; j < 16; ++j) {
+                    const int e = e0 + (j >> 3) * kWave + lane;
+                    if (e < n[j & 7]) {
+                        const int x = o[j & 7] + e;
                         cand_lds[x] = v[j];
-                        cand_p[x] = (uint16_t)pp;
+                        cand_p[x] = (uint16_t)(p0 + 4 * (j & 7));
                         atomicAdd(&h2[(v[j].x >> 10) & 1023u], 1u);
                     }
+                    more |= e0 + 2 * kWave < n[j & 7];
                 }
-                if (!__any(any)) break;
+                if (!more) break;   // wave-uniform: n[] and e0 are
             }
         }
     } else {
         for (int x = tid; x < nc; x += kSelThreads) atomicAdd(&h2[(cand(x).x >> 10) & 1023u], 1u);
     }
     __syncthreads();
-    const Digit dg2 = find_digit_wave(h2, need);
+    const Digit dg2 = find_digit_block(h2, need, sh_d, wave_tot);
     need -= dg2.above;
     const uint32_t prefix = (d1 << 20) | ((uint32_t)dg2.bin << 10);
     for (int x = tid; x < nc; x += kSelThreads) {
@@ -794,7 +790,7 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
         if ((k & 0xfffffc00u) == prefix) atomicAdd(&h3[k & 1023u], 1u);
     }
     __syncthreads();
-    const Digit dg3 = find_digit_wave(h3, need);
+    const Digit dg3 = find_digit_block(h3, need, sh_d, wave_tot);
     need -= dg3.above;                       // entries equal to tau to take
     const uint32_t tau = prefix | (uint32_t)dg3.bin;
     for (int x = tid; x < nc; x += kSelThreads) {
