@@ -53,6 +53,15 @@ constexpr int static_lds_bytes() {
            + 64;
 }
 
+// The largest chunk whose stash (probabilities, padding, one running maximum
+// per tile and row) fits in LDS beside the static arrays.
+template <int NRT>
+constexpr int max_fused_chunk() {
+    constexpr int kLds = 160 * 1024;
+    constexpr int floats_per_row = (kLds - static_lds_bytes<NRT>() - 1024) / 4 / (16 * NRT);
+    return (floats_per_row - kStashPad) * kTile / (kTile + 1) / 128 * 128;
+}
+
 __device__ __forceinline__ float safe_max(float m) { return m == -INFINITY ? 0.f : m; }
 
 
@@ -182,9 +191,8 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         for (int w = 0; w < kWaves; ++w) Mw = fmaxf(Mw, wml[w][tid].x);
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) Lw += wml[w][tid].y * fast_exp2(wml[w][tid].x - safe_max(Mw));
-        float* pm = reinterpret_cast<float*>(a.part_ml + (size_t)slot * kRowCap + tid);
-        st_dev(pm, Mw);
-        st_dev(pm + 1, Lw);
+        st_dev64(reinterpret_cast<uint64_t*>(a.part_ml + (size_t)slot * kRowCap + tid),
+                 __builtin_bit_cast(uint64_t, make_float2(Mw, Lw)));
     }
 
     // ---- wait for every chunk of this (sequence, KV head) -------------------
@@ -213,8 +221,10 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
 #pragma unroll
                 for (int uu = 0; uu < 8; ++uu) {
                     const int s2 = s0 + uu * kWaves;
-                    v[uu] = s2 < nchunk ? ld_dev2(a.part_ml + (size_t)(slot0 + s2) * kRowCap + rr)
-                                        : make_float2(-INFINITY, 0.f);
+                    v[uu] = s2 < nchunk
+                                ? __builtin_bit_cast(float2, ld_dev64(reinterpret_cast<const uint64_t*>(
+                                                                 a.part_ml + (size_t)(slot0 + s2) * kRowCap + rr)))
+                                : make_float2(-INFINITY, 0.f);
                 }
 #pragma unroll
                 for (int uu = 0; uu < 8; ++uu) ml_merge(Mx, Lx, v[uu].x, v[uu].y);
@@ -231,12 +241,26 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         row_lse[tid] = Lx > 0.f ? Mx + fast_log2(Lx) : INFINITY;
     }
     __syncthreads();
-    // tile factors: a stashed probability times its tile's factor is exact
+    // tile factors: a stashed probability times its tile's factor is exact.
+    // The table is rewritten transposed, [row][tile], so that the lanes of a
+    // wave (eight tiles, one row) read distinct banks below.
     const int nk = key_end - key_begin;
     const int ntl = (nk + kTile - 1) / kTile;
-    for (int x = tid; x < ntl * NRT * 16; x += kThreads) {
-        const int row = x % (NRT * 16);
-        mtile[x] = row < R ? fast_exp2(mtile[x] - row_lse[row]) : 0.f;
+    {
+        constexpr int kPer = (max_fused_chunk<NRT>() / kTile * NRT * 16 + kThreads - 1) / kThreads;
+        float f[kPer];
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {
+            const int x = tid + j * kThreads;
+            const int row = x % (NRT * 16);
+            f[j] = (x < ntl * NRT * 16 && row < R) ? fast_exp2(mtile[x] - row_lse[row]) : 0.f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {
+            const int x = tid + j * kThreads;
+            if (x < ntl * NRT * 16) mtile[(x % (NRT * 16)) * ntl + x / (NRT * 16)] = f[j];
+        }
     }
     __syncthreads();
 
@@ -248,20 +272,24 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         // four consecutive keys per thread (one 16-byte LDS read per row, four
         // rows in flight); the stash row stride and the chunk are multiples of
         // 4 floats, and 4 consecutive keys share one tile
+        const f32x4* stash4 = reinterpret_cast<const f32x4*>(stash);
+        const int stride4 = stride / 4;
         for (int k4 = 4 * tid; k4 < nk; k4 += 4 * kThreads) {
-            const float* ct = mtile + (k4 / kTile) * (NRT * 16);
+            const float* ct = mtile + k4 / kTile;   // ct[row * ntl]
             f32x4 sc = {0.f, 0.f, 0.f, 0.f};
             int row = r0;
             for (; row + 4 <= R; row += 4) {
                 f32x4 pr[4];
+                float cr[4];
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    pr[j] = *reinterpret_cast<const f32x4*>(stash + (row + j) * stride + k4);
+                for (int j = 0; j < 4; ++j) {
+                    pr[j] = stash4[(row + j) * stride4 + k4 / 4];
+                    cr[j] = ct[(row + j) * ntl];
+                }
 #pragma unroll
-                for (int j = 0; j < 4; ++j) sc += pr[j] * ct[row + j];
+                for (int j = 0; j < 4; ++j) sc += pr[j] * cr[j];
             }
-            for (; row < R; ++row)
-                sc += *reinterpret_cast<const f32x4*>(stash + row * stride + k4) * ct[row];
+            for (; row < R; ++row) sc += stash4[row * stride4 + k4 / 4] * ct[row * ntl];
 #pragma unroll
             for (int i = 0; i < 4; ++i)
                 if (k4 + i < nk) srow[key_begin + k4 + i] = sc[i];
@@ -337,17 +365,12 @@ hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, int n_rows_total,
 }  // namespace
 
 int fused_max_chunk(int row_tiles) {
-    constexpr int kLds = 160 * 1024;
-    int stat = 0;
     switch (row_tiles) {
-        case 1: stat = static_lds_bytes<1>(); break;
-        case 2: stat = static_lds_bytes<2>(); break;
-        case 3: stat = static_lds_bytes<3>(); break;
-        default: stat = static_lds_bytes<4>(); break;
+        case 1: return max_fused_chunk<1>();
+        case 2: return max_fused_chunk<2>();
+        case 3: return max_fused_chunk<3>();
+        default: return max_fused_chunk<4>();
     }
-    // per stash row: chunk probabilities, padding, chunk / kTile tile maxima
-    const int floats_per_row = (kLds - stat - 1024) / (int)sizeof(float) / (16 * row_tiles);
-    return (floats_per_row - kStashPad) * kTile / (kTile + 1) / 128 * 128;
 }
 
 hipError_t launch_verify_fused(const FusedArgs& a, int n_slots, int n_rows_total, int row_tiles,
