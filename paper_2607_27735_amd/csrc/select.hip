@@ -618,28 +618,36 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
     for (int x = tid; x < 2048; x += kSelThreads) hist[x] = 0u;   // now the unit's histogram
     __syncthreads();
     {
-        // wave w adds partitions w, w+4, ...; eight partitions' entries in flight
+        // wave w adds partitions w, w+4, ...: for eight partitions at once the
+        // entry counts and, speculatively, the first 64 entries are loaded
+        // together (entries past a count are stale and dropped), then any rest
         for (int p0 = wave; p0 < P; p0 += 4 * 8) {
             int n[8];
+            uint32_t v[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const int pp = p0 + 4 * j;
                 n[j] = pp < P ? (int)ld_dev32(info + (size_t)pp * 4 + 2) : 0;
+                v[j] = pp < P ? ld_dev32(a.hist + (up0 + pp) * 2048 + lane) : 0u;
             }
-            for (int e0 = 0; ; e0 += kWave) {
-                bool any = false;
-                uint32_t v[8];
+            bool more = false;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                if (lane < n[j]) atomicAdd(&hist[(v[j] >> 16) & 2047u], v[j] & 0xffffu);
+                more |= n[j] > kWave;
+            }
+            for (int e0 = kWave; more; e0 += kWave) {   // wave-uniform
+                more = false;
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
                     const int pp = p0 + 4 * j;
-                    const bool ok = e0 + lane < n[j];
-                    any |= e0 < n[j];
-                    v[j] = ok ? ld_dev32(a.hist + (up0 + pp) * 2048 + e0 + lane) : 0u;
+                    v[j] = e0 + lane < n[j] ? ld_dev32(a.hist + (up0 + pp) * 2048 + e0 + lane) : 0u;
                 }
 #pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    if (v[j] != 0u) atomicAdd(&hist[(v[j] >> 16) & 2047u], v[j] & 0xffffu);
-                if (!__any(any)) break;
+                for (int j = 0; j < 8; ++j) {
+                    if (e0 + lane < n[j]) atomicAdd(&hist[(v[j] >> 16) & 2047u], v[j] & 0xffffu);
+                    more |= n[j] > e0 + kWave;
+                }
             }
         }
     }
