@@ -3,22 +3,30 @@
 // Scores are non-negative fp32, so their bit patterns order like their
 // values.  Each (sequence, KV head) unit is cut into partitions of `part`
 // positions, one 256-thread workgroup per partition, so that a handful of
-// units still spreads over the whole chip.  Three kernels; the kernel
-// boundaries are the only synchronisation between workgroups.
+// units still spreads over the whole chip.  Two schedules:
 //
+// One kernel (calls of at most kFuseMaxGroups partitions, select_fused_kernel):
+// the partitions of a unit are resident together and exchange nonzero
+// histogram bins, then bin-d1 candidates through the workspace; every
+// partition then resolves the exact threshold and emits its own selections
+// (see the comment above that kernel).
+//
+// Three kernels (larger calls), the kernel boundaries being the only
+// synchronisation between workgroups:
 // hist:   each partition histograms the top 12 bits of its middle scores
 //         (2048 fine bins, plus 64 coarse bins of 32) into its own slot of
 //         the workspace: no atomics on global memory, nothing to clear.
 // mark:   every partition sums the coarse and then the fine slot histograms
 //         of its unit and finds the bin d1 holding the K_mid-th largest middle
-//         score.  It writes its words of the unit's position bitmask (sink,
-//         recent, middle positions above bin d1) and appends its bin-d1
-//         positions, in position order, to its own candidate segment.
+//         score.  It writes its words of the unit's bitmask of middle
+//         positions above bin d1 and appends its bin-d1 positions, in
+//         position order, to its own candidate segment.
 // finish: one workgroup per unit runs two 10-bit radix passes over the
 //         candidates for the exact threshold tau and `need`, the number of
 //         entries equal to tau that still fit; it marks the candidates above
-//         tau and the first `need` ties (lowest positions) and emits the set
-//         in ascending order by a block scan of per-thread popcounts.
+//         tau and the first `need` ties (lowest positions) and emits sink,
+//         middle selections (by a block scan of per-thread popcounts) and
+//         recent in ascending order.
 #include "device_common.h"
 #include "launch.h"
 
@@ -175,8 +183,6 @@ __device__ void finish_unit(const SelectArgs& a, int u, const Geom& g, uint32_t 
     const int tid = threadIdx.x;
     const size_t up0 = (size_t)u * a.parts;
     const uint32_t* mask = a.mask + (size_t)u * (a.parts * (a.part / 32));
-    auto ldw = [](const uint32_t* p) -> uint32_t { return *p; };
-    auto ldc = [](const uint2* p) -> uint2 { return *p; };
 
     __shared__ int sh_d[3];
     __shared__ int wave_tot[kSelWaves];
@@ -194,12 +200,12 @@ __device__ void finish_unit(const SelectArgs& a, int u, const Geom& g, uint32_t 
 #pragma unroll
     for (int j = 0; j < kWordsPerThread; ++j) {
         const int x = tid + j * kSelThreads;
-        mw[j] = x < n_words ? ldw(mask + x) : 0u;
+        mw[j] = x < n_words ? mask[x] : 0u;
     }
     const int per_p = (g.parts + kSelThreads - 1) / kSelThreads;
     const int q0 = min(g.parts, tid * per_p), q1 = min(g.parts, q0 + per_p);
     int my_cnt = 0;
-    for (int q = q0; q < q1; ++q) my_cnt += (int)ldw(a.cnt + up0 + q);
+    for (int q = q0; q < q1; ++q) my_cnt += (int)a.cnt[up0 + q];
     for (int x = tid; x < 1024; x += kSelThreads) {
         h2[x] = 0u;
         h3[x] = 0u;
@@ -214,7 +220,7 @@ __device__ void finish_unit(const SelectArgs& a, int u, const Geom& g, uint32_t 
         int o = block_scan(my_cnt, wave_tot, &nc_all);
         for (int q = q0; q < q1; ++q) {
             offs[q] = o;
-            o += (int)ldw(a.cnt + up0 + q);
+            o += (int)a.cnt[up0 + q];
         }
         if (tid == 0) offs[g.parts] = nc_all;
         __syncthreads();
@@ -226,7 +232,7 @@ __device__ void finish_unit(const SelectArgs& a, int u, const Geom& g, uint32_t 
 #pragma unroll
         for (int step = kMaxSelectParts / 2; step >= 1; step >>= 1)
             lo += (lo + step < g.parts && offs[lo + step] <= x) ? step : 0;
-        return ldc(a.seg + (up0 + lo) * a.part + (x - offs[lo]));
+        return a.seg[(up0 + lo) * a.part + (x - offs[lo])];
     };
     auto cand = [&](int x) -> uint2 { return cached ? cand_lds[x] : cand_global(x); };
 
@@ -288,7 +294,7 @@ __device__ void finish_unit(const SelectArgs& a, int u, const Geom& g, uint32_t 
         const int nw = min(kTailWords, n_words - cw);
         if (cw > 0) {
             __syncthreads();
-            for (int x = tid; x < nw; x += kSelThreads) lmask[x] = ldw(mask + cw + x);
+            for (int x = tid; x < nw; x += kSelThreads) lmask[x] = mask[cw + x];
             __syncthreads();
         }
         if (all_ties) {
