@@ -20,7 +20,7 @@ namespace {
 constexpr size_t kAlign = 256;
 constexpr int kVerifyRowCap = 64;
 constexpr int kDraftRowCap = 16;
-constexpr int kDraftChunk = 256;   // index entries per draft workgroup (4 waves)
+constexpr int kDraftChunk = 128;   // index entries per draft workgroup (4 waves of 32)
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 

@@ -1,8 +1,8 @@
 // draft.hip -- draft-step attention over the gathered sparse view (Eq. 5).
 //
 // The gather is fused: K/V rows named by the index set are read in place from
-// the dense cache, never copied.  A workgroup takes 256 consecutive entries of
-// one (sequence, KV head)'s index list, one wave per 64; each wave keeps an
+// the dense cache, never copied.  A workgroup takes 128 consecutive entries of
+// one (sequence, KV head)'s index list, one wave per 32; each wave keeps an
 // online softmax per query head of the group (up to 16 heads = one MFMA row
 // tile).  The four waves are merged through LDS into one partial output with
 // its (max, sum) per head, which the workgroup publishes with device-coherent
@@ -25,7 +25,7 @@ constexpr int kTile = 32;
 constexpr int kRowCap = 16;
 constexpr int kDraftWaves = 4;
 constexpr int kDraftThreads = kDraftWaves * kWave;
-constexpr int kWaveChunk = 2 * kTile;          // index entries per wave
+constexpr int kWaveChunk = kTile;              // index entries per wave
 constexpr int kParkStride = kHeadDim + 4;      // floats per parked head row
 
 __device__ __forceinline__ int a_row_key(int m) { return (m >> 2) + 4 * (m & 3); }
@@ -161,14 +161,12 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
         const uint16_t* vbase = a.v + cache_off;
         const int32_t* ib = a.idx + (size_t)it.unit * a.budget;
         const int last = it.n - 1;
-        // Lane l loads the cache row of entry l once; every K/V row of both
-        // tiles is then requested at once.
+        // Lane l loads the cache row of entry l once; every K/V row of the
+        // tile is then requested at once.
         const int my_row = min(max(ib[min(wbeg + lane, last)], 0), a.max_ctx - 1);
-        Gathered ta, tb;
+        Gathered ta;
         gather_tile(my_row, 0, kbase, vbase, m16, G, ta);
-        gather_tile(my_row, kTile, kbase, vbase, m16, G, tb);
         draft_tile(a, qop, ta, wbeg, wend, G, M, L, oacc);
-        if (wbeg + kTile < wend) draft_tile(a, qop, tb, wbeg + kTile, wend, G, M, L, oacc);
         L += shfl_xor_f(L, 16);
         L += shfl_xor_f(L, 32);
     }

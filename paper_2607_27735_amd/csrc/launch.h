@@ -98,7 +98,7 @@ int fused_max_chunk(int row_tiles);
 // <= kSelectTargetParts partitions.
 int select_part_len(int max_t);
 hipError_t launch_select(const SelectArgs& a, int n_units, hipStream_t stream);
-// One workgroup per `chunk` (256) index entries; no combine kernel.
+// One workgroup per `chunk` (128) index entries; no combine kernel.
 hipError_t launch_draft(const DraftArgs& a, int n_items, hipStream_t stream);
 
 }  // namespace ssl
