@@ -47,7 +47,7 @@ REPO = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(REPO, "profiles", "verify_traffic_llama8b_T32K.txt")
 OUR_KERNELS = ("verify_fused_kernel", "verify_stats_kernel", "verify_main_kernel",
                "verify_combine_kernel", "select_hist_kernel", "select_mark_kernel",
-               "select_finish_kernel", "select_fused_kernel", "draft_kernel", "draft_combine_kernel")
+               "select_finish_kernel", "select_fused_kernel", "draft_kernel")
 VERIFY_KERNELS = ("verify_fused_kernel", "verify_stats_kernel", "verify_main_kernel",
                   "verify_combine_kernel")
 
@@ -241,7 +241,7 @@ def main() -> int:
     vshape = B.Shape(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.max_ctx, w.max_q)
     schedule, vchunk, vitems = B.verify_plan(vshape, params, w.ctx_len, w.q_len)
     sched_name = "one-sweep" if schedule == B.VERIFY_ONE_SWEEP else "two-sweep"
-    verify_kernels = ("verify_fused_kernel + verify_combine_kernel" if schedule == B.VERIFY_ONE_SWEEP
+    verify_kernels = ("verify_fused_kernel" if schedule == B.VERIFY_ONE_SWEEP
                       else "verify_stats_kernel + verify_main_kernel + verify_combine_kernel")
 
     stream = torch.cuda.current_stream()

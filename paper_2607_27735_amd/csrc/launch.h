@@ -78,17 +78,17 @@ struct DraftArgs {
 // unit must be resident at once.
 struct FusedArgs {
     VerifyArgs v;           // part_ml / part_o indexed by slot
-    uint64_t* tag;          // [n_slots] publication tags (no initialisation needed)
+    uint64_t* tag;          // [n_slots] statistics tags (no initialisation needed)
+    uint64_t* tag_out;      // [n_slots] partial-output tags
     uint64_t call_tag;      // this call's tag: unique within the process
 };
 
 // Launchers return hipSuccess or the error of the launch.
 hipError_t launch_verify(const VerifyArgs& a, int n_items, int n_rows_total, int row_tiles,
                          hipStream_t stream);
-// Launches the single-sweep kernel over n_slots workgroups, then the combine
-// kernel over n_rows_total rows.  Returns the first launch error.
-hipError_t launch_verify_fused(const FusedArgs& a, int n_slots, int n_rows_total, int row_tiles,
-                               hipStream_t stream);
+// Launches the single-sweep kernel over n_slots workgroups (it adds the
+// chunks of each row itself).  Returns the launch error.
+hipError_t launch_verify_fused(const FusedArgs& a, int n_slots, int row_tiles, hipStream_t stream);
 // The combine kernel alone: out[row] = sum of the row's normalised partials.
 hipError_t launch_verify_combine(const VerifyArgs& a, int n_rows_total, hipStream_t stream);
 // Largest key chunk the single-sweep kernel can hold in LDS for row_tiles.

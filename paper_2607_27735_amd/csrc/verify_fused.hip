@@ -12,22 +12,24 @@
 //      for its chunk, and waits until every chunk of its head shows the tag;
 //   3. from the merged (max, sum) of all chunks it forms one factor per tile
 //      and row, so that a stashed probability times its factor is the exact
-//      probability, and writes the scores of its keys; it also writes its
-//      partial output already scaled to the exact normalizer, so that the
-//      two-sweep combine kernel only has to add the partials of each row.
+//      probability, and writes the scores of its keys; it then publishes its
+//      partial output already scaled to the exact normalizer, and a second
+//      tag;
+//   4. once every chunk's partial is out, the workgroup of chunk s adds the
+//      partials of rows s, s + nchunk, ... and writes them.
 //
 // Publication avoids agent-scope fences, which write back a whole L2 per wave
-// on this multi-XCD part: the few published words are written and read with
-// device-coherent (agent-scope relaxed atomic) stores and loads, and every
-// wave waits for its stores to complete before the tag is written.  The tags
-// need no initialisation: the host draws a fresh 64-bit tag for every call
-// from a process-wide sequence with a clock-seeded start, so a stale or
-// uninitialised word matches only by a 2^-64 accident.
+// on this multi-XCD part: the published statistics and partials are written
+// and read with device-coherent (agent-scope relaxed atomic) stores and
+// loads, and every wave waits for its stores to complete before a tag is
+// written.  The tags need no initialisation: the host draws a fresh 64-bit tag
+// for every call from a process-wide sequence with a clock-seeded start, so a
+// stale or uninitialised word matches only by a 2^-64 accident.
 //
 // The wait ends: workgroups are dispatched in index order and the chunks of
 // one head are consecutive, so when the lowest unfinished head waits, every
 // workgroup ahead of its chunks has finished and its chunks (at most a few
-// per XCD) are resident.  The wait is also bounded, so a broken invariant
+// per XCD) are resident.  The waits are also bounded, so a broken invariant
 // cannot hang the GPU (the results would then be wrong, never a fault).
 #include <algorithm>
 #include <atomic>
@@ -64,6 +66,19 @@ constexpr int max_fused_chunk() {
 
 __device__ __forceinline__ float safe_max(float m) { return m == -INFINITY ? 0.f : m; }
 
+// Wave 0 polls until tag[0 .. n) all equal `want`; the caller synchronises
+// the workgroup afterwards.
+__device__ __forceinline__ void wait_unit(const uint64_t* tag, int n, uint64_t want) {
+    const int lane = threadIdx.x & 63;
+    int spins = 0;
+    bool all_in;
+    do {
+        bool in = true;
+        for (int s2 = lane; s2 < n; s2 += kWave) in &= ld_dev64(tag + s2) == want;
+        all_in = __all(in);
+        if (!all_in) __builtin_amdgcn_s_sleep(1);
+    } while (!all_in && ++spins < kSpinLimit);
+}
 
 // One 32-key tile: online softmax and P.V; the tile's probabilities relative
 // to the running row maxima go to the LDS stash, those maxima to mtile.
@@ -199,16 +214,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     wait_stores_done();
     __syncthreads();
     if (tid == 0) st_dev64(fa.tag + slot, fa.call_tag);
-    if (wave == 0) {
-        int spins = 0;
-        bool all_in;
-        do {
-            bool in = true;
-            for (int s2 = lane; s2 < nchunk; s2 += kWave) in &= ld_dev64(fa.tag + slot0 + s2) == fa.call_tag;
-            all_in = __all(in);
-            if (!all_in) __builtin_amdgcn_s_sleep(1);
-        } while (!all_in && ++spins < kSpinLimit);
-    }
+    if (wave == 0) wait_unit(fa.tag + slot0, nchunk, fa.call_tag);
     __syncthreads();
 
     // ---- 3a. exact row statistics over every chunk of the head -------------
@@ -300,7 +306,8 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     // The stash is free now: per row tile, every wave parks its partial P.V,
     // scaled from its own row maxima to the exact normalizers, in a slice of
     // it, and all threads add the four slices (in wave order) and store the
-    // sum; the combine kernel then adds the chunks of each row.
+    // sum device-coherently: the workgroups that add a row's chunks below may
+    // run on other XCDs.
     {
         constexpr int kSliceStride = kParkStride;
         float* park = stash;                          // [kWaves][16][kParkStride]
@@ -327,15 +334,67 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
 #pragma unroll
                 for (int w = 1; w < kWaves; ++w)
                     o += *reinterpret_cast<const f32x4*>(park + (w * 16 + rr) * kSliceStride + 4 * c4);
-                *reinterpret_cast<f32x4*>(po + (size_t)(rt * 16 + rr) * kHeadDim + 4 * c4) = o;
+                uint64_t* d64 = reinterpret_cast<uint64_t*>(po + (size_t)(rt * 16 + rr) * kHeadDim + 4 * c4);
+                st_dev64(d64, __builtin_bit_cast(uint64_t, make_float2(o[0], o[1])));
+                st_dev64(d64 + 1, __builtin_bit_cast(uint64_t, make_float2(o[2], o[3])));
             }
+        }
+    }
+
+    // ---- 4. rows it.s, it.s + nchunk, ... summed over the unit's chunks ------
+    // Chunks are added in index order, eight interleaved groups of them and
+    // then the groups in order (the combine kernel's order).
+    wait_stores_done();
+    __syncthreads();
+    if (tid == 0) st_dev64(fa.tag_out + slot, fa.call_tag);
+    if (wave == 0) wait_unit(fa.tag_out + slot0, nchunk, fa.call_tag);
+    __syncthreads();
+    {
+        const int d4 = tid & 31, sg = tid >> 5;
+        f32x4* red = reinterpret_cast<f32x4*>(stash);   // [8][32]
+        for (int row = it.s; row < R; row += nchunk) {
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+            for (int s0 = sg; s0 < nchunk; s0 += 4 * 8) {
+                f32x4 v[4];
+#pragma unroll
+                for (int uu = 0; uu < 4; ++uu) {
+                    const int s2 = s0 + 8 * uu;
+                    const uint64_t* s64 = reinterpret_cast<const uint64_t*>(
+                        a.part_o + ((size_t)(slot0 + s2) * kRowCap + row) * kHeadDim + 4 * d4);
+                    if (s2 < nchunk) {
+                        const float2 lo = __builtin_bit_cast(float2, ld_dev64(s64));
+                        const float2 hi = __builtin_bit_cast(float2, ld_dev64(s64 + 1));
+                        v[uu] = f32x4{lo.x, lo.y, hi.x, hi.y};
+                    } else {
+                        v[uu] = f32x4{0.f, 0.f, 0.f, 0.f};
+                    }
+                }
+#pragma unroll
+                for (int uu = 0; uu < 4; ++uu) acc += v[uu];
+            }
+            red[sg * 32 + d4] = acc;
+            __syncthreads();
+            if (sg == 0) {
+                f32x4 o = red[d4];
+#pragma unroll
+                for (int gq = 1; gq < 8; ++gq) o += red[gq * 32 + d4];
+                const int j = row / a.group;
+                const int h = c * a.group + (row - j * a.group);
+                const size_t base = (((size_t)b * a.max_q + j) * a.n_q_heads + h) * kHeadDim + 4 * d4;
+                if (a.out_fp32) {
+                    *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out) + base) = o;
+                } else {
+                    const uint2 pk = make_uint2(pack_bf16(o[0], o[1]), pack_bf16(o[2], o[3]));
+                    *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + base) = pk;
+                }
+            }
+            __syncthreads();
         }
     }
 }
 
 template <int NRT>
-hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, int n_rows_total,
-                            hipStream_t stream) {
+hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, hipStream_t stream) {
     // the logit stash, later reused to park the waves' partial outputs
     const size_t dyn = std::max((size_t)NRT * 16 * (a.v.chunk + kStashPad + a.v.chunk / kTile),
                                 (size_t)kParkFloats) * sizeof(float);
@@ -357,9 +416,7 @@ hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, int n_rows_total,
         if (dev >= 0 && dev < kMaxDevices) raised[dev].store(true, std::memory_order_relaxed);
     }
     hipLaunchKernelGGL(verify_fused_kernel<NRT>, dim3(n_slots), dim3(kThreads), dyn, stream, a);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    return launch_verify_combine(a.v, n_rows_total, stream);
+    return hipGetLastError();
 }
 
 }  // namespace
@@ -373,13 +430,12 @@ int fused_max_chunk(int row_tiles) {
     }
 }
 
-hipError_t launch_verify_fused(const FusedArgs& a, int n_slots, int n_rows_total, int row_tiles,
-                               hipStream_t stream) {
+hipError_t launch_verify_fused(const FusedArgs& a, int n_slots, int row_tiles, hipStream_t stream) {
     switch (row_tiles) {
-        case 1: return launch_fused_nrt<1>(a, n_slots, n_rows_total, stream);
-        case 2: return launch_fused_nrt<2>(a, n_slots, n_rows_total, stream);
-        case 3: return launch_fused_nrt<3>(a, n_slots, n_rows_total, stream);
-        default: return launch_fused_nrt<4>(a, n_slots, n_rows_total, stream);
+        case 1: return launch_fused_nrt<1>(a, n_slots, stream);
+        case 2: return launch_fused_nrt<2>(a, n_slots, stream);
+        case 3: return launch_fused_nrt<3>(a, n_slots, stream);
+        default: return launch_fused_nrt<4>(a, n_slots, stream);
     }
 }
 

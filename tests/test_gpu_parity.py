@@ -55,6 +55,13 @@ SMALL = {
                                 ctx_len=[900], q_len=[6], window=2, budget=100),
     "chunk-ragged": lambda: generate(107, name="chunk-ragged", batch=1, n_q_heads=8,
                                      n_kv_heads=2, ctx_len=[4097], q_len=[3], budget=300),
+    # eight KV heads, several rows per finishing workgroup, one-chunk heads
+    "kv8-b3": lambda: _poison_padding(generate(
+        108, name="kv8-b3", batch=3, n_q_heads=32, n_kv_heads=8, ctx_len=[1000, 333, 2049],
+        q_len=[3, 1, 7], max_ctx=2100, max_q=8, budget=256)),
+    "kv8-g16": lambda: _poison_padding(generate(
+        109, name="kv8-g16", batch=3, n_q_heads=128, n_kv_heads=8, ctx_len=[1, 130, 700],
+        q_len=[1, 4, 4], max_ctx=720, max_q=4, budget=64)),
 }
 
 
