@@ -102,7 +102,7 @@ typedef struct {
  *  ONE_SWEEP  a single K+V pass whose chunks of one (sequence, KV head)
  *             exchange row statistics while resident together;
  *             SSL_ERR_UNSUPPORTED when it does not fit: a (sequence, KV head)
- *             may span at most 128 chunks of at most 2304 / 1152 / 768 / 512
+ *             may span at most 128 chunks of at most 2048 / 1024 / 640 / 512
  *             keys for up to 16 / 32 / 48 / 64 verify rows per KV head. */
 enum { SSL_VERIFY_AUTO = 0, SSL_VERIFY_TWO_SWEEP = 1, SSL_VERIFY_ONE_SWEEP = 2 };
 

@@ -152,7 +152,7 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
     plan->ml_off = 0;
     plan->o_off = align_up(slots_max * kVerifyRowCap * sizeof(float) * 2);
     plan->tag_off = plan->o_off + align_up(slots_max * kVerifyRowCap * 128 * sizeof(float));
-    plan->bytes = plan->tag_off + 2 * align_up((size_t)plan->fused_slots * sizeof(uint64_t));
+    plan->bytes = plan->tag_off + align_up((size_t)plan->fused_slots * sizeof(uint64_t));
     return SSL_OK;
 }
 
@@ -336,7 +336,6 @@ int ssl_verify_attn(const ssl_shape* shape, const ssl_params* params, const int3
         fa.v.chunk = plan.fused_chunk;
         fa.v.seq = plan.fseq;
         fa.tag = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + plan.tag_off);
-        fa.tag_out = fa.tag + align_up((size_t)plan.fused_slots * sizeof(uint64_t)) / sizeof(uint64_t);
         fa.call_tag = next_call_tag();
         return launch_verify_fused(fa, plan.fused_slots, plan.row_tiles, stream) ==
                        hipSuccess

@@ -78,8 +78,7 @@ struct DraftArgs {
 // unit must be resident at once.
 struct FusedArgs {
     VerifyArgs v;           // part_ml / part_o indexed by slot
-    uint64_t* tag;          // [n_slots] statistics tags (no initialisation needed)
-    uint64_t* tag_out;      // [n_slots] partial-output tags
+    uint64_t* tag;          // [n_slots] publication tags (no initialisation needed)
     uint64_t call_tag;      // this call's tag: unique within the process
 };
 

@@ -8,15 +8,14 @@
 //      softmax per verify row (P.V on the MFMA, as in the two-sweep kernel);
 //      it keeps in LDS the probabilities of its keys relative to the running
 //      row maxima, and those maxima for every 32-key tile;
-//   2. it publishes its (running max, sum) per row and then a 64-bit call tag
-//      for its chunk, and waits until every chunk of its head shows the tag;
+//   2. it publishes its (running max, sum) per row and its partial P.V
+//      relative to those maxima, then a 64-bit call tag for its chunk, and
+//      waits until every chunk of its head shows the tag;
 //   3. from the merged (max, sum) of all chunks it forms one factor per tile
 //      and row, so that a stashed probability times its factor is the exact
-//      probability, and writes the scores of its keys; it then publishes its
-//      partial output already scaled to the exact normalizer, and a second
-//      tag;
-//   4. once every chunk's partial is out, the workgroup of chunk s adds the
-//      partials of rows s, s + nchunk, ... and writes them.
+//      probability, and writes the scores of its keys;
+//   4. the workgroup of chunk s adds the partials of rows s, s + nchunk, ...,
+//      each scaled to the exact normalizer, and writes them.
 //
 // Publication avoids agent-scope fences, which write back a whole L2 per wave
 // on this multi-XCD part: the published statistics and partials are written
@@ -43,7 +42,7 @@ using namespace vc;
 
 constexpr int kStashPad = 4;          // floats of padding per stashed row
 constexpr int kParkStride = kHeadDim + 4;                 // floats per parked output row
-constexpr int kParkFloats = kWaves * 16 * kParkStride;    // one row tile of every wave
+constexpr int kParkFloats = 2 * 16 * kParkStride;         // two waves' slices of a row tile
 constexpr int kSpinLimit = 1 << 22;   // bounded wait (far above any real wait)
 
 template <int NRT>
@@ -56,11 +55,13 @@ constexpr int static_lds_bytes() {
 }
 
 // The largest chunk whose stash (probabilities, padding, one running maximum
-// per tile and row) fits in LDS beside the static arrays.
+// per tile and row) fits in LDS beside the static arrays and the parking
+// slices.
 template <int NRT>
 constexpr int max_fused_chunk() {
     constexpr int kLds = 160 * 1024;
-    constexpr int floats_per_row = (kLds - static_lds_bytes<NRT>() - 1024) / 4 / (16 * NRT);
+    constexpr int floats_per_row =
+        (kLds - static_lds_bytes<NRT>() - kParkFloats * 4 - 1024) / 4 / (16 * NRT);
     return (floats_per_row - kStashPad) * kTile / (kTile + 1) / 128 * 128;
 }
 
@@ -85,7 +86,7 @@ __device__ __forceinline__ void wait_unit(const uint64_t* tag, int n, uint64_t w
 template <int NRT>
 __device__ __forceinline__ void fused_tile(const VerifyArgs& a, const Rows<NRT>& r,
                                            const KVTile& tl, int key0, int kl0, float* stash,
-                                           int stride, float* mtile, int m16, int G,
+                                           int stride, float* mtile, int mts, int m16, int G,
                                            float (&M)[NRT], float (&L)[NRT],
                                            f32x4 (&oacc)[8][NRT]) {
     f32x4 acc[2][NRT];
@@ -114,7 +115,7 @@ __device__ __forceinline__ void fused_tile(const VerifyArgs& a, const Rows<NRT>&
             sum += p[e >> 2][rt][e & 3];
             srow[16 * (e >> 2) + G + 4 * (e & 3)] = p[e >> 2][rt][e & 3];
         }
-        if (G == 0) mtile[(kl0 / kTile) * (NRT * 16) + rt * 16 + m16] = Mn;
+        if (G == 0) mtile[(rt * 16 + m16) * mts + kl0 / kTile] = Mn;
         L[rt] = L[rt] * alpha + sum;
         M[rt] = fmaxf(M[rt], mt);
 #pragma unroll
@@ -159,7 +160,8 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     const int chunk = a.chunk;
     const int key_begin = it.key_begin, key_end = it.key_end;
     const int stride = chunk + kStashPad;
-    float* mtile = stash + NRT * 16 * stride;   // [chunk / kTile][NRT*16] running row maxima
+    const int mts = chunk / kTile;
+    float* mtile = stash + NRT * 16 * stride;   // [NRT*16][mts] running row maxima per tile
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int m16 = lane & 15, G = lane >> 4;
 
@@ -187,11 +189,11 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
             load_v(vbase, key_begin + t * kTile, T, m16, G, bf.v);
         },
         [&](const KVTile& bf, int t) {
-            fused_tile<NRT>(a, r, bf, key_begin + t * kTile, t * kTile, stash, stride, mtile, m16,
+            fused_tile<NRT>(a, r, bf, key_begin + t * kTile, t * kTile, stash, stride, mtile, mts, m16,
                             G, M, L, oacc);
         });
 
-    // ---- 2. publish the item's partial output and row statistics ----------
+    // ---- 2. publish the chunk's row statistics and partial output ----------
 #pragma unroll
     for (int rt = 0; rt < NRT; ++rt) {
         L[rt] += shfl_xor_f(L[rt], 16);
@@ -209,6 +211,56 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         st_dev64(reinterpret_cast<uint64_t*>(a.part_ml + (size_t)slot * kRowCap + tid),
                  __builtin_bit_cast(uint64_t, make_float2(Mw, Lw)));
     }
+    // the partial P.V relative to the workgroup's row maxima: per row tile,
+    // waves 2 and 3 park theirs, waves 0 and 1 add them, park the sums, and
+    // all threads add the two slices and store the rows device-coherently
+    {
+        float* park = stash + NRT * 16 * stride + (chunk / kTile) * (NRT * 16);   // [2][16][kParkStride]
+        float* po = a.part_o + (size_t)slot * kRowCap * kHeadDim;
+#pragma unroll
+        for (int rt = 0; rt < NRT; ++rt) {
+            const int row = rt * 16 + m16;
+            float mw = -INFINITY;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) mw = fmaxf(mw, wml[w][row].x);
+            const float f = fast_exp2(M[rt] - safe_max(mw));
+            float* slice = park + ((wave & 1) * 16 + m16) * kParkStride;
+            if (wave >= 2) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int c4 = 32 * G + 8 * i;
+                    *reinterpret_cast<f32x4*>(slice + c4) =
+                        f32x4{oacc[0][rt][i], oacc[1][rt][i], oacc[2][rt][i], oacc[3][rt][i]} * f;
+                    *reinterpret_cast<f32x4*>(slice + c4 + 4) =
+                        f32x4{oacc[4][rt][i], oacc[5][rt][i], oacc[6][rt][i], oacc[7][rt][i]} * f;
+                }
+            }
+            __syncthreads();
+            if (wave < 2) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int c4 = 32 * G + 8 * i;
+                    f32x4 lo = *reinterpret_cast<const f32x4*>(slice + c4);
+                    f32x4 hi = *reinterpret_cast<const f32x4*>(slice + c4 + 4);
+                    lo += f32x4{oacc[0][rt][i], oacc[1][rt][i], oacc[2][rt][i], oacc[3][rt][i]} * f;
+                    hi += f32x4{oacc[4][rt][i], oacc[5][rt][i], oacc[6][rt][i], oacc[7][rt][i]} * f;
+                    *reinterpret_cast<f32x4*>(slice + c4) = lo;
+                    *reinterpret_cast<f32x4*>(slice + c4 + 4) = hi;
+                }
+            }
+            __syncthreads();
+            const int rows_here = min(16, R - rt * 16);
+            for (int x = tid; x < rows_here * (kHeadDim / 4); x += kThreads) {
+                const int rr = x >> 5, q4 = x & 31;
+                const f32x4 o = *reinterpret_cast<const f32x4*>(park + rr * kParkStride + 4 * q4) +
+                                *reinterpret_cast<const f32x4*>(park + (16 + rr) * kParkStride + 4 * q4);
+                uint64_t* d64 = reinterpret_cast<uint64_t*>(po + (size_t)(rt * 16 + rr) * kHeadDim + 4 * q4);
+                st_dev64(d64, __builtin_bit_cast(uint64_t, make_float2(o[0], o[1])));
+                st_dev64(d64 + 1, __builtin_bit_cast(uint64_t, make_float2(o[2], o[3])));
+            }
+            __syncthreads();
+        }
+    }
 
     // ---- wait for every chunk of this (sequence, KV head) -------------------
     wait_stores_done();
@@ -216,6 +268,30 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     if (tid == 0) st_dev64(fa.tag + slot, fa.call_tag);
     if (wave == 0) wait_unit(fa.tag + slot0, nchunk, fa.call_tag);
     __syncthreads();
+
+    // The first chunks of this workgroup's first row in step 4 (all of them
+    // for up to 32 chunks), loaded now so that the round trip overlaps 3a, 3b.
+    const int d4 = tid & 31, sg = tid >> 5;
+    auto load_part = [&](int row, int s0, f32x4 (&v)[4], float (&m)[4]) {
+#pragma unroll
+        for (int uu = 0; uu < 4; ++uu) {
+            const int s2 = s0 + 8 * uu;
+            if (s2 < nchunk) {
+                const size_t rw = (size_t)(slot0 + s2) * kRowCap + row;
+                const uint64_t* s64 = reinterpret_cast<const uint64_t*>(a.part_o + rw * kHeadDim + 4 * d4);
+                const float2 lo = __builtin_bit_cast(float2, ld_dev64(s64));
+                const float2 hi = __builtin_bit_cast(float2, ld_dev64(s64 + 1));
+                v[uu] = f32x4{lo.x, lo.y, hi.x, hi.y};
+                m[uu] = __builtin_bit_cast(float2, ld_dev64(reinterpret_cast<const uint64_t*>(a.part_ml + rw))).x;
+            } else {
+                v[uu] = f32x4{0.f, 0.f, 0.f, 0.f};
+                m[uu] = -INFINITY;
+            }
+        }
+    };
+    f32x4 pv[4];
+    float pm[4];
+    if (it.s < R) load_part(it.s, sg, pv, pm);
 
     // ---- 3a. exact row statistics over every chunk of the head -------------
     {
@@ -247,25 +323,20 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         row_lse[tid] = Lx > 0.f ? Mx + fast_log2(Lx) : INFINITY;
     }
     __syncthreads();
-    // tile factors: a stashed probability times its tile's factor is exact.
-    // The table is rewritten transposed, [row][tile], so that the lanes of a
-    // wave (eight tiles, one row) read distinct banks below.
+    // tile factors, in place: a stashed probability times its tile's factor
+    // is exact.  The table is [row][tile], so that the lanes of a wave (eight
+    // tiles, one row) read distinct banks below.
     const int nk = key_end - key_begin;
     const int ntl = (nk + kTile - 1) / kTile;
     {
         constexpr int kPer = (max_fused_chunk<NRT>() / kTile * NRT * 16 + kThreads - 1) / kThreads;
-        float f[kPer];
 #pragma unroll
         for (int j = 0; j < kPer; ++j) {
             const int x = tid + j * kThreads;
-            const int row = x % (NRT * 16);
-            f[j] = (x < ntl * NRT * 16 && row < R) ? fast_exp2(mtile[x] - row_lse[row]) : 0.f;
-        }
-        __syncthreads();
-#pragma unroll
-        for (int j = 0; j < kPer; ++j) {
-            const int x = tid + j * kThreads;
-            if (x < ntl * NRT * 16) mtile[(x % (NRT * 16)) * ntl + x / (NRT * 16)] = f[j];
+            if (x < NRT * 16 * mts) {
+                const int row = x / mts, tile = x - row * mts;
+                mtile[x] = (tile < ntl && row < R) ? fast_exp2(mtile[x] - row_lse[row]) : 0.f;
+            }
         }
     }
     __syncthreads();
@@ -281,7 +352,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         const f32x4* stash4 = reinterpret_cast<const f32x4*>(stash);
         const int stride4 = stride / 4;
         for (int k4 = 4 * tid; k4 < nk; k4 += 4 * kThreads) {
-            const float* ct = mtile + k4 / kTile;   // ct[row * ntl]
+            const float* ct = mtile + k4 / kTile;   // ct[row * mts]
             f32x4 sc = {0.f, 0.f, 0.f, 0.f};
             int row = r0;
             for (; row + 4 <= R; row += 4) {
@@ -290,87 +361,42 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     pr[j] = stash4[(row + j) * stride4 + k4 / 4];
-                    cr[j] = ct[(row + j) * ntl];
+                    cr[j] = ct[(row + j) * mts];
                 }
 #pragma unroll
                 for (int j = 0; j < 4; ++j) sc += pr[j] * cr[j];
             }
-            for (; row < R; ++row) sc += stash4[row * stride4 + k4 / 4] * ct[row * ntl];
+            for (; row < R; ++row) sc += stash4[row * stride4 + k4 / 4] * ct[row * mts];
 #pragma unroll
             for (int i = 0; i < 4; ++i)
                 if (k4 + i < nk) srow[key_begin + k4 + i] = sc[i];
         }
     }
 
-    // ---- 3c. this chunk's output, scaled to the exact normalizer ------------
-    // The stash is free now: per row tile, every wave parks its partial P.V,
-    // scaled from its own row maxima to the exact normalizers, in a slice of
-    // it, and all threads add the four slices (in wave order) and store the
-    // sum device-coherently: the workgroups that add a row's chunks below may
-    // run on other XCDs.
-    {
-        constexpr int kSliceStride = kParkStride;
-        float* park = stash;                          // [kWaves][16][kParkStride]
-        float* po = a.part_o + (size_t)slot * kRowCap * kHeadDim;
-#pragma unroll
-        for (int rt = 0; rt < NRT; ++rt) {
-            __syncthreads();
-            const int row = rt * 16 + m16;
-            const float f = fast_exp2(safe_max(M[rt]) - row_lse[row]);
-            float* dst = park + (wave * 16 + m16) * kSliceStride;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int c = 32 * G + 8 * i;
-                *reinterpret_cast<f32x4*>(dst + c) =
-                    f32x4{oacc[0][rt][i], oacc[1][rt][i], oacc[2][rt][i], oacc[3][rt][i]} * f;
-                *reinterpret_cast<f32x4*>(dst + c + 4) =
-                    f32x4{oacc[4][rt][i], oacc[5][rt][i], oacc[6][rt][i], oacc[7][rt][i]} * f;
-            }
-            __syncthreads();
-            const int rows_here = min(16, R - rt * 16);
-            for (int x = tid; x < rows_here * (kHeadDim / 4); x += kThreads) {
-                const int rr = x >> 5, c4 = x & 31;
-                f32x4 o = *reinterpret_cast<const f32x4*>(park + rr * kSliceStride + 4 * c4);
-#pragma unroll
-                for (int w = 1; w < kWaves; ++w)
-                    o += *reinterpret_cast<const f32x4*>(park + (w * 16 + rr) * kSliceStride + 4 * c4);
-                uint64_t* d64 = reinterpret_cast<uint64_t*>(po + (size_t)(rt * 16 + rr) * kHeadDim + 4 * c4);
-                st_dev64(d64, __builtin_bit_cast(uint64_t, make_float2(o[0], o[1])));
-                st_dev64(d64 + 1, __builtin_bit_cast(uint64_t, make_float2(o[2], o[3])));
-            }
-        }
-    }
-
     // ---- 4. rows it.s, it.s + nchunk, ... summed over the unit's chunks ------
-    // Chunks are added in index order, eight interleaved groups of them and
-    // then the groups in order (the combine kernel's order).
-    wait_stores_done();
-    __syncthreads();
-    if (tid == 0) st_dev64(fa.tag_out + slot, fa.call_tag);
-    if (wave == 0) wait_unit(fa.tag_out + slot0, nchunk, fa.call_tag);
-    __syncthreads();
+    // A chunk's partial is relative to its maxima m: it enters with 2^(m - lse).
+    // Chunks are added in index order within eight interleaved groups, then
+    // the groups in order.
+    __syncthreads();   // the stash is free once every thread's scores are out
     {
-        const int d4 = tid & 31, sg = tid >> 5;
         f32x4* red = reinterpret_cast<f32x4*>(stash);   // [8][32]
         for (int row = it.s; row < R; row += nchunk) {
+            const float lse = row_lse[row];
             f32x4 acc = {0.f, 0.f, 0.f, 0.f};
             for (int s0 = sg; s0 < nchunk; s0 += 4 * 8) {
                 f32x4 v[4];
+                float m[4];
+                if (row == it.s && s0 == sg) {
 #pragma unroll
-                for (int uu = 0; uu < 4; ++uu) {
-                    const int s2 = s0 + 8 * uu;
-                    const uint64_t* s64 = reinterpret_cast<const uint64_t*>(
-                        a.part_o + ((size_t)(slot0 + s2) * kRowCap + row) * kHeadDim + 4 * d4);
-                    if (s2 < nchunk) {
-                        const float2 lo = __builtin_bit_cast(float2, ld_dev64(s64));
-                        const float2 hi = __builtin_bit_cast(float2, ld_dev64(s64 + 1));
-                        v[uu] = f32x4{lo.x, lo.y, hi.x, hi.y};
-                    } else {
-                        v[uu] = f32x4{0.f, 0.f, 0.f, 0.f};
+                    for (int uu = 0; uu < 4; ++uu) {
+                        v[uu] = pv[uu];
+                        m[uu] = pm[uu];
                     }
+                } else {
+                    load_part(row, s0, v, m);
                 }
 #pragma unroll
-                for (int uu = 0; uu < 4; ++uu) acc += v[uu];
+                for (int uu = 0; uu < 4; ++uu) acc += v[uu] * fast_exp2(m[uu] - lse);
             }
             red[sg * 32 + d4] = acc;
             __syncthreads();
@@ -395,9 +421,9 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
 
 template <int NRT>
 hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, hipStream_t stream) {
-    // the logit stash, later reused to park the waves' partial outputs
-    const size_t dyn = std::max((size_t)NRT * 16 * (a.v.chunk + kStashPad + a.v.chunk / kTile),
-                                (size_t)kParkFloats) * sizeof(float);
+    // the probability stash with its tile maxima, then the parking slices
+    const size_t dyn =
+        ((size_t)NRT * 16 * (a.v.chunk + kStashPad + a.v.chunk / kTile) + kParkFloats) * sizeof(float);
     // The kernel's dynamic LDS limit is raised to the largest stash once per
     // device (setting it twice is harmless, so a race between threads is too).
     constexpr int kMaxDevices = 64;
@@ -409,8 +435,9 @@ hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, hipStream_t stream)
         e = hipFuncSetAttribute(
             reinterpret_cast<const void*>(verify_fused_kernel<NRT>),
             hipFuncAttributeMaxDynamicSharedMemorySize,
-            (int)((size_t)NRT * 16 *
-                  (fused_max_chunk(NRT) + kStashPad + fused_max_chunk(NRT) / kTile) *
+            (int)(((size_t)NRT * 16 *
+                       (fused_max_chunk(NRT) + kStashPad + fused_max_chunk(NRT) / kTile) +
+                   kParkFloats) *
                   sizeof(float)));
         if (e != hipSuccess) return e;
         if (dev >= 0 && dev < kMaxDevices) raised[dev].store(true, std::memory_order_relaxed);
