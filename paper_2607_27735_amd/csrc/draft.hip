@@ -5,11 +5,11 @@
 // one (sequence, KV head)'s index list, one wave per 32; each wave keeps an
 // online softmax per query head of the group (up to 16 heads = one MFMA row
 // tile).  The four waves are merged through LDS into one partial output with
-// its (max, sum) per head, which the workgroup publishes with device-coherent
-// stores before writing its 64-bit call tag; it then looks once at the tags
-// of its (sequence, KV head).  The workgroup that sees all of them -- the last
-// to publish always does -- merges the partials and writes the output (two
-// that both see them write identical results).
+// its (max, sum) per head.  Every workgroup but the one of the unit's last
+// chunk publishes that partial with device-coherent stores, then its 64-bit
+// call tag, and leaves; the last chunk's workgroup waits for the other tags
+// of its (sequence, KV head), merges all partials in chunk order (its own
+// from LDS) and writes the output.
 //
 // The MFMA layouts are the verify kernel's: K.Q^T on the bf16 MFMA with the
 // keys as A rows, O^T = V^T P^T so a head's softmax state and output stay in
@@ -27,6 +27,7 @@ constexpr int kDraftWaves = 4;
 constexpr int kDraftThreads = kDraftWaves * kWave;
 constexpr int kWaveChunk = kTile;              // index entries per wave
 constexpr int kParkStride = kHeadDim + 4;      // floats per parked head row
+constexpr int kSpinLimit = 1 << 22;            // bounded wait (far above any real wait)
 
 __device__ __forceinline__ int a_row_key(int m) { return (m >> 2) + 4 * (m & 3); }
 
@@ -136,7 +137,6 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
     __shared__ float2 wml[kDraftWaves][kRowCap];
     __shared__ float2 gml[kRowCap];
     __shared__ float park[kDraftWaves][kRowCap][kParkStride];
-    __shared__ int sh_all;
 
     // ---- one wave: 64 entries of the index list ----------------------------
     const int wbeg = it.key_begin + wave * kWaveChunk;
@@ -200,40 +200,46 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
     }
     __syncthreads();
 
-    // ---- publish this workgroup's partial (g heads x 128, and (max, sum)) ----
+    // ---- every chunk but the unit's last publishes its partial and leaves ----
     const size_t wg = blockIdx.x;
-    for (int x = tid; x < g * (kHeadDim / 2); x += kDraftThreads) {
-        const int row = x / (kHeadDim / 2), c2 = x - row * (kHeadDim / 2);
-        float2 o = *reinterpret_cast<const float2*>(&park[0][row][2 * c2]);
+    const bool finisher = it.key_begin + a.chunk >= it.n;   // the unit's last chunk
+    if (!finisher) {
+        for (int x = tid; x < g * (kHeadDim / 2); x += kDraftThreads) {
+            const int row = x / (kHeadDim / 2), c2 = x - row * (kHeadDim / 2);
+            float2 o = *reinterpret_cast<const float2*>(&park[0][row][2 * c2]);
 #pragma unroll
-        for (int w = 1; w < kDraftWaves; ++w) {
-            const float2 v = *reinterpret_cast<const float2*>(&park[w][row][2 * c2]);
-            o.x += v.x;
-            o.y += v.y;
+            for (int w = 1; w < kDraftWaves; ++w) {
+                const float2 v = *reinterpret_cast<const float2*>(&park[w][row][2 * c2]);
+                o.x += v.x;
+                o.y += v.y;
+            }
+            st_dev64(reinterpret_cast<uint64_t*>(a.part_o + (wg * kRowCap + row) * kHeadDim) + c2,
+                     __builtin_bit_cast(uint64_t, o));
         }
-        st_dev64(reinterpret_cast<uint64_t*>(a.part_o + (wg * kRowCap + row) * kHeadDim) + c2,
-                 __builtin_bit_cast(uint64_t, o));
-    }
-    if (tid < g)
-        st_dev64(reinterpret_cast<uint64_t*>(a.part_ml + wg * kRowCap + tid),
-                 __builtin_bit_cast(uint64_t, gml[tid]));
-    wait_stores_done();
-    __syncthreads();
-    if (tid == 0) {
-        st_dev64(a.tag + wg, a.call_tag);
+        if (tid < g)
+            st_dev64(reinterpret_cast<uint64_t*>(a.part_ml + wg * kRowCap + tid),
+                     __builtin_bit_cast(uint64_t, gml[tid]));
         wait_stores_done();
+        __syncthreads();
+        if (tid == 0) st_dev64(a.tag + wg, a.call_tag);
+        return;
     }
-    __syncthreads();
+    // The last chunk waits for the others: they have lower workgroup indices,
+    // so they were dispatched first, and they never wait.  The wait is also
+    // bounded.
     if (wave == 0) {
-        bool in = true;
-        for (int j = lane; j < it.nchunk; j += kWave) in &= ld_dev64(a.tag + it.item0 + j) == a.call_tag;
-        const bool all_in = __all(in);
-        if (lane == 0) sh_all = all_in;
+        int spins = 0;
+        bool all_in;
+        do {
+            bool in = true;
+            for (int j = lane; j < it.nchunk - 1; j += kWave) in &= ld_dev64(a.tag + it.item0 + j) == a.call_tag;
+            all_in = __all(in);
+            if (!all_in) __builtin_amdgcn_s_sleep(1);
+        } while (!all_in && ++spins < kSpinLimit);
     }
     __syncthreads();
-    if (!sh_all) return;
 
-    // ---- the last to publish: merge the partials of every head ---------------
+    // ---- merge the partials of every head, in chunk order ---------------------
     for (int x = tid; x < g * (kHeadDim / 4); x += kDraftThreads) {
         const int row = x >> 5, d4 = x & 31;
         float Mx = -INFINITY, Lx = 0.f;
@@ -244,14 +250,23 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
 #pragma unroll
             for (int uu = 0; uu < 8; ++uu) {
                 const int j = j0 + uu;
-                const bool ok = j < it.nchunk;
-                const size_t slot = (size_t)(it.item0 + (ok ? j : 0)) * kRowCap + row;
-                const uint64_t mlw = ok ? ld_dev64(reinterpret_cast<const uint64_t*>(a.part_ml + slot)) : 0ull;
-                ml[uu] = ok ? __builtin_bit_cast(float2, mlw) : make_float2(-INFINITY, 0.f);
-                const uint64_t* po = reinterpret_cast<const uint64_t*>(a.part_o + slot * kHeadDim) + 2 * d4;
-                const uint64_t lo = ok ? ld_dev64(po) : 0ull, hi = ok ? ld_dev64(po + 1) : 0ull;
-                const float2 flo = __builtin_bit_cast(float2, lo), fhi = __builtin_bit_cast(float2, hi);
-                o[uu] = f32x4{flo.x, flo.y, fhi.x, fhi.y};
+                if (j + 1 < it.nchunk) {
+                    const size_t slot = (size_t)(it.item0 + j) * kRowCap + row;
+                    ml[uu] = __builtin_bit_cast(float2, ld_dev64(reinterpret_cast<const uint64_t*>(a.part_ml + slot)));
+                    const uint64_t* po = reinterpret_cast<const uint64_t*>(a.part_o + slot * kHeadDim) + 2 * d4;
+                    const float2 flo = __builtin_bit_cast(float2, ld_dev64(po));
+                    const float2 fhi = __builtin_bit_cast(float2, ld_dev64(po + 1));
+                    o[uu] = f32x4{flo.x, flo.y, fhi.x, fhi.y};
+                } else if (j + 1 == it.nchunk) {   // this workgroup's own partial
+                    ml[uu] = gml[row];
+                    f32x4 ov = *reinterpret_cast<const f32x4*>(&park[0][row][4 * d4]);
+#pragma unroll
+                    for (int w = 1; w < kDraftWaves; ++w) ov += *reinterpret_cast<const f32x4*>(&park[w][row][4 * d4]);
+                    o[uu] = ov;
+                } else {
+                    ml[uu] = make_float2(-INFINITY, 0.f);
+                    o[uu] = f32x4{0.f, 0.f, 0.f, 0.f};
+                }
             }
             float Mn = Mx;
 #pragma unroll
