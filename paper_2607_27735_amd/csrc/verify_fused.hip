@@ -323,23 +323,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         row_lse[tid] = Lx > 0.f ? Mx + fast_log2(Lx) : INFINITY;
     }
     __syncthreads();
-    // tile factors, in place: a stashed probability times its tile's factor
-    // is exact.  The table is [row][tile], so that the lanes of a wave (eight
-    // tiles, one row) read distinct banks below.
     const int nk = key_end - key_begin;
-    const int ntl = (nk + kTile - 1) / kTile;
-    {
-        constexpr int kPer = (max_fused_chunk<NRT>() / kTile * NRT * 16 + kThreads - 1) / kThreads;
-#pragma unroll
-        for (int j = 0; j < kPer; ++j) {
-            const int x = tid + j * kThreads;
-            if (x < NRT * 16 * mts) {
-                const int row = x / mts, tile = x - row * mts;
-                mtile[x] = (tile < ntl && row < R) ? fast_exp2(mtile[x] - row_lse[row]) : 0.f;
-            }
-        }
-    }
-    __syncthreads();
 
     // ---- 3b. scores of this chunk's keys from the stashed probabilities ----
     {
@@ -351,8 +335,11 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         // 4 floats, and 4 consecutive keys share one tile
         const f32x4* stash4 = reinterpret_cast<const f32x4*>(stash);
         const int stride4 = stride / 4;
+        // A stashed probability times its tile's factor 2^(m_tile - lse) is
+        // exact; the tile maxima are [row][tile], so the lanes of a wave
+        // (eight tiles, one row) read distinct banks.
         for (int k4 = 4 * tid; k4 < nk; k4 += 4 * kThreads) {
-            const float* ct = mtile + k4 / kTile;   // ct[row * mts]
+            const float* mt = mtile + k4 / kTile;   // mt[row * mts]
             f32x4 sc = {0.f, 0.f, 0.f, 0.f};
             int row = r0;
             for (; row + 4 <= R; row += 4) {
@@ -361,12 +348,13 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     pr[j] = stash4[(row + j) * stride4 + k4 / 4];
-                    cr[j] = ct[(row + j) * mts];
+                    cr[j] = fast_exp2(mt[(row + j) * mts] - row_lse[row + j]);
                 }
 #pragma unroll
                 for (int j = 0; j < 4; ++j) sc += pr[j] * cr[j];
             }
-            for (; row < R; ++row) sc += stash4[row * stride4 + k4 / 4] * ct[row * mts];
+            for (; row < R; ++row)
+                sc += stash4[row * stride4 + k4 / 4] * fast_exp2(mt[row * mts] - row_lse[row]);
 #pragma unroll
             for (int i = 0; i < 4; ++i)
                 if (k4 + i < nk) srow[key_begin + k4 + i] = sc[i];
