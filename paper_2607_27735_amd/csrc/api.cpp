@@ -216,7 +216,7 @@ int check_select(const ssl_shape* s, const ssl_params* p, const int32_t* ctx) {
 // position bitmask of every unit, sized for the longest context of the call.
 struct SelectPlan {
     int part, parts;
-    size_t hist_off, coarse_off, cnt_off, thr_off, mask_off, seg_off, info_off, tag_off, bytes;
+    size_t hist_off, coarse_off, cnt_off, thr_off, mask_off, seg_off, tag_off, bytes;
 };
 
 int plan_select(const ssl_shape* s, const int32_t* ctx, SelectPlan* plan) {
@@ -233,8 +233,7 @@ int plan_select(const ssl_shape* s, const int32_t* ctx, SelectPlan* plan) {
     plan->thr_off = plan->cnt_off + align_up(slots * sizeof(uint32_t));
     plan->mask_off = plan->thr_off + align_up(units * 2 * sizeof(uint32_t));
     plan->seg_off = plan->mask_off + align_up(slots * (plan->part / 32) * sizeof(uint32_t));
-    plan->info_off = plan->seg_off + align_up(slots * plan->part * 2 * sizeof(uint32_t));
-    plan->tag_off = plan->info_off + align_up(slots * 4 * sizeof(uint32_t));
+    plan->tag_off = plan->seg_off + align_up(slots * plan->part * 2 * sizeof(uint32_t));
     plan->bytes = plan->tag_off + align_up(slots * 4 * sizeof(uint64_t));
     return SSL_OK;
 }
@@ -383,7 +382,6 @@ int ssl_select_topb(const ssl_shape* shape, const ssl_params* params, const int3
     a.thr = reinterpret_cast<uint32_t*>(ws + plan.thr_off);
     a.mask = reinterpret_cast<uint32_t*>(ws + plan.mask_off);
     a.seg = reinterpret_cast<uint2*>(ws + plan.seg_off);
-    a.info = reinterpret_cast<uint32_t*>(ws + plan.info_off);
     a.tag = reinterpret_cast<uint64_t*>(ws + plan.tag_off);
     a.call_tag = next_call_tag();
     a.part = plan.part;

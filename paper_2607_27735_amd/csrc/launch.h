@@ -52,7 +52,6 @@ struct SelectArgs {
     uint32_t* thr;      // [units][2]           threshold bin d1 and the count needed from it
     uint32_t* mask;     // [units][parts * part / 32] position bitmask
     uint2* seg;         // [units][parts][part] candidate (score bits, position)
-    uint32_t* info;     // [units][parts][4] single-kernel exchange: counts, offset, ties taken
     uint64_t* tag;      // [units][parts][4] publication tags (no initialisation needed)
     uint64_t call_tag;  // this call's tag: unique within the process
     int32_t n_kv_heads, max_ctx, k_sink, k_recent, budget, batch, part, parts;

@@ -509,7 +509,8 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
 // index order and a unit's partitions are consecutive, so when the lowest
 // unfinished unit waits, every workgroup ahead of its partitions has finished)
 // and exchange what they need through the workspace with device-coherent
-// stores and loads, each exchange closed by a 64-bit call tag:
+// stores and loads, each exchange closed by tag words that carry the call tag
+// and the partition's counts (see tagged() below):
 //   A. every partition publishes its nonzero histogram bins (bin, count); all
 //      of them add the unit's bins and find the bin d1 holding the K_mid-th
 //      largest middle score and `need`;
@@ -525,26 +526,47 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
 // ---------------------------------------------------------------------------
 constexpr int kSpinLimit = 1 << 20;   // bounded wait (far above any real wait)
 
-// Wave 0 polls until tag[0], tag[stride], ... tag[(n-1)*stride] all equal
-// `want`; the caller synchronises the workgroup afterwards.
-__device__ __forceinline__ void wait_tags(const uint64_t* tag, int n, int stride, uint64_t want) {
+// A count travels in its tag word: the low 48 bits of the call tag above a
+// 16-bit count (the call tags are a process-wide sequence, so a stale word
+// matches only after 2^48 calls, an uninitialised one by a 2^-48 accident),
+// and the wait that finds the word valid has the count without another load.
+__device__ __forceinline__ uint64_t tagged(uint64_t call_tag, uint32_t count) {
+    return (call_tag << 16) | count;
+}
+
+// Wave 0 polls until the words tag[q*stride] (and tag[q*stride + 1] when c1
+// is given), q < n, all carry the call tag, then writes their counts to c0[q]
+// (and c1[q]); the caller synchronises the workgroup afterwards.
+__device__ __forceinline__ void wait_counts(const uint64_t* tag, int n, int stride, uint64_t call_tag,
+                                            uint32_t* c0, uint32_t* c1) {
     if ((threadIdx.x >> 6) != 0) return;
     const int lane = threadIdx.x & 63;
+    const uint64_t want = call_tag & 0xFFFFFFFFFFFFull;
+    constexpr int kPer = kMaxSelectParts / kWave;
+    uint64_t v0[kPer], v1[kPer];
     int spins = 0;
     bool all_in;
     do {
         bool in = true;
-        for (int q = lane; q < n; q += kWave) in &= ld_dev64(tag + (size_t)q * stride) == want;
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {
+            const int q = lane + j * kWave;
+            v0[j] = q < n ? ld_dev64(tag + (size_t)q * stride) : want << 16;
+            v1[j] = (q < n && c1) ? ld_dev64(tag + (size_t)q * stride + 1) : want << 16;
+        }
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) in &= (v0[j] >> 16) == want && (v1[j] >> 16) == want;
         all_in = __all(in);
         if (!all_in) __builtin_amdgcn_s_sleep(1);
     } while (!all_in && ++spins < kSpinLimit);
-}
-
-// Publishes this workgroup's stores, then its tag.
-__device__ __forceinline__ void publish_tag(uint64_t* tag, uint64_t value) {
-    wait_stores_done();
-    __syncthreads();
-    if (threadIdx.x == 0) st_dev64(tag, value);
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        const int q = lane + j * kWave;
+        if (q < n) {
+            c0[q] = (uint32_t)(v0[j] & 0xffffu);
+            if (c1) c1[q] = (uint32_t)(v1[j] & 0xffffu);
+        }
+    }
 }
 
 template <int NR>
@@ -562,9 +584,8 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
     const float* S = a.scores + (size_t)u * a.max_ctx;
     const size_t up0 = (size_t)u * a.parts;
     const int P = g.parts;
-    constexpr int kTags = 4;                  // tag slots per partition
-    uint64_t* tag = a.tag + up0 * kTags;      // [P][kTags]
-    uint32_t* info = a.info + up0 * 4;        // [P][4]: candidates, above d1, histogram entries
+    constexpr int kTags = 4;                  // tag words per partition: histogram entries,
+    uint64_t* tag = a.tag + up0 * kTags;      // candidates, middle above d1; [P][kTags]
     const uint64_t want = a.call_tag;
 
     __shared__ __attribute__((aligned(16))) uint32_t hist[2048];   // read as uint4
@@ -577,6 +598,7 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
     __shared__ uint32_t words[kSelectMaxRounds * kRound / 32];   // this partition's bitmask
     __shared__ int offs[kMaxSelectParts + 1];
     __shared__ uint32_t n_def[kMaxSelectParts], n_above[kMaxSelectParts], n_tie[kMaxSelectParts];
+    __shared__ uint32_t n_cnt[kMaxSelectParts];   // histogram entries, then candidates, per partition
     __shared__ uint2 cand_lds[kTailCand];
     __shared__ uint16_t cand_p[kTailCand];
 
@@ -616,10 +638,11 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
 #pragma unroll
         for (int q = 0; q < 8; ++q)
             if (hv[q] != 0u) st_dev32(dst + slot++, ((uint32_t)(8 * tid + q) << 16) | hv[q]);
-        if (tid == 0) st_dev32(info + (size_t)p * 4 + 2, (uint32_t)n_entries);
+        wait_stores_done();
+        __syncthreads();
+        if (tid == 0) st_dev64(tag + (size_t)p * kTags + 0, tagged(want, (uint32_t)n_entries));
     }
-    publish_tag(tag + (size_t)p * kTags + 0, want);
-    wait_tags(tag + 0, P, kTags, want);
+    wait_counts(tag + 0, P, kTags, want, n_cnt, nullptr);
     __syncthreads();
     for (int x = tid; x < 2048; x += kSelThreads) hist[x] = 0u;   // now the unit's histogram
     __syncthreads();
@@ -633,7 +656,7 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const int pp = p0 + 4 * j;
-                n[j] = pp < P ? (int)ld_dev32(info + (size_t)pp * 4 + 2) : 0;
+                n[j] = pp < P ? (int)n_cnt[pp] : 0;
                 v[j] = pp < P ? ld_dev32(a.hist + (up0 + pp) * 2048 + lane) : 0u;
             }
             bool more = false;
@@ -721,20 +744,20 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
     // my_def is per wave (ballots are wave-uniform): add the waves
     if (lane == 0) def_w[wave] = my_def;
     __syncthreads();
+    wait_stores_done();
+    __syncthreads();
     if (tid == 0) {
         int nd = 0;
 #pragma unroll
         for (int w = 0; w < kSelWaves; ++w) nd += def_w[w];
-        st_dev32(info + (size_t)p * 4 + 0, (uint32_t)run);
-        st_dev32(info + (size_t)p * 4 + 1, (uint32_t)nd);
+        st_dev64(tag + (size_t)p * kTags + 1, tagged(want, (uint32_t)run));
+        st_dev64(tag + (size_t)p * kTags + 2, tagged(want, (uint32_t)nd));
     }
-    publish_tag(tag + (size_t)p * kTags + 1, want);
-    wait_tags(tag + 1, P, kTags, want);
+    wait_counts(tag + 1, P, kTags, want, n_cnt, n_def);
     __syncthreads();
 
     // ---- C. every partition resolves tau ------------------------------------
-    const int my_cnt = tid < P ? (int)ld_dev32(info + (size_t)tid * 4 + 0) : 0;
-    if (tid < P) n_def[tid] = ld_dev32(info + (size_t)tid * 4 + 1);
+    const int my_cnt = tid < P ? (int)n_cnt[tid] : 0;
     int nc;
     {
         const int o = block_scan(my_cnt, wave_tot, &nc);
