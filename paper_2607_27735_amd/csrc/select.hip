@@ -599,6 +599,7 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
     __shared__ int offs[kMaxSelectParts + 1];
     __shared__ uint32_t n_def[kMaxSelectParts], n_above[kMaxSelectParts], n_tie[kMaxSelectParts];
     __shared__ uint32_t n_cnt[kMaxSelectParts];   // histogram entries, then candidates, per partition
+    __shared__ int n_eq;                          // candidates sharing tau's top 22 bits
     __shared__ uint2 cand_lds[kTailCand];
     __shared__ uint16_t cand_p[kTailCand];
 
@@ -617,6 +618,7 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
         n_above[tid] = 0u;
         n_tie[tid] = 0u;
     }
+    if (tid == 0) n_eq = 0;
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < 4 * NR; ++j)
@@ -822,19 +824,42 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
     const Digit dg2 = find_digit_block(h2, need, sh_d, wave_tot);
     need -= dg2.above;
     const uint32_t prefix = (d1 << 20) | ((uint32_t)dg2.bin << 10);
+    // Pass 3 (bits 9..0) over the candidates with that 22-bit prefix.  The
+    // candidates above the prefix are counted for their partition now; those
+    // with it are listed as (partition, low 10 bits) in the free histogram
+    // array for the final counts.
+    uint32_t* eq_list = hist;
     for (int x = tid; x < nc; x += kSelThreads) {
         const uint32_t k = cand(x).x;
-        if ((k & 0xfffffc00u) == prefix) atomicAdd(&h3[k & 1023u], 1u);
+        const uint32_t top = k & 0xfffffc00u;
+        if (top >= prefix) {
+            const int pp = cached ? (int)cand_p[x] : part_of(x);
+            if (top > prefix) {
+                atomicAdd(&n_above[pp], 1u);
+            } else {
+                atomicAdd(&h3[k & 1023u], 1u);
+                const int slot = atomicAdd(&n_eq, 1);
+                if (slot < 2048) eq_list[slot] = ((uint32_t)pp << 10) | (k & 1023u);
+            }
+        }
     }
     __syncthreads();
     const Digit dg3 = find_digit_block(h3, need, sh_d, wave_tot);
     need -= dg3.above;                       // entries equal to tau to take
     const uint32_t tau = prefix | (uint32_t)dg3.bin;
-    for (int x = tid; x < nc; x += kSelThreads) {
-        const uint32_t k = cand(x).x;
-        if (k >= tau) {
-            const int pp = cached ? (int)cand_p[x] : part_of(x);
-            atomicAdd(k > tau ? &n_above[pp] : &n_tie[pp], 1u);
+    const int neq = n_eq;
+    if (neq <= 2048) {
+        for (int x = tid; x < neq; x += kSelThreads) {
+            const uint32_t e = eq_list[x], lo = e & 1023u;
+            if (lo >= (uint32_t)dg3.bin) atomicAdd(lo > (uint32_t)dg3.bin ? &n_above[e >> 10] : &n_tie[e >> 10], 1u);
+        }
+    } else {
+        for (int x = tid; x < nc; x += kSelThreads) {
+            const uint32_t k = cand(x).x;
+            if ((k & 0xfffffc00u) == prefix && k >= tau) {
+                const int pp = cached ? (int)cand_p[x] : part_of(x);
+                atomicAdd(k > tau ? &n_above[pp] : &n_tie[pp], 1u);
+            }
         }
     }
     __syncthreads();
