@@ -595,7 +595,6 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
     __shared__ int def_w[kSelWaves];
     __shared__ int sh[4];
     __shared__ int sh_d[3];
-    __shared__ uint32_t words[kSelectMaxRounds * kRound / 32];   // this partition's bitmask
     __shared__ int offs[kMaxSelectParts + 1];
     __shared__ uint32_t n_def[kMaxSelectParts], n_above[kMaxSelectParts], n_tie[kMaxSelectParts];
     __shared__ uint32_t n_cnt[kMaxSelectParts];   // histogram entries, then candidates, per partition
@@ -724,10 +723,6 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
             candb[e] = __ballot(mid && dg == d1);
             n_w += __builtin_popcountll(candb[e]);
             my_def += __builtin_popcountll(defb[e]);
-        }
-        if (lane < 8) {
-            const uint64_t m = lane < 2 ? defb[0] : lane < 4 ? defb[1] : lane < 6 ? defb[2] : defb[3];
-            words[(r * kRound + wave * 256) / 32 + lane] = (lane & 1) ? (uint32_t)(m >> 32) : (uint32_t)m;
         }
         int round_total;
         int slot = run + block_scan(lane == 0 ? n_w : 0, wave_tot, &round_total);
@@ -879,49 +874,44 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
     const int offset = sh[2], take = sh[3];
 
     // ---- D. this partition's selections at its offset ------------------------
-    int tie_base = 0;   // ties of this partition before the current round (uniform)
+    // Straight from ballots over the keys: a selected key at position x goes
+    // to offset + (selected non-ties before x) + min(ties before x, take); a
+    // tie is selected while its rank among the partition's ties is < take.
+    // One block scan per round carries both counts (packed, 16 bits each).
+    int32_t* out = a.idx + (size_t)u * a.budget;
+    int run_a = 0, run_t = 0;   // non-ties selected and ties, before this round (uniform)
 #pragma unroll
     for (int r = 0; r < NR; ++r) {
-        uint64_t selb[4], tieb[4];
-        int n_t = 0;
+        const int base = p * a.part + r * kRound + wave * 256;
+        uint64_t ab[4], tb[4];
+        int na = 0, nt = 0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const uint32_t k = keys[4 * r + e];
-            const bool cd = k != kNone && bin12(k) == d1;
-            selb[e] = __ballot(cd && k > tau);
-            tieb[e] = __ballot(cd && k == tau);
-            n_t += __builtin_popcountll(tieb[e]);
+            const bool mid = k != kNone;
+            const uint32_t dg = bin12(k);
+            ab[e] = __ballot(mid && (dg > d1 || (dg == d1 && k > tau)));
+            tb[e] = __ballot(mid && dg == d1 && k == tau);
+            na += __builtin_popcountll(ab[e]);
+            nt += __builtin_popcountll(tb[e]);
         }
-        int round_ties;
-        int rank = tie_base + block_scan(lane == 0 ? n_t : 0, wave_tot, &round_ties);
-        rank = __builtin_amdgcn_readlane(rank, 0);
+        int round_tot;
+        int pre = block_scan(lane == 0 ? (na << 16) | nt : 0, wave_tot, &round_tot);
+        pre = __builtin_amdgcn_readlane(pre, 0);
+        int ca = run_a + (pre >> 16), ct = run_t + (pre & 0xffff);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            // ties in position order: the first `take` of this partition's
-            const bool mine = (tieb[e] >> lane) & 1ull;
-            selb[e] |= __ballot(mine && rank + __builtin_popcountll(tieb[e] & lt) < take);
-            rank += __builtin_popcountll(tieb[e]);
+            const int xa = ca + __builtin_popcountll(ab[e] & lt);
+            const int xt = ct + __builtin_popcountll(tb[e] & lt);
+            int pos = -1;
+            if ((ab[e] >> lane) & 1ull) pos = offset + xa + min(xt, take);
+            else if (((tb[e] >> lane) & 1ull) && xt < take) pos = offset + xa + xt;
+            if (pos >= 0 && pos < a.budget) out[pos] = base + e * 64 + lane;
+            ca += __builtin_popcountll(ab[e]);
+            ct += __builtin_popcountll(tb[e]);
         }
-        if (lane < 8) {
-            const uint64_t m = lane < 2 ? selb[0] : lane < 4 ? selb[1] : lane < 6 ? selb[2] : selb[3];
-            words[(r * kRound + wave * 256) / 32 + lane] |= (lane & 1) ? (uint32_t)(m >> 32) : (uint32_t)m;
-        }
-        tie_base += round_ties;
-    }
-    __syncthreads();
-    int32_t* out = a.idx + (size_t)u * a.budget;
-    {
-        const int nw = a.part / 32;   // words of this partition (<= 256: one per thread)
-        uint32_t m = tid < nw ? words[tid] : 0u;
-        int total;
-        int pos = offset + block_scan(__builtin_popcount(m), wave_tot, &total);
-        const int wbase = p * a.part + 32 * tid;
-        while (m) {
-            const int bit = __builtin_ctz(m);
-            m &= m - 1u;
-            if (pos < a.budget) out[pos] = wbase + bit;
-            ++pos;
-        }
+        run_a += round_tot >> 16;
+        run_t += round_tot & 0xffff;
     }
     if (p == 0) {
         // sink, recent and the count
