@@ -858,20 +858,37 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
         }
     }
     __syncthreads();
-    // ties go to the first partitions; offsets follow the sink
-    const int nt = tid < P ? (int)n_tie[tid] : 0;
-    int tie_total;
-    const int tie_before = block_scan(nt, wave_tot, &tie_total);
-    const int take_t = min(max(need - tie_before, 0), nt);
-    const int out_t = tid < P ? (int)n_def[tid] + (int)n_above[tid] + take_t : 0;
-    int total_mid;
-    const int off_t = g.s_end + block_scan(out_t, wave_tot, &total_mid);
-    if (tid == p) {
-        sh[2] = off_t;
-        sh[3] = take_t;
+    // ties go to the first partitions; offsets follow the sink (one wave
+    // scans up to 64 partitions, the workgroup more)
+    if (P <= kWave) {
+        if (wave == 0) {
+            const int nt = lane < P ? (int)n_tie[lane] : 0;
+            const int tie_before = wave_incl_scan(nt) - nt;
+            const int take_t = min(max(need - tie_before, 0), nt);
+            const int out_t = lane < P ? (int)n_def[lane] + (int)n_above[lane] + take_t : 0;
+            const int incl = wave_incl_scan(out_t);
+            if (lane == p) {
+                sh[2] = g.s_end + incl - out_t;
+                sh[3] = take_t;
+            }
+            if (lane == kWave - 1) sh[0] = incl;
+        }
+    } else {
+        const int nt = tid < P ? (int)n_tie[tid] : 0;
+        int tie_total;
+        const int tie_before = block_scan(nt, wave_tot, &tie_total);
+        const int take_t = min(max(need - tie_before, 0), nt);
+        const int out_t = tid < P ? (int)n_def[tid] + (int)n_above[tid] + take_t : 0;
+        int all_out;
+        const int off_t = g.s_end + block_scan(out_t, wave_tot, &all_out);
+        if (tid == p) {
+            sh[2] = off_t;
+            sh[3] = take_t;
+        }
+        if (tid == 0) sh[0] = all_out;
     }
     __syncthreads();
-    const int offset = sh[2], take = sh[3];
+    const int offset = sh[2], take = sh[3], total_mid = sh[0];
 
     // ---- D. this partition's selections at its offset ------------------------
     // Straight from ballots over the keys: a selected key at position x goes
