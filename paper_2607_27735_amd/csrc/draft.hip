@@ -28,6 +28,7 @@ constexpr int kDraftThreads = kDraftWaves * kWave;
 constexpr int kWaveChunk = kTile;              // index entries per wave
 constexpr int kParkStride = kHeadDim + 4;      // floats per parked head row
 constexpr int kSpinLimit = 1 << 22;            // bounded wait (far above any real wait)
+constexpr int kMergeBatch = 16;                // partials loaded at once by the merging workgroup
 
 __device__ __forceinline__ int a_row_key(int m) { return (m >> 2) + 4 * (m & 3); }
 
@@ -244,11 +245,11 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
         const int row = x >> 5, d4 = x & 31;
         float Mx = -INFINITY, Lx = 0.f;
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        for (int j0 = 0; j0 < it.nchunk; j0 += 8) {
-            float2 ml[8];
-            f32x4 o[8];
+        for (int j0 = 0; j0 < it.nchunk; j0 += kMergeBatch) {
+            float2 ml[kMergeBatch];
+            f32x4 o[kMergeBatch];
 #pragma unroll
-            for (int uu = 0; uu < 8; ++uu) {
+            for (int uu = 0; uu < kMergeBatch; ++uu) {
                 const int j = j0 + uu;
                 if (j + 1 < it.nchunk) {
                     const size_t slot = (size_t)(it.item0 + j) * kRowCap + row;
@@ -270,12 +271,12 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
             }
             float Mn = Mx;
 #pragma unroll
-            for (int uu = 0; uu < 8; ++uu) Mn = fmaxf(Mn, ml[uu].x);
+            for (int uu = 0; uu < kMergeBatch; ++uu) Mn = fmaxf(Mn, ml[uu].x);
             const float alpha = Mx == -INFINITY ? 0.f : fast_exp2(Mx - Mn);
             Lx *= alpha;
             acc *= alpha;
 #pragma unroll
-            for (int uu = 0; uu < 8; ++uu) {
+            for (int uu = 0; uu < kMergeBatch; ++uu) {
                 const float wgt = ml[uu].x == -INFINITY ? 0.f : fast_exp2(ml[uu].x - Mn);
                 Lx += ml[uu].y * wgt;
                 acc += o[uu] * wgt;
