@@ -173,6 +173,8 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
     }
 
     // ---- merge the four waves (fixed order) --------------------------------
+    // (every lane takes its head's maximum over the waves straight from wml;
+    // the first 16 threads also keep the merged (max, sum))
     if (G == 0) wml[wave][m16] = make_float2(M, L);
     __syncthreads();
     if (tid < kRowCap) {
@@ -185,9 +187,10 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
             Lx += wml[w][tid].x == -INFINITY ? 0.f : wml[w][tid].y * fast_exp2(wml[w][tid].x - Mx);
         gml[tid] = make_float2(Mx, Lx);
     }
-    __syncthreads();
     {
-        const float Mx = gml[m16].x;
+        float Mx = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < kDraftWaves; ++w) Mx = fmaxf(Mx, wml[w][m16].x);
         const float f = M == -INFINITY ? 0.f : fast_exp2(M - Mx);
         float* dst = &park[wave][m16][0];
 #pragma unroll
