@@ -127,5 +127,10 @@ __device__ __forceinline__ void ml_merge(float& M, float& L, float m, float l) {
 __device__ __forceinline__ u32x4 ld_u32x4(const uint16_t* p) {
     return *reinterpret_cast<const u32x4*>(p);
 }
+// The same load with the non-temporal hint, for K/V cache rows that are read
+// once per call: it streams measurably faster than the default policy.
+__device__ __forceinline__ u32x4 ld_stream_u32x4(const uint16_t* p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
 
 }  // namespace ssl

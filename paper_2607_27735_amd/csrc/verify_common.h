@@ -63,7 +63,7 @@ __device__ __forceinline__ void load_k(const uint16_t* kbase, int key0, int T, i
         const int key = min(key0 + 16 * t + a_row_key(m16), T - 1);
         const uint16_t* p = kbase + (size_t)key * kHeadDim + 8 * G;
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) kr[t][kb] = ld_u32x4(p + 32 * kb);
+        for (int kb = 0; kb < 4; ++kb) kr[t][kb] = ld_stream_u32x4(p + 32 * kb);
     }
 }
 
@@ -75,7 +75,7 @@ __device__ __forceinline__ void load_v(const uint16_t* vbase, int key0, int T, i
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
         const int key = min(key0 + 16 * (e >> 2) + G + 4 * (e & 3), T - 1);
-        vr[e] = ld_u32x4(vbase + (size_t)key * kHeadDim + 8 * m16);
+        vr[e] = ld_stream_u32x4(vbase + (size_t)key * kHeadDim + 8 * m16);
     }
 }
 
