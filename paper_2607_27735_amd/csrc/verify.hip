@@ -78,7 +78,7 @@ __global__ __launch_bounds__(kThreads) void verify_stats_kernel(VerifyArgs a) {
     const int ntile = (it.key_end - it.key_begin + kTile - 1) / kTile;
     tile_pipeline<4, KTile>(
         wave, ntile, kWaves,
-        [&](KTile& b, int t) { load_k(kbase, it.key_begin + t * kTile, it.T, m16, G, b.k); },
+        [&](KTile& b, int t) { load_k<false>(kbase, it.key_begin + t * kTile, it.T, m16, G, b.k); },
         [&](const KTile& b, int t) {
             stats_tile<NRT>(a, r, b.k, it.key_begin + t * kTile, G, M, L);
         });

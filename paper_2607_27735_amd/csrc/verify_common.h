@@ -56,6 +56,10 @@ __device__ __forceinline__ void load_rows(const VerifyArgs& a, int b, int c, int
 
 // K operand of a 32-key tile: lane (m16, G) holds key a_row_key(m16) (+16 for
 // the second half) and head-dim elements 32kb + 8G .. +8 of k-block kb.
+// Loads carry the non-temporal hint (they stream faster) unless the rows are
+// read again by a later kernel of the same call: the two-sweep statistics pass
+// keeps K in the memory-side cache for the second pass.
+template <bool kStream = true>
 __device__ __forceinline__ void load_k(const uint16_t* kbase, int key0, int T, int m16, int G,
                                        u32x4 (&kr)[2][4]) {
 #pragma unroll
@@ -63,7 +67,7 @@ __device__ __forceinline__ void load_k(const uint16_t* kbase, int key0, int T, i
         const int key = min(key0 + 16 * t + a_row_key(m16), T - 1);
         const uint16_t* p = kbase + (size_t)key * kHeadDim + 8 * G;
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) kr[t][kb] = ld_stream_u32x4(p + 32 * kb);
+        for (int kb = 0; kb < 4; ++kb) kr[t][kb] = kStream ? ld_stream_u32x4(p + 32 * kb) : ld_u32x4(p + 32 * kb);
     }
 }
 
