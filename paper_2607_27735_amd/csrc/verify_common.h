@@ -56,9 +56,11 @@ __device__ __forceinline__ void load_rows(const VerifyArgs& a, int b, int c, int
 
 // K operand of a 32-key tile: lane (m16, G) holds key a_row_key(m16) (+16 for
 // the second half) and head-dim elements 32kb + 8G .. +8 of k-block kb.
-// Loads carry the non-temporal hint (they stream faster) unless the rows are
-// read again by a later kernel of the same call: the two-sweep statistics pass
-// keeps K in the memory-side cache for the second pass.
+// With kStream the loads carry the non-temporal hint.  It streams faster when
+// the rows are read once by a single round of workgroups; the two-sweep
+// statistics pass leaves it off so that the second pass finds K in the
+// memory-side cache, and so does a one-sweep launch of several rounds, where
+// it measured slower.
 template <bool kStream = true>
 __device__ __forceinline__ void load_k(const uint16_t* kbase, int key0, int T, int m16, int G,
                                        u32x4 (&kr)[2][4]) {
@@ -74,12 +76,14 @@ __device__ __forceinline__ void load_k(const uint16_t* kbase, int key0, int T, i
 // V rows of a 32-key tile: slot e = 4t + i is key 16t + G + 4i, and lane
 // (m16, G) holds its head-dim elements 8*m16 .. +8; one load instruction
 // covers four whole consecutive rows.
+template <bool kStream = true>
 __device__ __forceinline__ void load_v(const uint16_t* vbase, int key0, int T, int m16, int G,
                                        u32x4 (&vr)[8]) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
         const int key = min(key0 + 16 * (e >> 2) + G + 4 * (e & 3), T - 1);
-        vr[e] = ld_stream_u32x4(vbase + (size_t)key * kHeadDim + 8 * m16);
+        const uint16_t* p = vbase + (size_t)key * kHeadDim + 8 * m16;
+        vr[e] = kStream ? ld_stream_u32x4(p) : ld_u32x4(p);
     }
 }
 

@@ -142,7 +142,7 @@ __device__ __forceinline__ void fused_tile(const VerifyArgs& a, const Rows<NRT>&
     }
 }
 
-template <int NRT>
+template <int NRT, bool kStream>
 __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     const VerifyArgs& a = fa.v;
     extern __shared__ __attribute__((aligned(16))) float stash[];   // [NRT*16][chunk + pad]
@@ -185,8 +185,8 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     tile_pipeline<(NRT <= 2 ? 3 : 2), KVTile>(
         wave, ntile, kWaves,
         [&](KVTile& bf, int t) {
-            load_k(kbase, key_begin + t * kTile, T, m16, G, bf.k);
-            load_v(vbase, key_begin + t * kTile, T, m16, G, bf.v);
+            load_k<kStream>(kbase, key_begin + t * kTile, T, m16, G, bf.k);
+            load_v<kStream>(vbase, key_begin + t * kTile, T, m16, G, bf.v);
         },
         [&](const KVTile& bf, int t) {
             fused_tile<NRT>(a, r, bf, key_begin + t * kTile, t * kTile, stash, stride, mtile, mts, m16,
@@ -412,25 +412,35 @@ hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, hipStream_t stream)
     // the probability stash with its tile maxima, then the parking slices
     const size_t dyn =
         ((size_t)NRT * 16 * (a.v.chunk + kStashPad + a.v.chunk / kTile) + kParkFloats) * sizeof(float);
-    // The kernel's dynamic LDS limit is raised to the largest stash once per
-    // device (setting it twice is harmless, so a race between threads is too).
+    // The kernels' dynamic LDS limit is raised to the largest stash, and the
+    // CU count read, once per device (doing either twice is harmless, so a
+    // race between threads is too).
     constexpr int kMaxDevices = 64;
-    static std::atomic<bool> raised[kMaxDevices];
+    static std::atomic<int> cus[kMaxDevices];   // 0: not set up yet
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
-    if (dev < 0 || dev >= kMaxDevices || !raised[dev].load(std::memory_order_relaxed)) {
-        e = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(verify_fused_kernel<NRT>),
-            hipFuncAttributeMaxDynamicSharedMemorySize,
-            (int)(((size_t)NRT * 16 *
-                       (fused_max_chunk(NRT) + kStashPad + fused_max_chunk(NRT) / kTile) +
-                   kParkFloats) *
-                  sizeof(float)));
+    int n_cu = dev >= 0 && dev < kMaxDevices ? cus[dev].load(std::memory_order_relaxed) : 0;
+    if (n_cu == 0) {
+        const int lds = (int)(((size_t)NRT * 16 *
+                                   (fused_max_chunk(NRT) + kStashPad + fused_max_chunk(NRT) / kTile) +
+                               kParkFloats) *
+                              sizeof(float));
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(verify_fused_kernel<NRT, true>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, lds);
         if (e != hipSuccess) return e;
-        if (dev >= 0 && dev < kMaxDevices) raised[dev].store(true, std::memory_order_relaxed);
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(verify_fused_kernel<NRT, false>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+        if (e != hipSuccess) return e;
+        e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e != hipSuccess) return e;
+        if (dev >= 0 && dev < kMaxDevices) cus[dev].store(n_cu, std::memory_order_relaxed);
     }
-    hipLaunchKernelGGL(verify_fused_kernel<NRT>, dim3(n_slots), dim3(kThreads), dyn, stream, a);
+    // non-temporal K/V loads when every workgroup runs in the first round
+    if (n_slots <= n_cu)
+        hipLaunchKernelGGL((verify_fused_kernel<NRT, true>), dim3(n_slots), dim3(kThreads), dyn, stream, a);
+    else
+        hipLaunchKernelGGL((verify_fused_kernel<NRT, false>), dim3(n_slots), dim3(kThreads), dyn, stream, a);
     return hipGetLastError();
 }
 
