@@ -533,6 +533,9 @@ constexpr int kSpinLimit = 1 << 20;   // bounded wait (far above any real wait)
 __device__ __forceinline__ uint64_t tagged(uint64_t call_tag, uint32_t count) {
     return (call_tag << 16) | count;
 }
+// the counts carried: histogram entries (<= 2048), candidates and middle
+// positions above d1 of one partition (<= its length)
+static_assert(kSelectMaxRounds * kRound <= 0xffff, "a partition's counts must fit 16 bits");
 
 // Wave 0 polls until the words tag[q*stride] (and tag[q*stride + 1] when c1
 // is given), q < n, all carry the call tag, then writes their counts to c0[q]
