@@ -44,6 +44,7 @@ constexpr int kStashPad = 4;          // floats of padding per stashed row
 constexpr int kParkStride = kHeadDim + 4;                 // floats per parked output row
 constexpr int kParkFloats = 2 * 16 * kParkStride;         // two waves' slices of a row tile
 constexpr int kSpinLimit = 1 << 22;   // bounded wait (far above any real wait)
+constexpr float kLazy = 8.f;          // reference-maximum slack, log2 units
 
 template <int NRT>
 constexpr int static_lds_bytes() {
@@ -82,7 +83,7 @@ __device__ __forceinline__ void wait_unit(const uint64_t* tag, int n, uint64_t w
 }
 
 // One 32-key tile: online softmax and P.V; the tile's probabilities relative
-// to the running row maxima go to the LDS stash, those maxima to mtile.
+// to the rows' reference maxima go to the LDS stash, those maxima to mtile.
 template <int NRT>
 __device__ __forceinline__ void fused_tile(const VerifyArgs& a, const Rows<NRT>& r,
                                            const KVTile& tl, int key0, int kl0, float* stash,
@@ -106,20 +107,28 @@ __device__ __forceinline__ void fused_tile(const VerifyArgs& a, const Rows<NRT>&
         }
         mt = fmaxf(mt, shfl_xor_f(mt, 16));
         mt = fmaxf(mt, shfl_xor_f(mt, 32));
-        const float Mn = safe_max(fmaxf(M[rt], mt));
-        const float alpha = fast_exp2(M[rt] - Mn);
+        // M is a reference maximum that moves only when a tile's maximum
+        // exceeds it by more than kLazy (log2 units): the accumulators are then
+        // rescaled, for the whole row tile at once, and rarely; probabilities
+        // relative to it stay below 2^kLazy.
+        const bool grow = mt > M[rt] + kLazy;   // M = -inf: any finite mt
+        if (__any(grow)) {
+            const float alpha = grow ? fast_exp2(M[rt] - mt) : 1.f;
+            M[rt] = grow ? mt : M[rt];
+            L[rt] *= alpha;
+#pragma unroll
+            for (int jd = 0; jd < 8; ++jd) oacc[jd][rt] *= alpha;
+        }
+        const float Mr = safe_max(M[rt]);
         float sum = 0.f;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-            p[e >> 2][rt][e & 3] = fast_exp2(y[e] - Mn);
+            p[e >> 2][rt][e & 3] = fast_exp2(y[e] - Mr);
             sum += p[e >> 2][rt][e & 3];
             srow[16 * (e >> 2) + G + 4 * (e & 3)] = p[e >> 2][rt][e & 3];
         }
-        if (G == 0) mtile[(rt * 16 + m16) * mts + kl0 / kTile] = Mn;
-        L[rt] = L[rt] * alpha + sum;
-        M[rt] = fmaxf(M[rt], mt);
-#pragma unroll
-        for (int jd = 0; jd < 8; ++jd) oacc[jd][rt] *= alpha;
+        if (G == 0) mtile[(rt * 16 + m16) * mts + kl0 / kTile] = Mr;
+        L[rt] += sum;
     }
     u32x4 pb[NRT];
 #pragma unroll
