@@ -191,7 +191,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         for (int jd = 0; jd < 8; ++jd) oacc[jd][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
     const int ntile = (key_end - key_begin + kTile - 1) / kTile;
-    tile_pipeline<(NRT <= 2 ? 3 : 2), KVTile>(
+    tile_pipeline<2, KVTile>(
         wave, ntile, kWaves,
         [&](KVTile& bf, int t) {
             load_k<kStream>(kbase, key_begin + t * kTile, T, m16, G, bf.k);
