@@ -351,6 +351,17 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
             const float* mt = mtile + k4 / kTile;   // mt[row * mts]
             f32x4 sc = {0.f, 0.f, 0.f, 0.f};
             int row = r0;
+            for (; row + 8 <= R; row += 8) {   // eight rows' reads in flight
+                f32x4 pr[8];
+                float cr[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    pr[j] = stash4[(row + j) * stride4 + k4 / 4];
+                    cr[j] = mt[(row + j) * mts] - row_lse[row + j];
+                }
+#pragma unroll
+                for (int j = 0; j < 8; ++j) sc += pr[j] * fast_exp2(cr[j]);
+            }
             for (; row + 4 <= R; row += 4) {
                 f32x4 pr[4];
                 float cr[4];
