@@ -259,15 +259,23 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
             }
             __syncthreads();
             const int rows_here = min(16, R - rt * 16);
-            for (int x = tid; x < rows_here * (kHeadDim / 4); x += kThreads) {
-                const int rr = x >> 5, q4 = x & 31;
-                const f32x4 o = *reinterpret_cast<const f32x4*>(park + rr * kParkStride + 4 * q4) +
-                                *reinterpret_cast<const f32x4*>(park + (16 + rr) * kParkStride + 4 * q4);
-                uint64_t* d64 = reinterpret_cast<uint64_t*>(po + (size_t)(rt * 16 + rr) * kHeadDim + 4 * q4);
-                st_dev64(d64, __builtin_bit_cast(uint64_t, make_float2(o[0], o[1])));
-                st_dev64(d64 + 1, __builtin_bit_cast(uint64_t, make_float2(o[2], o[3])));
+            f32x4 o[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {   // both halves' reads in flight
+                const int x = tid + h * kThreads, rr = x >> 5, q4 = x & 31;
+                o[h] = *reinterpret_cast<const f32x4*>(park + rr * kParkStride + 4 * q4) +
+                       *reinterpret_cast<const f32x4*>(park + (16 + rr) * kParkStride + 4 * q4);
             }
-            __syncthreads();
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int x = tid + h * kThreads, rr = x >> 5, q4 = x & 31;
+                if (rr < rows_here) {
+                    uint64_t* d64 = reinterpret_cast<uint64_t*>(po + (size_t)(rt * 16 + rr) * kHeadDim + 4 * q4);
+                    st_dev64(d64, __builtin_bit_cast(uint64_t, make_float2(o[h][0], o[h][1])));
+                    st_dev64(d64 + 1, __builtin_bit_cast(uint64_t, make_float2(o[h][2], o[h][3])));
+                }
+            }
+            if (rt + 1 < NRT) __syncthreads();   // (the last one: the tag's barrier below)
         }
     }
 
