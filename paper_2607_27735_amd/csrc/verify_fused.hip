@@ -70,16 +70,24 @@ __device__ __forceinline__ float safe_max(float m) { return m == -INFINITY ? 0.f
 
 // Wave 0 polls until tag[0 .. n) all equal `want`; the caller synchronises
 // the workgroup afterwards.
+// Up to 128 tags (the most chunks a head may have here); the next poll is
+// issued before the previous one is checked, so that the last tag is seen
+// about one round trip after it lands rather than one and a half.
 __device__ __forceinline__ void wait_unit(const uint64_t* tag, int n, uint64_t want) {
     const int lane = threadIdx.x & 63;
-    int spins = 0;
-    bool all_in;
-    do {
-        bool in = true;
-        for (int s2 = lane; s2 < n; s2 += kWave) in &= ld_dev64(tag + s2) == want;
-        all_in = __all(in);
-        if (!all_in) __builtin_amdgcn_s_sleep(1);
-    } while (!all_in && ++spins < kSpinLimit);
+    // every lane loads (lanes past n re-read the last tag): no branch around
+    // the loads, so the compiler need not wait for them where they are issued
+    const uint64_t* p0 = tag + min(lane, n - 1);
+    const uint64_t* p1 = tag + min(lane + kWave, n - 1);
+    const bool use1 = lane + kWave < n;
+    uint64_t c0 = ld_dev64(p0), c1 = ld_dev64(p1);
+    for (int spins = 0; spins < kSpinLimit; ++spins) {
+        const uint64_t n0 = ld_dev64(p0), n1 = ld_dev64(p1);
+        if (__all(c0 == want && (!use1 || c1 == want))) break;
+        __builtin_amdgcn_s_sleep(1);
+        c0 = n0;
+        c1 = n1;
+    }
 }
 
 // One 32-key tile: online softmax and P.V; the tile's probabilities relative
