@@ -62,9 +62,12 @@ __device__ __forceinline__ Geom geom_of(const SelectArgs& a, int b) {
 
 // Score bits of position i if it is a middle position, kNone otherwise.  The
 // load is clamped into [0, T) so that it is unconditional.
+// (The load is unconditional and the result masked, so that the compiler keeps
+// the loads of a thread's keys in flight together instead of branching around
+// each one and waiting for it.)
 __device__ __forceinline__ uint32_t key_of(const float* S, const Geom& g, int i) {
     const uint32_t v = __builtin_bit_cast(uint32_t, S[min(i, g.T - 1)]);
-    return (i >= g.s_end && i < g.r_start) ? v : kNone;
+    return v | ((i >= g.s_end && i < g.r_start) ? 0u : kNone);
 }
 
 // Exclusive prefix sum of one value per thread over the workgroup; *total gets
@@ -549,16 +552,22 @@ __device__ __forceinline__ void wait_counts(const uint64_t* tag, int n, int stri
     uint64_t v0[kPer], v1[kPer];
     int spins = 0;
     bool all_in;
+    // (every lane loads, lanes past n re-reading the last words: no branch
+    // around the loads, so that they are in flight together)
+    const int nj = (n + kWave - 1) / kWave;   // wave-uniform
     do {
         bool in = true;
 #pragma unroll
         for (int j = 0; j < kPer; ++j) {
-            const int q = lane + j * kWave;
-            v0[j] = q < n ? ld_dev64(tag + (size_t)q * stride) : want << 16;
-            v1[j] = (q < n && c1) ? ld_dev64(tag + (size_t)q * stride + 1) : want << 16;
+            if (j < nj) {
+                const size_t q = (size_t)min(lane + j * kWave, n - 1) * stride;
+                v0[j] = ld_dev64(tag + q);
+                v1[j] = c1 ? ld_dev64(tag + q + 1) : want << 16;
+            }
         }
 #pragma unroll
-        for (int j = 0; j < kPer; ++j) in &= (v0[j] >> 16) == want && (v1[j] >> 16) == want;
+        for (int j = 0; j < kPer; ++j)
+            if (j < nj) in &= (v0[j] >> 16) == want && (v1[j] >> 16) == want;
         all_in = __all(in);
         if (!all_in) __builtin_amdgcn_s_sleep(1);
     } while (!all_in && ++spins < kSpinLimit);
