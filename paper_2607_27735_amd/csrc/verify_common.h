@@ -105,27 +105,33 @@ __device__ __forceinline__ void qk_tile(const u32x4 (&kr)[2][4], const Rows<NRT>
 // Runs compute(tile) over the wave's tiles first, first + step, ... < ntile
 // with a ring of NBUF register buffers: while one tile is computed, the loads
 // of the next NBUF - 1 tiles are in flight.  load(buf, tile) issues loads only.
+// The steady-state loop issues its loads unconditionally: a load under a
+// branch makes the compiler's wait counts assume the path without it, so the
+// wait for the current tile would also wait for the tiles in flight.  The
+// last tiles are peeled off into a tail where the loads may be skipped.
 template <int NBUF, typename Buf, typename Load, typename Compute, typename Pre>
 __device__ __forceinline__ void tile_pipeline(int first, int ntile, int step, Load&& load,
                                               Compute&& compute, Pre&& pre) {
+    const int n = first < ntile ? (ntile - first + step - 1) / step : 0;
     Buf buf[NBUF];
 #pragma unroll
-    for (int p = 0; p < NBUF - 1; ++p) {
-        const int t = first + p * step;
-        if (t < ntile) load(buf[p], t);
-    }
+    for (int p = 0; p < NBUF - 1; ++p)
+        if (p < n) load(buf[p], first + p * step);
     // Every wave runs pre() once, with the first tiles' loads already in flight.
     pre();
-    int tt = first;
-    while (tt < ntile) {
+    int i = 0;
+    for (; i + 2 * NBUF - 1 <= n; i += NBUF) {
 #pragma unroll
         for (int p = 0; p < NBUF; ++p) {
-            if (tt < ntile) {
-                const int tn = tt + (NBUF - 1) * step;
-                if (tn < ntile) load(buf[(p + NBUF - 1) % NBUF], tn);
-                compute(buf[p], tt);
-            }
-            tt += step;
+            load(buf[(p + NBUF - 1) % NBUF], first + (i + p + NBUF - 1) * step);
+            compute(buf[p], first + (i + p) * step);
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < 2 * NBUF - 2; ++q) {
+        if (i + q < n) {
+            if (i + q + NBUF - 1 < n) load(buf[(q + NBUF - 1) % NBUF], first + (i + q + NBUF - 1) * step);
+            compute(buf[q % NBUF], first + (i + q) * step);
         }
     }
 }
