@@ -228,7 +228,7 @@ int plan_select(const ssl_shape* s, const int32_t* ctx, SelectPlan* plan) {
     const size_t slots = (size_t)s->batch * s->n_kv_heads * plan->parts;
     const size_t units = (size_t)s->batch * s->n_kv_heads;
     plan->hist_off = 0;
-    plan->coarse_off = plan->hist_off + align_up(slots * 2048 * sizeof(uint32_t));
+    plan->coarse_off = plan->hist_off + align_up(slots * kHistSlotWords * sizeof(uint32_t));
     plan->cnt_off = plan->coarse_off + align_up(slots * 64 * sizeof(uint32_t));
     plan->thr_off = plan->cnt_off + align_up(slots * sizeof(uint32_t));
     plan->mask_off = plan->thr_off + align_up(units * 2 * sizeof(uint32_t));

@@ -41,12 +41,15 @@ struct VerifyArgs {
 constexpr int kSelectMaxRounds = 8;
 constexpr int kSelectTargetParts = 32;
 constexpr int kMaxSelectParts = 256;
+// 32-bit words per partition in SelectArgs::hist: a dense 2048-bin histogram
+// (three-kernel path) or up to 2048 tagged 64-bit bin entries (one kernel).
+constexpr int kHistSlotWords = 4096;
 
 struct SelectArgs {
     const float* scores;
     int32_t* idx;
     int32_t* n_idx;
-    uint32_t* hist;     // [units][parts][2048] top-12-bit histogram of each partition
+    uint32_t* hist;     // [units][parts][kHistSlotWords] histogram of each partition's top 11 score bits
     uint32_t* coarse;   // [units][parts][64]   the same in bins of 32
     uint32_t* cnt;      // [units][parts]       candidates of each partition
     uint32_t* thr;      // [units][2]           threshold bin d1 and the count needed from it

@@ -116,7 +116,7 @@ __global__ __launch_bounds__(kSelThreads) void select_hist_kernel(SelectArgs a) 
     __syncthreads();
 
     const size_t up = (size_t)u * a.parts + p;
-    uint4* dst = reinterpret_cast<uint4*>(a.hist + up * 2048);
+    uint4* dst = reinterpret_cast<uint4*>(a.hist + up * kHistSlotWords);
     const uint4* src = reinterpret_cast<const uint4*>(hist);
     dst[tid] = src[tid];
     dst[tid + kSelThreads] = src[tid + kSelThreads];
@@ -432,7 +432,7 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const int pp = p0 + 8 * j;
-                    v[j] = pp < g.parts ? a.hist[(up0 + pp) * 2048 + dc * 32 + fb] : 0u;
+                    v[j] = pp < g.parts ? a.hist[(up0 + pp) * kHistSlotWords + dc * 32 + fb] : 0u;
                 }
 #pragma unroll
                 for (int j = 0; j < 4; ++j) s += v[j];
@@ -514,9 +514,9 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
 // and exchange what they need through the workspace with device-coherent
 // stores and loads, each exchange closed by tag words that carry the call tag
 // and the partition's counts (see tagged() below):
-//   A. every partition publishes its nonzero histogram bins (bin, count); all
-//      of them add the unit's bins and find the bin d1 holding the K_mid-th
-//      largest middle score and `need`;
+//   A. every partition publishes its nonzero histogram bins (bin, count),
+//      each entry tagged on its own; all of them add the unit's bins and find
+//      the bin d1 holding the K_mid-th largest middle score and `need`;
 //   B. every partition publishes its bin-d1 candidates (in position order),
 //      their count and its count of middle positions above d1;
 //   C. every partition gathers the unit's candidates and resolves tau by two
@@ -539,6 +539,18 @@ __device__ __forceinline__ uint64_t tagged(uint64_t call_tag, uint32_t count) {
 // the counts carried: histogram entries (<= 2048), candidates and middle
 // positions above d1 of one partition (<= its length)
 static_assert(kSelectMaxRounds * kRound <= 0xffff, "a partition's counts must fit 16 bits");
+
+// A published histogram entry carries its own tag, so that a reader can load
+// the entries in the same round trip as the tag word that gives their count:
+// the low 39 bits of the call tag above the bin (11 bits) and its count (14
+// bits).  A stale entry matches only 2^39 calls later.
+constexpr int kBinPayloadBits = 25;
+constexpr uint64_t kBinTagMask = (1ull << (64 - kBinPayloadBits)) - 1ull;
+__device__ __forceinline__ uint64_t bin_entry(uint64_t call_tag, uint32_t bin, uint32_t count) {
+    return ((call_tag & kBinTagMask) << kBinPayloadBits) | ((uint64_t)bin << 14) | count;
+}
+static_assert(kSelectMaxRounds * kRound < (1 << 14), "a bin count must fit 14 bits");
+static_assert(2048 * 2 <= kHistSlotWords, "a partition's bin entries must fit its slot");
 
 // Wave 0 polls until the words tag[q*stride] (and tag[q*stride + 1] when c1
 // is given), q < n, all carry the call tag, then writes their counts to c0[q]
@@ -609,7 +621,7 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
     __shared__ int sh_d[3];
     __shared__ int offs[kMaxSelectParts + 1];
     __shared__ uint32_t n_def[kMaxSelectParts], n_above[kMaxSelectParts], n_tie[kMaxSelectParts];
-    __shared__ uint32_t n_cnt[kMaxSelectParts];   // histogram entries, then candidates, per partition
+    __shared__ uint32_t n_cnt[kMaxSelectParts];   // candidates per partition
     __shared__ int n_eq;                          // candidates sharing tau's top 22 bits
     __shared__ uint2 cand_lds[kTailCand];
     __shared__ uint16_t cand_p[kTailCand];
@@ -647,48 +659,71 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
         for (int q = 0; q < 8; ++q) nz += hv[q] != 0u;
         int n_entries;
         int slot = block_scan(nz, wave_tot, &n_entries);
-        uint32_t* dst = a.hist + (up0 + p) * 2048;
+        uint64_t* dst = reinterpret_cast<uint64_t*>(a.hist + (up0 + p) * kHistSlotWords);
 #pragma unroll
         for (int q = 0; q < 8; ++q)
-            if (hv[q] != 0u) st_dev32(dst + slot++, ((uint32_t)(8 * tid + q) << 16) | hv[q]);
-        wait_stores_done();
-        __syncthreads();
+            if (hv[q] != 0u) st_dev64(dst + slot++, bin_entry(want, 8 * tid + q, hv[q]));
+        // (no wait for the entry stores: every entry carries the call tag)
         if (tid == 0) st_dev64(tag + (size_t)p * kTags + 0, tagged(want, (uint32_t)n_entries));
     }
-    wait_counts(tag + 0, P, kTags, want, n_cnt, nullptr);
     __syncthreads();
     for (int x = tid; x < 2048; x += kSelThreads) hist[x] = 0u;   // now the unit's histogram
     __syncthreads();
     {
-        // wave w adds partitions w, w+4, ...: for eight partitions at once the
-        // entry counts and, speculatively, the first 64 entries are loaded
-        // together (entries past a count are stale and dropped), then any rest
+        // wave w adds partitions w, w+4, ...: for eight partitions at once it
+        // polls their tag words and, in the same round trip, their first 64
+        // entries until the words and every entry below the count carry the
+        // call tag; then any entries past the first 64 the same way
+        const uint64_t want48 = want & 0xFFFFFFFFFFFFull;
+        const uint64_t etag = want & kBinTagMask;
         for (int p0 = wave; p0 < P; p0 += 4 * 8) {
             int n[8];
-            uint32_t v[8];
+            uint64_t v[8];
+            const uint64_t* ent[8];
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int pp = p0 + 4 * j;
-                n[j] = pp < P ? (int)n_cnt[pp] : 0;
-                v[j] = pp < P ? ld_dev32(a.hist + (up0 + pp) * 2048 + lane) : 0u;
-            }
+            for (int j = 0; j < 8; ++j)
+                ent[j] = reinterpret_cast<const uint64_t*>(a.hist + (up0 + min(p0 + 4 * j, P - 1)) * kHistSlotWords);
+            int spins = 0;
+            bool all_in;
+            do {
+                uint64_t tw[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    tw[j] = ld_dev64(tag + (size_t)min(p0 + 4 * j, P - 1) * kTags);
+                    v[j] = ld_dev64(ent[j] + lane);
+                }
+                bool in = true;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    n[j] = (int)(tw[j] & 0xffffu);
+                    in &= (tw[j] >> 16) == want48 && (lane >= n[j] || (v[j] >> kBinPayloadBits) == etag);
+                }
+                all_in = __all(in);
+                if (!all_in) __builtin_amdgcn_s_sleep(1);
+            } while (!all_in && ++spins < kSpinLimit);
             bool more = false;
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
-                if (lane < n[j]) atomicAdd(&hist[(v[j] >> 16) & 2047u], v[j] & 0xffffu);
-                more |= n[j] > kWave;
+                if (p0 + 4 * j < P && lane < n[j]) atomicAdd(&hist[(v[j] >> 14) & 2047u], (uint32_t)(v[j] & 0x3fffu));
+                more |= p0 + 4 * j < P && n[j] > kWave;
             }
             for (int e0 = kWave; more; e0 += kWave) {   // wave-uniform
+                spins = 0;
+                do {
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) v[j] = ld_dev64(ent[j] + min(e0 + lane, kHistSlotWords / 2 - 1));
+                    bool in = true;
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) in &= e0 + lane >= n[j] || (v[j] >> kBinPayloadBits) == etag;
+                    all_in = __all(in);
+                    if (!all_in) __builtin_amdgcn_s_sleep(1);
+                } while (!all_in && ++spins < kSpinLimit);
                 more = false;
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    const int pp = p0 + 4 * j;
-                    v[j] = e0 + lane < n[j] ? ld_dev32(a.hist + (up0 + pp) * 2048 + e0 + lane) : 0u;
-                }
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    if (e0 + lane < n[j]) atomicAdd(&hist[(v[j] >> 16) & 2047u], v[j] & 0xffffu);
-                    more |= n[j] > e0 + kWave;
+                    if (p0 + 4 * j < P && e0 + lane < n[j])
+                        atomicAdd(&hist[(v[j] >> 14) & 2047u], (uint32_t)(v[j] & 0x3fffu));
+                    more |= p0 + 4 * j < P && n[j] > e0 + kWave;
                 }
             }
         }
