@@ -164,7 +164,7 @@ int ssl_verify_attn(const ssl_shape *shape, const ssl_params *params,
  * n_idx[b] = n = ssl_index_count(T, ...); slots past n are not written.
  *
  * Workspace: ssl_select_workspace gives its size for these context lengths
- * (about 17 bytes per position of the longest context, per (b, c)); device
+ * (at most 25 bytes per position of the longest context, per (b, c)); device
  * memory, 16-byte aligned, owned by the caller, no initial contents needed.
  * A call uses it until the call's work on `stream` ends; calls that overlap
  * in time must not share one workspace.

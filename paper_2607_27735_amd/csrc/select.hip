@@ -66,7 +66,8 @@ __device__ __forceinline__ Geom geom_of(const SelectArgs& a, int b) {
 // the loads of a thread's keys in flight together instead of branching around
 // each one and waiting for it.)
 __device__ __forceinline__ uint32_t key_of(const float* S, const Geom& g, int i) {
-    const uint32_t v = __builtin_bit_cast(uint32_t, S[min(i, g.T - 1)]);
+    uint32_t v = __builtin_bit_cast(uint32_t, S[min(i, g.T - 1)]);
+    v = v == 0x80000000u ? 0u : v;   // -0 ranks as +0 (equal scores)
     return v | ((i >= g.s_end && i < g.r_start) ? 0u : kNone);
 }
 

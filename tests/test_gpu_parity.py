@@ -160,6 +160,9 @@ def test_select_special_cases():
         "all-equal": np.full(shape, 0.37, np.float32),
         "tiny-values": (rng.random(shape) * 1e-30).astype(np.float32),
         "one-huge": np.where(rng.random(shape) < 0.001, 1e30, 1e-3).astype(np.float32),
+        # -0 and +0 are equal scores: ties broken by position like any others
+        "signed-zeros": np.where(rng.random(shape) < 0.2, rng.random(shape),
+                                 np.where(rng.random(shape) < 0.5, -0.0, 0.0)).astype(np.float32),
     }
     for label, s32 in cases.items():
         for budget, ks, kr in [(300, 4, 32), (36, 4, 32), (3000, 4, 32), (301, 0, 0),
