@@ -12,7 +12,9 @@
  *            materializes the attention weights) and Sec. 3.2 Eq. 3 (per-head
  *            importance = attention mass received from the last W queries);
  *   select   Sec. 3.2 Eq. 4 (sink + top-K_mid of the remaining span + recent);
- *   draft    Sec. 3.2 Eq. 5 (attention over the gathered K/V rows);
+ *   draft    Sec. 3.2 Eq. 5 (attention over the gathered K/V rows), and one
+ *            step of a draft round (Sec. 3.1) over that view with its recent
+ *            window slid to the newest drafted token;
  *   control  Sec. 3.3 Eq. 6 (entropy EMAs), Eq. 7 (soft acceptance
  *            probability), Eq. 8 (speculation length maximizing expected
  *            tokens per unit cost).
@@ -274,6 +276,82 @@ int oracle_draft(int batch, int n_q_heads, int n_kv_heads, int head_dim, int max
             for (int e = 0; e < d; ++e) o[e] += P * widen_bf16(vc[(size_t)I[t] * d + e]);
         }
         free(x);
+    }
+    return 0;
+}
+
+/*
+ * One step of a draft round.  Sec. 3.1: the target model drafts k tokens one
+ * after another over the sparse view of Sec. 3.2 (Eq. 5).  The index set
+ * I = idx[b,c,0..n), n = oracle_index_count(T, ...), was built by Eq. 4 at
+ * T = base_len[b].  After i tokens have been drafted (cur = cur_len[b] = T + i,
+ * their K/V rows already in the cache) the step attends over
+ *     F = the entries of I below r_T = max(T - K_recent, min(K_sink, T)),
+ *         i.e. the sink and TopK parts, fixed for the whole round;
+ *     W = [max(r_T, cur - K_recent), cur), the recent window slid forward so
+ *         that it ends at the newest token.
+ * (Reading: the paper keeps the most recent tokens in the draft view but does
+ * not say how that window moves while a round drafts; here it slides and the
+ * budget stays n.)  Requires T <= cur <= T + K_recent, so that every drafted
+ * token lies in W, and cur <= max_ctx.  With x_t = sm_scale <q[b,h], k[b,c,t]>
+ * over t in F u W:  out[b,h] = sum_t softmax(x)_t v[b,c,t].
+ * Layouts as oracle_draft.  Returns 0 or -1.
+ */
+int oracle_draft_step(int batch, int n_q_heads, int n_kv_heads, int head_dim, int max_ctx,
+                      int budget, int k_sink, int k_recent, const int32_t *base_len,
+                      const int32_t *cur_len, const uint16_t *q_draft, const uint16_t *k,
+                      const uint16_t *v, const int32_t *idx, double sm_scale, double *out)
+{
+    if (batch < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads != 0 || head_dim < 1)
+        return -1;
+    if (budget < 1 || k_sink < 0 || k_recent < 0 || k_sink + k_recent > budget) return -1;
+    for (int b = 0; b < batch; ++b) {
+        const int T = base_len[b], cur = cur_len[b];
+        if (T < 1 || cur < T || cur - T > k_recent || cur > max_ctx) return -1;
+    }
+    const int g = n_q_heads / n_kv_heads;
+    const int d = head_dim;
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int bh = 0; bh < batch * n_q_heads; ++bh) {
+        const int b = bh / n_q_heads, h = bh % n_q_heads, c = h / g;
+        const int T = base_len[b], cur = cur_len[b];
+        const int n = oracle_index_count(T, k_sink, k_recent, budget);
+        const int s_end = k_sink < T ? k_sink : T;
+        const int r_T = (T - k_recent) > s_end ? (T - k_recent) : s_end;
+        const int w0 = (cur - k_recent) > r_T ? (cur - k_recent) : r_T;
+        const int32_t *I = idx + ((size_t)b * n_kv_heads + c) * budget;
+        /* the step's positions: F, then W */
+        int *S = (int *)malloc(sizeof(int) * (size_t)(n + k_recent + 1));
+        int m_S = 0;
+        for (int t = 0; t < n; ++t)
+            if (I[t] < r_T) S[m_S++] = I[t];
+        for (int t = w0; t < cur; ++t) S[m_S++] = t;
+        const uint16_t *kc = k + ((size_t)b * n_kv_heads + c) * max_ctx * d;
+        const uint16_t *vc = v + ((size_t)b * n_kv_heads + c) * max_ctx * d;
+        const uint16_t *qs = q_draft + ((size_t)b * n_q_heads + h) * d;
+        double *x = (double *)malloc(sizeof(double) * (size_t)(m_S > 0 ? m_S : 1));
+        double m = -INFINITY;
+        for (int t = 0; t < m_S; ++t) {
+            double dot = 0.0;
+            for (int e = 0; e < d; ++e)
+                dot += widen_bf16(qs[e]) * widen_bf16(kc[(size_t)S[t] * d + e]);
+            x[t] = sm_scale * dot;
+            if (x[t] > m) m = x[t];
+        }
+        double L = 0.0;
+        for (int t = 0; t < m_S; ++t) {
+            x[t] = exp(x[t] - m);
+            L += x[t];
+        }
+        double *o = out + ((size_t)b * n_q_heads + h) * d;
+        for (int e = 0; e < d; ++e) o[e] = 0.0;
+        for (int t = 0; t < m_S; ++t) {
+            const double P = x[t] / L;
+            for (int e = 0; e < d; ++e) o[e] += P * widen_bf16(vc[(size_t)S[t] * d + e]);
+        }
+        free(x);
+        free(S);
     }
     return 0;
 }

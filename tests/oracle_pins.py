@@ -365,6 +365,83 @@ def pin_draft_permutation(lib):
 
 
 # ---------------------------------------------------------------------------
+# draft round (Sec. 3.1 drafting loop over the Eq. 5 view, recent window slid)
+# ---------------------------------------------------------------------------
+
+def pin_draft_step_first_matches_sdpa(lib):
+    """Before any token is drafted the step is Eq. 5 over the select output:
+    SDPA over exactly those rows."""
+    rng = np.random.default_rng(71)
+    w = _tiny(72, hq=8, hkv=2, ctx=(90, 41), ql=(1, 1), B=24, k_sink=3, k_recent=6)
+    scores = rng.random((2, 2, w.max_ctx))
+    idx, n_idx = oracle.select(w, scores, lib=lib)
+    out = oracle.draft_step(w, idx, w.ctx_len, w.ctx_len, lib=lib)
+    q = _bf16_to_t64(w.q_draft); k = _bf16_to_t64(w.k); v = _bf16_to_t64(w.v)
+    for b in range(2):
+        for h in range(8):
+            c = h // 4
+            I = torch.from_numpy(idx[b, c, :n_idx[b]].astype(np.int64))
+            o = F.scaled_dot_product_attention(q[b, h][None, None, None], k[b, c, I][None, None],
+                                               v[b, c, I][None, None], scale=w.sm_scale)
+            assert np.abs(out[b, h] - o[0, 0, 0].numpy()).max() < 1e-12
+
+
+def pin_draft_step_worked_example(lib):
+    """Hand-worked sets.  T = 20, K_sink = 2, K_recent = 4, budget 9 (K_mid = 3),
+    middle span [2, 16) with the three largest scores at 5, 9, 13: the index set
+    is {0, 1, 5, 9, 13, 16..19}.  After i drafted tokens the recent window is
+    [16 + i, 20 + i).  A second sequence with T = 3 has sink {0, 1}, recent {2}
+    and window [max(2, T + i - 4), T + i): it grows to four positions and then
+    drops position 2.  With K = 0 the attention is uniform and with one-hot V
+    rows (row t = e_t) the output is 1/|S| exactly on the step's set."""
+    w = _tiny(73, hq=2, hkv=1, ctx=(24, 24), ql=(1, 1), B=9, k_sink=2, k_recent=4)
+    scores = np.full((2, 1, 24), 0.1)
+    scores[0, 0, [5, 9, 13]] = [0.9, 0.8, 0.7]
+    idx, n_idx = oracle.select(w, scores, ctx_len=np.array([20, 3]), lib=lib)
+    assert list(idx[0, 0, :n_idx[0]]) == [0, 1, 5, 9, 13, 16, 17, 18, 19]
+    assert list(idx[1, 0, :n_idx[1]]) == [0, 1, 2]
+    k0 = np.zeros_like(w.k)
+    v1 = np.zeros_like(w.v)
+    one = f32_to_bf16_bits(np.float32(1.0))
+    for t in range(24):
+        v1[:, :, t, t] = one
+    expect = {(0, 20): [0, 1, 5, 9, 13, 16, 17, 18, 19],
+              (0, 21): [0, 1, 5, 9, 13, 17, 18, 19, 20],
+              (0, 22): [0, 1, 5, 9, 13, 18, 19, 20, 21],
+              (0, 24): [0, 1, 5, 9, 13, 20, 21, 22, 23],
+              (1, 3): [0, 1, 2], (1, 5): [0, 1, 2, 3, 4], (1, 6): [0, 1, 2, 3, 4, 5],
+              (1, 7): [0, 1, 3, 4, 5, 6]}
+    for cur0, cur1 in ((20, 3), (21, 5), (22, 6), (24, 7)):
+        out = oracle.draft_step(w, idx, [20, 3], [cur0, cur1], k=k0, v=v1, lib=lib)
+        for b, cur in ((0, cur0), (1, cur1)):
+            want = np.zeros(128)
+            S = expect[(b, cur)]
+            want[S] = 1.0 / len(S)
+            for h in range(2):
+                assert np.abs(out[b, h] - want).max() < 1e-15, (b, cur, h)
+    # a drafted tail longer than the recent window, or shorter than T, is rejected
+    for cur in ([25, 3], [19, 3]):
+        try:
+            oracle.draft_step(w, idx, [20, 3], cur, lib=lib)
+        except ValueError:
+            continue
+        raise AssertionError(f"cur_len {cur} accepted")
+
+
+def pin_draft_step_value_one(lib):
+    """Softmax weights sum to one: V = 1 gives 1 at every step of a round."""
+    rng = np.random.default_rng(74)
+    w = _tiny(75, hq=4, hkv=2, ctx=(64, 64), ql=(1, 1), B=20, k_sink=2, k_recent=5)
+    scores = rng.random((2, 2, 64))
+    base = np.array([50, 17], dtype=np.int32)
+    idx, _ = oracle.select(w, scores, ctx_len=base, lib=lib)
+    v1 = np.full_like(w.v, f32_to_bf16_bits(np.float32(1.0)))
+    for i in range(6):
+        o = oracle.draft_step(w, idx, base, base + i, v=v1, lib=lib)
+        assert np.abs(o - 1.0).max() < 1e-12
+
+
+# ---------------------------------------------------------------------------
 # controller (Eq. 6-8)
 # ---------------------------------------------------------------------------
 
@@ -440,4 +517,6 @@ ALL_PINS = [pin_verify_matches_sdpa, pin_verify_value_one, pin_verify_zero_keys_
             pin_verify_planted_key, pin_scores_match_softmax, pin_scores_total_mass,
             pin_scores_permutation, pin_select_lexsort, pin_select_bruteforce_subsets,
             pin_select_special_cases, pin_draft_matches_sdpa, pin_draft_full_equals_dense,
-            pin_draft_permutation, pin_controller_closed_forms, pin_controller_argmax]
+            pin_draft_permutation, pin_draft_step_first_matches_sdpa,
+            pin_draft_step_worked_example, pin_draft_step_value_one,
+            pin_controller_closed_forms, pin_controller_argmax]

@@ -41,6 +41,13 @@ MUTANTS = [
      "const int b = bh / n_q_heads, h = bh % n_q_heads, c = h % n_kv_heads;"),
     ("draft_drops_last_index", "for (int t = 0; t < n; ++t) {\n            double dot",
      "for (int t = 0; t < n - 1; ++t) {\n            double dot"),
+    ("step_window_not_slid", "const int w0 = (cur - k_recent) > r_T ? (cur - k_recent) : r_T;",
+     "const int w0 = r_T;"),
+    ("step_fixed_part_inclusive", "if (I[t] < r_T) S[m_S++] = I[t];", "if (I[t] <= r_T) S[m_S++] = I[t];"),
+    ("step_window_misses_newest", "for (int t = w0; t < cur; ++t) S[m_S++] = t;",
+     "for (int t = w0; t < cur - 1; ++t) S[m_S++] = t;"),
+    ("step_fixed_part_from_cur", "const int r_T = (T - k_recent) > s_end ? (T - k_recent) : s_end;",
+     "const int r_T = (cur - k_recent) > s_end ? (cur - k_recent) : s_end;"),
     ("ema_weights_swapped", "return beta * prev + (1.0 - beta) * observed;",
      "return beta * observed + (1.0 - beta) * prev;"),
     ("accept_prob_inverted", "return ea / (ea + er);", "return er / (ea + er);"),
