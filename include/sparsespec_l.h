@@ -197,6 +197,43 @@ int ssl_draft_attn(const ssl_shape *shape, const ssl_params *params,
                    void *out, void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Draft round (Sec. 3.1: the target model drafts k tokens one after another
+ * over the sparse view of Sec. 3.2 Eq. 5).
+ *
+ * The index set idx[b,c,0..n) was built by ssl_select_topb at
+ * T = ctx_len_host[b] (n = ssl_index_count(T, ...)).  Its sink and TopK part,
+ * F = the entries below r_T = max(T - k_recent, min(k_sink, T)) (the first
+ * n_F = n - (T - r_T) entries), stays for the whole round; the recent window
+ * slides.  After i drafted tokens, cur = cur_len_host[b] = T + i with their
+ * K/V rows written to the cache, a step attends over F and
+ *   W = [max(r_T, cur - k_recent), cur)
+ * (so every drafted token lies in W; the entry count stays n when T is long):
+ *   out[b,h] = softmax_{t in F u W}(sm_scale * q_draft[b,h].k[b,c,t]) . v[b,c,t].
+ * Needs T <= cur <= min(T + k_recent, max_ctx) (else SSL_ERR_SHAPE).
+ *
+ * ssl_draft_materialize copies the rows of F, once per round, to
+ * k_sel / v_sel, caller-owned device buffers of [batch][Hkv][budget][128]
+ * bf16 (row e of (b, c) = cache row idx[b,c,e], e < n_F; other rows are not
+ * written).  ssl_draft_step reads F from them and W from the cache, so a step
+ * loads no index list and gathers nothing.  shape->max_q is not used.  Steps
+ * use a workspace as ssl_draft_attn does (size from
+ * ssl_draft_step_workspace); k_sel / v_sel must not change during a round.
+ * Errors as ssl_draft_attn, plus SSL_ERR_SHAPE for cur_len out of range.
+ */
+int ssl_draft_materialize(const ssl_shape *shape, const ssl_params *params,
+                          const int32_t *ctx_len_host, const void *k_cache,
+                          const void *v_cache, const int32_t *idx, void *k_sel, void *v_sel,
+                          hipStream_t stream);
+int ssl_draft_step_workspace(const ssl_shape *shape, const ssl_params *params,
+                             const int32_t *ctx_len_host, const int32_t *cur_len_host,
+                             size_t *bytes_out);
+int ssl_draft_step(const ssl_shape *shape, const ssl_params *params,
+                   const int32_t *ctx_len_host, const int32_t *cur_len_host,
+                   const void *q_draft, const void *k_cache, const void *v_cache,
+                   const void *k_sel, const void *v_sel, void *out, void *workspace,
+                   size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Adaptive speculation length (Sec. 3.3), host only.
  *
  * State: the class-mean entropies of accepted and rejected drafts, tracked by

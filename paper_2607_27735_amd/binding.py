@@ -36,6 +36,7 @@ EXPORTED = [
     "ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn",
     "ssl_select_workspace", "ssl_select_topb",
     "ssl_draft_workspace", "ssl_draft_attn",
+    "ssl_draft_materialize", "ssl_draft_step_workspace", "ssl_draft_step",
     "ssl_ctrl_create", "ssl_ctrl_destroy", "ssl_ctrl_observe", "ssl_ctrl_accept_prob",
     "ssl_ctrl_choose_k", "ssl_ctrl_get_state", "ssl_ctrl_set_state",
 ]
@@ -89,8 +90,13 @@ def load(path: Optional[str] = None):
     lib.ssl_select_topb.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _sz, _vp]
     lib.ssl_draft_workspace.argtypes = [sp, pp, _i32p, _szp]
     lib.ssl_draft_attn.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+    lib.ssl_draft_materialize.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp]
+    lib.ssl_draft_step_workspace.argtypes = [sp, pp, _i32p, _i32p, _szp]
+    lib.ssl_draft_step.argtypes = [sp, pp, _i32p, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz,
+                                   _vp]
     for f in ("ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn", "ssl_select_workspace",
-              "ssl_select_topb", "ssl_draft_workspace", "ssl_draft_attn"):
+              "ssl_select_topb", "ssl_draft_workspace", "ssl_draft_attn", "ssl_draft_materialize",
+              "ssl_draft_step_workspace", "ssl_draft_step"):
         getattr(lib, f).restype = ctypes.c_int
     lib.ssl_ctrl_create.argtypes = [ctypes.c_double, _i32p, ctypes.c_int32, ctypes.c_int32]
     lib.ssl_ctrl_create.restype = _vp
@@ -300,6 +306,80 @@ def draft_attn(q_draft: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: tor
                                  n_idx.ctypes.data_as(_i32p), _ptr(q_draft), _ptr(k), _ptr(v),
                                  _ptr(idx), _ptr(out), _ptr(workspace), workspace.numel(),
                                  _stream(stream)), "ssl_draft_attn")
+    return out
+
+
+# ---------------------------------------------------------------------------
+# draft round
+# ---------------------------------------------------------------------------
+
+def draft_materialize(k: torch.Tensor, v: torch.Tensor, idx: torch.Tensor, ctx_len_host,
+                      params: Params, k_sel: Optional[torch.Tensor] = None,
+                      v_sel: Optional[torch.Tensor] = None, stream=None):
+    """Copy the sink and TopK rows of the index sets built at ``ctx_len_host``
+    to ``k_sel`` / ``v_sel`` [B, Hkv, budget, 128] bf16 (allocated if None);
+    returns them."""
+    _need_gpu(k, v, idx)
+    if k.dtype != torch.bfloat16 or v.dtype != torch.bfloat16:
+        raise TypeError("k, v must be bfloat16")
+    if idx.dtype != torch.int32:
+        raise TypeError("idx must be int32")
+    batch, hkv, max_ctx, d = k.shape
+    if idx.shape != (batch, hkv, params.budget):
+        raise ValueError("idx must be [batch, n_kv_heads, budget]")
+    shape = Shape(batch, hkv, hkv, d, max_ctx, 1)
+    sel_shape = (batch, hkv, params.budget, d)
+    if k_sel is None:
+        k_sel = torch.empty(sel_shape, dtype=torch.bfloat16, device=k.device)
+    if v_sel is None:
+        v_sel = torch.empty(sel_shape, dtype=torch.bfloat16, device=k.device)
+    if tuple(k_sel.shape) != sel_shape or tuple(v_sel.shape) != sel_shape:
+        raise ValueError("k_sel / v_sel must be [batch, n_kv_heads, budget, 128]")
+    _need_gpu(k_sel, v_sel)
+    ctx = _host_i32(ctx_len_host)
+    _check(load().ssl_draft_materialize(ctypes.byref(shape), ctypes.byref(params),
+                                        ctx.ctypes.data_as(_i32p), _ptr(k), _ptr(v), _ptr(idx),
+                                        _ptr(k_sel), _ptr(v_sel), _stream(stream)),
+           "ssl_draft_materialize")
+    return k_sel, v_sel
+
+
+def draft_step_workspace_bytes(shape: Shape, params: Params, ctx_len_host, cur_len_host) -> int:
+    ctx, cur = _host_i32(ctx_len_host), _host_i32(cur_len_host)
+    n = ctypes.c_size_t(0)
+    _check(load().ssl_draft_step_workspace(ctypes.byref(shape), ctypes.byref(params),
+                                           ctx.ctypes.data_as(_i32p), cur.ctypes.data_as(_i32p),
+                                           ctypes.byref(n)), "ssl_draft_step_workspace")
+    return int(n.value)
+
+
+def draft_step(q_draft: torch.Tensor, k: torch.Tensor, v: torch.Tensor, k_sel: torch.Tensor,
+               v_sel: torch.Tensor, ctx_len_host, cur_len_host, params: Params,
+               out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+               stream=None) -> torch.Tensor:
+    """One draft-round step at lengths ``cur_len_host`` over the materialized
+    rows of the index sets built at ``ctx_len_host`` and the slid recent window."""
+    _need_gpu(q_draft, k, v, k_sel, v_sel)
+    if q_draft.dtype != torch.bfloat16 or k.dtype != torch.bfloat16 or v.dtype != torch.bfloat16:
+        raise TypeError("q_draft, k, v must be bfloat16")
+    batch, hq, d = q_draft.shape
+    _, hkv, max_ctx, _ = k.shape
+    if tuple(k_sel.shape) != (batch, hkv, params.budget, d) or k_sel.shape != v_sel.shape:
+        raise ValueError("k_sel / v_sel must be [batch, n_kv_heads, budget, 128]")
+    shape = Shape(batch, hq, hkv, d, max_ctx, 1)
+    ctx, cur = _host_i32(ctx_len_host), _host_i32(cur_len_host)
+    odt = torch.float32 if params.out_fp32 else torch.bfloat16
+    if out is None:
+        out = torch.zeros(q_draft.shape, dtype=odt, device=q_draft.device)
+    _need_gpu(out)
+    need = draft_step_workspace_bytes(shape, params, ctx, cur)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q_draft.device)
+    _check(load().ssl_draft_step(ctypes.byref(shape), ctypes.byref(params),
+                                 ctx.ctypes.data_as(_i32p), cur.ctypes.data_as(_i32p),
+                                 _ptr(q_draft), _ptr(k), _ptr(v), _ptr(k_sel), _ptr(v_sel),
+                                 _ptr(out), _ptr(workspace), workspace.numel(), _stream(stream)),
+           "ssl_draft_step")
     return out
 
 

@@ -201,6 +201,39 @@ int plan_draft(const ssl_shape* s, const ssl_params* p, const int32_t* n_idx, Dr
     return SSL_OK;
 }
 
+// A draft-round step over the index set built at T = ctx[b]: the sink and
+// TopK entries (n_fixed of them) stay, the recent window slides to end at
+// cur[b].  Entry counts per sequence go to the plan's seq table.
+struct StepPlan {
+    DraftPlan d;
+    int32_t n_fixed[kTableBatch];
+    int32_t win0[kTableBatch];
+    int max_fixed;
+};
+
+int plan_draft_step(const ssl_shape* s, const ssl_params* p, const int32_t* ctx,
+                    const int32_t* cur, StepPlan* plan) {
+    int rc = check_shape(s);
+    if (rc) return rc;
+    rc = check_budget(p);
+    if (rc) return rc;
+    if (!ctx || !cur) return SSL_ERR_NULL;
+    int32_t n_step[kTableBatch];
+    plan->max_fixed = 0;
+    for (int b = 0; b < s->batch; ++b) {
+        const int32_t T = ctx[b], c = cur[b];
+        if (T < 1 || c < T || c > s->max_ctx || (int64_t)c - T > p->k_recent) return SSL_ERR_SHAPE;
+        const int32_t n = ssl_index_count(T, p->k_sink, p->k_recent, p->budget);
+        const int32_t s_end = std::min(p->k_sink, T);
+        const int32_t r_T = std::max(T - p->k_recent, s_end);
+        plan->n_fixed[b] = n - (T - r_T);
+        plan->win0[b] = std::max(r_T, c - p->k_recent);
+        n_step[b] = plan->n_fixed[b] + (c - plan->win0[b]);
+        plan->max_fixed = std::max(plan->max_fixed, plan->n_fixed[b]);
+    }
+    return plan_draft(s, p, n_step, &plan->d);
+}
+
 int check_select(const ssl_shape* s, const ssl_params* p, const int32_t* ctx) {
     int rc = check_shape(s);
     if (rc) return rc;
@@ -420,7 +453,7 @@ int ssl_draft_attn(const ssl_shape* shape, const ssl_params* params, const int32
         return SSL_ERR_ALIGN;
     rc = check_workspace(workspace, workspace_bytes, plan.bytes);
     if (rc) return rc;
-    DraftArgs a;
+    DraftArgs a = {};
     a.q = static_cast<const uint16_t*>(q_draft);
     a.k = static_cast<const uint16_t*>(k_cache);
     a.v = static_cast<const uint16_t*>(v_cache);
@@ -440,6 +473,84 @@ int ssl_draft_attn(const ssl_shape* shape, const ssl_params* params, const int32
     a.scale_log2 = params->sm_scale * 1.4426950408889634f;
     a.seq = plan.seq;
     return launch_draft(a, plan.n_items, stream) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
+}
+
+int ssl_draft_materialize(const ssl_shape* shape, const ssl_params* params,
+                          const int32_t* ctx_len_host, const void* k_cache, const void* v_cache,
+                          const int32_t* idx, void* k_sel, void* v_sel, hipStream_t stream) {
+    StepPlan plan;
+    int rc = plan_draft_step(shape, params, ctx_len_host, ctx_len_host, &plan);
+    if (rc) return rc;
+    if (!k_cache || !v_cache || !idx || !k_sel || !v_sel) return SSL_ERR_NULL;
+    if (!aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(k_sel, 16) ||
+        !aligned(v_sel, 16) || !aligned(idx, 4))
+        return SSL_ERR_ALIGN;
+    DraftArgs a = {};
+    a.k = static_cast<const uint16_t*>(k_cache);
+    a.v = static_cast<const uint16_t*>(v_cache);
+    a.idx = idx;
+    a.k_sel = static_cast<uint16_t*>(k_sel);
+    a.v_sel = static_cast<uint16_t*>(v_sel);
+    a.n_kv_heads = shape->n_kv_heads;
+    a.max_ctx = shape->max_ctx;
+    a.budget = params->budget;
+    for (int b = 0; b < shape->batch; ++b) a.n_fixed[b] = plan.n_fixed[b];
+    return launch_draft_materialize(a, plan.max_fixed, shape->batch * shape->n_kv_heads,
+                                    stream) == hipSuccess
+               ? SSL_OK
+               : SSL_ERR_HIP;
+}
+
+int ssl_draft_step_workspace(const ssl_shape* shape, const ssl_params* params,
+                             const int32_t* ctx_len_host, const int32_t* cur_len_host,
+                             size_t* bytes_out) {
+    if (!bytes_out) return SSL_ERR_NULL;
+    StepPlan plan;
+    const int rc = plan_draft_step(shape, params, ctx_len_host, cur_len_host, &plan);
+    if (rc) return rc;
+    *bytes_out = plan.d.bytes;
+    return SSL_OK;
+}
+
+int ssl_draft_step(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
+                   const int32_t* cur_len_host, const void* q_draft, const void* k_cache,
+                   const void* v_cache, const void* k_sel, const void* v_sel, void* out,
+                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    StepPlan plan;
+    int rc = plan_draft_step(shape, params, ctx_len_host, cur_len_host, &plan);
+    if (rc) return rc;
+    if (!(params->sm_scale > 0.f) || !isfinite(params->sm_scale)) return SSL_ERR_SHAPE;
+    if (!q_draft || !k_cache || !v_cache || !k_sel || !v_sel || !out) return SSL_ERR_NULL;
+    if (!aligned(q_draft, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) ||
+        !aligned(k_sel, 16) || !aligned(v_sel, 16) || !aligned(out, 16))
+        return SSL_ERR_ALIGN;
+    rc = check_workspace(workspace, workspace_bytes, plan.d.bytes);
+    if (rc) return rc;
+    DraftArgs a = {};
+    a.q = static_cast<const uint16_t*>(q_draft);
+    a.k = static_cast<const uint16_t*>(k_cache);
+    a.v = static_cast<const uint16_t*>(v_cache);
+    a.k_sel = const_cast<uint16_t*>(static_cast<const uint16_t*>(k_sel));   // read only here
+    a.v_sel = const_cast<uint16_t*>(static_cast<const uint16_t*>(v_sel));
+    a.part_ml = reinterpret_cast<float2*>(static_cast<char*>(workspace) + plan.d.ml_off);
+    a.part_o = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.d.o_off);
+    a.tag = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + plan.d.tag_off);
+    a.call_tag = next_call_tag();
+    a.out = out;
+    a.n_q_heads = shape->n_q_heads;
+    a.n_kv_heads = shape->n_kv_heads;
+    a.group = shape->n_q_heads / shape->n_kv_heads;
+    a.max_ctx = shape->max_ctx;
+    a.budget = params->budget;
+    a.chunk = plan.d.chunk;
+    a.out_fp32 = params->out_fp32 ? 1 : 0;
+    a.scale_log2 = params->sm_scale * 1.4426950408889634f;
+    a.seq = plan.d.seq;
+    for (int b = 0; b < shape->batch; ++b) {
+        a.n_fixed[b] = plan.n_fixed[b];
+        a.win0[b] = plan.win0[b];
+    }
+    return launch_draft_step(a, plan.d.n_items, stream) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
 }
 
 }  // extern "C"

@@ -11,6 +11,14 @@
 // of its (sequence, KV head), merges all partials in chunk order (its own
 // from LDS) and writes the output.
 //
+// A draft round (Sec. 3.1: k tokens drafted one after another over this view)
+// first copies the sink and TopK rows of every index list into a compact
+// buffer (draft_materialize_kernel); each step then runs the same kernel with
+// entries that name either a row of that buffer or a row of the recent window,
+// which has slid to end at the newest drafted token and is read straight from
+// the cache: no index list to load, and each selected row is gathered once per
+// round instead of once per step.
+//
 // The MFMA layouts are the verify kernel's: K.Q^T on the bf16 MFMA with the
 // keys as A rows, O^T = V^T P^T so a head's softmax state and output stay in
 // the lane that owns the head; V is loaded as whole 256-byte rows per lane
@@ -58,22 +66,42 @@ struct Gathered {
     u32x4 v[8];
 };
 
+// Where the rows of the entries live: the dense cache of the unit, and (draft
+// round steps) the unit's materialized rows.  A row id with kSelBit set is a
+// row of the materialized copy.
+constexpr uint32_t kSelBit = 0x80000000u;
+struct RowSource {
+    const uint16_t* k;
+    const uint16_t* v;
+    const uint16_t* k_sel;
+    const uint16_t* v_sel;
+};
+
+template <bool kRound>
+__device__ __forceinline__ const uint16_t* row_ptr(const uint16_t* cache, const uint16_t* sel,
+                                                   uint32_t row) {
+    if (!kRound) return cache + (size_t)row * kHeadDim;
+    return (row & kSelBit) ? sel + (size_t)(row & ~kSelBit) * kHeadDim
+                           : cache + (size_t)row * kHeadDim;
+}
+
 // Gathers the K and V rows of the 32-key tile starting at chunk position p0.
-// Lane l of the wave holds the cache row of chunk position l in `my_row`;
-// the rows each lane needs are fetched from their owners by lane shuffles.
-__device__ __forceinline__ void gather_tile(int my_row, int p0, const uint16_t* kbase,
-                                            const uint16_t* vbase, int m16, int G, Gathered& t) {
+// Lane l of the wave holds the row id of chunk position l in `my_row`; the
+// rows each lane needs are fetched from their owners by lane shuffles.
+template <bool kRound>
+__device__ __forceinline__ void gather_tile(uint32_t my_row, int p0, const RowSource& src,
+                                            int m16, int G, Gathered& t) {
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-        const int row = __shfl(my_row, p0 + 16 * h + a_row_key(m16), kWave);
-        const uint16_t* p = kbase + (size_t)row * kHeadDim + 8 * G;
+        const uint32_t row = __shfl(my_row, p0 + 16 * h + a_row_key(m16), kWave);
+        const uint16_t* p = row_ptr<kRound>(src.k, src.k_sel, row) + 8 * G;
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) t.k[h][kb] = ld_u32x4(p + 32 * kb);
     }
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-        const int row = __shfl(my_row, p0 + 16 * (e >> 2) + G + 4 * (e & 3), kWave);
-        t.v[e] = ld_u32x4(vbase + (size_t)row * kHeadDim + 8 * m16);
+        const uint32_t row = __shfl(my_row, p0 + 16 * (e >> 2) + G + 4 * (e & 3), kWave);
+        t.v[e] = ld_u32x4(row_ptr<kRound>(src.v, src.v_sel, row) + 8 * m16);
     }
 }
 
@@ -129,6 +157,7 @@ __device__ __forceinline__ void draft_tile(const DraftArgs& a, const u32x4 (&qop
     }
 }
 
+template <bool kRound>
 __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
     const DItem it = decode_ditem(a.seq, blockIdx.x, a.n_kv_heads, a.chunk);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -158,15 +187,22 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
             for (int kb = 0; kb < 4; ++kb) qop[kb] = u32x4{0u, 0u, 0u, 0u};
         }
         const size_t cache_off = (size_t)it.unit * a.max_ctx * kHeadDim;
-        const uint16_t* kbase = a.k + cache_off;
-        const uint16_t* vbase = a.v + cache_off;
-        const int32_t* ib = a.idx + (size_t)it.unit * a.budget;
+        const size_t sel_off = (size_t)it.unit * a.budget * kHeadDim;
+        const RowSource src{a.k + cache_off, a.v + cache_off, a.k_sel + sel_off, a.v_sel + sel_off};
         const int last = it.n - 1;
-        // Lane l loads the cache row of entry l once; every K/V row of the
-        // tile is then requested at once.
-        const int my_row = min(max(ib[min(wbeg + lane, last)], 0), a.max_ctx - 1);
+        const int e = min(wbeg + lane, last);
+        // Lane l finds the row of entry l once; every K/V row of the tile is
+        // then requested at once.
+        uint32_t my_row;
+        if (!kRound) {
+            my_row = (uint32_t)min(max(a.idx[(size_t)it.unit * a.budget + e], 0), a.max_ctx - 1);
+        } else {
+            const int nf = a.n_fixed[it.b];
+            my_row = e < nf ? (uint32_t)e | kSelBit
+                            : (uint32_t)min(max(a.win0[it.b] + e - nf, 0), a.max_ctx - 1);
+        }
         Gathered ta;
-        gather_tile(my_row, 0, kbase, vbase, m16, G, ta);
+        gather_tile<kRound>(my_row, 0, src, m16, G, ta);
         draft_tile(a, qop, ta, wbeg, wend, G, M, L, oacc);
         L += shfl_xor_f(L, 16);
         L += shfl_xor_f(L, 32);
@@ -298,10 +334,54 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
     }
 }
 
+// Materialization for a draft round: workgroup (x, u) copies rows
+// 32x .. 32x + 31 of unit u's sink and TopK entries (the first n_fixed[b]
+// entries of its index list) from the cache to k_sel/v_sel.  Thread t moves
+// 16 bytes of two rows of K and of V, all four loads in flight together.
+constexpr int kMatRows = 32;
+__global__ __launch_bounds__(kDraftThreads) void draft_materialize_kernel(DraftArgs a) {
+    const int u = blockIdx.y, b = u / a.n_kv_heads;
+    const int nf = a.n_fixed[b];
+    const int q = threadIdx.x & 15, r = threadIdx.x >> 4;   // 16 rows per pass
+    const int32_t* ib = a.idx + (size_t)u * a.budget;
+    const size_t cache_off = (size_t)u * a.max_ctx * kHeadDim;
+    const size_t sel_off = (size_t)u * a.budget * kHeadDim;
+    int e[2];
+    u32x4 kk[2], vv[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        e[j] = blockIdx.x * kMatRows + 16 * j + r;
+        const int row = min(max(ib[min(e[j], max(nf - 1, 0))], 0), a.max_ctx - 1);
+        kk[j] = ld_u32x4(a.k + cache_off + (size_t)row * kHeadDim + 8 * q);
+        vv[j] = ld_u32x4(a.v + cache_off + (size_t)row * kHeadDim + 8 * q);
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        if (e[j] < nf) {
+            *reinterpret_cast<u32x4*>(a.k_sel + sel_off + (size_t)e[j] * kHeadDim + 8 * q) = kk[j];
+            *reinterpret_cast<u32x4*>(a.v_sel + sel_off + (size_t)e[j] * kHeadDim + 8 * q) = vv[j];
+        }
+    }
+}
+
 }  // namespace
 
 hipError_t launch_draft(const DraftArgs& a, int n_items, hipStream_t stream) {
-    hipLaunchKernelGGL(draft_kernel, dim3(n_items), dim3(kDraftThreads), 0, stream, a);
+    hipLaunchKernelGGL(draft_kernel<false>, dim3(n_items), dim3(kDraftThreads), 0, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_draft_step(const DraftArgs& a, int n_items, hipStream_t stream) {
+    hipLaunchKernelGGL(draft_kernel<true>, dim3(n_items), dim3(kDraftThreads), 0, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_draft_materialize(const DraftArgs& a, int max_fixed, int n_units,
+                                    hipStream_t stream) {
+    const int blocks = (max_fixed + kMatRows - 1) / kMatRows;
+    if (blocks < 1 || n_units < 1) return hipSuccess;
+    hipLaunchKernelGGL(draft_materialize_kernel, dim3(blocks, n_units), dim3(kDraftThreads), 0,
+                       stream, a);
     return hipGetLastError();
 }
 

@@ -73,7 +73,14 @@ struct DraftArgs {
     void* out;              // [batch][n_q][128]
     int32_t n_q_heads, n_kv_heads, group, max_ctx, budget, chunk, out_fp32;
     float scale_log2;
-    SeqTable seq;           // ctx[] holds n_idx per sequence
+    SeqTable seq;           // ctx[] holds the entry count per sequence
+    // Draft-round step only: entry e < n_fixed[b] is row e of k_sel/v_sel
+    // ([batch][n_kv][budget][128], the materialized sink and TopK rows);
+    // entry e >= n_fixed[b] is cache row win0[b] + e - n_fixed[b].
+    uint16_t* k_sel;        // written by the materialization, read by the steps
+    uint16_t* v_sel;
+    int32_t n_fixed[kTableBatch];
+    int32_t win0[kTableBatch];
 };
 
 // Single-sweep verify: the slots (items of v.seq / v.chunk) of one KV-head
@@ -101,5 +108,11 @@ int select_part_len(int max_t);
 hipError_t launch_select(const SelectArgs& a, int n_units, hipStream_t stream);
 // One workgroup per `chunk` (128) index entries; no combine kernel.
 hipError_t launch_draft(const DraftArgs& a, int n_items, hipStream_t stream);
+// Draft round: copy the sink and TopK rows (n_fixed per sequence) of every
+// (sequence, KV head) to k_sel/v_sel; then any number of steps over them and
+// the slid recent window.
+hipError_t launch_draft_materialize(const DraftArgs& a, int max_fixed, int n_units,
+                                    hipStream_t stream);
+hipError_t launch_draft_step(const DraftArgs& a, int n_items, hipStream_t stream);
 
 }  // namespace ssl

@@ -185,6 +185,49 @@ def test_draft_validation(lib):
     assert _draft(lib, ws_bytes=8) == B.SSL_ERR_WORKSPACE
 
 
+def _step(lib, shape=None, params=None, ctx=(4000,), cur=(4003,), q=FAKE, k=FAKE, v=FAKE,
+          ks=FAKE, vs=FAKE, out=FAKE, ws=FAKE, ws_bytes=1 << 40):
+    shape = shape or _shape(batch=len(ctx))
+    params = params or _params()
+    ca, cp = _i32(*ctx)
+    ua, up = _i32(*cur)
+    return lib.ssl_draft_step(ctypes.byref(shape), ctypes.byref(params), cp, up, q, k, v, ks, vs,
+                              out, ws, ws_bytes, None)
+
+
+def test_draft_round_validation(lib):
+    # the drafted tail must lie in the recent window: T <= cur <= T + k_recent, cur <= max_ctx
+    assert _step(lib, cur=(3999,)) == B.SSL_ERR_SHAPE
+    assert _step(lib, cur=(4033,)) == B.SSL_ERR_SHAPE
+    assert _step(lib, ctx=(4090,), cur=(4097,)) == B.SSL_ERR_SHAPE
+    assert _step(lib, ctx=(0,), cur=(0,)) == B.SSL_ERR_SHAPE
+    assert _step(lib, params=_params(k_recent=0), cur=(4001,)) == B.SSL_ERR_SHAPE
+    assert _step(lib, params=_params(budget=10)) == B.SSL_ERR_BUDGET
+    assert _step(lib, shape=_shape(n_q_heads=34, n_kv_heads=2)) == B.SSL_ERR_UNSUPPORTED
+    for name in ("q", "k", "v", "ks", "vs", "out"):
+        assert _step(lib, **{name: None}) == B.SSL_ERR_NULL
+        assert _step(lib, **{name: FAKE_ODD}) == B.SSL_ERR_ALIGN
+    assert _step(lib, ws=None) == B.SSL_ERR_WORKSPACE
+    assert _step(lib, ws_bytes=8) == B.SSL_ERR_WORKSPACE
+    # the workspace covers the step's entries, the same count as the draft's
+    s, p = _shape(), _params()
+    n1, n2 = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    ca, cp = _i32(4000)
+    ua, up = _i32(4020)
+    na, npp = _i32(B.index_count(4000, p.k_sink, p.k_recent, p.budget))
+    assert lib.ssl_draft_step_workspace(ctypes.byref(s), ctypes.byref(p), cp, up, ctypes.byref(n1)) == 0
+    assert lib.ssl_draft_workspace(ctypes.byref(s), ctypes.byref(p), npp, ctypes.byref(n2)) == 0
+    assert n1.value == n2.value > 0
+    # materialization: the same length checks, and its buffers are required
+    assert lib.ssl_draft_materialize(ctypes.byref(s), ctypes.byref(p), cp, FAKE, FAKE, FAKE,
+                                     None, FAKE, None) == B.SSL_ERR_NULL
+    assert lib.ssl_draft_materialize(ctypes.byref(s), ctypes.byref(p), cp, FAKE, FAKE, FAKE,
+                                     FAKE_ODD, FAKE, None) == B.SSL_ERR_ALIGN
+    za, zp = _i32(0)
+    assert lib.ssl_draft_materialize(ctypes.byref(s), ctypes.byref(p), zp, FAKE, FAKE, FAKE,
+                                     FAKE, FAKE, None) == B.SSL_ERR_SHAPE
+
+
 def test_status_strings(lib):
     seen = set()
     for code in range(0, -8, -1):

@@ -1,0 +1,125 @@
+"""GPU parity of the draft round against the oracle: the sink and TopK rows of
+the oracle's index sets are materialized once, then each step attends over them
+and the recent window slid to end at the newest drafted token.  The drafted
+tokens' K/V rows are cache rows past the base length (the generator fills them
+like every other row); the padding past the last step's length holds NaN and
+must never be read.  Every step's query is a new seeded draw."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_common import abs_v, check_outputs, dev_bf16, params_of
+from paper_2607_27735_amd import binding as B
+from paper_2607_27735_amd.workloads import f32_to_bf16_bits, generate, make_config
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU visible", allow_module_level=True)
+
+NAN_BF16 = np.uint16(0x7FC0)
+
+
+def _case(name):
+    """(workload, base lengths, drafted steps)."""
+    if name == "headline-8b-T32K":
+        # the 32K workload; its last six positions play the drafted tokens
+        w = make_config(2)
+        return w, w.ctx_len - 6, 6
+    spec = {
+        "small-b2": dict(seed=201, batch=2, n_q_heads=8, n_kv_heads=2, base=[3000, 700], steps=6,
+                         budget=300, k_sink=4, k_recent=32),
+        "tiny-T": dict(seed=202, batch=4, n_q_heads=8, n_kv_heads=2, base=[1, 5, 17, 33],
+                       steps=8, budget=16, k_sink=4, k_recent=8),
+        "g16": dict(seed=203, batch=2, n_q_heads=32, n_kv_heads=2, base=[513, 129], steps=5,
+                    budget=200, k_sink=4, k_recent=32),
+        "window-only": dict(seed=204, batch=1, n_q_heads=8, n_kv_heads=2, base=[100], steps=16,
+                            budget=16, k_sink=0, k_recent=16),
+        "kv8-ragged": dict(seed=205, batch=3, n_q_heads=32, n_kv_heads=8, base=[2049, 333, 1000],
+                           steps=7, budget=256, k_sink=4, k_recent=32),
+    }[name]
+    base = np.array(spec["base"], dtype=np.int32)
+    steps = spec["steps"]
+    w = generate(spec["seed"], name=name, batch=spec["batch"], n_q_heads=spec["n_q_heads"],
+                 n_kv_heads=spec["n_kv_heads"], ctx_len=list(base + steps),
+                 q_len=[1] * spec["batch"], max_ctx=int(base.max()) + steps + 4,
+                 budget=spec["budget"], k_sink=spec["k_sink"], k_recent=spec["k_recent"])
+    for b in range(w.batch):
+        w.k[b, :, base[b] + steps:] = NAN_BF16
+        w.v[b, :, base[b] + steps:] = NAN_BF16
+    return w, base, steps
+
+
+NAMES = ["small-b2", "tiny-T", "g16", "window-only", "kv8-ragged", "headline-8b-T32K"]
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_draft_round_matches_oracle(name):
+    w, base, steps = _case(name)
+    print(f"[draft round] {name}: batch {w.batch}, {w.n_q_heads}/{w.n_kv_heads} heads, "
+          f"base {list(base)}, {steps} steps, budget {w.budget}", flush=True)
+    rng = np.random.default_rng(int(base.sum()) + steps)
+    scores = rng.random((w.batch, w.n_kv_heads, w.max_ctx))
+    idx, n_idx = oracle.select(w, scores, ctx_len=base)
+    p = params_of(w)
+    k, v = dev_bf16(w.k), dev_bf16(w.v)
+    idx_d = torch.from_numpy(np.ascontiguousarray(idx)).cuda()
+    k_sel, v_sel = B.draft_materialize(k, v, idx_d, base, p)
+    torch.cuda.synchronize()
+    # the materialized rows are the cache rows of the sink and TopK entries, bit for bit
+    ks, vs = k_sel.view(torch.int16).cpu().numpy(), v_sel.view(torch.int16).cpu().numpy()
+    kc, vc = w.k.view(np.int16), w.v.view(np.int16)
+    for b in range(w.batch):
+        T = int(base[b])
+        r_T = max(T - w.k_recent, min(w.k_sink, T))
+        nf = int(n_idx[b]) - (T - r_T)
+        for c in range(w.n_kv_heads):
+            rows = idx[b, c, :nf]
+            assert np.all(rows < r_T)
+            assert np.array_equal(ks[b, c, :nf], kc[b, c, rows])
+            assert np.array_equal(vs[b, c, :nf], vc[b, c, rows])
+    worst = 0.0
+    for i in range(steps + 1):
+        qb = f32_to_bf16_bits(rng.standard_normal(w.q_draft.shape).astype(np.float32))
+        cur = base + i
+        o_ref = oracle.draft_step(w, idx, base, cur, q_draft=qb)
+        oabs = oracle.draft_step(w, idx, base, cur, q_draft=qb, v=abs_v(w))
+        o = B.draft_step(dev_bf16(qb), k, v, k_sel, v_sel, base, cur, p)
+        torch.cuda.synchronize()
+        o = o.float().cpu().numpy().astype(np.float64)
+        worst = max(worst, check_outputs(o, o_ref, oabs, np.ones(o_ref.shape[:2], dtype=bool),
+                                         what=f"draft step {i}"))
+        if i == 0:   # before any drafted token the step is the plain draft over idx
+            o0 = B.draft_attn(dev_bf16(qb), k, v, idx_d, n_idx, p)
+            torch.cuda.synchronize()
+            assert np.array_equal(o0.float().cpu().numpy(), o.astype(np.float32))
+    print(f"  worst max|dO| over the round = {worst:.2e}")
+
+
+def test_draft_round_bf16_outputs():
+    w, base, steps = _case("small-b2")
+    rng = np.random.default_rng(7)
+    scores = rng.random((w.batch, w.n_kv_heads, w.max_ctx))
+    idx, _ = oracle.select(w, scores, ctx_len=base)
+    p = params_of(w, out_fp32=False)
+    k, v = dev_bf16(w.k), dev_bf16(w.v)
+    k_sel, v_sel = B.draft_materialize(k, v, torch.from_numpy(idx).cuda(), base, p)
+    for i in (0, 3, steps):
+        o_ref = oracle.draft_step(w, idx, base, base + i)
+        oabs = oracle.draft_step(w, idx, base, base + i, v=abs_v(w))
+        o = B.draft_step(dev_bf16(w.q_draft), k, v, k_sel, v_sel, base, base + i, p)
+        torch.cuda.synchronize()
+        check_outputs(o.float().cpu().numpy().astype(np.float64), o_ref, oabs,
+                      np.ones(o_ref.shape[:2], dtype=bool), out_fp32=False, what=f"bf16 step {i}")
+
+
+def test_draft_round_rejects_long_tail():
+    w, base, steps = _case("small-b2")
+    p = params_of(w)
+    k, v = dev_bf16(w.k), dev_bf16(w.v)
+    sel = torch.zeros((w.batch, w.n_kv_heads, w.budget, 128), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(B.SSLError):
+        B.draft_step(dev_bf16(w.q_draft), k, v, sel, sel, base, base + w.k_recent + 1, p)
+    with pytest.raises(B.SSLError):
+        B.draft_step(dev_bf16(w.q_draft), k, v, sel, sel, base, base - 1, p)
