@@ -47,7 +47,8 @@ REPO = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(REPO, "profiles", "verify_traffic_llama8b_T32K.txt")
 OUR_KERNELS = ("verify_fused_kernel", "verify_stats_kernel", "verify_main_kernel",
                "verify_combine_kernel", "select_hist_kernel", "select_mark_kernel",
-               "select_finish_kernel", "select_fused_kernel", "draft_kernel")
+               "select_finish_kernel", "select_fused_kernel", "draft_materialize_kernel",
+               "draft_kernel")
 VERIFY_KERNELS = ("verify_fused_kernel", "verify_stats_kernel", "verify_main_kernel",
                   "verify_combine_kernel")
 
@@ -86,12 +87,87 @@ def summarize_trace(d: str, command: str) -> str:
                    f"| {float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} |")
     per_call = {}
     for r in rows:
-        k = kernel_short(r["Name"]).split("<")[0]
-        call = "verify" if k.startswith("verify") else "select" if k.startswith("select") else "draft"
+        short = kernel_short(r["Name"])
+        k = short.split("<")[0]
+        call = ("verify" if k.startswith("verify") else "select" if k.startswith("select")
+                else "draft round materialize" if "materialize" in k
+                else "draft round step (index list)" if short == "draft_kernel<1>"
+                else "draft round step (materialized rows)" if short == "draft_kernel<2>"
+                else "draft")
         per_call[call] = per_call.get(call, 0.0) + float(r["AverageNs"]) / 1e3
     out += ["", "sum of kernel averages per call: " +
             ", ".join(f"{c} {v:.2f} us" for c, v in per_call.items())]
     return "\n".join(out) + "\n"
+
+
+def draft_round_bench(B, w, kvs, qd, params, scores, stream, reps, torch, np):
+    """A draft round on the workload (next to the headline, not part of it):
+    the index sets are built at T - k (k = max q_len - 1, at most K_recent),
+    so that the last k cached positions play the drafted tokens; then one
+    materialization and the steps at lengths T - k + i, each timed as
+    ``reps`` back-to-back calls (rotating the KV copies and their own
+    materialized rows) between two HIP events, beside the plain draft call
+    over the same index lists."""
+    k = max(1, min(int(max(w.q_len)) - 1, w.k_recent))
+    base = np.maximum(w.ctx_len - k, 1).astype(np.int32)
+    dev = qd.device
+    idx = torch.zeros((w.batch, w.n_kv_heads, w.budget), dtype=torch.int32, device=dev)
+    n_idx = torch.zeros(w.batch, dtype=torch.int32, device=dev)
+    B.select_topb(scores, base, params, n_q_heads=w.n_q_heads, idx=idx, n_idx=n_idx,
+                  stream=stream)
+    n_host = [B.index_count(int(t), w.k_sink, w.k_recent, w.budget) for t in base]
+    out = torch.empty(qd.shape, dtype=torch.bfloat16, device=dev)
+    sel_shape = (w.batch, w.n_kv_heads, w.budget, w.head_dim)
+    rounds = [B.PreparedRound(qd, kk, vv, idx, base, k, params, out, stream=stream)
+              for (kk, vv) in kvs]
+    mats = [B.PreparedRound(qd, kk, vv, idx, base, k, params, out,
+                            k_sel=torch.empty(sel_shape, dtype=torch.bfloat16, device=dev),
+                            v_sel=torch.empty(sel_shape, dtype=torch.bfloat16, device=dev),
+                            stream=stream) for (kk, vv) in kvs]
+    n = len(rounds)
+    dshape = B.Shape(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.max_ctx, 1)
+    dws = torch.empty(max(B.draft_workspace_bytes(dshape, params, n_host), 1), dtype=torch.uint8,
+                      device=dev)
+
+    def timed(fn):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for r in range(n):
+            fn(r)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for r in range(reps):
+            fn(r)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    step_us = [timed(lambda r, i=i: rounds[r % n].step(i)) for i in range(k)]
+    mat_us = timed(lambda r: mats[r % n].materialize())
+    mstep_us = [timed(lambda r, i=i: mats[r % n].step(i)) for i in range(k)]
+    # the plain draft call, prepared like the round's calls (one ctypes call each)
+    import ctypes
+    lib = B.load()
+    n_arr = np.array(n_host, dtype=np.int32)
+    dargs = [(ctypes.byref(dshape), ctypes.byref(params), n_arr.ctypes.data_as(B._i32p),
+              qd.data_ptr(), kk.data_ptr(), vv.data_ptr(), idx.data_ptr(), out.data_ptr(),
+              dws.data_ptr(), dws.numel(), B._stream(stream)) for (kk, vv) in kvs]
+    for a in dargs:
+        B._check(lib.ssl_draft_attn(*a), "ssl_draft_attn")
+    draft_us = timed(lambda r: lib.ssl_draft_attn(*dargs[r % n]))
+    entries = sum(n_host) * w.n_kv_heads
+    step_bytes = entries * (w.head_dim * 2 * 2) + w.batch * w.n_q_heads * w.head_dim * 4
+    mean_step = statistics.fmean(step_us)
+    return {"k": k, "base_len": list(map(int, base)),
+            "step_us": [round(x, 3) for x in step_us], "step_us_mean": round(mean_step, 3),
+            "round_us": round(sum(step_us), 3),
+            "plain_draft_us": round(draft_us, 3),
+            "materialize_us": round(mat_us, 3),
+            "materialized_step_us_mean": round(statistics.fmean(mstep_us), 3),
+            "materialized_round_us": round(mat_us + sum(mstep_us), 3),
+            "step_alg_bytes": step_bytes,
+            "step_gbps": round(step_bytes / (mean_step * 1e-6) / 1e9, 1),
+            "timing": f"{reps} back-to-back calls per figure between two HIP events, "
+                      f"rotating {n} KV copies"}
 
 
 def summarize_traffic(fetch_dir: str, write_dir: str, copy_mib: int, command: str) -> str:
@@ -184,6 +260,8 @@ def main() -> int:
     ap.add_argument("--workload", type=int, default=2, help="named workload 1..5 (default 2)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-draft-round", action="store_true",
+                    help="skip the draft-round measurement printed beside the headline")
     ap.add_argument("--mode", choices=["eager", "graph"], default="eager")
     ap.add_argument("--verify-mode", choices=["auto", "two-sweep", "one-sweep"], default="auto")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -382,6 +460,9 @@ def main() -> int:
                      "timing": "K back-to-back verify calls between two HIP events on the launch stream"},
         "kernels": kernels,
     }
+    if not args.no_draft_round:
+        result["draft_round"] = draft_round_bench(B, w, kvs, qd, params, scores, stream,
+                                                  args.steps, torch, np)
     # sanity: score mass of every KV head equals min(W, q) * group
     s = scores.double().sum(dim=2).cpu().numpy()
     want = np.array([min(w.window, int(x)) * w.group for x in w.q_len])[:, None]

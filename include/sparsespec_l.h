@@ -211,14 +211,14 @@ int ssl_draft_attn(const ssl_shape *shape, const ssl_params *params,
  *   out[b,h] = softmax_{t in F u W}(sm_scale * q_draft[b,h].k[b,c,t]) . v[b,c,t].
  * Needs T <= cur <= min(T + k_recent, max_ctx) (else SSL_ERR_SHAPE).
  *
- * ssl_draft_materialize copies the rows of F, once per round, to
- * k_sel / v_sel, caller-owned device buffers of [batch][Hkv][budget][128]
- * bf16 (row e of (b, c) = cache row idx[b,c,e], e < n_F; other rows are not
- * written).  ssl_draft_step reads F from them and W from the cache, so a step
- * loads no index list and gathers nothing.  shape->max_q is not used.  Steps
- * use a workspace as ssl_draft_attn does (size from
- * ssl_draft_step_workspace); k_sel / v_sel must not change during a round.
- * Errors as ssl_draft_attn, plus SSL_ERR_SHAPE for cur_len out of range.
+ * ssl_draft_step reads W from the cache and F either through idx (k_sel and
+ * v_sel NULL) or from k_sel / v_sel (idx may then be NULL): caller-owned
+ * device buffers of [batch][Hkv][budget][128] bf16 that ssl_draft_materialize
+ * fills once per round (row e of (b, c) = cache row idx[b,c,e], e < n_F;
+ * other rows are not written).  shape->max_q is not used.  Steps use a
+ * workspace as ssl_draft_attn does (size from ssl_draft_step_workspace); idx,
+ * k_sel and v_sel must not change during a round.  Errors as ssl_draft_attn,
+ * plus SSL_ERR_SHAPE for cur_len out of range.
  */
 int ssl_draft_materialize(const ssl_shape *shape, const ssl_params *params,
                           const int32_t *ctx_len_host, const void *k_cache,
@@ -230,8 +230,8 @@ int ssl_draft_step_workspace(const ssl_shape *shape, const ssl_params *params,
 int ssl_draft_step(const ssl_shape *shape, const ssl_params *params,
                    const int32_t *ctx_len_host, const int32_t *cur_len_host,
                    const void *q_draft, const void *k_cache, const void *v_cache,
-                   const void *k_sel, const void *v_sel, void *out, void *workspace,
-                   size_t workspace_bytes, hipStream_t stream);
+                   const int32_t *idx, const void *k_sel, const void *v_sel, void *out,
+                   void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Adaptive speculation length (Sec. 3.3), host only.

@@ -92,8 +92,8 @@ def load(path: Optional[str] = None):
     lib.ssl_draft_attn.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
     lib.ssl_draft_materialize.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp]
     lib.ssl_draft_step_workspace.argtypes = [sp, pp, _i32p, _i32p, _szp]
-    lib.ssl_draft_step.argtypes = [sp, pp, _i32p, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz,
-                                   _vp]
+    lib.ssl_draft_step.argtypes = [sp, pp, _i32p, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                   _sz, _vp]
     for f in ("ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn", "ssl_select_workspace",
               "ssl_select_topb", "ssl_draft_workspace", "ssl_draft_attn", "ssl_draft_materialize",
               "ssl_draft_step_workspace", "ssl_draft_step"):
@@ -353,19 +353,31 @@ def draft_step_workspace_bytes(shape: Shape, params: Params, ctx_len_host, cur_l
     return int(n.value)
 
 
-def draft_step(q_draft: torch.Tensor, k: torch.Tensor, v: torch.Tensor, k_sel: torch.Tensor,
-               v_sel: torch.Tensor, ctx_len_host, cur_len_host, params: Params,
+def draft_step(q_draft: torch.Tensor, k: torch.Tensor, v: torch.Tensor, ctx_len_host,
+               cur_len_host, params: Params, idx: Optional[torch.Tensor] = None,
+               k_sel: Optional[torch.Tensor] = None, v_sel: Optional[torch.Tensor] = None,
                out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
                stream=None) -> torch.Tensor:
-    """One draft-round step at lengths ``cur_len_host`` over the materialized
-    rows of the index sets built at ``ctx_len_host`` and the slid recent window."""
-    _need_gpu(q_draft, k, v, k_sel, v_sel)
+    """One draft-round step at lengths ``cur_len_host`` over the sink and TopK
+    rows of the index sets built at ``ctx_len_host`` (through ``idx``, or the
+    materialized ``k_sel`` / ``v_sel``) and the slid recent window."""
+    _need_gpu(q_draft, k, v)
     if q_draft.dtype != torch.bfloat16 or k.dtype != torch.bfloat16 or v.dtype != torch.bfloat16:
         raise TypeError("q_draft, k, v must be bfloat16")
     batch, hq, d = q_draft.shape
     _, hkv, max_ctx, _ = k.shape
-    if tuple(k_sel.shape) != (batch, hkv, params.budget, d) or k_sel.shape != v_sel.shape:
-        raise ValueError("k_sel / v_sel must be [batch, n_kv_heads, budget, 128]")
+    if k_sel is not None or v_sel is not None:
+        if k_sel is None or v_sel is None:
+            raise ValueError("give both k_sel and v_sel, or neither")
+        _need_gpu(k_sel, v_sel)
+        if tuple(k_sel.shape) != (batch, hkv, params.budget, d) or k_sel.shape != v_sel.shape:
+            raise ValueError("k_sel / v_sel must be [batch, n_kv_heads, budget, 128]")
+    else:
+        if idx is None:
+            raise ValueError("idx is needed when no materialized rows are given")
+        _need_gpu(idx)
+        if idx.shape != (batch, hkv, params.budget) or idx.dtype != torch.int32:
+            raise ValueError("idx must be int32 [batch, n_kv_heads, budget]")
     shape = Shape(batch, hq, hkv, d, max_ctx, 1)
     ctx, cur = _host_i32(ctx_len_host), _host_i32(cur_len_host)
     odt = torch.float32 if params.out_fp32 else torch.bfloat16
@@ -377,8 +389,9 @@ def draft_step(q_draft: torch.Tensor, k: torch.Tensor, v: torch.Tensor, k_sel: t
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q_draft.device)
     _check(load().ssl_draft_step(ctypes.byref(shape), ctypes.byref(params),
                                  ctx.ctypes.data_as(_i32p), cur.ctypes.data_as(_i32p),
-                                 _ptr(q_draft), _ptr(k), _ptr(v), _ptr(k_sel), _ptr(v_sel),
-                                 _ptr(out), _ptr(workspace), workspace.numel(), _stream(stream)),
+                                 _ptr(q_draft), _ptr(k), _ptr(v), _ptr(idx), _ptr(k_sel),
+                                 _ptr(v_sel), _ptr(out), _ptr(workspace), workspace.numel(),
+                                 _stream(stream)),
            "ssl_draft_step")
     return out
 
@@ -491,3 +504,46 @@ class PreparedStep:
         self.verify()
         self.select()
         self.draft()
+
+
+class PreparedRound:
+    """A draft round over fixed device buffers: ``step(i)`` for i = 0 .. k_max
+    drafted tokens (lengths base_len + i), its fixed rows through ``idx`` or,
+    when ``k_sel`` / ``v_sel`` are given, from the copy ``materialize()`` makes
+    once per round.  The argument structures are built once, so each call is
+    one ctypes call on the stream given (default: torch's current stream at
+    construction)."""
+
+    def __init__(self, q_draft, k, v, idx, base_len, k_max: int, params: Params, out,
+                 k_sel=None, v_sel=None, stream=None):
+        self._lib = load()
+        _need_gpu(q_draft, k, v, idx, out)
+        sel = k_sel is not None
+        if sel:
+            _need_gpu(k_sel, v_sel)
+        batch, hq, d = q_draft.shape
+        _, hkv, max_ctx, _ = k.shape
+        self.shape = Shape(batch, hq, hkv, d, max_ctx, 1)
+        self.params = params
+        self.base = _host_i32(base_len)
+        self.curs = [_host_i32(self.base + i) for i in range(k_max + 1)]
+        need = max(draft_step_workspace_bytes(self.shape, params, self.base, c) for c in self.curs)
+        self.ws = torch.empty(max(need, 1), dtype=torch.uint8, device=q_draft.device)
+        self.tensors = (q_draft, k, v, idx, k_sel, v_sel, out)
+        self.stream = _stream(stream)
+        sp, pp = ctypes.byref(self.shape), ctypes.byref(params)
+        bp = self.base.ctypes.data_as(_i32p)
+        ks, vs = (k_sel.data_ptr(), v_sel.data_ptr()) if sel else (None, None)
+        self._m = (sp, pp, bp, k.data_ptr(), v.data_ptr(), idx.data_ptr(), ks, vs,
+                   self.stream) if sel else None
+        self._steps = [(sp, pp, bp, c.ctypes.data_as(_i32p), q_draft.data_ptr(), k.data_ptr(),
+                        v.data_ptr(), idx.data_ptr(), ks, vs, out.data_ptr(), self.ws.data_ptr(),
+                        self.ws.numel(), self.stream) for c in self.curs]
+
+    def materialize(self) -> None:
+        if self._m is None:
+            raise ValueError("this round reads its fixed rows through idx")
+        _check(self._lib.ssl_draft_materialize(*self._m), "ssl_draft_materialize")
+
+    def step(self, i: int) -> None:
+        _check(self._lib.ssl_draft_step(*self._steps[i]), "ssl_draft_step")

@@ -514,15 +514,18 @@ int ssl_draft_step_workspace(const ssl_shape* shape, const ssl_params* params,
 
 int ssl_draft_step(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
                    const int32_t* cur_len_host, const void* q_draft, const void* k_cache,
-                   const void* v_cache, const void* k_sel, const void* v_sel, void* out,
-                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                   const void* v_cache, const int32_t* idx, const void* k_sel, const void* v_sel,
+                   void* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
     StepPlan plan;
     int rc = plan_draft_step(shape, params, ctx_len_host, cur_len_host, &plan);
     if (rc) return rc;
     if (!(params->sm_scale > 0.f) || !isfinite(params->sm_scale)) return SSL_ERR_SHAPE;
-    if (!q_draft || !k_cache || !v_cache || !k_sel || !v_sel || !out) return SSL_ERR_NULL;
+    const bool sel = k_sel || v_sel;
+    if (!q_draft || !k_cache || !v_cache || !out) return SSL_ERR_NULL;
+    if (sel ? (!k_sel || !v_sel) : !idx) return SSL_ERR_NULL;
     if (!aligned(q_draft, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) ||
-        !aligned(k_sel, 16) || !aligned(v_sel, 16) || !aligned(out, 16))
+        !aligned(out, 16) || (sel && (!aligned(k_sel, 16) || !aligned(v_sel, 16))) ||
+        (!sel && !aligned(idx, 4)))
         return SSL_ERR_ALIGN;
     rc = check_workspace(workspace, workspace_bytes, plan.d.bytes);
     if (rc) return rc;
@@ -530,8 +533,9 @@ int ssl_draft_step(const ssl_shape* shape, const ssl_params* params, const int32
     a.q = static_cast<const uint16_t*>(q_draft);
     a.k = static_cast<const uint16_t*>(k_cache);
     a.v = static_cast<const uint16_t*>(v_cache);
-    a.k_sel = const_cast<uint16_t*>(static_cast<const uint16_t*>(k_sel));   // read only here
-    a.v_sel = const_cast<uint16_t*>(static_cast<const uint16_t*>(v_sel));
+    a.idx = sel ? nullptr : idx;
+    a.k_sel = sel ? const_cast<uint16_t*>(static_cast<const uint16_t*>(k_sel)) : nullptr;   // read only here
+    a.v_sel = sel ? const_cast<uint16_t*>(static_cast<const uint16_t*>(v_sel)) : nullptr;
     a.part_ml = reinterpret_cast<float2*>(static_cast<char*>(workspace) + plan.d.ml_off);
     a.part_o = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.d.o_off);
     a.tag = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + plan.d.tag_off);

@@ -12,12 +12,10 @@
 // from LDS) and writes the output.
 //
 // A draft round (Sec. 3.1: k tokens drafted one after another over this view)
-// first copies the sink and TopK rows of every index list into a compact
-// buffer (draft_materialize_kernel); each step then runs the same kernel with
-// entries that name either a row of that buffer or a row of the recent window,
-// which has slid to end at the newest drafted token and is read straight from
-// the cache: no index list to load, and each selected row is gathered once per
-// round instead of once per step.
+// runs the same kernel per step with entries that name either a fixed row (sink
+// or TopK: through the index list, or from a compact copy made once per round
+// by draft_materialize_kernel) or a row of the recent window, which has slid to
+// end at the newest drafted token and is read straight from the cache.
 //
 // The MFMA layouts are the verify kernel's: K.Q^T on the bf16 MFMA with the
 // keys as A rows, O^T = V^T P^T so a head's softmax state and output stay in
@@ -157,9 +155,18 @@ __device__ __forceinline__ void draft_tile(const DraftArgs& a, const u32x4 (&qop
     }
 }
 
-template <bool kRound>
+// Where an entry's row comes from: the index list (Eq. 5), or a draft-round
+// step whose fixed rows come through the index list or from the materialized
+// copy, and whose window rows are consecutive cache rows.
+constexpr int kPlain = 0, kRoundIdx = 1, kRoundSel = 2;
+
+template <int kMode>
 __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
     const DItem it = decode_ditem(a.seq, blockIdx.x, a.n_kv_heads, a.chunk);
+    // (read here, outside the wave-dependent branch below, so that they are
+    // scalar loads and not vector loads that the index load waits for)
+    const int nf = kMode == kPlain ? 0 : a.n_fixed[it.b];
+    const int win0 = kMode == kPlain ? 0 : a.win0[it.b];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int m16 = lane & 15, G = lane >> 4;
     const int g = a.group;
@@ -194,15 +201,18 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
         // Lane l finds the row of entry l once; every K/V row of the tile is
         // then requested at once.
         uint32_t my_row;
-        if (!kRound) {
+        if (kMode == kPlain) {
             my_row = (uint32_t)min(max(a.idx[(size_t)it.unit * a.budget + e], 0), a.max_ctx - 1);
         } else {
-            const int nf = a.n_fixed[it.b];
-            my_row = e < nf ? (uint32_t)e | kSelBit
-                            : (uint32_t)min(max(a.win0[it.b] + e - nf, 0), a.max_ctx - 1);
+            // (the index load does not wait for n_fixed: entry e < budget is in
+            // bounds, and its value is used only when e < n_fixed)
+            const int32_t fixed_row = kMode == kRoundIdx ? a.idx[(size_t)it.unit * a.budget + e] : 0;
+            my_row = e < nf ? (kMode == kRoundSel ? (uint32_t)e | kSelBit
+                                                  : (uint32_t)min(max(fixed_row, 0), a.max_ctx - 1))
+                            : (uint32_t)min(max(win0 + e - nf, 0), a.max_ctx - 1);
         }
         Gathered ta;
-        gather_tile<kRound>(my_row, 0, src, m16, G, ta);
+        gather_tile<kMode == kRoundSel>(my_row, 0, src, m16, G, ta);
         draft_tile(a, qop, ta, wbeg, wend, G, M, L, oacc);
         L += shfl_xor_f(L, 16);
         L += shfl_xor_f(L, 32);
@@ -367,12 +377,15 @@ __global__ __launch_bounds__(kDraftThreads) void draft_materialize_kernel(DraftA
 }  // namespace
 
 hipError_t launch_draft(const DraftArgs& a, int n_items, hipStream_t stream) {
-    hipLaunchKernelGGL(draft_kernel<false>, dim3(n_items), dim3(kDraftThreads), 0, stream, a);
+    hipLaunchKernelGGL(draft_kernel<kPlain>, dim3(n_items), dim3(kDraftThreads), 0, stream, a);
     return hipGetLastError();
 }
 
 hipError_t launch_draft_step(const DraftArgs& a, int n_items, hipStream_t stream) {
-    hipLaunchKernelGGL(draft_kernel<true>, dim3(n_items), dim3(kDraftThreads), 0, stream, a);
+    if (a.k_sel)
+        hipLaunchKernelGGL(draft_kernel<kRoundSel>, dim3(n_items), dim3(kDraftThreads), 0, stream, a);
+    else
+        hipLaunchKernelGGL(draft_kernel<kRoundIdx>, dim3(n_items), dim3(kDraftThreads), 0, stream, a);
     return hipGetLastError();
 }
 

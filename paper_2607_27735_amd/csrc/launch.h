@@ -74,9 +74,10 @@ struct DraftArgs {
     int32_t n_q_heads, n_kv_heads, group, max_ctx, budget, chunk, out_fp32;
     float scale_log2;
     SeqTable seq;           // ctx[] holds the entry count per sequence
-    // Draft-round step only: entry e < n_fixed[b] is row e of k_sel/v_sel
-    // ([batch][n_kv][budget][128], the materialized sink and TopK rows);
-    // entry e >= n_fixed[b] is cache row win0[b] + e - n_fixed[b].
+    // Draft-round step only: entry e < n_fixed[b] is cache row idx[e], or,
+    // when k_sel is set, row e of k_sel/v_sel ([batch][n_kv][budget][128], the
+    // materialized sink and TopK rows); entry e >= n_fixed[b] is cache row
+    // win0[b] + e - n_fixed[b].
     uint16_t* k_sel;        // written by the materialization, read by the steps
     uint16_t* v_sel;
     int32_t n_fixed[kTableBatch];

@@ -186,13 +186,13 @@ def test_draft_validation(lib):
 
 
 def _step(lib, shape=None, params=None, ctx=(4000,), cur=(4003,), q=FAKE, k=FAKE, v=FAKE,
-          ks=FAKE, vs=FAKE, out=FAKE, ws=FAKE, ws_bytes=1 << 40):
+          idx=FAKE, ks=FAKE, vs=FAKE, out=FAKE, ws=FAKE, ws_bytes=1 << 40):
     shape = shape or _shape(batch=len(ctx))
     params = params or _params()
     ca, cp = _i32(*ctx)
     ua, up = _i32(*cur)
-    return lib.ssl_draft_step(ctypes.byref(shape), ctypes.byref(params), cp, up, q, k, v, ks, vs,
-                              out, ws, ws_bytes, None)
+    return lib.ssl_draft_step(ctypes.byref(shape), ctypes.byref(params), cp, up, q, k, v, idx, ks,
+                              vs, out, ws, ws_bytes, None)
 
 
 def test_draft_round_validation(lib):
@@ -207,6 +207,10 @@ def test_draft_round_validation(lib):
     for name in ("q", "k", "v", "ks", "vs", "out"):
         assert _step(lib, **{name: None}) == B.SSL_ERR_NULL
         assert _step(lib, **{name: FAKE_ODD}) == B.SSL_ERR_ALIGN
+    # fixed rows through idx: idx required and aligned, k_sel / v_sel both absent
+    assert _step(lib, ks=None, vs=None, idx=None) == B.SSL_ERR_NULL
+    assert _step(lib, ks=None, vs=None, idx=FAKE + 2) == B.SSL_ERR_ALIGN
+    assert _step(lib, ks=None, vs=None, idx=FAKE, ws=None) == B.SSL_ERR_WORKSPACE
     assert _step(lib, ws=None) == B.SSL_ERR_WORKSPACE
     assert _step(lib, ws_bytes=8) == B.SSL_ERR_WORKSPACE
     # the workspace covers the step's entries, the same count as the draft's

@@ -85,11 +85,14 @@ def test_draft_round_matches_oracle(name):
         cur = base + i
         o_ref = oracle.draft_step(w, idx, base, cur, q_draft=qb)
         oabs = oracle.draft_step(w, idx, base, cur, q_draft=qb, v=abs_v(w))
-        o = B.draft_step(dev_bf16(qb), k, v, k_sel, v_sel, base, cur, p)
+        o = B.draft_step(dev_bf16(qb), k, v, base, cur, p, k_sel=k_sel, v_sel=v_sel)
+        o_idx = B.draft_step(dev_bf16(qb), k, v, base, cur, p, idx=idx_d)
         torch.cuda.synchronize()
         o = o.float().cpu().numpy().astype(np.float64)
         worst = max(worst, check_outputs(o, o_ref, oabs, np.ones(o_ref.shape[:2], dtype=bool),
                                          what=f"draft step {i}"))
+        # the fixed rows through idx: the same rows in the same order, the same result
+        assert np.array_equal(o_idx.float().cpu().numpy(), o.astype(np.float32))
         if i == 0:   # before any drafted token the step is the plain draft over idx
             o0 = B.draft_attn(dev_bf16(qb), k, v, idx_d, n_idx, p)
             torch.cuda.synchronize()
@@ -108,7 +111,7 @@ def test_draft_round_bf16_outputs():
     for i in (0, 3, steps):
         o_ref = oracle.draft_step(w, idx, base, base + i)
         oabs = oracle.draft_step(w, idx, base, base + i, v=abs_v(w))
-        o = B.draft_step(dev_bf16(w.q_draft), k, v, k_sel, v_sel, base, base + i, p)
+        o = B.draft_step(dev_bf16(w.q_draft), k, v, base, base + i, p, k_sel=k_sel, v_sel=v_sel)
         torch.cuda.synchronize()
         check_outputs(o.float().cpu().numpy().astype(np.float64), o_ref, oabs,
                       np.ones(o_ref.shape[:2], dtype=bool), out_fp32=False, what=f"bf16 step {i}")
@@ -120,6 +123,7 @@ def test_draft_round_rejects_long_tail():
     k, v = dev_bf16(w.k), dev_bf16(w.v)
     sel = torch.zeros((w.batch, w.n_kv_heads, w.budget, 128), dtype=torch.bfloat16, device="cuda")
     with pytest.raises(B.SSLError):
-        B.draft_step(dev_bf16(w.q_draft), k, v, sel, sel, base, base + w.k_recent + 1, p)
+        B.draft_step(dev_bf16(w.q_draft), k, v, base, base + w.k_recent + 1, p, k_sel=sel,
+                     v_sel=sel)
     with pytest.raises(B.SSLError):
-        B.draft_step(dev_bf16(w.q_draft), k, v, sel, sel, base, base - 1, p)
+        B.draft_step(dev_bf16(w.q_draft), k, v, base, base - 1, p, k_sel=sel, v_sel=sel)
