@@ -54,6 +54,12 @@ def _bind(lib):
     lib.oracle_draft_step.argtypes = [ctypes.c_int] * 8 + [_i32p, _i32p, _u16p, _u16p, _u16p,
                                                            _i32p, ctypes.c_double, _f64p]
     lib.oracle_draft_step.restype = ctypes.c_int
+    _f32p = ctypes.POINTER(ctypes.c_float)
+    lib.oracle_row_stats.argtypes = [ctypes.c_int] * 3 + [_u16p, _f32p, _f64p, _i32p]
+    lib.oracle_row_stats.restype = ctypes.c_int
+    lib.oracle_greedy_accept.argtypes = [ctypes.c_int] * 4 + [_i32p, _u16p, _f32p, _i32p, _i32p,
+                                                              _i32p]
+    lib.oracle_greedy_accept.restype = ctypes.c_int
     lib.oracle_index_count.argtypes = [ctypes.c_int] * 4
     lib.oracle_index_count.restype = ctypes.c_int
     lib.oracle_ema.argtypes = [ctypes.c_double] * 3
@@ -188,6 +194,50 @@ def draft_step(w, idx: np.ndarray, base_len, cur_len, *, q_draft=None, k=None, v
     if rc != 0:
         raise ValueError("oracle_draft_step rejected its arguments")
     return out
+
+
+def _logit_ptrs(logits: np.ndarray):
+    """(bf16 bits pointer, fp32 pointer, keep-alive array) for uint16 or float32 logits."""
+    if logits.dtype == np.uint16:
+        a = _c(logits, np.uint16)
+        return _p(a, _u16p), None, a
+    if logits.dtype == np.float32:
+        a = _c(logits, np.float32)
+        return None, a.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), a
+    raise TypeError("logits must be uint16 (bf16 bits) or float32")
+
+
+def row_stats(logits: np.ndarray, vocab: Optional[int] = None, lib=None):
+    """Per-row entropy (nats, float64) and argmax (lowest index) of
+    ``logits`` [n_rows][row_stride] (bf16 bits as uint16, or float32)."""
+    lib = lib or load()
+    n_rows, stride = logits.shape
+    V = stride if vocab is None else vocab
+    pb, pf, keep = _logit_ptrs(logits)
+    H = np.zeros(n_rows, dtype=np.float64)
+    a = np.zeros(n_rows, dtype=np.int32)
+    if lib.oracle_row_stats(n_rows, V, stride, pb, pf, _p(H, _f64p), _p(a, _i32p)) != 0:
+        raise ValueError("oracle_row_stats rejected its arguments")
+    return H, a
+
+
+def greedy_accept(logits: np.ndarray, draft: np.ndarray, k_len, vocab: Optional[int] = None,
+                  lib=None):
+    """Greedy verification: ``logits`` [batch][max_k + 1][row_stride], ``draft``
+    [batch][max_k] int32, ``k_len`` per sequence; returns (n_accepted, next_token)."""
+    lib = lib or load()
+    batch, rows, stride = logits.shape
+    max_k = rows - 1
+    V = stride if vocab is None else vocab
+    pb, pf, keep = _logit_ptrs(logits)
+    d = _c(draft, np.int32).reshape(batch, max_k)
+    kl = _c(k_len, np.int32)
+    m = np.zeros(batch, dtype=np.int32)
+    t = np.zeros(batch, dtype=np.int32)
+    if lib.oracle_greedy_accept(batch, max_k, V, stride, _p(kl, _i32p), pb, pf, _p(d, _i32p),
+                                _p(m, _i32p), _p(t, _i32p)) != 0:
+        raise ValueError("oracle_greedy_accept rejected its arguments")
+    return m, t
 
 
 def ema(prev: float, observed: float, beta: float, lib=None) -> float:

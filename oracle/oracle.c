@@ -413,3 +413,83 @@ int oracle_choose_k(const double *p, int n, const int32_t *cands, int n_cands,
     }
     return best;
 }
+
+/* ---------------------------------------------------------------------------
+ * Around the path: the statistics of token logits that the controller and the
+ * verification stage consume.
+ * ------------------------------------------------------------------------- */
+
+/*
+ * Per-row token statistics (Sec. 3.3: H_i is the entropy of the drafter's
+ * output distribution for draft token i; Sec. 2.1: verification keeps the
+ * drafted tokens the target model agrees with).  Row r of logits
+ * [n_rows][row_stride], its first vocab entries, as bf16 bit patterns
+ * (logits_bf16) or fp32 values (logits_f32; exactly one of the two given):
+ *     p = softmax(x),  entropy[r] = -sum_i p_i ln p_i  (nats),
+ *     argmax[r] = the lowest index of the largest logit.
+ * Either output may be NULL.  Returns 0 or -1.
+ */
+int oracle_row_stats(int n_rows, int vocab, int row_stride, const uint16_t *logits_bf16,
+                     const float *logits_f32, double *entropy, int32_t *argmax)
+{
+    if (n_rows < 1 || vocab < 1 || row_stride < vocab) return -1;
+    if ((logits_bf16 == NULL) == (logits_f32 == NULL)) return -1;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int r = 0; r < n_rows; ++r) {
+        double *x = (double *)malloc(sizeof(double) * (size_t)vocab);
+        for (int i = 0; i < vocab; ++i)
+            x[i] = logits_bf16 ? widen_bf16(logits_bf16[(size_t)r * row_stride + i])
+                               : (double)logits_f32[(size_t)r * row_stride + i];
+        int a = 0;
+        for (int i = 1; i < vocab; ++i)
+            if (x[i] > x[a]) a = i;
+        const double m = x[a];
+        double Z = 0.0;
+        for (int i = 0; i < vocab; ++i) Z += exp(x[i] - m);
+        double H = 0.0;
+        for (int i = 0; i < vocab; ++i) {
+            const double lp = x[i] - m - log(Z);      /* ln p_i */
+            H -= exp(lp) * lp;
+        }
+        if (entropy) entropy[r] = H;
+        if (argmax) argmax[r] = a;
+        free(x);
+    }
+    return 0;
+}
+
+/*
+ * Greedy verification (Sec. 2.1's verification stage with the greedy
+ * criterion; the paper does not spell out its acceptance rule).  Sequence b
+ * drafted k = k_len[b] tokens draft[b][0..k); its verify pass produced the
+ * k + 1 logit rows logits[b][0..k] (row j predicts the token after drafted
+ * token j - 1; layout [batch][max_k + 1][row_stride]).  With t_j = the argmax
+ * of row j (lowest index on ties):
+ *     n_accepted[b] = the largest m <= k with draft[b][j] == t_j for all j < m,
+ *     next_token[b] = t_m, the corrected (or, if m == k, the bonus) token.
+ * Returns 0 or -1.
+ */
+int oracle_greedy_accept(int batch, int max_k, int vocab, int row_stride, const int32_t *k_len,
+                         const uint16_t *logits_bf16, const float *logits_f32,
+                         const int32_t *draft, int32_t *n_accepted, int32_t *next_token)
+{
+    if (batch < 1 || max_k < 0 || vocab < 1 || row_stride < vocab) return -1;
+    if ((logits_bf16 == NULL) == (logits_f32 == NULL)) return -1;
+    for (int b = 0; b < batch; ++b)
+        if (k_len[b] < 0 || k_len[b] > max_k) return -1;
+    const int rows = batch * (max_k + 1);
+    int32_t *t = (int32_t *)malloc(sizeof(int32_t) * (size_t)rows);
+    const int rc = oracle_row_stats(rows, vocab, row_stride, logits_bf16, logits_f32, NULL, t);
+    if (rc == 0) {
+        for (int b = 0; b < batch; ++b) {
+            const int32_t *tb = t + (size_t)b * (max_k + 1);
+            const int32_t *db = draft + (size_t)b * max_k;
+            int m = 0;
+            while (m < k_len[b] && db[m] == tb[m]) ++m;
+            n_accepted[b] = m;
+            next_token[b] = tb[m];
+        }
+    }
+    free(t);
+    return rc;
+}

@@ -442,6 +442,72 @@ def pin_draft_step_value_one(lib):
 
 
 # ---------------------------------------------------------------------------
+# around the path: token entropy and greedy acceptance
+# ---------------------------------------------------------------------------
+
+def pin_row_stats_library(lib):
+    """Entropy against scipy (softmax, then Shannon entropy in nats) and argmax
+    against numpy (first occurrence), for bf16 and fp32 logits of several scales."""
+    from scipy.special import softmax
+    from scipy.stats import entropy
+    rng = np.random.default_rng(81)
+    V = 1000
+    x = rng.standard_normal((6, V)) * np.array([0.1, 1.0, 3.0, 10.0, 30.0, 1.0])[:, None]
+    x[5, 17] = 40.0                                      # a peaked row
+    for logits in (f32_to_bf16_bits(x.astype(np.float32)), x.astype(np.float32)):
+        H, a = oracle.row_stats(logits, lib=lib)
+        xs = (logits.astype(np.uint32) << 16).view(np.float32).astype(np.float64) \
+            if logits.dtype == np.uint16 else logits.astype(np.float64)
+        for r in range(6):
+            want = entropy(softmax(xs[r]))
+            assert abs(H[r] - want) <= 1e-12 * max(1.0, want), (r, H[r], want)
+            assert a[r] == int(np.argmax(xs[r]))
+    # only the first vocab entries of a row count
+    xpad = np.concatenate([x.astype(np.float32), np.full((6, 8), 99.0, np.float32)], axis=1)
+    H2, a2 = oracle.row_stats(xpad, vocab=V, lib=lib)
+    H1, a1 = oracle.row_stats(x.astype(np.float32), lib=lib)
+    assert np.array_equal(a1, a2) and np.abs(H1 - H2).max() < 1e-12
+
+
+def pin_row_stats_closed_forms(lib):
+    V = 4096
+    x = np.zeros((3, V), dtype=np.float32)              # uniform: ln V, ties to index 0
+    c = 5.0
+    x[1, 100] = c                                        # one raised logit
+    x[2, [9, 5, 3000]] = [2.0, 2.0, 1.0]                 # tie at the max: the lower index
+    H, a = oracle.row_stats(x, lib=lib)
+    assert abs(H[0] - math.log(V)) < 1e-12 and a[0] == 0
+    p1 = math.exp(c) / (math.exp(c) + V - 1)
+    want = -p1 * math.log(p1) - (1 - p1) * math.log((1 - p1) / (V - 1))
+    assert abs(H[1] - want) < 1e-11 and a[1] == 100     # (a 4096-term fp64 sum)
+    assert a[2] == 5
+
+
+def pin_greedy_accept_worked(lib):
+    """Row j's argmax is planted at t_j; the drafts agree with the first m rows."""
+    V, max_k = 300, 5
+    rng = np.random.default_rng(82)
+    t = rng.integers(0, V, size=(4, max_k + 1))
+    x = rng.standard_normal((4, max_k + 1, V)).astype(np.float32)
+    for b in range(4):
+        for j in range(max_k + 1):
+            x[b, j, t[b, j]] = 10.0
+    draft = t[:, :max_k].copy()
+    draft[0, 3] = (t[0, 3] + 1) % V                      # disagrees at 3: m = 3, next t_3
+    k_len = np.array([5, 5, 2, 0])                       # seq 1 agrees everywhere: bonus t_5
+    draft[2, 2:] = -1                                    # past k: never read
+    m, nxt = oracle.greedy_accept(x, draft, k_len, lib=lib)
+    assert list(m) == [3, 5, 2, 0]
+    assert list(nxt) == [t[0, 3], t[1, 5], t[2, 2], t[3, 0]]
+    # a tie at the max is read as its lower index
+    x[1, 1, :] = 0.0
+    x[1, 1, [7, 250]] = 10.0
+    draft[1, 1] = 250
+    m, nxt = oracle.greedy_accept(x, draft, k_len, lib=lib)
+    assert m[1] == 1 and nxt[1] == 7
+
+
+# ---------------------------------------------------------------------------
 # controller (Eq. 6-8)
 # ---------------------------------------------------------------------------
 
@@ -518,5 +584,6 @@ ALL_PINS = [pin_verify_matches_sdpa, pin_verify_value_one, pin_verify_zero_keys_
             pin_scores_permutation, pin_select_lexsort, pin_select_bruteforce_subsets,
             pin_select_special_cases, pin_draft_matches_sdpa, pin_draft_full_equals_dense,
             pin_draft_permutation, pin_draft_step_first_matches_sdpa,
-            pin_draft_step_worked_example, pin_draft_step_value_one,
+            pin_draft_step_worked_example, pin_draft_step_value_one, pin_row_stats_library,
+            pin_row_stats_closed_forms, pin_greedy_accept_worked,
             pin_controller_closed_forms, pin_controller_argmax]

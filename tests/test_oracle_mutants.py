@@ -48,6 +48,14 @@ MUTANTS = [
      "for (int t = w0; t < cur - 1; ++t) S[m_S++] = t;"),
     ("step_fixed_part_from_cur", "const int r_T = (T - k_recent) > s_end ? (T - k_recent) : s_end;",
      "const int r_T = (cur - k_recent) > s_end ? (cur - k_recent) : s_end;"),
+    ("entropy_log2", "const double lp = x[i] - m - log(Z);      /* ln p_i */",
+     "const double lp = (x[i] - m - log(Z)) / log(2.0);"),
+    ("entropy_unnormalized", "const double lp = x[i] - m - log(Z);      /* ln p_i */",
+     "const double lp = x[i] - m;"),
+    ("argmax_ties_to_last", "if (x[i] > x[a]) a = i;", "if (x[i] >= x[a]) a = i;"),
+    ("accept_one_past_mismatch", "while (m < k_len[b] && db[m] == tb[m]) ++m;",
+     "while (m < k_len[b] && db[m] == tb[m]) ++m;\n            if (m < k_len[b]) ++m;"),
+    ("next_token_from_row_after", "next_token[b] = tb[m];", "next_token[b] = tb[m < k_len[b] ? m + 1 : m];"),
     ("ema_weights_swapped", "return beta * prev + (1.0 - beta) * observed;",
      "return beta * observed + (1.0 - beta) * prev;"),
     ("accept_prob_inverted", "return ea / (ea + er);", "return er / (ea + er);"),
