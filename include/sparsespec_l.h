@@ -234,6 +234,50 @@ int ssl_draft_step(const ssl_shape *shape, const ssl_params *params,
                    void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Around the path: token statistics of logit rows.
+ *
+ * Sec. 3.3 drives the length controller with the entropy H_i of the
+ * drafter's output distribution for each drafted token (the ssl_ctrl_* calls
+ * below take them in nats); the verification stage (Sec. 2.1) keeps the
+ * longest prefix of drafted tokens the target model agrees with and adds one
+ * token of its own.  The paper does not spell out the acceptance rule; these
+ * calls implement the greedy one.
+ *
+ * Logit rows: logits[r][0..row_stride) of n_rows rows, bf16 (SSL_DT_BF16) or
+ * fp32 (SSL_DT_F32); entries [0, vocab) are the logits, the rest is padding
+ * that is never read.  row_stride * element size must be a multiple of 16
+ * bytes and logits 16-byte aligned; 1 <= vocab <= row_stride, vocab <= 524288.
+ * Logits must be finite.
+ *
+ * ssl_logit_stats: for each row, with p = softmax(logits[r][0..vocab)):
+ *   entropy[r] = -sum_i p_i ln p_i (nats, fp32), argmax[r] = the lowest index
+ *   of the largest logit.  Either output may be NULL, not both.
+ * ssl_greedy_accept: sequence b drafted k = k_len_host[b] <= max_k <= 63
+ *   tokens draft_tokens[b][0..k) (layout [batch][max_k]); its verify pass gave
+ *   the k + 1 rows logits[b][0..k] (layout [batch][max_k + 1][row_stride]; row j
+ *   scores the token after drafted token j - 1; rows past k are not read).
+ *   With t_j = argmax of row j:
+ *     n_accepted[b] = the largest m <= k with draft_tokens[b][j] == t_j, j < m;
+ *     next_token[b] = t_m (the corrected token, or the bonus one when m = k).
+ * Both use a caller workspace (size from the *_workspace calls, no initial
+ * contents needed; calls that overlap in time must not share one).  Errors:
+ * SSL_ERR_NULL, SSL_ERR_SHAPE (counts or sizes out of range, unknown dtype),
+ * SSL_ERR_UNSUPPORTED (vocab > 524288, batch > 64), SSL_ERR_ALIGN,
+ * SSL_ERR_WORKSPACE.
+ */
+enum { SSL_DT_BF16 = 0, SSL_DT_F32 = 1 };
+
+int ssl_logit_stats_workspace(int32_t n_rows, int32_t vocab, size_t *bytes_out);
+int ssl_logit_stats(const void *logits, int32_t dtype, int32_t n_rows, int32_t vocab,
+                    int32_t row_stride, float *entropy, int32_t *argmax, void *workspace,
+                    size_t workspace_bytes, hipStream_t stream);
+int ssl_greedy_accept_workspace(int32_t batch, int32_t max_k, int32_t vocab, size_t *bytes_out);
+int ssl_greedy_accept(const void *logits, int32_t dtype, int32_t batch, int32_t max_k,
+                      const int32_t *k_len_host, int32_t vocab, int32_t row_stride,
+                      const int32_t *draft_tokens, int32_t *n_accepted, int32_t *next_token,
+                      void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Adaptive speculation length (Sec. 3.3), host only.
  *
  * State: the class-mean entropies of accepted and rejected drafts, tracked by

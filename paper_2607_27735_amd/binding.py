@@ -37,6 +37,8 @@ EXPORTED = [
     "ssl_select_workspace", "ssl_select_topb",
     "ssl_draft_workspace", "ssl_draft_attn",
     "ssl_draft_materialize", "ssl_draft_step_workspace", "ssl_draft_step",
+    "ssl_logit_stats_workspace", "ssl_logit_stats", "ssl_greedy_accept_workspace",
+    "ssl_greedy_accept",
     "ssl_ctrl_create", "ssl_ctrl_destroy", "ssl_ctrl_observe", "ssl_ctrl_accept_prob",
     "ssl_ctrl_choose_k", "ssl_ctrl_get_state", "ssl_ctrl_set_state",
 ]
@@ -94,9 +96,16 @@ def load(path: Optional[str] = None):
     lib.ssl_draft_step_workspace.argtypes = [sp, pp, _i32p, _i32p, _szp]
     lib.ssl_draft_step.argtypes = [sp, pp, _i32p, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                    _sz, _vp]
+    _i32 = ctypes.c_int32
+    lib.ssl_logit_stats_workspace.argtypes = [_i32, _i32, _szp]
+    lib.ssl_logit_stats.argtypes = [_vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _sz, _vp]
+    lib.ssl_greedy_accept_workspace.argtypes = [_i32, _i32, _i32, _szp]
+    lib.ssl_greedy_accept.argtypes = [_vp, _i32, _i32, _i32, _i32p, _i32, _i32, _vp, _vp, _vp,
+                                      _vp, _sz, _vp]
     for f in ("ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn", "ssl_select_workspace",
               "ssl_select_topb", "ssl_draft_workspace", "ssl_draft_attn", "ssl_draft_materialize",
-              "ssl_draft_step_workspace", "ssl_draft_step"):
+              "ssl_draft_step_workspace", "ssl_draft_step", "ssl_logit_stats_workspace",
+              "ssl_logit_stats", "ssl_greedy_accept_workspace", "ssl_greedy_accept"):
         getattr(lib, f).restype = ctypes.c_int
     lib.ssl_ctrl_create.argtypes = [ctypes.c_double, _i32p, ctypes.c_int32, ctypes.c_int32]
     lib.ssl_ctrl_create.restype = _vp
@@ -394,6 +403,70 @@ def draft_step(q_draft: torch.Tensor, k: torch.Tensor, v: torch.Tensor, ctx_len_
                                  _stream(stream)),
            "ssl_draft_step")
     return out
+
+
+# ---------------------------------------------------------------------------
+# token statistics of logit rows
+# ---------------------------------------------------------------------------
+
+SSL_DT_BF16 = 0
+SSL_DT_F32 = 1
+
+
+def _logit_dtype(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return SSL_DT_BF16
+    if t.dtype == torch.float32:
+        return SSL_DT_F32
+    raise TypeError("logits must be bfloat16 or float32")
+
+
+def logit_stats(logits: torch.Tensor, vocab: Optional[int] = None, entropy: bool = True,
+                argmax: bool = True, stream=None):
+    """Per-row entropy (nats, fp32) and argmax (int32, lowest index on ties) of
+    logits [n_rows, row_stride] (rows contiguous); returns (entropy, argmax),
+    None for an output not asked for."""
+    _need_gpu(logits)
+    n_rows, stride = logits.shape
+    if logits.stride(1) != 1 or logits.stride(0) != stride:
+        raise ValueError("logits must be contiguous [n_rows, row_stride]")
+    V = stride if vocab is None else vocab
+    ent = torch.empty(n_rows, dtype=torch.float32, device=logits.device) if entropy else None
+    am = torch.empty(n_rows, dtype=torch.int32, device=logits.device) if argmax else None
+    n = ctypes.c_size_t(0)
+    _check(load().ssl_logit_stats_workspace(n_rows, V, ctypes.byref(n)), "ssl_logit_stats_workspace")
+    ws = torch.empty(max(int(n.value), 1), dtype=torch.uint8, device=logits.device)
+    _check(load().ssl_logit_stats(_ptr(logits), _logit_dtype(logits), n_rows, V, stride, _ptr(ent),
+                                  _ptr(am), _ptr(ws), ws.numel(), _stream(stream)),
+           "ssl_logit_stats")
+    return ent, am
+
+
+def greedy_accept(logits: torch.Tensor, draft_tokens: torch.Tensor, k_len_host,
+                  vocab: Optional[int] = None, stream=None):
+    """Greedy verification: logits [batch, max_k + 1, row_stride], draft_tokens
+    [batch, max_k] int32, k_len_host per sequence; returns (n_accepted,
+    next_token) int32 [batch]."""
+    _need_gpu(logits, draft_tokens)
+    batch, rows, stride = logits.shape
+    max_k = rows - 1
+    if not logits.is_contiguous():
+        raise ValueError("logits must be contiguous [batch, max_k + 1, row_stride]")
+    if draft_tokens.dtype != torch.int32 or tuple(draft_tokens.shape) != (batch, max_k):
+        raise ValueError("draft_tokens must be int32 [batch, max_k]")
+    V = stride if vocab is None else vocab
+    kl = _host_i32(k_len_host)
+    m = torch.empty(batch, dtype=torch.int32, device=logits.device)
+    nxt = torch.empty(batch, dtype=torch.int32, device=logits.device)
+    n = ctypes.c_size_t(0)
+    _check(load().ssl_greedy_accept_workspace(batch, max_k, V, ctypes.byref(n)),
+           "ssl_greedy_accept_workspace")
+    ws = torch.empty(max(int(n.value), 1), dtype=torch.uint8, device=logits.device)
+    _check(load().ssl_greedy_accept(_ptr(logits), _logit_dtype(logits), batch, max_k,
+                                    kl.ctypes.data_as(_i32p), V, stride, _ptr(draft_tokens),
+                                    _ptr(m), _ptr(nxt), _ptr(ws), ws.numel(), _stream(stream)),
+           "ssl_greedy_accept")
+    return m, nxt
 
 
 # ---------------------------------------------------------------------------

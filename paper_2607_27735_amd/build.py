@@ -19,7 +19,7 @@ LIB_NAME = "libsparsespec_l.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
 ARCH = "gfx950"
 
-HIP_SOURCES = ["verify.hip", "verify_fused.hip", "select.hip", "draft.hip"]
+HIP_SOURCES = ["verify.hip", "verify_fused.hip", "select.hip", "draft.hip", "logits.hip"]
 CXX_SOURCES = ["api.cpp", "controller.cpp"]
 
 

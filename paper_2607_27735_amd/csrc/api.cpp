@@ -557,4 +557,126 @@ int ssl_draft_step(const ssl_shape* shape, const ssl_params* params, const int32
     return launch_draft_step(a, plan.d.n_items, stream) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
 }
 
+// ---- token statistics of logit rows ----------------------------------------
+
+struct LogitPlan {
+    int n_chunks;
+    size_t part_off, tag_off, argmax_off, bytes;
+};
+
+int plan_logits(int32_t n_rows, int32_t vocab, LogitPlan* plan) {
+    if (n_rows < 1 || vocab < 1) return SSL_ERR_SHAPE;
+    if (vocab > kLogitChunk * kLogitMaxChunks) return SSL_ERR_UNSUPPORTED;
+    if ((int64_t)n_rows * ((vocab + kLogitChunk - 1) / kLogitChunk) > (1 << 30))
+        return SSL_ERR_UNSUPPORTED;
+    plan->n_chunks = (vocab + kLogitChunk - 1) / kLogitChunk;
+    const size_t slots = (size_t)n_rows * plan->n_chunks;
+    plan->part_off = 0;
+    plan->tag_off = align_up(slots * 4 * sizeof(float));
+    plan->argmax_off = plan->tag_off + align_up(slots * sizeof(uint64_t));
+    plan->bytes = plan->argmax_off + align_up((size_t)n_rows * sizeof(int32_t));
+    return SSL_OK;
+}
+
+int check_logits(const void* logits, int32_t dtype, int32_t vocab, int32_t row_stride) {
+    if (dtype != SSL_DT_BF16 && dtype != SSL_DT_F32) return SSL_ERR_SHAPE;
+    if (row_stride < vocab) return SSL_ERR_SHAPE;
+    if (!logits) return SSL_ERR_NULL;
+    const int64_t row_bytes = (int64_t)row_stride * (dtype == SSL_DT_F32 ? 4 : 2);
+    if (!aligned(logits, 16) || row_bytes % 16 != 0) return SSL_ERR_ALIGN;
+    return SSL_OK;
+}
+
+int ssl_logit_stats_workspace(int32_t n_rows, int32_t vocab, size_t* bytes_out) {
+    if (!bytes_out) return SSL_ERR_NULL;
+    LogitPlan plan;
+    const int rc = plan_logits(n_rows, vocab, &plan);
+    if (rc) return rc;
+    *bytes_out = plan.bytes;
+    return SSL_OK;
+}
+
+int ssl_logit_stats(const void* logits, int32_t dtype, int32_t n_rows, int32_t vocab,
+                    int32_t row_stride, float* entropy, int32_t* argmax, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream) {
+    LogitPlan plan;
+    int rc = plan_logits(n_rows, vocab, &plan);
+    if (rc) return rc;
+    rc = check_logits(logits, dtype, vocab, row_stride);
+    if (rc) return rc;
+    if (!entropy && !argmax) return SSL_ERR_NULL;
+    if ((entropy && !aligned(entropy, 4)) || (argmax && !aligned(argmax, 4))) return SSL_ERR_ALIGN;
+    rc = check_workspace(workspace, workspace_bytes, plan.bytes);
+    if (rc) return rc;
+    LogitArgs a = {};
+    a.logits = logits;
+    a.n_rows = n_rows;
+    a.vocab = vocab;
+    a.row_stride = row_stride;
+    a.n_chunks = plan.n_chunks;
+    a.entropy = entropy;
+    a.argmax = argmax;
+    a.part = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.part_off);
+    a.tag = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + plan.tag_off);
+    a.call_tag = next_call_tag();
+    a.rows_per_seq = 0;
+    return launch_logit_stats(a, dtype == SSL_DT_F32, stream) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
+}
+
+int ssl_greedy_accept_workspace(int32_t batch, int32_t max_k, int32_t vocab, size_t* bytes_out) {
+    if (!bytes_out) return SSL_ERR_NULL;
+    if (batch < 1 || max_k < 0) return SSL_ERR_SHAPE;
+    if (batch > kTableBatch || max_k > kAcceptMaxK) return SSL_ERR_UNSUPPORTED;
+    LogitPlan plan;
+    const int rc = plan_logits(batch * (max_k + 1), vocab, &plan);
+    if (rc) return rc;
+    *bytes_out = plan.bytes;
+    return SSL_OK;
+}
+
+int ssl_greedy_accept(const void* logits, int32_t dtype, int32_t batch, int32_t max_k,
+                      const int32_t* k_len_host, int32_t vocab, int32_t row_stride,
+                      const int32_t* draft_tokens, int32_t* n_accepted, int32_t* next_token,
+                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (batch < 1 || max_k < 0) return SSL_ERR_SHAPE;
+    if (batch > kTableBatch || max_k > kAcceptMaxK) return SSL_ERR_UNSUPPORTED;
+    LogitPlan plan;
+    int rc = plan_logits(batch * (max_k + 1), vocab, &plan);
+    if (rc) return rc;
+    rc = check_logits(logits, dtype, vocab, row_stride);
+    if (rc) return rc;
+    if (!k_len_host || !n_accepted || !next_token || (max_k > 0 && !draft_tokens))
+        return SSL_ERR_NULL;
+    for (int b = 0; b < batch; ++b)
+        if (k_len_host[b] < 0 || k_len_host[b] > max_k) return SSL_ERR_SHAPE;
+    if (!aligned(n_accepted, 4) || !aligned(next_token, 4) ||
+        (draft_tokens && !aligned(draft_tokens, 4)))
+        return SSL_ERR_ALIGN;
+    rc = check_workspace(workspace, workspace_bytes, plan.bytes);
+    if (rc) return rc;
+    char* ws = static_cast<char*>(workspace);
+    LogitArgs a = {};
+    a.logits = logits;
+    a.n_rows = batch * (max_k + 1);
+    a.vocab = vocab;
+    a.row_stride = row_stride;
+    a.n_chunks = plan.n_chunks;
+    a.entropy = nullptr;
+    a.argmax = reinterpret_cast<int32_t*>(ws + plan.argmax_off);
+    a.part = reinterpret_cast<float*>(ws + plan.part_off);
+    a.tag = reinterpret_cast<uint64_t*>(ws + plan.tag_off);
+    a.call_tag = next_call_tag();
+    a.rows_per_seq = max_k + 1;
+    for (int b = 0; b < batch; ++b) a.k_len[b] = k_len_host[b];
+    if (launch_logit_stats(a, dtype == SSL_DT_F32, stream) != hipSuccess) return SSL_ERR_HIP;
+    AcceptArgs c = {};
+    c.argmax = a.argmax;
+    c.draft = draft_tokens;
+    c.n_accepted = n_accepted;
+    c.next_token = next_token;
+    c.max_k = max_k;
+    for (int b = 0; b < batch; ++b) c.k_len[b] = k_len_host[b];
+    return launch_greedy_accept(c, batch, stream) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
+}
+
 }  // extern "C"

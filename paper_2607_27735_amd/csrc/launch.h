@@ -116,4 +116,33 @@ hipError_t launch_draft_materialize(const DraftArgs& a, int max_fixed, int n_uni
                                     hipStream_t stream);
 hipError_t launch_draft_step(const DraftArgs& a, int n_items, hipStream_t stream);
 
+// Token statistics of logit rows (entropy, argmax) and greedy acceptance.
+constexpr int kLogitChunk = 8192;        // logits per workgroup
+constexpr int kLogitMaxChunks = 64;      // chunks per row: vocab <= 524288
+constexpr int kAcceptMaxK = 63;          // drafted tokens per sequence (one wave)
+
+struct LogitArgs {
+    const void* logits;     // [n_rows][row_stride] bf16 or fp32
+    int32_t n_rows, vocab, row_stride, n_chunks;
+    float* entropy;         // [n_rows] nats, or null
+    int32_t* argmax;        // [n_rows], or null
+    float* part;            // [n_rows][n_chunks][4] chunk statistics
+    uint64_t* tag;          // [n_rows][n_chunks] publication tags (no initialisation needed)
+    uint64_t call_tag;
+    int32_t rows_per_seq;   // acceptance: max_k + 1 (rows past k_len[b] + 1 skipped); else 0
+    int32_t k_len[kTableBatch];
+};
+
+struct AcceptArgs {
+    const int32_t* argmax;  // [batch][max_k + 1]
+    const int32_t* draft;   // [batch][max_k]
+    int32_t* n_accepted;    // [batch]
+    int32_t* next_token;    // [batch]
+    int32_t max_k;
+    int32_t k_len[kTableBatch];
+};
+
+hipError_t launch_logit_stats(const LogitArgs& a, bool f32, hipStream_t stream);
+hipError_t launch_greedy_accept(const AcceptArgs& a, int batch, hipStream_t stream);
+
 }  // namespace ssl

@@ -232,6 +232,46 @@ def test_draft_round_validation(lib):
                                      FAKE, FAKE, None) == B.SSL_ERR_SHAPE
 
 
+def test_logit_stats_validation(lib):
+    n = ctypes.c_size_t(0)
+    assert lib.ssl_logit_stats_workspace(7, 128256, ctypes.byref(n)) == 0 and n.value > 0
+    assert lib.ssl_logit_stats_workspace(0, 100, ctypes.byref(n)) == B.SSL_ERR_SHAPE
+    assert lib.ssl_logit_stats_workspace(1, 524289, ctypes.byref(n)) == B.SSL_ERR_UNSUPPORTED
+
+    def call(logits=FAKE, dtype=0, rows=7, vocab=128256, stride=128256, ent=FAKE, am=FAKE,
+             ws=FAKE, ws_bytes=1 << 40):
+        return lib.ssl_logit_stats(logits, dtype, rows, vocab, stride, ent, am, ws, ws_bytes, None)
+    assert call(dtype=2) == B.SSL_ERR_SHAPE
+    assert call(stride=128000) == B.SSL_ERR_SHAPE
+    assert call(logits=None) == B.SSL_ERR_NULL
+    assert call(ent=None, am=None) == B.SSL_ERR_NULL
+    assert call(logits=FAKE_ODD) == B.SSL_ERR_ALIGN
+    assert call(vocab=100, stride=100) == B.SSL_ERR_ALIGN          # 200-byte rows
+    # 400-byte fp32 rows are aligned: the call gets as far as the workspace check
+    assert call(dtype=1, vocab=100, stride=100, ws=None) == B.SSL_ERR_WORKSPACE
+    assert call(ent=FAKE + 2) == B.SSL_ERR_ALIGN
+    assert call(ws=None) == B.SSL_ERR_WORKSPACE
+    assert call(ws_bytes=8) == B.SSL_ERR_WORKSPACE
+
+
+def test_greedy_accept_validation(lib):
+    n = ctypes.c_size_t(0)
+    assert lib.ssl_greedy_accept_workspace(4, 6, 128256, ctypes.byref(n)) == 0 and n.value > 0
+    assert lib.ssl_greedy_accept_workspace(65, 6, 100, ctypes.byref(n)) == B.SSL_ERR_UNSUPPORTED
+    assert lib.ssl_greedy_accept_workspace(1, 64, 100, ctypes.byref(n)) == B.SSL_ERR_UNSUPPORTED
+
+    def call(k=(6, 2), max_k=6, draft=FAKE, m=FAKE, nxt=FAKE, ws=FAKE, ws_bytes=1 << 40):
+        ka, kp = _i32(*k)
+        return lib.ssl_greedy_accept(FAKE, 0, len(k), max_k, kp, 128256, 128256, draft, m, nxt,
+                                     ws, ws_bytes, None)
+    assert call(k=(7, 2)) == B.SSL_ERR_SHAPE
+    assert call(k=(-1, 2)) == B.SSL_ERR_SHAPE
+    assert call(draft=None) == B.SSL_ERR_NULL
+    assert call(m=None) == B.SSL_ERR_NULL
+    assert call(nxt=FAKE + 1) == B.SSL_ERR_ALIGN
+    assert call(ws=None) == B.SSL_ERR_WORKSPACE
+
+
 def test_status_strings(lib):
     seen = set()
     for code in range(0, -8, -1):
