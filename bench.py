@@ -48,7 +48,7 @@ TRAFFIC_FILE = os.path.join(REPO, "profiles", "verify_traffic_llama8b_T32K.txt")
 OUR_KERNELS = ("verify_fused_kernel", "verify_stats_kernel", "verify_main_kernel",
                "verify_combine_kernel", "select_hist_kernel", "select_mark_kernel",
                "select_finish_kernel", "select_fused_kernel", "draft_materialize_kernel",
-               "draft_kernel")
+               "draft_kernel", "logit_stats_kernel", "greedy_accept_kernel")
 VERIFY_KERNELS = ("verify_fused_kernel", "verify_stats_kernel", "verify_main_kernel",
                   "verify_combine_kernel")
 
@@ -93,7 +93,8 @@ def summarize_trace(d: str, command: str) -> str:
                 else "draft round materialize" if "materialize" in k
                 else "draft round step (index list)" if short == "draft_kernel<1>"
                 else "draft round step (materialized rows)" if short == "draft_kernel<2>"
-                else "draft")
+                else "logit statistics" if k.startswith("logit")
+                else "greedy acceptance" if k.startswith("greedy") else "draft")
         per_call[call] = per_call.get(call, 0.0) + float(r["AverageNs"]) / 1e3
     out += ["", "sum of kernel averages per call: " +
             ", ".join(f"{c} {v:.2f} us" for c, v in per_call.items())]
@@ -168,6 +169,70 @@ def draft_round_bench(B, w, kvs, qd, params, scores, stream, reps, torch, np):
             "step_gbps": round(step_bytes / (mean_step * 1e-6) / 1e9, 1),
             "timing": f"{reps} back-to-back calls per figure between two HIP events, "
                       f"rotating {n} KV copies"}
+
+
+def vocab_side_bench(B, w, stream, reps, torch, np, vocab=128256):
+    """The token statistics around the path at this workload's step (next to
+    the headline, not part of it): draft entropies over k = max q_len - 1 draft
+    rows and greedy acceptance over the k + 1 verify rows of every sequence,
+    synthetic seeded bf16 logits over a Llama-3-sized vocabulary, each timed
+    as ``reps`` back-to-back calls (rotating copies beyond the 256 MB cache)
+    between two HIP events."""
+    import ctypes
+    from paper_2607_27735_amd.workloads import f32_to_bf16_bits
+    k = max(1, int(max(w.q_len)) - 1)
+    rng = np.random.default_rng(2024)
+    dev = torch.device("cuda:0")
+    draft_rows = w.batch * k
+    verify_rows = w.batch * (k + 1)
+    x = f32_to_bf16_bits((rng.standard_normal((verify_rows, vocab)) * 2.0).astype(np.float32))
+    logits = torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev)
+    copy_bytes = logits.numel() * 2
+    n = max(2, math.ceil((512 << 20) / copy_bytes) + 1)
+    copies = [logits] + [logits.clone() for _ in range(n - 1)]
+    lib = B.load()
+    # draft entropies: the first k rows of each copy stand for the draft logits
+    ent = torch.empty(draft_rows, dtype=torch.float32, device=dev)
+    nws = ctypes.c_size_t(0)
+    B._check(lib.ssl_logit_stats_workspace(draft_rows, vocab, ctypes.byref(nws)), "ws")
+    ws1 = torch.empty(max(nws.value, 1), dtype=torch.uint8, device=dev)
+    sargs = [(c.data_ptr(), B.SSL_DT_BF16, draft_rows, vocab, vocab, ent.data_ptr(), None,
+              ws1.data_ptr(), ws1.numel(), B._stream(stream)) for c in copies]
+    # acceptance: drafts agree with the verify argmax for the first half of each sequence
+    k_len = np.full(w.batch, k, dtype=np.int32)
+    draft = torch.zeros((w.batch, k), dtype=torch.int32, device=dev)
+    m = torch.empty(w.batch, dtype=torch.int32, device=dev)
+    nxt = torch.empty(w.batch, dtype=torch.int32, device=dev)
+    B._check(lib.ssl_greedy_accept_workspace(w.batch, k, vocab, ctypes.byref(nws)), "ws")
+    ws2 = torch.empty(max(nws.value, 1), dtype=torch.uint8, device=dev)
+    aargs = [(c.data_ptr(), B.SSL_DT_BF16, w.batch, k, k_len.ctypes.data_as(B._i32p), vocab, vocab,
+              draft.data_ptr(), m.data_ptr(), nxt.data_ptr(), ws2.data_ptr(), ws2.numel(),
+              B._stream(stream)) for c in copies]
+    for a in sargs:
+        B._check(lib.ssl_logit_stats(*a), "ssl_logit_stats")
+    for a in aargs:
+        B._check(lib.ssl_greedy_accept(*a), "ssl_greedy_accept")
+
+    def timed(fn):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for r in range(reps):
+            fn(r)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    ent_us = timed(lambda r: lib.ssl_logit_stats(*sargs[r % n]))
+    acc_us = timed(lambda r: lib.ssl_greedy_accept(*aargs[r % n]))
+    eb, ab = draft_rows * vocab * 2, verify_rows * vocab * 2
+    return {"vocab": vocab, "logits": "bf16, N(0, 2^2), seeded",
+            "entropy_rows": draft_rows, "entropy_us": round(ent_us, 3),
+            "entropy_gbps": round(eb / (ent_us * 1e-6) / 1e9, 1),
+            "accept_rows": verify_rows, "accept_us": round(acc_us, 3),
+            "accept_gbps": round(ab / (acc_us * 1e-6) / 1e9, 1),
+            "timing": f"{reps} back-to-back calls per figure between two HIP events, "
+                      f"rotating {n} logit copies"}
 
 
 def summarize_traffic(fetch_dir: str, write_dir: str, copy_mib: int, command: str) -> str:
@@ -261,7 +326,8 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-draft-round", action="store_true",
-                    help="skip the draft-round measurement printed beside the headline")
+                    help="skip the draft-round and vocabulary-side measurements printed "
+                         "beside the headline")
     ap.add_argument("--mode", choices=["eager", "graph"], default="eager")
     ap.add_argument("--verify-mode", choices=["auto", "two-sweep", "one-sweep"], default="auto")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -463,6 +529,7 @@ def main() -> int:
     if not args.no_draft_round:
         result["draft_round"] = draft_round_bench(B, w, kvs, qd, params, scores, stream,
                                                   args.steps, torch, np)
+        result["vocab_side"] = vocab_side_bench(B, w, stream, args.steps, torch, np)
     # sanity: score mass of every KV head equals min(W, q) * group
     s = scores.double().sum(dim=2).cpu().numpy()
     want = np.array([min(w.window, int(x)) * w.group for x in w.q_len])[:, None]
