@@ -62,6 +62,11 @@ SMALL = {
     "kv8-g16": lambda: _poison_padding(generate(
         109, name="kv8-g16", batch=3, n_q_heads=128, n_kv_heads=8, ctx_len=[1, 130, 700],
         q_len=[1, 4, 4], max_ctx=720, max_q=4, budget=64)),
+    # the first index of a sequence, seeded by its prompt: the last W = 16 prompt
+    # positions as the query block (64 rows per KV head at group 4)
+    "prefill-seed-g4": lambda: _poison_padding(generate(
+        110, name="prefill-seed-g4", batch=2, n_q_heads=32, n_kv_heads=8, ctx_len=[4096, 1500],
+        q_len=[16, 16], max_ctx=4100, budget=256, heavy_hitters=4)),
 }
 
 
