@@ -197,6 +197,33 @@ int ssl_draft_attn(const ssl_shape *shape, const ssl_params *params,
                    void *out, void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Paged KV cache, as serving engines keep it: the same calls with K and V in
+ * page pools instead of one contiguous row per (sequence, KV head).
+ *
+ * k_pages / v_pages: [n_pages][Hkv][page_size][128] bf16, 16-byte aligned;
+ * block_table: device int32 [batch][max_blocks]; key t of sequence b, KV head
+ * c is row t % page_size of head c in page block_table[b][t / page_size].
+ * page_size must be a multiple of 32.  Page ids are not checked: every entry
+ * the call reads must name a page of the pool.  Everything else (shapes, q,
+ * out, scores, idx, workspaces and their sizes, errors) is as in
+ * ssl_verify_attn / ssl_draft_attn; in addition SSL_ERR_SHAPE if page_size
+ * is not a positive multiple of 32, or the pages cannot hold a context
+ * (verify: ctx_len[b] > page_size * max_blocks; draft: max_ctx >
+ * page_size * max_blocks, since the indices may name any key below max_ctx).
+ */
+int ssl_verify_attn_paged(const ssl_shape *shape, const ssl_params *params,
+                          const int32_t *ctx_len_host, const int32_t *q_len_host,
+                          const void *q, const void *k_pages, const void *v_pages,
+                          const int32_t *block_table, int32_t page_size, int32_t max_blocks,
+                          void *out, float *scores, void *workspace, size_t workspace_bytes,
+                          hipStream_t stream);
+int ssl_draft_attn_paged(const ssl_shape *shape, const ssl_params *params,
+                         const int32_t *n_idx_host, const void *q_draft, const void *k_pages,
+                         const void *v_pages, const int32_t *block_table, int32_t page_size,
+                         int32_t max_blocks, const int32_t *idx, void *out, void *workspace,
+                         size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Draft round (Sec. 3.1: the target model drafts k tokens one after another
  * over the sparse view of Sec. 3.2 Eq. 5).
  *

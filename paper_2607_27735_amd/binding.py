@@ -36,6 +36,7 @@ EXPORTED = [
     "ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn",
     "ssl_select_workspace", "ssl_select_topb",
     "ssl_draft_workspace", "ssl_draft_attn",
+    "ssl_verify_attn_paged", "ssl_draft_attn_paged",
     "ssl_draft_materialize", "ssl_draft_step_workspace", "ssl_draft_step",
     "ssl_logit_stats_workspace", "ssl_logit_stats", "ssl_greedy_accept_workspace",
     "ssl_greedy_accept",
@@ -97,6 +98,10 @@ def load(path: Optional[str] = None):
     lib.ssl_draft_step.argtypes = [sp, pp, _i32p, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                    _sz, _vp]
     _i32 = ctypes.c_int32
+    lib.ssl_verify_attn_paged.argtypes = [sp, pp, _i32p, _i32p, _vp, _vp, _vp, _vp, _i32, _i32,
+                                          _vp, _vp, _vp, _sz, _vp]
+    lib.ssl_draft_attn_paged.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp,
+                                         _vp, _sz, _vp]
     lib.ssl_logit_stats_workspace.argtypes = [_i32, _i32, _szp]
     lib.ssl_logit_stats.argtypes = [_vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _sz, _vp]
     lib.ssl_greedy_accept_workspace.argtypes = [_i32, _i32, _i32, _szp]
@@ -104,7 +109,8 @@ def load(path: Optional[str] = None):
                                       _vp, _sz, _vp]
     for f in ("ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn", "ssl_select_workspace",
               "ssl_select_topb", "ssl_draft_workspace", "ssl_draft_attn", "ssl_draft_materialize",
-              "ssl_draft_step_workspace", "ssl_draft_step", "ssl_logit_stats_workspace",
+              "ssl_draft_step_workspace", "ssl_draft_step", "ssl_verify_attn_paged",
+              "ssl_draft_attn_paged", "ssl_logit_stats_workspace",
               "ssl_logit_stats", "ssl_greedy_accept_workspace", "ssl_greedy_accept"):
         getattr(lib, f).restype = ctypes.c_int
     lib.ssl_ctrl_create.argtypes = [ctypes.c_double, _i32p, ctypes.c_int32, ctypes.c_int32]
@@ -315,6 +321,75 @@ def draft_attn(q_draft: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: tor
                                  n_idx.ctypes.data_as(_i32p), _ptr(q_draft), _ptr(k), _ptr(v),
                                  _ptr(idx), _ptr(out), _ptr(workspace), workspace.numel(),
                                  _stream(stream)), "ssl_draft_attn")
+    return out
+
+
+# ---------------------------------------------------------------------------
+# paged KV cache
+# ---------------------------------------------------------------------------
+
+def verify_attn_paged(q: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Tensor,
+                      block_table: torch.Tensor, max_ctx: int, ctx_len, q_len, params: Params,
+                      out: Optional[torch.Tensor] = None, scores: Optional[torch.Tensor] = None,
+                      workspace: Optional[torch.Tensor] = None, stream=None
+                      ) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Verify attention + Eq. 3 scores over a paged cache: k_pages / v_pages
+    [n_pages, Hkv, page_size, 128] bf16, block_table [B, max_blocks] int32;
+    scores are [B, Hkv, max_ctx]."""
+    _need_gpu(q, k_pages, v_pages, block_table)
+    if q.dtype != torch.bfloat16 or k_pages.dtype != torch.bfloat16 or \
+            v_pages.dtype != torch.bfloat16:
+        raise TypeError("q, k_pages, v_pages must be bfloat16")
+    if block_table.dtype != torch.int32 or block_table.dim() != 2 or \
+            block_table.shape[0] != q.shape[0]:
+        raise ValueError("block_table must be int32 [batch, max_blocks]")
+    _, hkv, page, d = k_pages.shape
+    batch, max_q, hq, _ = q.shape
+    shape = Shape(batch, hq, hkv, d, max_ctx, max_q)
+    ctx, ql = _host_i32(ctx_len), _host_i32(q_len)
+    odt = torch.float32 if params.out_fp32 else torch.bfloat16
+    if out is None:
+        out = torch.zeros(q.shape, dtype=odt, device=q.device)
+    if scores is None:
+        scores = torch.zeros((batch, hkv, max_ctx), dtype=torch.float32, device=q.device)
+    _need_gpu(out, scores)
+    need = verify_workspace_bytes(shape, params, ctx, ql)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    _check(load().ssl_verify_attn_paged(ctypes.byref(shape), ctypes.byref(params),
+                                        ctx.ctypes.data_as(_i32p), ql.ctypes.data_as(_i32p),
+                                        _ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(block_table),
+                                        page, block_table.shape[1], _ptr(out), _ptr(scores),
+                                        _ptr(workspace), workspace.numel(), _stream(stream)),
+           "ssl_verify_attn_paged")
+    return out, scores
+
+
+def draft_attn_paged(q_draft: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Tensor,
+                     block_table: torch.Tensor, max_ctx: int, idx: torch.Tensor, n_idx_host,
+                     params: Params, out: Optional[torch.Tensor] = None,
+                     workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Eq. 5 draft attention over a paged cache (layouts as verify_attn_paged)."""
+    _need_gpu(q_draft, k_pages, v_pages, block_table, idx)
+    batch, hq, d = q_draft.shape
+    _, hkv, page, _ = k_pages.shape
+    if idx.dtype != torch.int32 or idx.shape != (batch, hkv, params.budget):
+        raise ValueError("idx must be int32 [batch, n_kv_heads, budget]")
+    shape = Shape(batch, hq, hkv, d, max_ctx, 1)
+    n_idx = _host_i32(n_idx_host)
+    odt = torch.float32 if params.out_fp32 else torch.bfloat16
+    if out is None:
+        out = torch.zeros(q_draft.shape, dtype=odt, device=q_draft.device)
+    _need_gpu(out)
+    need = draft_workspace_bytes(shape, params, n_idx)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q_draft.device)
+    _check(load().ssl_draft_attn_paged(ctypes.byref(shape), ctypes.byref(params),
+                                       n_idx.ctypes.data_as(_i32p), _ptr(q_draft), _ptr(k_pages),
+                                       _ptr(v_pages), _ptr(block_table), page,
+                                       block_table.shape[1], _ptr(idx), _ptr(out),
+                                       _ptr(workspace), workspace.numel(), _stream(stream)),
+           "ssl_draft_attn_paged")
     return out
 
 

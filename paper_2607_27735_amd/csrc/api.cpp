@@ -330,13 +330,34 @@ int ssl_verify_plan(const ssl_shape* shape, const ssl_params* params, const int3
     return SSL_OK;
 }
 
-int ssl_verify_attn(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
-                    const int32_t* q_len_host, const void* q, const void* k_cache,
-                    const void* v_cache, void* out, float* scores, void* workspace,
-                    size_t workspace_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Paged cache arguments: page_size a multiple of 32, every context within
+// max_blocks pages.
+int check_paged(const ssl_shape* s, const int32_t* ctx, const int32_t* block_table,
+                int32_t page_size, int32_t max_blocks) {
+    if (!block_table) return SSL_ERR_NULL;
+    if (!aligned(block_table, 4)) return SSL_ERR_ALIGN;
+    if (page_size < 32 || page_size % 32 != 0 || max_blocks < 1) return SSL_ERR_SHAPE;
+    for (int b = 0; b < s->batch; ++b)
+        if ((int64_t)ctx[b] > (int64_t)page_size * max_blocks) return SSL_ERR_SHAPE;
+    return SSL_OK;
+}
+
+int verify_call(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
+                const int32_t* q_len_host, const void* q, const void* k_cache,
+                const void* v_cache, const int32_t* block_table, int32_t page_size,
+                int32_t max_blocks, void* out, float* scores, void* workspace,
+                size_t workspace_bytes, hipStream_t stream) {
     VerifyPlan plan;
     int rc = plan_verify(shape, params, ctx_len_host, q_len_host, &plan);
     if (rc) return rc;
+    if (block_table || page_size || max_blocks) {
+        rc = check_paged(shape, ctx_len_host, block_table, page_size, max_blocks);
+        if (rc) return rc;
+    }
     if (!q || !k_cache || !v_cache || !out || !scores) return SSL_ERR_NULL;
     if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16) ||
         !aligned(scores, 4))
@@ -344,7 +365,7 @@ int ssl_verify_attn(const ssl_shape* shape, const ssl_params* params, const int3
     rc = check_workspace(workspace, workspace_bytes, plan.bytes);
     if (rc) return rc;
 
-    VerifyArgs a;
+    VerifyArgs a = {};
     a.q = static_cast<const uint16_t*>(q);
     a.k = static_cast<const uint16_t*>(k_cache);
     a.v = static_cast<const uint16_t*>(v_cache);
@@ -362,6 +383,9 @@ int ssl_verify_attn(const ssl_shape* shape, const ssl_params* params, const int3
     a.out_fp32 = params->out_fp32 ? 1 : 0;
     a.scale_log2 = params->sm_scale * 1.4426950408889634f;
     a.seq = plan.seq;
+    a.block_table = block_table;
+    a.page_size = page_size;
+    a.max_blocks = max_blocks;
     if (use_one_sweep(plan, params)) {
         FusedArgs fa;
         fa.v = a;
@@ -377,6 +401,28 @@ int ssl_verify_attn(const ssl_shape* shape, const ssl_params* params, const int3
     return launch_verify(a, plan.n_items, plan.n_rows, plan.row_tiles, stream) == hipSuccess
                ? SSL_OK
                : SSL_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ssl_verify_attn(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
+                    const int32_t* q_len_host, const void* q, const void* k_cache,
+                    const void* v_cache, void* out, float* scores, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream) {
+    return verify_call(shape, params, ctx_len_host, q_len_host, q, k_cache, v_cache, nullptr, 0, 0,
+                       out, scores, workspace, workspace_bytes, stream);
+}
+
+int ssl_verify_attn_paged(const ssl_shape* shape, const ssl_params* params,
+                          const int32_t* ctx_len_host, const int32_t* q_len_host, const void* q,
+                          const void* k_pages, const void* v_pages, const int32_t* block_table,
+                          int32_t page_size, int32_t max_blocks, void* out, float* scores,
+                          void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (!block_table) return SSL_ERR_NULL;
+    return verify_call(shape, params, ctx_len_host, q_len_host, q, k_pages, v_pages, block_table,
+                       page_size, max_blocks, out, scores, workspace, workspace_bytes, stream);
 }
 
 int ssl_select_workspace(const ssl_shape* shape, const ssl_params* params,
@@ -440,13 +486,25 @@ int ssl_draft_workspace(const ssl_shape* shape, const ssl_params* params,
     return SSL_OK;
 }
 
-int ssl_draft_attn(const ssl_shape* shape, const ssl_params* params, const int32_t* n_idx_host,
-                   const void* q_draft, const void* k_cache, const void* v_cache,
-                   const int32_t* idx, void* out, void* workspace, size_t workspace_bytes,
-                   hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+int draft_call(const ssl_shape* shape, const ssl_params* params, const int32_t* n_idx_host,
+               const void* q_draft, const void* k_cache, const void* v_cache,
+               const int32_t* block_table, int32_t page_size, int32_t max_blocks,
+               const int32_t* idx, void* out, void* workspace, size_t workspace_bytes,
+               hipStream_t stream) {
     DraftPlan plan;
     int rc = plan_draft(shape, params, n_idx_host, &plan);
     if (rc) return rc;
+    if (block_table) {
+        // every index is below max_ctx: the pages must cover max_ctx keys
+        if (!aligned(block_table, 4)) return SSL_ERR_ALIGN;
+        if (page_size < 32 || page_size % 32 != 0 || max_blocks < 1 ||
+            (int64_t)page_size * max_blocks < shape->max_ctx)
+            return SSL_ERR_SHAPE;
+    }
     if (!q_draft || !k_cache || !v_cache || !idx || !out) return SSL_ERR_NULL;
     if (!aligned(q_draft, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) ||
         !aligned(out, 16) || !aligned(idx, 4))
@@ -472,7 +530,32 @@ int ssl_draft_attn(const ssl_shape* shape, const ssl_params* params, const int32
     a.out_fp32 = params->out_fp32 ? 1 : 0;
     a.scale_log2 = params->sm_scale * 1.4426950408889634f;
     a.seq = plan.seq;
+    a.block_table = block_table;
+    a.page_size = page_size;
+    a.max_blocks = max_blocks;
     return launch_draft(a, plan.n_items, stream) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ssl_draft_attn(const ssl_shape* shape, const ssl_params* params, const int32_t* n_idx_host,
+                   const void* q_draft, const void* k_cache, const void* v_cache,
+                   const int32_t* idx, void* out, void* workspace, size_t workspace_bytes,
+                   hipStream_t stream) {
+    return draft_call(shape, params, n_idx_host, q_draft, k_cache, v_cache, nullptr, 0, 0, idx,
+                      out, workspace, workspace_bytes, stream);
+}
+
+int ssl_draft_attn_paged(const ssl_shape* shape, const ssl_params* params,
+                         const int32_t* n_idx_host, const void* q_draft, const void* k_pages,
+                         const void* v_pages, const int32_t* block_table, int32_t page_size,
+                         int32_t max_blocks, const int32_t* idx, void* out, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream) {
+    if (!block_table) return SSL_ERR_NULL;
+    return draft_call(shape, params, n_idx_host, q_draft, k_pages, v_pages, block_table, page_size,
+                      max_blocks, idx, out, workspace, workspace_bytes, stream);
 }
 
 int ssl_draft_materialize(const ssl_shape* shape, const ssl_params* params,

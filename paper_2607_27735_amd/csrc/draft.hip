@@ -158,7 +158,7 @@ __device__ __forceinline__ void draft_tile(const DraftArgs& a, const u32x4 (&qop
 // Where an entry's row comes from: the index list (Eq. 5), or a draft-round
 // step whose fixed rows come through the index list or from the materialized
 // copy, and whose window rows are consecutive cache rows.
-constexpr int kPlain = 0, kRoundIdx = 1, kRoundSel = 2;
+constexpr int kPlain = 0, kRoundIdx = 1, kRoundSel = 2, kPlainPaged = 3;
 
 template <int kMode>
 __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
@@ -193,7 +193,8 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) qop[kb] = u32x4{0u, 0u, 0u, 0u};
         }
-        const size_t cache_off = (size_t)it.unit * a.max_ctx * kHeadDim;
+        // (paged: rows are numbered over the whole page pool)
+        const size_t cache_off = kMode == kPlainPaged ? 0 : (size_t)it.unit * a.max_ctx * kHeadDim;
         const size_t sel_off = (size_t)it.unit * a.budget * kHeadDim;
         const RowSource src{a.k + cache_off, a.v + cache_off, a.k_sel + sel_off, a.v_sel + sel_off};
         const int last = it.n - 1;
@@ -203,6 +204,10 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
         uint32_t my_row;
         if (kMode == kPlain) {
             my_row = (uint32_t)min(max(a.idx[(size_t)it.unit * a.budget + e], 0), a.max_ctx - 1);
+        } else if (kMode == kPlainPaged) {
+            const int row = min(max(a.idx[(size_t)it.unit * a.budget + e], 0), a.max_ctx - 1);
+            const int pg = a.block_table[(size_t)it.b * a.max_blocks + row / a.page_size];
+            my_row = (uint32_t)(((size_t)pg * a.n_kv_heads + it.c) * a.page_size + row % a.page_size);
         } else {
             // (the index load does not wait for n_fixed: entry e < budget is in
             // bounds, and its value is used only when e < n_fixed)
@@ -377,7 +382,10 @@ __global__ __launch_bounds__(kDraftThreads) void draft_materialize_kernel(DraftA
 }  // namespace
 
 hipError_t launch_draft(const DraftArgs& a, int n_items, hipStream_t stream) {
-    hipLaunchKernelGGL(draft_kernel<kPlain>, dim3(n_items), dim3(kDraftThreads), 0, stream, a);
+    if (a.block_table)
+        hipLaunchKernelGGL(draft_kernel<kPlainPaged>, dim3(n_items), dim3(kDraftThreads), 0, stream, a);
+    else
+        hipLaunchKernelGGL(draft_kernel<kPlain>, dim3(n_items), dim3(kDraftThreads), 0, stream, a);
     return hipGetLastError();
 }
 

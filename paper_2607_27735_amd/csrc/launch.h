@@ -32,6 +32,11 @@ struct VerifyArgs {
     int32_t n_q_heads, n_kv_heads, group, max_ctx, max_q, window, chunk, out_fp32;
     float scale_log2;   // sm_scale * log2(e)
     SeqTable seq;
+    // Paged cache (block_table non-null): k and v are page pools
+    // [n_pages][n_kv][page_size][128], and key t of sequence b is row
+    // t % page_size of page block_table[b * max_blocks + t / page_size].
+    const int32_t* block_table;
+    int32_t page_size, max_blocks;
 };
 
 // Select splits each (sequence, KV head) unit into partitions of `part`
@@ -82,6 +87,9 @@ struct DraftArgs {
     uint16_t* v_sel;
     int32_t n_fixed[kTableBatch];
     int32_t win0[kTableBatch];
+    // Paged cache, as in VerifyArgs (plain draft only).
+    const int32_t* block_table;
+    int32_t page_size, max_blocks;
 };
 
 // Single-sweep verify: the slots (items of v.seq / v.chunk) of one KV-head

@@ -62,7 +62,7 @@ __device__ __forceinline__ void stats_tile(const VerifyArgs& a, const Rows<NRT>&
     }
 }
 
-template <int NRT>
+template <int NRT, bool kPaged>
 __global__ __launch_bounds__(kThreads) void verify_stats_kernel(VerifyArgs a) {
     const Item it = decode_item(a.seq, blockIdx.x, a.n_kv_heads, a.chunk);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -78,7 +78,14 @@ __global__ __launch_bounds__(kThreads) void verify_stats_kernel(VerifyArgs a) {
     const int ntile = (it.key_end - it.key_begin + kTile - 1) / kTile;
     tile_pipeline<4, KTile>(
         wave, ntile, kWaves,
-        [&](KTile& b, int t) { load_k<false>(kbase, it.key_begin + t * kTile, it.T, m16, G, b.k); },
+        [&](KTile& b, int t) {
+            const int key0 = it.key_begin + t * kTile;
+            if constexpr (kPaged)
+                load_k<false>(a.k + paged_row(a, it.b, it.c, key0) * kHeadDim, 0, it.T - key0, m16,
+                              G, b.k);
+            else
+                load_k<false>(kbase, key0, it.T, m16, G, b.k);
+        },
         [&](const KTile& b, int t) {
             stats_tile<NRT>(a, r, b.k, it.key_begin + t * kTile, G, M, L);
         });
@@ -167,7 +174,7 @@ __device__ __forceinline__ void main_tile(const VerifyArgs& a, const Rows<NRT>& 
     }
 }
 
-template <int NRT>
+template <int NRT, bool kPaged>
 __global__ __launch_bounds__(kThreads) void verify_main_kernel(VerifyArgs a) {
     const Item it = decode_item(a.seq, blockIdx.x, a.n_kv_heads, a.chunk);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -229,8 +236,8 @@ __global__ __launch_bounds__(kThreads) void verify_main_kernel(VerifyArgs a) {
     tile_pipeline<(NRT <= 2 ? 3 : 2), KVTile>(
         wave, ntile, kWaves,
         [&](KVTile& b, int t) {
-            load_k(kbase, it.key_begin + t * kTile, it.T, m16, G, b.k);
-            load_v(vbase, it.key_begin + t * kTile, it.T, m16, G, b.v);
+            load_kv_tile<kPaged, true>(a, kbase, vbase, it.b, it.c, it.key_begin + t * kTile, it.T,
+                                       m16, G, b);
         },
         [&](const KVTile& b, int t) {
             main_tile<NRT>(a, r, lse, b.k, b.v, it.key_begin + t * kTile, it.key_end, srow, m16,
@@ -322,8 +329,13 @@ __global__ __launch_bounds__(kCombineThreads) void verify_combine_kernel(VerifyA
 template <int NRT>
 hipError_t launch_verify_nrt(const VerifyArgs& a, int n_items, int n_rows_total,
                              hipStream_t stream) {
-    hipLaunchKernelGGL(verify_stats_kernel<NRT>, dim3(n_items), dim3(kThreads), 0, stream, a);
-    hipLaunchKernelGGL(verify_main_kernel<NRT>, dim3(n_items), dim3(kThreads), 0, stream, a);
+    if (a.block_table) {
+        hipLaunchKernelGGL((verify_stats_kernel<NRT, true>), dim3(n_items), dim3(kThreads), 0, stream, a);
+        hipLaunchKernelGGL((verify_main_kernel<NRT, true>), dim3(n_items), dim3(kThreads), 0, stream, a);
+    } else {
+        hipLaunchKernelGGL((verify_stats_kernel<NRT, false>), dim3(n_items), dim3(kThreads), 0, stream, a);
+        hipLaunchKernelGGL((verify_main_kernel<NRT, false>), dim3(n_items), dim3(kThreads), 0, stream, a);
+    }
     hipLaunchKernelGGL(verify_combine_kernel, dim3(n_rows_total), dim3(kCombineThreads), 0, stream, a);
     return hipGetLastError();
 }

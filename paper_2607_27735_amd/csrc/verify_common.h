@@ -87,6 +87,30 @@ __device__ __forceinline__ void load_v(const uint16_t* vbase, int key0, int T, i
     }
 }
 
+// Paged cache: the row of key key0 of (sequence b, KV head c), for a tile
+// starting at a multiple of kTile.  Pages hold a multiple of kTile keys, so
+// the tile's rows (clamped to the sequence's last key) lie in that page.
+__device__ __forceinline__ size_t paged_row(const VerifyArgs& a, int b, int c, int key0) {
+    const int pg = a.block_table[(size_t)b * a.max_blocks + key0 / a.page_size];
+    return ((size_t)pg * a.n_kv_heads + c) * a.page_size + key0 % a.page_size;
+}
+
+// Loads the K and V tile at key0 from the dense cache (unit bases kbase,
+// vbase) or, with kPaged, through the block table.
+template <bool kPaged, bool kStream, typename Tile>
+__device__ __forceinline__ void load_kv_tile(const VerifyArgs& a, const uint16_t* kbase,
+                                             const uint16_t* vbase, int b, int c, int key0,
+                                             int T, int m16, int G, Tile& bf) {
+    if constexpr (kPaged) {
+        const size_t r0 = paged_row(a, b, c, key0) * kHeadDim;
+        load_k<kStream>(a.k + r0, 0, T - key0, m16, G, bf.k);
+        load_v<kStream>(a.v + r0, 0, T - key0, m16, G, bf.v);
+    } else {
+        load_k<kStream>(kbase, key0, T, m16, G, bf.k);
+        load_v<kStream>(vbase, key0, T, m16, G, bf.v);
+    }
+}
+
 // Logits^T tile: acc[t][rt][i] = q(row rt*16+m16) . k(key 16t + G + 4i).
 template <int NRT>
 __device__ __forceinline__ void qk_tile(const u32x4 (&kr)[2][4], const Rows<NRT>& r,

@@ -159,7 +159,7 @@ __device__ __forceinline__ void fused_tile(const VerifyArgs& a, const Rows<NRT>&
     }
 }
 
-template <int NRT, bool kStream>
+template <int NRT, bool kStream, bool kPaged>
 __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     const VerifyArgs& a = fa.v;
     extern __shared__ __attribute__((aligned(16))) float stash[];   // [NRT*16][chunk + pad]
@@ -202,8 +202,8 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     tile_pipeline<2, KVTile>(
         wave, ntile, kWaves,
         [&](KVTile& bf, int t) {
-            load_k<kStream>(kbase, key_begin + t * kTile, T, m16, G, bf.k);
-            load_v<kStream>(vbase, key_begin + t * kTile, T, m16, G, bf.v);
+            load_kv_tile<kPaged, kStream>(a, kbase, vbase, b, c, key_begin + t * kTile, T, m16, G,
+                                          bf);
         },
         [&](const KVTile& bf, int t) {
             fused_tile<NRT>(a, r, bf, key_begin + t * kTile, t * kTile, stash, stride, mtile, mts, m16,
@@ -462,21 +462,31 @@ hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, hipStream_t stream)
                                    (fused_max_chunk(NRT) + kStashPad + fused_max_chunk(NRT) / kTile) +
                                kParkFloats) *
                               sizeof(float));
-        e = hipFuncSetAttribute(reinterpret_cast<const void*>(verify_fused_kernel<NRT, true>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-        if (e != hipSuccess) return e;
-        e = hipFuncSetAttribute(reinterpret_cast<const void*>(verify_fused_kernel<NRT, false>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-        if (e != hipSuccess) return e;
+        const void* fns[4] = {reinterpret_cast<const void*>(verify_fused_kernel<NRT, true, false>),
+                              reinterpret_cast<const void*>(verify_fused_kernel<NRT, false, false>),
+                              reinterpret_cast<const void*>(verify_fused_kernel<NRT, true, true>),
+                              reinterpret_cast<const void*>(verify_fused_kernel<NRT, false, true>)};
+        for (const void* f : fns) {
+            e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+            if (e != hipSuccess) return e;
+        }
         e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
         if (e != hipSuccess) return e;
         if (dev >= 0 && dev < kMaxDevices) cus[dev].store(n_cu, std::memory_order_relaxed);
     }
     // non-temporal K/V loads when every workgroup runs in the first round
-    if (n_slots <= n_cu)
-        hipLaunchKernelGGL((verify_fused_kernel<NRT, true>), dim3(n_slots), dim3(kThreads), dyn, stream, a);
-    else
-        hipLaunchKernelGGL((verify_fused_kernel<NRT, false>), dim3(n_slots), dim3(kThreads), dyn, stream, a);
+    const bool paged = a.v.block_table != nullptr;
+    if (n_slots <= n_cu) {
+        if (paged)
+            hipLaunchKernelGGL((verify_fused_kernel<NRT, true, true>), dim3(n_slots), dim3(kThreads), dyn, stream, a);
+        else
+            hipLaunchKernelGGL((verify_fused_kernel<NRT, true, false>), dim3(n_slots), dim3(kThreads), dyn, stream, a);
+    } else {
+        if (paged)
+            hipLaunchKernelGGL((verify_fused_kernel<NRT, false, true>), dim3(n_slots), dim3(kThreads), dyn, stream, a);
+        else
+            hipLaunchKernelGGL((verify_fused_kernel<NRT, false, false>), dim3(n_slots), dim3(kThreads), dyn, stream, a);
+    }
     return hipGetLastError();
 }
 

@@ -272,6 +272,31 @@ def test_greedy_accept_validation(lib):
     assert call(ws=None) == B.SSL_ERR_WORKSPACE
 
 
+def test_paged_validation(lib):
+    s, p = _shape(), _params()
+    ca, cp = _i32(4000)
+    qa, qp = _i32(7)
+
+    def ver(bt=FAKE, page=64, blocks=64, ws=FAKE, ws_bytes=1 << 40):
+        return lib.ssl_verify_attn_paged(ctypes.byref(s), ctypes.byref(p), cp, qp, FAKE, FAKE,
+                                         FAKE, bt, page, blocks, FAKE, FAKE, ws, ws_bytes, None)
+    assert ver(bt=None) == B.SSL_ERR_NULL
+    assert ver(bt=FAKE + 2) == B.SSL_ERR_ALIGN
+    assert ver(page=48) == B.SSL_ERR_SHAPE            # not a multiple of 32
+    assert ver(page=0) == B.SSL_ERR_SHAPE
+    assert ver(blocks=62) == B.SSL_ERR_SHAPE          # 62 * 64 < 4000
+    assert ver(ws=None) == B.SSL_ERR_WORKSPACE         # valid otherwise: stops at the workspace
+    na, npp = _i32(256)
+
+    def dra(bt=FAKE, page=64, blocks=64, ws=FAKE):
+        return lib.ssl_draft_attn_paged(ctypes.byref(s), ctypes.byref(p), npp, FAKE, FAKE, FAKE,
+                                        bt, page, blocks, FAKE, FAKE, ws, 1 << 40, None)
+    assert dra(bt=None) == B.SSL_ERR_NULL
+    assert dra(page=16) == B.SSL_ERR_SHAPE
+    assert dra(blocks=63) == B.SSL_ERR_SHAPE          # 63 * 64 < max_ctx 4096
+    assert dra(ws=None) == B.SSL_ERR_WORKSPACE
+
+
 def test_status_strings(lib):
     seen = set()
     for code in range(0, -8, -1):
