@@ -235,6 +235,88 @@ def vocab_side_bench(B, w, stream, reps, torch, np, vocab=128256):
                       f"rotating {n} logit copies"}
 
 
+def paged_bench(B, w, kvs, q, qd, params, stream, reps, torch, np, page=128):
+    """Verify and draft over a paged copy of the workload's cache (next to the
+    headline, not part of it): each KV copy's rows are placed in a page pool of
+    its own under a shuffled block table; each figure is ``reps`` back-to-back
+    calls (rotating the pools) between two HIP events, beside the same calls on
+    the dense copies."""
+    import ctypes
+    dev = q.device
+    rng = np.random.default_rng(7)
+    max_blocks = (w.max_ctx + page - 1) // page
+    pools = []
+    for (k, v) in kvs:
+        n_pages = w.batch * max_blocks
+        perm = torch.from_numpy(rng.permutation(n_pages).astype(np.int64)).to(dev)
+        # dense [B, Hkv, max_blocks * page, d] -> pages [B * max_blocks, Hkv, page, d]
+        def to_pages(x):
+            pad = max_blocks * page - w.max_ctx
+            if pad:
+                x = torch.nn.functional.pad(x, (0, 0, 0, pad))
+            x = x.reshape(w.batch, w.n_kv_heads, max_blocks, page, w.head_dim)
+            x = x.permute(0, 2, 1, 3, 4).reshape(n_pages, w.n_kv_heads, page, w.head_dim)
+            out = torch.empty_like(x)
+            out[perm] = x
+            return out
+        bt = perm.reshape(w.batch, max_blocks).to(torch.int32)
+        pools.append((to_pages(k), to_pages(v), bt.contiguous()))
+    lib = B.load()
+    vshape = B.Shape(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.max_ctx, w.max_q)
+    ctx, ql = B._host_i32(w.ctx_len), B._host_i32(w.q_len)
+    out = torch.empty(q.shape, dtype=torch.bfloat16, device=dev)
+    sc = torch.empty((w.batch, w.n_kv_heads, w.max_ctx), dtype=torch.float32, device=dev)
+    vws = torch.empty(max(B.verify_workspace_bytes(vshape, params, ctx, ql), 1), dtype=torch.uint8,
+                      device=dev)
+    n_idx = np.array([B.index_count(int(t), w.k_sink, w.k_recent, w.budget) for t in w.ctx_len],
+                     dtype=np.int32)
+    dshape = B.Shape(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.max_ctx, 1)
+    dws = torch.empty(max(B.draft_workspace_bytes(dshape, params, n_idx), 1), dtype=torch.uint8,
+                      device=dev)
+    idx = torch.zeros((w.batch, w.n_kv_heads, w.budget), dtype=torch.int32, device=dev)
+    B.verify_attn(q, kvs[0][0], kvs[0][1], w.ctx_len, w.q_len, params, out=out, scores=sc,
+                  stream=stream)
+    B.select_topb(sc, w.ctx_len, params, n_q_heads=w.n_q_heads, idx=idx, stream=stream)
+    dout = torch.empty(qd.shape, dtype=torch.bfloat16, device=dev)
+    sp, pp = ctypes.byref(vshape), ctypes.byref(params)
+    cp, qp = ctx.ctypes.data_as(B._i32p), ql.ctypes.data_as(B._i32p)
+    dsp, np_ = ctypes.byref(dshape), n_idx.ctypes.data_as(B._i32p)
+    st = B._stream(stream)
+    pv = [(sp, pp, cp, qp, q.data_ptr(), kp.data_ptr(), vp.data_ptr(), bt.data_ptr(), page,
+           max_blocks, out.data_ptr(), sc.data_ptr(), vws.data_ptr(), vws.numel(), st)
+          for (kp, vp, bt) in pools]
+    dv = [(sp, pp, cp, qp, q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), sc.data_ptr(),
+           vws.data_ptr(), vws.numel(), st) for (k, v) in kvs]
+    pd = [(dsp, pp, np_, qd.data_ptr(), kp.data_ptr(), vp.data_ptr(), bt.data_ptr(), page,
+           max_blocks, idx.data_ptr(), dout.data_ptr(), dws.data_ptr(), dws.numel(), st)
+          for (kp, vp, bt) in pools]
+    dd = [(dsp, pp, np_, qd.data_ptr(), k.data_ptr(), v.data_ptr(), idx.data_ptr(),
+           dout.data_ptr(), dws.data_ptr(), dws.numel(), st) for (k, v) in kvs]
+    n = len(pools)
+
+    def timed(fn, args):
+        for a in args:
+            B._check(fn(*a), "paged bench")
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for r in range(reps):
+            fn(*args[r % n])
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    res = {"page_size": page, "max_blocks": max_blocks,
+           "verify_paged_us": round(timed(lib.ssl_verify_attn_paged, pv), 3),
+           "verify_dense_us": round(timed(lib.ssl_verify_attn, dv), 3),
+           "draft_paged_us": round(timed(lib.ssl_draft_attn_paged, pd), 3),
+           "draft_dense_us": round(timed(lib.ssl_draft_attn, dd), 3),
+           "timing": f"{reps} back-to-back calls per figure between two HIP events, "
+                     f"rotating {n} pools / dense copies; block tables shuffled"}
+    del pools
+    return res
+
+
 def summarize_traffic(fetch_dir: str, write_dir: str, copy_mib: int, command: str) -> str:
     """HBM traffic per launch from two rocprofv3 --pmc runs (FETCH_SIZE, then
     WRITE_SIZE, KiB per dispatch), each scaled by what the counter reads for
@@ -530,6 +612,7 @@ def main() -> int:
         result["draft_round"] = draft_round_bench(B, w, kvs, qd, params, scores, stream,
                                                   args.steps, torch, np)
         result["vocab_side"] = vocab_side_bench(B, w, stream, args.steps, torch, np)
+        result["paged"] = paged_bench(B, w, kvs, q, qd, params, stream, args.steps, torch, np)
     # sanity: score mass of every KV head equals min(W, q) * group
     s = scores.double().sum(dim=2).cpu().numpy()
     want = np.array([min(w.window, int(x)) * w.group for x in w.q_len])[:, None]
