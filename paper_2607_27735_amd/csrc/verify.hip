@@ -76,13 +76,14 @@ __global__ __launch_bounds__(kThreads) void verify_stats_kernel(VerifyArgs a) {
     for (int rt = 0; rt < NRT; ++rt) { M[rt] = -INFINITY; L[rt] = 0.f; }
 
     const int ntile = (it.key_end - it.key_begin + kTile - 1) / kTile;
+    const int pages = kPaged ? wave_pages(a, it.b, it.key_begin, ntile, wave, lane) : 0;
     tile_pipeline<4, KTile>(
         wave, ntile, kWaves,
         [&](KTile& b, int t) {
             const int key0 = it.key_begin + t * kTile;
             if constexpr (kPaged)
-                load_k<false>(a.k + paged_row(a, it.b, it.c, key0) * kHeadDim, 0, it.T - key0, m16,
-                              G, b.k);
+                load_k<false>(a.k + paged_row(a, tile_page(pages, t, wave), it.c, key0) * kHeadDim,
+                              0, it.T - key0, m16, G, b.k);
             else
                 load_k<false>(kbase, key0, it.T, m16, G, b.k);
         },
@@ -187,6 +188,7 @@ __global__ __launch_bounds__(kThreads) void verify_main_kernel(VerifyArgs a) {
     const uint16_t* vbase = a.v + cache_off;
     float* srow = a.scores + (size_t)it.unit * a.max_ctx;
     const int ntile = (it.key_end - it.key_begin + kTile - 1) / kTile;
+    const int pages = kPaged ? wave_pages(a, it.b, it.key_begin, ntile, wave, lane) : 0;
 
     // Row log-sum-exp from the statistics of every item of this (sequence, KV
     // head), computed while the first K/V tiles are loading: thread t merges
@@ -236,8 +238,8 @@ __global__ __launch_bounds__(kThreads) void verify_main_kernel(VerifyArgs a) {
     tile_pipeline<(NRT <= 2 ? 3 : 2), KVTile>(
         wave, ntile, kWaves,
         [&](KVTile& b, int t) {
-            load_kv_tile<kPaged, true>(a, kbase, vbase, it.b, it.c, it.key_begin + t * kTile, it.T,
-                                       m16, G, b);
+            load_kv_tile<kPaged, true>(a, kbase, vbase, kPaged ? tile_page(pages, t, wave) : 0, it.c,
+                                       it.key_begin + t * kTile, it.T, m16, G, b);
         },
         [&](const KVTile& b, int t) {
             main_tile<NRT>(a, r, lse, b.k, b.v, it.key_begin + t * kTile, it.key_end, srow, m16,

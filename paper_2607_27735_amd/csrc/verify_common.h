@@ -87,22 +87,35 @@ __device__ __forceinline__ void load_v(const uint16_t* vbase, int key0, int T, i
     }
 }
 
-// Paged cache: the row of key key0 of (sequence b, KV head c), for a tile
-// starting at a multiple of kTile.  Pages hold a multiple of kTile keys, so
-// the tile's rows (clamped to the sequence's last key) lie in that page.
-__device__ __forceinline__ size_t paged_row(const VerifyArgs& a, int b, int c, int key0) {
-    const int pg = a.block_table[(size_t)b * a.max_blocks + key0 / a.page_size];
-    return ((size_t)pg * a.n_kv_heads + c) * a.page_size + key0 % a.page_size;
+// Paged cache.  Pages hold a multiple of kTile keys, so a tile (starting at a
+// multiple of kTile; its rows clamped to the sequence's last key) lies in one
+// page.  A wave's tiles are first, first + kWaves, ...: lane l of
+// wave_pages() holds the page of the wave's tile l, loaded once before the
+// sweep, and a tile reads it back with readlane instead of waiting for a
+// table load in front of its own loads.
+__device__ __forceinline__ int wave_pages(const VerifyArgs& a, int b, int key_begin, int ntile,
+                                          int first, int lane) {
+    const int t = min(first + kWaves * lane, ntile - 1);
+    return a.block_table[(size_t)b * a.max_blocks + (key_begin + t * kTile) / a.page_size];
+}
+
+__device__ __forceinline__ size_t paged_row(const VerifyArgs& a, int page, int c, int key0) {
+    return ((size_t)page * a.n_kv_heads + c) * a.page_size + key0 % a.page_size;
+}
+
+// The page of tile t (wave-uniform) from wave_pages()' lanes.
+__device__ __forceinline__ int tile_page(int pages, int t, int first) {
+    return __builtin_amdgcn_readlane(pages, (t - first) / kWaves);
 }
 
 // Loads the K and V tile at key0 from the dense cache (unit bases kbase,
-// vbase) or, with kPaged, through the block table.
+// vbase) or, with kPaged, from page `page`.
 template <bool kPaged, bool kStream, typename Tile>
 __device__ __forceinline__ void load_kv_tile(const VerifyArgs& a, const uint16_t* kbase,
-                                             const uint16_t* vbase, int b, int c, int key0,
+                                             const uint16_t* vbase, int page, int c, int key0,
                                              int T, int m16, int G, Tile& bf) {
     if constexpr (kPaged) {
-        const size_t r0 = paged_row(a, b, c, key0) * kHeadDim;
+        const size_t r0 = paged_row(a, page, c, key0) * kHeadDim;
         load_k<kStream>(a.k + r0, 0, T - key0, m16, G, bf.k);
         load_v<kStream>(a.v + r0, 0, T - key0, m16, G, bf.v);
     } else {

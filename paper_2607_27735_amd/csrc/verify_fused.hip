@@ -199,11 +199,12 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         for (int jd = 0; jd < 8; ++jd) oacc[jd][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
     const int ntile = (key_end - key_begin + kTile - 1) / kTile;
+    const int pages = kPaged ? wave_pages(a, b, key_begin, ntile, wave, lane) : 0;
     tile_pipeline<2, KVTile>(
         wave, ntile, kWaves,
         [&](KVTile& bf, int t) {
-            load_kv_tile<kPaged, kStream>(a, kbase, vbase, b, c, key_begin + t * kTile, T, m16, G,
-                                          bf);
+            load_kv_tile<kPaged, kStream>(a, kbase, vbase, kPaged ? tile_page(pages, t, wave) : 0,
+                                          c, key_begin + t * kTile, T, m16, G, bf);
         },
         [&](const KVTile& bf, int t) {
             fused_tile<NRT>(a, r, bf, key_begin + t * kTile, t * kTile, stash, stride, mtile, mts, m16,
