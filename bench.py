@@ -74,6 +74,20 @@ def kernel_short(name: str) -> str:
     return name
 
 
+def is_paged(short: str) -> bool:
+    """Whether a kernel (short name with template arguments) is the paged-cache
+    instance: the last template flag of the verify kernels, mode 3 of the draft."""
+    if "<" not in short:
+        return False
+    args = [x.strip() for x in short.split("<", 1)[1].rstrip(">").split(",")]
+    k = short.split("<")[0]
+    if k == "verify_fused_kernel":
+        return len(args) == 3 and args[2] == "true"
+    if k in ("verify_stats_kernel", "verify_main_kernel"):
+        return len(args) == 2 and args[1] == "true"
+    return k == "draft_kernel" and args == ["3"]
+
+
 def summarize_trace(d: str, command: str) -> str:
     """Markdown table of a rocprofv3 --kernel-trace --stats run."""
     import csv
@@ -89,7 +103,9 @@ def summarize_trace(d: str, command: str) -> str:
     for r in rows:
         short = kernel_short(r["Name"])
         k = short.split("<")[0]
-        call = ("verify" if k.startswith("verify") else "select" if k.startswith("select")
+        call = ("verify (paged)" if k.startswith("verify") and is_paged(short)
+                else "draft (paged)" if is_paged(short)
+                else "verify" if k.startswith("verify") else "select" if k.startswith("select")
                 else "draft round materialize" if "materialize" in k
                 else "draft round step (index list)" if short == "draft_kernel<1>"
                 else "draft round step (materialized rows)" if short == "draft_kernel<2>"
@@ -354,7 +370,7 @@ def summarize_traffic(fetch_dir: str, write_dir: str, copy_mib: int, command: st
         fb = fetch.get(k, 0.0) * 1024.0 * f_fac
         wb = write.get(k, 0.0) * 1024.0 * w_fac
         lines.append(f"{k} = fetch {fb:.0f} write {wb:.0f} bytes per launch")
-        if k.split("<")[0] in VERIFY_KERNELS:
+        if k.split("<")[0] in VERIFY_KERNELS and not is_paged(k):
             call_bytes += fb + wb
     lines.append(f"verify_call_traffic_bytes = {call_bytes:.0f}")
     return "\n".join(lines) + "\n"
