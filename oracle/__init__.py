@@ -60,6 +60,12 @@ def _bind(lib):
     lib.oracle_greedy_accept.argtypes = [ctypes.c_int] * 4 + [_i32p, _u16p, _f32p, _i32p, _i32p,
                                                               _i32p]
     lib.oracle_greedy_accept.restype = ctypes.c_int
+    lib.oracle_head_scores.argtypes = [ctypes.c_int] * 6 + [_i32p, _i32p, _u16p, _u16p,
+                                                            ctypes.c_double, ctypes.c_int, _f64p]
+    lib.oracle_head_scores.restype = ctypes.c_int
+    lib.oracle_draft_heads.argtypes = [ctypes.c_int] * 6 + [_i32p, _u16p, _u16p, _u16p, _i32p,
+                                                            ctypes.c_double, _f64p]
+    lib.oracle_draft_heads.restype = ctypes.c_int
     lib.oracle_index_count.argtypes = [ctypes.c_int] * 4
     lib.oracle_index_count.restype = ctypes.c_int
     lib.oracle_ema.argtypes = [ctypes.c_double] * 3
@@ -238,6 +244,40 @@ def greedy_accept(logits: np.ndarray, draft: np.ndarray, k_len, vocab: Optional[
                                 _p(m, _i32p), _p(t, _i32p)) != 0:
         raise ValueError("oracle_greedy_accept rejected its arguments")
     return m, t
+
+
+def head_scores(w, *, q=None, k=None, ctx_len=None, q_len=None, lib=None):
+    """Eq. 3 per query head: float64 ``[batch][Hq][max_ctx]``."""
+    lib = lib or load()
+    q = _c(w.q if q is None else q, np.uint16)
+    k = _c(w.k if k is None else k, np.uint16)
+    ctx = _c(w.ctx_len if ctx_len is None else ctx_len, np.int32)
+    ql = _c(w.q_len if q_len is None else q_len, np.int32)
+    sc = np.zeros((w.batch, w.n_q_heads, w.max_ctx), dtype=np.float64)
+    rc = lib.oracle_head_scores(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.max_ctx, w.max_q,
+                                _p(ctx, _i32p), _p(ql, _i32p), _p(q, _u16p), _p(k, _u16p),
+                                float(w.sm_scale), int(w.window), _p(sc, _f64p))
+    if rc != 0:
+        raise ValueError("oracle_head_scores rejected its arguments")
+    return sc
+
+
+def draft_heads(w, idx: np.ndarray, n_idx: np.ndarray, *, q_draft=None, k=None, v=None, lib=None):
+    """Eq. 5 with one index set per query head (idx ``[batch][Hq][budget]``);
+    float64 ``[batch][Hq][d]``."""
+    lib = lib or load()
+    qd = _c(w.q_draft if q_draft is None else q_draft, np.uint16)
+    k = _c(w.k if k is None else k, np.uint16)
+    v = _c(w.v if v is None else v, np.uint16)
+    idx = _c(idx, np.int32)
+    n = _c(n_idx, np.int32)
+    out = np.zeros((w.batch, w.n_q_heads, w.head_dim), dtype=np.float64)
+    rc = lib.oracle_draft_heads(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.max_ctx,
+                                idx.shape[-1], _p(n, _i32p), _p(qd, _u16p), _p(k, _u16p),
+                                _p(v, _u16p), _p(idx, _i32p), float(w.sm_scale), _p(out, _f64p))
+    if rc != 0:
+        raise ValueError("oracle_draft_heads rejected its arguments")
+    return out
 
 
 def ema(prev: float, observed: float, beta: float, lib=None) -> float:

@@ -493,3 +493,109 @@ int oracle_greedy_accept(int batch, int max_k, int vocab, int row_stride, const 
     free(t);
     return rc;
 }
+
+/* ---------------------------------------------------------------------------
+ * Per-query-head variant of Eq. 3 / Eq. 5 (Sec. 3.2 states importance "for
+ * every layer and attention head"; the main path keeps it per KV head).
+ * ------------------------------------------------------------------------- */
+
+/*
+ * Eq. 3 per query head: scores[b,h,i] = sum over the last min(W, q) verify
+ * rows j of P_{j,h,i}, the softmax probability of row j, head h on key i
+ * (causal as in oracle_verify).  Layout [batch][Hq][max_ctx]; entries past T
+ * are left untouched, entries below T start at 0.  Returns 0 or -1.
+ */
+int oracle_head_scores(int batch, int n_q_heads, int n_kv_heads, int head_dim, int max_ctx,
+                       int max_q, const int32_t *ctx_len, const int32_t *q_len,
+                       const uint16_t *q, const uint16_t *k, double sm_scale, int window,
+                       double *scores)
+{
+    if (batch < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads != 0 || head_dim < 1 ||
+        window < 1)
+        return -1;
+    for (int b = 0; b < batch; ++b)
+        if (q_len[b] < 1 || q_len[b] > max_q || ctx_len[b] < q_len[b] || ctx_len[b] > max_ctx)
+            return -1;
+    const int g = n_q_heads / n_kv_heads;
+    const int d = head_dim;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int bh = 0; bh < batch * n_q_heads; ++bh) {
+        const int b = bh / n_q_heads, h = bh % n_q_heads, c = h / g;
+        const int T = ctx_len[b], nq = q_len[b];
+        const int w = window < nq ? window : nq;
+        double *S = scores + ((size_t)b * n_q_heads + h) * max_ctx;
+        const uint16_t *kc = k + ((size_t)b * n_kv_heads + c) * max_ctx * d;
+        double *x = (double *)malloc(sizeof(double) * (size_t)T);
+        for (int i = 0; i < T; ++i) S[i] = 0.0;
+        for (int j = nq - w; j < nq; ++j) {
+            const int p = T - nq + j;
+            const uint16_t *qs = q + (((size_t)b * max_q + j) * n_q_heads + h) * d;
+            double m = -INFINITY;
+            for (int i = 0; i <= p; ++i) {
+                double dot = 0.0;
+                for (int e = 0; e < d; ++e)
+                    dot += widen_bf16(qs[e]) * widen_bf16(kc[(size_t)i * d + e]);
+                x[i] = sm_scale * dot;
+                if (x[i] > m) m = x[i];
+            }
+            double L = 0.0;
+            for (int i = 0; i <= p; ++i) {
+                x[i] = exp(x[i] - m);
+                L += x[i];
+            }
+            for (int i = 0; i <= p; ++i) S[i] += x[i] / L;
+        }
+        free(x);
+    }
+    return 0;
+}
+
+/*
+ * Eq. 5 with one index set per query head: head h of sequence b attends over
+ * the n = n_idx[b] rows I = idx[b,h,0..n) of its KV head c = h / g.
+ * Layouts: idx [batch][Hq][budget], q_draft / out [batch][Hq][d].
+ * Returns 0 or -1.
+ */
+int oracle_draft_heads(int batch, int n_q_heads, int n_kv_heads, int head_dim, int max_ctx,
+                       int budget, const int32_t *n_idx, const uint16_t *q_draft,
+                       const uint16_t *k, const uint16_t *v, const int32_t *idx,
+                       double sm_scale, double *out)
+{
+    if (batch < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads != 0 || head_dim < 1)
+        return -1;
+    for (int b = 0; b < batch; ++b)
+        if (n_idx[b] < 1 || n_idx[b] > budget) return -1;
+    const int g = n_q_heads / n_kv_heads;
+    const int d = head_dim;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int bh = 0; bh < batch * n_q_heads; ++bh) {
+        const int b = bh / n_q_heads, h = bh % n_q_heads, c = h / g;
+        const int n = n_idx[b];
+        const int32_t *I = idx + ((size_t)b * n_q_heads + h) * budget;
+        const uint16_t *kc = k + ((size_t)b * n_kv_heads + c) * max_ctx * d;
+        const uint16_t *vc = v + ((size_t)b * n_kv_heads + c) * max_ctx * d;
+        const uint16_t *qs = q_draft + ((size_t)b * n_q_heads + h) * d;
+        double *x = (double *)malloc(sizeof(double) * (size_t)n);
+        double m = -INFINITY;
+        for (int t = 0; t < n; ++t) {
+            double dot = 0.0;
+            for (int e = 0; e < d; ++e)
+                dot += widen_bf16(qs[e]) * widen_bf16(kc[(size_t)I[t] * d + e]);
+            x[t] = sm_scale * dot;
+            if (x[t] > m) m = x[t];
+        }
+        double L = 0.0;
+        for (int t = 0; t < n; ++t) {
+            x[t] = exp(x[t] - m);
+            L += x[t];
+        }
+        double *o = out + ((size_t)b * n_q_heads + h) * d;
+        for (int e = 0; e < d; ++e) o[e] = 0.0;
+        for (int t = 0; t < n; ++t) {
+            const double P = x[t] / L;
+            for (int e = 0; e < d; ++e) o[e] += P * widen_bf16(vc[(size_t)I[t] * d + e]);
+        }
+        free(x);
+    }
+    return 0;
+}

@@ -442,6 +442,60 @@ def pin_draft_step_value_one(lib):
 
 
 # ---------------------------------------------------------------------------
+# per-query-head scores and draft (Eq. 3 / Eq. 5 per attention head)
+# ---------------------------------------------------------------------------
+
+def pin_head_scores_match_softmax(lib):
+    """Per-head Eq. 3 against torch.softmax weights of each query head, the
+    per-head mass min(W, q), and the group sum against the per-KV-head scores."""
+    w = _tiny(91, hq=8, hkv=2, ctx=(50, 33), ql=(5, 3), window=4)
+    S = oracle.head_scores(w, lib=lib)
+    q = _bf16_to_t64(w.q)
+    k = _bf16_to_t64(w.k)
+    g = w.group
+    for b in range(w.batch):
+        T, nq = int(w.ctx_len[b]), int(w.q_len[b])
+        wn = min(w.window, nq)
+        for h in range(w.n_q_heads):
+            c = h // g
+            logits = (q[b, nq - wn:nq, h, :] @ k[b, c, :T].T) * w.sm_scale     # [wn, T]
+            rows = torch.arange(nq - wn, nq) + (T - nq)
+            mask = torch.arange(T)[None, :] <= rows[:, None]
+            P = torch.softmax(logits.masked_fill(~mask, -math.inf), dim=-1)
+            assert np.abs(S[b, h, :T] - P.sum(dim=0).numpy()).max() < 1e-12
+            assert abs(S[b, h, :T].sum() - wn) < 1e-10
+    _, Skv = oracle.verify(w, lib=lib)
+    Sg = S.reshape(w.batch, w.n_kv_heads, g, w.max_ctx).sum(axis=2)
+    assert np.abs(Sg - Skv).max() < 1e-12
+
+
+def pin_draft_heads(lib):
+    """Per-head draft against SDPA per head; with one set shared by a group's
+    heads it is the per-KV-head draft."""
+    rng = np.random.default_rng(92)
+    w = _tiny(93, hq=8, hkv=2, ctx=(70, 40), ql=(1, 1), B=16)
+    n_idx = np.array([16, 11], dtype=np.int32)
+    idx = np.zeros((2, 8, 16), dtype=np.int32)
+    for b in range(2):
+        for h in range(8):
+            idx[b, h, :n_idx[b]] = np.sort(rng.choice(int(w.ctx_len[b]), n_idx[b], replace=False))
+    out = oracle.draft_heads(w, idx, n_idx, lib=lib)
+    qd = _bf16_to_t64(w.q_draft); k = _bf16_to_t64(w.k); v = _bf16_to_t64(w.v)
+    for b in range(2):
+        for h in range(8):
+            c = h // 4
+            I = torch.from_numpy(idx[b, h, :n_idx[b]].astype(np.int64))
+            o = F.scaled_dot_product_attention(qd[b, h][None, None, None], k[b, c, I][None, None],
+                                               v[b, c, I][None, None], scale=w.sm_scale)
+            assert np.abs(out[b, h] - o[0, 0, 0].numpy()).max() < 1e-12
+    shared = idx.reshape(2, 2, 4, 16)[:, :, 0, :]                  # head 4c's set for the group
+    per_head = np.repeat(shared, 4, axis=1)
+    o1 = oracle.draft_heads(w, per_head, n_idx, lib=lib)
+    o2 = oracle.draft(w, shared, n_idx, lib=lib)
+    assert np.abs(o1 - o2).max() < 1e-12
+
+
+# ---------------------------------------------------------------------------
 # around the path: token entropy and greedy acceptance
 # ---------------------------------------------------------------------------
 
@@ -585,5 +639,6 @@ ALL_PINS = [pin_verify_matches_sdpa, pin_verify_value_one, pin_verify_zero_keys_
             pin_select_special_cases, pin_draft_matches_sdpa, pin_draft_full_equals_dense,
             pin_draft_permutation, pin_draft_step_first_matches_sdpa,
             pin_draft_step_worked_example, pin_draft_step_value_one, pin_row_stats_library,
-            pin_row_stats_closed_forms, pin_greedy_accept_worked,
+            pin_row_stats_closed_forms, pin_greedy_accept_worked, pin_head_scores_match_softmax,
+            pin_draft_heads,
             pin_controller_closed_forms, pin_controller_argmax]

@@ -56,6 +56,11 @@ MUTANTS = [
     ("accept_one_past_mismatch", "while (m < k_len[b] && db[m] == tb[m]) ++m;",
      "while (m < k_len[b] && db[m] == tb[m]) ++m;\n            if (m < k_len[b]) ++m;"),
     ("next_token_from_row_after", "next_token[b] = tb[m];", "next_token[b] = tb[m < k_len[b] ? m + 1 : m];"),
+    ("head_scores_kv_head_modulo", "const int b = bh / n_q_heads, h = bh % n_q_heads, c = h / g;\n        const int T = ctx_len[b], nq = q_len[b];",
+     "const int b = bh / n_q_heads, h = bh % n_q_heads, c = h % n_kv_heads;\n        const int T = ctx_len[b], nq = q_len[b];"),
+    ("head_scores_all_rows", "for (int j = nq - w; j < nq; ++j) {", "for (int j = 0; j < nq; ++j) {"),
+    ("draft_heads_shared_set", "const int32_t *I = idx + ((size_t)b * n_q_heads + h) * budget;",
+     "const int32_t *I = idx + ((size_t)b * n_q_heads + c * g) * budget;"),
     ("ema_weights_swapped", "return beta * prev + (1.0 - beta) * observed;",
      "return beta * observed + (1.0 - beta) * prev;"),
     ("accept_prob_inverted", "return ea / (ea + er);", "return er / (ea + er);"),
