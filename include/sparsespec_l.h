@@ -93,6 +93,16 @@ typedef struct {
     int32_t budget;      /* K_total = K_sink + K_mid + K_recent of Eq. 4 */
     int32_t out_fp32;    /* 1: outputs are fp32, 0: bf16 (round to nearest even) */
     int32_t verify_mode; /* SSL_VERIFY_AUTO, SSL_VERIFY_TWO_SWEEP or SSL_VERIFY_ONE_SWEEP */
+    int32_t per_head;    /* 0: importance and index sets per KV head (Eq. 3 summed over the
+                          *    query heads of the group);
+                          * 1: per query head (Sec. 3.2 keeps importance for every attention
+                          *    head): verify writes scores [batch][Hq][max_ctx] (each head's
+                          *    own window rows), select builds one index set per query head
+                          *    (scores, idx [batch][Hq][...]), and draft gives each query
+                          *    head its own set idx[b][h] over the rows of KV head h / group.
+                          *    Two-sweep verify needs the group to be 1, 2, 4, 8 or 16
+                          *    (SSL_ERR_UNSUPPORTED otherwise); the draft-round calls do not
+                          *    take it (SSL_ERR_UNSUPPORTED).  Other values: SSL_ERR_SHAPE. */
 } ssl_params;
 
 /* How ssl_verify_attn schedules its work (results agree to rounding):

@@ -55,7 +55,7 @@ class Params(ctypes.Structure):
     _fields_ = [("sm_scale", ctypes.c_float), ("window", ctypes.c_int32),
                 ("k_sink", ctypes.c_int32), ("k_recent", ctypes.c_int32),
                 ("budget", ctypes.c_int32), ("out_fp32", ctypes.c_int32),
-                ("verify_mode", ctypes.c_int32)]
+                ("verify_mode", ctypes.c_int32), ("per_head", ctypes.c_int32)]
 
 
 class SSLError(RuntimeError):
@@ -164,9 +164,10 @@ def _need_gpu(*ts: torch.Tensor) -> None:
 
 
 def make_params(sm_scale: float, window: int = 16, k_sink: int = 4, k_recent: int = 32,
-                budget: int = 2048, out_fp32: bool = False, verify_mode: int = VERIFY_AUTO) -> Params:
+                budget: int = 2048, out_fp32: bool = False, verify_mode: int = VERIFY_AUTO,
+                per_head: bool = False) -> Params:
     return Params(float(sm_scale), int(window), int(k_sink), int(k_recent), int(budget),
-                  1 if out_fp32 else 0, int(verify_mode))
+                  1 if out_fp32 else 0, int(verify_mode), 1 if per_head else 0)
 
 
 def index_count(T: int, k_sink: int, k_recent: int, budget: int) -> int:
@@ -222,13 +223,14 @@ def verify_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, ctx_len, q_le
     odt = torch.float32 if params.out_fp32 else torch.bfloat16
     if out is None:
         out = torch.zeros(q.shape, dtype=odt, device=q.device)
+    heads = shape.n_q_heads if params.per_head else shape.n_kv_heads   # score rows per sequence
     if scores is None:
-        scores = torch.zeros((shape.batch, shape.n_kv_heads, shape.max_ctx), dtype=torch.float32,
+        scores = torch.zeros((shape.batch, heads, shape.max_ctx), dtype=torch.float32,
                              device=q.device)
     _need_gpu(out, scores)
     if out.dtype != odt or scores.dtype != torch.float32:
         raise TypeError("out dtype must match params.out_fp32; scores must be float32")
-    if out.shape != q.shape or scores.shape != (shape.batch, shape.n_kv_heads, shape.max_ctx):
+    if out.shape != q.shape or scores.shape != (shape.batch, heads, shape.max_ctx):
         raise ValueError("out/scores shape")
     need = verify_workspace_bytes(shape, params, ctx, ql)
     if workspace is None or workspace.numel() < need:
@@ -307,8 +309,9 @@ def draft_attn(q_draft: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: tor
     batch, hq, d = q_draft.shape
     _, hkv, max_ctx, _ = k.shape
     shape = Shape(batch, hq, hkv, d, max_ctx, 1)
-    if idx.shape != (batch, hkv, params.budget):
-        raise ValueError("idx must be [batch, n_kv_heads, budget]")
+    units = hq if params.per_head else hkv
+    if idx.shape != (batch, units, params.budget):
+        raise ValueError("idx must be [batch, n_kv_heads (n_q_heads if per_head), budget]")
     n_idx = _host_i32(n_idx_host)
     odt = torch.float32 if params.out_fp32 else torch.bfloat16
     if out is None:
@@ -351,7 +354,7 @@ def verify_attn_paged(q: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Ten
     if out is None:
         out = torch.zeros(q.shape, dtype=odt, device=q.device)
     if scores is None:
-        scores = torch.zeros((batch, hkv, max_ctx), dtype=torch.float32, device=q.device)
+        scores = torch.zeros((batch, hq if params.per_head else hkv, max_ctx), dtype=torch.float32, device=q.device)
     _need_gpu(out, scores)
     need = verify_workspace_bytes(shape, params, ctx, ql)
     if workspace is None or workspace.numel() < need:
@@ -373,8 +376,9 @@ def draft_attn_paged(q_draft: torch.Tensor, k_pages: torch.Tensor, v_pages: torc
     _need_gpu(q_draft, k_pages, v_pages, block_table, idx)
     batch, hq, d = q_draft.shape
     _, hkv, page, _ = k_pages.shape
-    if idx.dtype != torch.int32 or idx.shape != (batch, hkv, params.budget):
-        raise ValueError("idx must be int32 [batch, n_kv_heads, budget]")
+    units = hq if params.per_head else hkv
+    if idx.dtype != torch.int32 or idx.shape != (batch, units, params.budget):
+        raise ValueError("idx must be int32 [batch, n_kv_heads (n_q_heads if per_head), budget]")
     shape = Shape(batch, hq, hkv, d, max_ctx, 1)
     n_idx = _host_i32(n_idx_host)
     odt = torch.float32 if params.out_fp32 else torch.bfloat16

@@ -40,7 +40,16 @@ int check_budget(const ssl_params* p) {
     if (!p) return SSL_ERR_NULL;
     if (p->budget < 1 || p->k_sink < 0 || p->k_recent < 0) return SSL_ERR_BUDGET;
     if ((int64_t)p->k_sink + p->k_recent > p->budget) return SSL_ERR_BUDGET;
+    if (p->per_head != 0 && p->per_head != 1) return SSL_ERR_SHAPE;
     return SSL_OK;
+}
+
+// One index set per query head: select and draft work on units (sequence,
+// query head), each reading the cache rows of KV head h / group.
+ssl_shape unit_shape(const ssl_shape* s, const ssl_params* p) {
+    ssl_shape u = *s;
+    if (p->per_head) u.n_kv_heads = s->n_q_heads;
+    return u;
 }
 
 // Verify work decomposition.  Two-sweep items are (sequence, KV head, key
@@ -386,6 +395,12 @@ int verify_call(const ssl_shape* shape, const ssl_params* params, const int32_t*
     a.block_table = block_table;
     a.page_size = page_size;
     a.max_blocks = max_blocks;
+    a.per_head = params->per_head;
+    if (params->per_head && !use_one_sweep(plan, params)) {
+        // two sweeps sum a head's rows across the 16 lanes of a row tile
+        const int g = a.group;
+        if (g > 16 || (g & (g - 1)) != 0) return SSL_ERR_UNSUPPORTED;
+    }
     if (use_one_sweep(plan, params)) {
         FusedArgs fa;
         fa.v = a;
@@ -430,8 +445,9 @@ int ssl_select_workspace(const ssl_shape* shape, const ssl_params* params,
     if (!bytes_out) return SSL_ERR_NULL;
     int rc = check_select(shape, params, ctx_len_host);
     if (rc) return rc;
+    const ssl_shape us = unit_shape(shape, params);
     SelectPlan plan;
-    rc = plan_select(shape, ctx_len_host, &plan);
+    rc = plan_select(&us, ctx_len_host, &plan);
     if (rc) return rc;
     *bytes_out = plan.bytes;
     return SSL_OK;
@@ -444,8 +460,9 @@ int ssl_select_topb(const ssl_shape* shape, const ssl_params* params, const int3
     if (rc) return rc;
     if (!scores || !idx || !n_idx) return SSL_ERR_NULL;
     if (!aligned(scores, 4) || !aligned(idx, 4) || !aligned(n_idx, 4)) return SSL_ERR_ALIGN;
+    const ssl_shape us = unit_shape(shape, params);
     SelectPlan plan;
-    rc = plan_select(shape, ctx_len_host, &plan);
+    rc = plan_select(&us, ctx_len_host, &plan);
     if (rc) return rc;
     rc = check_workspace(workspace, workspace_bytes, plan.bytes);
     if (rc) return rc;
@@ -465,22 +482,25 @@ int ssl_select_topb(const ssl_shape* shape, const ssl_params* params, const int3
     a.call_tag = next_call_tag();
     a.part = plan.part;
     a.parts = plan.parts;
-    a.n_kv_heads = shape->n_kv_heads;
+    a.n_kv_heads = us.n_kv_heads;
     a.max_ctx = shape->max_ctx;
     a.k_sink = params->k_sink;
     a.k_recent = params->k_recent;
     a.budget = params->budget;
     a.batch = shape->batch;
     for (int b = 0; b < shape->batch; ++b) a.ctx[b] = ctx_len_host[b];
-    return launch_select(a, shape->batch * shape->n_kv_heads, stream) == hipSuccess ? SSL_OK
-                                                                                   : SSL_ERR_HIP;
+    return launch_select(a, shape->batch * us.n_kv_heads, stream) == hipSuccess ? SSL_OK
+                                                                                : SSL_ERR_HIP;
 }
 
 int ssl_draft_workspace(const ssl_shape* shape, const ssl_params* params,
                         const int32_t* n_idx_host, size_t* bytes_out) {
-    if (!bytes_out) return SSL_ERR_NULL;
+    if (!bytes_out || !shape || !params) return SSL_ERR_NULL;
+    int rc = check_budget(params);
+    if (rc) return rc;
+    const ssl_shape us = unit_shape(shape, params);
     DraftPlan plan;
-    const int rc = plan_draft(shape, params, n_idx_host, &plan);
+    rc = plan_draft(&us, params, n_idx_host, &plan);
     if (rc) return rc;
     *bytes_out = plan.bytes;
     return SSL_OK;
@@ -495,8 +515,12 @@ int draft_call(const ssl_shape* shape, const ssl_params* params, const int32_t* 
                const int32_t* block_table, int32_t page_size, int32_t max_blocks,
                const int32_t* idx, void* out, void* workspace, size_t workspace_bytes,
                hipStream_t stream) {
+    if (!shape || !params) return SSL_ERR_NULL;
+    int rc = check_budget(params);
+    if (rc) return rc;
+    const ssl_shape us = unit_shape(shape, params);
     DraftPlan plan;
-    int rc = plan_draft(shape, params, n_idx_host, &plan);
+    rc = plan_draft(&us, params, n_idx_host, &plan);
     if (rc) return rc;
     if (block_table) {
         // every index is below max_ctx: the pages must cover max_ctx keys
@@ -522,8 +546,10 @@ int draft_call(const ssl_shape* shape, const ssl_params* params, const int32_t* 
     a.call_tag = next_call_tag();
     a.out = out;
     a.n_q_heads = shape->n_q_heads;
-    a.n_kv_heads = shape->n_kv_heads;
-    a.group = shape->n_q_heads / shape->n_kv_heads;
+    a.n_kv_heads = us.n_kv_heads;
+    a.group = us.n_q_heads / us.n_kv_heads;
+    a.kv_div = shape->n_kv_heads == us.n_kv_heads ? 1 : shape->n_q_heads / shape->n_kv_heads;
+    a.n_kv_real = shape->n_kv_heads;
     a.max_ctx = shape->max_ctx;
     a.budget = params->budget;
     a.chunk = plan.chunk;
@@ -564,6 +590,7 @@ int ssl_draft_materialize(const ssl_shape* shape, const ssl_params* params,
     StepPlan plan;
     int rc = plan_draft_step(shape, params, ctx_len_host, ctx_len_host, &plan);
     if (rc) return rc;
+    if (params->per_head) return SSL_ERR_UNSUPPORTED;
     if (!k_cache || !v_cache || !idx || !k_sel || !v_sel) return SSL_ERR_NULL;
     if (!aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(k_sel, 16) ||
         !aligned(v_sel, 16) || !aligned(idx, 4))
@@ -575,6 +602,8 @@ int ssl_draft_materialize(const ssl_shape* shape, const ssl_params* params,
     a.k_sel = static_cast<uint16_t*>(k_sel);
     a.v_sel = static_cast<uint16_t*>(v_sel);
     a.n_kv_heads = shape->n_kv_heads;
+    a.kv_div = 1;
+    a.n_kv_real = shape->n_kv_heads;
     a.max_ctx = shape->max_ctx;
     a.budget = params->budget;
     for (int b = 0; b < shape->batch; ++b) a.n_fixed[b] = plan.n_fixed[b];
@@ -602,6 +631,7 @@ int ssl_draft_step(const ssl_shape* shape, const ssl_params* params, const int32
     StepPlan plan;
     int rc = plan_draft_step(shape, params, ctx_len_host, cur_len_host, &plan);
     if (rc) return rc;
+    if (params->per_head) return SSL_ERR_UNSUPPORTED;
     if (!(params->sm_scale > 0.f) || !isfinite(params->sm_scale)) return SSL_ERR_SHAPE;
     const bool sel = k_sel || v_sel;
     if (!q_draft || !k_cache || !v_cache || !out) return SSL_ERR_NULL;
@@ -627,6 +657,8 @@ int ssl_draft_step(const ssl_shape* shape, const ssl_params* params, const int32
     a.n_q_heads = shape->n_q_heads;
     a.n_kv_heads = shape->n_kv_heads;
     a.group = shape->n_q_heads / shape->n_kv_heads;
+    a.kv_div = 1;
+    a.n_kv_real = shape->n_kv_heads;
     a.max_ctx = shape->max_ctx;
     a.budget = params->budget;
     a.chunk = plan.d.chunk;

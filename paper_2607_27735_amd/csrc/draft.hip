@@ -193,8 +193,11 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) qop[kb] = u32x4{0u, 0u, 0u, 0u};
         }
-        // (paged: rows are numbered over the whole page pool)
-        const size_t cache_off = kMode == kPlainPaged ? 0 : (size_t)it.unit * a.max_ctx * kHeadDim;
+        // (paged: rows are numbered over the whole page pool; per-head units
+        // read the rows of cache head it.c / kv_div)
+        const int kvc = it.c / a.kv_div;
+        const size_t cache_off = kMode == kPlainPaged
+            ? 0 : ((size_t)it.b * a.n_kv_real + kvc) * a.max_ctx * kHeadDim;
         const size_t sel_off = (size_t)it.unit * a.budget * kHeadDim;
         const RowSource src{a.k + cache_off, a.v + cache_off, a.k_sel + sel_off, a.v_sel + sel_off};
         const int last = it.n - 1;
@@ -207,7 +210,7 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
         } else if (kMode == kPlainPaged) {
             const int row = min(max(a.idx[(size_t)it.unit * a.budget + e], 0), a.max_ctx - 1);
             const int pg = a.block_table[(size_t)it.b * a.max_blocks + row / a.page_size];
-            my_row = (uint32_t)(((size_t)pg * a.n_kv_heads + it.c) * a.page_size + row % a.page_size);
+            my_row = (uint32_t)(((size_t)pg * a.n_kv_real + kvc) * a.page_size + row % a.page_size);
         } else {
             // (the index load does not wait for n_fixed: entry e < budget is in
             // bounds, and its value is used only when e < n_fixed)

@@ -37,6 +37,9 @@ struct VerifyArgs {
     // t % page_size of page block_table[b * max_blocks + t / page_size].
     const int32_t* block_table;
     int32_t page_size, max_blocks;
+    // 1: scores per query head, [batch][n_q][max_ctx] (Eq. 3 for each head of
+    // the group on its own); 0: per KV head, summed over the group.
+    int32_t per_head;
 };
 
 // Select splits each (sequence, KV head) unit into partitions of `part`
@@ -90,6 +93,10 @@ struct DraftArgs {
     // Paged cache, as in VerifyArgs (plain draft only).
     const int32_t* block_table;
     int32_t page_size, max_blocks;
+    // Units are (sequence, head u) with n_kv_heads heads; their K/V rows are
+    // those of cache head u / kv_div of n_kv_real (one index set per query
+    // head: n_kv_heads = n_q, group 1, kv_div = the GQA group).
+    int32_t kv_div, n_kv_real;
 };
 
 // Single-sweep verify: the slots (items of v.seq / v.chunk) of one KV-head

@@ -113,7 +113,7 @@ __global__ __launch_bounds__(kThreads) void verify_stats_kernel(VerifyArgs a) {
 // ---------------------------------------------------------------------------
 // Sweep 2: exact probabilities -> scores and per-item P.V.
 // ---------------------------------------------------------------------------
-template <int NRT>
+template <int NRT, bool kPerHead>
 __device__ __forceinline__ void main_tile(const VerifyArgs& a, const Rows<NRT>& r,
                                           const float (&lse)[NRT], const u32x4 (&kr)[2][4],
                                           const u32x4 (&vr)[8], int key0, int key_end,
@@ -134,6 +134,29 @@ __device__ __forceinline__ void main_tile(const VerifyArgs& a, const Rows<NRT>& 
                                                 : 0.f;
             }
 
+    // One index set per query head (the group divides 16, so head hh owns the
+    // lanes m16 = hh mod group of every row tile): lane m16 < group sums its
+    // head's window rows for the lane group's eight keys and writes them.
+    if constexpr (kPerHead) {
+        float hs[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int t = e >> 2, i = e & 3;
+            float s = 0.f;
+#pragma unroll
+            for (int rt = 0; rt < NRT; ++rt) s += r.inwin[rt] ? p[t][rt][i] : 0.f;
+            for (int o = 8; o >= a.group; o >>= 1) s += __shfl_xor(s, o, kWave);
+            hs[e] = s;
+        }
+        if (m16 < a.group) {
+            float* hrow = srow + (size_t)m16 * a.max_ctx;   // srow: head c * group of this sequence
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int key = key0 + 16 * (e >> 2) + G + 4 * (e & 3);
+                if (key < key_end) hrow[key] = hs[e];
+            }
+        }
+    } else {
     // Scores: sum of P over the window rows; rows live on the 16 lanes of the
     // DPP row and on the row tiles.
     float sp[8];
@@ -151,6 +174,7 @@ __device__ __forceinline__ void main_tile(const VerifyArgs& a, const Rows<NRT>& 
         for (int e = 1; e < 8; ++e) val = (m16 == e) ? sp[e] : val;
         const int key = key0 + 16 * (m16 >> 2) + G + 4 * (m16 & 3);
         if (key < key_end) srow[key] = val;
+    }
     }
 
     // O^T += V^T P^T.  B operand: slot e = 4t + i of P^T for the lane's row.
@@ -175,7 +199,7 @@ __device__ __forceinline__ void main_tile(const VerifyArgs& a, const Rows<NRT>& 
     }
 }
 
-template <int NRT, bool kPaged>
+template <int NRT, bool kPaged, bool kPerHead>
 __global__ __launch_bounds__(kThreads) void verify_main_kernel(VerifyArgs a) {
     const Item it = decode_item(a.seq, blockIdx.x, a.n_kv_heads, a.chunk);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -186,7 +210,9 @@ __global__ __launch_bounds__(kThreads) void verify_main_kernel(VerifyArgs a) {
     const size_t cache_off = (size_t)it.unit * a.max_ctx * kHeadDim;
     const uint16_t* kbase = a.k + cache_off;
     const uint16_t* vbase = a.v + cache_off;
-    float* srow = a.scores + (size_t)it.unit * a.max_ctx;
+    // (per-head scores: the row of the group's first query head)
+    float* srow = a.scores + (a.per_head ? ((size_t)it.b * a.n_q_heads + it.c * a.group) * a.max_ctx
+                                         : (size_t)it.unit * a.max_ctx);
     const int ntile = (it.key_end - it.key_begin + kTile - 1) / kTile;
     const int pages = kPaged ? wave_pages(a, it.b, it.key_begin, ntile, wave, lane) : 0;
 
@@ -242,7 +268,7 @@ __global__ __launch_bounds__(kThreads) void verify_main_kernel(VerifyArgs a) {
                                        it.key_begin + t * kTile, it.T, m16, G, b);
         },
         [&](const KVTile& b, int t) {
-            main_tile<NRT>(a, r, lse, b.k, b.v, it.key_begin + t * kTile, it.key_end, srow, m16,
+            main_tile<NRT, kPerHead>(a, r, lse, b.k, b.v, it.key_begin + t * kTile, it.key_end, srow, m16,
                            G, oacc);
         },
         row_lse);
@@ -331,12 +357,19 @@ __global__ __launch_bounds__(kCombineThreads) void verify_combine_kernel(VerifyA
 template <int NRT>
 hipError_t launch_verify_nrt(const VerifyArgs& a, int n_items, int n_rows_total,
                              hipStream_t stream) {
+    const dim3 grid(n_items), block(kThreads);
     if (a.block_table) {
-        hipLaunchKernelGGL((verify_stats_kernel<NRT, true>), dim3(n_items), dim3(kThreads), 0, stream, a);
-        hipLaunchKernelGGL((verify_main_kernel<NRT, true>), dim3(n_items), dim3(kThreads), 0, stream, a);
+        hipLaunchKernelGGL((verify_stats_kernel<NRT, true>), grid, block, 0, stream, a);
+        if (a.per_head)
+            hipLaunchKernelGGL((verify_main_kernel<NRT, true, true>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((verify_main_kernel<NRT, true, false>), grid, block, 0, stream, a);
     } else {
-        hipLaunchKernelGGL((verify_stats_kernel<NRT, false>), dim3(n_items), dim3(kThreads), 0, stream, a);
-        hipLaunchKernelGGL((verify_main_kernel<NRT, false>), dim3(n_items), dim3(kThreads), 0, stream, a);
+        hipLaunchKernelGGL((verify_stats_kernel<NRT, false>), grid, block, 0, stream, a);
+        if (a.per_head)
+            hipLaunchKernelGGL((verify_main_kernel<NRT, false, true>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((verify_main_kernel<NRT, false, false>), grid, block, 0, stream, a);
     }
     hipLaunchKernelGGL(verify_combine_kernel, dim3(n_rows_total), dim3(kCombineThreads), 0, stream, a);
     return hipGetLastError();

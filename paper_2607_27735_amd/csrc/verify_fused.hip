@@ -364,7 +364,21 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         // A stashed probability times its tile's factor 2^(m_tile - lse) is
         // exact; the tile maxima are [row][tile], so the lanes of a wave
         // (eight tiles, one row) read distinct banks.
-        for (int k4 = 4 * tid; k4 < nk; k4 += 4 * kThreads) {
+        // one index set per query head: head hh of the group sums its own
+        // window rows r0 + hh, r0 + hh + group, ...
+        for (int k4 = 4 * tid; a.per_head && k4 < nk; k4 += 4 * kThreads) {
+            const float* mt = mtile + k4 / kTile;
+            for (int hh = 0; hh < a.group; ++hh) {
+                f32x4 sc = {0.f, 0.f, 0.f, 0.f};
+                for (int row = r0 + hh; row < R; row += a.group)
+                    sc += stash4[row * stride4 + k4 / 4] * fast_exp2(mt[row * mts] - row_lse[row]);
+                float* hrow = a.scores + ((size_t)b * a.n_q_heads + c * a.group + hh) * a.max_ctx;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (k4 + i < nk) hrow[key_begin + k4 + i] = sc[i];
+            }
+        }
+        for (int k4 = 4 * tid; !a.per_head && k4 < nk; k4 += 4 * kThreads) {
             const float* mt = mtile + k4 / kTile;   // mt[row * mts]
             f32x4 sc = {0.f, 0.f, 0.f, 0.f};
             int row = r0;

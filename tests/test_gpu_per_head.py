@@ -1,0 +1,93 @@
+"""GPU parity of the per-query-head variant (one importance vector and one index
+set per query head instead of per KV head) against the oracle: verify's
+per-head scores (both schedules; the outputs are unchanged), select over the
+query heads, and the draft with one set per head reading its KV head's rows."""
+from types import SimpleNamespace
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_common import Dev, abs_v, check_index_structure, check_outputs, check_scores, params_of
+from paper_2607_27735_amd import binding as B
+from paper_2607_27735_amd.workloads import generate
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU visible", allow_module_level=True)
+
+CASES = {
+    "g4-b2": lambda: generate(501, name="g4-b2", batch=2, n_q_heads=16, n_kv_heads=4,
+                              ctx_len=[2500, 700], q_len=[5, 3], budget=200),
+    "g8-b1": lambda: generate(502, name="g8-b1", batch=1, n_q_heads=16, n_kv_heads=2,
+                              ctx_len=[3000], q_len=[6], budget=256, window=4),
+    "g1-mha": lambda: generate(503, name="g1-mha", batch=1, n_q_heads=4, n_kv_heads=4,
+                               ctx_len=[900], q_len=[4], budget=64),
+}
+MODES = {"two-sweep": B.VERIFY_TWO_SWEEP, "one-sweep": B.VERIFY_ONE_SWEEP}
+
+
+def _params(w, mode=B.VERIFY_AUTO, out_fp32=True):
+    p = params_of(w, out_fp32=out_fp32, mode=mode)
+    p.per_head = 1
+    return p
+
+
+@pytest.mark.parametrize("mode", list(MODES))
+@pytest.mark.parametrize("name", list(CASES))
+def test_per_head_verify(name, mode):
+    w = CASES[name]()
+    print(f"[per-head verify] {name} {mode}", flush=True)
+    out_ref, _ = oracle.verify(w)
+    oabs, _ = oracle.verify(w, v=abs_v(w))
+    S_ref = oracle.head_scores(w)
+    d = Dev(w)
+    sc = torch.full((w.batch, w.n_q_heads, w.max_ctx), -1.0, dtype=torch.float32, device="cuda")
+    out, sc = B.verify_attn(d.q, d.k, d.v, w.ctx_len, w.q_len, _params(w, MODES[mode]), scores=sc)
+    torch.cuda.synchronize()
+    out = out.float().cpu().numpy().astype(np.float64)
+    sc = sc.cpu().numpy().astype(np.float64)
+    mask = np.arange(w.max_q)[None, :, None] < w.q_len[:, None, None] * np.ones((1, 1, w.n_q_heads), bool)
+    check_outputs(out, out_ref, oabs, mask, what="per-head verify O")
+    check_scores(sc, S_ref, w.ctx_len, what="per-head S")
+    for b in range(w.batch):
+        assert np.all(sc[b, :, w.ctx_len[b]:] == -1.0)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_per_head_select_and_draft(name):
+    w = CASES[name]()
+    S_ref = oracle.head_scores(w)
+    s32 = S_ref.astype(np.float32)
+    # select over the query heads: the oracle sees them as units
+    wq = SimpleNamespace(batch=w.batch, n_kv_heads=w.n_q_heads, ctx_len=w.ctx_len,
+                         k_sink=w.k_sink, k_recent=w.k_recent, budget=w.budget)
+    idx_ref, n_ref = oracle.select(wq, s32.astype(np.float64))
+    p = _params(w)
+    idx, n_idx = B.select_topb(torch.from_numpy(s32).cuda(), w.ctx_len, p, n_q_heads=w.n_q_heads)
+    torch.cuda.synchronize()
+    idx, n_idx = idx.cpu().numpy(), n_idx.cpu().numpy()
+    assert np.array_equal(n_idx, n_ref)
+    for b in range(w.batch):
+        assert np.array_equal(idx[b, :, :n_ref[b]], idx_ref[b, :, :n_ref[b]])
+    check_index_structure(idx, n_idx, w.ctx_len, w.k_sink, w.k_recent, w.budget)
+    # draft: head h over its own set, rows of KV head h / group
+    idx_dev = np.where(idx_ref < 0, 0, idx_ref).astype(np.int32)
+    o_ref = oracle.draft_heads(w, idx_dev, n_ref)
+    oa = oracle.draft_heads(w, idx_dev, n_ref, v=abs_v(w))
+    d = Dev(w)
+    o = B.draft_attn(d.qd, d.k, d.v, torch.from_numpy(idx_dev).cuda(), n_ref, p)
+    torch.cuda.synchronize()
+    check_outputs(o.float().cpu().numpy().astype(np.float64), o_ref, oa,
+                  np.ones(o_ref.shape[:2], dtype=bool), what="per-head draft")
+
+
+def test_per_head_limits():
+    w = generate(504, name="g3", batch=1, n_q_heads=6, n_kv_heads=2, ctx_len=[500], q_len=[4],
+                 budget=64)
+    d = Dev(w)
+    with pytest.raises(B.SSLError):   # two sweeps need a group dividing 16
+        B.verify_attn(d.q, d.k, d.v, w.ctx_len, w.q_len, _params(w, B.VERIFY_TWO_SWEEP),
+                      scores=torch.zeros((1, 6, w.max_ctx), dtype=torch.float32, device="cuda"))
