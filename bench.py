@@ -376,6 +376,29 @@ def summarize_traffic(fetch_dir: str, write_dir: str, copy_mib: int, command: st
     return "\n".join(lines) + "\n"
 
 
+def summarize_mfma(d: str, command: str) -> str:
+    """MFMA use per launch from a rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 run:
+    the share of SIMD cycles the matrix cores were busy, and the bf16 MFMA
+    flops one launch issues."""
+    import csv
+    import glob
+    f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+    per = {}
+    for r in csv.DictReader(open(f)):
+        k = kernel_short(r["Kernel_Name"])
+        if k.split("<")[0] in OUR_KERNELS:
+            per.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    lines = ["# MFMA use per launch, llama8b-T32K workload (rocprofv3 MfmaUtil, MfmaFlopsBF16)",
+             f"command = {command}",
+             f"sources_sha256 = {sources_sha256()}"]
+    for k in sorted(per):
+        c = per[k]
+        util = statistics.fmean(c.get("MfmaUtil", [0.0]))
+        flops = statistics.fmean(c.get("MfmaFlopsBF16", [0.0]))
+        lines.append(f"{k} = mfma busy {util:.2f} % of SIMD cycles, bf16 MFMA flops {flops:.0f} per launch")
+    return "\n".join(lines) + "\n"
+
+
 def measured_traffic():
     """Traffic per verify call from the committed summary, if it was taken on
     the current sources; else None."""
@@ -434,10 +457,16 @@ def main() -> int:
                     help="print a summary of a rocprofv3 --kernel-trace --stats output and exit")
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print HBM traffic per launch from two rocprofv3 --pmc outputs and exit")
+    ap.add_argument("--summarize-mfma", metavar="DIR",
+                    help="print MFMA use per launch from a rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 "
+                         "output and exit")
     ap.add_argument("--command-text", default="", help="the profiling command, for summaries")
     args = ap.parse_args()
     if args.summarize_trace:
         sys.stdout.write(summarize_trace(args.summarize_trace, args.command_text))
+        return 0
+    if args.summarize_mfma:
+        sys.stdout.write(summarize_mfma(args.summarize_mfma, args.command_text))
         return 0
     if args.summarize_traffic:
         sys.stdout.write(summarize_traffic(*args.summarize_traffic, args.copy_calibration_mib,
