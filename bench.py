@@ -415,6 +415,31 @@ def measured_traffic():
         return None
 
 
+MFMA_FILE = os.path.join(REPO, "profiles", "verify_mfma_llama8b_T32K.txt")
+MFMA_PEAK_TFLOPS = 2500.0   # dense bf16
+
+
+def measured_mfma(kernel: str, avg_us: float):
+    """MFMA use of one launch of ``kernel`` from the committed counter summary,
+    if it was taken on the current sources; else None."""
+    try:
+        kv = {}
+        for line in open(MFMA_FILE):
+            if " = " in line and not line.startswith("#"):
+                k, v = line.split(" = ", 1)
+                kv[k.strip()] = v.strip()
+        if kv.get("sources_sha256") != sources_sha256() or kernel not in kv:
+            return None
+        words = kv[kernel].split()
+        busy, flops = float(words[2]), float(words[10])
+        tflops = flops / (avg_us * 1e-6) / 1e12
+        return {"kernel": kernel, "bf16_flops_per_launch": flops, "tflops": round(tflops, 1),
+                "peak_tflops": MFMA_PEAK_TFLOPS, "frac": round(tflops / MFMA_PEAK_TFLOPS, 4),
+                "busy_pct_of_simd_cycles": busy}
+    except (OSError, ValueError, IndexError):
+        return None
+
+
 def cpu_baseline(w, seconds: float):
     import numpy as np
     import oracle
@@ -653,6 +678,8 @@ def main() -> int:
                      "timing": "K back-to-back verify calls between two HIP events on the launch stream"},
         "kernels": kernels,
     }
+    if args.workload == 2 and args.mode == "eager" and args.verify_mode == "auto":
+        result["mfma"] = measured_mfma("verify_fused_kernel<2, true, false>", v_avg)
     if not args.no_draft_round:
         result["draft_round"] = draft_round_bench(B, w, kvs, qd, params, scores, stream,
                                                   args.steps, torch, np)
