@@ -117,6 +117,36 @@ def summarize_trace(d: str, command: str) -> str:
     return "\n".join(out) + "\n"
 
 
+def graph_step_bench(B, kvs, q, qd, w, params, out, scores, idx, n_idx, dout, stream, reps, torch):
+    """The same step captured in a HIP graph, one graph per KV copy: K replays
+    back to back, wall clock between two synchronizations."""
+    cap = torch.cuda.Stream()
+    cap.wait_stream(stream)
+    graphs = []
+    for (k, v) in kvs:
+        with torch.cuda.stream(cap):
+            st = B.PreparedStep(q, k, v, qd, w.ctx_len, w.q_len, params, out, scores, idx, n_idx,
+                                dout, stream=cap)
+            st.step()   # eager warm-up on the capture stream
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cap):
+            st.step()
+        graphs.append((g, st))
+    stream.wait_stream(cap)
+    torch.cuda.synchronize()
+    for g, _ in graphs:
+        g.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(reps):
+        graphs[i % len(graphs)][0].replay()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    return {"step_us": round((t1 - t0) * 1e6 / reps, 3),
+            "timing": f"{reps} replays back to back of one captured step graph per KV copy "
+                      f"({len(graphs)} copies), wall clock between two synchronizations"}
+
+
 def draft_round_bench(B, w, kvs, qd, params, scores, stream, reps, torch, np):
     """A draft round on the workload (next to the headline, not part of it):
     the index sets are built at T - k (k = max q_len - 1, at most K_recent),
@@ -475,6 +505,8 @@ def main() -> int:
                     help="skip the draft-round and vocabulary-side measurements printed "
                          "beside the headline")
     ap.add_argument("--mode", choices=["eager", "graph"], default="eager")
+    ap.add_argument("--no-graph-step", action="store_true",
+                    help="skip the captured-step figure printed beside the eager headline")
     ap.add_argument("--verify-mode", choices=["auto", "two-sweep", "one-sweep"], default="auto")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="end with three plain device copies of this size (counter calibration)")
@@ -549,9 +581,10 @@ def main() -> int:
 
     calls = ("verify", "select", "draft")
     graphs = None
+    step_graphs = []
     if args.mode == "graph":
-        # One graph per call and KV copy: launches replay without host
-        # marshalling, and events between replays time each call.
+        # Per KV copy, one graph per call (events between their replays time
+        # each call) and one graph of the whole step (the headline).
         graphs = []
         cap = torch.cuda.Stream()
         cap.wait_stream(stream)
@@ -559,13 +592,19 @@ def main() -> int:
             with torch.cuda.stream(cap):
                 st = B.PreparedStep(q, k, v, qd, w.ctx_len, w.q_len, params, out, scores, idx,
                                     n_idx, dout, stream=cap)
+            with torch.cuda.stream(cap):   # eager warm-up on the capture stream
+                st.step()
             gs = []
             for name in calls:
                 g = torch.cuda.CUDAGraph()
                 with torch.cuda.graph(g, stream=cap):
                     getattr(st, name)()
                 gs.append(g)
+            sg = torch.cuda.CUDAGraph()   # the whole step, for the headline
+            with torch.cuda.graph(sg, stream=cap):
+                st.step()
             graphs.append(gs)
+            step_graphs.append((sg, st))
         stream.wait_stream(cap)
         for i in range(args.warmup):
             for g in graphs[i % n_copies]:
@@ -577,8 +616,7 @@ def main() -> int:
     t0 = time.perf_counter()
     for i in range(args.steps):
         if graphs is not None:
-            for g in graphs[i % n_copies]:
-                g.replay()
+            step_graphs[i % n_copies][0].replay()
         else:
             steps[i % n_copies].step()
     torch.cuda.synchronize()
@@ -680,6 +718,9 @@ def main() -> int:
     }
     if args.workload == 2 and args.mode == "eager" and args.verify_mode == "auto":
         result["mfma"] = measured_mfma("verify_fused_kernel<2, true, false>", v_avg)
+    if args.mode == "eager" and not args.no_graph_step:
+        result["graph_step"] = graph_step_bench(B, kvs, q, qd, w, params, out, scores, idx, n_idx,
+                                                dout, stream, args.steps, torch)
     if not args.no_draft_round:
         result["draft_round"] = draft_round_bench(B, w, kvs, qd, params, scores, stream,
                                                   args.steps, torch, np)

@@ -42,10 +42,17 @@
  *  - Host arrays (ctx_len, q_len, n_idx_host) are read during the call only.
  *  - The workspace is caller-allocated device memory of at least the size the
  *    matching *_workspace function reports; its contents need no
- *    initialization and are scratch after the call returns.
+ *    initialization.  A call made under graph capture keeps in it, between
+ *    replays, one word per exchange group (KV-head unit, logit row); other
+ *    data may overwrite it between calls.
  *  - Calls are asynchronous on `stream`; the library allocates nothing, keeps
  *    no global state and never synchronizes.  Two calls that share a
  *    workspace must be ordered on one stream.
+ *  - Calls may be captured in a HIP graph and the graph replayed any number
+ *    of times, also with new contents in the captured input buffers: a call
+ *    that finds its stream capturing has its kernels' cross-workgroup
+ *    exchanges take a new tag on every replay from those workspace words.
+ *    No call records a memset or an allocation.
  *  - Every argument check happens on the host before any HIP call, so a
  *    rejected call has no effect on the device.  Device-side data (scores,
  *    idx) is not validated: index values outside [0, max_ctx) are clamped

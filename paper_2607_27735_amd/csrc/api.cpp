@@ -75,11 +75,25 @@ uint64_t next_call_tag() {
     return seq.fetch_add(1, std::memory_order_relaxed) + 1;
 }
 
+// The workspace's exchange epochs, passed to the kernels only when the launch
+// is being captured into a graph: every replay of a captured launch repeats
+// its call tag, and the epochs give each replay a new exchange tag.  Eager
+// launches have a new call tag each and skip the epochs' load and advance.
+// If the query fails, its error is cleared and the epochs are used.
+uint64_t* epochs_if_captured(hipStream_t stream, char* ws, size_t off) {
+    hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(stream, &st) != hipSuccess) {
+        (void)hipGetLastError();
+        st = hipStreamCaptureStatusActive;
+    }
+    return st == hipStreamCaptureStatusNone ? nullptr : reinterpret_cast<uint64_t*>(ws + off);
+}
+
 struct VerifyPlan {
     int chunk, n_items, n_rows, row_tiles;
     bool fused_ok;
     int fused_chunk, fused_slots;
-    size_t ml_off, o_off, tag_off, bytes;
+    size_t ml_off, o_off, tag_off, epoch_off, bytes;
     SeqTable seq;
     SeqTable fseq;   // the one-sweep slots as items
 };
@@ -161,7 +175,8 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
     plan->ml_off = 0;
     plan->o_off = align_up(slots_max * kVerifyRowCap * sizeof(float) * 2);
     plan->tag_off = plan->o_off + align_up(slots_max * kVerifyRowCap * 128 * sizeof(float));
-    plan->bytes = plan->tag_off + align_up((size_t)plan->fused_slots * sizeof(uint64_t));
+    plan->epoch_off = plan->tag_off + align_up((size_t)plan->fused_slots * sizeof(uint64_t));
+    plan->bytes = plan->epoch_off + align_up((size_t)plan->fused_slots * sizeof(uint64_t));
     return SSL_OK;
 }
 
@@ -175,7 +190,7 @@ bool use_one_sweep(const VerifyPlan& plan, const ssl_params* p) {
 
 struct DraftPlan {
     int chunk, n_items, n_rows;
-    size_t ml_off, o_off, tag_off, bytes;
+    size_t ml_off, o_off, tag_off, epoch_off, bytes;
     SeqTable seq;
 };
 
@@ -206,7 +221,8 @@ int plan_draft(const ssl_shape* s, const ssl_params* p, const int32_t* n_idx, Dr
     plan->ml_off = 0;
     plan->o_off = align_up((size_t)items * kDraftRowCap * sizeof(float) * 2);
     plan->tag_off = plan->o_off + align_up((size_t)items * kDraftRowCap * 128 * sizeof(float));
-    plan->bytes = plan->tag_off + align_up((size_t)items * sizeof(uint64_t));
+    plan->epoch_off = plan->tag_off + align_up((size_t)items * sizeof(uint64_t));
+    plan->bytes = plan->epoch_off + align_up((size_t)items * sizeof(uint64_t));
     return SSL_OK;
 }
 
@@ -258,7 +274,7 @@ int check_select(const ssl_shape* s, const ssl_params* p, const int32_t* ctx) {
 // position bitmask of every unit, sized for the longest context of the call.
 struct SelectPlan {
     int part, parts;
-    size_t hist_off, coarse_off, cnt_off, thr_off, mask_off, seg_off, tag_off, bytes;
+    size_t hist_off, coarse_off, cnt_off, thr_off, mask_off, seg_off, tag_off, epoch_off, bytes;
 };
 
 int plan_select(const ssl_shape* s, const int32_t* ctx, SelectPlan* plan) {
@@ -276,7 +292,8 @@ int plan_select(const ssl_shape* s, const int32_t* ctx, SelectPlan* plan) {
     plan->mask_off = plan->thr_off + align_up(units * 2 * sizeof(uint32_t));
     plan->seg_off = plan->mask_off + align_up(slots * (plan->part / 32) * sizeof(uint32_t));
     plan->tag_off = plan->seg_off + align_up(slots * plan->part * 2 * sizeof(uint32_t));
-    plan->bytes = plan->tag_off + align_up(slots * 4 * sizeof(uint64_t));
+    plan->epoch_off = plan->tag_off + align_up(slots * 4 * sizeof(uint64_t));
+    plan->bytes = plan->epoch_off + align_up(units * sizeof(uint64_t));
     return SSL_OK;
 }
 
@@ -407,6 +424,7 @@ int verify_call(const ssl_shape* shape, const ssl_params* params, const int32_t*
         fa.v.chunk = plan.fused_chunk;
         fa.v.seq = plan.fseq;
         fa.tag = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + plan.tag_off);
+        fa.epoch = epochs_if_captured(stream, static_cast<char*>(workspace), plan.epoch_off);
         fa.call_tag = next_call_tag();
         return launch_verify_fused(fa, plan.fused_slots, plan.row_tiles, stream) ==
                        hipSuccess
@@ -479,6 +497,7 @@ int ssl_select_topb(const ssl_shape* shape, const ssl_params* params, const int3
     a.mask = reinterpret_cast<uint32_t*>(ws + plan.mask_off);
     a.seg = reinterpret_cast<uint2*>(ws + plan.seg_off);
     a.tag = reinterpret_cast<uint64_t*>(ws + plan.tag_off);
+    a.epoch = epochs_if_captured(stream, ws, plan.epoch_off);
     a.call_tag = next_call_tag();
     a.part = plan.part;
     a.parts = plan.parts;
@@ -543,6 +562,7 @@ int draft_call(const ssl_shape* shape, const ssl_params* params, const int32_t* 
     a.part_ml = reinterpret_cast<float2*>(static_cast<char*>(workspace) + plan.ml_off);
     a.part_o = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.o_off);
     a.tag = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + plan.tag_off);
+    a.epoch = epochs_if_captured(stream, static_cast<char*>(workspace), plan.epoch_off);
     a.call_tag = next_call_tag();
     a.out = out;
     a.n_q_heads = shape->n_q_heads;
@@ -652,6 +672,7 @@ int ssl_draft_step(const ssl_shape* shape, const ssl_params* params, const int32
     a.part_ml = reinterpret_cast<float2*>(static_cast<char*>(workspace) + plan.d.ml_off);
     a.part_o = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.d.o_off);
     a.tag = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + plan.d.tag_off);
+    a.epoch = epochs_if_captured(stream, static_cast<char*>(workspace), plan.d.epoch_off);
     a.call_tag = next_call_tag();
     a.out = out;
     a.n_q_heads = shape->n_q_heads;
@@ -676,7 +697,7 @@ int ssl_draft_step(const ssl_shape* shape, const ssl_params* params, const int32
 
 struct LogitPlan {
     int n_chunks;
-    size_t part_off, tag_off, argmax_off, bytes;
+    size_t part_off, tag_off, epoch_off, argmax_off, bytes;
 };
 
 int plan_logits(int32_t n_rows, int32_t vocab, LogitPlan* plan) {
@@ -688,7 +709,8 @@ int plan_logits(int32_t n_rows, int32_t vocab, LogitPlan* plan) {
     const size_t slots = (size_t)n_rows * plan->n_chunks;
     plan->part_off = 0;
     plan->tag_off = align_up(slots * 4 * sizeof(float));
-    plan->argmax_off = plan->tag_off + align_up(slots * sizeof(uint64_t));
+    plan->epoch_off = plan->tag_off + align_up(slots * sizeof(uint64_t));
+    plan->argmax_off = plan->epoch_off + align_up((size_t)n_rows * sizeof(uint64_t));
     plan->bytes = plan->argmax_off + align_up((size_t)n_rows * sizeof(int32_t));
     return SSL_OK;
 }
@@ -733,6 +755,7 @@ int ssl_logit_stats(const void* logits, int32_t dtype, int32_t n_rows, int32_t v
     a.argmax = argmax;
     a.part = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.part_off);
     a.tag = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + plan.tag_off);
+    a.epoch = epochs_if_captured(stream, static_cast<char*>(workspace), plan.epoch_off);
     a.call_tag = next_call_tag();
     a.rows_per_seq = 0;
     return launch_logit_stats(a, dtype == SSL_DT_F32, stream) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
@@ -780,6 +803,7 @@ int ssl_greedy_accept(const void* logits, int32_t dtype, int32_t batch, int32_t 
     a.argmax = reinterpret_cast<int32_t*>(ws + plan.argmax_off);
     a.part = reinterpret_cast<float*>(ws + plan.part_off);
     a.tag = reinterpret_cast<uint64_t*>(ws + plan.tag_off);
+    a.epoch = epochs_if_captured(stream, ws, plan.epoch_off);
     a.call_tag = next_call_tag();
     a.rows_per_seq = max_k + 1;
     for (int b = 0; b < batch; ++b) a.k_len[b] = k_len_host[b];

@@ -104,6 +104,31 @@ __device__ __forceinline__ float2 ld_dev2(const float2* p) {
     const float* f = reinterpret_cast<const float*>(p);
     return make_float2(ld_dev(f), ld_dev(f + 1));
 }
+// The tag that workgroups of one cross-workgroup exchange publish and wait
+// for: the host's call tag (a process-wide sequence with a random start) plus
+// the exchange group's epoch, a workspace word that the group's finisher
+// advances by one once every member has read it.  The epoch makes replays of a
+// launch captured in a graph, whose call tag is fixed, use a new tag each
+// time (eager launches, whose call tags already differ, pass no epoch words
+// and skip both the load and the advance); the odd factor keeps 2^39 consecutive epochs distinct in the low 39
+// bits that the shortest tags keep, and makes an epoch word that other data
+// overwrote line up with a stale tag only by accident.
+__device__ __forceinline__ uint64_t exchange_tag(uint64_t call_tag, uint64_t epoch) {
+    return call_tag + epoch * 0x9E3779B97F4A7C15ull;
+}
+
+// The wave-uniform 64-bit value v, moved to scalar registers here.  A uniform
+// value loaded from memory is otherwise moved right where it is loaded, and
+// the move waits for the load there; called where the value is first needed,
+// after a wait that already covers the load, the move costs nothing.
+__device__ __forceinline__ uint64_t scalar_here(uint64_t v) {
+    uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+    asm volatile("" : "+v"(lo), "+v"(hi));
+    lo = __builtin_amdgcn_readfirstlane(lo);
+    hi = __builtin_amdgcn_readfirstlane(hi);
+    return ((uint64_t)hi << 32) | lo;
+}
+
 // (the signal fences keep the compiler from moving memory accesses across it)
 __device__ __forceinline__ void wait_stores_done() {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);

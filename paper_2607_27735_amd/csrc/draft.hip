@@ -170,6 +170,10 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int m16 = lane & 15, G = lane >> 4;
     const int g = a.group;
+    // The unit's exchange epoch (exchange_tag), loaded first so that the
+    // waits for the index loads cover its round trip; the last chunk advances
+    // it at its end, when every other chunk has published, and so has read it.
+    const uint64_t ep = a.epoch ? ld_dev64(a.epoch + it.item0) : 0ull;
 
     __shared__ float2 wml[kDraftWaves][kRowCap];
     __shared__ float2 gml[kRowCap];
@@ -261,6 +265,8 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
     // ---- every chunk but the unit's last publishes its partial and leaves ----
     const size_t wg = blockIdx.x;
     const bool finisher = it.key_begin + a.chunk >= it.n;   // the unit's last chunk
+    const uint64_t epv = scalar_here(ep);
+    const uint64_t want = exchange_tag(a.call_tag, epv);
     if (!finisher) {
         for (int x = tid; x < g * (kHeadDim / 2); x += kDraftThreads) {
             const int row = x / (kHeadDim / 2), c2 = x - row * (kHeadDim / 2);
@@ -279,7 +285,7 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
                      __builtin_bit_cast(uint64_t, gml[tid]));
         wait_stores_done();
         __syncthreads();
-        if (tid == 0) st_dev64(a.tag + wg, a.call_tag);
+        if (tid == 0) st_dev64(a.tag + wg, want);
         return;
     }
     // The last chunk waits for the others: they have lower workgroup indices,
@@ -290,7 +296,7 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
         bool all_in;
         do {
             bool in = true;
-            for (int j = lane; j < it.nchunk - 1; j += kWave) in &= ld_dev64(a.tag + it.item0 + j) == a.call_tag;
+            for (int j = lane; j < it.nchunk - 1; j += kWave) in &= ld_dev64(a.tag + it.item0 + j) == want;
             all_in = __all(in);
             if (!all_in) __builtin_amdgcn_s_sleep(1);
         } while (!all_in && ++spins < kSpinLimit);
@@ -350,6 +356,9 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
             *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + base) = pk;
         }
     }
+    // every other chunk has published, so has read the epoch; advanced last,
+    // after the workgroup's final wait for loads
+    if (a.epoch && tid == 0 && it.nchunk > 1) st_dev64(a.epoch + it.item0, epv + 1);
 }
 
 // Materialization for a draft round: workgroup (x, u) copies rows

@@ -64,7 +64,8 @@ struct SelectArgs {
     uint32_t* mask;     // [units][parts * part / 32] position bitmask
     uint2* seg;         // [units][parts][part] candidate (score bits, position)
     uint64_t* tag;      // [units][parts][4] publication tags (no initialisation needed)
-    uint64_t call_tag;  // this call's tag: unique within the process
+    uint64_t* epoch;    // [units] exchange epochs (any initial value), or null
+    uint64_t call_tag;  // this call's tag: unique within the process (see exchange_tag)
     int32_t n_kv_heads, max_ctx, k_sink, k_recent, budget, batch, part, parts;
     int32_t ctx[kTableBatch];
 };
@@ -77,7 +78,8 @@ struct DraftArgs {
     float2* part_ml;        // [n_items][16]       per-workgroup (max, sum) per head
     float* part_o;          // [n_items][16][128]  per-workgroup partial outputs
     uint64_t* tag;          // [n_items] publication tags (no initialisation needed)
-    uint64_t call_tag;      // this call's tag: unique within the process
+    uint64_t* epoch;        // [n_items] exchange epoch of each unit at its first item, or null
+    uint64_t call_tag;      // this call's tag: unique within the process (see exchange_tag)
     void* out;              // [batch][n_q][128]
     int32_t n_q_heads, n_kv_heads, group, max_ctx, budget, chunk, out_fp32;
     float scale_log2;
@@ -104,7 +106,8 @@ struct DraftArgs {
 struct FusedArgs {
     VerifyArgs v;           // part_ml / part_o indexed by slot
     uint64_t* tag;          // [n_slots] publication tags (no initialisation needed)
-    uint64_t call_tag;      // this call's tag: unique within the process
+    uint64_t* epoch;        // [n_slots] exchange epoch of each unit at its first slot, or null
+    uint64_t call_tag;      // this call's tag: unique within the process (see exchange_tag)
 };
 
 // Launchers return hipSuccess or the error of the launch.
@@ -143,6 +146,7 @@ struct LogitArgs {
     int32_t* argmax;        // [n_rows], or null
     float* part;            // [n_rows][n_chunks][4] chunk statistics
     uint64_t* tag;          // [n_rows][n_chunks] publication tags (no initialisation needed)
+    uint64_t* epoch;        // [n_rows] exchange epochs (any initial value), or null
     uint64_t call_tag;
     int32_t rows_per_seq;   // acceptance: max_k + 1 (rows past k_len[b] + 1 skipped); else 0
     int32_t k_len[kTableBatch];

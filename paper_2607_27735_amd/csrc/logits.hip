@@ -129,6 +129,10 @@ __global__ __launch_bounds__(kThreads) void logit_stats_kernel(LogitArgs a) {
         if (j > a.k_len[b]) return;
     }
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // The row's exchange epoch (exchange_tag), loaded before the logits so that
+    // the wait for them covers its round trip; the last chunk advances it at
+    // its end, when every other chunk has published, and so has read it.
+    const uint64_t ep = a.epoch ? ld_dev64(a.epoch + row) : 0ull;
     __shared__ Stat ws[kThreads / kWave];
     Stat st = wave_merge(chunk_stat<kF32>(a, row, chunk, tid));
     if (lane == 0) ws[wave] = st;
@@ -142,6 +146,8 @@ __global__ __launch_bounds__(kThreads) void logit_stats_kernel(LogitArgs a) {
         return;
     }
     const size_t slot = (size_t)row * a.n_chunks;
+    const uint64_t epv = scalar_here(ep);
+    const uint64_t want = exchange_tag(a.call_tag, epv);
     if (chunk + 1 < a.n_chunks) {   // publish and leave
         if (lane == 0) {
             st_dev64(reinterpret_cast<uint64_t*>(a.part + 4 * (slot + chunk)),
@@ -149,7 +155,7 @@ __global__ __launch_bounds__(kThreads) void logit_stats_kernel(LogitArgs a) {
             st_dev64(reinterpret_cast<uint64_t*>(a.part + 4 * (slot + chunk)) + 1,
                      __builtin_bit_cast(uint64_t, make_float2(st.t, __builtin_bit_cast(float, st.a))));
             wait_stores_done();
-            st_dev64(a.tag + slot + chunk, a.call_tag);
+            st_dev64(a.tag + slot + chunk, want);
         }
         return;
     }
@@ -159,7 +165,7 @@ __global__ __launch_bounds__(kThreads) void logit_stats_kernel(LogitArgs a) {
     bool all_in;
     const int c = min(lane, a.n_chunks - 2);
     do {
-        all_in = __all(lane >= a.n_chunks - 1 || ld_dev64(a.tag + slot + c) == a.call_tag);
+        all_in = __all(lane >= a.n_chunks - 1 || ld_dev64(a.tag + slot + c) == want);
         if (!all_in) __builtin_amdgcn_s_sleep(1);
     } while (!all_in && ++spins < kSpinLimit);
     Stat mine;
@@ -177,7 +183,10 @@ __global__ __launch_bounds__(kThreads) void logit_stats_kernel(LogitArgs a) {
         mine.a = 0x7fffffff;
     }
     mine = wave_merge(mine);
-    if (lane == 0) write_row(a, row, mine);
+    if (lane == 0) {
+        write_row(a, row, mine);
+        if (a.epoch) st_dev64(a.epoch + row, epv + 1);   // every other chunk has read it
+    }
 }
 
 // Greedy acceptance: one wave per sequence over the argmax of its k + 1 rows.

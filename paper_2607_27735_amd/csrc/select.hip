@@ -530,10 +530,10 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
 // ---------------------------------------------------------------------------
 constexpr int kSpinLimit = 1 << 20;   // bounded wait (far above any real wait)
 
-// A count travels in its tag word: the low 48 bits of the call tag above a
-// 16-bit count (the call tags are a process-wide sequence, so a stale word
-// matches only after 2^48 calls, an uninitialised one by a 2^-48 accident),
-// and the wait that finds the word valid has the count without another load.
+// A count travels in its tag word: the low 48 bits of the exchange tag above
+// a 16-bit count (successive calls on a workspace use different exchange
+// tags, so a stale or uninitialised word matches only by accident), and the
+// wait that finds the word valid has the count without another load.
 __device__ __forceinline__ uint64_t tagged(uint64_t call_tag, uint32_t count) {
     return (call_tag << 16) | count;
 }
@@ -543,8 +543,8 @@ static_assert(kSelectMaxRounds * kRound <= 0xffff, "a partition's counts must fi
 
 // A published histogram entry carries its own tag, so that a reader can load
 // the entries in the same round trip as the tag word that gives their count:
-// the low 39 bits of the call tag above the bin (11 bits) and its count (14
-// bits).  A stale entry matches only 2^39 calls later.
+// the low 39 bits of the exchange tag above the bin (11 bits) and its count
+// (14 bits).
 constexpr int kBinPayloadBits = 25;
 constexpr uint64_t kBinTagMask = (1ull << (64 - kBinPayloadBits)) - 1ull;
 __device__ __forceinline__ uint64_t bin_entry(uint64_t call_tag, uint32_t bin, uint32_t count) {
@@ -611,7 +611,6 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
     const int P = g.parts;
     constexpr int kTags = 4;                  // tag words per partition: histogram entries,
     uint64_t* tag = a.tag + up0 * kTags;      // candidates, middle above d1; [P][kTags]
-    const uint64_t want = a.call_tag;
 
     __shared__ __attribute__((aligned(16))) uint32_t hist[2048];   // read as uint4
     __shared__ __attribute__((aligned(16))) uint32_t h2[1024];
@@ -633,6 +632,11 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
 #pragma unroll
         for (int e = 0; e < 4; ++e)
             keys[4 * r + e] = key_of(S, g, p * a.part + r * kRound + wave * 256 + e * 64 + lane);
+    // The unit's exchange epoch (exchange_tag), loaded with the scores so that
+    // the wait for them covers its round trip (the tag is formed only after
+    // that wait); partition 0 advances it at its end, when every partition has
+    // published, and so has read it.
+    const uint64_t ep = a.epoch ? ld_dev64(a.epoch + u) : 0ull;
     for (int x = tid; x < 2048; x += kSelThreads) hist[x] = 0u;
     for (int x = tid; x < 1024; x += kSelThreads) {
         h2[x] = 0u;
@@ -648,6 +652,8 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
     for (int j = 0; j < 4 * NR; ++j)
         if (keys[j] != kNone) atomicAdd(&hist[bin12(keys[j])], 1u);
     __syncthreads();
+    const uint64_t epv = scalar_here(ep);
+    const uint64_t want = exchange_tag(a.call_tag, epv);
 
     // ---- A. nonzero histogram bins -----------------------------------------
     {
@@ -987,6 +993,9 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
         for (int x = tid; x < n_recent; x += kSelThreads)
             if (rbase + x < a.budget) out[rbase + x] = g.r_start + x;
         if (c_head == 0 && tid == 0) a.n_idx[b] = rbase + n_recent;
+        // every partition has published, so has read the epoch; advanced last,
+        // after the kernel's final wait for loads
+        if (a.epoch && tid == 0) st_dev64(a.epoch + u, epv + 1);
     }
 }
 

@@ -212,6 +212,11 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         });
 
     // ---- 2. publish the chunk's row statistics and partial output ----------
+    // The unit's exchange epoch (exchange_tag), loaded here so that its round
+    // trip overlaps the stores below (the tag is formed only after the wait
+    // for them); chunk 0 advances it at its end, when every chunk has
+    // published, and so has read it.
+    const uint64_t ep = fa.epoch ? ld_dev64(fa.epoch + slot0) : 0ull;
 #pragma unroll
     for (int rt = 0; rt < NRT; ++rt) {
         L[rt] += shfl_xor_f(L[rt], 16);
@@ -291,8 +296,10 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     // ---- wait for every chunk of this (sequence, KV head) -------------------
     wait_stores_done();
     __syncthreads();
-    if (tid == 0) st_dev64(fa.tag + slot, fa.call_tag);
-    if (wave == 0) wait_unit(fa.tag + slot0, nchunk, fa.call_tag);
+    const uint64_t epv = scalar_here(ep);
+    const uint64_t want = exchange_tag(fa.call_tag, epv);
+    if (tid == 0) st_dev64(fa.tag + slot, want);
+    if (wave == 0) wait_unit(fa.tag + slot0, nchunk, want);
     __syncthreads();
 
     // The first chunks of this workgroup's first row in step 4 (all of them
@@ -456,6 +463,9 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
             __syncthreads();
         }
     }
+    // every chunk has published, so has read the epoch; advanced last, after
+    // the workgroup's final wait for loads
+    if (fa.epoch && tid == 0 && slot == slot0) st_dev64(fa.epoch + slot0, epv + 1);
 }
 
 template <int NRT>

@@ -1,0 +1,97 @@
+"""Calls captured in a HIP graph and replayed with new contents in the
+captured input buffers.  Each replay must equal the eager calls on the same
+inputs, bit for bit: the kernels are deterministic (fixed merge orders, no
+floating-point atomics).  Verify (one sweep), select, draft, a draft-round step
+and the logit statistics exchange partial results between workgroups behind
+tags, and a replay reuses the call tag fixed at capture; the workspace epochs
+must give every replay a new one, or a replay could take the previous
+replay's partials as its own.  Replays alternate with eager calls and
+synchronisations, and every replay is checked."""
+import pytest
+import torch
+
+from paper_2607_27735_amd import binding as B
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU visible", allow_module_level=True)
+
+BATCH, HQ, HKV, D = 1, 32, 8, 128
+T, QLEN, MAX_CTX, BUDGET = 16384, 7, 16392, 1024
+K_ROUND, ROUND_STEP = 3, 2
+N_LOGIT_ROWS, VOCAB = 6, 128256
+REPLAYS = 4
+
+
+def _refill(gen, *ts):
+    for t in ts:
+        t.copy_(torch.randn(t.shape, generator=gen, device=t.device, dtype=torch.float32).to(t.dtype))
+
+
+def test_graph_replays_match_eager_calls():
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2607)
+    q = torch.empty(BATCH, QLEN, HQ, D, dtype=torch.bfloat16, device=dev)
+    k = torch.empty(BATCH, HKV, MAX_CTX, D, dtype=torch.bfloat16, device=dev)
+    v = torch.empty_like(k)
+    qd = torch.empty(BATCH, HQ, D, dtype=torch.bfloat16, device=dev)
+    logits = torch.empty(N_LOGIT_ROWS, VOCAB, dtype=torch.bfloat16, device=dev)
+    _refill(gen, q, k, v, qd, logits)
+    params = B.make_params(D ** -0.5, budget=BUDGET, out_fp32=True)
+    ctx, ql = [T], [QLEN]
+    n_idx_host = B.index_count(T, params.k_sink, params.k_recent, BUDGET)
+
+    out = torch.empty(BATCH, QLEN, HQ, D, dtype=torch.float32, device=dev)
+    scores = torch.empty(BATCH, HKV, MAX_CTX, dtype=torch.float32, device=dev)
+    idx = torch.empty(BATCH, HKV, BUDGET, dtype=torch.int32, device=dev)
+    n_idx = torch.empty(BATCH, dtype=torch.int32, device=dev)
+    dout = torch.empty(BATCH, HQ, D, dtype=torch.float32, device=dev)
+    rout = torch.empty(BATCH, HQ, D, dtype=torch.float32, device=dev)
+
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    st = B.PreparedStep(q, k, v, qd, ctx, ql, params, out, scores, idx, n_idx, dout, stream=cap)
+    rnd = B.PreparedRound(qd, k, v, idx, ctx, K_ROUND, params, rout, stream=cap)
+    assert B.verify_plan(st.shape, params, ctx, ql)[0] == B.VERIFY_ONE_SWEEP
+    with torch.cuda.stream(cap):   # eager warm-up: one-time launcher set-up stays out of the graph
+        st.step()
+        rnd.step(ROUND_STEP)
+        B.logit_stats(logits)
+    torch.cuda.synchronize()
+
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=cap):
+        st.step()
+        rnd.step(ROUND_STEP)
+        ent_g, am_g = B.logit_stats(logits)
+    torch.cuda.synchronize()
+
+    for r in range(REPLAYS):
+        print(f"[graph] replay {r}: new inputs, replay, eager reference", flush=True)
+        _refill(gen, q, k, v, qd, logits)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+
+        out_e, scores_e = B.verify_attn(q, k, v, ctx, ql, params)
+        idx_e, n_idx_e = B.select_topb(scores_e, ctx, params)
+        dout_e = B.draft_attn(qd, k, v, idx_e, [n_idx_host], params)
+        rout_e = torch.empty_like(rout)
+        B.PreparedRound(qd, k, v, idx_e, ctx, K_ROUND, params, rout_e).step(ROUND_STEP)
+        ent_e, am_e = B.logit_stats(logits)
+        torch.cuda.synchronize()
+
+        assert torch.equal(out, out_e), f"replay {r}: verify output"
+        assert torch.equal(scores[:, :, :T], scores_e[:, :, :T]), f"replay {r}: scores"
+        assert torch.equal(n_idx, n_idx_e), f"replay {r}: n_idx"
+        assert torch.equal(idx[:, :, :n_idx_host], idx_e[:, :, :n_idx_host]), f"replay {r}: idx"
+        assert torch.equal(dout, dout_e), f"replay {r}: draft output"
+        assert torch.equal(rout, rout_e), f"replay {r}: draft-round step output"
+        assert torch.equal(am_g, am_e), f"replay {r}: argmax"
+        assert torch.equal(ent_g, ent_e), f"replay {r}: entropy"
+        # the inputs changed, so a replay that returned the previous results fails
+        if r > 0:
+            assert not torch.equal(out, prev_out), f"replay {r}: output did not change"
+        prev_out = out.clone()
