@@ -350,7 +350,9 @@ double ssl_ctrl_accept_prob(const ssl_ctrl *ctrl, double H);
 /* Eq. 8 over the first n draft entropies: the candidate k <= n maximizing
  * (1 + sum_{m<=k} prod_{i<=m} p_i) / (k*c_draft + c_verify), ties to the
  * smaller k.  Returns k_default before both classes are observed, and
- * SSL_ERR_SHAPE if no candidate is <= n. */
+ * SSL_ERR_SHAPE if no candidate is <= n, n < 0, or the costs are not finite
+ * with c_draft >= 0 and c_verify > 0 (a negative return is always an error:
+ * candidates are >= 0). */
 int32_t ssl_ctrl_choose_k(const ssl_ctrl *ctrl, const double *H, int32_t n,
                           double c_draft, double c_verify);
 

@@ -70,6 +70,8 @@ def _bind(lib):
     lib.oracle_index_count.restype = ctypes.c_int
     lib.oracle_ema.argtypes = [ctypes.c_double] * 3
     lib.oracle_ema.restype = ctypes.c_double
+    lib.oracle_ctrl_observe.argtypes = [_f64p, _f64p, ctypes.c_int, ctypes.c_int, ctypes.c_double]
+    lib.oracle_ctrl_observe.restype = ctypes.c_int
     lib.oracle_accept_prob.argtypes = [ctypes.c_double] * 3
     lib.oracle_accept_prob.restype = ctypes.c_double
     lib.oracle_expected_accepted.argtypes = [_f64p, ctypes.c_int]
@@ -282,6 +284,18 @@ def draft_heads(w, idx: np.ndarray, n_idx: np.ndarray, *, q_draft=None, k=None, 
 
 def ema(prev: float, observed: float, beta: float, lib=None) -> float:
     return float((lib or load()).oracle_ema(prev, observed, beta))
+
+
+def ctrl_observe(state: Sequence[float], H: Sequence[float], n_accepted: int, beta: float,
+                 lib=None) -> list:
+    """Eq. 6 after one verification: returns the new state
+    ``[h_acc, h_rej, seen_acc, seen_rej]`` (see ``oracle_ctrl_observe``)."""
+    st = _c(list(state), np.float64)
+    ha = _c(list(H) if len(H) else [0.0], np.float64)
+    if (lib or load()).oracle_ctrl_observe(_p(st, _f64p), _p(ha, _f64p), len(H), int(n_accepted),
+                                           float(beta)) != 0:
+        raise ValueError("oracle_ctrl_observe rejected its arguments")
+    return [float(x) for x in st]
 
 
 def accept_prob(H: float, h_acc: float, h_rej: float, lib=None) -> float:

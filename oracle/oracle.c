@@ -366,6 +366,38 @@ double oracle_ema(double prev, double observed, double beta)
     return beta * prev + (1.0 - beta) * observed;
 }
 
+/*
+ * Eq. 6 applied to one verification (readings of Sec. 3.3, which labels every
+ * drafted token accepted or rejected and tracks one mean entropy per label):
+ * H[0 .. n_drafted) are the draft entropies in drafting order and the first
+ * n_accepted of them were accepted.  The accepted label observes the mean of
+ * H[0 .. n_accepted), the rejected label the mean of H[n_accepted ..
+ * n_drafted).  A label's first observation sets its mean; later ones move it
+ * by one EMA step with coefficient beta.  A label with no tokens in this
+ * verification keeps its state.
+ * state[0 .. 4) = {h_acc, h_rej, seen_acc, seen_rej}, updated in place.
+ * Returns 0, or -1 on bad counts.
+ */
+int oracle_ctrl_observe(double *state, const double *H, int n_drafted, int n_accepted,
+                        double beta)
+{
+    if (n_drafted < 0 || n_accepted < 0 || n_accepted > n_drafted) return -1;
+    for (int cls = 0; cls < 2; ++cls) {
+        const int lo = cls == 0 ? 0 : n_accepted;
+        const int hi = cls == 0 ? n_accepted : n_drafted;
+        if (hi == lo) continue;                 /* no token carries this label */
+        double sum = 0.0;
+        for (int i = lo; i < hi; ++i) sum += H[i];
+        const double mean = sum / (double)(hi - lo);
+        if (state[2 + cls] != 0.0)
+            state[cls] = oracle_ema(state[cls], mean, beta);
+        else
+            state[cls] = mean;
+        state[2 + cls] = 1.0;
+    }
+    return 0;
+}
+
 /* Eq. 7, as printed: softmax over the negative L1 distances to the centers. */
 double oracle_accept_prob(double H, double h_acc, double h_rej)
 {

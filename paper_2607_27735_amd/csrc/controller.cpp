@@ -84,6 +84,9 @@ int32_t ssl_ctrl_choose_k(const ssl_ctrl* c, const double* H, int32_t n, double 
                           double c_verify) {
     if (!c || (n > 0 && !H)) return SSL_ERR_NULL;
     if (n < 0) return SSL_ERR_SHAPE;
+    // Eq. 8 divides by k * c_draft + c_verify
+    if (!isfinite(c_draft) || !isfinite(c_verify) || c_draft < 0.0 || !(c_verify > 0.0))
+        return SSL_ERR_SHAPE;
     if (!c->seen_acc || !c->seen_rej) return c->k_default;
     // Prefix sums of the acceptance-prefix probabilities, then one pass over
     // the candidates.

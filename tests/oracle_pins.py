@@ -21,6 +21,7 @@ from __future__ import annotations
 
 import itertools
 import math
+import statistics
 
 import numpy as np
 import torch
@@ -600,6 +601,45 @@ def pin_controller_closed_forms(lib):
     assert abs(oracle.expected_accepted(p, 2, lib=lib) - (0.9 + 0.45)) < 1e-12
 
 
+def pin_controller_observe(lib):
+    """Eq. 6 over one verification: label means by drafting order, first
+    observation sets a label's mean, a label without tokens keeps its state."""
+    fresh = [123.0, -5.0, 0.0, 0.0]          # unseen labels: the stored values are stale
+    H = [0.2, 0.4, 0.9, 3.0, 5.0]
+    st = oracle.ctrl_observe(fresh, H, 3, 0.9, lib=lib)
+    assert st[2] == 1.0 and st[3] == 1.0
+    assert abs(st[0] - statistics.fmean(H[:3])) < 1e-15
+    assert abs(st[1] - statistics.fmean(H[3:])) < 1e-15
+    # the accepted tokens are the first ones drafted
+    st = oracle.ctrl_observe(fresh, [0.0, 0.0, 0.0, 9.0, 9.0], 3, 0.5, lib=lib)
+    assert st[:2] == [0.0, 9.0]
+    # a label with no tokens keeps its mean and its seen flag
+    st = oracle.ctrl_observe([1.5, 2.5, 1.0, 1.0], [7.0, 8.0], 0, 0.9, lib=lib)
+    assert st[0] == 1.5 and abs(st[1] - (0.9 * 2.5 + 0.1 * 7.5)) < 1e-12
+    st = oracle.ctrl_observe([1.5, 2.5, 1.0, 0.0], [7.0, 8.0], 2, 0.9, lib=lib)
+    assert st[1:] == [2.5, 1.0, 0.0]
+    assert oracle.ctrl_observe([1.5, 2.5, 1.0, 1.0], [], 0, 0.9, lib=lib) == [1.5, 2.5, 1.0, 1.0]
+    # step response: a label first seen at x0, then n verifications whose
+    # tokens of that label all have entropy y, sits at y + (x0 - y) beta^n
+    for beta in (0.0, 0.6, 0.9, 1.0):
+        st = oracle.ctrl_observe(fresh, [4.0, 4.0, 1.0], 2, beta, lib=lib)
+        for n in range(1, 7):
+            st = oracle.ctrl_observe(st, [0.5, 0.5, 0.5, 3.0], 3, beta, lib=lib)
+            assert abs(st[0] - (0.5 + 3.5 * beta ** n)) < 1e-12
+            assert abs(st[1] - (3.0 + (1.0 - 3.0) * beta ** n)) < 1e-12
+    # a constant-entropy stream is a fixed point
+    st = oracle.ctrl_observe(fresh, [0.7, 0.7], 1, 0.3, lib=lib)
+    for _ in range(5):
+        st = oracle.ctrl_observe(st, [0.7] * 6, 4, 0.3, lib=lib)
+        assert st[:2] == [0.7, 0.7]
+    try:
+        oracle.ctrl_observe(fresh, [0.1, 0.2], 3, 0.9, lib=lib)
+    except ValueError:
+        pass
+    else:
+        raise AssertionError("more accepted than drafted tokens was not refused")
+
+
 def pin_controller_argmax(lib):
     cands = list(range(1, 21))
     # free drafting with positive acceptance: the longest candidate wins
@@ -641,4 +681,4 @@ ALL_PINS = [pin_verify_matches_sdpa, pin_verify_value_one, pin_verify_zero_keys_
             pin_draft_step_worked_example, pin_draft_step_value_one, pin_row_stats_library,
             pin_row_stats_closed_forms, pin_greedy_accept_worked, pin_head_scores_match_softmax,
             pin_draft_heads,
-            pin_controller_closed_forms, pin_controller_argmax]
+            pin_controller_closed_forms, pin_controller_observe, pin_controller_argmax]

@@ -23,29 +23,25 @@ def test_cold_start_returns_default(lib):
     assert c.choose_k([0.1] * 20, 0.1, 1.0) != -1
 
 
-def test_ema_matches_oracle():
+def test_observe_matches_oracle():
+    """Eq. 6 with the label means of one verification (the oracle's
+    oracle_ctrl_observe), over random verifications including empty labels."""
     rng = np.random.default_rng(1)
     beta = 0.85
     c = B.Controller(beta=beta)
-    h_acc = h_rej = None
-    for _ in range(40):
+    st_ref = [0.0, 0.0, 0.0, 0.0]
+    for _ in range(60):
         n = int(rng.integers(0, 12))
         m = int(rng.integers(0, n + 1))
         H = list(rng.random(n) * 4)
         c.observe(H, m)
-        # reading: class means of the accepted prefix / the rest; first
-        # observation initializes a class; empty classes are not updated
-        if m > 0:
-            mean = float(np.mean(H[:m]))
-            h_acc = mean if h_acc is None else oracle.ema(h_acc, mean, beta)
-        if n > m:
-            mean = float(np.mean(H[m:]))
-            h_rej = mean if h_rej is None else oracle.ema(h_rej, mean, beta)
+        st_ref = oracle.ctrl_observe(st_ref, H, m, beta)
         st = c.state()
-        if h_acc is not None:
-            assert st[2] and abs(st[0] - h_acc) < 1e-12
-        if h_rej is not None:
-            assert st[3] and abs(st[1] - h_rej) < 1e-12
+        assert st[2] == bool(st_ref[2]) and st[3] == bool(st_ref[3])
+        if st_ref[2]:
+            assert abs(st[0] - st_ref[0]) < 1e-12
+        if st_ref[3]:
+            assert abs(st[1] - st_ref[1]) < 1e-12
 
 
 def test_accept_prob_matches_oracle():
@@ -92,6 +88,20 @@ def test_choose_k_errors_and_candidates():
         B.Controller(beta=1.5)
     with pytest.raises(B.SSLError):
         c.observe([0.1, 0.2], 3)
+
+
+@pytest.mark.parametrize("cd,cv", [(0.1, 0.0), (0.1, -1.0), (-0.1, 1.0), (float("nan"), 1.0),
+                                   (0.1, float("nan")), (float("inf"), 1.0), (0.1, float("inf"))])
+def test_choose_k_rejects_bad_costs(cd, cv):
+    """Eq. 8 divides by k C_d + C_v: costs must be finite, C_d >= 0 and C_v > 0."""
+    c = B.Controller(candidates=[1, 2, 4], k_default=2)
+    c.set_state(0.5, 2.0, True, True)
+    with pytest.raises(B.SSLError) as e:
+        c.choose_k([0.1] * 4, cd, cv)
+    assert e.value.status == B.SSL_ERR_SHAPE
+    c.set_state(0.0, 0.0, False, False)            # also before both labels are seen
+    with pytest.raises(B.SSLError):
+        c.choose_k([0.1] * 4, cd, cv)
 
 
 def test_feedback_direction():

@@ -63,6 +63,13 @@ MUTANTS = [
      "const int32_t *I = idx + ((size_t)b * n_q_heads + c * g) * budget;"),
     ("ema_weights_swapped", "return beta * prev + (1.0 - beta) * observed;",
      "return beta * observed + (1.0 - beta) * prev;"),
+    ("observe_no_first_init", "if (state[2 + cls] != 0.0)", "if (1)"),
+    ("observe_empty_label_updated", "if (hi == lo) continue;                 /* no token carries this label */", ""),
+    ("observe_split_off_by_one", "const int lo = cls == 0 ? 0 : n_accepted;",
+     "const int lo = cls == 0 ? 0 : n_accepted + 1;"),
+    ("observe_mean_over_all_drafts", "for (int i = lo; i < hi; ++i) sum += H[i];",
+     "for (int i = 0; i < n_drafted; ++i) sum += H[i];"),
+    ("observe_seen_flag_not_set", "        state[2 + cls] = 1.0;\n", ""),
     ("accept_prob_inverted", "return ea / (ea + er);", "return er / (ea + er);"),
     ("expected_drops_last_term", "for (int m = 1; m <= k; ++m) {", "for (int m = 1; m < k; ++m) {"),
     ("expected_sum_not_product", "for (int i = 0; i < m; ++i) prod *= p[i];",
