@@ -42,17 +42,35 @@
  *  - Host arrays (ctx_len, q_len, n_idx_host) are read during the call only.
  *  - The workspace is caller-allocated device memory of at least the size the
  *    matching *_workspace function reports; its contents need no
- *    initialization.  A call made under graph capture keeps in it, between
- *    replays, one word per exchange group (KV-head unit, logit row); other
- *    data may overwrite it between calls.
- *  - Calls are asynchronous on `stream`; the library allocates nothing, keeps
- *    no global state and never synchronizes.  Two calls that share a
+ *    initialization.  Every workspace layout starts with the same 64 KiB of
+ *    exchange epochs (8192 words, one per exchange group: KV-head unit or
+ *    logit row), which calls made under graph capture keep between replays
+ *    and only ever advance; no call stores anything else there, so calls may
+ *    share a workspace, captured or not.
+ *  - Calls are asynchronous on `stream`; the library allocates nothing and
+ *    synchronizes only in ssl_exchange_status.  Two calls that share a
  *    workspace must be ordered on one stream.
+ *  - Process state kept by the library: a 64-bit call-tag sequence (host),
+ *    per device the CU count, the one-sweep verify kernel's raised LDS limit
+ *    and its occupancy (host, read once), the CU budget of ssl_set_cu_budget
+ *    and the settings of ssl_test_exchange_faults (host), and one exchange
+ *    status word per device (device memory, see ssl_exchange_status).
  *  - Calls may be captured in a HIP graph and the graph replayed any number
  *    of times, also with new contents in the captured input buffers: a call
  *    that finds its stream capturing has its kernels' cross-workgroup
- *    exchanges take a new tag on every replay from those workspace words.
- *    No call records a memset or an allocation.
+ *    exchanges take a new tag on every replay from the workspace's epochs.
+ *    A captured call with more than 8192 exchange groups is refused
+ *    (SSL_ERR_UNSUPPORTED).  No call records a memset or an allocation.
+ *  - Kernels whose workgroups exchange partial results (one-sweep verify,
+ *    one-kernel select, draft and draft steps, logit statistics) wait for
+ *    each other with bounded polls.  The plans keep every group that must be
+ *    resident at once within half of what the device's CUs hold (see
+ *    ssl_set_cu_budget).  A wait that still gives up (e.g. because other work
+ *    held CUs) leaves that call's results unspecified and raises a bit of the
+ *    device's exchange status word (ssl_exchange_status); under capture it
+ *    also marks the group's epoch, and every later captured call on that
+ *    workspace then gives up at once (raising the bit again) until the
+ *    workspace is filled with zeros.
  *  - Every argument check happens on the host before any HIP call, so a
  *    rejected call has no effect on the device.  Device-side data (scores,
  *    idx) is not validated: index values outside [0, max_ctx) are clamped
@@ -126,6 +144,48 @@ enum { SSL_VERIFY_AUTO = 0, SSL_VERIFY_TWO_SWEEP = 1, SSL_VERIFY_ONE_SWEEP = 2 }
 /* Human-readable text of a status code (static storage). */
 const char *ssl_status_string(int status);
 
+/* An identifier of the sources this library was built from (a hash of the
+ * kernel, ABI and build sources; static storage), so that a caller can tell a
+ * stale build from a current one. */
+const char *ssl_build_id(void);
+
+/*
+ * Exchange health (see the conventions above).  Bits of the status word, one
+ * per kernel family whose bounded cross-workgroup wait gave up since the word
+ * was last read:
+ */
+enum {
+    SSL_EXCHANGE_VERIFY = 1,  /* one-sweep ssl_verify_attn / _paged */
+    SSL_EXCHANGE_SELECT = 2,  /* one-kernel ssl_select_topb */
+    SSL_EXCHANGE_DRAFT = 4,   /* ssl_draft_attn / _paged, ssl_draft_step */
+    SSL_EXCHANGE_LOGITS = 8   /* ssl_logit_stats, ssl_greedy_accept */
+};
+/* Reads and clears the current device's status word in the order of
+ * `stream` (after the work queued before it), waits for `stream`, and stores
+ * the bits in *flags_out (0: every exchange since the last read completed).
+ * It synchronizes, so it may not be captured (SSL_ERR_UNSUPPORTED while
+ * `stream` captures).  Bits raised by work on other streams that is still
+ * running may be reported by a later read.  Errors: SSL_ERR_NULL,
+ * SSL_ERR_HIP. */
+int ssl_exchange_status(hipStream_t stream, uint32_t *flags_out);
+
+/* The CU count that verify and select plans count on (process-wide; 0, the
+ * default, uses the device's own count).  A caller that runs other kernels
+ * beside these calls can lower it so that the one-sweep verify and the
+ * one-kernel select are chosen only where their exchange groups fit in the
+ * CUs left to them.  It also sizes the one-sweep chunks and is read by
+ * ssl_verify_plan and the *_workspace calls, also without a GPU.  Errors:
+ * SSL_ERR_SHAPE if n_cu < 0. */
+int ssl_set_cu_budget(int32_t n_cu);
+
+/* Testing the give-up path, process-wide: spin_limit > 0 bounds every
+ * exchange wait to that many polls (0 restores the default), and
+ * mismatch_tags = 1 makes every workgroup publish tags that no wait accepts,
+ * so that every exchange of later calls gives up, raises its status bit and
+ * leaves its outputs unwritten (all kernels still finish).  Errors:
+ * SSL_ERR_SHAPE on a negative limit or mismatch_tags not 0 or 1. */
+int ssl_test_exchange_faults(int32_t spin_limit, int32_t mismatch_tags);
+
 /* Number of indices Eq. 4 yields for T positions:
  * min(k_sink,T) + min(K_mid, |middle span|) + |recent span|, where the recent
  * span is [max(T - k_recent, min(k_sink, T)), T).  Equals T when T <= budget.
@@ -191,6 +251,14 @@ int ssl_verify_attn(const ssl_shape *shape, const ssl_params *params,
  */
 int ssl_select_workspace(const ssl_shape *shape, const ssl_params *params,
                          const int32_t *ctx_len_host, size_t *bytes_out);
+/* The schedule ssl_select_topb would use: *one_kernel_out = 1 when the
+ * partitions of every unit exchange inside one kernel (calls of at most 256
+ * partitions whose units' partitions fit in half of what the device holds at
+ * once), 0 for the three-kernel schedule; *part_out = positions per
+ * partition, *parts_out = partitions of the longest context.  Host only. */
+int ssl_select_plan(const ssl_shape *shape, const ssl_params *params,
+                    const int32_t *ctx_len_host, int32_t *one_kernel_out, int32_t *part_out,
+                    int32_t *parts_out);
 int ssl_select_topb(const ssl_shape *shape, const ssl_params *params,
                     const int32_t *ctx_len_host, const float *scores,
                     int32_t *idx, int32_t *n_idx,

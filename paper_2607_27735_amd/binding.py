@@ -32,9 +32,10 @@ VERIFY_TWO_SWEEP = 1
 VERIFY_ONE_SWEEP = 2
 
 EXPORTED = [
-    "ssl_status_string", "ssl_index_count",
+    "ssl_status_string", "ssl_build_id", "ssl_exchange_status", "ssl_set_cu_budget",
+    "ssl_test_exchange_faults", "ssl_index_count",
     "ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn",
-    "ssl_select_workspace", "ssl_select_topb",
+    "ssl_select_workspace", "ssl_select_plan", "ssl_select_topb",
     "ssl_draft_workspace", "ssl_draft_attn",
     "ssl_verify_attn_paged", "ssl_draft_attn_paged",
     "ssl_draft_materialize", "ssl_draft_step_workspace", "ssl_draft_step",
@@ -73,7 +74,8 @@ _szp = ctypes.POINTER(ctypes.c_size_t)
 
 
 def load(path: Optional[str] = None):
-    """Load the HIP library (raises if it has not been built)."""
+    """Load the HIP library.  Raises if it has not been built, or if it was
+    built from sources other than the ones in this tree."""
     global _lib
     if _lib is not None and path is None:
         return _lib
@@ -81,15 +83,30 @@ def load(path: Optional[str] = None):
     if not os.path.exists(p):
         raise RuntimeError(f"{p} not found: build it with `python -m paper_2607_27735_amd.build`")
     lib = ctypes.CDLL(p)
+    lib.ssl_build_id.argtypes = []
+    lib.ssl_build_id.restype = ctypes.c_char_p
+    if path is None:
+        from .build import source_id
+        built, tree = lib.ssl_build_id().decode(), source_id()
+        if built != tree:
+            raise RuntimeError(f"{p} was built from other sources (build id {built}, tree {tree}): "
+                               "rebuild it with `python -m paper_2607_27735_amd.build`")
     sp, pp = ctypes.POINTER(Shape), ctypes.POINTER(Params)
     lib.ssl_status_string.argtypes = [ctypes.c_int]
     lib.ssl_status_string.restype = ctypes.c_char_p
+    lib.ssl_exchange_status.argtypes = [_vp, ctypes.POINTER(ctypes.c_uint32)]
+    lib.ssl_exchange_status.restype = ctypes.c_int
+    lib.ssl_set_cu_budget.argtypes = [ctypes.c_int32]
+    lib.ssl_set_cu_budget.restype = ctypes.c_int
+    lib.ssl_test_exchange_faults.argtypes = [ctypes.c_int32, ctypes.c_int32]
+    lib.ssl_test_exchange_faults.restype = ctypes.c_int
     lib.ssl_index_count.argtypes = [ctypes.c_int32] * 4
     lib.ssl_index_count.restype = ctypes.c_int32
     lib.ssl_verify_workspace.argtypes = [sp, pp, _i32p, _i32p, _szp]
     lib.ssl_verify_attn.argtypes = [sp, pp, _i32p, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
     lib.ssl_verify_plan.argtypes = [sp, pp, _i32p, _i32p, _i32p, _i32p, _i32p]
     lib.ssl_select_workspace.argtypes = [sp, pp, _i32p, _szp]
+    lib.ssl_select_plan.argtypes = [sp, pp, _i32p, _i32p, _i32p, _i32p]
     lib.ssl_select_topb.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _sz, _vp]
     lib.ssl_draft_workspace.argtypes = [sp, pp, _i32p, _szp]
     lib.ssl_draft_attn.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
@@ -108,7 +125,7 @@ def load(path: Optional[str] = None):
     lib.ssl_greedy_accept.argtypes = [_vp, _i32, _i32, _i32, _i32p, _i32, _i32, _vp, _vp, _vp,
                                       _vp, _sz, _vp]
     for f in ("ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn", "ssl_select_workspace",
-              "ssl_select_topb", "ssl_draft_workspace", "ssl_draft_attn", "ssl_draft_materialize",
+              "ssl_select_topb", "ssl_select_plan", "ssl_draft_workspace", "ssl_draft_attn", "ssl_draft_materialize",
               "ssl_draft_step_workspace", "ssl_draft_step", "ssl_verify_attn_paged",
               "ssl_draft_attn_paged", "ssl_logit_stats_workspace",
               "ssl_logit_stats", "ssl_greedy_accept_workspace", "ssl_greedy_accept"):
@@ -134,6 +151,33 @@ def load(path: Optional[str] = None):
 
 def status_string(status: int) -> str:
     return load().ssl_status_string(int(status)).decode()
+
+
+def build_id() -> str:
+    return load().ssl_build_id().decode()
+
+
+EXCHANGE_VERIFY, EXCHANGE_SELECT, EXCHANGE_DRAFT, EXCHANGE_LOGITS = 1, 2, 4, 8
+
+
+def exchange_status(stream=None) -> int:
+    """Reads and clears the current device's exchange status bits (waits for
+    the stream)."""
+    flags = ctypes.c_uint32(0)
+    _check(load().ssl_exchange_status(_stream(stream), ctypes.byref(flags)), "ssl_exchange_status")
+    return int(flags.value)
+
+
+def set_cu_budget(n_cu: int) -> None:
+    """CU count the verify and select plans count on (0: the device's own)."""
+    _check(load().ssl_set_cu_budget(int(n_cu)), "ssl_set_cu_budget")
+
+
+def test_exchange_faults(spin_limit: int = 0, mismatch_tags: bool = False) -> None:
+    """Testing only: bound exchange waits to spin_limit polls and make every
+    published tag unacceptable (see the header)."""
+    _check(load().ssl_test_exchange_faults(int(spin_limit), 1 if mismatch_tags else 0),
+           "ssl_test_exchange_faults")
 
 
 def _check(status: int, where: str) -> None:
@@ -272,6 +316,16 @@ def select_topb(scores: torch.Tensor, ctx_len, params: Params, n_q_heads: Option
                                   _ptr(n_idx), _ptr(ws), ws.numel(), _stream(stream)),
            "ssl_select_topb")
     return idx, n_idx
+
+
+def select_plan(shape: Shape, params: Params, ctx_len) -> Tuple[bool, int, int]:
+    """(one kernel?, positions per partition, partitions) that select_topb would use."""
+    ctx = _host_i32(ctx_len)
+    one, part, parts = ctypes.c_int32(0), ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(load().ssl_select_plan(ctypes.byref(shape), ctypes.byref(params),
+                                  ctx.ctypes.data_as(_i32p), ctypes.byref(one), ctypes.byref(part),
+                                  ctypes.byref(parts)), "ssl_select_plan")
+    return bool(one.value), int(part.value), int(parts.value)
 
 
 def select_workspace_bytes(shape: Shape, params: Params, ctx_len) -> int:
@@ -614,7 +668,7 @@ class PreparedStep:
     """
 
     def __init__(self, q, k, v, q_draft, ctx_len, q_len, params: Params, out, scores, idx, n_idx,
-                 draft_out, stream=None):
+                 draft_out, stream=None, shared_workspace: bool = False):
         self._lib = load()
         _need_gpu(q, k, v, q_draft, out, scores, idx, n_idx, draft_out)
         self.shape = verify_shape(q, k)
@@ -628,9 +682,13 @@ class PreparedStep:
         vws = verify_workspace_bytes(self.shape, params, self.ctx, self.ql)
         sws = select_workspace_bytes(self.shape, params, self.ctx)
         dws = draft_workspace_bytes(self.dshape, params, self.n_idx_host)
-        self.vws = torch.empty(max(vws, 1), dtype=torch.uint8, device=q.device)
-        self.sws = torch.empty(max(sws, 1), dtype=torch.uint8, device=q.device)
-        self.dws = torch.empty(max(dws, 1), dtype=torch.uint8, device=q.device)
+        if shared_workspace:   # one buffer for the three calls, ordered on one stream
+            self.vws = torch.empty(max(vws, sws, dws, 1), dtype=torch.uint8, device=q.device)
+            self.sws = self.dws = self.vws
+        else:
+            self.vws = torch.empty(max(vws, 1), dtype=torch.uint8, device=q.device)
+            self.sws = torch.empty(max(sws, 1), dtype=torch.uint8, device=q.device)
+            self.dws = torch.empty(max(dws, 1), dtype=torch.uint8, device=q.device)
         self.tensors = (q, k, v, q_draft, out, scores, idx, n_idx, draft_out)
         self.stream = _stream(stream)
         sp, pp = ctypes.byref(self.shape), ctypes.byref(params)

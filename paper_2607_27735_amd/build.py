@@ -19,8 +19,26 @@ LIB_NAME = "libsparsespec_l.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
 ARCH = "gfx950"
 
-HIP_SOURCES = ["verify.hip", "verify_fused.hip", "select.hip", "draft.hip", "logits.hip"]
+HIP_SOURCES = ["verify.hip", "verify_fused.hip", "select.hip", "draft.hip", "logits.hip",
+               "status.hip"]
 CXX_SOURCES = ["api.cpp", "controller.cpp"]
+
+
+def source_id() -> str:
+    """Hash of every source the library is built from (kernels, ABI, headers and
+    this build script); the library reports it through ssl_build_id()."""
+    import hashlib
+    files = [os.path.join(CSRC, f) for f in sorted(os.listdir(CSRC))
+             if f.endswith((".hip", ".cpp", ".h"))]
+    files += [os.path.join(INCLUDE, f) for f in sorted(os.listdir(INCLUDE)) if f.endswith(".h")]
+    files.append(os.path.abspath(__file__))
+    h = hashlib.sha256()
+    for f in files:
+        h.update(os.path.basename(f).encode() + b"\0")
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+        h.update(b"\0")
+    return h.hexdigest()[:16]
 
 
 def hipcc() -> str:
@@ -29,8 +47,9 @@ def hipcc() -> str:
     return path if os.path.exists(path) else (shutil.which("hipcc") or path)
 
 
-def _compile(src: str, obj: str, is_hip: bool) -> None:
-    cmd = [hipcc(), "-c", "-fPIC", "-O3", "-std=c++17", "-Wall", "-I", INCLUDE, "-I", CSRC]
+def _compile(src: str, obj: str, is_hip: bool, build_id: str) -> None:
+    cmd = [hipcc(), "-c", "-fPIC", "-O3", "-std=c++17", "-Wall", "-I", INCLUDE, "-I", CSRC,
+           f'-DSSL_BUILD_ID="{build_id}"']
     if is_hip:
         # gfx950 only; packed fp32 arithmetic is kept out of the generated code.
         cmd += ["-x", "hip", f"--offload-arch={ARCH}",
@@ -44,11 +63,12 @@ def _compile(src: str, obj: str, is_hip: bool) -> None:
 def build(verbose: bool = False) -> str:
     out_dir = os.path.join(HERE, "_build")
     os.makedirs(out_dir, exist_ok=True)
+    bid = source_id()
     jobs = []
     for s in HIP_SOURCES:
-        jobs.append((os.path.join(CSRC, s), os.path.join(out_dir, s + ".o"), True))
+        jobs.append((os.path.join(CSRC, s), os.path.join(out_dir, s + ".o"), True, bid))
     for s in CXX_SOURCES:
-        jobs.append((os.path.join(CSRC, s), os.path.join(out_dir, s + ".o"), False))
+        jobs.append((os.path.join(CSRC, s), os.path.join(out_dir, s + ".o"), False, bid))
     with ThreadPoolExecutor(max_workers=min(8, len(jobs))) as ex:
         list(ex.map(lambda j: _compile(*j), jobs))
     tmp = LIB_PATH + ".tmp%d" % os.getpid()

@@ -15,6 +15,10 @@
 
 using namespace ssl;
 
+static_assert(SSL_EXCHANGE_VERIFY == kStatusVerify && SSL_EXCHANGE_SELECT == kStatusSelect &&
+                  SSL_EXCHANGE_DRAFT == kStatusDraft && SSL_EXCHANGE_LOGITS == kStatusLogits,
+              "status bits of the ABI and the kernels agree");
+
 namespace {
 
 constexpr size_t kAlign = 256;
@@ -75,25 +79,83 @@ uint64_t next_call_tag() {
     return seq.fetch_add(1, std::memory_order_relaxed) + 1;
 }
 
-// The workspace's exchange epochs, passed to the kernels only when the launch
-// is being captured into a graph: every replay of a captured launch repeats
-// its call tag, and the epochs give each replay a new exchange tag.  Eager
-// launches have a new call tag each and skip the epochs' load and advance.
-// If the query fails, its error is cleared and the epochs are used.
-uint64_t* epochs_if_captured(hipStream_t stream, char* ws, size_t off) {
+// The workspace's exchange epochs (its first kEpochWords words, one per
+// exchange group), passed to the kernels only when the launch is being
+// captured into a graph: every replay of a captured launch repeats its call
+// tag, and the epochs give each replay a new exchange tag.  Eager launches
+// have a new call tag each and skip the epochs' load and advance.  If the
+// query fails, its error is cleared and the epochs are used.  A captured call
+// with more exchange groups than epoch words is refused.
+int epochs_if_captured(hipStream_t stream, void* ws, int64_t n_groups, uint64_t** epochs) {
     hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
     if (hipStreamIsCapturing(stream, &st) != hipSuccess) {
         (void)hipGetLastError();
         st = hipStreamCaptureStatusActive;
     }
-    return st == hipStreamCaptureStatusNone ? nullptr : reinterpret_cast<uint64_t*>(ws + off);
+    *epochs = nullptr;
+    if (st == hipStreamCaptureStatusNone) return SSL_OK;
+    if (n_groups > kEpochWords) return SSL_ERR_UNSUPPORTED;
+    *epochs = static_cast<uint64_t*>(ws);
+    return SSL_OK;
+}
+
+// Process-wide settings: the CU count plans assume (0: the device's own), and
+// the test hook that makes every exchange wait give up.
+std::atomic<int32_t> g_cu_budget{0};
+std::atomic<int32_t> g_spin_limit{0};      // 0: kDefaultSpinLimit
+std::atomic<uint64_t> g_tag_flip{0};
+
+// What an exchanging kernel needs besides its data (the device's status word
+// is looked up once per device).
+int make_exchange(Exchange* xc) {
+    uint32_t* word = nullptr;
+    if (exchange_status_word(&word) != hipSuccess) return SSL_ERR_HIP;
+    xc->status = word;
+    xc->tag_flip = g_tag_flip.load(std::memory_order_relaxed);
+    const int32_t lim = g_spin_limit.load(std::memory_order_relaxed);
+    xc->spin_limit = lim > 0 ? lim : kDefaultSpinLimit;
+    return SSL_OK;
+}
+
+// Compute units the plans may count on: the caller's budget if one is set,
+// else the current device's count (read once per device), else 256 (the
+// MI355X's count) when no device can be queried.
+constexpr int kDefaultCUs = 256;
+int device_cus() {
+    const int32_t budget = g_cu_budget.load(std::memory_order_relaxed);
+    if (budget > 0) return budget;
+    constexpr int kMaxDevices = 64;
+    static std::atomic<int> cus[kMaxDevices];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return kDefaultCUs;
+    }
+    const bool cached = dev >= 0 && dev < kMaxDevices;
+    int n = cached ? cus[dev].load(std::memory_order_relaxed) : 0;
+    if (n == 0) {
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1) {
+            (void)hipGetLastError();
+            return kDefaultCUs;
+        }
+        if (cached) cus[dev].store(n, std::memory_order_relaxed);
+    }
+    return n;
+}
+
+// Exchange groups whose members must all be resident at once get at most half
+// of what the device holds (blocks_per_cu workgroups on each CU; 1 when the
+// device cannot be queried), which leaves room for an uneven spread of the
+// group over the chip's dies.
+int64_t resident_group_cap(int blocks_per_cu) {
+    return std::max<int64_t>(1, (int64_t)device_cus() * std::max(blocks_per_cu, 1) / 2);
 }
 
 struct VerifyPlan {
     int chunk, n_items, n_rows, row_tiles;
     bool fused_ok;
     int fused_chunk, fused_slots;
-    size_t ml_off, o_off, tag_off, epoch_off, bytes;
+    size_t ml_off, o_off, tag_off, bytes;
     SeqTable seq;
     SeqTable fseq;   // the one-sweep slots as items
 };
@@ -143,20 +205,24 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
 
     // One-sweep: chunks (multiples of 128 keys, at most what the LDS logit
     // stash holds) of about one slot per CU over the whole call, but never
-    // more than kFusedMaxSlotsPerUnit slots per (sequence, KV head), all of
-    // which must be resident together.
+    // more slots per (sequence, KV head) than can be resident together: at
+    // most kFusedMaxSlotsPerUnit, and at most half of what the device's CUs
+    // hold at once.
     plan->fused_ok = false;
     plan->fused_slots = 0;
     plan->fused_chunk = 0;
     const int cap = fused_max_chunk(plan->row_tiles);
+    const int64_t max_slots =
+        std::min<int64_t>(kFusedMaxSlotsPerUnit, resident_group_cap(fused_blocks_per_cu(plan->row_tiles)));
     int max_ctx = 0;
     for (int b = 0; b < s->batch; ++b) max_ctx = std::max(max_ctx, ctx[b]);
-    const int64_t per_unit_min = ((int64_t)max_ctx + kFusedMaxSlotsPerUnit - 1) / kFusedMaxSlotsPerUnit;
-    const int64_t spread = (total_keys + 255) / 256;
+    const int64_t per_unit_min = ((int64_t)max_ctx + max_slots - 1) / max_slots;
+    const int64_t n_cu = device_cus();
+    const int64_t spread = (total_keys + n_cu - 1) / n_cu;
     int64_t fc = std::max(per_unit_min, spread);
     fc = std::max<int64_t>(128, (fc + 127) / 128 * 128);
     if (fc > cap) fc = cap / 128 * 128;
-    if (fc >= 128 && ((int64_t)max_ctx + fc - 1) / fc <= kFusedMaxSlotsPerUnit) {
+    if (fc >= 128 && ((int64_t)max_ctx + fc - 1) / fc <= max_slots) {
         int64_t slots = 0;
         plan->fseq = plan->seq;
         for (int b = 0; b < s->batch; ++b) {
@@ -172,11 +238,10 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
     }
     if (p->verify_mode == SSL_VERIFY_ONE_SWEEP && !plan->fused_ok) return SSL_ERR_UNSUPPORTED;
     const size_t slots_max = (size_t)std::max(plan->n_items, plan->fused_slots);
-    plan->ml_off = 0;
-    plan->o_off = align_up(slots_max * kVerifyRowCap * sizeof(float) * 2);
+    plan->ml_off = kEpochBytes;
+    plan->o_off = plan->ml_off + align_up(slots_max * kVerifyRowCap * sizeof(float) * 2);
     plan->tag_off = plan->o_off + align_up(slots_max * kVerifyRowCap * 128 * sizeof(float));
-    plan->epoch_off = plan->tag_off + align_up((size_t)plan->fused_slots * sizeof(uint64_t));
-    plan->bytes = plan->epoch_off + align_up((size_t)plan->fused_slots * sizeof(uint64_t));
+    plan->bytes = plan->tag_off + align_up((size_t)plan->fused_slots * sizeof(uint64_t));
     return SSL_OK;
 }
 
@@ -189,8 +254,8 @@ bool use_one_sweep(const VerifyPlan& plan, const ssl_params* p) {
 }
 
 struct DraftPlan {
-    int chunk, n_items, n_rows;
-    size_t ml_off, o_off, tag_off, epoch_off, bytes;
+    int chunk, n_items, n_rows, n_units;
+    size_t ml_off, o_off, tag_off, bytes;
     SeqTable seq;
 };
 
@@ -218,11 +283,11 @@ int plan_draft(const ssl_shape* s, const ssl_params* p, const int32_t* n_idx, Dr
     plan->chunk = chunk;
     plan->n_items = (int)items;
     plan->n_rows = s->batch * s->n_q_heads;
-    plan->ml_off = 0;
-    plan->o_off = align_up((size_t)items * kDraftRowCap * sizeof(float) * 2);
+    plan->n_units = s->batch * s->n_kv_heads;
+    plan->ml_off = kEpochBytes;
+    plan->o_off = plan->ml_off + align_up((size_t)items * kDraftRowCap * sizeof(float) * 2);
     plan->tag_off = plan->o_off + align_up((size_t)items * kDraftRowCap * 128 * sizeof(float));
-    plan->epoch_off = plan->tag_off + align_up((size_t)items * sizeof(uint64_t));
-    plan->bytes = plan->epoch_off + align_up((size_t)items * sizeof(uint64_t));
+    plan->bytes = plan->tag_off + align_up((size_t)items * sizeof(uint64_t));
     return SSL_OK;
 }
 
@@ -274,7 +339,8 @@ int check_select(const ssl_shape* s, const ssl_params* p, const int32_t* ctx) {
 // position bitmask of every unit, sized for the longest context of the call.
 struct SelectPlan {
     int part, parts;
-    size_t hist_off, coarse_off, cnt_off, thr_off, mask_off, seg_off, tag_off, epoch_off, bytes;
+    bool fused;
+    size_t hist_off, coarse_off, cnt_off, thr_off, mask_off, seg_off, tag_off, bytes;
 };
 
 int plan_select(const ssl_shape* s, const int32_t* ctx, SelectPlan* plan) {
@@ -285,15 +351,18 @@ int plan_select(const ssl_shape* s, const int32_t* ctx, SelectPlan* plan) {
     if (plan->parts > ssl::kMaxSelectParts) return SSL_ERR_UNSUPPORTED;
     const size_t slots = (size_t)s->batch * s->n_kv_heads * plan->parts;
     const size_t units = (size_t)s->batch * s->n_kv_heads;
-    plan->hist_off = 0;
+    // one kernel when the call is small and a unit's partitions can all be
+    // resident at once
+    plan->fused = slots <= (size_t)kSelectFuseMaxGroups &&
+                  plan->parts <= resident_group_cap(select_blocks_per_cu(plan->part));
+    plan->hist_off = kEpochBytes;
     plan->coarse_off = plan->hist_off + align_up(slots * kHistSlotWords * sizeof(uint32_t));
     plan->cnt_off = plan->coarse_off + align_up(slots * 64 * sizeof(uint32_t));
     plan->thr_off = plan->cnt_off + align_up(slots * sizeof(uint32_t));
     plan->mask_off = plan->thr_off + align_up(units * 2 * sizeof(uint32_t));
     plan->seg_off = plan->mask_off + align_up(slots * (plan->part / 32) * sizeof(uint32_t));
     plan->tag_off = plan->seg_off + align_up(slots * plan->part * 2 * sizeof(uint32_t));
-    plan->epoch_off = plan->tag_off + align_up(slots * 4 * sizeof(uint64_t));
-    plan->bytes = plan->epoch_off + align_up(units * sizeof(uint64_t));
+    plan->bytes = plan->tag_off + align_up(slots * 4 * sizeof(uint64_t));
     return SSL_OK;
 }
 
@@ -320,6 +389,36 @@ const char* ssl_status_string(int status) {
         case SSL_ERR_HIP: return "HIP kernel launch failed";
         default: return "unknown status";
     }
+}
+
+#ifndef SSL_BUILD_ID
+#define SSL_BUILD_ID "unknown"
+#endif
+
+const char* ssl_build_id(void) { return SSL_BUILD_ID; }
+
+int ssl_exchange_status(hipStream_t stream, uint32_t* flags_out) {
+    if (!flags_out) return SSL_ERR_NULL;
+    hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(stream, &st) != hipSuccess) {
+        (void)hipGetLastError();
+        return SSL_ERR_HIP;
+    }
+    if (st != hipStreamCaptureStatusNone) return SSL_ERR_UNSUPPORTED;
+    return take_exchange_status(stream, flags_out) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
+}
+
+int ssl_set_cu_budget(int32_t n_cu) {
+    if (n_cu < 0) return SSL_ERR_SHAPE;
+    g_cu_budget.store(n_cu, std::memory_order_relaxed);
+    return SSL_OK;
+}
+
+int ssl_test_exchange_faults(int32_t spin_limit, int32_t mismatch_tags) {
+    if (spin_limit < 0 || (mismatch_tags != 0 && mismatch_tags != 1)) return SSL_ERR_SHAPE;
+    g_spin_limit.store(spin_limit, std::memory_order_relaxed);
+    g_tag_flip.store(mismatch_tags ? 0x5A5A5A5A5A5A5A5Aull : 0ull, std::memory_order_relaxed);
+    return SSL_OK;
 }
 
 int32_t ssl_index_count(int32_t T, int32_t k_sink, int32_t k_recent, int32_t budget) {
@@ -424,7 +523,10 @@ int verify_call(const ssl_shape* shape, const ssl_params* params, const int32_t*
         fa.v.chunk = plan.fused_chunk;
         fa.v.seq = plan.fseq;
         fa.tag = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + plan.tag_off);
-        fa.epoch = epochs_if_captured(stream, static_cast<char*>(workspace), plan.epoch_off);
+        rc = epochs_if_captured(stream, workspace, (int64_t)shape->batch * shape->n_kv_heads, &fa.epoch);
+        if (rc) return rc;
+        rc = make_exchange(&fa.xc);
+        if (rc) return rc;
         fa.call_tag = next_call_tag();
         return launch_verify_fused(fa, plan.fused_slots, plan.row_tiles, stream) ==
                        hipSuccess
@@ -471,6 +573,21 @@ int ssl_select_workspace(const ssl_shape* shape, const ssl_params* params,
     return SSL_OK;
 }
 
+int ssl_select_plan(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
+                    int32_t* one_kernel_out, int32_t* part_out, int32_t* parts_out) {
+    if (!one_kernel_out || !part_out || !parts_out) return SSL_ERR_NULL;
+    int rc = check_select(shape, params, ctx_len_host);
+    if (rc) return rc;
+    const ssl_shape us = unit_shape(shape, params);
+    SelectPlan plan;
+    rc = plan_select(&us, ctx_len_host, &plan);
+    if (rc) return rc;
+    *one_kernel_out = plan.fused ? 1 : 0;
+    *part_out = plan.part;
+    *parts_out = plan.parts;
+    return SSL_OK;
+}
+
 int ssl_select_topb(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
                     const float* scores, int32_t* idx, int32_t* n_idx, void* workspace,
                     size_t workspace_bytes, hipStream_t stream) {
@@ -497,8 +614,14 @@ int ssl_select_topb(const ssl_shape* shape, const ssl_params* params, const int3
     a.mask = reinterpret_cast<uint32_t*>(ws + plan.mask_off);
     a.seg = reinterpret_cast<uint2*>(ws + plan.seg_off);
     a.tag = reinterpret_cast<uint64_t*>(ws + plan.tag_off);
-    a.epoch = epochs_if_captured(stream, ws, plan.epoch_off);
+    if (plan.fused) {   // the three-kernel schedule exchanges nothing inside a kernel
+        rc = epochs_if_captured(stream, ws, (int64_t)shape->batch * us.n_kv_heads, &a.epoch);
+        if (rc) return rc;
+    }
+    rc = make_exchange(&a.xc);
+    if (rc) return rc;
     a.call_tag = next_call_tag();
+    a.fused = plan.fused ? 1 : 0;
     a.part = plan.part;
     a.parts = plan.parts;
     a.n_kv_heads = us.n_kv_heads;
@@ -562,7 +685,10 @@ int draft_call(const ssl_shape* shape, const ssl_params* params, const int32_t* 
     a.part_ml = reinterpret_cast<float2*>(static_cast<char*>(workspace) + plan.ml_off);
     a.part_o = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.o_off);
     a.tag = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + plan.tag_off);
-    a.epoch = epochs_if_captured(stream, static_cast<char*>(workspace), plan.epoch_off);
+    rc = epochs_if_captured(stream, workspace, plan.n_units, &a.epoch);
+    if (rc) return rc;
+    rc = make_exchange(&a.xc);
+    if (rc) return rc;
     a.call_tag = next_call_tag();
     a.out = out;
     a.n_q_heads = shape->n_q_heads;
@@ -672,7 +798,10 @@ int ssl_draft_step(const ssl_shape* shape, const ssl_params* params, const int32
     a.part_ml = reinterpret_cast<float2*>(static_cast<char*>(workspace) + plan.d.ml_off);
     a.part_o = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.d.o_off);
     a.tag = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + plan.d.tag_off);
-    a.epoch = epochs_if_captured(stream, static_cast<char*>(workspace), plan.d.epoch_off);
+    rc = epochs_if_captured(stream, workspace, plan.d.n_units, &a.epoch);
+    if (rc) return rc;
+    rc = make_exchange(&a.xc);
+    if (rc) return rc;
     a.call_tag = next_call_tag();
     a.out = out;
     a.n_q_heads = shape->n_q_heads;
@@ -697,7 +826,7 @@ int ssl_draft_step(const ssl_shape* shape, const ssl_params* params, const int32
 
 struct LogitPlan {
     int n_chunks;
-    size_t part_off, tag_off, epoch_off, argmax_off, bytes;
+    size_t part_off, tag_off, argmax_off, bytes;
 };
 
 int plan_logits(int32_t n_rows, int32_t vocab, LogitPlan* plan) {
@@ -707,10 +836,9 @@ int plan_logits(int32_t n_rows, int32_t vocab, LogitPlan* plan) {
         return SSL_ERR_UNSUPPORTED;
     plan->n_chunks = (vocab + kLogitChunk - 1) / kLogitChunk;
     const size_t slots = (size_t)n_rows * plan->n_chunks;
-    plan->part_off = 0;
-    plan->tag_off = align_up(slots * 4 * sizeof(float));
-    plan->epoch_off = plan->tag_off + align_up(slots * sizeof(uint64_t));
-    plan->argmax_off = plan->epoch_off + align_up((size_t)n_rows * sizeof(uint64_t));
+    plan->part_off = kEpochBytes;
+    plan->tag_off = plan->part_off + align_up(slots * 4 * sizeof(float));
+    plan->argmax_off = plan->tag_off + align_up(slots * sizeof(uint64_t));
     plan->bytes = plan->argmax_off + align_up((size_t)n_rows * sizeof(int32_t));
     return SSL_OK;
 }
@@ -755,7 +883,10 @@ int ssl_logit_stats(const void* logits, int32_t dtype, int32_t n_rows, int32_t v
     a.argmax = argmax;
     a.part = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.part_off);
     a.tag = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + plan.tag_off);
-    a.epoch = epochs_if_captured(stream, static_cast<char*>(workspace), plan.epoch_off);
+    rc = epochs_if_captured(stream, workspace, n_rows, &a.epoch);
+    if (rc) return rc;
+    rc = make_exchange(&a.xc);
+    if (rc) return rc;
     a.call_tag = next_call_tag();
     a.rows_per_seq = 0;
     return launch_logit_stats(a, dtype == SSL_DT_F32, stream) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
@@ -803,7 +934,10 @@ int ssl_greedy_accept(const void* logits, int32_t dtype, int32_t batch, int32_t 
     a.argmax = reinterpret_cast<int32_t*>(ws + plan.argmax_off);
     a.part = reinterpret_cast<float*>(ws + plan.part_off);
     a.tag = reinterpret_cast<uint64_t*>(ws + plan.tag_off);
-    a.epoch = epochs_if_captured(stream, ws, plan.epoch_off);
+    rc = epochs_if_captured(stream, ws, a.n_rows, &a.epoch);
+    if (rc) return rc;
+    rc = make_exchange(&a.xc);
+    if (rc) return rc;
     a.call_tag = next_call_tag();
     a.rows_per_seq = max_k + 1;
     for (int b = 0; b < batch; ++b) a.k_len[b] = k_len_host[b];

@@ -13,6 +13,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "launch.h"
+
 namespace ssl {
 
 constexpr int kHeadDim = 128;
@@ -116,6 +118,26 @@ __device__ __forceinline__ float2 ld_dev2(const float2* p) {
 __device__ __forceinline__ uint64_t exchange_tag(uint64_t call_tag, uint64_t epoch) {
     return call_tag + epoch * 0x9E3779B97F4A7C15ull;
 }
+
+// A bounded wait gave up (one thread per workgroup calls this): the device's
+// status word gets the kernel family's bit and, for a call under graph
+// capture, the group's epoch word the mark kEpochDirty, so that every later
+// captured call on the workspace gives up at once instead of matching tags
+// that members of the failed call published late.  (When the group's
+// finisher did complete, every member had read the epoch, and its advance may
+// overwrite the mark: then no stale tag can match.)
+__device__ __forceinline__ void exchange_gave_up(const Exchange& xc, uint32_t bit,
+                                                 uint64_t* epoch_word) {
+    __hip_atomic_fetch_or(xc.status, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (epoch_word) st_dev64(epoch_word, kEpochDirty);
+}
+
+// The group's finisher advances the epoch once every member has read it.
+__device__ __forceinline__ void epoch_advance(uint64_t* epoch_word) {
+    __hip_atomic_fetch_add(epoch_word, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ bool epoch_is_dirty(uint64_t epoch) { return epoch == kEpochDirty; }
 
 // The wave-uniform 64-bit value v, moved to scalar registers here.  A uniform
 // value loaded from memory is otherwise moved right where it is loaded, and

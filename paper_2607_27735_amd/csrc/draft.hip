@@ -33,7 +33,6 @@ constexpr int kDraftWaves = 4;
 constexpr int kDraftThreads = kDraftWaves * kWave;
 constexpr int kWaveChunk = kTile;              // index entries per wave
 constexpr int kParkStride = kHeadDim + 4;      // floats per parked head row
-constexpr int kSpinLimit = 1 << 22;            // bounded wait (far above any real wait)
 constexpr int kMergeBatch = 16;                // partials loaded at once by the merging workgroup
 
 __device__ __forceinline__ int a_row_key(int m) { return (m >> 2) + 4 * (m & 3); }
@@ -173,8 +172,9 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
     // The unit's exchange epoch (exchange_tag), loaded first so that the
     // waits for the index loads cover its round trip; the last chunk advances
     // it at its end, when every other chunk has published, and so has read it.
-    const uint64_t ep = a.epoch ? ld_dev64(a.epoch + it.item0) : 0ull;
+    const uint64_t ep = a.epoch ? ld_dev64(a.epoch + it.unit) : 0ull;
 
+    __shared__ int wait_failed;
     __shared__ float2 wml[kDraftWaves][kRowCap];
     __shared__ float2 gml[kRowCap];
     __shared__ float park[kDraftWaves][kRowCap][kParkStride];
@@ -267,6 +267,10 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
     const bool finisher = it.key_begin + a.chunk >= it.n;   // the unit's last chunk
     const uint64_t epv = scalar_here(ep);
     const uint64_t want = exchange_tag(a.call_tag, epv);
+    if (epoch_is_dirty(epv)) {   // an earlier captured call on this workspace gave up
+        if (tid == 0) exchange_gave_up(a.xc, kStatusDraft, nullptr);
+        return;
+    }
     if (!finisher) {
         for (int x = tid; x < g * (kHeadDim / 2); x += kDraftThreads) {
             const int row = x / (kHeadDim / 2), c2 = x - row * (kHeadDim / 2);
@@ -285,12 +289,12 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
                      __builtin_bit_cast(uint64_t, gml[tid]));
         wait_stores_done();
         __syncthreads();
-        if (tid == 0) st_dev64(a.tag + wg, want);
+        if (tid == 0) st_dev64(a.tag + wg, want ^ a.xc.tag_flip);
         return;
     }
     // The last chunk waits for the others: they have lower workgroup indices,
     // so they were dispatched first, and they never wait.  The wait is also
-    // bounded.
+    // bounded: if it gives up, the status word says so and no output is written.
     if (wave == 0) {
         int spins = 0;
         bool all_in;
@@ -299,9 +303,14 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
             for (int j = lane; j < it.nchunk - 1; j += kWave) in &= ld_dev64(a.tag + it.item0 + j) == want;
             all_in = __all(in);
             if (!all_in) __builtin_amdgcn_s_sleep(1);
-        } while (!all_in && ++spins < kSpinLimit);
+        } while (!all_in && ++spins < a.xc.spin_limit);
+        if (lane == 0) wait_failed = !all_in;
     }
     __syncthreads();
+    if (wait_failed) {
+        if (tid == 0) exchange_gave_up(a.xc, kStatusDraft, a.epoch ? a.epoch + it.unit : nullptr);
+        return;
+    }
 
     // ---- merge the partials of every head, in chunk order ---------------------
     for (int x = tid; x < g * (kHeadDim / 4); x += kDraftThreads) {
@@ -358,7 +367,7 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
     }
     // every other chunk has published, so has read the epoch; advanced last,
     // after the workgroup's final wait for loads
-    if (a.epoch && tid == 0 && it.nchunk > 1) st_dev64(a.epoch + it.item0, epv + 1);
+    if (a.epoch && tid == 0 && it.nchunk > 1) epoch_advance(a.epoch + it.unit);
 }
 
 // Materialization for a draft round: workgroup (x, u) copies rows

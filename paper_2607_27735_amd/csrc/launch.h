@@ -10,6 +10,43 @@ namespace ssl {
 
 constexpr int kTableBatch = 64;   // per-sequence tables travel as kernel arguments
 
+// Every workspace layout starts with kEpochWords 64-bit exchange epochs, one
+// per exchange group (KV-head unit, logit row) of a call made under graph
+// capture: calls that share a workspace then share these words, which every
+// call only ever advances, and no call keeps other data there.
+constexpr int kEpochWords = 8192;
+constexpr size_t kEpochBytes = (size_t)kEpochWords * sizeof(uint64_t);
+// Stored in an epoch word when an exchange of its group gave up: every later
+// captured call on that workspace gives up at once (and says so) until the
+// caller clears the workspace.  A whole 64-bit value, not a bit, so that a
+// workspace's initial contents look marked only by a 2^-64 accident.
+constexpr uint64_t kEpochDirty = 0xD1A7E5C0FFEE5EEDull;
+
+// The device's exchange status word: one bit per kernel family whose bounded
+// cross-workgroup wait gave up (its results are then unspecified).
+enum : uint32_t {
+    kStatusVerify = 1u,   // one-sweep verify
+    kStatusSelect = 2u,   // one-kernel select
+    kStatusDraft = 4u,    // draft and draft-round steps
+    kStatusLogits = 8u    // logit statistics and acceptance
+};
+
+// What every exchanging kernel needs beyond its data: where to report a wait
+// that gave up, how long to wait, and (tests only) a mask XORed into every tag
+// it publishes, so that no wait can succeed.
+struct Exchange {
+    uint32_t* status;       // the device's status word
+    uint64_t tag_flip;      // 0 except when testing the give-up path
+    int32_t spin_limit;     // polls before a wait gives up
+};
+constexpr int32_t kDefaultSpinLimit = 1 << 20;
+
+// The current device's status word (its address is looked up once per device).
+hipError_t exchange_status_word(uint32_t** word);
+// Reads and clears the current device's status word in stream order, then
+// waits for the stream.
+hipError_t take_exchange_status(hipStream_t stream, uint32_t* flags);
+
 // Per-sequence table, passed by value.  Work items of sequence b are
 // [item_start[b], item_start[b + 1]); rows of the combine kernel likewise
 // [row_start[b], row_start[b + 1]).
@@ -66,6 +103,8 @@ struct SelectArgs {
     uint64_t* tag;      // [units][parts][4] publication tags (no initialisation needed)
     uint64_t* epoch;    // [units] exchange epochs (any initial value), or null
     uint64_t call_tag;  // this call's tag: unique within the process (see exchange_tag)
+    Exchange xc;
+    int32_t fused;      // 1: one kernel (the partitions of a unit exchange while resident)
     int32_t n_kv_heads, max_ctx, k_sink, k_recent, budget, batch, part, parts;
     int32_t ctx[kTableBatch];
 };
@@ -78,8 +117,9 @@ struct DraftArgs {
     float2* part_ml;        // [n_items][16]       per-workgroup (max, sum) per head
     float* part_o;          // [n_items][16][128]  per-workgroup partial outputs
     uint64_t* tag;          // [n_items] publication tags (no initialisation needed)
-    uint64_t* epoch;        // [n_items] exchange epoch of each unit at its first item, or null
+    uint64_t* epoch;        // [units] exchange epochs (any initial value), or null
     uint64_t call_tag;      // this call's tag: unique within the process (see exchange_tag)
+    Exchange xc;
     void* out;              // [batch][n_q][128]
     int32_t n_q_heads, n_kv_heads, group, max_ctx, budget, chunk, out_fp32;
     float scale_log2;
@@ -106,8 +146,9 @@ struct DraftArgs {
 struct FusedArgs {
     VerifyArgs v;           // part_ml / part_o indexed by slot
     uint64_t* tag;          // [n_slots] publication tags (no initialisation needed)
-    uint64_t* epoch;        // [n_slots] exchange epoch of each unit at its first slot, or null
+    uint64_t* epoch;        // [units] exchange epochs (any initial value), or null
     uint64_t call_tag;      // this call's tag: unique within the process (see exchange_tag)
+    Exchange xc;
 };
 
 // Launchers return hipSuccess or the error of the launch.
@@ -120,11 +161,20 @@ hipError_t launch_verify_fused(const FusedArgs& a, int n_slots, int row_tiles, h
 hipError_t launch_verify_combine(const VerifyArgs& a, int n_rows_total, hipStream_t stream);
 // Largest key chunk the single-sweep kernel can hold in LDS for row_tiles.
 int fused_max_chunk(int row_tiles);
+// Workgroups of the single-sweep kernel (row_tiles, at its largest LDS use)
+// and of the one-kernel select (partition length part) that one CU of the
+// current device holds at once; 0 if the device cannot be queried.
+int fused_blocks_per_cu(int row_tiles);
+int select_blocks_per_cu(int part);
 // Partition length for the longest context max_t: the smallest multiple of
 // 1024 (in powers of two, at most kSelectMaxRounds * 1024) that keeps a unit at
 // <= kSelectTargetParts partitions.
 int select_part_len(int max_t);
+// a.fused chooses the schedule (the caller checks that a unit's partitions fit
+// on the device at once).
 hipError_t launch_select(const SelectArgs& a, int n_units, hipStream_t stream);
+// Calls of at most this many partition workgroups may run as one kernel.
+constexpr int kSelectFuseMaxGroups = 256;
 // One workgroup per `chunk` (128) index entries; no combine kernel.
 hipError_t launch_draft(const DraftArgs& a, int n_items, hipStream_t stream);
 // Draft round: copy the sink and TopK rows (n_fixed per sequence) of every
@@ -148,6 +198,7 @@ struct LogitArgs {
     uint64_t* tag;          // [n_rows][n_chunks] publication tags (no initialisation needed)
     uint64_t* epoch;        // [n_rows] exchange epochs (any initial value), or null
     uint64_t call_tag;
+    Exchange xc;
     int32_t rows_per_seq;   // acceptance: max_k + 1 (rows past k_len[b] + 1 skipped); else 0
     int32_t k_len[kTableBatch];
 };

@@ -25,7 +25,6 @@ namespace ssl {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kSpinLimit = 1 << 22;   // bounded wait (far above any real wait)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -148,6 +147,10 @@ __global__ __launch_bounds__(kThreads) void logit_stats_kernel(LogitArgs a) {
     const size_t slot = (size_t)row * a.n_chunks;
     const uint64_t epv = scalar_here(ep);
     const uint64_t want = exchange_tag(a.call_tag, epv);
+    if (epoch_is_dirty(epv)) {   // an earlier captured call on this workspace gave up
+        if (lane == 0) exchange_gave_up(a.xc, kStatusLogits, nullptr);
+        return;
+    }
     if (chunk + 1 < a.n_chunks) {   // publish and leave
         if (lane == 0) {
             st_dev64(reinterpret_cast<uint64_t*>(a.part + 4 * (slot + chunk)),
@@ -155,19 +158,24 @@ __global__ __launch_bounds__(kThreads) void logit_stats_kernel(LogitArgs a) {
             st_dev64(reinterpret_cast<uint64_t*>(a.part + 4 * (slot + chunk)) + 1,
                      __builtin_bit_cast(uint64_t, make_float2(st.t, __builtin_bit_cast(float, st.a))));
             wait_stores_done();
-            st_dev64(a.tag + slot + chunk, want);
+            st_dev64(a.tag + slot + chunk, want ^ a.xc.tag_flip);
         }
         return;
     }
     // the row's last chunk: wait for the others, then merge all in chunk order
-    // (lane c holds chunk c; the shuffle tree's order is fixed)
+    // (lane c holds chunk c; the shuffle tree's order is fixed); if the bounded
+    // wait gives up, the status word says so and the row is not written
     int spins = 0;
     bool all_in;
     const int c = min(lane, a.n_chunks - 2);
     do {
         all_in = __all(lane >= a.n_chunks - 1 || ld_dev64(a.tag + slot + c) == want);
         if (!all_in) __builtin_amdgcn_s_sleep(1);
-    } while (!all_in && ++spins < kSpinLimit);
+    } while (!all_in && ++spins < a.xc.spin_limit);
+    if (!all_in) {
+        if (lane == 0) exchange_gave_up(a.xc, kStatusLogits, a.epoch ? a.epoch + row : nullptr);
+        return;
+    }
     Stat mine;
     const float2 ms = __builtin_bit_cast(float2, ld_dev64(reinterpret_cast<const uint64_t*>(a.part + 4 * (slot + c))));
     const float2 ta = __builtin_bit_cast(float2, ld_dev64(reinterpret_cast<const uint64_t*>(a.part + 4 * (slot + c)) + 1));
@@ -185,7 +193,7 @@ __global__ __launch_bounds__(kThreads) void logit_stats_kernel(LogitArgs a) {
     mine = wave_merge(mine);
     if (lane == 0) {
         write_row(a, row, mine);
-        if (a.epoch) st_dev64(a.epoch + row, epv + 1);   // every other chunk has read it
+        if (a.epoch) epoch_advance(a.epoch + row);   // every other chunk has read it
     }
 }
 

@@ -5,7 +5,8 @@
 // positions, one 256-thread workgroup per partition, so that a handful of
 // units still spreads over the whole chip.  Two schedules:
 //
-// One kernel (calls of at most kFuseMaxGroups partitions, select_fused_kernel):
+// One kernel (calls of at most kSelectFuseMaxGroups partitions whose units'
+// partitions fit on the device at once, select_fused_kernel):
 // the partitions of a unit are resident together and exchange nonzero
 // histogram bins, then bin-d1 candidates through the workspace; every
 // partition then resolves the exact threshold and emits its own selections
@@ -508,7 +509,7 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
 }
 
 // ---------------------------------------------------------------------------
-// One kernel for calls of at most kFuseMaxGroups partition workgroups.  The
+// One kernel for calls of at most kSelectFuseMaxGroups partition workgroups.  The
 // partitions of one unit are resident together (workgroups are dispatched in
 // index order and a unit's partitions are consecutive, so when the lowest
 // unfinished unit waits, every workgroup ahead of its partitions has finished)
@@ -526,9 +527,11 @@ __global__ __launch_bounds__(kSelThreads) void select_mark_kernel(SelectArgs a) 
 //      (ties go to the lowest positions, i.e. the first partitions);
 //   D. every partition emits its own selections at its offset; partition 0
 //      also emits the sink and recent ranges and n_idx.
-// Every wait is bounded: a broken invariant gives wrong indices, never a hang.
+// Every wait is bounded: a partition whose wait gives up reports it on the
+// device's status word and leaves without writing indices (the partitions
+// waiting on it then give up too), so a broken invariant never hangs and never
+// uses counts that were not validated.
 // ---------------------------------------------------------------------------
-constexpr int kSpinLimit = 1 << 20;   // bounded wait (far above any real wait)
 
 // A count travels in its tag word: the low 48 bits of the exchange tag above
 // a 16-bit count (successive calls on a workspace use different exchange
@@ -555,9 +558,11 @@ static_assert(2048 * 2 <= kHistSlotWords, "a partition's bin entries must fit it
 
 // Wave 0 polls until the words tag[q*stride] (and tag[q*stride + 1] when c1
 // is given), q < n, all carry the call tag, then writes their counts to c0[q]
-// (and c1[q]); the caller synchronises the workgroup afterwards.
+// (and c1[q]); after spin_limit polls it gives up and sets *failed instead.
+// The caller synchronises the workgroup afterwards.
 __device__ __forceinline__ void wait_counts(const uint64_t* tag, int n, int stride, uint64_t call_tag,
-                                            uint32_t* c0, uint32_t* c1) {
+                                            uint32_t* c0, uint32_t* c1, int spin_limit,
+                                            int* failed) {
     if ((threadIdx.x >> 6) != 0) return;
     const int lane = threadIdx.x & 63;
     const uint64_t want = call_tag & 0xFFFFFFFFFFFFull;
@@ -583,7 +588,11 @@ __device__ __forceinline__ void wait_counts(const uint64_t* tag, int n, int stri
             if (j < nj) in &= (v0[j] >> 16) == want && (v1[j] >> 16) == want;
         all_in = __all(in);
         if (!all_in) __builtin_amdgcn_s_sleep(1);
-    } while (!all_in && ++spins < kSpinLimit);
+    } while (!all_in && ++spins < spin_limit);
+    if (!all_in) {
+        if (lane == 0) *failed = 1;
+        return;
+    }
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
         const int q = lane + j * kWave;
@@ -625,6 +634,12 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
     __shared__ int n_eq;                          // candidates sharing tau's top 22 bits
     __shared__ uint2 cand_lds[kTailCand];
     __shared__ uint16_t cand_p[kTailCand];
+    __shared__ int wait_failed;
+    // a wait gave up (or an earlier captured call on this workspace did):
+    // report it and leave (workgroup-uniform: called after a barrier)
+    auto give_up = [&]() {
+        if (tid == 0) exchange_gave_up(a.xc, kStatusSelect, a.epoch ? a.epoch + u : nullptr);
+    };
 
     uint32_t keys[4 * NR];
 #pragma unroll
@@ -646,7 +661,10 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
         n_above[tid] = 0u;
         n_tie[tid] = 0u;
     }
-    if (tid == 0) n_eq = 0;
+    if (tid == 0) {
+        n_eq = 0;
+        wait_failed = 0;
+    }
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < 4 * NR; ++j)
@@ -654,6 +672,11 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
     __syncthreads();
     const uint64_t epv = scalar_here(ep);
     const uint64_t want = exchange_tag(a.call_tag, epv);
+    const uint64_t pub = want ^ a.xc.tag_flip;   // what this partition publishes
+    if (epoch_is_dirty(epv)) {   // an earlier captured call on this workspace gave up
+        give_up();
+        return;
+    }
 
     // ---- A. nonzero histogram bins -----------------------------------------
     {
@@ -669,9 +692,9 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
         uint64_t* dst = reinterpret_cast<uint64_t*>(a.hist + (up0 + p) * kHistSlotWords);
 #pragma unroll
         for (int q = 0; q < 8; ++q)
-            if (hv[q] != 0u) st_dev64(dst + slot++, bin_entry(want, 8 * tid + q, hv[q]));
+            if (hv[q] != 0u) st_dev64(dst + slot++, bin_entry(pub, 8 * tid + q, hv[q]));
         // (no wait for the entry stores: every entry carries the call tag)
-        if (tid == 0) st_dev64(tag + (size_t)p * kTags + 0, tagged(want, (uint32_t)n_entries));
+        if (tid == 0) st_dev64(tag + (size_t)p * kTags + 0, tagged(pub, (uint32_t)n_entries));
     }
     __syncthreads();
     for (int x = tid; x < 2048; x += kSelThreads) hist[x] = 0u;   // now the unit's histogram
@@ -683,7 +706,8 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
         // call tag; then any entries past the first 64 the same way
         const uint64_t want48 = want & 0xFFFFFFFFFFFFull;
         const uint64_t etag = want & kBinTagMask;
-        for (int p0 = wave; p0 < P; p0 += 4 * 8) {
+        bool gave_up = false;
+        for (int p0 = wave; p0 < P && !gave_up; p0 += 4 * 8) {
             int n[8];
             uint64_t v[8];
             const uint64_t* ent[8];
@@ -707,7 +731,11 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
                 }
                 all_in = __all(in);
                 if (!all_in) __builtin_amdgcn_s_sleep(1);
-            } while (!all_in && ++spins < kSpinLimit);
+            } while (!all_in && ++spins < a.xc.spin_limit);
+            if (!all_in) {   // wave-uniform
+                gave_up = true;
+                break;
+            }
             bool more = false;
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
@@ -724,7 +752,11 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
                     for (int j = 0; j < 8; ++j) in &= e0 + lane >= n[j] || (v[j] >> kBinPayloadBits) == etag;
                     all_in = __all(in);
                     if (!all_in) __builtin_amdgcn_s_sleep(1);
-                } while (!all_in && ++spins < kSpinLimit);
+                } while (!all_in && ++spins < a.xc.spin_limit);
+                if (!all_in) {
+                    gave_up = true;
+                    break;
+                }
                 more = false;
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
@@ -734,8 +766,13 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
                 }
             }
         }
+        if (gave_up && lane == 0) wait_failed = 1;
     }
     __syncthreads();
+    if (wait_failed) {
+        give_up();
+        return;
+    }
     {
         // thread t: bins 2047-8t down to 2040-8t
         const uint4 h0 = *reinterpret_cast<const uint4*>(hist + 2040 - 8 * tid);
@@ -801,11 +838,15 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
         int nd = 0;
 #pragma unroll
         for (int w = 0; w < kSelWaves; ++w) nd += def_w[w];
-        st_dev64(tag + (size_t)p * kTags + 1, tagged(want, (uint32_t)run));
-        st_dev64(tag + (size_t)p * kTags + 2, tagged(want, (uint32_t)nd));
+        st_dev64(tag + (size_t)p * kTags + 1, tagged(pub, (uint32_t)run));
+        st_dev64(tag + (size_t)p * kTags + 2, tagged(pub, (uint32_t)nd));
     }
-    wait_counts(tag + 1, P, kTags, want, n_cnt, n_def);
+    wait_counts(tag + 1, P, kTags, want, n_cnt, n_def, a.xc.spin_limit, &wait_failed);
     __syncthreads();
+    if (wait_failed) {
+        give_up();
+        return;
+    }
 
     // ---- C. every partition resolves tau ------------------------------------
     const int my_cnt = tid < P ? (int)n_cnt[tid] : 0;
@@ -995,18 +1036,16 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
         if (c_head == 0 && tid == 0) a.n_idx[b] = rbase + n_recent;
         // every partition has published, so has read the epoch; advanced last,
         // after the kernel's final wait for loads
-        if (a.epoch && tid == 0) st_dev64(a.epoch + u, epv + 1);
+        if (a.epoch && tid == 0) epoch_advance(a.epoch + u);
     }
 }
 
-// Calls of at most kFuseMaxGroups partition workgroups run as one kernel;
-// larger ones as histogram, mark and finish kernels.
-constexpr int kFuseMaxGroups = 256;
-
+// One kernel when the caller chose it (a.fused); otherwise histogram, mark and
+// finish kernels.
 template <int NR>
 void launch_nr(const SelectArgs& a, int n_units, hipStream_t stream) {
     const dim3 grid(a.parts, n_units), block(kSelThreads);
-    if ((long long)a.parts * n_units <= kFuseMaxGroups) {
+    if (a.fused) {
         hipLaunchKernelGGL(select_fused_kernel<NR>, grid, block, 0, stream, a);
     } else {
         hipLaunchKernelGGL(select_hist_kernel<NR>, grid, block, 0, stream, a);
@@ -1021,6 +1060,26 @@ int select_part_len(int max_t) {
     int nr = 1;
     while (nr < kSelectMaxRounds && (long long)nr * kRound * kSelectTargetParts < max_t) nr <<= 1;
     return nr * kRound;
+}
+
+template <int NR>
+int blocks_per_cu_nr() {
+    int blocks = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, select_fused_kernel<NR>, kSelThreads, 0) !=
+        hipSuccess) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    return blocks;
+}
+
+int select_blocks_per_cu(int part) {
+    switch (part / kRound) {
+        case 1: return blocks_per_cu_nr<1>();
+        case 2: return blocks_per_cu_nr<2>();
+        case 4: return blocks_per_cu_nr<4>();
+        default: return blocks_per_cu_nr<8>();
+    }
 }
 
 hipError_t launch_select(const SelectArgs& a, int n_units, hipStream_t stream) {

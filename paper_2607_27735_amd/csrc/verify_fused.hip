@@ -27,9 +27,10 @@
 //
 // The wait ends: workgroups are dispatched in index order and the chunks of
 // one head are consecutive, so when the lowest unfinished head waits, every
-// workgroup ahead of its chunks has finished and its chunks (at most a few
-// per XCD) are resident.  The waits are also bounded, so a broken invariant
-// cannot hang the GPU (the results would then be wrong, never a fault).
+// workgroup ahead of its chunks has finished and its chunks are resident (the
+// host plans at most half of what the device's CUs hold at once per head).
+// The wait is also bounded: a workgroup whose wait gives up reports it on the
+// device's status word and leaves without writing scores or outputs.
 #include <algorithm>
 #include <atomic>
 
@@ -43,7 +44,6 @@ using namespace vc;
 constexpr int kStashPad = 4;          // floats of padding per stashed row
 constexpr int kParkStride = kHeadDim + 4;                 // floats per parked output row
 constexpr int kParkFloats = 2 * 16 * kParkStride;         // two waves' slices of a row tile
-constexpr int kSpinLimit = 1 << 22;   // bounded wait (far above any real wait)
 constexpr float kLazy = 8.f;          // reference-maximum slack, log2 units
 
 template <int NRT>
@@ -68,12 +68,12 @@ constexpr int max_fused_chunk() {
 
 __device__ __forceinline__ float safe_max(float m) { return m == -INFINITY ? 0.f : m; }
 
-// Wave 0 polls until tag[0 .. n) all equal `want`; the caller synchronises
-// the workgroup afterwards.
+// Wave 0 polls until tag[0 .. n) all equal `want` (true), or gives up after
+// spin_limit polls (false); the caller synchronises the workgroup afterwards.
 // Up to 128 tags (the most chunks a head may have here); the next poll is
 // issued before the previous one is checked, so that the last tag is seen
 // about one round trip after it lands rather than one and a half.
-__device__ __forceinline__ void wait_unit(const uint64_t* tag, int n, uint64_t want) {
+__device__ __forceinline__ bool wait_unit(const uint64_t* tag, int n, uint64_t want, int spin_limit) {
     const int lane = threadIdx.x & 63;
     // every lane loads (lanes past n re-read the last tag): no branch around
     // the loads, so the compiler need not wait for them where they are issued
@@ -81,13 +81,14 @@ __device__ __forceinline__ void wait_unit(const uint64_t* tag, int n, uint64_t w
     const uint64_t* p1 = tag + min(lane + kWave, n - 1);
     const bool use1 = lane + kWave < n;
     uint64_t c0 = ld_dev64(p0), c1 = ld_dev64(p1);
-    for (int spins = 0; spins < kSpinLimit; ++spins) {
+    for (int spins = 0; spins < spin_limit; ++spins) {
         const uint64_t n0 = ld_dev64(p0), n1 = ld_dev64(p1);
-        if (__all(c0 == want && (!use1 || c1 == want))) break;
+        if (__all(c0 == want && (!use1 || c1 == want))) return true;
         __builtin_amdgcn_s_sleep(1);
         c0 = n0;
         c1 = n1;
     }
+    return false;
 }
 
 // One 32-key tile: online softmax and P.V; the tile's probabilities relative
@@ -167,6 +168,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     __shared__ float2 row_ml[kRowCap];
     __shared__ float row_lse[kRowCap];
     __shared__ float2 lse_part[kWaves][kRowCap];
+    __shared__ int wait_failed;
 
     const int slot = blockIdx.x;
     const Item it = decode_item(a.seq, slot, a.n_kv_heads, a.chunk);
@@ -216,7 +218,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     // trip overlaps the stores below (the tag is formed only after the wait
     // for them); chunk 0 advances it at its end, when every chunk has
     // published, and so has read it.
-    const uint64_t ep = fa.epoch ? ld_dev64(fa.epoch + slot0) : 0ull;
+    const uint64_t ep = fa.epoch ? ld_dev64(fa.epoch + unit) : 0ull;
 #pragma unroll
     for (int rt = 0; rt < NRT; ++rt) {
         L[rt] += shfl_xor_f(L[rt], 16);
@@ -298,9 +300,18 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     __syncthreads();
     const uint64_t epv = scalar_here(ep);
     const uint64_t want = exchange_tag(fa.call_tag, epv);
-    if (tid == 0) st_dev64(fa.tag + slot, want);
-    if (wave == 0) wait_unit(fa.tag + slot0, nchunk, want);
+    // a dirty epoch: an earlier captured call on this workspace gave up
+    const bool clean = !epoch_is_dirty(epv);
+    if (clean && tid == 0) st_dev64(fa.tag + slot, want ^ fa.xc.tag_flip);
+    if (clean && wave == 0) {
+        const bool in = wait_unit(fa.tag + slot0, nchunk, want, fa.xc.spin_limit);
+        if (lane == 0) wait_failed = !in;
+    }
     __syncthreads();
+    if (!clean || wait_failed) {
+        if (tid == 0) exchange_gave_up(fa.xc, kStatusVerify, fa.epoch ? fa.epoch + unit : nullptr);
+        return;
+    }
 
     // The first chunks of this workgroup's first row in step 4 (all of them
     // for up to 32 chunks), loaded now so that the round trip overlaps 3a, 3b.
@@ -465,28 +476,29 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     }
     // every chunk has published, so has read the epoch; advanced last, after
     // the workgroup's final wait for loads
-    if (fa.epoch && tid == 0 && slot == slot0) st_dev64(fa.epoch + slot0, epv + 1);
+    if (fa.epoch && tid == 0 && slot == slot0) epoch_advance(fa.epoch + unit);
 }
 
 template <int NRT>
-hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, hipStream_t stream) {
+constexpr size_t fused_lds_bytes(int chunk) {
     // the probability stash with its tile maxima, then the parking slices
-    const size_t dyn =
-        ((size_t)NRT * 16 * (a.v.chunk + kStashPad + a.v.chunk / kTile) + kParkFloats) * sizeof(float);
-    // The kernels' dynamic LDS limit is raised to the largest stash, and the
-    // CU count read, once per device (doing either twice is harmless, so a
-    // race between threads is too).
+    return ((size_t)NRT * 16 * (chunk + kStashPad + chunk / kTile) + kParkFloats) * sizeof(float);
+}
+
+// Once per device and row-tile count: the kernels' dynamic LDS limit is raised
+// to the largest stash, and the CU count and the workgroups a CU holds at that
+// LDS use are read (doing this twice is harmless, so a race between threads is
+// too).  Packed as n_cu * 16 + blocks per CU.
+template <int NRT>
+hipError_t fused_setup(int* n_cu, int* per_cu) {
     constexpr int kMaxDevices = 64;
-    static std::atomic<int> cus[kMaxDevices];   // 0: not set up yet
+    static std::atomic<int> state[kMaxDevices];   // packed + 1; 0: not set up yet
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
-    int n_cu = dev >= 0 && dev < kMaxDevices ? cus[dev].load(std::memory_order_relaxed) : 0;
-    if (n_cu == 0) {
-        const int lds = (int)(((size_t)NRT * 16 *
-                                   (fused_max_chunk(NRT) + kStashPad + fused_max_chunk(NRT) / kTile) +
-                               kParkFloats) *
-                              sizeof(float));
+    int st = dev >= 0 && dev < kMaxDevices ? state[dev].load(std::memory_order_relaxed) : 0;
+    if (st == 0) {
+        const int lds = (int)fused_lds_bytes<NRT>(max_fused_chunk<NRT>());
         const void* fns[4] = {reinterpret_cast<const void*>(verify_fused_kernel<NRT, true, false>),
                               reinterpret_cast<const void*>(verify_fused_kernel<NRT, false, false>),
                               reinterpret_cast<const void*>(verify_fused_kernel<NRT, true, true>),
@@ -495,10 +507,26 @@ hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, hipStream_t stream)
             e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
             if (e != hipSuccess) return e;
         }
-        e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+        int cu = 0, blocks = 0;
+        e = hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev);
         if (e != hipSuccess) return e;
-        if (dev >= 0 && dev < kMaxDevices) cus[dev].store(n_cu, std::memory_order_relaxed);
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, verify_fused_kernel<NRT, true, false>,
+                                                         kThreads, lds);
+        if (e != hipSuccess) return e;
+        st = cu * 16 + std::min(blocks, 15) + 1;
+        if (dev >= 0 && dev < kMaxDevices) state[dev].store(st, std::memory_order_relaxed);
     }
+    *n_cu = (st - 1) / 16;
+    *per_cu = (st - 1) % 16;
+    return hipSuccess;
+}
+
+template <int NRT>
+hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, hipStream_t stream) {
+    const size_t dyn = fused_lds_bytes<NRT>(a.v.chunk);
+    int n_cu = 0, per_cu = 0;
+    const hipError_t e = fused_setup<NRT>(&n_cu, &per_cu);
+    if (e != hipSuccess) return e;
     // non-temporal K/V loads when every workgroup runs in the first round
     const bool paged = a.v.block_table != nullptr;
     if (n_slots <= n_cu) {
@@ -515,6 +543,16 @@ hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, hipStream_t stream)
     return hipGetLastError();
 }
 
+template <int NRT>
+int blocks_per_cu_nrt() {
+    int n_cu = 0, per_cu = 0;
+    if (fused_setup<NRT>(&n_cu, &per_cu) != hipSuccess) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    return per_cu;
+}
+
 }  // namespace
 
 int fused_max_chunk(int row_tiles) {
@@ -523,6 +561,15 @@ int fused_max_chunk(int row_tiles) {
         case 2: return max_fused_chunk<2>();
         case 3: return max_fused_chunk<3>();
         default: return max_fused_chunk<4>();
+    }
+}
+
+int fused_blocks_per_cu(int row_tiles) {
+    switch (row_tiles) {
+        case 1: return blocks_per_cu_nrt<1>();
+        case 2: return blocks_per_cu_nrt<2>();
+        case 3: return blocks_per_cu_nrt<3>();
+        default: return blocks_per_cu_nrt<4>();
     }
 }
 

@@ -357,3 +357,88 @@ def test_verify_plan_schedules(lib):
         else:
             with pytest.raises(B.SSLError):
                 B.verify_plan(shape, one, ctx, ql)
+
+
+# ---------------------------------------------------------------------------
+# build identity, exchange health, co-residency planning
+# ---------------------------------------------------------------------------
+
+def test_build_id_matches_tree(lib):
+    from paper_2607_27735_amd import build
+    assert B.build_id() == build.source_id()
+
+
+def test_load_refuses_a_stale_library(lib, monkeypatch):
+    from paper_2607_27735_amd import build
+    monkeypatch.setattr(build, "source_id", lambda: "0" * 16)
+    monkeypatch.setattr(B, "_lib", None)
+    with pytest.raises(RuntimeError, match="built from other sources"):
+        B.load()
+
+
+def test_exchange_hooks_validate(lib):
+    assert lib.ssl_exchange_status(None, None) == B.SSL_ERR_NULL
+    assert lib.ssl_set_cu_budget(-1) == B.SSL_ERR_SHAPE
+    assert lib.ssl_test_exchange_faults(-1, 0) == B.SSL_ERR_SHAPE
+    assert lib.ssl_test_exchange_faults(16, 2) == B.SSL_ERR_SHAPE
+    assert lib.ssl_test_exchange_faults(0, 0) == B.SSL_OK
+
+
+@pytest.fixture
+def cu_budget(lib):
+    yield lambda n: B.set_cu_budget(n)
+    B.set_cu_budget(0)
+
+
+def _plan_32k(rows_q=7, group=4, T=32768, batch=1, hkv=8):
+    s = _shape(batch=batch, n_q_heads=hkv * group, n_kv_heads=hkv, max_ctx=T, max_q=rows_q)
+    p = _params(budget=2048)
+    return s, p, [T] * batch, [rows_q] * batch
+
+
+def test_verify_plan_follows_the_cu_budget(lib, cu_budget):
+    """The one-sweep schedule needs every chunk of a (sequence, KV head) resident
+    at once, within half of what the CUs hold (one workgroup per CU here): the
+    32K workload's heads take 32 chunks of 1024 keys (the LDS stash's limit at
+    28 rows), which fit a 64-CU budget but not a 62-CU one."""
+    s, p, ctx, ql = _plan_32k()
+    cu_budget(256)
+    assert B.verify_plan(s, p, ctx, ql) == (B.VERIFY_ONE_SWEEP, 1024, 256)
+    cu_budget(64)
+    assert B.verify_plan(s, p, ctx, ql) == (B.VERIFY_ONE_SWEEP, 1024, 256)
+    cu_budget(62)
+    assert B.verify_plan(s, p, ctx, ql)[0] == B.VERIFY_TWO_SWEEP
+    cu_budget(16)
+    assert B.verify_plan(s, p, ctx, ql)[0] == B.VERIFY_TWO_SWEEP
+    # a one-sweep request that cannot be resident is refused, not launched
+    one = _params(budget=2048, verify_mode=B.VERIFY_ONE_SWEEP)
+    n = ctypes.c_size_t(0)
+    ctx_a, ctx_p = _i32(*ctx)
+    q_a, q_p = _i32(*ql)
+    assert lib.ssl_verify_workspace(ctypes.byref(s), ctypes.byref(one), ctx_p, q_p,
+                                    ctypes.byref(n)) == B.SSL_ERR_UNSUPPORTED
+    # a short context still fits in a small budget
+    s2, p2, ctx2, ql2 = _plan_32k(T=4096)
+    assert B.verify_plan(s2, p2, ctx2, ql2)[0] == B.VERIFY_ONE_SWEEP
+
+
+def test_select_plan_follows_the_cu_budget(lib, cu_budget):
+    s, p, ctx, _ = _plan_32k()
+    cu_budget(256)
+    assert B.select_plan(s, p, ctx) == (True, 1024, 32)
+    cu_budget(32)          # 16 resident partitions < 32 per unit: three kernels
+    assert B.select_plan(s, p, ctx) == (False, 1024, 32)
+    cu_budget(256)         # more than 256 partitions in the call: three kernels
+    s8, p8, ctx8, _ = _plan_32k(batch=2)
+    assert B.select_plan(s8, p8, ctx8)[0] is False
+
+
+def test_every_workspace_starts_with_the_epoch_words(lib):
+    """All layouts share a 64 KiB prefix of exchange epochs (8192 words), so calls
+    that share a workspace never store other data over each other's epochs."""
+    s, p, ctx, ql = _plan_32k()
+    assert B.verify_workspace_bytes(s, p, ctx, ql) > 65536
+    assert B.select_workspace_bytes(s, p, ctx) > 65536
+    assert B.draft_workspace_bytes(s, p, [2048]) > 65536
+    n = ctypes.c_size_t(0)
+    assert lib.ssl_logit_stats_workspace(1, 1000, ctypes.byref(n)) == B.SSL_OK and n.value > 65536

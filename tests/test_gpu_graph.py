@@ -95,3 +95,55 @@ def test_graph_replays_match_eager_calls():
         if r > 0:
             assert not torch.equal(out, prev_out), f"replay {r}: output did not change"
         prev_out = out.clone()
+
+
+def test_graph_with_one_shared_workspace():
+    """verify -> select (three kernels: more than 256 partitions) -> draft
+    captured with ONE workspace for the three calls, replayed with new inputs.
+    Every layout keeps its exchange epochs in the same leading words, so the
+    select histograms never land on the draft's epochs."""
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2608)
+    batch, t, max_ctx = 3, 16384, 16392
+    q = torch.empty(batch, QLEN, HQ, D, dtype=torch.bfloat16, device=dev)
+    k = torch.empty(batch, HKV, max_ctx, D, dtype=torch.bfloat16, device=dev)
+    v = torch.empty_like(k)
+    qd = torch.empty(batch, HQ, D, dtype=torch.bfloat16, device=dev)
+    _refill(gen, q, k, v, qd)
+    params = B.make_params(D ** -0.5, budget=BUDGET, out_fp32=True)
+    ctx, ql = [t] * batch, [QLEN] * batch
+    n_idx_host = B.index_count(t, params.k_sink, params.k_recent, BUDGET)
+    out = torch.empty(batch, QLEN, HQ, D, dtype=torch.float32, device=dev)
+    scores = torch.empty(batch, HKV, max_ctx, dtype=torch.float32, device=dev)
+    idx = torch.empty(batch, HKV, BUDGET, dtype=torch.int32, device=dev)
+    n_idx = torch.empty(batch, dtype=torch.int32, device=dev)
+    dout = torch.empty(batch, HQ, D, dtype=torch.float32, device=dev)
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    st = B.PreparedStep(q, k, v, qd, ctx, ql, params, out, scores, idx, n_idx, dout, stream=cap,
+                        shared_workspace=True)
+    assert B.verify_plan(st.shape, params, ctx, ql)[0] == B.VERIFY_ONE_SWEEP
+    assert B.select_plan(st.shape, params, ctx)[0] is False
+    with torch.cuda.stream(cap):
+        st.step()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=cap):
+        st.step()
+    torch.cuda.synchronize()
+    for r in range(REPLAYS):
+        print(f"[graph, shared workspace] replay {r}", flush=True)
+        _refill(gen, q, k, v, qd)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        out_e, scores_e = B.verify_attn(q, k, v, ctx, ql, params)
+        idx_e, n_idx_e = B.select_topb(scores_e, ctx, params)
+        dout_e = B.draft_attn(qd, k, v, idx_e, [n_idx_host] * batch, params)
+        torch.cuda.synchronize()
+        assert torch.equal(out, out_e), f"replay {r}: verify output"
+        assert torch.equal(scores[:, :, :t], scores_e[:, :, :t]), f"replay {r}: scores"
+        assert torch.equal(idx[:, :, :n_idx_host], idx_e[:, :, :n_idx_host]), f"replay {r}: idx"
+        assert torch.equal(dout, dout_e), f"replay {r}: draft output"
+    assert B.exchange_status() == 0
