@@ -213,6 +213,27 @@ int32_t ssl_index_count(int32_t T, int32_t k_sink, int32_t k_recent, int32_t bud
 int ssl_verify_workspace(const ssl_shape *shape, const ssl_params *params,
                          const int32_t *ctx_len_host, const int32_t *q_len_host,
                          size_t *bytes_out);
+/*
+ * ssl_verify_attn for callers that cannot allocate device memory (code under
+ * HIP graph capture, serving loops and harnesses that forbid allocation): the
+ * same computation, arguments, limits and errors, with no workspace argument.
+ * Its workspace is a 128 MiB device array the library holds on each GPU it
+ * runs on until the process ends (it fits every workspace of the five
+ * workloads the library is measured on; the largest needs 105 MiB).  The call
+ * itself allocates nothing.  SSL_ERR_WORKSPACE if ssl_verify_workspace reports
+ * more than 128 MiB for these arguments; SSL_ERR_HIP if the array's address
+ * cannot be found on the current device.  Every call on one GPU shares that
+ * GPU's array: calls that overlap in time on one GPU (concurrent streams,
+ * threads, or graphs replayed concurrently) race and give unspecified results.
+ * The array needs no initial contents; an eager call re-arms the exchange
+ * epochs of the units it covers, lifting the mark that a captured call whose
+ * exchange gave up may have left.
+ */
+int ssl_verify_attn_static(const ssl_shape *shape, const ssl_params *params,
+                           const int32_t *ctx_len_host, const int32_t *q_len_host,
+                           const void *q, const void *k_cache, const void *v_cache,
+                           void *out, float *scores, hipStream_t stream);
+
 /* The schedule ssl_verify_attn would use for these arguments: *schedule_out
  * = SSL_VERIFY_ONE_SWEEP or SSL_VERIFY_TWO_SWEEP (one sweep still falls back
  * to two if the device refuses the co-resident launch), *chunk_out = keys per

@@ -34,7 +34,7 @@ VERIFY_ONE_SWEEP = 2
 EXPORTED = [
     "ssl_status_string", "ssl_build_id", "ssl_exchange_status", "ssl_set_cu_budget",
     "ssl_test_exchange_faults", "ssl_index_count",
-    "ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn",
+    "ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn", "ssl_verify_attn_static",
     "ssl_select_workspace", "ssl_select_plan", "ssl_select_topb",
     "ssl_draft_workspace", "ssl_draft_attn",
     "ssl_verify_attn_paged", "ssl_draft_attn_paged",
@@ -105,6 +105,7 @@ def load(path: Optional[str] = None):
     lib.ssl_verify_workspace.argtypes = [sp, pp, _i32p, _i32p, _szp]
     lib.ssl_verify_attn.argtypes = [sp, pp, _i32p, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
     lib.ssl_verify_plan.argtypes = [sp, pp, _i32p, _i32p, _i32p, _i32p, _i32p]
+    lib.ssl_verify_attn_static.argtypes = [sp, pp, _i32p, _i32p, _vp, _vp, _vp, _vp, _vp, _vp]
     lib.ssl_select_workspace.argtypes = [sp, pp, _i32p, _szp]
     lib.ssl_select_plan.argtypes = [sp, pp, _i32p, _i32p, _i32p, _i32p]
     lib.ssl_select_topb.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _sz, _vp]
@@ -124,7 +125,8 @@ def load(path: Optional[str] = None):
     lib.ssl_greedy_accept_workspace.argtypes = [_i32, _i32, _i32, _szp]
     lib.ssl_greedy_accept.argtypes = [_vp, _i32, _i32, _i32, _i32p, _i32, _i32, _vp, _vp, _vp,
                                       _vp, _sz, _vp]
-    for f in ("ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn", "ssl_select_workspace",
+    for f in ("ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn",
+              "ssl_verify_attn_static", "ssl_select_workspace",
               "ssl_select_topb", "ssl_select_plan", "ssl_draft_workspace", "ssl_draft_attn", "ssl_draft_materialize",
               "ssl_draft_step_workspace", "ssl_draft_step", "ssl_verify_attn_paged",
               "ssl_draft_attn_paged", "ssl_logit_stats_workspace",
@@ -285,6 +287,24 @@ def verify_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, ctx_len, q_le
                                   _ptr(workspace), workspace.numel(), _stream(stream)),
            "ssl_verify_attn")
     return out, scores
+
+
+def verify_attn_static(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, ctx_len, q_len,
+                       params: Params, out: torch.Tensor, scores: torch.Tensor,
+                       stream=None) -> None:
+    """ssl_verify_attn_static: verify attention into caller-given ``out`` and
+    ``scores`` with the library's own device scratch as the workspace (no
+    allocation anywhere in the call)."""
+    _need_gpu(q, k, v, out, scores)
+    if q.dtype != torch.bfloat16 or k.dtype != torch.bfloat16 or v.dtype != torch.bfloat16:
+        raise TypeError("q, k, v must be bfloat16")
+    shape = verify_shape(q, k)
+    ctx, ql = _host_i32(ctx_len), _host_i32(q_len)
+    _check(load().ssl_verify_attn_static(ctypes.byref(shape), ctypes.byref(params),
+                                         ctx.ctypes.data_as(_i32p), ql.ctypes.data_as(_i32p),
+                                         _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(scores),
+                                         _stream(stream)),
+           "ssl_verify_attn_static")
 
 
 # ---------------------------------------------------------------------------

@@ -62,20 +62,23 @@ ssl_shape unit_shape(const ssl_shape* s, const ssl_params* p) {
 // outputs for whichever schedule needs more, plus the one-sweep tags.
 constexpr int kFusedMaxSlotsPerUnit = 128;
 
+// A 64-bit mixing function (the finaliser of Steele et al.'s splitmix64).
+uint64_t mix64(uint64_t x) {
+    x ^= x >> 33;
+    x *= 0xff51afd7ed558ccdull;
+    x ^= x >> 33;
+    x *= 0xc4ceb9fe1a85ec53ull;
+    x ^= x >> 33;
+    return x;
+}
+
 // One-sweep publication tags: a process-wide sequence whose start mixes the
 // clock and the process id, so that tags differ between calls and, with
 // overwhelming probability, from whatever a workspace held before.
 uint64_t next_call_tag() {
-    static std::atomic<uint64_t> seq{[] {
-        uint64_t x = (uint64_t)std::chrono::steady_clock::now().time_since_epoch().count();
-        x ^= (uint64_t)getpid() << 32;
-        x ^= x >> 33;   // splitmix64 finaliser
-        x *= 0xff51afd7ed558ccdull;
-        x ^= x >> 33;
-        x *= 0xc4ceb9fe1a85ec53ull;
-        x ^= x >> 33;
-        return x;
-    }()};
+    static std::atomic<uint64_t> seq{mix64(
+        (uint64_t)std::chrono::steady_clock::now().time_since_epoch().count() ^
+        ((uint64_t)getpid() << 32))};
     return seq.fetch_add(1, std::memory_order_relaxed) + 1;
 }
 
@@ -475,7 +478,7 @@ int verify_call(const ssl_shape* shape, const ssl_params* params, const int32_t*
                 const int32_t* q_len_host, const void* q, const void* k_cache,
                 const void* v_cache, const int32_t* block_table, int32_t page_size,
                 int32_t max_blocks, void* out, float* scores, void* workspace,
-                size_t workspace_bytes, hipStream_t stream) {
+                size_t workspace_bytes, hipStream_t stream, const StaticScratch* scratch = nullptr) {
     VerifyPlan plan;
     int rc = plan_verify(shape, params, ctx_len_host, q_len_host, &plan);
     if (rc) return rc;
@@ -487,6 +490,13 @@ int verify_call(const ssl_shape* shape, const ssl_params* params, const int32_t*
     if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16) ||
         !aligned(scores, 4))
         return SSL_ERR_ALIGN;
+    if (scratch) {
+        // the library's static scratch: refuse what it cannot hold, then (the
+        // arguments all checked) look up its address on this device
+        if (plan.bytes > scratch->bytes) return SSL_ERR_WORKSPACE;
+        if (scratch->address(&workspace) != hipSuccess) return SSL_ERR_HIP;
+        workspace_bytes = scratch->bytes;
+    }
     rc = check_workspace(workspace, workspace_bytes, plan.bytes);
     if (rc) return rc;
 
@@ -528,6 +538,11 @@ int verify_call(const ssl_shape* shape, const ssl_params* params, const int32_t*
         rc = make_exchange(&fa.xc);
         if (rc) return rc;
         fa.call_tag = next_call_tag();
+        // An eager call on the static scratch, which no caller can clear,
+        // re-arms its units' epochs with a value unrelated to earlier epochs,
+        // lifting the mark a captured call that gave up may have left there.
+        fa.heal = scratch && !fa.epoch ? static_cast<uint64_t*>(workspace) : nullptr;
+        fa.heal_value = mix64(fa.call_tag);
         return launch_verify_fused(fa, plan.fused_slots, plan.row_tiles, stream) ==
                        hipSuccess
                    ? SSL_OK
@@ -539,6 +554,18 @@ int verify_call(const ssl_shape* shape, const ssl_params* params, const int32_t*
 }
 
 }  // namespace
+
+namespace ssl {
+
+int verify_attn_static_scratch(const ssl_shape* shape, const ssl_params* params,
+                               const int32_t* ctx_len_host, const int32_t* q_len_host,
+                               const void* q, const void* k_cache, const void* v_cache, void* out,
+                               float* scores, const StaticScratch& scratch, hipStream_t stream) {
+    return verify_call(shape, params, ctx_len_host, q_len_host, q, k_cache, v_cache, nullptr, 0, 0,
+                       out, scores, nullptr, 0, stream, &scratch);
+}
+
+}  // namespace ssl
 
 extern "C" {
 

@@ -149,7 +149,19 @@ struct FusedArgs {
     uint64_t* epoch;        // [units] exchange epochs (any initial value), or null
     uint64_t call_tag;      // this call's tag: unique within the process (see exchange_tag)
     Exchange xc;
+    // Eager calls on the library's static scratch: epoch words of the call's
+    // units to set to heal_value + unit at the end (null otherwise).
+    uint64_t* heal;
+    uint64_t heal_value;
 };
+
+// The library's static device scratch (the no-allocation entry point): its
+// size, and how to find its address on the current device.
+struct StaticScratch {
+    size_t bytes;
+    hipError_t (*address)(void** ptr);
+};
+
 
 // Launchers return hipSuccess or the error of the launch.
 hipError_t launch_verify(const VerifyArgs& a, int n_items, int n_rows_total, int row_tiles,

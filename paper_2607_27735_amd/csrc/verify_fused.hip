@@ -477,6 +477,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     // every chunk has published, so has read the epoch; advanced last, after
     // the workgroup's final wait for loads
     if (fa.epoch && tid == 0 && slot == slot0) epoch_advance(fa.epoch + unit);
+    if (fa.heal && tid == 0 && slot == slot0) st_dev64(fa.heal + unit, fa.heal_value + unit);
 }
 
 template <int NRT>

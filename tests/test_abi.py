@@ -442,3 +442,31 @@ def test_every_workspace_starts_with_the_epoch_words(lib):
     assert B.draft_workspace_bytes(s, p, [2048]) > 65536
     n = ctypes.c_size_t(0)
     assert lib.ssl_logit_stats_workspace(1, 1000, ctypes.byref(n)) == B.SSL_OK and n.value > 65536
+
+
+def test_static_verify_validates_before_any_hip_call(lib):
+    """ssl_verify_attn_static checks its arguments, and that the workspace its
+    plan needs fits the library's 128 MiB scratch, before looking the scratch
+    up (so these errors need no GPU)."""
+    s, p = _shape(), _params()
+    ctx, cp = _i32(4000)
+    ql, qp = _i32(5)
+    f = lib.ssl_verify_attn_static
+    assert f(None, ctypes.byref(p), cp, qp, FAKE, FAKE, FAKE, FAKE, FAKE, None) == B.SSL_ERR_NULL
+    assert f(ctypes.byref(s), ctypes.byref(p), cp, qp, None, FAKE, FAKE, FAKE, FAKE,
+             None) == B.SSL_ERR_NULL
+    assert f(ctypes.byref(s), ctypes.byref(p), cp, qp, FAKE_ODD, FAKE, FAKE, FAKE, FAKE,
+             None) == B.SSL_ERR_ALIGN
+    bad = _shape(head_dim=64)
+    assert f(ctypes.byref(bad), ctypes.byref(p), cp, qp, FAKE, FAKE, FAKE, FAKE, FAKE,
+             None) == B.SSL_ERR_UNSUPPORTED
+    # 16 sequences of 131072 keys: a workspace beyond the scratch
+    big = _shape(batch=16, max_ctx=131072)
+    ctxb, cbp = _i32(*[131072] * 16)
+    qlb, qbp = _i32(*[5] * 16)
+    n = ctypes.c_size_t(0)
+    assert lib.ssl_verify_workspace(ctypes.byref(big), ctypes.byref(p), cbp, qbp,
+                                    ctypes.byref(n)) == B.SSL_OK
+    assert n.value > 128 << 20
+    assert f(ctypes.byref(big), ctypes.byref(p), cbp, qbp, FAKE, FAKE, FAKE, FAKE, FAKE,
+             None) == B.SSL_ERR_WORKSPACE
