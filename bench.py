@@ -493,6 +493,126 @@ def cpu_baseline(w, seconds: float):
                       f"units with {threads} threads available"}
 
 
+def oracle_times(w, threads: int, repeats: int):
+    """The oracle's verify, select and draft on the workload, each timed on its
+    own (median of ``repeats``), with ``threads`` OpenMP threads."""
+    import numpy as np
+    import oracle
+    oracle.set_num_threads(threads)
+    tv, ts, td = [], [], []
+    for _ in range(repeats):
+        t0 = time.perf_counter()
+        _, s = oracle.verify(w)
+        t1 = time.perf_counter()
+        idx, n_idx = oracle.select(w, s)
+        t2 = time.perf_counter()
+        oracle.draft(w, np.maximum(idx, 0), n_idx)
+        t3 = time.perf_counter()
+        tv.append(t1 - t0)
+        ts.append(t2 - t1)
+        td.append(t3 - t2)
+    med = lambda x: round(statistics.median(x) * 1e6, 1)
+    return {"threads": threads, "repeats": repeats, "verify_us": med(tv), "select_us": med(ts),
+            "draft_us": med(td),
+            "step_us": round(statistics.median([a + b + c for a, b, c in zip(tv, ts, td)]) * 1e6, 1)}
+
+
+def workload_entry(B, n: int, steps: int, warmup: int, torch, np, cpu: bool):
+    """One named workload measured on its own: bare steps back to back (wall
+    clock), per-call durations from HIP events between the calls (median, p10,
+    p90), each call's average launch from ``steps`` back-to-back calls between
+    two events (GB/s and fraction of the HBM peak from its algorithmic bytes),
+    and the CPU oracle's per-kernel times on the host."""
+    from paper_2607_27735_amd.workloads import make_config
+    t_gen = time.perf_counter()
+    w = make_config(n)
+    t_gen = time.perf_counter() - t_gen
+    dev = torch.device("cuda:0")
+
+    def up(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16).copy()).view(
+            torch.bfloat16).to(dev)
+
+    q, qd = up(w.q), up(w.q_draft)
+    k0, v0 = up(w.k), up(w.v)
+    kv_bytes = k0.numel() * 2 * 2
+    n_copies = max(2, math.ceil((512 << 20) / kv_bytes) + 1)
+    kvs = [(k0, v0)] + [(k0.clone(), v0.clone()) for _ in range(n_copies - 1)]
+    params = B.make_params(w.sm_scale, window=w.window, k_sink=w.k_sink, k_recent=w.k_recent,
+                           budget=w.budget, out_fp32=False)
+    out = torch.empty(q.shape, dtype=torch.bfloat16, device=dev)
+    scores = torch.zeros((w.batch, w.n_kv_heads, w.max_ctx), dtype=torch.float32, device=dev)
+    idx = torch.zeros((w.batch, w.n_kv_heads, w.budget), dtype=torch.int32, device=dev)
+    n_idx = torch.zeros(w.batch, dtype=torch.int32, device=dev)
+    dout = torch.empty(qd.shape, dtype=torch.bfloat16, device=dev)
+    stream = torch.cuda.current_stream()
+    sts = [B.PreparedStep(q, k, v, qd, w.ctx_len, w.q_len, params, out, scores, idx, n_idx, dout,
+                          stream=stream) for (k, v) in kvs]
+    vshape = B.verify_shape(q, k0)
+    schedule, vchunk, vitems = B.verify_plan(vshape, params, w.ctx_len, w.q_len)
+    sel_one, _, sel_parts = B.select_plan(vshape, params, w.ctx_len)
+    for i in range(max(warmup, n_copies)):
+        sts[i % n_copies].step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        sts[i % n_copies].step()
+    torch.cuda.synchronize()
+    step_us = (time.perf_counter() - t0) * 1e6 / steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    for i in range(steps):
+        st, e = sts[i % n_copies], ev[i]
+        e[0].record(stream)
+        st.verify()
+        e[1].record(stream)
+        st.select()
+        e[2].record(stream)
+        st.draft()
+        e[3].record(stream)
+    torch.cuda.synchronize()
+    calls = ("verify", "select", "draft")
+    b2b = {}
+    for c in calls:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for i in range(steps):
+            getattr(sts[i % n_copies], c)()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        b2b[c] = e0.elapsed_time(e1) * 1e3 / steps
+    nbytes, _ = algorithmic_bytes(w, out_bytes=2)
+    entry = {"name": w.name, "batch": w.batch, "n_q_heads": w.n_q_heads,
+             "n_kv_heads": w.n_kv_heads, "ctx_len": list(map(int, w.ctx_len)),
+             "q_len": list(map(int, w.q_len)), "budget": w.budget,
+             "verify_schedule": "one-sweep" if schedule == B.VERIFY_ONE_SWEEP else "two-sweep",
+             "verify_items": vitems, "select_schedule": "one kernel" if sel_one else "three kernels",
+             "select_partitions_per_unit": sel_parts,
+             "step_us": round(step_us, 3), "step_alg_bytes": sum(nbytes.values()),
+             "step_hbm_frac": round(sum(nbytes.values()) / (step_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+             "steps": steps, "kv_copies_rotated": n_copies, "calls": {}}
+    for j, c in enumerate(calls):
+        per = [ev[i][j].elapsed_time(ev[i][j + 1]) * 1e3 for i in range(steps)]
+        gbps = nbytes[c] / (b2b[c] * 1e-6) / 1e9
+        entry["calls"][c] = {"median_us": round(statistics.median(per), 3),
+                             "p10_us": round(float(np.percentile(per, 10)), 3),
+                             "p90_us": round(float(np.percentile(per, 90)), 3),
+                             "back_to_back_us": round(b2b[c], 3), "alg_bytes": nbytes[c],
+                             "gbps": round(gbps, 1), "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4)}
+    assert B.exchange_status(stream) == 0, "an exchange wait gave up"
+    del sts, kvs, q, qd, k0, v0, out, scores, idx, n_idx, dout
+    torch.cuda.empty_cache()
+    if cpu:
+        threads = min(len(os.sched_getaffinity(0)), 16)
+        entry["oracle"] = oracle_times(w, threads, 3 if n <= 2 else 1)
+        if n == 1:
+            entry["oracle_single_thread"] = oracle_times(w, 1, 3)
+            import oracle
+            oracle.set_num_threads(threads)
+    entry["input_generation_s"] = round(t_gen, 1)
+    return entry
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -504,6 +624,8 @@ def main() -> int:
     ap.add_argument("--no-draft-round", action="store_true",
                     help="skip the draft-round and vocabulary-side measurements printed "
                          "beside the headline")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the per-workload table (all five named workloads)")
     ap.add_argument("--mode", choices=["eager", "graph"], default="eager")
     ap.add_argument("--no-graph-step", action="store_true",
                     help="skip the captured-step figure printed beside the eager headline")
@@ -726,6 +848,8 @@ def main() -> int:
                                                   args.steps, torch, np)
         result["vocab_side"] = vocab_side_bench(B, w, stream, args.steps, torch, np)
         result["paged"] = paged_bench(B, w, kvs, q, qd, params, stream, args.steps, torch, np)
+    # every cross-workgroup exchange of the timed calls completed
+    result["exchange_status"] = B.exchange_status(stream)
     # sanity: score mass of every KV head equals min(W, q) * group
     s = scores.double().sum(dim=2).cpu().numpy()
     want = np.array([min(w.window, int(x)) * w.group for x in w.q_len])[:, None]
@@ -740,6 +864,15 @@ def main() -> int:
         del src, dst
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    if not args.no_workloads:
+        del steps, kvs
+        torch.cuda.empty_cache()
+        result["workloads"] = {}
+        for n in sorted(CONFIGS):
+            print(f"[bench] workload {n}", file=sys.stderr, flush=True)
+            result["workloads"][str(n)] = workload_entry(
+                B, n, args.steps if n <= 2 else min(args.steps, 20), args.warmup, torch, np,
+                cpu=not args.no_cpu_baseline)
     print(json.dumps(result), flush=True)
     return 0
 
