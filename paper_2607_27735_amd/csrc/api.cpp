@@ -24,7 +24,6 @@ namespace {
 constexpr size_t kAlign = 256;
 constexpr int kVerifyRowCap = 64;
 constexpr int kDraftRowCap = 16;
-constexpr int kDraftChunk = 128;   // index entries per draft workgroup (4 waves of 32)
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -273,10 +272,14 @@ int plan_draft(const ssl_shape* s, const ssl_params* p, const int32_t* n_idx, Dr
     if (g > kDraftRowCap) return SSL_ERR_UNSUPPORTED;
     memset(&plan->seq, 0, sizeof plan->seq);
     plan->seq.n_seq = s->batch;
-    const int chunk = kDraftChunk;
-    int64_t items = 0;
+    int64_t entries = 0;
     for (int b = 0; b < s->batch; ++b) {
         if (n_idx[b] < 1 || n_idx[b] > p->budget) return SSL_ERR_SHAPE;
+        entries += (int64_t)n_idx[b] * s->n_kv_heads;
+    }
+    const int chunk = draft_chunk_for(entries, device_cus());
+    int64_t items = 0;
+    for (int b = 0; b < s->batch; ++b) {
         plan->seq.item_start[b] = (int32_t)items;
         plan->seq.ctx[b] = n_idx[b];
         items += (int64_t)s->n_kv_heads * ((n_idx[b] + chunk - 1) / chunk);

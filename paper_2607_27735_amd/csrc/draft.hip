@@ -23,6 +23,7 @@
 // group and transposed in registers with byte permutes.
 #include "device_common.h"
 #include "launch.h"
+#include "verify_common.h"
 
 namespace ssl {
 namespace {
@@ -31,7 +32,6 @@ constexpr int kTile = 32;
 constexpr int kRowCap = 16;
 constexpr int kDraftWaves = 4;
 constexpr int kDraftThreads = kDraftWaves * kWave;
-constexpr int kWaveChunk = kTile;              // index entries per wave
 constexpr int kParkStride = kHeadDim + 4;      // floats per parked head row
 constexpr int kMergeBatch = 16;                // partials loaded at once by the merging workgroup
 
@@ -159,8 +159,14 @@ __device__ __forceinline__ void draft_tile(const DraftArgs& a, const u32x4 (&qop
 // copy, and whose window rows are consecutive cache rows.
 constexpr int kPlain = 0, kRoundIdx = 1, kRoundSel = 2, kPlainPaged = 3;
 
-template <int kMode>
-__global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
+// TPW tiles of 32 entries per wave (4 * 32 * TPW entries per workgroup): a
+// wave finds the rows of all its entries at once (64 per lane map), then
+// gathers tile t + 1 while it computes tile t (a two-deep register ring; a
+// third buffer measured no faster).  At most 256 registers per lane, so that
+// a CU holds two workgroups even at four tiles per wave (the 8B batch-8
+// workload's draft: 46.7 -> 25.8 us with both, from 1 tile per wave).
+template <int kMode, int TPW>
+__global__ __launch_bounds__(kDraftThreads, 2) void draft_kernel(DraftArgs a) {
     const DItem it = decode_ditem(a.seq, blockIdx.x, a.n_kv_heads, a.chunk);
     // (read here, outside the wave-dependent branch below, so that they are
     // scalar loads and not vector loads that the index load waits for)
@@ -179,9 +185,9 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
     __shared__ float2 gml[kRowCap];
     __shared__ float park[kDraftWaves][kRowCap][kParkStride];
 
-    // ---- one wave: 64 entries of the index list ----------------------------
-    const int wbeg = it.key_begin + wave * kWaveChunk;
-    const int wend = min(wbeg + kWaveChunk, it.key_end);
+    // ---- one wave: 32 * TPW entries of the index list -----------------------
+    const int wbeg = it.key_begin + wave * kTile * TPW;
+    const int wend = min(wbeg + kTile * TPW, it.key_end);
     float M = -INFINITY, L = 0.f;
     f32x4 oacc[8];
 #pragma unroll
@@ -205,27 +211,46 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
         const size_t sel_off = (size_t)it.unit * a.budget * kHeadDim;
         const RowSource src{a.k + cache_off, a.v + cache_off, a.k_sel + sel_off, a.v_sel + sel_off};
         const int last = it.n - 1;
-        const int e = min(wbeg + lane, last);
-        // Lane l finds the row of entry l once; every K/V row of the tile is
-        // then requested at once.
-        uint32_t my_row;
-        if (kMode == kPlain) {
-            my_row = (uint32_t)min(max(a.idx[(size_t)it.unit * a.budget + e], 0), a.max_ctx - 1);
-        } else if (kMode == kPlainPaged) {
-            const int row = min(max(a.idx[(size_t)it.unit * a.budget + e], 0), a.max_ctx - 1);
-            const int pg = a.block_table[(size_t)it.b * a.max_blocks + row / a.page_size];
-            my_row = (uint32_t)(((size_t)pg * a.n_kv_real + kvc) * a.page_size + row % a.page_size);
-        } else {
-            // (the index load does not wait for n_fixed: entry e < budget is in
-            // bounds, and its value is used only when e < n_fixed)
-            const int32_t fixed_row = kMode == kRoundIdx ? a.idx[(size_t)it.unit * a.budget + e] : 0;
-            my_row = e < nf ? (kMode == kRoundSel ? (uint32_t)e | kSelBit
-                                                  : (uint32_t)min(max(fixed_row, 0), a.max_ctx - 1))
-                            : (uint32_t)min(max(win0 + e - nf, 0), a.max_ctx - 1);
+        // Lane l of map j finds the row of entry 64 j + l once; every K/V row
+        // of a tile is then requested at once.
+        constexpr int kMaps = (TPW + 1) / 2;
+        int32_t raw[kMaps];
+#pragma unroll
+        for (int j = 0; j < kMaps; ++j) {   // all index loads in flight together
+            const int e = min(wbeg + 64 * j + lane, last);
+            raw[j] = (kMode == kPlain || kMode == kPlainPaged || kMode == kRoundIdx)
+                         ? a.idx[(size_t)it.unit * a.budget + e] : 0;
         }
-        Gathered ta;
-        gather_tile<kMode == kRoundSel>(my_row, 0, src, m16, G, ta);
-        draft_tile(a, qop, ta, wbeg, wend, G, M, L, oacc);
+        uint32_t my_row[kMaps];
+#pragma unroll
+        for (int j = 0; j < kMaps; ++j) {
+            const int e = min(wbeg + 64 * j + lane, last);
+            if (kMode == kPlain) {
+                my_row[j] = (uint32_t)min(max(raw[j], 0), a.max_ctx - 1);
+            } else if (kMode == kPlainPaged) {
+                const int row = min(max(raw[j], 0), a.max_ctx - 1);
+                const int pg = a.block_table[(size_t)it.b * a.max_blocks + row / a.page_size];
+                my_row[j] = (uint32_t)(((size_t)pg * a.n_kv_real + kvc) * a.page_size + row % a.page_size);
+            } else {
+                // (the index load does not wait for n_fixed: entry e < budget is
+                // in bounds, and its value is used only when e < n_fixed)
+                my_row[j] = e < nf ? (kMode == kRoundSel ? (uint32_t)e | kSelBit
+                                                         : (uint32_t)min(max(raw[j], 0), a.max_ctx - 1))
+                                   : (uint32_t)min(max(win0 + e - nf, 0), a.max_ctx - 1);
+            }
+        }
+        const int ntile = (wend - wbeg + kTile - 1) / kTile;   // wave-uniform
+        vc::tile_pipeline<2, Gathered>(
+            0, ntile, 1,
+            [&](Gathered& t, int tile) {
+                uint32_t r = my_row[0];
+#pragma unroll
+                for (int j = 1; j < kMaps; ++j) r = (tile >> 1) == j ? my_row[j] : r;
+                gather_tile<kMode == kRoundSel>(r, 32 * (tile & 1), src, m16, G, t);
+            },
+            [&](const Gathered& t, int tile) {
+                draft_tile(a, qop, t, wbeg + kTile * tile, wend, G, M, L, oacc);
+            });
         L += shfl_xor_f(L, 16);
         L += shfl_xor_f(L, 32);
     }
@@ -400,21 +425,44 @@ __global__ __launch_bounds__(kDraftThreads) void draft_materialize_kernel(DraftA
     }
 }
 
+template <int kMode>
+void launch_mode(const DraftArgs& a, int n_items, hipStream_t stream) {
+    switch (a.chunk / (kDraftWaves * kTile)) {
+        case 4:
+            hipLaunchKernelGGL((draft_kernel<kMode, 4>), dim3(n_items), dim3(kDraftThreads), 0, stream, a);
+            break;
+        case 2:
+            hipLaunchKernelGGL((draft_kernel<kMode, 2>), dim3(n_items), dim3(kDraftThreads), 0, stream, a);
+            break;
+        default:
+            hipLaunchKernelGGL((draft_kernel<kMode, 1>), dim3(n_items), dim3(kDraftThreads), 0, stream, a);
+            break;
+    }
+}
+
 }  // namespace
+
+int draft_chunk_for(int64_t entries, int n_cu) {
+    // the most tiles per wave that still leave a workgroup per CU
+    for (int tpw = 4; tpw > 1; tpw >>= 1)
+        if (entries / ((int64_t)kDraftWaves * kTile * tpw) >= (int64_t)n_cu)
+            return kDraftWaves * kTile * tpw;
+    return kDraftWaves * kTile;
+}
 
 hipError_t launch_draft(const DraftArgs& a, int n_items, hipStream_t stream) {
     if (a.block_table)
-        hipLaunchKernelGGL(draft_kernel<kPlainPaged>, dim3(n_items), dim3(kDraftThreads), 0, stream, a);
+        launch_mode<kPlainPaged>(a, n_items, stream);
     else
-        hipLaunchKernelGGL(draft_kernel<kPlain>, dim3(n_items), dim3(kDraftThreads), 0, stream, a);
+        launch_mode<kPlain>(a, n_items, stream);
     return hipGetLastError();
 }
 
 hipError_t launch_draft_step(const DraftArgs& a, int n_items, hipStream_t stream) {
     if (a.k_sel)
-        hipLaunchKernelGGL(draft_kernel<kRoundSel>, dim3(n_items), dim3(kDraftThreads), 0, stream, a);
+        launch_mode<kRoundSel>(a, n_items, stream);
     else
-        hipLaunchKernelGGL(draft_kernel<kRoundIdx>, dim3(n_items), dim3(kDraftThreads), 0, stream, a);
+        launch_mode<kRoundIdx>(a, n_items, stream);
     return hipGetLastError();
 }
 

@@ -187,7 +187,10 @@ int select_part_len(int max_t);
 hipError_t launch_select(const SelectArgs& a, int n_units, hipStream_t stream);
 // Calls of at most this many partition workgroups may run as one kernel.
 constexpr int kSelectFuseMaxGroups = 256;
-// One workgroup per `chunk` (128) index entries; no combine kernel.
+// Index entries per draft workgroup for a call of `entries` entries (all
+// units) on n_cu CUs: 128, 256 or 512 (32, 64 or 128 per wave).
+int draft_chunk_for(int64_t entries, int n_cu);
+// One workgroup per `chunk` index entries; no combine kernel.
 hipError_t launch_draft(const DraftArgs& a, int n_items, hipStream_t stream);
 // Draft round: copy the sink and TopK rows (n_fixed per sequence) of every
 // (sequence, KV head) to k_sel/v_sel; then any number of steps over them and

@@ -56,6 +56,23 @@ NAMES = ["small-b2", "tiny-T", "g16", "window-only", "kv8-ragged", "headline-8b-
 
 @pytest.mark.parametrize("name", NAMES)
 def test_draft_round_matches_oracle(name):
+    _check_round(name)
+
+
+@pytest.mark.parametrize("cus", [1, 4])
+@pytest.mark.parametrize("name", ["small-b2", "kv8-ragged"])
+def test_draft_round_wide_workgroups(name, cus):
+    """Planned for 1 or 4 CUs, the draft kernels take 512 or 256 entries per
+    workgroup (4 or 2 tiles per wave, ragged last tiles) on these small
+    rounds: the same bars against the oracle."""
+    B.set_cu_budget(cus)
+    try:
+        _check_round(name)
+    finally:
+        B.set_cu_budget(0)
+
+
+def _check_round(name):
     w, base, steps = _case(name)
     print(f"[draft round] {name}: batch {w.batch}, {w.n_q_heads}/{w.n_kv_heads} heads, "
           f"base {list(base)}, {steps} steps, budget {w.budget}", flush=True)

@@ -103,3 +103,15 @@ def test_paged_verify_and_draft(name, mode):
     od = gpu_draft(d, idx_dev, n_ref)
     check_outputs(o, o_ref, oa, np.ones(o_ref.shape[:2], dtype=bool), what="paged draft")
     assert np.array_equal(o, od)
+    # planned for one CU: 512 entries per workgroup (4 tiles per wave)
+    B.set_cu_budget(1)
+    try:
+        o4 = B.draft_attn_paged(d.qd, kpd, vpd, btd, w.max_ctx, torch.from_numpy(idx_dev).cuda(),
+                                n_ref, p)
+        torch.cuda.synchronize()
+        od4 = gpu_draft(d, idx_dev, n_ref)
+    finally:
+        B.set_cu_budget(0)
+    o4 = o4.float().cpu().numpy().astype(np.float64)
+    check_outputs(o4, o_ref, oa, np.ones(o_ref.shape[:2], dtype=bool), what="paged draft, wide")
+    assert np.array_equal(o4, od4)

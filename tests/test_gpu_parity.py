@@ -153,6 +153,24 @@ def test_draft_matches_oracle(name):
                   what="draft-bf16")
 
 
+@pytest.mark.parametrize("cus", [1, 4])
+@pytest.mark.parametrize("name", ["ragged-b3", "g16", "kv8-b3", "chunk-ragged"])
+def test_draft_wide_workgroups(name, cus):
+    """Planned for 1 or 4 CUs, the draft takes 512 or 256 entries per workgroup
+    (4 or 2 tiles per wave, ragged last tiles and units); same bars."""
+    w, out_ref, s_ref, oabs_ref = small_case(name)
+    idx_ref, n_ref = oracle.select(w, s_ref.astype(np.float32).astype(np.float64))
+    idx_dev = np.where(idx_ref < 0, 0, idx_ref).astype(np.int32)
+    o_ref = oracle.draft(w, idx_dev, n_ref)
+    oabs = oracle.draft(w, idx_dev, n_ref, v=abs_v(w))
+    B.set_cu_budget(cus)
+    try:
+        o = gpu_draft(Dev(w), idx_dev, n_ref)
+    finally:
+        B.set_cu_budget(0)
+    check_outputs(o, o_ref, oabs, np.ones(o_ref.shape[:2], dtype=bool), what="draft")
+
+
 def test_select_special_cases():
     w = generate(201, name="sel", batch=2, n_q_heads=4, n_kv_heads=2, ctx_len=[3000, 2500],
                  q_len=[1, 1], budget=300, head_dim=128)
