@@ -75,8 +75,10 @@
  *    rejected call has no effect on the device.  Device-side data (scores,
  *    idx) is not validated: index values outside [0, max_ctx) are clamped
  *    (results are then meaningless but memory stays in bounds).
- *  - Limits: head_dim 128; 1 <= batch <= 64; q_len * group <= 64;
- *    max_q <= 64; n_q_heads / n_kv_heads <= 16 for the draft call.
+ *  - Limits: head_dim 128; 1 <= batch <= 64; max_q <= 64; group <= 64 for
+ *    verify (more than 64 rows per KV head, q_len * group > 64, run the
+ *    two-sweep schedule once per block of 64 / group positions);
+ *    n_q_heads / n_kv_heads <= 16 for the draft call.
  */
 #ifndef SPARSESPEC_L_H
 #define SPARSESPEC_L_H
@@ -206,9 +208,13 @@ int32_t ssl_index_count(int32_t T, int32_t k_sink, int32_t k_recent, int32_t bud
  * Errors: SSL_ERR_SHAPE if n_q_heads % n_kv_heads, q_len < 1,
  * q_len > ctx_len, ctx_len > max_ctx, q_len > max_q, max_q > 64, window < 1,
  * sm_scale not positive and finite, or verify_mode unknown;
- * SSL_ERR_UNSUPPORTED if head_dim != 128, batch > 64, q_len * group > 64, or
- * a one-sweep request that does not fit.  The workspace size covers both
- * schedules.
+ * SSL_ERR_UNSUPPORTED if head_dim != 128, batch > 64, group > 64, or a
+ * one-sweep request that does not fit (including any with q_len * group >
+ * 64).  When a KV head has more than 64 verify rows (e.g. Eq. 3 seeded over
+ * the last W = 16 prompt positions of a group of 8), the call runs the
+ * two-sweep schedule once per block of 64 / group positions, last positions
+ * first, and adds the later blocks' scores to the first's.  The workspace
+ * size covers both schedules.
  */
 int ssl_verify_workspace(const ssl_shape *shape, const ssl_params *params,
                          const int32_t *ctx_len_host, const int32_t *q_len_host,

@@ -155,6 +155,7 @@ int64_t resident_group_cap(int blocks_per_cu) {
 
 struct VerifyPlan {
     int chunk, n_items, n_rows, row_tiles;
+    int block_pos;   // verify positions per launch (row blocks); >= every q_len when one block
     bool fused_ok;
     int fused_chunk, fused_slots;
     size_t ml_off, o_off, tag_off, bytes;
@@ -181,7 +182,17 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
         max_rows = std::max(max_rows, ql[b] * g);
         total_keys += (int64_t)ctx[b] * s->n_kv_heads;
     }
-    if (max_rows > kVerifyRowCap) return SSL_ERR_UNSUPPORTED;
+    // More rows per KV head than one launch holds (e.g. Eq. 3 over the last
+    // W = 16 prompt positions of a group of 8): the two-sweep schedule runs
+    // once per block of positions, the scores of later blocks added.
+    if (g > kVerifyRowCap) return SSL_ERR_UNSUPPORTED;
+    plan->block_pos = kVerifyRowCap / g;
+    if (max_rows > kVerifyRowCap) {
+        if (p->verify_mode == SSL_VERIFY_ONE_SWEEP) return SSL_ERR_UNSUPPORTED;
+        max_rows = plan->block_pos * g;
+    } else {
+        plan->block_pos = s->max_q;
+    }
     plan->row_tiles = (max_rows + 15) / 16;
 
     // Two-sweep chunk: a power of two in [128, 2048] giving about one item per CU.
@@ -196,7 +207,7 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
         plan->seq.ctx[b] = ctx[b];
         plan->seq.qlen[b] = ql[b];
         items += (int64_t)s->n_kv_heads * ((ctx[b] + chunk - 1) / chunk);
-        rows += (int64_t)s->n_kv_heads * ql[b] * g;
+        rows += (int64_t)s->n_kv_heads * std::min(ql[b], plan->block_pos) * g;
     }
     if (items > (1 << 30) || rows > (1 << 30)) return SSL_ERR_UNSUPPORTED;
     plan->seq.item_start[s->batch] = (int32_t)items;
@@ -224,7 +235,7 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
     int64_t fc = std::max(per_unit_min, spread);
     fc = std::max<int64_t>(128, (fc + 127) / 128 * 128);
     if (fc > cap) fc = cap / 128 * 128;
-    if (fc >= 128 && ((int64_t)max_ctx + fc - 1) / fc <= max_slots) {
+    if (plan->block_pos >= s->max_q && fc >= 128 && ((int64_t)max_ctx + fc - 1) / fc <= max_slots) {
         int64_t slots = 0;
         plan->fseq = plan->seq;
         for (int b = 0; b < s->batch; ++b) {
@@ -525,6 +536,12 @@ int verify_call(const ssl_shape* shape, const ssl_params* params, const int32_t*
     a.page_size = page_size;
     a.max_blocks = max_blocks;
     a.per_head = params->per_head;
+    for (int b = 0; b < shape->batch; ++b) {   // one block: every sequence, all its rows
+        a.sid[b] = b;
+        a.qoff[b] = 0;
+        a.qfull[b] = q_len_host[b];
+    }
+    a.score_add = 0;
     if (params->per_head && !use_one_sweep(plan, params)) {
         // two sweeps sum a head's rows across the 16 lanes of a row tile
         const int g = a.group;
@@ -551,9 +568,44 @@ int verify_call(const ssl_shape* shape, const ssl_params* params, const int32_t*
                    ? SSL_OK
                    : SSL_ERR_HIP;
     }
-    return launch_verify(a, plan.n_items, plan.n_rows, plan.row_tiles, stream) == hipSuccess
-               ? SSL_OK
-               : SSL_ERR_HIP;
+    if (plan.block_pos >= shape->max_q)
+        return launch_verify(a, plan.n_items, plan.n_rows, plan.row_tiles, stream) == hipSuccess
+                   ? SSL_OK
+                   : SSL_ERR_HIP;
+    // Row blocks, the last positions of every sequence first (that block has
+    // all sequences, so it writes every score; later blocks add theirs).  A
+    // block's table holds only the sequences that still have positions.
+    int max_q = 0;
+    for (int b = 0; b < shape->batch; ++b) max_q = std::max(max_q, q_len_host[b]);
+    const int P = plan.block_pos, g = a.group;
+    for (int k = 0; k * P < max_q; ++k) {
+        VerifyArgs blk = a;
+        memset(&blk.seq, 0, sizeof blk.seq);
+        int n = 0;
+        int64_t items = 0, rows = 0;
+        for (int b = 0; b < shape->batch; ++b) {
+            const int j_end = q_len_host[b] - k * P;
+            if (j_end <= 0) continue;
+            const int j0 = std::max(0, j_end - P);
+            blk.seq.item_start[n] = (int32_t)items;
+            blk.seq.row_start[n] = (int32_t)rows;
+            blk.seq.ctx[n] = ctx_len_host[b];
+            blk.seq.qlen[n] = j_end - j0;
+            blk.sid[n] = b;
+            blk.qoff[n] = j0;
+            blk.qfull[n] = q_len_host[b];
+            items += (int64_t)shape->n_kv_heads * ((ctx_len_host[b] + plan.chunk - 1) / plan.chunk);
+            rows += (int64_t)shape->n_kv_heads * (j_end - j0) * g;
+            ++n;
+        }
+        blk.seq.n_seq = n;
+        blk.seq.item_start[n] = (int32_t)items;
+        blk.seq.row_start[n] = (int32_t)rows;
+        blk.score_add = k > 0 ? 1 : 0;
+        if (launch_verify(blk, (int)items, (int)rows, plan.row_tiles, stream) != hipSuccess)
+            return SSL_ERR_HIP;
+    }
+    return SSL_OK;
 }
 
 }  // namespace

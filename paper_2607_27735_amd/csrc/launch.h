@@ -77,6 +77,16 @@ struct VerifyArgs {
     // 1: scores per query head, [batch][n_q][max_ctx] (Eq. 3 for each head of
     // the group on its own); 0: per KV head, summed over the group.
     int32_t per_head;
+    // Row blocks (a KV head with more verify rows than one launch holds runs
+    // one launch per block of positions).  Per entry of seq: the sequence it
+    // is (sid), the first of its verify positions in this block (qoff; the
+    // block's count is seq.qlen) and its verify positions in all (qfull), so
+    // that causal limits and the Eq. 3 window are those of the whole call.
+    // One block: sid = b, qoff = 0, qfull = qlen.
+    int32_t sid[kTableBatch];
+    int32_t qoff[kTableBatch];
+    int32_t qfull[kTableBatch];
+    int32_t score_add;   // 1: add this block's scores to those already written
 };
 
 // Select splits each (sequence, KV head) unit into partitions of `part`

@@ -64,11 +64,11 @@ __device__ __forceinline__ void stats_tile(const VerifyArgs& a, const Rows<NRT>&
 
 template <int NRT, bool kPaged>
 __global__ __launch_bounds__(kThreads) void verify_stats_kernel(VerifyArgs a) {
-    const Item it = decode_item(a.seq, blockIdx.x, a.n_kv_heads, a.chunk);
+    const Item it = decode_item(a, a.seq, blockIdx.x, a.chunk);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int m16 = lane & 15, G = lane >> 4;
     Rows<NRT> r;
-    load_rows<NRT>(a, it.b, it.c, it.T, it.nq, m16, G, r);
+    load_rows<NRT>(a, it.b, it.c, it.T, it.nq, it.qoff, it.qfull, m16, G, r);
     const uint16_t* kbase = a.k + (size_t)it.unit * a.max_ctx * kHeadDim;
 
     float M[NRT], L[NRT];
@@ -153,7 +153,7 @@ __device__ __forceinline__ void main_tile(const VerifyArgs& a, const Rows<NRT>& 
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const int key = key0 + 16 * (e >> 2) + G + 4 * (e & 3);
-                if (key < key_end) hrow[key] = hs[e];
+                if (key < key_end) hrow[key] = a.score_add ? hrow[key] + hs[e] : hs[e];
             }
         }
     } else {
@@ -173,7 +173,7 @@ __device__ __forceinline__ void main_tile(const VerifyArgs& a, const Rows<NRT>& 
 #pragma unroll
         for (int e = 1; e < 8; ++e) val = (m16 == e) ? sp[e] : val;
         const int key = key0 + 16 * (m16 >> 2) + G + 4 * (m16 & 3);
-        if (key < key_end) srow[key] = val;
+        if (key < key_end) srow[key] = a.score_add ? srow[key] + val : val;
     }
     }
 
@@ -201,12 +201,12 @@ __device__ __forceinline__ void main_tile(const VerifyArgs& a, const Rows<NRT>& 
 
 template <int NRT, bool kPaged, bool kPerHead>
 __global__ __launch_bounds__(kThreads) void verify_main_kernel(VerifyArgs a) {
-    const Item it = decode_item(a.seq, blockIdx.x, a.n_kv_heads, a.chunk);
+    const Item it = decode_item(a, a.seq, blockIdx.x, a.chunk);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int m16 = lane & 15, G = lane >> 4;
 
     Rows<NRT> r;
-    load_rows<NRT>(a, it.b, it.c, it.T, it.nq, m16, G, r);
+    load_rows<NRT>(a, it.b, it.c, it.T, it.nq, it.qoff, it.qfull, m16, G, r);
     const size_t cache_off = (size_t)it.unit * a.max_ctx * kHeadDim;
     const uint16_t* kbase = a.k + cache_off;
     const uint16_t* vbase = a.v + cache_off;
@@ -314,14 +314,15 @@ constexpr int kCombineGroups = kCombineThreads / 32;
 __global__ __launch_bounds__(kCombineThreads) void verify_combine_kernel(VerifyArgs a) {
     const SeqTable& st = a.seq;
     const int gr = blockIdx.x;
-    int b = 0;
-    while (b + 1 < st.n_seq && gr >= st.row_start[b + 1]) ++b;
-    const int R = st.qlen[b] * a.group;
-    const int local = gr - st.row_start[b];
+    int bt = 0;
+    while (bt + 1 < st.n_seq && gr >= st.row_start[bt + 1]) ++bt;
+    const int b = a.sid[bt];
+    const int R = st.qlen[bt] * a.group;
+    const int local = gr - st.row_start[bt];
     const int c = local / R;
     const int row = local - c * R;
-    const int nchunk = (st.ctx[b] + a.chunk - 1) / a.chunk;
-    const int item0 = st.item_start[b] + c * nchunk;
+    const int nchunk = (st.ctx[bt] + a.chunk - 1) / a.chunk;
+    const int item0 = st.item_start[bt] + c * nchunk;
     const int d4 = threadIdx.x & 31, sg = threadIdx.x >> 5;
     const f32x4* po = reinterpret_cast<const f32x4*>(a.part_o);
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -343,8 +344,9 @@ __global__ __launch_bounds__(kCombineThreads) void verify_combine_kernel(VerifyA
     f32x4 o = red[0][d4];
 #pragma unroll
     for (int gq = 1; gq < kCombineGroups; ++gq) o += red[gq][d4];
-    const int j = row / a.group;
-    const int h = c * a.group + (row - j * a.group);
+    const int jl = row / a.group;
+    const int h = c * a.group + (row - jl * a.group);
+    const int j = a.qoff[bt] + jl;
     const size_t base = (((size_t)b * a.max_q + j) * a.n_q_heads + h) * kHeadDim + 4 * d4;
     if (a.out_fp32) {
         *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out) + base) = o;

@@ -27,20 +27,22 @@ struct Rows {
     u32x4 q[NRT][4];    // B operand (Q^T): row's head-dim slice per 32-wide k-block
 };
 
+// Row rt*16 + m16 of a launch is verify position qoff + row / group of the
+// sequence (of its qfull positions) and query head c*group + row % group.
 template <int NRT>
-__device__ __forceinline__ void load_rows(const VerifyArgs& a, int b, int c, int T, int nq, int m16,
-                                          int G, Rows<NRT>& r) {
+__device__ __forceinline__ void load_rows(const VerifyArgs& a, int b, int c, int T, int nq, int qoff,
+                                          int qfull, int m16, int G, Rows<NRT>& r) {
     const int g = a.group;
     const int R = nq * g;
-    const int wn = min(a.window, nq);
+    const int wn = min(a.window, qfull);
 #pragma unroll
     for (int rt = 0; rt < NRT; ++rt) {
         const int row = rt * 16 + m16;
         if (row < R) {
-            const int j = row / g;
-            const int hh = row - j * g;
-            r.plim[rt] = T - nq + j;
-            r.inwin[rt] = j >= nq - wn;
+            const int j = qoff + row / g;
+            const int hh = row - (j - qoff) * g;
+            r.plim[rt] = T - qfull + j;
+            r.inwin[rt] = j >= qfull - wn;
             const uint16_t* qp =
                 a.q + (((size_t)b * a.max_q + j) * a.n_q_heads + c * g + hh) * kHeadDim + 8 * G;
 #pragma unroll
@@ -188,26 +190,33 @@ struct KVTile {
 };
 
 // A work item: (sequence b, KV head c, key chunk s) of a launch whose items
-// are numbered sequence by sequence, head by head, chunk by chunk.
+// are numbered sequence by sequence, head by head, chunk by chunk.  bt is the
+// sequence's entry in the launch's tables, b the sequence itself (a.sid[bt]).
 struct Item {
-    int b, c, s, nchunk, T, nq, key_begin, key_end, unit, item0;
+    int b, bt, c, s, nchunk, T, nq, qoff, qfull, key_begin, key_end, unit, item0;
 };
 
-__device__ __forceinline__ Item decode_item(const SeqTable& st, int item, int n_kv, int chunk) {
+__device__ __forceinline__ Item decode_item(const VerifyArgs& a, const SeqTable& st, int item,
+                                            int chunk) {
+    const int n_kv = a.n_kv_heads;
     Item it;
-    int b = 0;
-    while (b + 1 < st.n_seq && item >= st.item_start[b + 1]) ++b;
+    int bt = 0;
+    while (bt + 1 < st.n_seq && item >= st.item_start[bt + 1]) ++bt;
+    const int b = a.sid[bt];
     it.b = b;
-    it.T = st.ctx[b];
-    it.nq = st.qlen[b];
+    it.bt = bt;
+    it.T = st.ctx[bt];
+    it.nq = st.qlen[bt];
+    it.qoff = a.qoff[bt];
+    it.qfull = a.qfull[bt];
     it.nchunk = (it.T + chunk - 1) / chunk;
-    const int local = item - st.item_start[b];
+    const int local = item - st.item_start[bt];
     it.c = local / it.nchunk;
     it.s = local - it.c * it.nchunk;
     it.key_begin = it.s * chunk;
     it.key_end = min(it.key_begin + chunk, it.T);
     it.unit = b * n_kv + it.c;
-    it.item0 = st.item_start[b] + it.c * it.nchunk;
+    it.item0 = st.item_start[bt] + it.c * it.nchunk;
     return it;
 }
 

@@ -171,7 +171,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     __shared__ int wait_failed;
 
     const int slot = blockIdx.x;
-    const Item it = decode_item(a.seq, slot, a.n_kv_heads, a.chunk);
+    const Item it = decode_item(a, a.seq, slot, a.chunk);
     const int unit = it.unit, b = it.b, c = it.c;
     const int slot0 = it.item0, nchunk = it.nchunk;
     const int T = it.T, nq = it.nq;
@@ -185,7 +185,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     const int m16 = lane & 15, G = lane >> 4;
 
     Rows<NRT> r;
-    load_rows<NRT>(a, b, c, T, nq, m16, G, r);
+    load_rows<NRT>(a, b, c, T, nq, it.qoff, it.qfull, m16, G, r);
     const size_t cache_off = (size_t)unit * a.max_ctx * kHeadDim;
     const uint16_t* kbase = a.k + cache_off;
     const uint16_t* vbase = a.v + cache_off;

@@ -87,7 +87,13 @@ def test_verify_validation(lib):
     assert _verify(lib, ctx=(4097,)) == B.SSL_ERR_SHAPE                 # ctx_len > max_ctx
     assert _verify(lib, ql=(9,)) == B.SSL_ERR_SHAPE                     # q_len > max_q
     assert _verify(lib, shape=_shape(max_q=65)) == B.SSL_ERR_SHAPE
-    assert _verify(lib, shape=_shape(n_q_heads=64, max_q=16), ql=(9,)) == B.SSL_ERR_UNSUPPORTED
+    # more than 64 rows per KV head: row blocks, two sweeps only
+    assert _verify(lib, shape=_shape(n_q_heads=64, max_q=16), ql=(9,),
+                   params=_params(verify_mode=2)) == B.SSL_ERR_UNSUPPORTED
+    assert B.verify_plan(_shape(n_q_heads=64, max_q=16), _params(), [4000], [16])[0] == \
+        B.VERIFY_TWO_SWEEP
+    assert _verify(lib, shape=_shape(n_q_heads=128, n_kv_heads=1), ql=(1,)) == \
+        B.SSL_ERR_UNSUPPORTED                                        # group > 64
     assert _verify(lib, params=_params(window=0)) == B.SSL_ERR_SHAPE
     assert _verify(lib, params=_params(sm_scale=0.0)) == B.SSL_ERR_SHAPE
     assert _verify(lib, params=_params(sm_scale=float("nan"))) == B.SSL_ERR_SHAPE

@@ -67,7 +67,21 @@ SMALL = {
     "prefill-seed-g4": lambda: _poison_padding(generate(
         110, name="prefill-seed-g4", batch=2, n_q_heads=32, n_kv_heads=8, ctx_len=[4096, 1500],
         q_len=[16, 16], max_ctx=4100, budget=256, heavy_hitters=4)),
+    # the same at the 70B shape (group 8): 128 rows per KV head, two row blocks
+    "prefill-seed-g8": lambda: _poison_padding(generate(
+        111, name="prefill-seed-g8", batch=2, n_q_heads=64, n_kv_heads=8, ctx_len=[4096, 1500],
+        q_len=[16, 16], max_ctx=4100, budget=256, heavy_hitters=4)),
+    # row blocks over a ragged batch (blocks of 8 positions: the second block
+    # has no rows of the second sequence) with the window ending inside a block
+    "rowblocks-ragged": lambda: _poison_padding(generate(
+        112, name="rowblocks-ragged", batch=3, n_q_heads=16, n_kv_heads=2, ctx_len=[3000, 700, 2049],
+        q_len=[20, 3, 11], max_ctx=3010, max_q=20, window=12, budget=200)),
 }
+
+
+def _row_blocks(w):
+    """Whether a KV head has more verify rows than one launch holds (64)."""
+    return int(max(w.q_len)) * (w.n_q_heads // w.n_kv_heads) > 64
 
 
 @functools.lru_cache(maxsize=None)
@@ -92,6 +106,11 @@ def test_verify_matches_oracle(name, mode):
     w, out_ref, s_ref, oabs_ref = small_case(name)
     print(f"[verify {mode}] {w.describe()}", flush=True)
     d = Dev(w)
+    if _row_blocks(w) and mode == "one-sweep":
+        with pytest.raises(B.SSLError) as e:      # row blocks take two sweeps
+            gpu_verify(d, out_fp32=True, mode=MODES[mode])
+        assert e.value.status == B.SSL_ERR_UNSUPPORTED
+        return
     out, s = gpu_verify(d, out_fp32=True, mode=MODES[mode])
     mask = _row_mask(w)
     err = check_outputs(out, out_ref, oabs_ref, mask)
