@@ -54,6 +54,8 @@ def _bind(lib):
     lib.oracle_draft_step.argtypes = [ctypes.c_int] * 8 + [_i32p, _i32p, _u16p, _u16p, _u16p,
                                                            _i32p, ctypes.c_double, _f64p]
     lib.oracle_draft_step.restype = ctypes.c_int
+    lib.oracle_draft_step_heads.argtypes = lib.oracle_draft_step.argtypes
+    lib.oracle_draft_step_heads.restype = ctypes.c_int
     _f32p = ctypes.POINTER(ctypes.c_float)
     lib.oracle_row_stats.argtypes = [ctypes.c_int] * 3 + [_u16p, _f32p, _f64p, _i32p]
     lib.oracle_row_stats.restype = ctypes.c_int
@@ -180,10 +182,11 @@ def draft(w, idx: np.ndarray, n_idx: np.ndarray, *, q_draft=None, k=None, v=None
 
 
 def draft_step(w, idx: np.ndarray, base_len, cur_len, *, q_draft=None, k=None, v=None,
-               k_sink=None, k_recent=None, lib=None):
+               k_sink=None, k_recent=None, per_head=False, lib=None):
     """One draft-round step: attention over the fixed sink/TopK part of the
     index set built at ``base_len`` plus the recent window slid to end at
-    ``cur_len``; float64 ``[batch][Hq][d]``.  The budget is ``idx.shape[-1]``."""
+    ``cur_len``; float64 ``[batch][Hq][d]``.  The budget is ``idx.shape[-1]``.
+    ``per_head``: idx holds one set per query head ``[batch][Hq][budget]``."""
     lib = lib or load()
     qd = _c(w.q_draft if q_draft is None else q_draft, np.uint16)
     k = _c(w.k if k is None else k, np.uint16)
@@ -195,10 +198,11 @@ def draft_step(w, idx: np.ndarray, base_len, cur_len, *, q_draft=None, k=None, v
     kr = int(w.k_recent if k_recent is None else k_recent)
     B = idx.shape[-1]
     out = np.zeros((w.batch, w.n_q_heads, w.head_dim), dtype=np.float64)
-    rc = lib.oracle_draft_step(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.max_ctx, B,
-                               ks, kr, _p(base, _i32p), _p(cur, _i32p), _p(qd, _u16p),
-                               _p(k, _u16p), _p(v, _u16p), _p(idx, _i32p), float(w.sm_scale),
-                               _p(out, _f64p))
+    fn = lib.oracle_draft_step_heads if per_head else lib.oracle_draft_step
+    rc = fn(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.max_ctx, B,
+            ks, kr, _p(base, _i32p), _p(cur, _i32p), _p(qd, _u16p),
+            _p(k, _u16p), _p(v, _u16p), _p(idx, _i32p), float(w.sm_scale),
+            _p(out, _f64p))
     if rc != 0:
         raise ValueError("oracle_draft_step rejected its arguments")
     return out

@@ -297,10 +297,11 @@ int oracle_draft(int batch, int n_q_heads, int n_kv_heads, int head_dim, int max
  * over t in F u W:  out[b,h] = sum_t softmax(x)_t v[b,c,t].
  * Layouts as oracle_draft.  Returns 0 or -1.
  */
-int oracle_draft_step(int batch, int n_q_heads, int n_kv_heads, int head_dim, int max_ctx,
-                      int budget, int k_sink, int k_recent, const int32_t *base_len,
-                      const int32_t *cur_len, const uint16_t *q_draft, const uint16_t *k,
-                      const uint16_t *v, const int32_t *idx, double sm_scale, double *out)
+static int draft_step_sets(int per_head, int batch, int n_q_heads, int n_kv_heads, int head_dim,
+                           int max_ctx, int budget, int k_sink, int k_recent,
+                           const int32_t *base_len, const int32_t *cur_len,
+                           const uint16_t *q_draft, const uint16_t *k, const uint16_t *v,
+                           const int32_t *idx, double sm_scale, double *out)
 {
     if (batch < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads != 0 || head_dim < 1)
         return -1;
@@ -320,7 +321,9 @@ int oracle_draft_step(int batch, int n_q_heads, int n_kv_heads, int head_dim, in
         const int s_end = k_sink < T ? k_sink : T;
         const int r_T = (T - k_recent) > s_end ? (T - k_recent) : s_end;
         const int w0 = (cur - k_recent) > r_T ? (cur - k_recent) : r_T;
-        const int32_t *I = idx + ((size_t)b * n_kv_heads + c) * budget;
+        /* the index set of head h: its own (per_head), else its KV head's */
+        const int32_t *I = per_head ? idx + ((size_t)b * n_q_heads + h) * budget
+                                    : idx + ((size_t)b * n_kv_heads + c) * budget;
         /* the step's positions: F, then W */
         int *S = (int *)malloc(sizeof(int) * (size_t)(n + k_recent + 1));
         int m_S = 0;
@@ -354,6 +357,31 @@ int oracle_draft_step(int batch, int n_q_heads, int n_kv_heads, int head_dim, in
         free(S);
     }
     return 0;
+}
+
+int oracle_draft_step(int batch, int n_q_heads, int n_kv_heads, int head_dim, int max_ctx,
+                      int budget, int k_sink, int k_recent, const int32_t *base_len,
+                      const int32_t *cur_len, const uint16_t *q_draft, const uint16_t *k,
+                      const uint16_t *v, const int32_t *idx, double sm_scale, double *out)
+{
+    return draft_step_sets(0, batch, n_q_heads, n_kv_heads, head_dim, max_ctx, budget, k_sink,
+                           k_recent, base_len, cur_len, q_draft, k, v, idx, sm_scale, out);
+}
+
+/*
+ * The same step with one index set per query head (Sec. 3.2 keeps importance
+ * for every attention head): idx is [batch][Hq][budget], the set of head h
+ * built at base_len by select over that head's scores; head h attends over the
+ * fixed part of its own set and the shared slid window, with the rows of its
+ * KV head h / (Hq/Hkv).
+ */
+int oracle_draft_step_heads(int batch, int n_q_heads, int n_kv_heads, int head_dim, int max_ctx,
+                            int budget, int k_sink, int k_recent, const int32_t *base_len,
+                            const int32_t *cur_len, const uint16_t *q_draft, const uint16_t *k,
+                            const uint16_t *v, const int32_t *idx, double sm_scale, double *out)
+{
+    return draft_step_sets(1, batch, n_q_heads, n_kv_heads, head_dim, max_ctx, budget, k_sink,
+                           k_recent, base_len, cur_len, q_draft, k, v, idx, sm_scale, out);
 }
 
 /* ---------------------------------------------------------------------------

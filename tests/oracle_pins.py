@@ -442,6 +442,46 @@ def pin_draft_step_value_one(lib):
         assert np.abs(o - 1.0).max() < 1e-12
 
 
+def pin_draft_step_heads(lib):
+    """The draft-round step with one index set per query head: (1) when every
+    head of a group carries its KV head's set it is the per-KV-head step;
+    (2) before any drafted token it is the per-head Eq. 5 draft over those
+    sets; (3) hand-worked sets: with K = 0 and one-hot V rows each head's output
+    is uniform exactly on its own fixed rows plus the shared slid window."""
+    rng = np.random.default_rng(94)
+    w = _tiny(95, hq=8, hkv=2, ctx=(64, 64), ql=(1, 1), B=20, k_sink=2, k_recent=5)
+    base = np.array([50, 17], dtype=np.int32)
+    idx_kv, _ = oracle.select(w, rng.random((2, 2, 64)), ctx_len=base, lib=lib)
+    shared = np.repeat(idx_kv, 4, axis=1)                        # [2][8][B]
+    for i in range(6):
+        a = oracle.draft_step(w, shared, base, base + i, per_head=True, lib=lib)
+        b = oracle.draft_step(w, idx_kv, base, base + i, lib=lib)
+        assert np.abs(a - b).max() < 1e-15
+    # per-head sets from per-head scores (a select over the query heads as units)
+    wh = _tiny(95, hq=8, hkv=8, ctx=(64, 64), ql=(1, 1), B=20, k_sink=2, k_recent=5)
+    idx_h, n_h = oracle.select(wh, rng.random((2, 8, 64)), ctx_len=base, lib=lib)
+    assert len(set(map(tuple, idx_h[0, :, :n_h[0]].tolist()))) > 1      # the sets differ
+    first = oracle.draft_step(w, idx_h, base, base, per_head=True, lib=lib)
+    assert np.abs(first - oracle.draft_heads(w, idx_h, n_h, lib=lib)).max() < 1e-15
+    # hand-worked: T = 20, sink 2, recent 4, budget 8 (K_mid 2); head 0 keeps
+    # {5, 9}, head 1 {7, 13}; after i drafted tokens the window is [16+i, 20+i)
+    w2 = _tiny(96, hq=2, hkv=1, ctx=(24,), ql=(1,), B=8, k_sink=2, k_recent=4)
+    idx2 = np.array([[[0, 1, 5, 9, 16, 17, 18, 19], [0, 1, 7, 13, 16, 17, 18, 19]]],
+                    dtype=np.int32)
+    k0 = np.zeros_like(w2.k)
+    v1 = np.zeros_like(w2.v)
+    one = f32_to_bf16_bits(np.float32(1.0))
+    for t in range(24):
+        v1[:, :, t, t] = one
+    for i in (0, 1, 4):
+        out = oracle.draft_step(w2, idx2, [20], [20 + i], k=k0, v=v1, per_head=True, lib=lib)
+        for h, fixed in ((0, [0, 1, 5, 9]), (1, [0, 1, 7, 13])):
+            S = fixed + list(range(16 + i, 20 + i))
+            want = np.zeros(128)
+            want[S] = 1.0 / len(S)
+            assert np.abs(out[0, h] - want).max() < 1e-15, (h, i)
+
+
 # ---------------------------------------------------------------------------
 # per-query-head scores and draft (Eq. 3 / Eq. 5 per attention head)
 # ---------------------------------------------------------------------------
@@ -678,7 +718,7 @@ ALL_PINS = [pin_verify_matches_sdpa, pin_verify_value_one, pin_verify_zero_keys_
             pin_scores_permutation, pin_select_lexsort, pin_select_bruteforce_subsets,
             pin_select_special_cases, pin_draft_matches_sdpa, pin_draft_full_equals_dense,
             pin_draft_permutation, pin_draft_step_first_matches_sdpa,
-            pin_draft_step_worked_example, pin_draft_step_value_one, pin_row_stats_library,
+            pin_draft_step_worked_example, pin_draft_step_value_one, pin_draft_step_heads, pin_row_stats_library,
             pin_row_stats_closed_forms, pin_greedy_accept_worked, pin_head_scores_match_softmax,
             pin_draft_heads,
             pin_controller_closed_forms, pin_controller_observe, pin_controller_argmax]

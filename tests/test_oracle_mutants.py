@@ -48,6 +48,10 @@ MUTANTS = [
      "for (int t = w0; t < cur - 1; ++t) S[m_S++] = t;"),
     ("step_fixed_part_from_cur", "const int r_T = (T - k_recent) > s_end ? (T - k_recent) : s_end;",
      "const int r_T = (cur - k_recent) > s_end ? (cur - k_recent) : s_end;"),
+    ("step_heads_use_group_set", "const int32_t *I = per_head ? idx + ((size_t)b * n_q_heads + h) * budget",
+     "const int32_t *I = per_head ? idx + ((size_t)b * n_q_heads + c * g) * budget"),
+    ("step_heads_ignore_own_set", "const int32_t *I = per_head ? idx",
+     "const int32_t *I = 0 ? idx"),
     ("entropy_log2", "const double lp = x[i] - m - log(Z);      /* ln p_i */",
      "const double lp = (x[i] - m - log(Z)) / log(2.0);"),
     ("entropy_unnormalized", "const double lp = x[i] - m - log(Z);      /* ln p_i */",
