@@ -128,8 +128,11 @@ typedef struct {
                           *    (scores, idx [batch][Hq][...]), and draft gives each query
                           *    head its own set idx[b][h] over the rows of KV head h / group.
                           *    Two-sweep verify needs the group to be 1, 2, 4, 8 or 16
-                          *    (SSL_ERR_UNSUPPORTED otherwise); the draft-round calls do not
-                          *    take it (SSL_ERR_UNSUPPORTED).  Other values: SSL_ERR_SHAPE. */
+                          *    (SSL_ERR_UNSUPPORTED otherwise); the draft-round calls take
+                          *    idx [batch][Hq][budget] and k_sel / v_sel
+                          *    [batch][Hq][budget][128], each query head attending over the
+                          *    fixed rows of its own set and the shared slid window.  Other
+                          *    values: SSL_ERR_SHAPE. */
 } ssl_params;
 
 /* How ssl_verify_attn schedules its work (results agree to rounding):

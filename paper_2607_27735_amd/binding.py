@@ -477,9 +477,11 @@ def draft_attn_paged(q_draft: torch.Tensor, k_pages: torch.Tensor, v_pages: torc
 
 def draft_materialize(k: torch.Tensor, v: torch.Tensor, idx: torch.Tensor, ctx_len_host,
                       params: Params, k_sel: Optional[torch.Tensor] = None,
-                      v_sel: Optional[torch.Tensor] = None, stream=None):
+                      v_sel: Optional[torch.Tensor] = None, stream=None,
+                      n_q_heads: Optional[int] = None):
     """Copy the sink and TopK rows of the index sets built at ``ctx_len_host``
-    to ``k_sel`` / ``v_sel`` [B, Hkv, budget, 128] bf16 (allocated if None);
+    to ``k_sel`` / ``v_sel`` [B, units, budget, 128] bf16 (allocated if None;
+    units = Hkv, or Hq with ``params.per_head``, which needs ``n_q_heads``);
     returns them."""
     _need_gpu(k, v, idx)
     if k.dtype != torch.bfloat16 or v.dtype != torch.bfloat16:
@@ -487,16 +489,18 @@ def draft_materialize(k: torch.Tensor, v: torch.Tensor, idx: torch.Tensor, ctx_l
     if idx.dtype != torch.int32:
         raise TypeError("idx must be int32")
     batch, hkv, max_ctx, d = k.shape
-    if idx.shape != (batch, hkv, params.budget):
-        raise ValueError("idx must be [batch, n_kv_heads, budget]")
-    shape = Shape(batch, hkv, hkv, d, max_ctx, 1)
-    sel_shape = (batch, hkv, params.budget, d)
+    hq = hkv if n_q_heads is None else int(n_q_heads)
+    units = hq if params.per_head else hkv
+    if idx.shape != (batch, units, params.budget):
+        raise ValueError("idx must be [batch, units, budget]")
+    shape = Shape(batch, hq, hkv, d, max_ctx, 1)
+    sel_shape = (batch, units, params.budget, d)
     if k_sel is None:
         k_sel = torch.empty(sel_shape, dtype=torch.bfloat16, device=k.device)
     if v_sel is None:
         v_sel = torch.empty(sel_shape, dtype=torch.bfloat16, device=k.device)
     if tuple(k_sel.shape) != sel_shape or tuple(v_sel.shape) != sel_shape:
-        raise ValueError("k_sel / v_sel must be [batch, n_kv_heads, budget, 128]")
+        raise ValueError("k_sel / v_sel must be [batch, units, budget, 128]")
     _need_gpu(k_sel, v_sel)
     ctx = _host_i32(ctx_len_host)
     _check(load().ssl_draft_materialize(ctypes.byref(shape), ctypes.byref(params),
@@ -528,18 +532,19 @@ def draft_step(q_draft: torch.Tensor, k: torch.Tensor, v: torch.Tensor, ctx_len_
         raise TypeError("q_draft, k, v must be bfloat16")
     batch, hq, d = q_draft.shape
     _, hkv, max_ctx, _ = k.shape
+    units = hq if params.per_head else hkv
     if k_sel is not None or v_sel is not None:
         if k_sel is None or v_sel is None:
             raise ValueError("give both k_sel and v_sel, or neither")
         _need_gpu(k_sel, v_sel)
-        if tuple(k_sel.shape) != (batch, hkv, params.budget, d) or k_sel.shape != v_sel.shape:
-            raise ValueError("k_sel / v_sel must be [batch, n_kv_heads, budget, 128]")
+        if tuple(k_sel.shape) != (batch, units, params.budget, d) or k_sel.shape != v_sel.shape:
+            raise ValueError("k_sel / v_sel must be [batch, units, budget, 128]")
     else:
         if idx is None:
             raise ValueError("idx is needed when no materialized rows are given")
         _need_gpu(idx)
-        if idx.shape != (batch, hkv, params.budget) or idx.dtype != torch.int32:
-            raise ValueError("idx must be int32 [batch, n_kv_heads, budget]")
+        if idx.shape != (batch, units, params.budget) or idx.dtype != torch.int32:
+            raise ValueError("idx must be int32 [batch, units, budget]")
     shape = Shape(batch, hq, hkv, d, max_ctx, 1)
     ctx, cur = _host_i32(ctx_len_host), _host_i32(cur_len_host)
     odt = torch.float32 if params.out_fp32 else torch.bfloat16

@@ -815,10 +815,13 @@ int ssl_draft_attn_paged(const ssl_shape* shape, const ssl_params* params,
 int ssl_draft_materialize(const ssl_shape* shape, const ssl_params* params,
                           const int32_t* ctx_len_host, const void* k_cache, const void* v_cache,
                           const int32_t* idx, void* k_sel, void* v_sel, hipStream_t stream) {
-    StepPlan plan;
-    int rc = plan_draft_step(shape, params, ctx_len_host, ctx_len_host, &plan);
+    if (!shape || !params) return SSL_ERR_NULL;
+    int rc = check_budget(params);
     if (rc) return rc;
-    if (params->per_head) return SSL_ERR_UNSUPPORTED;
+    const ssl_shape us = unit_shape(shape, params);   // per_head: one unit per query head
+    StepPlan plan;
+    rc = plan_draft_step(&us, params, ctx_len_host, ctx_len_host, &plan);
+    if (rc) return rc;
     if (!k_cache || !v_cache || !idx || !k_sel || !v_sel) return SSL_ERR_NULL;
     if (!aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(k_sel, 16) ||
         !aligned(v_sel, 16) || !aligned(idx, 4))
@@ -829,13 +832,13 @@ int ssl_draft_materialize(const ssl_shape* shape, const ssl_params* params,
     a.idx = idx;
     a.k_sel = static_cast<uint16_t*>(k_sel);
     a.v_sel = static_cast<uint16_t*>(v_sel);
-    a.n_kv_heads = shape->n_kv_heads;
-    a.kv_div = 1;
+    a.n_kv_heads = us.n_kv_heads;
+    a.kv_div = shape->n_kv_heads == us.n_kv_heads ? 1 : shape->n_q_heads / shape->n_kv_heads;
     a.n_kv_real = shape->n_kv_heads;
     a.max_ctx = shape->max_ctx;
     a.budget = params->budget;
     for (int b = 0; b < shape->batch; ++b) a.n_fixed[b] = plan.n_fixed[b];
-    return launch_draft_materialize(a, plan.max_fixed, shape->batch * shape->n_kv_heads,
+    return launch_draft_materialize(a, plan.max_fixed, shape->batch * us.n_kv_heads,
                                     stream) == hipSuccess
                ? SSL_OK
                : SSL_ERR_HIP;
@@ -844,9 +847,12 @@ int ssl_draft_materialize(const ssl_shape* shape, const ssl_params* params,
 int ssl_draft_step_workspace(const ssl_shape* shape, const ssl_params* params,
                              const int32_t* ctx_len_host, const int32_t* cur_len_host,
                              size_t* bytes_out) {
-    if (!bytes_out) return SSL_ERR_NULL;
+    if (!bytes_out || !shape || !params) return SSL_ERR_NULL;
+    int rc = check_budget(params);
+    if (rc) return rc;
+    const ssl_shape us = unit_shape(shape, params);
     StepPlan plan;
-    const int rc = plan_draft_step(shape, params, ctx_len_host, cur_len_host, &plan);
+    rc = plan_draft_step(&us, params, ctx_len_host, cur_len_host, &plan);
     if (rc) return rc;
     *bytes_out = plan.d.bytes;
     return SSL_OK;
@@ -856,10 +862,13 @@ int ssl_draft_step(const ssl_shape* shape, const ssl_params* params, const int32
                    const int32_t* cur_len_host, const void* q_draft, const void* k_cache,
                    const void* v_cache, const int32_t* idx, const void* k_sel, const void* v_sel,
                    void* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
-    StepPlan plan;
-    int rc = plan_draft_step(shape, params, ctx_len_host, cur_len_host, &plan);
+    if (!shape || !params) return SSL_ERR_NULL;
+    int rc = check_budget(params);
     if (rc) return rc;
-    if (params->per_head) return SSL_ERR_UNSUPPORTED;
+    const ssl_shape us = unit_shape(shape, params);   // per_head: one unit per query head
+    StepPlan plan;
+    rc = plan_draft_step(&us, params, ctx_len_host, cur_len_host, &plan);
+    if (rc) return rc;
     if (!(params->sm_scale > 0.f) || !isfinite(params->sm_scale)) return SSL_ERR_SHAPE;
     const bool sel = k_sel || v_sel;
     if (!q_draft || !k_cache || !v_cache || !out) return SSL_ERR_NULL;
@@ -887,9 +896,9 @@ int ssl_draft_step(const ssl_shape* shape, const ssl_params* params, const int32
     a.call_tag = next_call_tag();
     a.out = out;
     a.n_q_heads = shape->n_q_heads;
-    a.n_kv_heads = shape->n_kv_heads;
-    a.group = shape->n_q_heads / shape->n_kv_heads;
-    a.kv_div = 1;
+    a.n_kv_heads = us.n_kv_heads;
+    a.group = us.n_q_heads / us.n_kv_heads;
+    a.kv_div = shape->n_kv_heads == us.n_kv_heads ? 1 : shape->n_q_heads / shape->n_kv_heads;
     a.n_kv_real = shape->n_kv_heads;
     a.max_ctx = shape->max_ctx;
     a.budget = params->budget;

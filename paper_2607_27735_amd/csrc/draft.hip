@@ -397,15 +397,17 @@ __global__ __launch_bounds__(kDraftThreads, 2) void draft_kernel(DraftArgs a) {
 
 // Materialization for a draft round: workgroup (x, u) copies rows
 // 32x .. 32x + 31 of unit u's sink and TopK entries (the first n_fixed[b]
-// entries of its index list) from the cache to k_sel/v_sel.  Thread t moves
-// 16 bytes of two rows of K and of V, all four loads in flight together.
+// entries of its index list) from the cache to k_sel/v_sel (a unit per query
+// head reads the rows of its KV head).  Thread t moves 16 bytes of two rows
+// of K and of V, all four loads in flight together.
 constexpr int kMatRows = 32;
 __global__ __launch_bounds__(kDraftThreads) void draft_materialize_kernel(DraftArgs a) {
     const int u = blockIdx.y, b = u / a.n_kv_heads;
     const int nf = a.n_fixed[b];
     const int q = threadIdx.x & 15, r = threadIdx.x >> 4;   // 16 rows per pass
     const int32_t* ib = a.idx + (size_t)u * a.budget;
-    const size_t cache_off = (size_t)u * a.max_ctx * kHeadDim;
+    const int kvc = (u - b * a.n_kv_heads) / a.kv_div;
+    const size_t cache_off = ((size_t)b * a.n_kv_real + kvc) * a.max_ctx * kHeadDim;
     const size_t sel_off = (size_t)u * a.budget * kHeadDim;
     int e[2];
     u32x4 kk[2], vv[2];

@@ -1,7 +1,8 @@
 """GPU parity of the per-query-head variant (one importance vector and one index
 set per query head instead of per KV head) against the oracle: verify's
 per-head scores (both schedules; the outputs are unchanged), select over the
-query heads, and the draft with one set per head reading its KV head's rows."""
+query heads, the draft with one set per head reading its KV head's rows, and
+a draft round over those sets."""
 from types import SimpleNamespace
 
 import numpy as np
@@ -91,3 +92,37 @@ def test_per_head_limits():
     with pytest.raises(B.SSLError):   # two sweeps need a group dividing 16
         B.verify_attn(d.q, d.k, d.v, w.ctx_len, w.q_len, _params(w, B.VERIFY_TWO_SWEEP),
                       scores=torch.zeros((1, 6, w.max_ctx), dtype=torch.float32, device="cuda"))
+
+
+@pytest.mark.parametrize("name", ["g4-b2", "g8-b1"])
+def test_per_head_draft_round(name):
+    """A draft round with one index set per query head (built at the base
+    lengths by select over per-head scores): every step, through the index
+    lists and from the materialized rows, against the oracle's per-head step;
+    the drafted tokens' rows are cache rows past the base lengths."""
+    from paper_2607_27735_amd.workloads import f32_to_bf16_bits
+    w = CASES[name]()
+    steps = 5
+    base = (w.ctx_len - steps).astype(np.int32)
+    rng = np.random.default_rng(int(base.sum()))
+    wq = SimpleNamespace(batch=w.batch, n_kv_heads=w.n_q_heads, ctx_len=base,
+                         k_sink=w.k_sink, k_recent=w.k_recent, budget=w.budget)
+    idx, n_idx = oracle.select(wq, rng.random((w.batch, w.n_q_heads, w.max_ctx)), ctx_len=base)
+    p = _params(w)
+    d = Dev(w)
+    idx_d = torch.from_numpy(np.ascontiguousarray(idx)).cuda()
+    k_sel, v_sel = B.draft_materialize(d.k, d.v, idx_d, base, p, n_q_heads=w.n_q_heads)
+    torch.cuda.synchronize()
+    for i in range(steps + 1):
+        qb = f32_to_bf16_bits(rng.standard_normal(w.q_draft.shape).astype(np.float32))
+        cur = base + i
+        o_ref = oracle.draft_step(w, idx, base, cur, q_draft=qb, per_head=True)
+        oabs = oracle.draft_step(w, idx, base, cur, q_draft=qb, v=abs_v(w), per_head=True)
+        qd = torch.from_numpy(qb.view(np.int16).copy()).view(torch.bfloat16).cuda()
+        o_sel = B.draft_step(qd, d.k, d.v, base, cur, p, k_sel=k_sel, v_sel=v_sel)
+        o_idx = B.draft_step(qd, d.k, d.v, base, cur, p, idx=idx_d)
+        torch.cuda.synchronize()
+        o_sel = o_sel.float().cpu().numpy().astype(np.float64)
+        check_outputs(o_sel, o_ref, oabs, np.ones(o_ref.shape[:2], dtype=bool),
+                      what=f"per-head draft step {i}")
+        assert np.array_equal(o_idx.float().cpu().numpy().astype(np.float64), o_sel)
