@@ -85,16 +85,16 @@ def is_paged(short: str) -> bool:
         return len(args) == 3 and args[2] == "true"
     if k in ("verify_stats_kernel", "verify_main_kernel"):
         return len(args) == 2 and args[1] == "true"
-    return k == "draft_kernel" and args == ["3"]
+    return k == "draft_kernel" and args[0] == "3"
 
 
-def summarize_trace(d: str, command: str) -> str:
+def summarize_trace(d: str, command: str, title: str = "") -> str:
     """Markdown table of a rocprofv3 --kernel-trace --stats run."""
     import csv
     import glob
     f = glob.glob(os.path.join(d, "**", "*kernel_stats.csv"), recursive=True)[0]
     rows = [r for r in csv.DictReader(open(f)) if any(k in r["Name"] for k in OUR_KERNELS)]
-    out = [f"command: `{command}`", "",
+    out = ([f"# Kernel trace: {title}", ""] if title else []) + [f"command: `{command}`", "",
            "| kernel | calls | avg us | min us | max us |", "|---|---:|---:|---:|---:|"]
     for r in sorted(rows, key=lambda r: -float(r["AverageNs"])):
         out.append(f"| {kernel_short(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} "
@@ -103,12 +103,13 @@ def summarize_trace(d: str, command: str) -> str:
     for r in rows:
         short = kernel_short(r["Name"])
         k = short.split("<")[0]
+        mode = short.split("<", 1)[1].split(",")[0].strip(" >") if "<" in short else ""
         call = ("verify (paged)" if k.startswith("verify") and is_paged(short)
                 else "draft (paged)" if is_paged(short)
                 else "verify" if k.startswith("verify") else "select" if k.startswith("select")
                 else "draft round materialize" if "materialize" in k
-                else "draft round step (index list)" if short == "draft_kernel<1>"
-                else "draft round step (materialized rows)" if short == "draft_kernel<2>"
+                else "draft round step (index list)" if k == "draft_kernel" and mode == "1"
+                else "draft round step (materialized rows)" if k == "draft_kernel" and mode == "2"
                 else "logit statistics" if k.startswith("logit")
                 else "greedy acceptance" if k.startswith("greedy") else "draft")
         per_call[call] = per_call.get(call, 0.0) + float(r["AverageNs"]) / 1e3
@@ -363,7 +364,8 @@ def paged_bench(B, w, kvs, q, qd, params, stream, reps, torch, np, page=128):
     return res
 
 
-def summarize_traffic(fetch_dir: str, write_dir: str, copy_mib: int, command: str) -> str:
+def summarize_traffic(fetch_dir: str, write_dir: str, copy_mib: int, command: str,
+                      title: str = "llama8b-T32K workload") -> str:
     """HBM traffic per launch from two rocprofv3 --pmc runs (FETCH_SIZE, then
     WRITE_SIZE, KiB per dispatch), each scaled by what the counter reads for
     the plain device copy of copy_mib MiB that the same command ends with."""
@@ -387,7 +389,7 @@ def summarize_traffic(fetch_dir: str, write_dir: str, copy_mib: int, command: st
     cw, write = load(write_dir, "WRITE_SIZE")
     f_fac = copy_bytes / (statistics.fmean(cf) * 1024.0)
     w_fac = copy_bytes / (statistics.fmean(cw) * 1024.0)
-    lines = [f"# HBM traffic per launch, llama8b-T32K workload (rocprofv3 FETCH_SIZE / WRITE_SIZE)",
+    lines = [f"# HBM traffic per launch, {title} (rocprofv3 FETCH_SIZE / WRITE_SIZE)",
              f"command = {command}",
              f"sources_sha256 = {sources_sha256()}",
              f"copy_bytes = {copy_bytes}",
@@ -640,16 +642,18 @@ def main() -> int:
                     help="print MFMA use per launch from a rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 "
                          "output and exit")
     ap.add_argument("--command-text", default="", help="the profiling command, for summaries")
+    ap.add_argument("--title", default="", help="the workload a summary covers, for its title")
     args = ap.parse_args()
     if args.summarize_trace:
-        sys.stdout.write(summarize_trace(args.summarize_trace, args.command_text))
+        sys.stdout.write(summarize_trace(args.summarize_trace, args.command_text, args.title))
         return 0
     if args.summarize_mfma:
         sys.stdout.write(summarize_mfma(args.summarize_mfma, args.command_text))
         return 0
     if args.summarize_traffic:
         sys.stdout.write(summarize_traffic(*args.summarize_traffic, args.copy_calibration_mib,
-                                           args.command_text))
+                                           args.command_text,
+                                           args.title or "llama8b-T32K workload"))
         return 0
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the hot path runs on one GPU; see the design "
