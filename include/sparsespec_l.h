@@ -312,6 +312,31 @@ int ssl_draft_attn(const ssl_shape *shape, const ssl_params *params,
                    void *out, void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Select and the first draft step in one call (Sec. 3.2: Eq. 4 builds the
+ * recallable set, Eq. 5 attends over it): ssl_select_topb, then
+ * ssl_draft_attn over the index sets it builds (n_idx = ssl_index_count at
+ * T = ctx_len_host[b]), with the same arguments, layouts and results (the
+ * draft's sums may be ordered differently).  Where select runs as one kernel
+ * (ssl_select_plan; partitions of at most 4096 positions, at most 16 query
+ * heads per unit) that kernel also runs the draft step: each partition
+ * attends over the rows it selected and the partitions' partial results are
+ * merged inside the kernel, so the index sets are never read back.  Otherwise
+ * the two calls run one after the other on `stream`.  The workspace size comes
+ * from ssl_select_draft_workspace.  Errors: those of the two calls.  When an
+ * exchange gives up (SSL_EXCHANGE_SELECT raised), the one-kernel form writes
+ * neither index sets nor draft outputs for the unit; the two-call form then
+ * drafts over idx as it stood (indices are clamped into [0, max_ctx), so no
+ * access leaves the cache) and the draft output is meaningless.
+ */
+int ssl_select_draft_workspace(const ssl_shape *shape, const ssl_params *params,
+                               const int32_t *ctx_len_host, size_t *bytes_out);
+int ssl_select_draft(const ssl_shape *shape, const ssl_params *params,
+                     const int32_t *ctx_len_host, const float *scores, int32_t *idx,
+                     int32_t *n_idx, const void *q_draft, const void *k_cache,
+                     const void *v_cache, void *out, void *workspace, size_t workspace_bytes,
+                     hipStream_t stream);
+
+/*
  * Paged KV cache, as serving engines keep it: the same calls with K and V in
  * page pools instead of one contiguous row per (sequence, KV head).
  *

@@ -35,7 +35,8 @@ EXPORTED = [
     "ssl_status_string", "ssl_build_id", "ssl_exchange_status", "ssl_set_cu_budget",
     "ssl_test_exchange_faults", "ssl_index_count",
     "ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn", "ssl_verify_attn_static",
-    "ssl_select_workspace", "ssl_select_plan", "ssl_select_topb",
+    "ssl_select_workspace", "ssl_select_plan", "ssl_select_topb", "ssl_select_draft_workspace",
+    "ssl_select_draft",
     "ssl_draft_workspace", "ssl_draft_attn",
     "ssl_verify_attn_paged", "ssl_draft_attn_paged",
     "ssl_draft_materialize", "ssl_draft_step_workspace", "ssl_draft_step",
@@ -108,6 +109,8 @@ def load(path: Optional[str] = None):
     lib.ssl_verify_attn_static.argtypes = [sp, pp, _i32p, _i32p, _vp, _vp, _vp, _vp, _vp, _vp]
     lib.ssl_select_workspace.argtypes = [sp, pp, _i32p, _szp]
     lib.ssl_select_plan.argtypes = [sp, pp, _i32p, _i32p, _i32p, _i32p]
+    lib.ssl_select_draft_workspace.argtypes = [sp, pp, _i32p, _szp]
+    lib.ssl_select_draft.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
     lib.ssl_select_topb.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _sz, _vp]
     lib.ssl_draft_workspace.argtypes = [sp, pp, _i32p, _szp]
     lib.ssl_draft_attn.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
@@ -127,7 +130,8 @@ def load(path: Optional[str] = None):
                                       _vp, _sz, _vp]
     for f in ("ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn",
               "ssl_verify_attn_static", "ssl_select_workspace",
-              "ssl_select_topb", "ssl_select_plan", "ssl_draft_workspace", "ssl_draft_attn", "ssl_draft_materialize",
+              "ssl_select_topb", "ssl_select_plan", "ssl_select_draft_workspace",
+              "ssl_select_draft", "ssl_draft_workspace", "ssl_draft_attn", "ssl_draft_materialize",
               "ssl_draft_step_workspace", "ssl_draft_step", "ssl_verify_attn_paged",
               "ssl_draft_attn_paged", "ssl_logit_stats_workspace",
               "ssl_logit_stats", "ssl_greedy_accept_workspace", "ssl_greedy_accept"):
@@ -355,6 +359,50 @@ def select_workspace_bytes(shape: Shape, params: Params, ctx_len) -> int:
                                        ctx.ctypes.data_as(_i32p), ctypes.byref(n)),
            "ssl_select_workspace")
     return int(n.value)
+
+
+def select_draft_workspace_bytes(shape: Shape, params: Params, ctx_len) -> int:
+    ctx = _host_i32(ctx_len)
+    n = ctypes.c_size_t(0)
+    _check(load().ssl_select_draft_workspace(ctypes.byref(shape), ctypes.byref(params),
+                                             ctx.ctypes.data_as(_i32p), ctypes.byref(n)),
+           "ssl_select_draft_workspace")
+    return int(n.value)
+
+
+def select_draft(scores: torch.Tensor, ctx_len, params: Params, q_draft: torch.Tensor,
+                 k: torch.Tensor, v: torch.Tensor, idx: Optional[torch.Tensor] = None,
+                 n_idx: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                 workspace: Optional[torch.Tensor] = None, stream=None):
+    """Eq. 4 index sets and the first Eq. 5 draft step over them in one call;
+    returns (idx, n_idx, out)."""
+    _need_gpu(scores, q_draft, k, v)
+    if scores.dtype != torch.float32:
+        raise TypeError("scores must be float32")
+    batch, hq, d = q_draft.shape
+    _, hkv, max_ctx, _ = k.shape
+    units = hq if params.per_head else hkv
+    if tuple(scores.shape) != (batch, units, max_ctx):
+        raise ValueError("scores must be [batch, units, max_ctx]")
+    shape = Shape(batch, hq, hkv, d, max_ctx, 1)
+    ctx = _host_i32(ctx_len)
+    if idx is None:
+        idx = torch.empty((batch, units, params.budget), dtype=torch.int32, device=scores.device)
+    if n_idx is None:
+        n_idx = torch.empty(batch, dtype=torch.int32, device=scores.device)
+    odt = torch.float32 if params.out_fp32 else torch.bfloat16
+    if out is None:
+        out = torch.empty(q_draft.shape, dtype=odt, device=q_draft.device)
+    _need_gpu(idx, n_idx, out)
+    need = select_draft_workspace_bytes(shape, params, ctx)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=scores.device)
+    _check(load().ssl_select_draft(ctypes.byref(shape), ctypes.byref(params),
+                                   ctx.ctypes.data_as(_i32p), _ptr(scores), _ptr(idx), _ptr(n_idx),
+                                   _ptr(q_draft), _ptr(k), _ptr(v), _ptr(out), _ptr(workspace),
+                                   workspace.numel(), _stream(stream)),
+           "ssl_select_draft")
+    return idx, n_idx, out
 
 
 # ---------------------------------------------------------------------------
@@ -705,7 +753,8 @@ class PreparedStep:
         self.dshape = Shape(self.shape.batch, self.shape.n_q_heads, self.shape.n_kv_heads,
                             self.shape.head_dim, self.shape.max_ctx, 1)
         vws = verify_workspace_bytes(self.shape, params, self.ctx, self.ql)
-        sws = select_workspace_bytes(self.shape, params, self.ctx)
+        sws = max(select_workspace_bytes(self.shape, params, self.ctx),
+                  select_draft_workspace_bytes(self.dshape, params, self.ctx))
         dws = draft_workspace_bytes(self.dshape, params, self.n_idx_host)
         if shared_workspace:   # one buffer for the three calls, ordered on one stream
             self.vws = torch.empty(max(vws, sws, dws, 1), dtype=torch.uint8, device=q.device)
@@ -725,6 +774,9 @@ class PreparedStep:
         self._d = (ctypes.byref(self.dshape), pp, self.n_idx_host.ctypes.data_as(_i32p),
                    q_draft.data_ptr(), k.data_ptr(), v.data_ptr(), idx.data_ptr(),
                    draft_out.data_ptr(), self.dws.data_ptr(), self.dws.numel(), self.stream)
+        self._sd = (ctypes.byref(self.dshape), pp, cp, scores.data_ptr(), idx.data_ptr(),
+                    n_idx.data_ptr(), q_draft.data_ptr(), k.data_ptr(), v.data_ptr(),
+                    draft_out.data_ptr(), self.sws.data_ptr(), self.sws.numel(), self.stream)
 
     def verify(self) -> None:
         _check(self._lib.ssl_verify_attn(*self._v), "ssl_verify_attn")
@@ -735,7 +787,16 @@ class PreparedStep:
     def draft(self) -> None:
         _check(self._lib.ssl_draft_attn(*self._d), "ssl_draft_attn")
 
+    def select_draft(self) -> None:
+        """select and the first draft step in one call (ssl_select_draft)."""
+        _check(self._lib.ssl_select_draft(*self._sd), "ssl_select_draft")
+
     def step(self) -> None:
+        self.verify()
+        self.select_draft()
+
+    def step_separate(self) -> None:
+        """The same step as three calls (verify, select, draft)."""
         self.verify()
         self.select()
         self.draft()

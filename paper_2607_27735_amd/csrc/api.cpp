@@ -622,6 +622,91 @@ int verify_attn_static_scratch(const ssl_shape* shape, const ssl_params* params,
 
 }  // namespace ssl
 
+namespace {
+
+// The first draft step that ssl_select_draft hands to the select kernel.
+struct DraftInputs {
+    const void* q_draft;
+    const void* k_cache;
+    const void* v_cache;
+    void* out;
+};
+
+// Whether select's one-kernel schedule also runs the first draft step: the
+// kernel's row list holds 4096 entries (partitions of at most 4096 positions)
+// and the draft tile holds 16 query heads.
+bool select_draft_fused(const SelectPlan& plan, int group) {
+    return plan.fused && plan.part <= 4096 && group <= 16;
+}
+
+size_t select_draft_part_bytes(const SelectPlan& plan, int64_t units) {
+    return align_up((size_t)units * plan.parts * 16 * kSelectDraftStride * sizeof(float));
+}
+
+int select_call(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
+                const float* scores, int32_t* idx, int32_t* n_idx, void* workspace,
+                size_t workspace_bytes, hipStream_t stream, const DraftInputs* draft) {
+    int rc = check_select(shape, params, ctx_len_host);
+    if (rc) return rc;
+    if (!scores || !idx || !n_idx) return SSL_ERR_NULL;
+    if (!aligned(scores, 4) || !aligned(idx, 4) || !aligned(n_idx, 4)) return SSL_ERR_ALIGN;
+    const ssl_shape us = unit_shape(shape, params);
+    SelectPlan plan;
+    rc = plan_select(&us, ctx_len_host, &plan);
+    if (rc) return rc;
+    const int64_t units = (int64_t)shape->batch * us.n_kv_heads;
+    const size_t need = plan.bytes + (draft ? select_draft_part_bytes(plan, units) : 0);
+    rc = check_workspace(workspace, workspace_bytes, need);
+    if (rc) return rc;
+    char* ws = static_cast<char*>(workspace);
+    SelectArgs a;
+    memset(&a, 0, sizeof a);
+    a.scores = scores;
+    a.idx = idx;
+    a.n_idx = n_idx;
+    a.hist = reinterpret_cast<uint32_t*>(ws + plan.hist_off);
+    a.coarse = reinterpret_cast<uint32_t*>(ws + plan.coarse_off);
+    a.cnt = reinterpret_cast<uint32_t*>(ws + plan.cnt_off);
+    a.thr = reinterpret_cast<uint32_t*>(ws + plan.thr_off);
+    a.mask = reinterpret_cast<uint32_t*>(ws + plan.mask_off);
+    a.seg = reinterpret_cast<uint2*>(ws + plan.seg_off);
+    a.tag = reinterpret_cast<uint64_t*>(ws + plan.tag_off);
+    if (plan.fused) {   // the three-kernel schedule exchanges nothing inside a kernel
+        rc = epochs_if_captured(stream, ws, units, &a.epoch);
+        if (rc) return rc;
+    }
+    rc = make_exchange(&a.xc);
+    if (rc) return rc;
+    a.call_tag = next_call_tag();
+    a.fused = plan.fused ? 1 : 0;
+    a.part = plan.part;
+    a.parts = plan.parts;
+    a.n_kv_heads = us.n_kv_heads;
+    a.max_ctx = shape->max_ctx;
+    a.k_sink = params->k_sink;
+    a.k_recent = params->k_recent;
+    a.budget = params->budget;
+    a.batch = shape->batch;
+    for (int b = 0; b < shape->batch; ++b) a.ctx[b] = ctx_len_host[b];
+    if (draft) {
+        a.with_draft = 1;
+        a.d.q = static_cast<const uint16_t*>(draft->q_draft);
+        a.d.k = static_cast<const uint16_t*>(draft->k_cache);
+        a.d.v = static_cast<const uint16_t*>(draft->v_cache);
+        a.d.out = draft->out;
+        a.d.part = reinterpret_cast<float*>(ws + plan.bytes);
+        a.d.n_q_heads = shape->n_q_heads;
+        a.d.group = us.n_q_heads / us.n_kv_heads;
+        a.d.kv_div = shape->n_kv_heads == us.n_kv_heads ? 1 : shape->n_q_heads / shape->n_kv_heads;
+        a.d.n_kv_real = shape->n_kv_heads;
+        a.d.out_fp32 = params->out_fp32 ? 1 : 0;
+        a.d.scale_log2 = params->sm_scale * 1.4426950408889634f;
+    }
+    return launch_select(a, (int)units, stream) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
+}
+
+}  // namespace
+
 extern "C" {
 
 int ssl_verify_attn(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
@@ -673,48 +758,8 @@ int ssl_select_plan(const ssl_shape* shape, const ssl_params* params, const int3
 int ssl_select_topb(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
                     const float* scores, int32_t* idx, int32_t* n_idx, void* workspace,
                     size_t workspace_bytes, hipStream_t stream) {
-    int rc = check_select(shape, params, ctx_len_host);
-    if (rc) return rc;
-    if (!scores || !idx || !n_idx) return SSL_ERR_NULL;
-    if (!aligned(scores, 4) || !aligned(idx, 4) || !aligned(n_idx, 4)) return SSL_ERR_ALIGN;
-    const ssl_shape us = unit_shape(shape, params);
-    SelectPlan plan;
-    rc = plan_select(&us, ctx_len_host, &plan);
-    if (rc) return rc;
-    rc = check_workspace(workspace, workspace_bytes, plan.bytes);
-    if (rc) return rc;
-    char* ws = static_cast<char*>(workspace);
-    SelectArgs a;
-    memset(&a, 0, sizeof a);
-    a.scores = scores;
-    a.idx = idx;
-    a.n_idx = n_idx;
-    a.hist = reinterpret_cast<uint32_t*>(ws + plan.hist_off);
-    a.coarse = reinterpret_cast<uint32_t*>(ws + plan.coarse_off);
-    a.cnt = reinterpret_cast<uint32_t*>(ws + plan.cnt_off);
-    a.thr = reinterpret_cast<uint32_t*>(ws + plan.thr_off);
-    a.mask = reinterpret_cast<uint32_t*>(ws + plan.mask_off);
-    a.seg = reinterpret_cast<uint2*>(ws + plan.seg_off);
-    a.tag = reinterpret_cast<uint64_t*>(ws + plan.tag_off);
-    if (plan.fused) {   // the three-kernel schedule exchanges nothing inside a kernel
-        rc = epochs_if_captured(stream, ws, (int64_t)shape->batch * us.n_kv_heads, &a.epoch);
-        if (rc) return rc;
-    }
-    rc = make_exchange(&a.xc);
-    if (rc) return rc;
-    a.call_tag = next_call_tag();
-    a.fused = plan.fused ? 1 : 0;
-    a.part = plan.part;
-    a.parts = plan.parts;
-    a.n_kv_heads = us.n_kv_heads;
-    a.max_ctx = shape->max_ctx;
-    a.k_sink = params->k_sink;
-    a.k_recent = params->k_recent;
-    a.budget = params->budget;
-    a.batch = shape->batch;
-    for (int b = 0; b < shape->batch; ++b) a.ctx[b] = ctx_len_host[b];
-    return launch_select(a, shape->batch * us.n_kv_heads, stream) == hipSuccess ? SSL_OK
-                                                                                : SSL_ERR_HIP;
+    return select_call(shape, params, ctx_len_host, scores, idx, n_idx, workspace, workspace_bytes,
+                       stream, nullptr);
 }
 
 int ssl_draft_workspace(const ssl_shape* shape, const ssl_params* params,
@@ -810,6 +855,66 @@ int ssl_draft_attn_paged(const ssl_shape* shape, const ssl_params* params,
     if (!block_table) return SSL_ERR_NULL;
     return draft_call(shape, params, n_idx_host, q_draft, k_pages, v_pages, block_table, page_size,
                       max_blocks, idx, out, workspace, workspace_bytes, stream);
+}
+
+// select + the first draft step: the draft's entries per sequence (Eq. 4's
+// count at T = ctx_len), and whether the select kernel runs the draft itself.
+namespace {
+int select_draft_plan(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx,
+                      SelectPlan* plan, bool* fused, int32_t* n_idx_host, size_t* bytes) {
+    int rc = check_select(shape, params, ctx);
+    if (rc) return rc;
+    if (!(params->sm_scale > 0.f) || !isfinite(params->sm_scale)) return SSL_ERR_SHAPE;
+    const ssl_shape us = unit_shape(shape, params);
+    rc = plan_select(&us, ctx, plan);
+    if (rc) return rc;
+    for (int b = 0; b < shape->batch; ++b)
+        n_idx_host[b] = ssl_index_count(ctx[b], params->k_sink, params->k_recent, params->budget);
+    DraftPlan dp;
+    rc = plan_draft(&us, params, n_idx_host, &dp);
+    if (rc) return rc;
+    *fused = select_draft_fused(*plan, us.n_q_heads / us.n_kv_heads);
+    *bytes = *fused ? plan->bytes + select_draft_part_bytes(*plan, (int64_t)shape->batch * us.n_kv_heads)
+                    : std::max(plan->bytes, dp.bytes);
+    return SSL_OK;
+}
+}  // namespace
+
+int ssl_select_draft_workspace(const ssl_shape* shape, const ssl_params* params,
+                               const int32_t* ctx_len_host, size_t* bytes_out) {
+    if (!bytes_out) return SSL_ERR_NULL;
+    SelectPlan plan;
+    bool fused = false;
+    int32_t n_idx_host[kTableBatch];
+    return select_draft_plan(shape, params, ctx_len_host, &plan, &fused, n_idx_host, bytes_out);
+}
+
+int ssl_select_draft(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
+                     const float* scores, int32_t* idx, int32_t* n_idx, const void* q_draft,
+                     const void* k_cache, const void* v_cache, void* out, void* workspace,
+                     size_t workspace_bytes, hipStream_t stream) {
+    SelectPlan plan;
+    bool fused = false;
+    int32_t n_idx_host[kTableBatch];
+    size_t need = 0;
+    int rc = select_draft_plan(shape, params, ctx_len_host, &plan, &fused, n_idx_host, &need);
+    if (rc) return rc;
+    if (!scores || !idx || !n_idx || !q_draft || !k_cache || !v_cache || !out) return SSL_ERR_NULL;
+    if (!aligned(scores, 4) || !aligned(idx, 4) || !aligned(n_idx, 4) || !aligned(q_draft, 16) ||
+        !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16))
+        return SSL_ERR_ALIGN;
+    rc = check_workspace(workspace, workspace_bytes, need);
+    if (rc) return rc;
+    if (fused) {
+        const DraftInputs d{q_draft, k_cache, v_cache, out};
+        return select_call(shape, params, ctx_len_host, scores, idx, n_idx, workspace,
+                           workspace_bytes, stream, &d);
+    }
+    rc = select_call(shape, params, ctx_len_host, scores, idx, n_idx, workspace, workspace_bytes,
+                     stream, nullptr);
+    if (rc) return rc;
+    return draft_call(shape, params, n_idx_host, q_draft, k_cache, v_cache, nullptr, 0, 0, idx, out,
+                      workspace, workspace_bytes, stream);
 }
 
 int ssl_draft_materialize(const ssl_shape* shape, const ssl_params* params,

@@ -100,6 +100,20 @@ constexpr int kMaxSelectParts = 256;
 // (three-kernel path) or up to 2048 tagged 64-bit bin entries (one kernel).
 constexpr int kHistSlotWords = 4096;
 
+// The first draft step over the index sets, run by the one-kernel select
+// (Eq. 5 with the rows each partition selected): per unit, query heads
+// [c*group, (c+1)*group) of q, rows of cache head c / kv_div.
+struct SelectDraft {
+    const uint16_t* q;      // [batch][n_q][128]
+    const uint16_t* k;      // [batch][n_kv_real][max_ctx][128]
+    const uint16_t* v;
+    void* out;              // [batch][n_q][128]
+    float* part;            // [units][parts][16][132] per partition and head: max, sum, 2 spare, P.V
+    int32_t n_q_heads, group, kv_div, n_kv_real, out_fp32;
+    float scale_log2;
+};
+constexpr int kSelectDraftStride = 132;   // floats per (partition, head) partial
+
 struct SelectArgs {
     const float* scores;
     int32_t* idx;
@@ -115,6 +129,8 @@ struct SelectArgs {
     uint64_t call_tag;  // this call's tag: unique within the process (see exchange_tag)
     Exchange xc;
     int32_t fused;      // 1: one kernel (the partitions of a unit exchange while resident)
+    int32_t with_draft; // 1: the one kernel also runs the first draft step (d)
+    SelectDraft d;
     int32_t n_kv_heads, max_ctx, k_sink, k_recent, budget, batch, part, parts;
     int32_t ctx[kTableBatch];
 };

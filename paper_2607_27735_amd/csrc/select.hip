@@ -29,7 +29,9 @@
 //         middle selections (by a block scan of per-thread popcounts) and
 //         recent in ascending order.
 #include "device_common.h"
+#include "draft_common.h"
 #include "launch.h"
+#include "verify_common.h"
 
 namespace ssl {
 namespace {
@@ -603,23 +605,202 @@ __device__ __forceinline__ void wait_counts(const uint64_t* tag, int n, int stri
     }
 }
 
-template <int NR>
+constexpr int kTags = 4;   // tag words per partition: histogram entries, candidates,
+                           // middle above d1, draft partial
+
+// The first draft step (Eq. 5) over the rows partition p selected, run by the
+// select kernel so that no second launch reads the index set back.  Entries
+// e < n_mid are the partition's selected middle positions (rows_l[e], or
+// mid_base + e when its whole range is selected); then s_len sink positions
+// and n_rec recent ones (partition 0 only).  Each wave attends over tiles of
+// 32 entries (two-deep gather ring); the four waves merge through LDS; every
+// partition but 0 publishes its partial per query head with device-coherent
+// stores and then a tag, and partition 0 waits for those tags (bounded),
+// merges the partials in partition order and writes the output.  Called by
+// every thread of the workgroup; returns whether partition 0 completed (the
+// caller then advances the exchange epoch).
+__device__ bool select_draft_tail(const SelectArgs& a, const Geom& g, int u, int p, int n_mid,
+                                  int mid_base, int s_len, int n_rec, const uint32_t* rows_l,
+                                  float* park, float2* wml, float2* gml, int* wait_failed,
+                                  uint64_t* tag, uint64_t want, uint64_t pub) {
+    using dc::kTile;
+    const SelectDraft& d = a.d;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int m16 = lane & 15, G = lane >> 4;
+    const int b = u / a.n_kv_heads, c = u - b * a.n_kv_heads;
+    const int gq = d.group;
+    const int n = n_mid + s_len + n_rec;
+    const size_t cache_off = ((size_t)b * d.n_kv_real + c / d.kv_div) * a.max_ctx * kHeadDim;
+    const dc::RowSource src{d.k + cache_off, d.v + cache_off, nullptr, nullptr};
+    auto row_of = [&](int e) -> uint32_t {
+        e = min(e, n - 1);
+        if (e < n_mid) return mid_base >= 0 ? (uint32_t)(mid_base + e) : rows_l[e];
+        e -= n_mid;
+        return e < s_len ? (uint32_t)e : (uint32_t)(g.r_start + e - s_len);
+    };
+    u32x4 qop[4];
+    if (m16 < gq) {
+        const uint16_t* qp = d.q + ((size_t)b * d.n_q_heads + c * gq + m16) * kHeadDim + 8 * G;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) qop[kb] = ld_u32x4(qp + 32 * kb);
+    } else {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) qop[kb] = u32x4{0u, 0u, 0u, 0u};
+    }
+    float M = -INFINITY, L = 0.f;
+    f32x4 oacc[8];
+#pragma unroll
+    for (int jd = 0; jd < 8; ++jd) oacc[jd] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int ntile = (n + kTile - 1) / kTile;
+    vc::tile_pipeline<2, dc::Gathered>(
+        wave, ntile, kSelWaves,
+        [&](dc::Gathered& t, int tile) {
+            dc::gather_tile<false>(row_of(tile * kTile + (lane & 31)), 0, src, m16, G, t);
+        },
+        [&](const dc::Gathered& t, int tile) {
+            dc::draft_tile(d.scale_log2, qop, t, tile * kTile, n, G, M, L, oacc);
+        });
+    L += shfl_xor_f(L, 16);
+    L += shfl_xor_f(L, 32);
+
+    // the four waves, merged in a fixed order: (max, sum) per head in gml, the
+    // waves' P.V scaled to that max parked in LDS ([wave][head][stride])
+    constexpr int kStride = kSelectDraftStride;
+    if (G == 0) wml[wave * 16 + m16] = make_float2(M, L);
+    __syncthreads();
+    if (tid < 16) {
+        float Mx = -INFINITY, Lx = 0.f;
+#pragma unroll
+        for (int w = 0; w < kSelWaves; ++w) Mx = fmaxf(Mx, wml[w * 16 + tid].x);
+#pragma unroll
+        for (int w = 0; w < kSelWaves; ++w) {
+            const float2 v = wml[w * 16 + tid];
+            Lx += v.x == -INFINITY ? 0.f : v.y * fast_exp2(v.x - Mx);
+        }
+        gml[tid] = make_float2(Mx, Lx);
+    }
+    {
+        float Mx = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < kSelWaves; ++w) Mx = fmaxf(Mx, wml[w * 16 + m16].x);
+        const float f = M == -INFINITY ? 0.f : fast_exp2(M - Mx);
+        float* dst = park + (wave * 16 + m16) * kStride + 4;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int cc = 32 * G + 8 * i;
+            *reinterpret_cast<f32x4*>(dst + cc) = f32x4{oacc[0][i], oacc[1][i], oacc[2][i], oacc[3][i]} * f;
+            *reinterpret_cast<f32x4*>(dst + cc + 4) = f32x4{oacc[4][i], oacc[5][i], oacc[6][i], oacc[7][i]} * f;
+        }
+    }
+    __syncthreads();
+
+    const int P = g.parts;
+    float* part0 = d.part + (size_t)u * a.parts * 16 * kStride;   // [P][16][kStride]
+    if (p != 0) {   // publish the partition's partial and its tag, then leave
+        float* dp = part0 + (size_t)p * 16 * kStride;
+        for (int x = tid; x < gq * (kHeadDim / 2); x += kSelThreads) {
+            const int row = x / (kHeadDim / 2), c2 = x - row * (kHeadDim / 2);
+            float2 o = *reinterpret_cast<const float2*>(park + row * kStride + 4 + 2 * c2);
+#pragma unroll
+            for (int w = 1; w < kSelWaves; ++w) {
+                const float2 v = *reinterpret_cast<const float2*>(park + (w * 16 + row) * kStride + 4 + 2 * c2);
+                o.x += v.x;
+                o.y += v.y;
+            }
+            st_dev64(reinterpret_cast<uint64_t*>(dp + row * kStride + 4) + c2, __builtin_bit_cast(uint64_t, o));
+        }
+        if (tid < gq)
+            st_dev64(reinterpret_cast<uint64_t*>(dp + tid * kStride), __builtin_bit_cast(uint64_t, gml[tid]));
+        wait_stores_done();
+        __syncthreads();
+        if (tid == 0) st_dev64(tag + (size_t)p * kTags + 3, pub);
+        return false;
+    }
+    // partition 0: the others never wait for it, so their tags arrive
+    if (wave == 0) {
+        int spins = 0;
+        bool all_in;
+        do {
+            bool in = true;
+            for (int pp = 1 + lane; pp < P; pp += kWave) in &= ld_dev64(tag + (size_t)pp * kTags + 3) == want;
+            all_in = __all(in);
+            if (!all_in) __builtin_amdgcn_s_sleep(1);
+        } while (!all_in && ++spins < a.xc.spin_limit);
+        if (lane == 0) *wait_failed = !all_in;
+    }
+    __syncthreads();
+    if (*wait_failed) {
+        if (tid == 0) exchange_gave_up(a.xc, kStatusSelect, a.epoch ? a.epoch + u : nullptr);
+        return false;
+    }
+    constexpr int kBatch = 16;
+    for (int x = tid; x < gq * (kHeadDim / 4); x += kSelThreads) {
+        const int row = x >> 5, d4 = x & 31;
+        float Mx = -INFINITY, Lx = 0.f;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int p0 = 0; p0 < P; p0 += kBatch) {
+            float2 ml[kBatch];
+            f32x4 o[kBatch];
+#pragma unroll
+            for (int uu = 0; uu < kBatch; ++uu) {
+                const int pp = p0 + uu;
+                if (pp == 0) {
+                    ml[uu] = gml[row];
+                    f32x4 ov = *reinterpret_cast<const f32x4*>(park + row * kStride + 4 + 4 * d4);
+#pragma unroll
+                    for (int w = 1; w < kSelWaves; ++w)
+                        ov += *reinterpret_cast<const f32x4*>(park + (w * 16 + row) * kStride + 4 + 4 * d4);
+                    o[uu] = ov;
+                } else if (pp < P) {
+                    const float* dp = part0 + ((size_t)pp * 16 + row) * kStride;
+                    ml[uu] = __builtin_bit_cast(float2, ld_dev64(reinterpret_cast<const uint64_t*>(dp)));
+                    const uint64_t* po = reinterpret_cast<const uint64_t*>(dp + 4) + 2 * d4;
+                    const float2 lo = __builtin_bit_cast(float2, ld_dev64(po));
+                    const float2 hi = __builtin_bit_cast(float2, ld_dev64(po + 1));
+                    o[uu] = f32x4{lo.x, lo.y, hi.x, hi.y};
+                } else {
+                    ml[uu] = make_float2(-INFINITY, 0.f);
+                    o[uu] = f32x4{0.f, 0.f, 0.f, 0.f};
+                }
+            }
+            float Mn = Mx;
+#pragma unroll
+            for (int uu = 0; uu < kBatch; ++uu) Mn = fmaxf(Mn, ml[uu].x);
+            const float alpha = Mx == -INFINITY ? 0.f : fast_exp2(Mx - Mn);
+            Lx *= alpha;
+            acc *= alpha;
+#pragma unroll
+            for (int uu = 0; uu < kBatch; ++uu) {
+                const float wgt = ml[uu].x == -INFINITY ? 0.f : fast_exp2(ml[uu].x - Mn);
+                Lx += ml[uu].y * wgt;
+                acc += o[uu] * wgt;
+            }
+            Mx = Mn;
+        }
+        acc *= 1.0f / Lx;
+        const size_t base = ((size_t)b * d.n_q_heads + c * gq + row) * kHeadDim + 4 * d4;
+        if (d.out_fp32) {
+            *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(d.out) + base) = acc;
+        } else {
+            const uint2 pk = make_uint2(pack_bf16(acc[0], acc[1]), pack_bf16(acc[2], acc[3]));
+            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(d.out) + base) = pk;
+        }
+    }
+    return true;
+}
+
+template <int NR, bool kDraft>
 __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a) {
+    static_assert(!kDraft || NR * kRound <= 4096, "the draft step's row list holds 4096 entries");
     const int p = blockIdx.x, u = blockIdx.y;
     const int b = u / a.n_kv_heads;
     const int c_head = u - b * a.n_kv_heads;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const Geom g = geom_of(a, b);
     if (p >= g.parts) return;
-    if (g.simple) {
-        if (p == 0) emit_ranges(a, u, g);
-        return;
-    }
-    const float* S = a.scores + (size_t)u * a.max_ctx;
     const size_t up0 = (size_t)u * a.parts;
     const int P = g.parts;
-    constexpr int kTags = 4;                  // tag words per partition: histogram entries,
-    uint64_t* tag = a.tag + up0 * kTags;      // candidates, middle above d1; [P][kTags]
+    uint64_t* tag = a.tag + up0 * kTags;      // [P][kTags]
 
     __shared__ __attribute__((aligned(16))) uint32_t hist[2048];   // read as uint4
     __shared__ __attribute__((aligned(16))) uint32_t h2[1024];
@@ -632,14 +813,41 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
     __shared__ uint32_t n_def[kMaxSelectParts], n_above[kMaxSelectParts], n_tie[kMaxSelectParts];
     __shared__ uint32_t n_cnt[kMaxSelectParts];   // candidates per partition
     __shared__ int n_eq;                          // candidates sharing tau's top 22 bits
-    __shared__ uint2 cand_lds[kTailCand];
-    __shared__ uint16_t cand_p[kTailCand];
+    __shared__ __attribute__((aligned(16))) uint2 cand_lds[kTailCand];   // later: the draft's park
+    __shared__ __attribute__((aligned(16))) uint16_t cand_p[kTailCand];  // later: the draft's rows
     __shared__ int wait_failed;
+    __shared__ float2 d_wml[kDraft ? kSelWaves * 16 : 1], d_gml[kDraft ? 16 : 1];
     // a wait gave up (or an earlier captured call on this workspace did):
     // report it and leave (workgroup-uniform: called after a barrier)
     auto give_up = [&]() {
         if (tid == 0) exchange_gave_up(a.xc, kStatusSelect, a.epoch ? a.epoch + u : nullptr);
     };
+    float* d_park = reinterpret_cast<float*>(cand_lds);
+    uint32_t* d_rows = reinterpret_cast<uint32_t*>(cand_p);
+
+    if (g.simple) {
+        if (p == 0) emit_ranges(a, u, g);
+        if constexpr (kDraft) {
+            // every middle position or none: ranges, no list
+            const uint64_t epv = scalar_here(a.epoch ? ld_dev64(a.epoch + u) : 0ull);
+            if (tid == 0) wait_failed = 0;
+            __syncthreads();
+            if (epoch_is_dirty(epv)) {
+                give_up();
+                return;
+            }
+            const uint64_t want = exchange_tag(a.call_tag, epv);
+            const int lo = p * a.part, hi = min(lo + a.part, g.T);
+            const bool all = g.all_mid;
+            const bool done = select_draft_tail(
+                a, g, u, p, all ? hi - lo : 0, all ? lo : -1, !all && p == 0 ? g.s_end : 0,
+                !all && p == 0 ? g.T - g.r_start : 0, d_rows, d_park, d_wml, d_gml, &wait_failed,
+                tag, want, want ^ a.xc.tag_flip);
+            if (done && a.epoch && tid == 0) epoch_advance(a.epoch + u);
+        }
+        return;
+    }
+    const float* S = a.scores + (size_t)u * a.max_ctx;
 
     uint32_t keys[4 * NR];
 #pragma unroll
@@ -1019,6 +1227,7 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
             if ((ab[e] >> lane) & 1ull) pos = offset + xa + min(xt, take);
             else if (((tb[e] >> lane) & 1ull) && xt < take) pos = offset + xa + xt;
             if (pos >= 0 && pos < a.budget) out[pos] = base + e * 64 + lane;
+            if (kDraft && pos >= 0) d_rows[pos - offset] = (uint32_t)(base + e * 64 + lane);
             ca += __builtin_popcountll(ab[e]);
             ct += __builtin_popcountll(tb[e]);
         }
@@ -1036,7 +1245,16 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(SelectArgs a)
         if (c_head == 0 && tid == 0) a.n_idx[b] = rbase + n_recent;
         // every partition has published, so has read the epoch; advanced last,
         // after the kernel's final wait for loads
-        if (a.epoch && tid == 0) epoch_advance(a.epoch + u);
+        if (!kDraft && a.epoch && tid == 0) epoch_advance(a.epoch + u);
+    }
+    if constexpr (kDraft) {
+        // this partition's middle selections: the non-ties and its first ties
+        const int n_mid = run_a + min(run_t, take);
+        __syncthreads();   // the row list and the free candidate cache
+        const bool done = select_draft_tail(
+            a, g, u, p, n_mid, -1, p == 0 ? g.s_end : 0, p == 0 ? g.T - g.r_start : 0, d_rows,
+            d_park, d_wml, d_gml, &wait_failed, tag, want, pub);
+        if (done && a.epoch && tid == 0) epoch_advance(a.epoch + u);
     }
 }
 
@@ -1046,7 +1264,13 @@ template <int NR>
 void launch_nr(const SelectArgs& a, int n_units, hipStream_t stream) {
     const dim3 grid(a.parts, n_units), block(kSelThreads);
     if (a.fused) {
-        hipLaunchKernelGGL(select_fused_kernel<NR>, grid, block, 0, stream, a);
+        if constexpr (NR <= 4) {
+            if (a.with_draft) {
+                hipLaunchKernelGGL((select_fused_kernel<NR, true>), grid, block, 0, stream, a);
+                return;
+            }
+        }
+        hipLaunchKernelGGL((select_fused_kernel<NR, false>), grid, block, 0, stream, a);
     } else {
         hipLaunchKernelGGL(select_hist_kernel<NR>, grid, block, 0, stream, a);
         hipLaunchKernelGGL(select_mark_kernel<NR>, grid, block, 0, stream, a);
@@ -1065,7 +1289,7 @@ int select_part_len(int max_t) {
 template <int NR>
 int blocks_per_cu_nr() {
     int blocks = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, select_fused_kernel<NR>, kSelThreads, 0) !=
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, select_fused_kernel<NR, false>, kSelThreads, 0) !=
         hipSuccess) {
         (void)hipGetLastError();
         return 0;

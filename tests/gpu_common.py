@@ -196,3 +196,19 @@ def check_band(idx, n_idx, s_ref, ctx_len, ks, kr, budget, eps=1e-3, units=None)
             tau = float(np.partition(mid, len(mid) - take)[len(mid) - take])
             assert np.all(m[mid > tau * (1 + eps)]), "clearly-above position missing"
             assert not np.any(m[mid < tau * (1 - eps)]), "clearly-below position selected"
+
+
+def gpu_select_draft(d: Dev, scores32: np.ndarray, out_fp32=True, budget=None, k_sink=None,
+                     k_recent=None, ctx_len=None):
+    """ssl_select_draft on the given fp32 scores: (idx, n_idx, draft out)."""
+    w = d.w
+    p = params_of(w, out_fp32=out_fp32, budget=budget, k_sink=k_sink, k_recent=k_recent)
+    s = torch.from_numpy(np.ascontiguousarray(scores32, dtype=np.float32)).cuda()
+    idx = torch.full((w.batch, w.n_kv_heads, p.budget), -7, dtype=torch.int32, device="cuda")
+    n_idx = torch.full((w.batch,), -1, dtype=torch.int32, device="cuda")
+    odt = torch.float32 if out_fp32 else torch.bfloat16
+    out = torch.full(d.qd.shape, -7.0, dtype=odt, device="cuda")
+    B.select_draft(s, w.ctx_len if ctx_len is None else ctx_len, p, d.qd, d.k, d.v, idx=idx,
+                   n_idx=n_idx, out=out)
+    torch.cuda.synchronize()
+    return idx.cpu().numpy(), n_idx.cpu().numpy(), out.float().cpu().numpy().astype(np.float64)

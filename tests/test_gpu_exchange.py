@@ -75,15 +75,22 @@ class Inputs:
         B.draft_step(self.qd, self.k, self.v, [T - 2] * BATCH, self.ctx, self.params, idx=src,
                      out=rout)
         ent, am = B.logit_stats(self.logits)
+        # select and the first draft step in one kernel, on the verify scores
+        idx2 = torch.full((BATCH, HKV, BUDGET), -7, dtype=torch.int32, device=dev)
+        n_idx2 = torch.full((BATCH,), -1, dtype=torch.int32, device=dev)
+        sdout = torch.full((BATCH, HQ, D), SENT, dtype=torch.float32, device=dev)
+        B.select_draft(sc if idx_in is None else torch.ones_like(sc), self.ctx, self.params, self.qd,
+                       self.k, self.v, idx=idx2, n_idx=n_idx2, out=sdout)
         torch.cuda.synchronize()
-        return out, sc, idx, n_idx, dout, rout, ent, am
+        return out, sc, idx, n_idx, dout, rout, ent, am, idx2, n_idx2, sdout
 
 
 def test_plans_use_the_exchanging_schedules():
     x = Inputs()
     s = B.verify_shape(x.q, x.k)
     assert B.verify_plan(s, x.params, x.ctx, x.ql)[0] == B.VERIFY_ONE_SWEEP
-    assert B.select_plan(s, x.params, x.ctx)[0] is True
+    one_kernel, part, _ = B.select_plan(s, x.params, x.ctx)
+    assert one_kernel is True and part <= 4096   # select_draft drafts inside the select kernel
 
 
 def test_status_stays_clear_on_normal_calls():
@@ -97,7 +104,7 @@ def test_every_wait_gives_up_and_every_kernel_finishes():
     assert B.exchange_status() == 0
     idx_good = good[2]
     B.test_exchange_faults(64, True)
-    out, sc, idx, n_idx, dout, rout, ent, am = x.run()
+    out, sc, idx, n_idx, dout, rout, ent, am, idx2, n_idx2, sdout = x.run()
     flags = B.exchange_status()
     B.test_exchange_faults(0, False)
     assert flags == ALL, f"status {flags:#x}, expected {ALL:#x}"
@@ -105,6 +112,7 @@ def test_every_wait_gives_up_and_every_kernel_finishes():
     assert torch.all(out == SENT) and torch.all(sc == SENT)
     assert torch.all(idx == -7) and torch.all(n_idx == -1)
     assert torch.all(dout == SENT) and torch.all(rout == SENT)
+    assert torch.all(idx2 == -7) and torch.all(n_idx2 == -1) and torch.all(sdout == SENT)
     # the draft kernels on a valid index set give up the same way
     out2 = x.run(idx_in=idx_good)
     B.test_exchange_faults(0, False)

@@ -1,7 +1,7 @@
 """Calls captured in a HIP graph and replayed with new contents in the
 captured input buffers.  Each replay must equal the eager calls on the same
 inputs, bit for bit: the kernels are deterministic (fixed merge orders, no
-floating-point atomics).  Verify (one sweep), select, draft, a draft-round step
+floating-point atomics).  Verify (one sweep), select with the first draft step, a draft-round step
 and the logit statistics exchange partial results between workgroups behind
 tags, and a replay reuses the call tag fixed at capture; the workspace epochs
 must give every replay a new one, or a replay could take the previous
@@ -77,7 +77,8 @@ def test_graph_replays_match_eager_calls():
 
         out_e, scores_e = B.verify_attn(q, k, v, ctx, ql, params)
         idx_e, n_idx_e = B.select_topb(scores_e, ctx, params)
-        dout_e = B.draft_attn(qd, k, v, idx_e, [n_idx_host], params)
+        # the step's select and first draft step run as one call
+        _, _, dout_e = B.select_draft(scores_e, ctx, params, qd, k, v)
         rout_e = torch.empty_like(rout)
         B.PreparedRound(qd, k, v, idx_e, ctx, K_ROUND, params, rout_e).step(ROUND_STEP)
         ent_e, am_e = B.logit_stats(logits)
@@ -99,7 +100,7 @@ def test_graph_replays_match_eager_calls():
 
 def test_graph_with_one_shared_workspace():
     """verify -> select (three kernels: more than 256 partitions) -> draft
-    captured with ONE workspace for the three calls, replayed with new inputs.
+    captured with ONE workspace for the calls, replayed with new inputs.
     Every layout keeps its exchange epochs in the same leading words, so the
     select histograms never land on the draft's epochs."""
     dev = torch.device("cuda:0")
@@ -140,7 +141,9 @@ def test_graph_with_one_shared_workspace():
         torch.cuda.synchronize()
         out_e, scores_e = B.verify_attn(q, k, v, ctx, ql, params)
         idx_e, n_idx_e = B.select_topb(scores_e, ctx, params)
-        dout_e = B.draft_attn(qd, k, v, idx_e, [n_idx_host] * batch, params)
+        _, _, dout_e = B.select_draft(scores_e, ctx, params, qd, k, v)
+        # (select runs as three kernels here, so the draft is the plain draft call)
+        assert torch.equal(dout_e, B.draft_attn(qd, k, v, idx_e, [n_idx_host] * batch, params))
         torch.cuda.synchronize()
         assert torch.equal(out, out_e), f"replay {r}: verify output"
         assert torch.equal(scores[:, :, :t], scores_e[:, :, :t]), f"replay {r}: scores"

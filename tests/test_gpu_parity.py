@@ -14,8 +14,8 @@ import torch
 
 import oracle
 from gpu_common import (Dev, abs_v, check_band, check_index_structure, check_outputs,
-                        check_score_mass, check_scores, gpu_draft, gpu_select, gpu_verify,
-                        params_of)
+                        check_score_mass, check_scores, gpu_draft, gpu_select, gpu_select_draft,
+                        gpu_verify, params_of)
 from paper_2607_27735_amd import binding as B
 from paper_2607_27735_amd.workloads import f32_to_bf16_bits, generate, make_config
 
@@ -188,6 +188,51 @@ def test_draft_wide_workgroups(name, cus):
     finally:
         B.set_cu_budget(0)
     check_outputs(o, o_ref, oabs, np.ones(o_ref.shape[:2], dtype=bool), what="draft")
+
+
+def _check_select_draft(w, s32, budget=None, k_sink=None, k_recent=None, out_fp32=True):
+    """ssl_select_draft against the oracle: index sets bit-exact with the
+    oracle's select on the same fp32 scores, the draft over them at the draft
+    bar, slots past n_idx untouched."""
+    budget = w.budget if budget is None else budget
+    ks = w.k_sink if k_sink is None else k_sink
+    kr = w.k_recent if k_recent is None else k_recent
+    idx_ref, n_ref = oracle.select(w, s32.astype(np.float64), budget=budget, k_sink=ks,
+                                   k_recent=kr)
+    idx, n_idx, o = gpu_select_draft(Dev(w), s32, out_fp32=out_fp32, budget=budget, k_sink=ks,
+                                     k_recent=kr)
+    assert np.array_equal(n_idx, n_ref)
+    for b in range(w.batch):
+        assert np.array_equal(idx[b, :, :n_ref[b]], idx_ref[b, :, :n_ref[b]])
+    check_index_structure(idx, n_idx, w.ctx_len, ks, kr, budget)
+    idx_dev = np.where(idx_ref < 0, 0, idx_ref).astype(np.int32)
+    o_ref = oracle.draft(w, idx_dev, n_ref)
+    oabs = oracle.draft(w, idx_dev, n_ref, v=abs_v(w))
+    check_outputs(o, o_ref, oabs, np.ones(o_ref.shape[:2], dtype=bool), out_fp32=out_fp32,
+                  what="select+draft")
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_select_draft_matches_oracle(name):
+    w, out_ref, s_ref, oabs_ref = small_case(name)
+    _check_select_draft(w, s_ref.astype(np.float32))
+
+
+def test_select_draft_special_cases():
+    """Units that need no radix select (every middle position taken, or none)
+    run the draft over ranges; ties, zeros and one huge score."""
+    w = generate(205, name="seldraft", batch=2, n_q_heads=8, n_kv_heads=2, ctx_len=[3000, 2500],
+                 q_len=[1, 1], budget=300)
+    rng = np.random.default_rng(9)
+    shape = (w.batch, w.n_kv_heads, w.max_ctx)
+    for label, s32 in {"random": rng.random(shape).astype(np.float32),
+                       "quantized-ties": (rng.integers(0, 5, shape) / 4.0).astype(np.float32),
+                       "all-zero": np.zeros(shape, np.float32),
+                       "one-huge": np.where(rng.random(shape) < 0.001, 1e30, 1e-3).astype(np.float32)
+                       }.items():
+        for budget, ks, kr in [(300, 4, 32), (3000, 4, 32), (64, 64, 0), (10, 0, 10), (36, 4, 32)]:
+            print(f"[select+draft] {label} budget {budget} sink {ks} recent {kr}", flush=True)
+            _check_select_draft(w, s32, budget=budget, k_sink=ks, k_recent=kr)
 
 
 def test_select_special_cases():
@@ -371,6 +416,9 @@ def test_workload_full_size(n):
         got = sum(int(p) in set(idx_e[b, c, :n_e[b]].tolist())
                   for b in range(w.batch) for c in range(w.n_kv_heads) for p in hp[b, c])
         print(f"  planted heavy hitters selected: {got}/{hp.size}")
+
+    # select and the first draft step in one call (the benchmark's step)
+    _check_select_draft(w, s32, out_fp32=False)
 
     # draft on the oracle's index sets, all heads
     idx_dev = np.where(idx_ref < 0, 0, idx_ref).astype(np.int32)

@@ -83,6 +83,15 @@ def test_per_head_select_and_draft(name):
     torch.cuda.synchronize()
     check_outputs(o.float().cpu().numpy().astype(np.float64), o_ref, oa,
                   np.ones(o_ref.shape[:2], dtype=bool), what="per-head draft")
+    # select and the first draft step in one call, over the per-head scores
+    idx2, n2, o2 = B.select_draft(torch.from_numpy(s32).cuda(), w.ctx_len, p, d.qd, d.k, d.v)
+    torch.cuda.synchronize()
+    idx2, n2 = idx2.cpu().numpy(), n2.cpu().numpy()
+    assert np.array_equal(n2, n_ref)
+    for b in range(w.batch):
+        assert np.array_equal(idx2[b, :, :n_ref[b]], idx_ref[b, :, :n_ref[b]])
+    check_outputs(o2.float().cpu().numpy().astype(np.float64), o_ref, oa,
+                  np.ones(o_ref.shape[:2], dtype=bool), what="per-head select_draft")
 
 
 def test_per_head_limits():
