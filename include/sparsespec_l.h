@@ -100,7 +100,7 @@ enum {
     SSL_ERR_BUDGET = -4,      /* budget < 1, k_sink/k_recent < 0 or k_sink + k_recent > budget */
     SSL_ERR_ALIGN = -5,       /* device pointer not 16-byte (tensors) / 4-byte (int, fp32) aligned */
     SSL_ERR_WORKSPACE = -6,   /* workspace NULL or smaller than required */
-    SSL_ERR_HIP = -7          /* a HIP launch failed (hipGetLastError after the launches) */
+    SSL_ERR_HIP = -7          /* a HIP call failed (ssl_last_hip_error names it) */
 };
 
 typedef struct {
@@ -173,6 +173,10 @@ enum {
  * running may be reported by a later read.  Errors: SSL_ERR_NULL,
  * SSL_ERR_HIP. */
 int ssl_exchange_status(hipStream_t stream, uint32_t *flags_out);
+
+/* The name of the HIP error (hipGetErrorName) behind the calling thread's
+ * last SSL_ERR_HIP; "hipSuccess" if it has had none.  A static string. */
+const char *ssl_last_hip_error(void);
 
 /* The CU count that verify and select plans count on (process-wide; 0, the
  * default, uses the device's own count).  A caller that runs other kernels
@@ -335,6 +339,38 @@ int ssl_select_draft(const ssl_shape *shape, const ssl_params *params,
                      int32_t *n_idx, const void *q_draft, const void *k_cache,
                      const void *v_cache, void *out, void *workspace, size_t workspace_bytes,
                      hipStream_t stream);
+
+/*
+ * One decode step of the hot path in one call (Sec. 3.1: verify the drafted
+ * tokens against the dense cache; Sec. 3.2: Eq. 3 scores from that pass, the
+ * Eq. 4 recallable set, the Eq. 5 sparse draft step over it):
+ * ssl_verify_attn, then ssl_select_draft on the scores it writes, with the
+ * arguments and results of those two calls (q_draft, draft_out and idx/n_idx
+ * as there; draft_out has the verify output's dtype).  Where verify takes one
+ * sweep (ssl_verify_plan) in a single round of workgroups (every chunk of the
+ * call resident at once) with chunks of at least 512 keys, params->per_head
+ * is 0 and a KV head has at most 16 query heads, ONE kernel runs the whole
+ * step: every chunk workgroup of a
+ * (sequence, KV head) is also that unit's select partition over the scores it
+ * has just computed and drafts over the rows it selected, so neither the
+ * scores nor the index sets are read back.  Otherwise the calls run one after
+ * the other on `stream`.  ssl_decode_step_plan reports which (one_kernel_out
+ * = 1 or 0).  The workspace size comes from ssl_decode_step_workspace.
+ * Errors: those of the two calls.  When an exchange gives up, the status word
+ * holds SSL_EXCHANGE_VERIFY or SSL_EXCHANGE_SELECT and the outputs that
+ * depended on it are not written (see ssl_select_draft for the two-call form).
+ */
+int ssl_decode_step_workspace(const ssl_shape *shape, const ssl_params *params,
+                              const int32_t *ctx_len_host, const int32_t *q_len_host,
+                              size_t *bytes_out);
+int ssl_decode_step_plan(const ssl_shape *shape, const ssl_params *params,
+                         const int32_t *ctx_len_host, const int32_t *q_len_host,
+                         int32_t *one_kernel_out);
+int ssl_decode_step(const ssl_shape *shape, const ssl_params *params, const int32_t *ctx_len_host,
+                    const int32_t *q_len_host, const void *q, const void *k_cache,
+                    const void *v_cache, void *out, float *scores, int32_t *idx, int32_t *n_idx,
+                    const void *q_draft, void *draft_out, void *workspace, size_t workspace_bytes,
+                    hipStream_t stream);
 
 /*
  * Paged KV cache, as serving engines keep it: the same calls with K and V in

@@ -32,11 +32,12 @@ VERIFY_TWO_SWEEP = 1
 VERIFY_ONE_SWEEP = 2
 
 EXPORTED = [
-    "ssl_status_string", "ssl_build_id", "ssl_exchange_status", "ssl_set_cu_budget",
+    "ssl_status_string", "ssl_build_id", "ssl_exchange_status", "ssl_last_hip_error",
+    "ssl_set_cu_budget",
     "ssl_test_exchange_faults", "ssl_index_count",
     "ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn", "ssl_verify_attn_static",
     "ssl_select_workspace", "ssl_select_plan", "ssl_select_topb", "ssl_select_draft_workspace",
-    "ssl_select_draft",
+    "ssl_select_draft", "ssl_decode_step_workspace", "ssl_decode_step_plan", "ssl_decode_step",
     "ssl_draft_workspace", "ssl_draft_attn",
     "ssl_verify_attn_paged", "ssl_draft_attn_paged",
     "ssl_draft_materialize", "ssl_draft_step_workspace", "ssl_draft_step",
@@ -63,7 +64,10 @@ class Params(ctypes.Structure):
 class SSLError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
-        super().__init__(f"{where}: {status_string(status)} (status {status})")
+        msg = f"{where}: {status_string(status)} (status {status})"
+        if status == SSL_ERR_HIP and _lib is not None:
+            msg += f": {_lib.ssl_last_hip_error().decode()}"
+        super().__init__(msg)
 
 
 _lib = None
@@ -95,6 +99,8 @@ def load(path: Optional[str] = None):
     sp, pp = ctypes.POINTER(Shape), ctypes.POINTER(Params)
     lib.ssl_status_string.argtypes = [ctypes.c_int]
     lib.ssl_status_string.restype = ctypes.c_char_p
+    lib.ssl_last_hip_error.argtypes = []
+    lib.ssl_last_hip_error.restype = ctypes.c_char_p
     lib.ssl_exchange_status.argtypes = [_vp, ctypes.POINTER(ctypes.c_uint32)]
     lib.ssl_exchange_status.restype = ctypes.c_int
     lib.ssl_set_cu_budget.argtypes = [ctypes.c_int32]
@@ -112,6 +118,9 @@ def load(path: Optional[str] = None):
     lib.ssl_select_draft_workspace.argtypes = [sp, pp, _i32p, _szp]
     lib.ssl_select_draft.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
     lib.ssl_select_topb.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _sz, _vp]
+    lib.ssl_decode_step_workspace.argtypes = [sp, pp, _i32p, _i32p, _szp]
+    lib.ssl_decode_step_plan.argtypes = [sp, pp, _i32p, _i32p, _i32p]
+    lib.ssl_decode_step.argtypes = [sp, pp, _i32p, _i32p] + [_vp] * 10 + [_sz, _vp]
     lib.ssl_draft_workspace.argtypes = [sp, pp, _i32p, _szp]
     lib.ssl_draft_attn.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
     lib.ssl_draft_materialize.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _vp, _vp]
@@ -403,6 +412,82 @@ def select_draft(scores: torch.Tensor, ctx_len, params: Params, q_draft: torch.T
                                    workspace.numel(), _stream(stream)),
            "ssl_select_draft")
     return idx, n_idx, out
+
+
+# ---------------------------------------------------------------------------
+# the whole decode step
+# ---------------------------------------------------------------------------
+
+def decode_step_workspace_bytes(shape: Shape, params: Params, ctx_len, q_len) -> int:
+    ctx, ql = _host_i32(ctx_len), _host_i32(q_len)
+    n = ctypes.c_size_t(0)
+    _check(load().ssl_decode_step_workspace(ctypes.byref(shape), ctypes.byref(params),
+                                            ctx.ctypes.data_as(_i32p), ql.ctypes.data_as(_i32p),
+                                            ctypes.byref(n)), "ssl_decode_step_workspace")
+    return int(n.value)
+
+
+def decode_step_plan(shape: Shape, params: Params, ctx_len, q_len) -> bool:
+    """Whether decode_step runs as one kernel."""
+    ctx, ql = _host_i32(ctx_len), _host_i32(q_len)
+    one = ctypes.c_int32(0)
+    _check(load().ssl_decode_step_plan(ctypes.byref(shape), ctypes.byref(params),
+                                       ctx.ctypes.data_as(_i32p), ql.ctypes.data_as(_i32p),
+                                       ctypes.byref(one)), "ssl_decode_step_plan")
+    return bool(one.value)
+
+
+def decode_step(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, q_draft: torch.Tensor, ctx_len,
+                q_len, params: Params, out: Optional[torch.Tensor] = None,
+                scores: Optional[torch.Tensor] = None, idx: Optional[torch.Tensor] = None,
+                n_idx: Optional[torch.Tensor] = None, draft_out: Optional[torch.Tensor] = None,
+                workspace: Optional[torch.Tensor] = None, stream=None):
+    """Verify (+ Eq. 3 scores), Eq. 4 select and the first Eq. 5 draft step
+    in one call; returns (out, scores, idx, n_idx, draft_out)."""
+    _need_gpu(q, k, v, q_draft)
+    if any(t.dtype != torch.bfloat16 for t in (q, k, v, q_draft)):
+        raise TypeError("q, k, v, q_draft must be bfloat16")
+    if k.shape != v.shape or q.shape[0] != k.shape[0] or q.shape[3] != k.shape[3]:
+        raise ValueError("q/k/v shapes disagree")
+    shape = verify_shape(q, k)
+    if tuple(q_draft.shape) != (shape.batch, shape.n_q_heads, shape.head_dim):
+        raise ValueError("q_draft must be [batch, n_q_heads, 128]")
+    ctx, ql = _host_i32(ctx_len), _host_i32(q_len)
+    if len(ctx) != shape.batch or len(ql) != shape.batch:
+        raise ValueError("ctx_len / q_len need one entry per sequence")
+    units = shape.n_q_heads if params.per_head else shape.n_kv_heads   # score rows, index sets
+    dev = q.device
+    odt = torch.float32 if params.out_fp32 else torch.bfloat16
+    if out is None:
+        out = torch.zeros(q.shape, dtype=odt, device=dev)
+    if scores is None:
+        scores = torch.zeros((shape.batch, units, shape.max_ctx), dtype=torch.float32, device=dev)
+    if idx is None:
+        idx = torch.empty((shape.batch, units, params.budget), dtype=torch.int32, device=dev)
+    if n_idx is None:
+        n_idx = torch.empty(shape.batch, dtype=torch.int32, device=dev)
+    if draft_out is None:
+        draft_out = torch.empty(q_draft.shape, dtype=odt, device=dev)
+    _need_gpu(out, scores, idx, n_idx, draft_out)
+    if out.dtype != odt or draft_out.dtype != odt or scores.dtype != torch.float32:
+        raise TypeError("out/draft_out dtype must match params.out_fp32; scores must be float32")
+    if idx.dtype != torch.int32 or n_idx.dtype != torch.int32:
+        raise TypeError("idx and n_idx must be int32")
+    if (out.shape != q.shape or draft_out.shape != q_draft.shape
+            or scores.shape != (shape.batch, units, shape.max_ctx)
+            or idx.shape != (shape.batch, units, params.budget)
+            or n_idx.shape != (shape.batch,)):
+        raise ValueError("output shapes")
+    need = decode_step_workspace_bytes(shape, params, ctx, ql)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    _check(load().ssl_decode_step(ctypes.byref(shape), ctypes.byref(params),
+                                  ctx.ctypes.data_as(_i32p), ql.ctypes.data_as(_i32p), _ptr(q),
+                                  _ptr(k), _ptr(v), _ptr(out), _ptr(scores), _ptr(idx),
+                                  _ptr(n_idx), _ptr(q_draft), _ptr(draft_out), _ptr(workspace),
+                                  workspace.numel(), _stream(stream)),
+           "ssl_decode_step")
+    return out, scores, idx, n_idx, draft_out
 
 
 # ---------------------------------------------------------------------------
@@ -735,9 +820,10 @@ class Controller:
 class PreparedStep:
     """One verify + select + draft step over fixed device buffers.
 
-    All argument structures are built once, so each ``verify()`` /
-    ``select()`` / ``draft()`` is one ctypes call into the library on the
-    stream given (default: torch's current stream at construction).
+    All argument structures are built once, so ``step()`` (the whole step,
+    ssl_decode_step) and each ``verify()`` / ``select()`` / ``draft()`` /
+    ``select_draft()`` is one ctypes call into the library on the stream
+    given (default: torch's current stream at construction).
     """
 
     def __init__(self, q, k, v, q_draft, ctx_len, q_len, params: Params, out, scores, idx, n_idx,
@@ -756,13 +842,18 @@ class PreparedStep:
         sws = max(select_workspace_bytes(self.shape, params, self.ctx),
                   select_draft_workspace_bytes(self.dshape, params, self.ctx))
         dws = draft_workspace_bytes(self.dshape, params, self.n_idx_host)
-        if shared_workspace:   # one buffer for the three calls, ordered on one stream
-            self.vws = torch.empty(max(vws, sws, dws, 1), dtype=torch.uint8, device=q.device)
-            self.sws = self.dws = self.vws
+        # the one-call step has a workspace of its own (with shared_workspace
+        # the three-call form's buffer, made large enough)
+        stws = decode_step_workspace_bytes(self.shape, params, self.ctx, self.ql)
+        if shared_workspace:   # one buffer for every call, ordered on one stream
+            self.vws = torch.empty(max(vws, sws, dws, stws, 1), dtype=torch.uint8, device=q.device)
+            self.sws = self.dws = self.stws = self.vws
         else:
             self.vws = torch.empty(max(vws, 1), dtype=torch.uint8, device=q.device)
             self.sws = torch.empty(max(sws, 1), dtype=torch.uint8, device=q.device)
             self.dws = torch.empty(max(dws, 1), dtype=torch.uint8, device=q.device)
+            self.stws = torch.empty(max(stws, 1), dtype=torch.uint8, device=q.device)
+        self.one_kernel = decode_step_plan(self.shape, params, self.ctx, self.ql)
         self.tensors = (q, k, v, q_draft, out, scores, idx, n_idx, draft_out)
         self.stream = _stream(stream)
         sp, pp = ctypes.byref(self.shape), ctypes.byref(params)
@@ -777,6 +868,9 @@ class PreparedStep:
         self._sd = (ctypes.byref(self.dshape), pp, cp, scores.data_ptr(), idx.data_ptr(),
                     n_idx.data_ptr(), q_draft.data_ptr(), k.data_ptr(), v.data_ptr(),
                     draft_out.data_ptr(), self.sws.data_ptr(), self.sws.numel(), self.stream)
+        self._st = (sp, pp, cp, qp, q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                    scores.data_ptr(), idx.data_ptr(), n_idx.data_ptr(), q_draft.data_ptr(),
+                    draft_out.data_ptr(), self.stws.data_ptr(), self.stws.numel(), self.stream)
 
     def verify(self) -> None:
         _check(self._lib.ssl_verify_attn(*self._v), "ssl_verify_attn")
@@ -792,6 +886,11 @@ class PreparedStep:
         _check(self._lib.ssl_select_draft(*self._sd), "ssl_select_draft")
 
     def step(self) -> None:
+        """The whole step in one call (ssl_decode_step)."""
+        _check(self._lib.ssl_decode_step(*self._st), "ssl_decode_step")
+
+    def step_two_calls(self) -> None:
+        """The same step as verify, then select_draft."""
         self.verify()
         self.select_draft()
 

@@ -27,6 +27,16 @@ constexpr int kDraftRowCap = 16;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+// The HIP error behind this thread's last SSL_ERR_HIP (ssl_last_hip_error).
+thread_local hipError_t t_last_hip = hipSuccess;
+
+// SSL_OK for hipSuccess; otherwise records e and returns SSL_ERR_HIP.
+int hip_rc(hipError_t e) {
+    if (e == hipSuccess) return SSL_OK;
+    t_last_hip = e;
+    return SSL_ERR_HIP;
+}
+
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 int check_shape(const ssl_shape* s) {
@@ -61,7 +71,7 @@ ssl_shape unit_shape(const ssl_shape* s, const ssl_params* p) {
 // outputs for whichever schedule needs more, plus the one-sweep tags.
 constexpr int kFusedMaxSlotsPerUnit = 128;
 
-// A 64-bit mixing function (the finaliser of Steele et al.'s splitmix64).
+// A 64-bit mixing function (the 64-bit finaliser of Appleby's MurmurHash3).
 uint64_t mix64(uint64_t x) {
     x ^= x >> 33;
     x *= 0xff51afd7ed558ccdull;
@@ -111,7 +121,7 @@ std::atomic<uint64_t> g_tag_flip{0};
 // is looked up once per device).
 int make_exchange(Exchange* xc) {
     uint32_t* word = nullptr;
-    if (exchange_status_word(&word) != hipSuccess) return SSL_ERR_HIP;
+    if (const int hip_st = hip_rc(exchange_status_word(&word))) return hip_st;
     xc->status = word;
     xc->tag_flip = g_tag_flip.load(std::memory_order_relaxed);
     const int32_t lim = g_spin_limit.load(std::memory_order_relaxed);
@@ -379,7 +389,7 @@ int plan_select(const ssl_shape* s, const int32_t* ctx, SelectPlan* plan) {
     plan->mask_off = plan->thr_off + align_up(units * 2 * sizeof(uint32_t));
     plan->seg_off = plan->mask_off + align_up(slots * (plan->part / 32) * sizeof(uint32_t));
     plan->tag_off = plan->seg_off + align_up(slots * plan->part * 2 * sizeof(uint32_t));
-    plan->bytes = plan->tag_off + align_up(slots * 4 * sizeof(uint64_t));
+    plan->bytes = plan->tag_off + align_up(slots * kSelectTagWords * sizeof(uint64_t));
     return SSL_OK;
 }
 
@@ -403,7 +413,7 @@ const char* ssl_status_string(int status) {
         case SSL_ERR_BUDGET: return "invalid budget: need budget >= 1, k_sink, k_recent >= 0, k_sink + k_recent <= budget";
         case SSL_ERR_ALIGN: return "device pointer is not suitably aligned";
         case SSL_ERR_WORKSPACE: return "workspace missing or too small";
-        case SSL_ERR_HIP: return "HIP kernel launch failed";
+        case SSL_ERR_HIP: return "a HIP call failed (ssl_last_hip_error names it)";
         default: return "unknown status";
     }
 }
@@ -417,13 +427,15 @@ const char* ssl_build_id(void) { return SSL_BUILD_ID; }
 int ssl_exchange_status(hipStream_t stream, uint32_t* flags_out) {
     if (!flags_out) return SSL_ERR_NULL;
     hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
-    if (hipStreamIsCapturing(stream, &st) != hipSuccess) {
+    if (const int hip_st = hip_rc(hipStreamIsCapturing(stream, &st))) {
         (void)hipGetLastError();
-        return SSL_ERR_HIP;
+        return hip_st;
     }
     if (st != hipStreamCaptureStatusNone) return SSL_ERR_UNSUPPORTED;
-    return take_exchange_status(stream, flags_out) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
+    return hip_rc(take_exchange_status(stream, flags_out));
 }
+
+const char* ssl_last_hip_error(void) { return hipGetErrorName(t_last_hip); }
 
 int ssl_set_cu_budget(int32_t n_cu) {
     if (n_cu < 0) return SSL_ERR_SHAPE;
@@ -508,7 +520,7 @@ int verify_call(const ssl_shape* shape, const ssl_params* params, const int32_t*
         // the library's static scratch: refuse what it cannot hold, then (the
         // arguments all checked) look up its address on this device
         if (plan.bytes > scratch->bytes) return SSL_ERR_WORKSPACE;
-        if (scratch->address(&workspace) != hipSuccess) return SSL_ERR_HIP;
+        if (const int hip_st = hip_rc(scratch->address(&workspace))) return hip_st;
         workspace_bytes = scratch->bytes;
     }
     rc = check_workspace(workspace, workspace_bytes, plan.bytes);
@@ -548,7 +560,7 @@ int verify_call(const ssl_shape* shape, const ssl_params* params, const int32_t*
         if (g > 16 || (g & (g - 1)) != 0) return SSL_ERR_UNSUPPORTED;
     }
     if (use_one_sweep(plan, params)) {
-        FusedArgs fa;
+        FusedArgs fa = {};
         fa.v = a;
         fa.v.chunk = plan.fused_chunk;
         fa.v.seq = plan.fseq;
@@ -563,15 +575,10 @@ int verify_call(const ssl_shape* shape, const ssl_params* params, const int32_t*
         // lifting the mark a captured call that gave up may have left there.
         fa.heal = scratch && !fa.epoch ? static_cast<uint64_t*>(workspace) : nullptr;
         fa.heal_value = mix64(fa.call_tag);
-        return launch_verify_fused(fa, plan.fused_slots, plan.row_tiles, stream) ==
-                       hipSuccess
-                   ? SSL_OK
-                   : SSL_ERR_HIP;
+        return hip_rc(launch_verify_fused(fa, plan.fused_slots, plan.row_tiles, stream));
     }
     if (plan.block_pos >= shape->max_q)
-        return launch_verify(a, plan.n_items, plan.n_rows, plan.row_tiles, stream) == hipSuccess
-                   ? SSL_OK
-                   : SSL_ERR_HIP;
+        return hip_rc(launch_verify(a, plan.n_items, plan.n_rows, plan.row_tiles, stream));
     // Row blocks, the last positions of every sequence first (that block has
     // all sequences, so it writes every score; later blocks add theirs).  A
     // block's table holds only the sequences that still have positions.
@@ -602,8 +609,7 @@ int verify_call(const ssl_shape* shape, const ssl_params* params, const int32_t*
         blk.seq.item_start[n] = (int32_t)items;
         blk.seq.row_start[n] = (int32_t)rows;
         blk.score_add = k > 0 ? 1 : 0;
-        if (launch_verify(blk, (int)items, (int)rows, plan.row_tiles, stream) != hipSuccess)
-            return SSL_ERR_HIP;
+        if (const int hip_st = hip_rc(launch_verify(blk, (int)items, (int)rows, plan.row_tiles, stream))) return hip_st;
     }
     return SSL_OK;
 }
@@ -702,7 +708,7 @@ int select_call(const ssl_shape* shape, const ssl_params* params, const int32_t*
         a.d.out_fp32 = params->out_fp32 ? 1 : 0;
         a.d.scale_log2 = params->sm_scale * 1.4426950408889634f;
     }
-    return launch_select(a, (int)units, stream) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
+    return hip_rc(launch_select(a, (int)units, stream));
 }
 
 }  // namespace
@@ -832,7 +838,7 @@ int draft_call(const ssl_shape* shape, const ssl_params* params, const int32_t* 
     a.block_table = block_table;
     a.page_size = page_size;
     a.max_blocks = max_blocks;
-    return launch_draft(a, plan.n_items, stream) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
+    return hip_rc(launch_draft(a, plan.n_items, stream));
 }
 
 }  // namespace
@@ -917,6 +923,179 @@ int ssl_select_draft(const ssl_shape* shape, const ssl_params* params, const int
                       workspace, workspace_bytes, stream);
 }
 
+}  // extern "C"
+
+namespace {
+
+// The whole decode step: one kernel where verify takes one sweep (then every
+// chunk workgroup of a unit is also a select partition and drafts over its
+// selections), else verify, then select_draft, on one workspace.
+struct DecodePlan {
+    VerifyPlan v;
+    bool one_kernel;
+    int parts;   // chunks of the longest context: the select arrays' partition stride
+    size_t hist_off, seg_off, tag_off, part_off, bytes;
+};
+
+int plan_decode(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, const int32_t* ql,
+                DecodePlan* plan) {
+    int rc = plan_verify(s, p, ctx, ql, &plan->v);
+    if (rc) return rc;
+    ssl_shape ds = *s;
+    ds.max_q = 1;
+    SelectPlan sp;
+    bool sd_fused = false;
+    int32_t n_idx_host[kTableBatch];
+    size_t sd_bytes = 0;
+    rc = select_draft_plan(&ds, p, ctx, &sp, &sd_fused, n_idx_host, &sd_bytes);
+    if (rc) return rc;
+    // One kernel only when every chunk workgroup of the call is resident at
+    // once (with more, later units wait behind earlier units' select and
+    // draft exchanges instead of streaming: measured far slower) and chunks
+    // hold at least kStepMinChunk keys (smaller chunks make many small select
+    // partitions, whose exchanges measured slower than select's own).
+    constexpr int kStepMinChunk = 512;
+    const int g = s->n_q_heads / s->n_kv_heads;
+    const int64_t resident = (int64_t)device_cus() * std::max(fused_blocks_per_cu(plan->v.row_tiles), 1);
+    plan->one_kernel = use_one_sweep(plan->v, p) && !p->per_head && g <= 16 &&
+                       plan->v.fused_slots <= resident && plan->v.fused_chunk >= kStepMinChunk;
+    if (!plan->one_kernel) {
+        plan->parts = 0;
+        plan->hist_off = plan->seg_off = plan->tag_off = plan->part_off = 0;
+        plan->bytes = std::max(plan->v.bytes, sd_bytes);
+        return SSL_OK;
+    }
+    const int chunk = plan->v.fused_chunk;
+    int max_t = 0;
+    for (int b = 0; b < s->batch; ++b) max_t = std::max(max_t, ctx[b]);
+    plan->parts = (max_t + chunk - 1) / chunk;
+    const size_t slots = (size_t)s->batch * s->n_kv_heads * plan->parts;
+    plan->hist_off = align_up(plan->v.bytes);
+    plan->seg_off = plan->hist_off + align_up(slots * kHistSlotWords * sizeof(uint32_t));
+    plan->tag_off = plan->seg_off + align_up(slots * chunk * 2 * sizeof(uint32_t));
+    plan->part_off = plan->tag_off + align_up(slots * kSelectTagWords * sizeof(uint64_t));
+    plan->bytes = plan->part_off + align_up(slots * 16 * kSelectDraftStride * sizeof(float));
+    return SSL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ssl_decode_step_workspace(const ssl_shape* shape, const ssl_params* params,
+                              const int32_t* ctx_len_host, const int32_t* q_len_host,
+                              size_t* bytes_out) {
+    if (!bytes_out) return SSL_ERR_NULL;
+    DecodePlan plan;
+    const int rc = plan_decode(shape, params, ctx_len_host, q_len_host, &plan);
+    if (rc) return rc;
+    *bytes_out = plan.bytes;
+    return SSL_OK;
+}
+
+int ssl_decode_step_plan(const ssl_shape* shape, const ssl_params* params,
+                         const int32_t* ctx_len_host, const int32_t* q_len_host,
+                         int32_t* one_kernel_out) {
+    if (!one_kernel_out) return SSL_ERR_NULL;
+    DecodePlan plan;
+    const int rc = plan_decode(shape, params, ctx_len_host, q_len_host, &plan);
+    if (rc) return rc;
+    *one_kernel_out = plan.one_kernel ? 1 : 0;
+    return SSL_OK;
+}
+
+int ssl_decode_step(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
+                    const int32_t* q_len_host, const void* q, const void* k_cache,
+                    const void* v_cache, void* out, float* scores, int32_t* idx, int32_t* n_idx,
+                    const void* q_draft, void* draft_out, void* workspace, size_t workspace_bytes,
+                    hipStream_t stream) {
+    DecodePlan plan;
+    int rc = plan_decode(shape, params, ctx_len_host, q_len_host, &plan);
+    if (rc) return rc;
+    if (!q || !k_cache || !v_cache || !out || !scores || !idx || !n_idx || !q_draft || !draft_out)
+        return SSL_ERR_NULL;
+    if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16) ||
+        !aligned(scores, 4) || !aligned(idx, 4) || !aligned(n_idx, 4) || !aligned(q_draft, 16) ||
+        !aligned(draft_out, 16))
+        return SSL_ERR_ALIGN;
+    rc = check_workspace(workspace, workspace_bytes, plan.bytes);
+    if (rc) return rc;
+    ssl_shape ds = *shape;
+    ds.max_q = 1;
+    if (!plan.one_kernel) {
+        rc = verify_call(shape, params, ctx_len_host, q_len_host, q, k_cache, v_cache, nullptr, 0, 0,
+                         out, scores, workspace, workspace_bytes, stream);
+        if (rc) return rc;
+        return ssl_select_draft(&ds, params, ctx_len_host, scores, idx, n_idx, q_draft, k_cache,
+                                v_cache, draft_out, workspace, workspace_bytes, stream);
+    }
+    char* ws = static_cast<char*>(workspace);
+    const VerifyPlan& vp = plan.v;
+    FusedArgs fa = {};
+    VerifyArgs& a = fa.v;
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k_cache);
+    a.v = static_cast<const uint16_t*>(v_cache);
+    a.part_ml = reinterpret_cast<float2*>(ws + vp.ml_off);
+    a.part_o = reinterpret_cast<float*>(ws + vp.o_off);
+    a.scores = scores;
+    a.out = out;
+    a.n_q_heads = shape->n_q_heads;
+    a.n_kv_heads = shape->n_kv_heads;
+    a.group = shape->n_q_heads / shape->n_kv_heads;
+    a.max_ctx = shape->max_ctx;
+    a.max_q = shape->max_q;
+    a.window = params->window;
+    a.chunk = vp.fused_chunk;
+    a.out_fp32 = params->out_fp32 ? 1 : 0;
+    a.scale_log2 = params->sm_scale * 1.4426950408889634f;
+    a.seq = vp.fseq;
+    for (int b = 0; b < shape->batch; ++b) {
+        a.sid[b] = b;
+        a.qfull[b] = q_len_host[b];
+    }
+    fa.tag = reinterpret_cast<uint64_t*>(ws + vp.tag_off);
+    const int64_t units = (int64_t)shape->batch * shape->n_kv_heads;
+    rc = epochs_if_captured(stream, workspace, units, &fa.epoch);
+    if (rc) return rc;
+    rc = make_exchange(&fa.xc);
+    if (rc) return rc;
+    fa.call_tag = next_call_tag();
+    fa.step = 1;
+    SelectArgs& sa = fa.sel;
+    sa.idx = idx;
+    sa.n_idx = n_idx;
+    sa.hist = reinterpret_cast<uint32_t*>(ws + plan.hist_off);
+    sa.seg = reinterpret_cast<uint2*>(ws + plan.seg_off);
+    sa.tag = reinterpret_cast<uint64_t*>(ws + plan.tag_off);
+    sa.epoch = fa.epoch;
+    sa.call_tag = fa.call_tag;
+    sa.xc = fa.xc;
+    sa.fused = 1;
+    sa.with_draft = 1;
+    sa.d.q = static_cast<const uint16_t*>(q_draft);
+    sa.d.k = a.k;
+    sa.d.v = a.v;
+    sa.d.out = draft_out;
+    sa.d.part = reinterpret_cast<float*>(ws + plan.part_off);
+    sa.d.n_q_heads = shape->n_q_heads;
+    sa.d.group = a.group;
+    sa.d.kv_div = 1;
+    sa.d.n_kv_real = shape->n_kv_heads;
+    sa.d.out_fp32 = a.out_fp32;
+    sa.d.scale_log2 = a.scale_log2;
+    sa.n_kv_heads = shape->n_kv_heads;
+    sa.max_ctx = shape->max_ctx;
+    sa.k_sink = params->k_sink;
+    sa.k_recent = params->k_recent;
+    sa.budget = params->budget;
+    sa.batch = shape->batch;
+    sa.part = vp.fused_chunk;
+    sa.parts = plan.parts;
+    for (int b = 0; b < shape->batch; ++b) sa.ctx[b] = ctx_len_host[b];
+    return hip_rc(launch_verify_fused(fa, vp.fused_slots, vp.row_tiles, stream));
+}
+
 int ssl_draft_materialize(const ssl_shape* shape, const ssl_params* params,
                           const int32_t* ctx_len_host, const void* k_cache, const void* v_cache,
                           const int32_t* idx, void* k_sel, void* v_sel, hipStream_t stream) {
@@ -943,10 +1122,7 @@ int ssl_draft_materialize(const ssl_shape* shape, const ssl_params* params,
     a.max_ctx = shape->max_ctx;
     a.budget = params->budget;
     for (int b = 0; b < shape->batch; ++b) a.n_fixed[b] = plan.n_fixed[b];
-    return launch_draft_materialize(a, plan.max_fixed, shape->batch * us.n_kv_heads,
-                                    stream) == hipSuccess
-               ? SSL_OK
-               : SSL_ERR_HIP;
+    return hip_rc(launch_draft_materialize(a, plan.max_fixed, shape->batch * us.n_kv_heads, stream));
 }
 
 int ssl_draft_step_workspace(const ssl_shape* shape, const ssl_params* params,
@@ -1015,7 +1191,7 @@ int ssl_draft_step(const ssl_shape* shape, const ssl_params* params, const int32
         a.n_fixed[b] = plan.n_fixed[b];
         a.win0[b] = plan.win0[b];
     }
-    return launch_draft_step(a, plan.d.n_items, stream) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
+    return hip_rc(launch_draft_step(a, plan.d.n_items, stream));
 }
 
 // ---- token statistics of logit rows ----------------------------------------
@@ -1085,7 +1261,7 @@ int ssl_logit_stats(const void* logits, int32_t dtype, int32_t n_rows, int32_t v
     if (rc) return rc;
     a.call_tag = next_call_tag();
     a.rows_per_seq = 0;
-    return launch_logit_stats(a, dtype == SSL_DT_F32, stream) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
+    return hip_rc(launch_logit_stats(a, dtype == SSL_DT_F32, stream));
 }
 
 int ssl_greedy_accept_workspace(int32_t batch, int32_t max_k, int32_t vocab, size_t* bytes_out) {
@@ -1137,7 +1313,7 @@ int ssl_greedy_accept(const void* logits, int32_t dtype, int32_t batch, int32_t 
     a.call_tag = next_call_tag();
     a.rows_per_seq = max_k + 1;
     for (int b = 0; b < batch; ++b) a.k_len[b] = k_len_host[b];
-    if (launch_logit_stats(a, dtype == SSL_DT_F32, stream) != hipSuccess) return SSL_ERR_HIP;
+    if (const int hip_st = hip_rc(launch_logit_stats(a, dtype == SSL_DT_F32, stream))) return hip_st;
     AcceptArgs c = {};
     c.argmax = a.argmax;
     c.draft = draft_tokens;
@@ -1145,7 +1321,7 @@ int ssl_greedy_accept(const void* logits, int32_t dtype, int32_t batch, int32_t 
     c.next_token = next_token;
     c.max_k = max_k;
     for (int b = 0; b < batch; ++b) c.k_len[b] = k_len_host[b];
-    return launch_greedy_accept(c, batch, stream) == hipSuccess ? SSL_OK : SSL_ERR_HIP;
+    return hip_rc(launch_greedy_accept(c, batch, stream));
 }
 
 }  // extern "C"

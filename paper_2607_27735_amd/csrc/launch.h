@@ -99,6 +99,8 @@ constexpr int kMaxSelectParts = 256;
 // 32-bit words per partition in SelectArgs::hist: a dense 2048-bin histogram
 // (three-kernel path) or up to 2048 tagged 64-bit bin entries (one kernel).
 constexpr int kHistSlotWords = 4096;
+// 64-bit tag words per partition in SelectArgs::tag.
+constexpr int kSelectTagWords = 4;
 
 // The first draft step over the index sets, run by the one-kernel select
 // (Eq. 5 with the rows each partition selected): per unit, query heads
@@ -124,7 +126,7 @@ struct SelectArgs {
     uint32_t* thr;      // [units][2]           threshold bin d1 and the count needed from it
     uint32_t* mask;     // [units][parts * part / 32] position bitmask
     uint2* seg;         // [units][parts][part] candidate (score bits, position)
-    uint64_t* tag;      // [units][parts][4] publication tags (no initialisation needed)
+    uint64_t* tag;      // [units][parts][kSelectTagWords] publication tags (no initialisation needed)
     uint64_t* epoch;    // [units] exchange epochs (any initial value), or null
     uint64_t call_tag;  // this call's tag: unique within the process (see exchange_tag)
     Exchange xc;
@@ -179,6 +181,13 @@ struct FusedArgs {
     // units to set to heal_value + unit at the end (null otherwise).
     uint64_t* heal;
     uint64_t heal_value;
+    // Whole decode step (step = 1): after its outputs and scores, each
+    // workgroup runs the one-kernel select as partition s (the chunk) of its
+    // unit over the scores it has just computed, and then the first draft
+    // step over its selections (sel.part = chunk, sel.parts = the most chunks
+    // of a unit, sel.with_draft = 1; same call tag, epochs and status word).
+    int32_t step;
+    SelectArgs sel;
 };
 
 // The library's static device scratch (the no-allocation entry point): its
@@ -193,7 +202,8 @@ struct StaticScratch {
 hipError_t launch_verify(const VerifyArgs& a, int n_items, int n_rows_total, int row_tiles,
                          hipStream_t stream);
 // Launches the single-sweep kernel over n_slots workgroups (it adds the
-// chunks of each row itself).  Returns the launch error.
+// chunks of each row itself; with a.step it also selects and drafts).
+// Returns the launch error.
 hipError_t launch_verify_fused(const FusedArgs& a, int n_slots, int row_tiles, hipStream_t stream);
 // The combine kernel alone: out[row] = sum of the row's normalised partials.
 hipError_t launch_verify_combine(const VerifyArgs& a, int n_rows_total, hipStream_t stream);

@@ -34,6 +34,7 @@
 #include <algorithm>
 #include <atomic>
 
+#include "select_common.h"
 #include "verify_common.h"
 
 namespace ssl {
@@ -160,7 +161,31 @@ __device__ __forceinline__ void fused_tile(const VerifyArgs& a, const Rows<NRT>&
     }
 }
 
-template <int NRT, bool kStream, bool kPaged>
+// The decode step's select (partition p of unit u): the keys in the select
+// layout from the chunk's score bits in skeys (LDS), then the one-kernel
+// select and draft step (select_common.h) with the stash as their LDS.
+template <int NR>
+__device__ __forceinline__ bool step_select(const SelectArgs& sa, const Geom& g, int p, int u,
+                                            const uint32_t* skeys, int nk, int key_begin,
+                                            SelLds& L, uint64_t want) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint32_t keys[4 * NR];
+#pragma unroll
+    for (int r = 0; r < NR; ++r)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int x = r * kRound + wave * 256 + e * 64 + lane;   // chunk-local position
+            const int pos = key_begin + x;
+            uint32_t v = x < nk ? skeys[x] : kNone;
+            v = v == 0x80000000u ? 0u : v;   // -0 ranks as +0, as select reads it
+            keys[4 * r + e] = (x < nk && pos >= g.s_end && pos < g.r_start) ? v : kNone;
+        }
+    __syncthreads();   // every key is read: the stash becomes the select's
+    select_local_hist<NR>(keys, L);
+    return select_partition<NR, true>(sa, g, p, u, keys, L, want);
+}
+
+template <int NRT, bool kStream, bool kPaged, bool kStep>
 __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     const VerifyArgs& a = fa.v;
     extern __shared__ __attribute__((aligned(16))) float stash[];   // [NRT*16][chunk + pad]
@@ -396,6 +421,9 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
                     if (k4 + i < nk) hrow[key_begin + k4 + i] = sc[i];
             }
         }
+        // (decode step: the chunk's score bits also go to skeys, in the
+        // parking slices, free since step 2)
+        uint32_t* skeys = reinterpret_cast<uint32_t*>(stash + NRT * 16 * stride + mts * (NRT * 16));
         for (int k4 = 4 * tid; !a.per_head && k4 < nk; k4 += 4 * kThreads) {
             const float* mt = mtile + k4 / kTile;   // mt[row * mts]
             f32x4 sc = {0.f, 0.f, 0.f, 0.f};
@@ -427,6 +455,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
                 if (k4 + i < nk) srow[key_begin + k4 + i] = sc[i];
+            if constexpr (kStep) *reinterpret_cast<f32x4*>(skeys + k4) = sc;   // k4 + 3 < chunk
         }
     }
 
@@ -474,6 +503,24 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
             __syncthreads();
         }
     }
+    if constexpr (kStep) {
+        // ---- 5. select (Eq. 4) and the first draft step (Eq. 5) ------------
+        const SelectArgs& sa = fa.sel;
+        const Geom g = geom_of(sa, b);
+        SelLds& L = *reinterpret_cast<SelLds*>(stash);
+        const uint32_t* skeys = reinterpret_cast<const uint32_t*>(stash + NRT * 16 * stride + mts * (NRT * 16));
+        bool done;
+        if (g.simple) {
+            __syncthreads();   // the stash becomes the select's
+            done = select_simple<true>(sa, g, it.s, unit, L, want);
+        } else if (NRT > 1 || chunk <= kRound) {
+            done = step_select<1>(sa, g, it.s, unit, skeys, nk, key_begin, L, want);
+        } else {
+            done = step_select<NRT == 1 ? 2 : 1>(sa, g, it.s, unit, skeys, nk, key_begin, L, want);
+        }
+        // chunk 0 goes on only when every exchange of the step completed
+        if (!done) return;
+    }
     // every chunk has published, so has read the epoch; advanced last, after
     // the workgroup's final wait for loads
     if (fa.epoch && tid == 0 && slot == slot0) epoch_advance(fa.epoch + unit);
@@ -499,11 +546,13 @@ hipError_t fused_setup(int* n_cu, int* per_cu) {
     if (e != hipSuccess) return e;
     int st = dev >= 0 && dev < kMaxDevices ? state[dev].load(std::memory_order_relaxed) : 0;
     if (st == 0) {
-        const int lds = (int)fused_lds_bytes<NRT>(max_fused_chunk<NRT>());
-        const void* fns[4] = {reinterpret_cast<const void*>(verify_fused_kernel<NRT, true, false>),
-                              reinterpret_cast<const void*>(verify_fused_kernel<NRT, false, false>),
-                              reinterpret_cast<const void*>(verify_fused_kernel<NRT, true, true>),
-                              reinterpret_cast<const void*>(verify_fused_kernel<NRT, false, true>)};
+        const int lds = (int)std::max(fused_lds_bytes<NRT>(max_fused_chunk<NRT>()), sizeof(SelLds));
+        const void* fns[6] = {reinterpret_cast<const void*>(verify_fused_kernel<NRT, true, false, false>),
+                              reinterpret_cast<const void*>(verify_fused_kernel<NRT, false, false, false>),
+                              reinterpret_cast<const void*>(verify_fused_kernel<NRT, true, true, false>),
+                              reinterpret_cast<const void*>(verify_fused_kernel<NRT, false, true, false>),
+                              reinterpret_cast<const void*>(verify_fused_kernel<NRT, true, false, true>),
+                              reinterpret_cast<const void*>(verify_fused_kernel<NRT, false, false, true>)};
         for (const void* f : fns) {
             e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
             if (e != hipSuccess) return e;
@@ -511,7 +560,7 @@ hipError_t fused_setup(int* n_cu, int* per_cu) {
         int cu = 0, blocks = 0;
         e = hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev);
         if (e != hipSuccess) return e;
-        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, verify_fused_kernel<NRT, true, false>,
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, verify_fused_kernel<NRT, true, false, false>,
                                                          kThreads, lds);
         if (e != hipSuccess) return e;
         st = cu * 16 + std::min(blocks, 15) + 1;
@@ -524,22 +573,32 @@ hipError_t fused_setup(int* n_cu, int* per_cu) {
 
 template <int NRT>
 hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, hipStream_t stream) {
-    const size_t dyn = fused_lds_bytes<NRT>(a.v.chunk);
     int n_cu = 0, per_cu = 0;
     const hipError_t e = fused_setup<NRT>(&n_cu, &per_cu);
     if (e != hipSuccess) return e;
     // non-temporal K/V loads when every workgroup runs in the first round
     const bool paged = a.v.block_table != nullptr;
-    if (n_slots <= n_cu) {
-        if (paged)
-            hipLaunchKernelGGL((verify_fused_kernel<NRT, true, true>), dim3(n_slots), dim3(kThreads), dyn, stream, a);
+    const bool stream1 = n_slots <= n_cu;
+    const dim3 grid(n_slots), block(kThreads);
+    if (a.step) {   // (dense caches only; the host checks)
+        const size_t dyn = std::max(fused_lds_bytes<NRT>(a.v.chunk), sizeof(SelLds));
+        if (stream1)
+            hipLaunchKernelGGL((verify_fused_kernel<NRT, true, false, true>), grid, block, dyn, stream, a);
         else
-            hipLaunchKernelGGL((verify_fused_kernel<NRT, true, false>), dim3(n_slots), dim3(kThreads), dyn, stream, a);
+            hipLaunchKernelGGL((verify_fused_kernel<NRT, false, false, true>), grid, block, dyn, stream, a);
+        return hipGetLastError();
+    }
+    const size_t dyn = fused_lds_bytes<NRT>(a.v.chunk);
+    if (stream1) {
+        if (paged)
+            hipLaunchKernelGGL((verify_fused_kernel<NRT, true, true, false>), grid, block, dyn, stream, a);
+        else
+            hipLaunchKernelGGL((verify_fused_kernel<NRT, true, false, false>), grid, block, dyn, stream, a);
     } else {
         if (paged)
-            hipLaunchKernelGGL((verify_fused_kernel<NRT, false, true>), dim3(n_slots), dim3(kThreads), dyn, stream, a);
+            hipLaunchKernelGGL((verify_fused_kernel<NRT, false, true, false>), grid, block, dyn, stream, a);
         else
-            hipLaunchKernelGGL((verify_fused_kernel<NRT, false, false>), dim3(n_slots), dim3(kThreads), dyn, stream, a);
+            hipLaunchKernelGGL((verify_fused_kernel<NRT, false, false, false>), grid, block, dyn, stream, a);
     }
     return hipGetLastError();
 }

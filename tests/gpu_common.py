@@ -212,3 +212,64 @@ def gpu_select_draft(d: Dev, scores32: np.ndarray, out_fp32=True, budget=None, k
                    n_idx=n_idx, out=out)
     torch.cuda.synchronize()
     return idx.cpu().numpy(), n_idx.cpu().numpy(), out.float().cpu().numpy().astype(np.float64)
+
+
+def gpu_decode_step(d: Dev, out_fp32=True, budget=None, k_sink=None, k_recent=None, mode=B.VERIFY_AUTO):
+    """ssl_decode_step into sentinel-filled outputs: (out, scores, idx, n_idx,
+    draft out) on the host, outputs as float64."""
+    w = d.w
+    p = params_of(w, out_fp32=out_fp32, budget=budget, k_sink=k_sink, k_recent=k_recent, mode=mode)
+    odt = torch.float32 if out_fp32 else torch.bfloat16
+    out = torch.full(d.q.shape, -7.0, dtype=odt, device="cuda")
+    sc = torch.full((w.batch, w.n_kv_heads, w.max_ctx), -1.0, dtype=torch.float32, device="cuda")
+    idx = torch.full((w.batch, w.n_kv_heads, p.budget), -7, dtype=torch.int32, device="cuda")
+    n_idx = torch.full((w.batch,), -1, dtype=torch.int32, device="cuda")
+    dout = torch.full(d.qd.shape, -7.0, dtype=odt, device="cuda")
+    B.decode_step(d.q, d.k, d.v, d.qd, w.ctx_len, w.q_len, p, out=out, scores=sc, idx=idx,
+                  n_idx=n_idx, draft_out=dout)
+    torch.cuda.synchronize()
+    f64 = lambda t: t.float().cpu().numpy().astype(np.float64)
+    return f64(out), sc.cpu().numpy(), idx.cpu().numpy(), n_idx.cpu().numpy(), f64(dout)
+
+
+def check_decode_step(w, out_ref, s_ref, oabs_ref, out_fp32=True, budget=None, k_sink=None,
+                      k_recent=None, expect_one_kernel=None):
+    """ssl_decode_step against verify_attn (bit for bit) and the oracle (see
+    test_gpu_decode_step); returns whether the step ran as one kernel."""
+    d = Dev(w)
+    p = params_of(w, out_fp32=out_fp32, budget=budget, k_sink=k_sink, k_recent=k_recent)
+    one = B.decode_step_plan(B.verify_shape(d.q, d.k), p, w.ctx_len, w.q_len)
+    print(f"[decode step] {w.describe()} one kernel: {one}", flush=True)
+    if expect_one_kernel is not None:
+        assert one == expect_one_kernel
+    out, s, idx, n_idx, dout = gpu_decode_step(d, out_fp32=out_fp32, budget=budget, k_sink=k_sink,
+                                               k_recent=k_recent)
+    # verify: the same arithmetic as verify_attn, and the oracle's bars
+    out_v, s_v = gpu_verify(d, out_fp32=out_fp32)
+    mask = np.arange(w.max_q)[None, :, None] < w.q_len[:, None, None] * np.ones(
+        (1, 1, w.n_q_heads), dtype=bool)
+    assert np.array_equal(out[mask], out_v[mask]), "outputs differ from verify_attn"
+    for b in range(w.batch):
+        T = int(w.ctx_len[b])
+        assert np.array_equal(s[b, :, :T], s_v[b, :, :T]), "scores differ from verify_attn"
+        assert np.all(s[b, :, T:] == -1.0)
+    assert np.all(out[~mask] == -7.0)
+    check_outputs(out, out_ref, oabs_ref, mask, out_fp32=out_fp32)
+    check_scores(s, s_ref, w.ctx_len)
+    check_score_mass(s, w)
+    # select: bit-exact against the oracle's select on the step's own scores
+    ks = w.k_sink if k_sink is None else k_sink
+    kr = w.k_recent if k_recent is None else k_recent
+    bud = w.budget if budget is None else budget
+    idx_ref, n_ref = oracle.select(w, s.astype(np.float64), budget=bud, k_sink=ks, k_recent=kr)
+    assert np.array_equal(n_idx, n_ref)
+    for b in range(w.batch):
+        assert np.array_equal(idx[b, :, :n_ref[b]], idx_ref[b, :, :n_ref[b]])
+    check_index_structure(idx, n_idx, w.ctx_len, ks, kr, bud)
+    # draft over those index sets
+    idx_dev = np.where(idx_ref < 0, 0, idx_ref).astype(np.int32)
+    o_ref = oracle.draft(w, idx_dev, n_ref)
+    oabs = oracle.draft(w, idx_dev, n_ref, v=abs_v(w))
+    check_outputs(dout, o_ref, oabs, np.ones(o_ref.shape[:2], dtype=bool), out_fp32=out_fp32,
+                  what="decode-step draft")
+    return one

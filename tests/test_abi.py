@@ -41,6 +41,17 @@ def test_header_symbols_exported(lib):
     assert sorted(B.EXPORTED) == names
 
 
+def test_every_export_has_argtypes(lib):
+    """Without argtypes ctypes passes Python ints as 32-bit C ints, which
+    truncates pointers and stream handles: every call that takes arguments
+    must declare them."""
+    for n in B.EXPORTED:
+        f = getattr(lib, n)
+        if n in ("ssl_build_id", "ssl_last_hip_error"):
+            continue
+        assert f.argtypes, f"{n} has no argtypes"
+
+
 def _shape(**kw):
     d = dict(batch=1, n_q_heads=32, n_kv_heads=8, head_dim=128, max_ctx=4096, max_q=8)
     d.update(kw)
@@ -167,6 +178,46 @@ def test_select_validation(lib):
     ca3, cp3 = _i32((1 << 21) + 1)                       # beyond 256 partitions of 8192
     assert lib.ssl_select_workspace(ctypes.byref(s2), ctypes.byref(p), cp3,
                                     ctypes.byref(n)) == B.SSL_ERR_UNSUPPORTED
+
+
+def _decode(lib, shape=None, params=None, ctx=(4096,), ql=(7,), q=FAKE, k=FAKE, v=FAKE, out=FAKE,
+            scores=FAKE, idx=FAKE, n_idx=FAKE, qd=FAKE, dout=FAKE, ws=FAKE, ws_bytes=1 << 40):
+    shape = shape or _shape(batch=len(ctx))
+    params = params or _params()
+    ca, cp = _i32(*ctx)
+    qa, qp = _i32(*ql)
+    return lib.ssl_decode_step(ctypes.byref(shape), ctypes.byref(params), cp, qp, q, k, v, out,
+                               scores, idx, n_idx, qd, dout, ws, ws_bytes, None)
+
+
+def test_decode_step_validation(lib):
+    # the verify checks, then the select and draft checks, before any HIP call
+    assert _decode(lib, ql=(0,)) == B.SSL_ERR_SHAPE
+    assert _decode(lib, ctx=(4097,)) == B.SSL_ERR_SHAPE
+    assert _decode(lib, shape=_shape(head_dim=64)) == B.SSL_ERR_UNSUPPORTED
+    assert _decode(lib, params=_params(budget=0)) == B.SSL_ERR_BUDGET
+    assert _decode(lib, params=_params(k_sink=200, k_recent=57)) == B.SSL_ERR_BUDGET
+    assert _decode(lib, params=_params(sm_scale=0.0)) == B.SSL_ERR_SHAPE
+    for name in ("q", "k", "v", "out", "scores", "idx", "n_idx", "qd", "dout"):
+        assert _decode(lib, **{name: None}) == B.SSL_ERR_NULL, name
+        assert _decode(lib, **{name: FAKE_ODD}) == B.SSL_ERR_ALIGN, name
+    assert _decode(lib, ws=None) == B.SSL_ERR_WORKSPACE
+    assert _decode(lib, ws_bytes=8) == B.SSL_ERR_WORKSPACE
+    n = ctypes.c_size_t(0)
+    ca, cp = _i32(4096)
+    qa, qp = _i32(7)
+    s, p = _shape(), _params()
+    assert lib.ssl_decode_step_workspace(ctypes.byref(s), ctypes.byref(p), cp, qp,
+                                         ctypes.byref(n)) == 0
+    assert n.value > 65536   # the epoch prefix and more
+    assert _decode(lib, ws_bytes=n.value - 1) == B.SSL_ERR_WORKSPACE
+    one = ctypes.c_int32(-1)
+    assert lib.ssl_decode_step_plan(ctypes.byref(s), ctypes.byref(p), cp, qp,
+                                    ctypes.byref(one)) == 0
+    assert one.value in (0, 1)
+    assert lib.ssl_decode_step_plan(ctypes.byref(s), ctypes.byref(p), cp, qp, None) == B.SSL_ERR_NULL
+    assert lib.ssl_decode_step_workspace(ctypes.byref(s), ctypes.byref(p), cp, qp,
+                                         None) == B.SSL_ERR_NULL
 
 
 def _draft(lib, shape=None, params=None, nidx=(256,), q=FAKE, k=FAKE, v=FAKE, idx=FAKE, out=FAKE,
@@ -446,6 +497,7 @@ def test_every_workspace_starts_with_the_epoch_words(lib):
     assert B.verify_workspace_bytes(s, p, ctx, ql) > 65536
     assert B.select_workspace_bytes(s, p, ctx) > 65536
     assert B.draft_workspace_bytes(s, p, [2048]) > 65536
+    assert B.decode_step_workspace_bytes(s, p, ctx, ql) > 65536
     n = ctypes.c_size_t(0)
     assert lib.ssl_logit_stats_workspace(1, 1000, ctypes.byref(n)) == B.SSL_OK and n.value > 65536
 

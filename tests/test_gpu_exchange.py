@@ -81,8 +81,16 @@ class Inputs:
         sdout = torch.full((BATCH, HQ, D), SENT, dtype=torch.float32, device=dev)
         B.select_draft(sc if idx_in is None else torch.ones_like(sc), self.ctx, self.params, self.qd,
                        self.k, self.v, idx=idx2, n_idx=n_idx2, out=sdout)
+        # the whole step in one kernel
+        step = (torch.full((BATCH, QLEN, HQ, D), SENT, dtype=torch.float32, device=dev),
+                torch.full((BATCH, HKV, MAX_CTX), SENT, dtype=torch.float32, device=dev),
+                torch.full((BATCH, HKV, BUDGET), -7, dtype=torch.int32, device=dev),
+                torch.full((BATCH,), -1, dtype=torch.int32, device=dev),
+                torch.full((BATCH, HQ, D), SENT, dtype=torch.float32, device=dev))
+        B.decode_step(self.q, self.k, self.v, self.qd, self.ctx, self.ql, self.params, out=step[0],
+                      scores=step[1], idx=step[2], n_idx=step[3], draft_out=step[4])
         torch.cuda.synchronize()
-        return out, sc, idx, n_idx, dout, rout, ent, am, idx2, n_idx2, sdout
+        return (out, sc, idx, n_idx, dout, rout, ent, am, idx2, n_idx2, sdout) + step
 
 
 def test_plans_use_the_exchanging_schedules():
@@ -91,11 +99,15 @@ def test_plans_use_the_exchanging_schedules():
     assert B.verify_plan(s, x.params, x.ctx, x.ql)[0] == B.VERIFY_ONE_SWEEP
     one_kernel, part, _ = B.select_plan(s, x.params, x.ctx)
     assert one_kernel is True and part <= 4096   # select_draft drafts inside the select kernel
+    assert B.decode_step_plan(s, x.params, x.ctx, x.ql)   # the whole step is one kernel
 
 
 def test_status_stays_clear_on_normal_calls():
-    Inputs().run()
+    r = Inputs().run()
     assert B.exchange_status() == 0
+    # the one-kernel step equals the separate calls on outputs, scores and index sets
+    assert torch.equal(r[11], r[0]) and torch.equal(r[12], r[1])
+    assert torch.equal(r[13], r[2]) and torch.equal(r[14], r[3])
 
 
 def test_every_wait_gives_up_and_every_kernel_finishes():
@@ -104,7 +116,8 @@ def test_every_wait_gives_up_and_every_kernel_finishes():
     assert B.exchange_status() == 0
     idx_good = good[2]
     B.test_exchange_faults(64, True)
-    out, sc, idx, n_idx, dout, rout, ent, am, idx2, n_idx2, sdout = x.run()
+    (out, sc, idx, n_idx, dout, rout, ent, am, idx2, n_idx2, sdout,
+     st_out, st_sc, st_idx, st_n, st_dout) = x.run()
     flags = B.exchange_status()
     B.test_exchange_faults(0, False)
     assert flags == ALL, f"status {flags:#x}, expected {ALL:#x}"
@@ -113,6 +126,8 @@ def test_every_wait_gives_up_and_every_kernel_finishes():
     assert torch.all(idx == -7) and torch.all(n_idx == -1)
     assert torch.all(dout == SENT) and torch.all(rout == SENT)
     assert torch.all(idx2 == -7) and torch.all(n_idx2 == -1) and torch.all(sdout == SENT)
+    assert torch.all(st_out == SENT) and torch.all(st_sc == SENT) and torch.all(st_idx == -7)
+    assert torch.all(st_n == -1) and torch.all(st_dout == SENT)
     # the draft kernels on a valid index set give up the same way
     out2 = x.run(idx_in=idx_good)
     B.test_exchange_faults(0, False)

@@ -1,8 +1,9 @@
 """Calls captured in a HIP graph and replayed with new contents in the
 captured input buffers.  Each replay must equal the eager calls on the same
 inputs, bit for bit: the kernels are deterministic (fixed merge orders, no
-floating-point atomics).  Verify (one sweep), select with the first draft step, a draft-round step
-and the logit statistics exchange partial results between workgroups behind
+floating-point atomics).  The whole decode step (one kernel: verify, select
+and the first draft step), the separate calls, a draft-round step and the
+logit statistics exchange partial results between workgroups behind
 tags, and a replay reuses the call tag fixed at capture; the workspace epochs
 must give every replay a new one, or a replay could take the previous
 replay's partials as its own.  Replays alternate with eager calls and
@@ -55,6 +56,7 @@ def test_graph_replays_match_eager_calls():
     st = B.PreparedStep(q, k, v, qd, ctx, ql, params, out, scores, idx, n_idx, dout, stream=cap)
     rnd = B.PreparedRound(qd, k, v, idx, ctx, K_ROUND, params, rout, stream=cap)
     assert B.verify_plan(st.shape, params, ctx, ql)[0] == B.VERIFY_ONE_SWEEP
+    assert st.one_kernel
     with torch.cuda.stream(cap):   # eager warm-up: one-time launcher set-up stays out of the graph
         st.step()
         rnd.step(ROUND_STEP)
@@ -75,10 +77,15 @@ def test_graph_replays_match_eager_calls():
         g.replay()
         torch.cuda.synchronize()
 
-        out_e, scores_e = B.verify_attn(q, k, v, ctx, ql, params)
-        idx_e, n_idx_e = B.select_topb(scores_e, ctx, params)
-        # the step's select and first draft step run as one call
-        _, _, dout_e = B.select_draft(scores_e, ctx, params, qd, k, v)
+        # the step is one call (one kernel here): its eager run, then the
+        # separate calls, whose outputs, scores and index sets it must equal
+        out_e, scores_e, idx_e, n_idx_e, dout_e = B.decode_step(q, k, v, qd, ctx, ql, params)
+        out_v, scores_v = B.verify_attn(q, k, v, ctx, ql, params)
+        idx_s, n_idx_s = B.select_topb(scores_v, ctx, params)
+        torch.cuda.synchronize()
+        assert torch.equal(out_e, out_v) and torch.equal(scores_e[:, :, :T], scores_v[:, :, :T])
+        assert torch.equal(n_idx_e, n_idx_s) and torch.equal(idx_e[:, :, :n_idx_host],
+                                                             idx_s[:, :, :n_idx_host])
         rout_e = torch.empty_like(rout)
         B.PreparedRound(qd, k, v, idx_e, ctx, K_ROUND, params, rout_e).step(ROUND_STEP)
         ent_e, am_e = B.logit_stats(logits)
@@ -99,8 +106,8 @@ def test_graph_replays_match_eager_calls():
 
 
 def test_graph_with_one_shared_workspace():
-    """verify -> select (three kernels: more than 256 partitions) -> draft
-    captured with ONE workspace for the calls, replayed with new inputs.
+    """verify -> select (three kernels: more than 256 partitions) -> draft as
+    separate calls, captured with ONE workspace for the calls, replayed with new inputs.
     Every layout keeps its exchange epochs in the same leading words, so the
     select histograms never land on the draft's epochs."""
     dev = torch.device("cuda:0")
@@ -127,11 +134,11 @@ def test_graph_with_one_shared_workspace():
     assert B.verify_plan(st.shape, params, ctx, ql)[0] == B.VERIFY_ONE_SWEEP
     assert B.select_plan(st.shape, params, ctx)[0] is False
     with torch.cuda.stream(cap):
-        st.step()
+        st.step_separate()
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=cap):
-        st.step()
+        st.step_separate()
     torch.cuda.synchronize()
     for r in range(REPLAYS):
         print(f"[graph, shared workspace] replay {r}", flush=True)
@@ -141,9 +148,7 @@ def test_graph_with_one_shared_workspace():
         torch.cuda.synchronize()
         out_e, scores_e = B.verify_attn(q, k, v, ctx, ql, params)
         idx_e, n_idx_e = B.select_topb(scores_e, ctx, params)
-        _, _, dout_e = B.select_draft(scores_e, ctx, params, qd, k, v)
-        # (select runs as three kernels here, so the draft is the plain draft call)
-        assert torch.equal(dout_e, B.draft_attn(qd, k, v, idx_e, [n_idx_host] * batch, params))
+        dout_e = B.draft_attn(qd, k, v, idx_e, [n_idx_host] * batch, params)
         torch.cuda.synchronize()
         assert torch.equal(out, out_e), f"replay {r}: verify output"
         assert torch.equal(scores[:, :, :t], scores_e[:, :, :t]), f"replay {r}: scores"

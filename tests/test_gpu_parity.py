@@ -13,9 +13,9 @@ import pytest
 import torch
 
 import oracle
-from gpu_common import (Dev, abs_v, check_band, check_index_structure, check_outputs,
-                        check_score_mass, check_scores, gpu_draft, gpu_select, gpu_select_draft,
-                        gpu_verify, params_of)
+from gpu_common import (Dev, abs_v, check_band, check_decode_step, check_index_structure,
+                        check_outputs, check_score_mass, check_scores, gpu_draft, gpu_select,
+                        gpu_select_draft, gpu_verify, params_of)
 from paper_2607_27735_amd import binding as B
 from paper_2607_27735_amd.workloads import f32_to_bf16_bits, generate, make_config
 
@@ -417,8 +417,13 @@ def test_workload_full_size(n):
                   for b in range(w.batch) for c in range(w.n_kv_heads) for p in hp[b, c])
         print(f"  planted heavy hitters selected: {got}/{hp.size}")
 
-    # select and the first draft step in one call (the benchmark's step)
+    # select and the first draft step in one call
     _check_select_draft(w, s32, out_fp32=False)
+    # the whole step in one call (the benchmark's step): one kernel where
+    # verify takes one sweep in one round of workgroups of >= 512-key chunks
+    # (32K)
+    one = check_decode_step(w, out_ref, s_ref, oabs_ref, out_fp32=False)
+    assert one == (n == 2)
 
     # draft on the oracle's index sets, all heads
     idx_dev = np.where(idx_ref < 0, 0, idx_ref).astype(np.int32)
