@@ -81,8 +81,8 @@ def is_paged(short: str) -> bool:
         return False
     args = [x.strip() for x in short.split("<", 1)[1].rstrip(">").split(",")]
     k = short.split("<")[0]
-    if k == "verify_fused_kernel":
-        return len(args) == 3 and args[2] == "true"
+    if k == "verify_fused_kernel":   # <row tiles, stream, paged, whole step>
+        return len(args) >= 3 and args[2] == "true"
     if k in ("verify_stats_kernel", "verify_main_kernel"):
         return len(args) == 2 and args[1] == "true"
     return k == "draft_kernel" and args[0] == "3"
@@ -104,7 +104,11 @@ def summarize_trace(d: str, command: str, title: str = "") -> str:
         short = kernel_short(r["Name"])
         k = short.split("<")[0]
         mode = short.split("<", 1)[1].split(",")[0].strip(" >") if "<" in short else ""
-        call = ("verify (paged)" if k.startswith("verify") and is_paged(short)
+        step_kernel = (k == "verify_fused_kernel" and "<" in short
+                       and short.rstrip(">").split(",")[-1].strip() == "true"
+                       and len(short.split(",")) == 4)
+        call = ("decode step (one kernel)" if step_kernel
+                else "verify (paged)" if k.startswith("verify") and is_paged(short)
                 else "draft (paged)" if is_paged(short)
                 else "verify" if k.startswith("verify") else "select" if k.startswith("select")
                 else "draft round materialize" if "materialize" in k
@@ -590,6 +594,7 @@ def workload_entry(B, n: int, steps: int, warmup: int, torch, np, cpu: bool):
              "verify_schedule": "one-sweep" if schedule == B.VERIFY_ONE_SWEEP else "two-sweep",
              "verify_items": vitems, "select_schedule": "one kernel" if sel_one else "three kernels",
              "select_partitions_per_unit": sel_parts,
+             "step_call": "one kernel" if sts[0].one_kernel else "verify, then select_draft",
              "step_us": round(step_us, 3), "step_alg_bytes": sum(nbytes.values()),
              "step_hbm_frac": round(sum(nbytes.values()) / (step_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
              "steps": steps, "kv_copies_rotated": n_copies, "calls": {}}
@@ -827,7 +832,10 @@ def main() -> int:
                    "q_len": list(map(int, w.q_len)), "budget": w.budget,
                    "launch": args.mode, "kv_copies_rotated": n_copies,
                    "verify_schedule": sched_name, "verify_chunk": vchunk,
-                   "verify_items": vitems},
+                   "verify_items": vitems,
+                   "step_call": "ssl_decode_step (" + ("one kernel: verify, select and the first "
+                                "draft step" if steps[0].one_kernel else
+                                "verify, then select_draft") + ")"},
         "gpu_step_us_median": round(statistics.median(step_us), 3),
         "step_alg_bytes": step_total,
         "step_hbm_gbps": round(step_total / (ms_per_step * 1e-3) / 1e9, 1),
@@ -843,7 +851,7 @@ def main() -> int:
         "kernels": kernels,
     }
     if args.workload == 2 and args.mode == "eager" and args.verify_mode == "auto":
-        result["mfma"] = measured_mfma("verify_fused_kernel<2, true, false>", v_avg)
+        result["mfma"] = measured_mfma("verify_fused_kernel<2, true, false, false>", v_avg)
     if args.mode == "eager" and not args.no_graph_step:
         result["graph_step"] = graph_step_bench(B, kvs, q, qd, w, params, out, scores, idx, n_idx,
                                                 dout, stream, args.steps, torch)
