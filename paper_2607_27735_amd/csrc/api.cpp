@@ -15,8 +15,10 @@
 
 using namespace ssl;
 
-static_assert(SSL_EXCHANGE_VERIFY == kStatusVerify && SSL_EXCHANGE_SELECT == kStatusSelect &&
-                  SSL_EXCHANGE_DRAFT == kStatusDraft && SSL_EXCHANGE_LOGITS == kStatusLogits,
+static_assert((uint32_t)SSL_EXCHANGE_VERIFY == kStatusVerify &&
+                  (uint32_t)SSL_EXCHANGE_SELECT == kStatusSelect &&
+                  (uint32_t)SSL_EXCHANGE_DRAFT == kStatusDraft &&
+                  (uint32_t)SSL_EXCHANGE_LOGITS == kStatusLogits,
               "status bits of the ABI and the kernels agree");
 
 namespace {
