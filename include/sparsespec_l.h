@@ -435,6 +435,24 @@ int ssl_draft_step(const ssl_shape *shape, const ssl_params *params,
                    const void *q_draft, const void *k_cache, const void *v_cache,
                    const int32_t *idx, const void *k_sel, const void *v_sel, void *out,
                    void *workspace, size_t workspace_bytes, hipStream_t stream);
+/* The draft round over a paged cache (pages and block table as in
+ * ssl_verify_attn_paged; the drafted tokens' rows written to their pages):
+ * the same calls and results, every cache row (sink, TopK and window) read
+ * through the block table; materialized rows stay a dense per-unit copy.
+ * Workspaces as ssl_draft_step_workspace.  In addition SSL_ERR_NULL without a
+ * block table and SSL_ERR_SHAPE if page_size is not a positive multiple of
+ * 32 or max_ctx > page_size * max_blocks. */
+int ssl_draft_materialize_paged(const ssl_shape *shape, const ssl_params *params,
+                                const int32_t *ctx_len_host, const void *k_pages,
+                                const void *v_pages, const int32_t *block_table, int32_t page_size,
+                                int32_t max_blocks, const int32_t *idx, void *k_sel, void *v_sel,
+                                hipStream_t stream);
+int ssl_draft_step_paged(const ssl_shape *shape, const ssl_params *params,
+                         const int32_t *ctx_len_host, const int32_t *cur_len_host,
+                         const void *q_draft, const void *k_pages, const void *v_pages,
+                         const int32_t *block_table, int32_t page_size, int32_t max_blocks,
+                         const int32_t *idx, const void *k_sel, const void *v_sel, void *out,
+                         void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Around the path: token statistics of logit rows.

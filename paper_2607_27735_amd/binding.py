@@ -41,6 +41,7 @@ EXPORTED = [
     "ssl_draft_workspace", "ssl_draft_attn",
     "ssl_verify_attn_paged", "ssl_draft_attn_paged",
     "ssl_draft_materialize", "ssl_draft_step_workspace", "ssl_draft_step",
+    "ssl_draft_materialize_paged", "ssl_draft_step_paged",
     "ssl_logit_stats_workspace", "ssl_logit_stats", "ssl_greedy_accept_workspace",
     "ssl_greedy_accept",
     "ssl_ctrl_create", "ssl_ctrl_destroy", "ssl_ctrl_observe", "ssl_ctrl_accept_prob",
@@ -132,6 +133,10 @@ def load(path: Optional[str] = None):
                                           _vp, _vp, _vp, _sz, _vp]
     lib.ssl_draft_attn_paged.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp,
                                          _vp, _sz, _vp]
+    lib.ssl_draft_materialize_paged.argtypes = [sp, pp, _i32p, _vp, _vp, _vp, _i32, _i32, _vp,
+                                                _vp, _vp, _vp]
+    lib.ssl_draft_step_paged.argtypes = [sp, pp, _i32p, _i32p, _vp, _vp, _vp, _vp, _i32, _i32,
+                                         _vp, _vp, _vp, _vp, _vp, _sz, _vp]
     lib.ssl_logit_stats_workspace.argtypes = [_i32, _i32, _szp]
     lib.ssl_logit_stats.argtypes = [_vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _sz, _vp]
     lib.ssl_greedy_accept_workspace.argtypes = [_i32, _i32, _i32, _szp]
@@ -142,7 +147,8 @@ def load(path: Optional[str] = None):
               "ssl_select_topb", "ssl_select_plan", "ssl_select_draft_workspace",
               "ssl_select_draft", "ssl_draft_workspace", "ssl_draft_attn", "ssl_draft_materialize",
               "ssl_draft_step_workspace", "ssl_draft_step", "ssl_verify_attn_paged",
-              "ssl_draft_attn_paged", "ssl_logit_stats_workspace",
+              "ssl_draft_attn_paged", "ssl_draft_materialize_paged", "ssl_draft_step_paged",
+              "ssl_logit_stats_workspace",
               "ssl_logit_stats", "ssl_greedy_accept_workspace", "ssl_greedy_accept"):
         getattr(lib, f).restype = ctypes.c_int
     lib.ssl_ctrl_create.argtypes = [ctypes.c_double, _i32p, ctypes.c_int32, ctypes.c_int32]
@@ -693,6 +699,83 @@ def draft_step(q_draft: torch.Tensor, k: torch.Tensor, v: torch.Tensor, ctx_len_
                                  _ptr(v_sel), _ptr(out), _ptr(workspace), workspace.numel(),
                                  _stream(stream)),
            "ssl_draft_step")
+    return out
+
+
+def draft_materialize_paged(k_pages: torch.Tensor, v_pages: torch.Tensor,
+                            block_table: torch.Tensor, max_ctx: int, idx: torch.Tensor,
+                            ctx_len_host, params: Params, k_sel: Optional[torch.Tensor] = None,
+                            v_sel: Optional[torch.Tensor] = None, stream=None,
+                            n_q_heads: Optional[int] = None):
+    """draft_materialize over a paged cache (k_pages / v_pages [n_pages, Hkv,
+    page_size, 128] bf16, block_table [B, max_blocks] int32); k_sel / v_sel
+    stay dense [B, units, budget, 128]."""
+    _need_gpu(k_pages, v_pages, block_table, idx)
+    if k_pages.dtype != torch.bfloat16 or v_pages.dtype != torch.bfloat16:
+        raise TypeError("k_pages, v_pages must be bfloat16")
+    if block_table.dtype != torch.int32 or block_table.dim() != 2:
+        raise ValueError("block_table must be int32 [batch, max_blocks]")
+    _, hkv, page, d = k_pages.shape
+    batch = block_table.shape[0]
+    hq = hkv if n_q_heads is None else int(n_q_heads)
+    units = hq if params.per_head else hkv
+    if idx.dtype != torch.int32 or idx.shape != (batch, units, params.budget):
+        raise ValueError("idx must be int32 [batch, units, budget]")
+    shape = Shape(batch, hq, hkv, d, int(max_ctx), 1)
+    sel_shape = (batch, units, params.budget, d)
+    if k_sel is None:
+        k_sel = torch.empty(sel_shape, dtype=torch.bfloat16, device=k_pages.device)
+    if v_sel is None:
+        v_sel = torch.empty(sel_shape, dtype=torch.bfloat16, device=k_pages.device)
+    if tuple(k_sel.shape) != sel_shape or tuple(v_sel.shape) != sel_shape:
+        raise ValueError("k_sel / v_sel must be [batch, units, budget, 128]")
+    _need_gpu(k_sel, v_sel)
+    ctx = _host_i32(ctx_len_host)
+    _check(load().ssl_draft_materialize_paged(ctypes.byref(shape), ctypes.byref(params),
+                                              ctx.ctypes.data_as(_i32p), _ptr(k_pages),
+                                              _ptr(v_pages), _ptr(block_table), int(page),
+                                              int(block_table.shape[1]), _ptr(idx), _ptr(k_sel),
+                                              _ptr(v_sel), _stream(stream)),
+           "ssl_draft_materialize_paged")
+    return k_sel, v_sel
+
+
+def draft_step_paged(q_draft: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Tensor,
+                     block_table: torch.Tensor, max_ctx: int, ctx_len_host, cur_len_host,
+                     params: Params, idx: Optional[torch.Tensor] = None,
+                     k_sel: Optional[torch.Tensor] = None, v_sel: Optional[torch.Tensor] = None,
+                     out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                     stream=None) -> torch.Tensor:
+    """draft_step over a paged cache (layouts as draft_materialize_paged)."""
+    _need_gpu(q_draft, k_pages, v_pages, block_table)
+    if any(t.dtype != torch.bfloat16 for t in (q_draft, k_pages, v_pages)):
+        raise TypeError("q_draft, k_pages, v_pages must be bfloat16")
+    if block_table.dtype != torch.int32 or block_table.dim() != 2:
+        raise ValueError("block_table must be int32 [batch, max_blocks]")
+    batch, hq, d = q_draft.shape
+    _, hkv, page, _ = k_pages.shape
+    units = hq if params.per_head else hkv
+    if (k_sel is None) != (v_sel is None):
+        raise ValueError("give both k_sel and v_sel, or neither")
+    if k_sel is None and (idx is None or idx.dtype != torch.int32
+                          or idx.shape != (batch, units, params.budget)):
+        raise ValueError("idx must be int32 [batch, units, budget] when no materialized rows are given")
+    shape = Shape(batch, hq, hkv, d, int(max_ctx), 1)
+    ctx, cur = _host_i32(ctx_len_host), _host_i32(cur_len_host)
+    odt = torch.float32 if params.out_fp32 else torch.bfloat16
+    if out is None:
+        out = torch.zeros(q_draft.shape, dtype=odt, device=q_draft.device)
+    _need_gpu(out)
+    need = draft_step_workspace_bytes(shape, params, ctx, cur)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q_draft.device)
+    _check(load().ssl_draft_step_paged(ctypes.byref(shape), ctypes.byref(params),
+                                       ctx.ctypes.data_as(_i32p), cur.ctypes.data_as(_i32p),
+                                       _ptr(q_draft), _ptr(k_pages), _ptr(v_pages),
+                                       _ptr(block_table), int(page), int(block_table.shape[1]),
+                                       _ptr(idx), _ptr(k_sel), _ptr(v_sel), _ptr(out),
+                                       _ptr(workspace), workspace.numel(), _stream(stream)),
+           "ssl_draft_step_paged")
     return out
 
 

@@ -787,6 +787,18 @@ int ssl_draft_workspace(const ssl_shape* shape, const ssl_params* params,
 
 namespace {
 
+// A paged cache for the draft calls (none when block_table is NULL): every
+// row they read is below max_ctx, so the pages must cover max_ctx keys.
+int check_draft_pages(const ssl_shape* shape, const int32_t* block_table, int32_t page_size,
+                      int32_t max_blocks) {
+    if (!block_table) return SSL_OK;
+    if (!aligned(block_table, 4)) return SSL_ERR_ALIGN;
+    if (page_size < 32 || page_size % 32 != 0 || max_blocks < 1 ||
+        (int64_t)page_size * max_blocks < shape->max_ctx)
+        return SSL_ERR_SHAPE;
+    return SSL_OK;
+}
+
 int draft_call(const ssl_shape* shape, const ssl_params* params, const int32_t* n_idx_host,
                const void* q_draft, const void* k_cache, const void* v_cache,
                const int32_t* block_table, int32_t page_size, int32_t max_blocks,
@@ -799,13 +811,8 @@ int draft_call(const ssl_shape* shape, const ssl_params* params, const int32_t* 
     DraftPlan plan;
     rc = plan_draft(&us, params, n_idx_host, &plan);
     if (rc) return rc;
-    if (block_table) {
-        // every index is below max_ctx: the pages must cover max_ctx keys
-        if (!aligned(block_table, 4)) return SSL_ERR_ALIGN;
-        if (page_size < 32 || page_size % 32 != 0 || max_blocks < 1 ||
-            (int64_t)page_size * max_blocks < shape->max_ctx)
-            return SSL_ERR_SHAPE;
-    }
+    rc = check_draft_pages(shape, block_table, page_size, max_blocks);
+    if (rc) return rc;
     if (!q_draft || !k_cache || !v_cache || !idx || !out) return SSL_ERR_NULL;
     if (!aligned(q_draft, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) ||
         !aligned(out, 16) || !aligned(idx, 4))
@@ -1098,15 +1105,22 @@ int ssl_decode_step(const ssl_shape* shape, const ssl_params* params, const int3
     return hip_rc(launch_verify_fused(fa, vp.fused_slots, vp.row_tiles, stream));
 }
 
-int ssl_draft_materialize(const ssl_shape* shape, const ssl_params* params,
-                          const int32_t* ctx_len_host, const void* k_cache, const void* v_cache,
-                          const int32_t* idx, void* k_sel, void* v_sel, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+int materialize_call(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
+                     const void* k_cache, const void* v_cache, const int32_t* block_table,
+                     int32_t page_size, int32_t max_blocks, const int32_t* idx, void* k_sel,
+                     void* v_sel, hipStream_t stream) {
     if (!shape || !params) return SSL_ERR_NULL;
     int rc = check_budget(params);
     if (rc) return rc;
     const ssl_shape us = unit_shape(shape, params);   // per_head: one unit per query head
     StepPlan plan;
     rc = plan_draft_step(&us, params, ctx_len_host, ctx_len_host, &plan);
+    if (rc) return rc;
+    rc = check_draft_pages(shape, block_table, page_size, max_blocks);
     if (rc) return rc;
     if (!k_cache || !v_cache || !idx || !k_sel || !v_sel) return SSL_ERR_NULL;
     if (!aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(k_sel, 16) ||
@@ -1123,8 +1137,32 @@ int ssl_draft_materialize(const ssl_shape* shape, const ssl_params* params,
     a.n_kv_real = shape->n_kv_heads;
     a.max_ctx = shape->max_ctx;
     a.budget = params->budget;
+    a.block_table = block_table;
+    a.page_size = page_size;
+    a.max_blocks = max_blocks;
     for (int b = 0; b < shape->batch; ++b) a.n_fixed[b] = plan.n_fixed[b];
     return hip_rc(launch_draft_materialize(a, plan.max_fixed, shape->batch * us.n_kv_heads, stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+int ssl_draft_materialize(const ssl_shape* shape, const ssl_params* params,
+                          const int32_t* ctx_len_host, const void* k_cache, const void* v_cache,
+                          const int32_t* idx, void* k_sel, void* v_sel, hipStream_t stream) {
+    return materialize_call(shape, params, ctx_len_host, k_cache, v_cache, nullptr, 0, 0, idx,
+                            k_sel, v_sel, stream);
+}
+
+int ssl_draft_materialize_paged(const ssl_shape* shape, const ssl_params* params,
+                                const int32_t* ctx_len_host, const void* k_pages,
+                                const void* v_pages, const int32_t* block_table, int32_t page_size,
+                                int32_t max_blocks, const int32_t* idx, void* k_sel, void* v_sel,
+                                hipStream_t stream) {
+    if (!block_table) return SSL_ERR_NULL;
+    return materialize_call(shape, params, ctx_len_host, k_pages, v_pages, block_table, page_size,
+                            max_blocks, idx, k_sel, v_sel, stream);
 }
 
 int ssl_draft_step_workspace(const ssl_shape* shape, const ssl_params* params,
@@ -1141,10 +1179,15 @@ int ssl_draft_step_workspace(const ssl_shape* shape, const ssl_params* params,
     return SSL_OK;
 }
 
-int ssl_draft_step(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
-                   const int32_t* cur_len_host, const void* q_draft, const void* k_cache,
-                   const void* v_cache, const int32_t* idx, const void* k_sel, const void* v_sel,
-                   void* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+int draft_step_call(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
+                    const int32_t* cur_len_host, const void* q_draft, const void* k_cache,
+                    const void* v_cache, const int32_t* block_table, int32_t page_size,
+                    int32_t max_blocks, const int32_t* idx, const void* k_sel, const void* v_sel,
+                    void* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
     if (!shape || !params) return SSL_ERR_NULL;
     int rc = check_budget(params);
     if (rc) return rc;
@@ -1153,6 +1196,8 @@ int ssl_draft_step(const ssl_shape* shape, const ssl_params* params, const int32
     rc = plan_draft_step(&us, params, ctx_len_host, cur_len_host, &plan);
     if (rc) return rc;
     if (!(params->sm_scale > 0.f) || !isfinite(params->sm_scale)) return SSL_ERR_SHAPE;
+    rc = check_draft_pages(shape, block_table, page_size, max_blocks);
+    if (rc) return rc;
     const bool sel = k_sel || v_sel;
     if (!q_draft || !k_cache || !v_cache || !out) return SSL_ERR_NULL;
     if (sel ? (!k_sel || !v_sel) : !idx) return SSL_ERR_NULL;
@@ -1189,11 +1234,39 @@ int ssl_draft_step(const ssl_shape* shape, const ssl_params* params, const int32
     a.out_fp32 = params->out_fp32 ? 1 : 0;
     a.scale_log2 = params->sm_scale * 1.4426950408889634f;
     a.seq = plan.d.seq;
+    a.block_table = block_table;
+    a.page_size = page_size;
+    a.max_blocks = max_blocks;
     for (int b = 0; b < shape->batch; ++b) {
         a.n_fixed[b] = plan.n_fixed[b];
         a.win0[b] = plan.win0[b];
     }
     return hip_rc(launch_draft_step(a, plan.d.n_items, stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+int ssl_draft_step(const ssl_shape* shape, const ssl_params* params, const int32_t* ctx_len_host,
+                   const int32_t* cur_len_host, const void* q_draft, const void* k_cache,
+                   const void* v_cache, const int32_t* idx, const void* k_sel, const void* v_sel,
+                   void* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    return draft_step_call(shape, params, ctx_len_host, cur_len_host, q_draft, k_cache, v_cache,
+                           nullptr, 0, 0, idx, k_sel, v_sel, out, workspace, workspace_bytes,
+                           stream);
+}
+
+int ssl_draft_step_paged(const ssl_shape* shape, const ssl_params* params,
+                         const int32_t* ctx_len_host, const int32_t* cur_len_host,
+                         const void* q_draft, const void* k_pages, const void* v_pages,
+                         const int32_t* block_table, int32_t page_size, int32_t max_blocks,
+                         const int32_t* idx, const void* k_sel, const void* v_sel, void* out,
+                         void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (!block_table) return SSL_ERR_NULL;
+    return draft_step_call(shape, params, ctx_len_host, cur_len_host, q_draft, k_pages, v_pages,
+                           block_table, page_size, max_blocks, idx, k_sel, v_sel, out, workspace,
+                           workspace_bytes, stream);
 }
 
 // ---- token statistics of logit rows ----------------------------------------

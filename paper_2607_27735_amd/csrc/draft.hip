@@ -61,8 +61,22 @@ __device__ __forceinline__ DItem decode_ditem(const SeqTable& st, int item, int 
 
 // Where an entry's row comes from: the index list (Eq. 5), or a draft-round
 // step whose fixed rows come through the index list or from the materialized
-// copy, and whose window rows are consecutive cache rows.
-constexpr int kPlain = 0, kRoundIdx = 1, kRoundSel = 2, kPlainPaged = 3;
+// copy, and whose window rows are consecutive cache rows; each from the dense
+// cache or through the block table of a paged one.
+constexpr int kPlain = 0, kRoundIdx = 1, kRoundSel = 2, kPlainPaged = 3, kRoundIdxPaged = 4,
+              kRoundSelPaged = 5;
+constexpr bool mode_paged(int m) { return m == kPlainPaged || m == kRoundIdxPaged || m == kRoundSelPaged; }
+constexpr bool mode_round(int m) { return m == kRoundIdx || m == kRoundSel || m == kRoundIdxPaged || m == kRoundSelPaged; }
+constexpr bool mode_sel(int m) { return m == kRoundSel || m == kRoundSelPaged; }
+
+// Row r of cache head kvc of sequence b: dense, an offset from the unit's
+// base; paged, a row of the page pool (rows numbered over the whole pool).
+template <bool kPaged>
+__device__ __forceinline__ uint32_t cache_row(const DraftArgs& a, int b, int kvc, int r) {
+    if (!kPaged) return (uint32_t)r;
+    const int pg = a.block_table[(size_t)b * a.max_blocks + r / a.page_size];
+    return (uint32_t)(((size_t)pg * a.n_kv_real + kvc) * a.page_size + r % a.page_size);
+}
 
 // TPW tiles of 32 entries per wave (4 * 32 * TPW entries per workgroup): a
 // wave finds the rows of all its entries at once (64 per lane map), then
@@ -75,8 +89,8 @@ __global__ __launch_bounds__(kDraftThreads, 2) void draft_kernel(DraftArgs a) {
     const DItem it = decode_ditem(a.seq, blockIdx.x, a.n_kv_heads, a.chunk);
     // (read here, outside the wave-dependent branch below, so that they are
     // scalar loads and not vector loads that the index load waits for)
-    const int nf = kMode == kPlain ? 0 : a.n_fixed[it.b];
-    const int win0 = kMode == kPlain ? 0 : a.win0[it.b];
+    const int nf = mode_round(kMode) ? a.n_fixed[it.b] : 0;
+    const int win0 = mode_round(kMode) ? a.win0[it.b] : 0;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int m16 = lane & 15, G = lane >> 4;
     const int g = a.group;
@@ -111,7 +125,7 @@ __global__ __launch_bounds__(kDraftThreads, 2) void draft_kernel(DraftArgs a) {
         // (paged: rows are numbered over the whole page pool; per-head units
         // read the rows of cache head it.c / kv_div)
         const int kvc = it.c / a.kv_div;
-        const size_t cache_off = kMode == kPlainPaged
+        const size_t cache_off = mode_paged(kMode)
             ? 0 : ((size_t)it.b * a.n_kv_real + kvc) * a.max_ctx * kHeadDim;
         const size_t sel_off = (size_t)it.unit * a.budget * kHeadDim;
         const RowSource src{a.k + cache_off, a.v + cache_off, a.k_sel + sel_off, a.v_sel + sel_off};
@@ -123,25 +137,22 @@ __global__ __launch_bounds__(kDraftThreads, 2) void draft_kernel(DraftArgs a) {
 #pragma unroll
         for (int j = 0; j < kMaps; ++j) {   // all index loads in flight together
             const int e = min(wbeg + 64 * j + lane, last);
-            raw[j] = (kMode == kPlain || kMode == kPlainPaged || kMode == kRoundIdx)
-                         ? a.idx[(size_t)it.unit * a.budget + e] : 0;
+            raw[j] = !mode_sel(kMode) ? a.idx[(size_t)it.unit * a.budget + e] : 0;
         }
         uint32_t my_row[kMaps];
 #pragma unroll
         for (int j = 0; j < kMaps; ++j) {
             const int e = min(wbeg + 64 * j + lane, last);
-            if (kMode == kPlain) {
-                my_row[j] = (uint32_t)min(max(raw[j], 0), a.max_ctx - 1);
-            } else if (kMode == kPlainPaged) {
-                const int row = min(max(raw[j], 0), a.max_ctx - 1);
-                const int pg = a.block_table[(size_t)it.b * a.max_blocks + row / a.page_size];
-                my_row[j] = (uint32_t)(((size_t)pg * a.n_kv_real + kvc) * a.page_size + row % a.page_size);
+            constexpr bool kPg = mode_paged(kMode);
+            if (!mode_round(kMode)) {
+                my_row[j] = cache_row<kPg>(a, it.b, kvc, min(max(raw[j], 0), a.max_ctx - 1));
             } else {
                 // (the index load does not wait for n_fixed: entry e < budget is
                 // in bounds, and its value is used only when e < n_fixed)
-                my_row[j] = e < nf ? (kMode == kRoundSel ? (uint32_t)e | kSelBit
-                                                         : (uint32_t)min(max(raw[j], 0), a.max_ctx - 1))
-                                   : (uint32_t)min(max(win0 + e - nf, 0), a.max_ctx - 1);
+                const int r = e < nf ? min(max(raw[j], 0), a.max_ctx - 1)
+                                     : min(max(win0 + e - nf, 0), a.max_ctx - 1);
+                my_row[j] = (mode_sel(kMode) && e < nf) ? (uint32_t)e | kSelBit
+                                                        : cache_row<kPg>(a, it.b, kvc, r);
             }
         }
         const int ntile = (wend - wbeg + kTile - 1) / kTile;   // wave-uniform
@@ -151,7 +162,7 @@ __global__ __launch_bounds__(kDraftThreads, 2) void draft_kernel(DraftArgs a) {
                 uint32_t r = my_row[0];
 #pragma unroll
                 for (int j = 1; j < kMaps; ++j) r = (tile >> 1) == j ? my_row[j] : r;
-                gather_tile<kMode == kRoundSel>(r, 32 * (tile & 1), src, m16, G, t);
+                gather_tile<mode_sel(kMode)>(r, 32 * (tile & 1), src, m16, G, t);
             },
             [&](const Gathered& t, int tile) {
                 draft_tile(a.scale_log2, qop, t, wbeg + kTile * tile, wend, G, M, L, oacc);
@@ -302,24 +313,26 @@ __global__ __launch_bounds__(kDraftThreads, 2) void draft_kernel(DraftArgs a) {
 
 // Materialization for a draft round: workgroup (x, u) copies rows
 // 32x .. 32x + 31 of unit u's sink and TopK entries (the first n_fixed[b]
-// entries of its index list) from the cache to k_sel/v_sel (a unit per query
-// head reads the rows of its KV head).  Thread t moves 16 bytes of two rows
-// of K and of V, all four loads in flight together.
+// entries of its index list) from the cache (dense, or paged through the
+// block table) to k_sel/v_sel (a unit per query head reads the rows of its KV
+// head).  Thread t moves 16 bytes of two rows of K and of V, all four loads
+// in flight together.
 constexpr int kMatRows = 32;
+template <bool kPaged>
 __global__ __launch_bounds__(kDraftThreads) void draft_materialize_kernel(DraftArgs a) {
     const int u = blockIdx.y, b = u / a.n_kv_heads;
     const int nf = a.n_fixed[b];
     const int q = threadIdx.x & 15, r = threadIdx.x >> 4;   // 16 rows per pass
     const int32_t* ib = a.idx + (size_t)u * a.budget;
     const int kvc = (u - b * a.n_kv_heads) / a.kv_div;
-    const size_t cache_off = ((size_t)b * a.n_kv_real + kvc) * a.max_ctx * kHeadDim;
+    const size_t cache_off = kPaged ? 0 : ((size_t)b * a.n_kv_real + kvc) * a.max_ctx * kHeadDim;
     const size_t sel_off = (size_t)u * a.budget * kHeadDim;
     int e[2];
     u32x4 kk[2], vv[2];
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
         e[j] = blockIdx.x * kMatRows + 16 * j + r;
-        const int row = min(max(ib[min(e[j], max(nf - 1, 0))], 0), a.max_ctx - 1);
+        const int row = cache_row<kPaged>(a, b, kvc, min(max(ib[min(e[j], max(nf - 1, 0))], 0), a.max_ctx - 1));
         kk[j] = ld_u32x4(a.k + cache_off + (size_t)row * kHeadDim + 8 * q);
         vv[j] = ld_u32x4(a.v + cache_off + (size_t)row * kHeadDim + 8 * q);
     }
@@ -366,10 +379,17 @@ hipError_t launch_draft(const DraftArgs& a, int n_items, hipStream_t stream) {
 }
 
 hipError_t launch_draft_step(const DraftArgs& a, int n_items, hipStream_t stream) {
-    if (a.k_sel)
-        launch_mode<kRoundSel>(a, n_items, stream);
-    else
-        launch_mode<kRoundIdx>(a, n_items, stream);
+    if (a.block_table) {
+        if (a.k_sel)
+            launch_mode<kRoundSelPaged>(a, n_items, stream);
+        else
+            launch_mode<kRoundIdxPaged>(a, n_items, stream);
+    } else {
+        if (a.k_sel)
+            launch_mode<kRoundSel>(a, n_items, stream);
+        else
+            launch_mode<kRoundIdx>(a, n_items, stream);
+    }
     return hipGetLastError();
 }
 
@@ -377,8 +397,12 @@ hipError_t launch_draft_materialize(const DraftArgs& a, int max_fixed, int n_uni
                                     hipStream_t stream) {
     const int blocks = (max_fixed + kMatRows - 1) / kMatRows;
     if (blocks < 1 || n_units < 1) return hipSuccess;
-    hipLaunchKernelGGL(draft_materialize_kernel, dim3(blocks, n_units), dim3(kDraftThreads), 0,
-                       stream, a);
+    if (a.block_table)
+        hipLaunchKernelGGL(draft_materialize_kernel<true>, dim3(blocks, n_units),
+                           dim3(kDraftThreads), 0, stream, a);
+    else
+        hipLaunchKernelGGL(draft_materialize_kernel<false>, dim3(blocks, n_units),
+                           dim3(kDraftThreads), 0, stream, a);
     return hipGetLastError();
 }
 

@@ -352,6 +352,29 @@ def test_paged_validation(lib):
     assert dra(page=16) == B.SSL_ERR_SHAPE
     assert dra(blocks=63) == B.SSL_ERR_SHAPE          # 63 * 64 < max_ctx 4096
     assert dra(ws=None) == B.SSL_ERR_WORKSPACE
+    # the draft round over pages: the step's and the materialization's checks
+    ua, up = _i32(4003)
+
+    def stp(bt=FAKE, page=64, blocks=64, ws=FAKE, cur=up):
+        return lib.ssl_draft_step_paged(ctypes.byref(s), ctypes.byref(p), cp, cur, FAKE, FAKE,
+                                        FAKE, bt, page, blocks, FAKE, None, None, FAKE, ws,
+                                        1 << 40, None)
+    assert stp(bt=None) == B.SSL_ERR_NULL
+    assert stp(bt=FAKE + 2) == B.SSL_ERR_ALIGN
+    assert stp(page=40) == B.SSL_ERR_SHAPE
+    assert stp(blocks=63) == B.SSL_ERR_SHAPE          # the pages must cover max_ctx
+    ba, bp = _i32(4097)
+    assert stp(cur=bp) == B.SSL_ERR_SHAPE             # cur past max_ctx
+    assert stp(ws=None) == B.SSL_ERR_WORKSPACE
+
+    def mat(bt=FAKE, page=64, blocks=64, k_sel=FAKE):
+        return lib.ssl_draft_materialize_paged(ctypes.byref(s), ctypes.byref(p), cp, FAKE, FAKE,
+                                               bt, page, blocks, FAKE, k_sel, FAKE, None)
+    assert mat(bt=None) == B.SSL_ERR_NULL
+    assert mat(page=0) == B.SSL_ERR_SHAPE
+    assert mat(blocks=1) == B.SSL_ERR_SHAPE
+    assert mat(k_sel=None) == B.SSL_ERR_NULL
+    assert mat(k_sel=FAKE_ODD) == B.SSL_ERR_ALIGN
 
 
 def test_status_strings(lib):

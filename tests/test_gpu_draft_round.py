@@ -144,3 +144,47 @@ def test_draft_round_rejects_long_tail():
                      v_sel=sel)
     with pytest.raises(B.SSLError):
         B.draft_step(dev_bf16(w.q_draft), k, v, base, base - 1, p, k_sel=sel, v_sel=sel)
+
+
+@pytest.mark.parametrize("page", [32, 128])
+@pytest.mark.parametrize("name", ["small-b2", "tiny-T", "kv8-ragged", "headline-8b-T32K"])
+def test_paged_draft_round(name, page):
+    """The round over a paged cache (shuffled block table, NaN in every pool
+    row no table entry names below the round's last length): the materialized
+    rows equal the dense ones, and every step, through the index list and from
+    the materialized rows, equals the dense round bit for bit and meets the
+    oracle's bar."""
+    from test_gpu_paged import paged
+    w, base, steps = _case(name)
+    print(f"[paged draft round] {name}, page {page}", flush=True)
+    rng = np.random.default_rng(int(base.sum()) + page)
+    scores = rng.random((w.batch, w.n_kv_heads, w.max_ctx))
+    idx, n_idx = oracle.select(w, scores, ctx_len=base)
+    p = params_of(w)
+    k, v = dev_bf16(w.k), dev_bf16(w.v)
+    kp, vp, bt, max_blocks = paged(w, page, seed=page + 11)   # the pages hold rows < ctx_len
+    kpd, vpd, btd = dev_bf16(kp), dev_bf16(vp), torch.from_numpy(bt).cuda()
+    idx_d = torch.from_numpy(np.ascontiguousarray(idx)).cuda()
+    k_sel, v_sel = B.draft_materialize(k, v, idx_d, base, p)
+    pk_sel, pv_sel = B.draft_materialize_paged(kpd, vpd, btd, w.max_ctx, idx_d, base, p)
+    torch.cuda.synchronize()
+    for b in range(w.batch):
+        T = int(base[b])
+        nf = int(n_idx[b]) - (T - max(T - w.k_recent, min(w.k_sink, T)))
+        assert torch.equal(pk_sel[b, :, :nf], k_sel[b, :, :nf])
+        assert torch.equal(pv_sel[b, :, :nf], v_sel[b, :, :nf])
+    for i in range(steps + 1):
+        qb = f32_to_bf16_bits(rng.standard_normal(w.q_draft.shape).astype(np.float32))
+        qd = dev_bf16(qb)
+        cur = base + i
+        o_dense = B.draft_step(qd, k, v, base, cur, p, idx=idx_d)
+        o_pi = B.draft_step_paged(qd, kpd, vpd, btd, w.max_ctx, base, cur, p, idx=idx_d)
+        o_ps = B.draft_step_paged(qd, kpd, vpd, btd, w.max_ctx, base, cur, p, k_sel=pk_sel,
+                                  v_sel=pv_sel)
+        torch.cuda.synchronize()
+        assert torch.equal(o_pi, o_dense), f"step {i}: paged (index list) differs from dense"
+        assert torch.equal(o_ps, o_dense), f"step {i}: paged (materialized) differs from dense"
+        o_ref = oracle.draft_step(w, idx, base, cur, q_draft=qb)
+        oabs = oracle.draft_step(w, idx, base, cur, q_draft=qb, v=abs_v(w))
+        check_outputs(o_ps.float().cpu().numpy().astype(np.float64), o_ref, oabs,
+                      np.ones(o_ref.shape[:2], dtype=bool), what=f"paged draft step {i}")
