@@ -62,6 +62,9 @@ def _bind(lib):
     lib.oracle_greedy_accept.argtypes = [ctypes.c_int] * 4 + [_i32p, _u16p, _f32p, _i32p, _i32p,
                                                               _i32p]
     lib.oracle_greedy_accept.restype = ctypes.c_int
+    lib.oracle_spec_accept.argtypes = [ctypes.c_int] * 4 + [_i32p, _f32p, _f32p, ctypes.c_double,
+                                                            _i32p, _f64p, _f64p, _i32p, _i32p]
+    lib.oracle_spec_accept.restype = ctypes.c_int
     lib.oracle_head_scores.argtypes = [ctypes.c_int] * 6 + [_i32p, _i32p, _u16p, _u16p,
                                                             ctypes.c_double, ctypes.c_int, _f64p]
     lib.oracle_head_scores.restype = ctypes.c_int
@@ -250,6 +253,35 @@ def greedy_accept(logits: np.ndarray, draft: np.ndarray, k_len, vocab: Optional[
                                 _p(m, _i32p), _p(t, _i32p)) != 0:
         raise ValueError("oracle_greedy_accept rejected its arguments")
     return m, t
+
+
+def spec_accept(tlogits: np.ndarray, dlogits: np.ndarray, draft: np.ndarray, k_len, tau: float,
+                u_acc: np.ndarray, u_smp: np.ndarray, vocab: Optional[int] = None, lib=None):
+    """Speculative sampling (see ``oracle_spec_accept``): ``tlogits``
+    [batch][max_k + 1][row_stride] and ``dlogits`` [batch][max_k][row_stride]
+    float32 logits, ``draft`` [batch][max_k] int32, ``u_acc`` [batch][max_k]
+    and ``u_smp`` [batch] uniforms in [0, 1); returns (n_accepted, next_token)."""
+    lib = lib or load()
+    batch, rows, stride = tlogits.shape
+    max_k = rows - 1
+    V = stride if vocab is None else vocab
+    t = _c(tlogits, np.float32).reshape(batch, max_k + 1, stride)
+    d = _c(dlogits, np.float32).reshape(batch, max_k, stride) if max_k > 0 else \
+        np.zeros((batch, 1, stride), np.float32)
+    dr = _c(draft, np.int32).reshape(batch, max(max_k, 1)) if max_k > 0 else \
+        np.zeros((batch, 1), np.int32)
+    ua = _c(u_acc, np.float64).reshape(batch, max(max_k, 1)) if max_k > 0 else \
+        np.zeros((batch, 1), np.float64)
+    us = _c(u_smp, np.float64).reshape(batch)
+    kl = _c(k_len, np.int32)
+    m = np.zeros(batch, dtype=np.int32)
+    nt = np.zeros(batch, dtype=np.int32)
+    f32p = ctypes.POINTER(ctypes.c_float)
+    if lib.oracle_spec_accept(batch, max_k, V, stride, _p(kl, _i32p), _p(t, f32p), _p(d, f32p),
+                              float(tau), _p(dr, _i32p), _p(ua, _f64p), _p(us, _f64p),
+                              _p(m, _i32p), _p(nt, _i32p)) != 0:
+        raise ValueError("oracle_spec_accept rejected its arguments")
+    return m, nt
 
 
 def head_scores(w, *, q=None, k=None, ctx_len=None, q_len=None, lib=None):

@@ -554,6 +554,107 @@ int oracle_greedy_accept(int batch, int max_k, int vocab, int row_stride, const 
     return rc;
 }
 
+/* One logit row at temperature tau as a distribution: its largest scaled
+ * logit m and normalizer Z = sum_i exp(x_i / tau - m). */
+static void row_dist(const float *x, int vocab, double tau, double *m, double *Z)
+{
+    double mx = -INFINITY;
+    for (int i = 0; i < vocab; ++i) {
+        const double y = (double)x[i] / tau;
+        if (y > mx) mx = y;
+    }
+    double z = 0.0;
+    for (int i = 0; i < vocab; ++i) z += exp((double)x[i] / tau - mx);
+    *m = mx;
+    *Z = z;
+}
+
+static double row_prob(const float *x, int i, double tau, double m, double Z)
+{
+    return exp((double)x[i] / tau - m) / Z;
+}
+
+/* The smallest index whose cumulative mass (in index order) exceeds
+ * u * total; the last index with mass when rounding leaves none. */
+static int draw_by_inversion(const double *w, int vocab, double u)
+{
+    double total = 0.0;
+    for (int i = 0; i < vocab; ++i) total += w[i];
+    const double target = u * total;
+    double run = 0.0;
+    int last = 0;
+    for (int i = 0; i < vocab; ++i) {
+        if (w[i] > 0.0) last = i;
+        run += w[i];
+        if (run > target) return i;
+    }
+    return last;
+}
+
+/*
+ * Speculative sampling, the verification rule that keeps the target model's
+ * output distribution (Sec. 1 and Sec. 2.1 rely on it; the paper does not
+ * print it).  Sequence b drafted k = k_len[b] tokens x_j = draft[b][j] from
+ * the drafter's logit rows dlogits[b][j] (layout [batch][max_k][row_stride]);
+ * its verify pass gave the target rows tlogits[b][0..k] (layout
+ * [batch][max_k + 1][row_stride]; row j scores the token after drafted token
+ * j - 1).  At temperature tau > 0 let p_j = softmax(tlogits[b][j] / tau) and
+ * q_j = softmax(dlogits[b][j] / tau).  With the caller's uniforms
+ * u_acc[b][j] ([batch][max_k]) and u_smp[b] in [0, 1):
+ *   drafted token j passes when u_acc[b][j] * q_j(x_j) < p_j(x_j), i.e. with
+ *   probability min(1, p_j(x_j) / q_j(x_j));
+ *   n_accepted[b] = m, the number that pass before the first that does not;
+ *   next_token[b] is drawn by inversion with u_smp[b] from
+ *   r(x) = max(0, p_m(x) - q_m(x)) when m < k (from p_m if r has no mass),
+ *   or from p_k when every drafted token passed.
+ * Returns 0 or -1.
+ */
+int oracle_spec_accept(int batch, int max_k, int vocab, int row_stride, const int32_t *k_len,
+                       const float *tlogits, const float *dlogits, double tau,
+                       const int32_t *draft, const double *u_acc, const double *u_smp,
+                       int32_t *n_accepted, int32_t *next_token)
+{
+    if (batch < 1 || max_k < 0 || vocab < 1 || row_stride < vocab || !(tau > 0.0)) return -1;
+    for (int b = 0; b < batch; ++b)
+        if (k_len[b] < 0 || k_len[b] > max_k) return -1;
+    double *w = (double *)malloc(sizeof(double) * (size_t)vocab);
+    for (int b = 0; b < batch; ++b) {
+        const int k = k_len[b];
+        int m = 0;
+        for (; m < k; ++m) {
+            const float *t = tlogits + ((size_t)b * (max_k + 1) + m) * row_stride;
+            const float *d = dlogits + ((size_t)b * max_k + m) * row_stride;
+            const int x = draft[(size_t)b * max_k + m];
+            double mt, zt, md, zd;
+            row_dist(t, vocab, tau, &mt, &zt);
+            row_dist(d, vocab, tau, &md, &zd);
+            const double p = row_prob(t, x, tau, mt, zt);
+            const double q = row_prob(d, x, tau, md, zd);
+            if (!(u_acc[(size_t)b * max_k + m] * q < p)) break;
+        }
+        const float *t = tlogits + ((size_t)b * (max_k + 1) + m) * row_stride;
+        double mt, zt;
+        row_dist(t, vocab, tau, &mt, &zt);
+        double mass = 0.0;
+        if (m < k) {   /* the residual of the first rejected position */
+            const float *d = dlogits + ((size_t)b * max_k + m) * row_stride;
+            double md, zd;
+            row_dist(d, vocab, tau, &md, &zd);
+            for (int i = 0; i < vocab; ++i) {
+                const double r = row_prob(t, i, tau, mt, zt) - row_prob(d, i, tau, md, zd);
+                w[i] = r > 0.0 ? r : 0.0;
+                mass += w[i];
+            }
+        }
+        if (!(mass > 0.0))
+            for (int i = 0; i < vocab; ++i) w[i] = row_prob(t, i, tau, mt, zt);
+        n_accepted[b] = m;
+        next_token[b] = draw_by_inversion(w, vocab, u_smp[b]);
+    }
+    free(w);
+    return 0;
+}
+
 /* ---------------------------------------------------------------------------
  * Per-query-head variant of Eq. 3 / Eq. 5 (Sec. 3.2 states importance "for
  * every layer and attention head"; the main path keeps it per KV head).

@@ -603,6 +603,130 @@ def pin_greedy_accept_worked(lib):
 
 
 # ---------------------------------------------------------------------------
+# speculative sampling (the distribution-preserving verification rule)
+# ---------------------------------------------------------------------------
+
+def _log_rows(*probs):
+    return np.log(np.array(probs, dtype=np.float64)).astype(np.float32)
+
+
+def pin_spec_accept_worked(lib):
+    """Hand-worked: V = 3, two drafted tokens.  Target rows p0 = (.5, .3, .2),
+    p1 = (.1, .6, .3), p2 = (.2, .2, .6); drafter rows q0 = (.25, .5, .25),
+    q1 = (.3, .3, .4); drafted tokens 1 (p/q = .6) and 2 (p/q = .75)."""
+    t = _log_rows([.5, .3, .2], [.1, .6, .3], [.2, .2, .6])[None]
+    d = _log_rows([.25, .5, .25], [.3, .3, .4])[None]
+    x = np.array([[1, 2]])
+    def run(u_acc, u_smp, k=2):
+        m, n = oracle.spec_accept(t, d, x, [k], 1.0, np.array([u_acc]), np.array([u_smp]), lib=lib)
+        return int(m[0]), int(n[0])
+    # both pass; bonus from p2 = (.2, .2, .6): cumulative (.2, .4, 1), .3 -> 1
+    assert run([.5, .7], .3) == (2, 1)
+    assert run([.5, .7], .41) == (2, 2)
+    # the first fails (.65 >= .6): residual max(0, p0 - q0) = (.25, 0, 0) -> 0
+    assert run([.65, .1], .99) == (0, 0)
+    # the second fails (.8 >= .75): residual max(0, p1 - q1) = (0, .3, 0) -> 1,
+    # even for u = 0 (the first index whose cumulative mass exceeds 0)
+    assert run([.1, .8], .0) == (1, 1)
+    assert run([.1, .8], .999) == (1, 1)
+    # nothing drafted: the token comes from p0 = (.5, .3, .2): .9 -> 2, .5 -> 1
+    assert run([.9, .9], .9, k=0) == (0, 2)
+    assert run([.9, .9], .55, k=0) == (0, 1)
+    assert run([.9, .9], .45, k=0) == (0, 0)
+
+
+def pin_spec_accept_identical_distributions(lib):
+    """A drafter equal to the target passes every token (u q < p = q for u < 1),
+    and the bonus token is drawn from the last target row by inversion."""
+    rng = np.random.default_rng(91)
+    batch, max_k, V = 5, 4, 200
+    t = (rng.standard_normal((batch, max_k + 1, V)) * 2).astype(np.float32)
+    d = t[:, :max_k].copy()
+    x = rng.integers(0, V, (batch, max_k))
+    k_len = np.array([4, 3, 0, 1, 4])
+    u_acc = rng.random((batch, max_k)) * 0.999
+    u_smp = rng.random(batch)
+    m, nxt = oracle.spec_accept(t, d, x, k_len, 0.7, u_acc, u_smp, lib=lib)
+    assert np.array_equal(m, k_len)
+    for b in range(batch):
+        z = t[b, k_len[b]].astype(np.float64) / 0.7
+        p = np.exp(z - z.max())
+        c = np.cumsum(p / p.sum())
+        assert nxt[b] == int(np.searchsorted(c, u_smp[b], side="right"))
+
+
+def pin_spec_accept_preserves_target_distribution(lib):
+    """The committed first token is distributed as the target's p0 whatever the
+    drafter's q0.  Over a grid of N uniforms: a(x) = the fraction with which
+    drafted token x passes, R(y) = the fraction of residual draws giving y
+    (a drafted token that always fails, a grid of draw uniforms).  Then
+    P(token = y) = sum_x q0(x) [a(x) [y = x] + (1 - a(x)) R(y)] must equal
+    p0(y) to within the grid's resolution."""
+    N = 4000
+    grid = (np.arange(N) + 0.5) / N
+    for seed in (92, 93, 94):
+        rng = np.random.default_rng(seed)
+        V = 6
+        t = np.log(np.stack([rng.dirichlet(np.ones(V)), rng.dirichlet(np.ones(V))]))[None]
+        t = t.astype(np.float32)
+        d = np.log(rng.dirichlet(np.ones(V)))[None, None].astype(np.float32)
+        p0 = np.exp(t[0, 0].astype(np.float64)); p0 /= p0.sum()
+        q0 = np.exp(d[0, 0].astype(np.float64)); q0 /= q0.sum()
+        tb, db, ones = np.repeat(t, N, axis=0), np.repeat(d, N, axis=0), np.ones(N, np.int32)
+        a = np.zeros(V)
+        for xv in range(V):
+            m, _ = oracle.spec_accept(tb, db, np.full((N, 1), xv), ones, 1.0, grid[:, None],
+                                      grid, lib=lib)
+            a[xv] = m.mean()
+        x_fail = int(np.argmin(p0 / q0))          # p0 < q0 there: u just below 1 fails
+        m, y = oracle.spec_accept(tb, db, np.full((N, 1), x_fail), ones, 1.0,
+                                  np.full((N, 1), 1.0 - 1e-12), grid, lib=lib)
+        assert not m.any()
+        R = np.bincount(y, minlength=V) / N
+        prob = (q0 * a) + (q0 * (1 - a)).sum() * R
+        assert np.abs(prob - p0).max() < 3.0 / N, (prob, p0)
+        # and each part separately: the pass rate min(1, p/q), the residual's shape
+        assert np.abs(a - np.minimum(1.0, p0 / q0)).max() < 1.5 / N
+        r = np.maximum(p0 - q0, 0.0)
+        assert np.abs(R - r / r.sum()).max() < 1.5 / N
+
+
+def pin_spec_accept_temperature(lib):
+    """Only logits / tau matter: (2 x, tau = 2) draws exactly what (x, tau = 1) does."""
+    rng = np.random.default_rng(95)
+    batch, max_k, V = 6, 5, 64
+    t = rng.standard_normal((batch, max_k + 1, V)).astype(np.float32)
+    d = (t[:, :max_k] + 0.7 * rng.standard_normal((batch, max_k, V))).astype(np.float32)
+    x = rng.integers(0, V, (batch, max_k))
+    k_len = np.array([5, 5, 3, 1, 0, 2])
+    u_acc, u_smp = rng.random((batch, max_k)), rng.random(batch)
+    a = oracle.spec_accept(t, d, x, k_len, 1.0, u_acc, u_smp, lib=lib)
+    b = oracle.spec_accept(2 * t, 2 * d, x, k_len, 2.0, u_acc, u_smp, lib=lib)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    assert len(set(a[0].tolist())) > 1   # the draws differ between sequences
+
+
+def pin_spec_accept_greedy_limit(lib):
+    """As tau -> 0 both distributions become one-hot at their argmax: a drafted
+    token equal to the drafter's argmax passes exactly when it is the target's
+    argmax, and the next token is the target argmax: greedy verification."""
+    rng = np.random.default_rng(96)
+    batch, max_k, V = 8, 6, 50
+    t = rng.standard_normal((batch, max_k + 1, V)).astype(np.float32)
+    d = rng.standard_normal((batch, max_k, V)).astype(np.float32)
+    am = t.argmax(axis=2)
+    for b in range(batch):   # agree with the target on a prefix of random length
+        for j in range(rng.integers(0, max_k + 1)):
+            d[b, j, am[b, j]] = d[b, j].max() + 1.0
+    x = d.argmax(axis=2)
+    k_len = rng.integers(0, max_k + 1, batch)
+    m, nxt = oracle.spec_accept(t, d, x, k_len, 1e-4, rng.random((batch, max_k)),
+                                rng.random(batch), lib=lib)
+    mg, ng = oracle.greedy_accept(t, x, k_len, lib=lib)
+    assert np.array_equal(m, mg) and np.array_equal(nxt, ng)
+
+
+# ---------------------------------------------------------------------------
 # controller (Eq. 6-8)
 # ---------------------------------------------------------------------------
 
@@ -719,6 +843,8 @@ ALL_PINS = [pin_verify_matches_sdpa, pin_verify_value_one, pin_verify_zero_keys_
             pin_select_special_cases, pin_draft_matches_sdpa, pin_draft_full_equals_dense,
             pin_draft_permutation, pin_draft_step_first_matches_sdpa,
             pin_draft_step_worked_example, pin_draft_step_value_one, pin_draft_step_heads, pin_row_stats_library,
-            pin_row_stats_closed_forms, pin_greedy_accept_worked, pin_head_scores_match_softmax,
+            pin_row_stats_closed_forms, pin_greedy_accept_worked, pin_spec_accept_worked,
+            pin_spec_accept_identical_distributions, pin_spec_accept_preserves_target_distribution,
+            pin_spec_accept_temperature, pin_spec_accept_greedy_limit, pin_head_scores_match_softmax,
             pin_draft_heads,
             pin_controller_closed_forms, pin_controller_observe, pin_controller_argmax]

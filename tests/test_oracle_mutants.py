@@ -16,6 +16,19 @@ _SRC = os.path.join(os.path.dirname(oracle.__file__), "oracle.c")
 
 # (name, text in oracle.c, replacement)
 MUTANTS = [
+    ("spec_residual_unclipped", "w[i] = r > 0.0 ? r : 0.0;", "w[i] = r;"),
+    ("spec_accept_inverted", "if (!(u_acc[(size_t)b * max_k + m] * q < p)) break;",
+     "if (!(u_acc[(size_t)b * max_k + m] * p < q)) break;"),
+    ("spec_accept_ratio_capped_low", "if (!(u_acc[(size_t)b * max_k + m] * q < p)) break;",
+     "if (!(u_acc[(size_t)b * max_k + m] < 0.5 * p / q)) break;"),
+    ("spec_bonus_from_last_draft_row",
+     "const float *t = tlogits + ((size_t)b * (max_k + 1) + m) * row_stride;\n        double mt, zt;",
+     "const float *t = tlogits + ((size_t)b * (max_k + 1) + (m == k && m > 0 ? m - 1 : m)) * row_stride;\n        double mt, zt;"),
+    ("spec_residual_from_target_only", "const double r = row_prob(t, i, tau, mt, zt) - row_prob(d, i, tau, md, zd);",
+     "const double r = row_prob(t, i, tau, mt, zt);"),
+    ("spec_draft_tau_ignored", "const double q = row_prob(d, x, tau, md, zd);",
+     "const double q = row_prob(d, x, 1.0, md, zd);"),
+    ("spec_inversion_ge", "if (run > target) return i;", "if (run >= target) return i;"),
     ("drop_softmax_scale", "x[i] = sm_scale * dot;", "x[i] = dot;"),
     ("gqa_head_interleaved", "const int h = c * g + hh;", "const int h = hh * n_kv_heads + c;"),
     ("causal_off_by_one", "const int p = T - nq + j;", "const int p = T - nq + j - 1;"),
