@@ -462,7 +462,8 @@ int ssl_draft_step_paged(const ssl_shape *shape, const ssl_params *params,
  * below take them in nats); the verification stage (Sec. 2.1) keeps the
  * longest prefix of drafted tokens the target model agrees with and adds one
  * token of its own.  The paper does not spell out the acceptance rule; these
- * calls implement the greedy one.
+ * calls implement the greedy one, and ssl_spec_accept below the speculative
+ * sampling one.
  *
  * Logit rows: logits[r][0..row_stride) of n_rows rows, bf16 (SSL_DT_BF16) or
  * fp32 (SSL_DT_F32); entries [0, vocab) are the logits, the rest is padding
@@ -497,6 +498,36 @@ int ssl_greedy_accept(const void *logits, int32_t dtype, int32_t batch, int32_t 
                       const int32_t *k_len_host, int32_t vocab, int32_t row_stride,
                       const int32_t *draft_tokens, int32_t *n_accepted, int32_t *next_token,
                       void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Speculative sampling: the verification rule that keeps the target model's
+ * output distribution (Sec. 1 and Sec. 2.1 rely on it; the paper does not
+ * print it).  Sequence b drafted k = k_len_host[b] <= max_k <= 63 tokens
+ * x_j = draft_tokens[b][j] ([batch][max_k]) from the drafter's logit rows
+ * draft_logits[b][j] ([batch][max_k][row_stride]); its verify pass gave the
+ * target rows target_logits[b][0..k] ([batch][max_k + 1][row_stride]).  With
+ * p_j = softmax(target row j / temperature), q_j = softmax(drafter row j /
+ * temperature) and the caller's uniforms in [0, 1), u_accept[b][j]
+ * ([batch][max_k]) and u_sample[b] ([batch]):
+ *   drafted token j passes when u_accept[b][j] * q_j(x_j) < p_j(x_j);
+ *   n_accepted[b] = m, the number that pass before the first that fails;
+ *   next_token[b] = the smallest x whose cumulative mass (index order)
+ *   exceeds u_sample[b] times the total, of max(0, p_m - q_m) when m < k
+ *   (of p_m if that has no mass), of p_k when all k passed.
+ * Both logit tensors have the dtype and layout rules of ssl_logit_stats; rows
+ * past a sequence's k (+1 for the target) are not read.  The arithmetic is
+ * fp32: decisions within fp32 rounding of a boundary may go either way.
+ * temperature must be finite and > 0 (greedy verification is
+ * ssl_greedy_accept).  Token ids are clamped into [0, vocab).  Errors as
+ * ssl_greedy_accept, plus SSL_ERR_SHAPE for the temperature.
+ */
+int ssl_spec_accept_workspace(int32_t batch, int32_t max_k, int32_t vocab, size_t *bytes_out);
+int ssl_spec_accept(const void *target_logits, const void *draft_logits, int32_t dtype,
+                    int32_t batch, int32_t max_k, const int32_t *k_len_host, int32_t vocab,
+                    int32_t row_stride, const int32_t *draft_tokens, float temperature,
+                    const float *u_accept, const float *u_sample, int32_t *n_accepted,
+                    int32_t *next_token, void *workspace, size_t workspace_bytes,
+                    hipStream_t stream);
 
 /*
  * Adaptive speculation length (Sec. 3.3), host only.

@@ -43,7 +43,7 @@ EXPORTED = [
     "ssl_draft_materialize", "ssl_draft_step_workspace", "ssl_draft_step",
     "ssl_draft_materialize_paged", "ssl_draft_step_paged",
     "ssl_logit_stats_workspace", "ssl_logit_stats", "ssl_greedy_accept_workspace",
-    "ssl_greedy_accept",
+    "ssl_greedy_accept", "ssl_spec_accept_workspace", "ssl_spec_accept",
     "ssl_ctrl_create", "ssl_ctrl_destroy", "ssl_ctrl_observe", "ssl_ctrl_accept_prob",
     "ssl_ctrl_choose_k", "ssl_ctrl_get_state", "ssl_ctrl_set_state",
 ]
@@ -142,6 +142,9 @@ def load(path: Optional[str] = None):
     lib.ssl_greedy_accept_workspace.argtypes = [_i32, _i32, _i32, _szp]
     lib.ssl_greedy_accept.argtypes = [_vp, _i32, _i32, _i32, _i32p, _i32, _i32, _vp, _vp, _vp,
                                       _vp, _sz, _vp]
+    lib.ssl_spec_accept_workspace.argtypes = [_i32, _i32, _i32, _szp]
+    lib.ssl_spec_accept.argtypes = [_vp, _vp, _i32, _i32, _i32, _i32p, _i32, _i32, _vp,
+                                    ctypes.c_float, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
     for f in ("ssl_verify_workspace", "ssl_verify_plan", "ssl_verify_attn",
               "ssl_verify_attn_static", "ssl_select_workspace",
               "ssl_select_topb", "ssl_select_plan", "ssl_select_draft_workspace",
@@ -149,7 +152,8 @@ def load(path: Optional[str] = None):
               "ssl_draft_step_workspace", "ssl_draft_step", "ssl_verify_attn_paged",
               "ssl_draft_attn_paged", "ssl_draft_materialize_paged", "ssl_draft_step_paged",
               "ssl_logit_stats_workspace",
-              "ssl_logit_stats", "ssl_greedy_accept_workspace", "ssl_greedy_accept"):
+              "ssl_logit_stats", "ssl_greedy_accept_workspace", "ssl_greedy_accept",
+              "ssl_spec_accept_workspace", "ssl_spec_accept"):
         getattr(lib, f).restype = ctypes.c_int
     lib.ssl_ctrl_create.argtypes = [ctypes.c_double, _i32p, ctypes.c_int32, ctypes.c_int32]
     lib.ssl_ctrl_create.restype = _vp
@@ -840,6 +844,44 @@ def greedy_accept(logits: torch.Tensor, draft_tokens: torch.Tensor, k_len_host,
                                     kl.ctypes.data_as(_i32p), V, stride, _ptr(draft_tokens),
                                     _ptr(m), _ptr(nxt), _ptr(ws), ws.numel(), _stream(stream)),
            "ssl_greedy_accept")
+    return m, nxt
+
+
+def spec_accept(target_logits: torch.Tensor, draft_logits: torch.Tensor,
+                draft_tokens: torch.Tensor, k_len_host, temperature: float,
+                u_accept: torch.Tensor, u_sample: torch.Tensor, vocab: Optional[int] = None,
+                stream=None):
+    """Speculative sampling: target_logits [batch, max_k + 1, row_stride],
+    draft_logits [batch, max_k, row_stride] (same dtype), draft_tokens
+    [batch, max_k] int32, u_accept [batch, max_k] and u_sample [batch] float32
+    uniforms in [0, 1); returns (n_accepted, next_token) int32 [batch]."""
+    _need_gpu(target_logits, draft_logits, draft_tokens, u_accept, u_sample)
+    batch, rows, stride = target_logits.shape
+    max_k = rows - 1
+    if not target_logits.is_contiguous() or not draft_logits.is_contiguous():
+        raise ValueError("logits must be contiguous")
+    if draft_logits.dtype != target_logits.dtype or \
+            tuple(draft_logits.shape) != (batch, max_k, stride):
+        raise ValueError("draft_logits must be [batch, max_k, row_stride] of the target's dtype")
+    if draft_tokens.dtype != torch.int32 or tuple(draft_tokens.shape) != (batch, max_k):
+        raise ValueError("draft_tokens must be int32 [batch, max_k]")
+    if u_accept.dtype != torch.float32 or tuple(u_accept.shape) != (batch, max_k) or \
+            u_sample.dtype != torch.float32 or tuple(u_sample.shape) != (batch,):
+        raise ValueError("u_accept float32 [batch, max_k], u_sample float32 [batch]")
+    V = stride if vocab is None else vocab
+    kl = _host_i32(k_len_host)
+    m = torch.empty(batch, dtype=torch.int32, device=target_logits.device)
+    nxt = torch.empty(batch, dtype=torch.int32, device=target_logits.device)
+    n = ctypes.c_size_t(0)
+    _check(load().ssl_spec_accept_workspace(batch, max_k, V, ctypes.byref(n)),
+           "ssl_spec_accept_workspace")
+    ws = torch.empty(max(int(n.value), 1), dtype=torch.uint8, device=target_logits.device)
+    _check(load().ssl_spec_accept(_ptr(target_logits), _ptr(draft_logits),
+                                  _logit_dtype(target_logits), batch, max_k,
+                                  kl.ctypes.data_as(_i32p), V, stride, _ptr(draft_tokens),
+                                  float(temperature), _ptr(u_accept), _ptr(u_sample), _ptr(m),
+                                  _ptr(nxt), _ptr(ws), ws.numel(), _stream(stream)),
+           "ssl_spec_accept")
     return m, nxt
 
 

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(HERE, LIB_NAME)
 ARCH = "gfx950"
 
 HIP_SOURCES = ["verify.hip", "verify_fused.hip", "select.hip", "draft.hip", "logits.hip",
-               "status.hip", "static_scratch.hip"]
+               "spec.hip", "status.hip", "static_scratch.hip"]
 CXX_SOURCES = ["api.cpp", "controller.cpp"]
 
 

@@ -1400,3 +1400,90 @@ int ssl_greedy_accept(const void* logits, int32_t dtype, int32_t batch, int32_t 
 }
 
 }  // extern "C"
+
+namespace {
+
+// Speculative sampling workspace: chunk and row statistics of the 2 max_k + 1
+// rows of every sequence, the picked positions and the chunk masses.
+struct SpecPlan {
+    int n_chunks;
+    size_t chunk_off, row_off, pick_off, mass_off, bytes;
+};
+
+int plan_spec(int32_t batch, int32_t max_k, int32_t vocab, SpecPlan* plan) {
+    if (batch < 1 || max_k < 0 || vocab < 1) return SSL_ERR_SHAPE;
+    if (batch > kTableBatch || max_k > kAcceptMaxK) return SSL_ERR_UNSUPPORTED;
+    if (vocab > kLogitChunk * kLogitMaxChunks) return SSL_ERR_UNSUPPORTED;
+    plan->n_chunks = (vocab + kLogitChunk - 1) / kLogitChunk;
+    const size_t rows = (size_t)batch * (2 * max_k + 1);
+    plan->chunk_off = kEpochBytes;
+    plan->row_off = plan->chunk_off + align_up(rows * plan->n_chunks * sizeof(float2));
+    plan->pick_off = plan->row_off + align_up(rows * sizeof(float2));
+    plan->mass_off = plan->pick_off + align_up((size_t)batch * sizeof(int32_t));
+    plan->bytes = plan->mass_off + align_up((size_t)batch * plan->n_chunks * sizeof(float2));
+    return SSL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ssl_spec_accept_workspace(int32_t batch, int32_t max_k, int32_t vocab, size_t* bytes_out) {
+    if (!bytes_out) return SSL_ERR_NULL;
+    SpecPlan plan;
+    const int rc = plan_spec(batch, max_k, vocab, &plan);
+    if (rc) return rc;
+    *bytes_out = plan.bytes;
+    return SSL_OK;
+}
+
+int ssl_spec_accept(const void* target_logits, const void* draft_logits, int32_t dtype,
+                    int32_t batch, int32_t max_k, const int32_t* k_len_host, int32_t vocab,
+                    int32_t row_stride, const int32_t* draft_tokens, float temperature,
+                    const float* u_accept, const float* u_sample, int32_t* n_accepted,
+                    int32_t* next_token, void* workspace, size_t workspace_bytes,
+                    hipStream_t stream) {
+    SpecPlan plan;
+    int rc = plan_spec(batch, max_k, vocab, &plan);
+    if (rc) return rc;
+    if (!(temperature > 0.f) || !isfinite(temperature) || !isfinite(1.0f / temperature))
+        return SSL_ERR_SHAPE;
+    rc = check_logits(target_logits, dtype, vocab, row_stride);
+    if (rc) return rc;
+    if (max_k > 0) {
+        rc = check_logits(draft_logits, dtype, vocab, row_stride);
+        if (rc) return rc;
+    }
+    if (!k_len_host || !u_sample || !n_accepted || !next_token ||
+        (max_k > 0 && (!draft_tokens || !u_accept)))
+        return SSL_ERR_NULL;
+    for (int b = 0; b < batch; ++b)
+        if (k_len_host[b] < 0 || k_len_host[b] > max_k) return SSL_ERR_SHAPE;
+    if (!aligned(u_sample, 4) || !aligned(n_accepted, 4) || !aligned(next_token, 4) ||
+        (draft_tokens && !aligned(draft_tokens, 4)) || (u_accept && !aligned(u_accept, 4)))
+        return SSL_ERR_ALIGN;
+    rc = check_workspace(workspace, workspace_bytes, plan.bytes);
+    if (rc) return rc;
+    char* ws = static_cast<char*>(workspace);
+    SpecArgs a = {};
+    a.tlogits = target_logits;
+    a.dlogits = draft_logits;
+    a.vocab = vocab;
+    a.row_stride = row_stride;
+    a.n_chunks = plan.n_chunks;
+    a.max_k = max_k;
+    a.inv_tau = 1.0f / temperature;
+    a.draft = draft_tokens;
+    a.u_acc = u_accept;
+    a.u_smp = u_sample;
+    a.n_accepted = n_accepted;
+    a.next_token = next_token;
+    a.chunk_ms = reinterpret_cast<float2*>(ws + plan.chunk_off);
+    a.row_ms = reinterpret_cast<float2*>(ws + plan.row_off);
+    a.pick = reinterpret_cast<int32_t*>(ws + plan.pick_off);
+    a.mass = reinterpret_cast<float2*>(ws + plan.mass_off);
+    for (int b = 0; b < batch; ++b) a.k_len[b] = k_len_host[b];
+    return hip_rc(launch_spec_accept(a, batch, dtype == SSL_DT_F32, stream));
+}
+
+}  // extern "C"

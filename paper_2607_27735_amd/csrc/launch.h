@@ -266,4 +266,26 @@ struct AcceptArgs {
 hipError_t launch_logit_stats(const LogitArgs& a, bool f32, hipStream_t stream);
 hipError_t launch_greedy_accept(const AcceptArgs& a, int batch, hipStream_t stream);
 
+// Speculative sampling.  Rows of sequence b: target rows 0..max_k of tlogits
+// ([batch][max_k + 1][row_stride]) and drafter rows 0..max_k-1 of dlogits
+// ([batch][max_k][row_stride]); in the tables below they are rows
+// 0..2 max_k of the sequence (drafter row j at max_k + 1 + j).
+struct SpecArgs {
+    const void* tlogits;
+    const void* dlogits;
+    int32_t vocab, row_stride, n_chunks, max_k;
+    float inv_tau;           // 1 / temperature
+    const int32_t* draft;    // [batch][max_k]
+    const float* u_acc;      // [batch][max_k] uniforms in [0, 1)
+    const float* u_smp;      // [batch]
+    int32_t* n_accepted;     // [batch]
+    int32_t* next_token;     // [batch]
+    float2* chunk_ms;        // [batch][2 max_k + 1][n_chunks] (max, sum) of x / tau per chunk
+    float2* row_ms;          // [batch][2 max_k + 1] the same per row
+    int32_t* pick;           // [batch] the first failing position (or k)
+    float2* mass;            // [batch][n_chunks] (residual, target) mass per chunk
+    int32_t k_len[kTableBatch];
+};
+hipError_t launch_spec_accept(const SpecArgs& a, int batch, bool f32, hipStream_t stream);
+
 }  // namespace ssl

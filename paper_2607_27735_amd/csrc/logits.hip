@@ -20,6 +20,7 @@
 // workgroup per sequence over the rows' argmax.
 #include "device_common.h"
 #include "launch.h"
+#include "logit_common.h"
 
 namespace ssl {
 namespace {
@@ -62,41 +63,20 @@ __device__ __forceinline__ Stat wave_merge(Stat x) {
     return x;
 }
 
-// The 32 logits of thread `tid` in chunk `chunk` of a row: element indices
-// chunk * kChunk + (j * kThreads + tid) * kPer + e.  Loads are clamped into
-// the row's last 16-byte block and elements at or past vocab are masked.
+// The (max, sum, sum x e, argmax) of thread tid's 32 logits of chunk `chunk`
+// of a row (lc::load_chunk's layout).
 template <bool kF32>
 __device__ __forceinline__ Stat chunk_stat(const LogitArgs& a, int row, int chunk, int tid) {
-    constexpr int kPer = kF32 ? 4 : 8;            // logits per 16-byte load
-    constexpr int kLoads = 32 / kPer;
-    const int last_blk = (a.vocab - 1) / kPer;
-    const int blk0 = chunk * (kLogitChunk / kPer);
     const char* base = static_cast<const char*>(a.logits) +
                        (size_t)row * a.row_stride * (kF32 ? 4 : 2);
-    uint4 raw[kLoads];
-#pragma unroll
-    for (int j = 0; j < kLoads; ++j) {
-        const int blk = min(blk0 + j * kThreads + tid, last_blk);
-        raw[j] = *reinterpret_cast<const uint4*>(base + (size_t)blk * 16);
-    }
     float x[32];
-#pragma unroll
-    for (int j = 0; j < kLoads; ++j) {
-        const uint32_t w[4] = {raw[j].x, raw[j].y, raw[j].z, raw[j].w};
-#pragma unroll
-        for (int e = 0; e < kPer; ++e) {
-            const int i = (blk0 + j * kThreads + tid) * kPer + e;
-            float v = kF32 ? __builtin_bit_cast(float, w[e])
-                           : ((e & 1) ? bf16_hi(w[e >> 1]) : bf16_lo(w[e >> 1]));
-            x[j * kPer + e] = i < a.vocab ? v : -INFINITY;
-        }
-    }
+    lc::load_chunk<kF32>(base, a.vocab, chunk, tid, x);
     Stat st;
     st.m = -INFINITY;
     st.a = 0x7fffffff;
 #pragma unroll
     for (int q = 0; q < 32; ++q) {
-        const int i = (blk0 + (q / kPer) * kThreads + tid) * kPer + (q % kPer);
+        const int i = lc::elem<kF32>(chunk, q, tid);
         if (x[q] > st.m) {   // elements in increasing index order: the first max stays
             st.m = x[q];
             st.a = i;

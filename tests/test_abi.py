@@ -329,6 +329,33 @@ def test_greedy_accept_validation(lib):
     assert call(ws=None) == B.SSL_ERR_WORKSPACE
 
 
+def test_spec_accept_validation(lib):
+    n = ctypes.c_size_t(0)
+    assert lib.ssl_spec_accept_workspace(4, 6, 128256, ctypes.byref(n)) == 0 and n.value > 65536
+    assert lib.ssl_spec_accept_workspace(65, 6, 100, ctypes.byref(n)) == B.SSL_ERR_UNSUPPORTED
+    assert lib.ssl_spec_accept_workspace(1, 64, 100, ctypes.byref(n)) == B.SSL_ERR_UNSUPPORTED
+    assert lib.ssl_spec_accept_workspace(1, 4, (1 << 19) + 1, ctypes.byref(n)) == B.SSL_ERR_UNSUPPORTED
+    assert lib.ssl_spec_accept_workspace(0, 4, 100, ctypes.byref(n)) == B.SSL_ERR_SHAPE
+
+    def call(k=(6, 2), max_k=6, tau=1.0, tl=FAKE, dl=FAKE, dtype=0, stride=128256, draft=FAKE,
+             ua=FAKE, us=FAKE, m=FAKE, nxt=FAKE, ws=FAKE, ws_bytes=1 << 40):
+        ka, kp = _i32(*k)
+        return lib.ssl_spec_accept(tl, dl, dtype, len(k), max_k, kp, 128256, stride, draft, tau,
+                                   ua, us, m, nxt, ws, ws_bytes, None)
+    for tau in (0.0, -1.0, float("nan"), float("inf"), 1e-39):
+        assert call(tau=tau) == B.SSL_ERR_SHAPE, tau
+    assert call(k=(7, 2)) == B.SSL_ERR_SHAPE
+    assert call(dtype=5) == B.SSL_ERR_SHAPE
+    assert call(stride=100) == B.SSL_ERR_SHAPE
+    assert call(stride=128257) == B.SSL_ERR_ALIGN        # rows must stay 16-byte aligned
+    for name in ("tl", "dl", "draft", "ua", "us", "m", "nxt"):
+        assert call(**{name: None}) == B.SSL_ERR_NULL, name
+    assert call(m=FAKE + 2) == B.SSL_ERR_ALIGN
+    assert call(ws=None) == B.SSL_ERR_WORKSPACE
+    # nothing drafted anywhere: the drafter's rows, tokens and pass uniforms are not needed
+    assert call(k=(0, 0), max_k=0, dl=None, draft=None, ua=None, ws=None) == B.SSL_ERR_WORKSPACE
+
+
 def test_paged_validation(lib):
     s, p = _shape(), _params()
     ca, cp = _i32(4000)
