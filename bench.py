@@ -88,6 +88,15 @@ def is_paged(short: str) -> bool:
     return k == "draft_kernel" and args[0] == "3"
 
 
+def is_step_kernel(short: str) -> bool:
+    """Whether a kernel (short name with template arguments) is the one-kernel
+    decode step: the verify kernel's fourth template flag."""
+    if not short.startswith("verify_fused_kernel<"):
+        return False
+    args = [x.strip() for x in short.split("<", 1)[1].rstrip(">").split(",")]
+    return len(args) == 4 and args[3] == "true"
+
+
 def summarize_trace(d: str, command: str, title: str = "") -> str:
     """Markdown table of a rocprofv3 --kernel-trace --stats run."""
     import csv
@@ -104,10 +113,7 @@ def summarize_trace(d: str, command: str, title: str = "") -> str:
         short = kernel_short(r["Name"])
         k = short.split("<")[0]
         mode = short.split("<", 1)[1].split(",")[0].strip(" >") if "<" in short else ""
-        step_kernel = (k == "verify_fused_kernel" and "<" in short
-                       and short.rstrip(">").split(",")[-1].strip() == "true"
-                       and len(short.split(",")) == 4)
-        call = ("decode step (one kernel)" if step_kernel
+        call = ("decode step (one kernel)" if is_step_kernel(short)
                 else "verify (paged)" if k.startswith("verify") and is_paged(short)
                 else "draft (paged)" if is_paged(short)
                 else "verify" if k.startswith("verify") else "select" if k.startswith("select")
@@ -259,10 +265,22 @@ def vocab_side_bench(B, w, stream, reps, torch, np, vocab=128256):
     aargs = [(c.data_ptr(), B.SSL_DT_BF16, w.batch, k, k_len.ctypes.data_as(B._i32p), vocab, vocab,
               draft.data_ptr(), m.data_ptr(), nxt.data_ptr(), ws2.data_ptr(), ws2.numel(),
               B._stream(stream)) for c in copies]
+    # speculative sampling: the k + 1 verify rows of each sequence as the
+    # target, the first k rows of the next copy as the drafter's rows
+    u_acc = torch.from_numpy(rng.random((w.batch, k)).astype(np.float32)).to(dev)
+    u_smp = torch.from_numpy(rng.random(w.batch).astype(np.float32)).to(dev)
+    B._check(lib.ssl_spec_accept_workspace(w.batch, k, vocab, ctypes.byref(nws)), "ws")
+    ws3 = torch.empty(max(nws.value, 1), dtype=torch.uint8, device=dev)
+    pargs = [(c.data_ptr(), copies[(i + 1) % n].data_ptr(), B.SSL_DT_BF16, w.batch, k,
+              k_len.ctypes.data_as(B._i32p), vocab, vocab, draft.data_ptr(), 1.0,
+              u_acc.data_ptr(), u_smp.data_ptr(), m.data_ptr(), nxt.data_ptr(), ws3.data_ptr(),
+              ws3.numel(), B._stream(stream)) for i, c in enumerate(copies)]
     for a in sargs:
         B._check(lib.ssl_logit_stats(*a), "ssl_logit_stats")
     for a in aargs:
         B._check(lib.ssl_greedy_accept(*a), "ssl_greedy_accept")
+    for a in pargs:
+        B._check(lib.ssl_spec_accept(*a), "ssl_spec_accept")
 
     def timed(fn):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -276,12 +294,14 @@ def vocab_side_bench(B, w, stream, reps, torch, np, vocab=128256):
 
     ent_us = timed(lambda r: lib.ssl_logit_stats(*sargs[r % n]))
     acc_us = timed(lambda r: lib.ssl_greedy_accept(*aargs[r % n]))
+    spec_us = timed(lambda r: lib.ssl_spec_accept(*pargs[r % n]))
     eb, ab = draft_rows * vocab * 2, verify_rows * vocab * 2
     return {"vocab": vocab, "logits": "bf16, N(0, 2^2), seeded",
             "entropy_rows": draft_rows, "entropy_us": round(ent_us, 3),
             "entropy_gbps": round(eb / (ent_us * 1e-6) / 1e9, 1),
             "accept_rows": verify_rows, "accept_us": round(acc_us, 3),
             "accept_gbps": round(ab / (acc_us * 1e-6) / 1e9, 1),
+            "spec_accept_rows": verify_rows + draft_rows, "spec_accept_us": round(spec_us, 3),
             "timing": f"{reps} back-to-back calls per figure between two HIP events, "
                       f"rotating {n} logit copies"}
 
@@ -401,14 +421,18 @@ def summarize_traffic(fetch_dir: str, write_dir: str, copy_mib: int, command: st
              f"copy_write_kib = {statistics.fmean(cw):.1f}",
              f"fetch_factor = {f_fac:.4f}",
              f"write_factor = {w_fac:.4f}"]
-    call_bytes = 0.0
+    call_bytes = step_bytes = 0.0
     for k in sorted(set(fetch) | set(write)):
         fb = fetch.get(k, 0.0) * 1024.0 * f_fac
         wb = write.get(k, 0.0) * 1024.0 * w_fac
         lines.append(f"{k} = fetch {fb:.0f} write {wb:.0f} bytes per launch")
-        if k.split("<")[0] in VERIFY_KERNELS and not is_paged(k):
+        if is_step_kernel(k):
+            step_bytes += fb + wb
+        elif k.split("<")[0] in VERIFY_KERNELS and not is_paged(k):
             call_bytes += fb + wb
     lines.append(f"verify_call_traffic_bytes = {call_bytes:.0f}")
+    if step_bytes:
+        lines.append(f"decode_step_kernel_traffic_bytes = {step_bytes:.0f}")
     return "\n".join(lines) + "\n"
 
 
