@@ -113,7 +113,9 @@ def summarize_trace(d: str, command: str, title: str = "") -> str:
         short = kernel_short(r["Name"])
         k = short.split("<")[0]
         mode = short.split("<", 1)[1].split(",")[0].strip(" >") if "<" in short else ""
+        sel_draft = k == "select_fused_kernel" and short.rstrip(">").endswith("true")
         call = ("decode step (one kernel)" if is_step_kernel(short)
+                else "select + first draft step (one kernel)" if sel_draft
                 else "verify (paged)" if k.startswith("verify") and is_paged(short)
                 else "draft (paged)" if is_paged(short)
                 else "verify" if k.startswith("verify") else "select" if k.startswith("select")
