@@ -64,7 +64,7 @@ __device__ __forceinline__ void stats_tile(const VerifyArgs& a, const Rows<NRT>&
 
 template <int NRT, bool kPaged>
 __global__ __launch_bounds__(kThreads) void verify_stats_kernel(VerifyArgs a) {
-    const Item it = decode_item(a, a.seq, blockIdx.x, a.chunk);
+    const Item it = decode_item<true>(a, a.seq, blockIdx.x, a.chunk);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int m16 = lane & 15, G = lane >> 4;
     Rows<NRT> r;
@@ -201,7 +201,7 @@ __device__ __forceinline__ void main_tile(const VerifyArgs& a, const Rows<NRT>& 
 
 template <int NRT, bool kPaged, bool kPerHead>
 __global__ __launch_bounds__(kThreads) void verify_main_kernel(VerifyArgs a) {
-    const Item it = decode_item(a, a.seq, blockIdx.x, a.chunk);
+    const Item it = decode_item<true>(a, a.seq, blockIdx.x, a.chunk);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int m16 = lane & 15, G = lane >> 4;
 

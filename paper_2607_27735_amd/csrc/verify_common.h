@@ -192,23 +192,27 @@ struct KVTile {
 // A work item: (sequence b, KV head c, key chunk s) of a launch whose items
 // are numbered sequence by sequence, head by head, chunk by chunk.  bt is the
 // sequence's entry in the launch's tables, b the sequence itself (a.sid[bt]).
+// A launch over whole sequences (kBlocks false: sid[bt] = bt, qoff 0, qfull
+// the sequence's q_len) skips those tables, so that the first K/V addresses do
+// not wait for one more dependent load of the launch arguments.
 struct Item {
     int b, bt, c, s, nchunk, T, nq, qoff, qfull, key_begin, key_end, unit, item0;
 };
 
+template <bool kBlocks>
 __device__ __forceinline__ Item decode_item(const VerifyArgs& a, const SeqTable& st, int item,
                                             int chunk) {
     const int n_kv = a.n_kv_heads;
     Item it;
     int bt = 0;
     while (bt + 1 < st.n_seq && item >= st.item_start[bt + 1]) ++bt;
-    const int b = a.sid[bt];
+    const int b = kBlocks ? a.sid[bt] : bt;
     it.b = b;
     it.bt = bt;
     it.T = st.ctx[bt];
     it.nq = st.qlen[bt];
-    it.qoff = a.qoff[bt];
-    it.qfull = a.qfull[bt];
+    it.qoff = kBlocks ? a.qoff[bt] : 0;
+    it.qfull = kBlocks ? a.qfull[bt] : it.nq;
     it.nchunk = (it.T + chunk - 1) / chunk;
     const int local = item - st.item_start[bt];
     it.c = local / it.nchunk;

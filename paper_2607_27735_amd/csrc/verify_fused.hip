@@ -81,13 +81,19 @@ __device__ __forceinline__ bool wait_unit(const uint64_t* tag, int n, uint64_t w
     const uint64_t* p0 = tag + min(lane, n - 1);
     const uint64_t* p1 = tag + min(lane + kWave, n - 1);
     const bool use1 = lane + kWave < n;
-    uint64_t c0 = ld_dev64(p0), c1 = ld_dev64(p1);
-    for (int spins = 0; spins < spin_limit; ++spins) {
-        const uint64_t n0 = ld_dev64(p0), n1 = ld_dev64(p1);
-        if (__all(c0 == want && (!use1 || c1 == want))) return true;
+    // Two polls alternate between two register pairs, each reloaded only after
+    // its check: a loop that copied the newer poll into the older one's
+    // registers would wait for that poll to land at every turn (the copy
+    // needs the value), and only one poll would be in flight.
+    uint64_t a0 = ld_dev64(p0), a1 = ld_dev64(p1);
+    for (int spins = 0; spins < spin_limit; spins += 2) {
+        const uint64_t b0 = ld_dev64(p0), b1 = ld_dev64(p1);
+        if (__all(a0 == want && (!use1 || a1 == want))) return true;
         __builtin_amdgcn_s_sleep(1);
-        c0 = n0;
-        c1 = n1;
+        a0 = ld_dev64(p0);
+        a1 = ld_dev64(p1);
+        if (__all(b0 == want && (!use1 || b1 == want))) return true;
+        __builtin_amdgcn_s_sleep(1);
     }
     return false;
 }
@@ -196,7 +202,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     __shared__ int wait_failed;
 
     const int slot = blockIdx.x;
-    const Item it = decode_item(a, a.seq, slot, a.chunk);
+    const Item it = decode_item<false>(a, a.seq, slot, a.chunk);
     const int unit = it.unit, b = it.b, c = it.c;
     const int slot0 = it.item0, nchunk = it.nchunk;
     const int T = it.T, nq = it.nq;
