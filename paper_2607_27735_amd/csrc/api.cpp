@@ -170,7 +170,7 @@ struct VerifyPlan {
     int block_pos;   // verify positions per launch (row blocks); >= every q_len when one block
     bool fused_ok;
     int fused_chunk, fused_slots;
-    size_t ml_off, o_off, tag_off, bytes;
+    size_t ml_off, o_off, bytes;
     SeqTable seq;
     SeqTable fseq;   // the one-sweep slots as items
 };
@@ -263,10 +263,10 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
     }
     if (p->verify_mode == SSL_VERIFY_ONE_SWEEP && !plan->fused_ok) return SSL_ERR_UNSUPPORTED;
     const size_t slots_max = (size_t)std::max(plan->n_items, plan->fused_slots);
+    // per item and row: (max, sum), each word tagged in the one-sweep schedule
     plan->ml_off = kEpochBytes;
-    plan->o_off = plan->ml_off + align_up(slots_max * kVerifyRowCap * sizeof(float) * 2);
-    plan->tag_off = plan->o_off + align_up(slots_max * kVerifyRowCap * 128 * sizeof(float));
-    plan->bytes = plan->tag_off + align_up((size_t)plan->fused_slots * sizeof(uint64_t));
+    plan->o_off = plan->ml_off + align_up(slots_max * kVerifyRowCap * sizeof(uint64_t) * 2);
+    plan->bytes = plan->o_off + align_up(slots_max * kVerifyRowCap * 128 * sizeof(float));
     return SSL_OK;
 }
 
@@ -566,7 +566,6 @@ int verify_call(const ssl_shape* shape, const ssl_params* params, const int32_t*
         fa.v = a;
         fa.v.chunk = plan.fused_chunk;
         fa.v.seq = plan.fseq;
-        fa.tag = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + plan.tag_off);
         rc = epochs_if_captured(stream, workspace, (int64_t)shape->batch * shape->n_kv_heads, &fa.epoch);
         if (rc) return rc;
         rc = make_exchange(&fa.xc);
@@ -1063,7 +1062,6 @@ int ssl_decode_step(const ssl_shape* shape, const ssl_params* params, const int3
         a.sid[b] = b;
         a.qfull[b] = q_len_host[b];
     }
-    fa.tag = reinterpret_cast<uint64_t*>(ws + vp.tag_off);
     const int64_t units = (int64_t)shape->batch * shape->n_kv_heads;
     rc = epochs_if_captured(stream, workspace, units, &fa.epoch);
     if (rc) return rc;

@@ -62,7 +62,8 @@ struct VerifyArgs {
     const uint16_t* q;
     const uint16_t* k;
     const uint16_t* v;
-    float2* part_ml;    // [n_items][64]  per-split (max, sum) in the log2 domain
+    float2* part_ml;    // [n_items][64]  per-split (max, sum) in the log2 domain (two
+                        // sweeps; the one-sweep kernel keeps a tagged word pair per row)
     float* part_o;      // [n_items][64][128] per-split sum of P * V
     float* scores;      // [batch][n_kv][max_ctx]
     void* out;          // [batch][max_q][n_q][128]
@@ -172,8 +173,7 @@ struct DraftArgs {
 // Single-sweep verify: the slots (items of v.seq / v.chunk) of one KV-head
 // unit must be resident at once.
 struct FusedArgs {
-    VerifyArgs v;           // part_ml / part_o indexed by slot
-    uint64_t* tag;          // [n_slots] publication tags (no initialisation needed)
+    VerifyArgs v;           // part_ml ([slot][64] tagged (max, sum) word pairs) / part_o by slot
     uint64_t* epoch;        // [units] exchange epochs (any initial value), or null
     uint64_t call_tag;      // this call's tag: unique within the process (see exchange_tag)
     Exchange xc;

@@ -8,9 +8,11 @@
 //      softmax per verify row (P.V on the MFMA, as in the two-sweep kernel);
 //      it keeps in LDS the probabilities of its keys relative to the running
 //      row maxima, and those maxima for every 32-key tile;
-//   2. it publishes its (running max, sum) per row and its partial P.V
-//      relative to those maxima, then a 64-bit call tag for its chunk, and
-//      waits until every chunk of its head shows the tag;
+//   2. it publishes its partial P.V relative to the running maxima and, once
+//      those stores have landed, its (running max, sum) per row, each 64-bit
+//      word carrying the low 32 bits of the call's exchange tag above the
+//      value; it then polls the (max, sum) words of every chunk of its head
+//      until all carry the tag, so the poll that finds them delivers them;
 //   3. from the merged (max, sum) of all chunks it forms one factor per tile
 //      and row, so that a stashed probability times its factor is the exact
 //      probability, and writes the scores of its keys;
@@ -20,10 +22,11 @@
 // Publication avoids agent-scope fences, which write back a whole L2 per wave
 // on this multi-XCD part: the published statistics and partials are written
 // and read with device-coherent (agent-scope relaxed atomic) stores and
-// loads, and every wave waits for its stores to complete before a tag is
-// written.  The tags need no initialisation: the host draws a fresh 64-bit tag
-// for every call from a process-wide sequence with a clock-seeded start, so a
-// stale or uninitialised word matches only by a 2^-64 accident.
+// loads, and every wave waits for its partial-output stores to complete
+// before the tagged statistics are written.  The tags need no initialisation:
+// the host draws a fresh tag for every call from a process-wide sequence with
+// a clock-seeded start (consecutive calls differ in the low 32 bits for 2^32
+// calls), so a stale or uninitialised word matches only by a 2^-32 accident.
 //
 // The wait ends: workgroups are dispatched in index order and the chunks of
 // one head are consecutive, so when the lowest unfinished head waits, every
@@ -50,7 +53,6 @@ constexpr float kLazy = 8.f;          // reference-maximum slack, log2 units
 template <int NRT>
 constexpr int static_lds_bytes() {
     return kWaves * NRT * 16 * 8            // wml
-           + kRowCap * 8                    // row_ml
            + kRowCap * 4                    // row_lse
            + kWaves * kRowCap * 8           // lse_part
            + 64;
@@ -68,35 +70,6 @@ constexpr int max_fused_chunk() {
 }
 
 __device__ __forceinline__ float safe_max(float m) { return m == -INFINITY ? 0.f : m; }
-
-// Wave 0 polls until tag[0 .. n) all equal `want` (true), or gives up after
-// spin_limit polls (false); the caller synchronises the workgroup afterwards.
-// Up to 128 tags (the most chunks a head may have here); the next poll is
-// issued before the previous one is checked, so that the last tag is seen
-// about one round trip after it lands rather than one and a half.
-__device__ __forceinline__ bool wait_unit(const uint64_t* tag, int n, uint64_t want, int spin_limit) {
-    const int lane = threadIdx.x & 63;
-    // every lane loads (lanes past n re-read the last tag): no branch around
-    // the loads, so the compiler need not wait for them where they are issued
-    const uint64_t* p0 = tag + min(lane, n - 1);
-    const uint64_t* p1 = tag + min(lane + kWave, n - 1);
-    const bool use1 = lane + kWave < n;
-    // Two polls alternate between two register pairs, each reloaded only after
-    // its check: a loop that copied the newer poll into the older one's
-    // registers would wait for that poll to land at every turn (the copy
-    // needs the value), and only one poll would be in flight.
-    uint64_t a0 = ld_dev64(p0), a1 = ld_dev64(p1);
-    for (int spins = 0; spins < spin_limit; spins += 2) {
-        const uint64_t b0 = ld_dev64(p0), b1 = ld_dev64(p1);
-        if (__all(a0 == want && (!use1 || a1 == want))) return true;
-        __builtin_amdgcn_s_sleep(1);
-        a0 = ld_dev64(p0);
-        a1 = ld_dev64(p1);
-        if (__all(b0 == want && (!use1 || b1 == want))) return true;
-        __builtin_amdgcn_s_sleep(1);
-    }
-    return false;
-}
 
 // One 32-key tile: online softmax and P.V; the tile's probabilities relative
 // to the rows' reference maxima go to the LDS stash, those maxima to mtile.
@@ -196,7 +169,6 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     const VerifyArgs& a = fa.v;
     extern __shared__ __attribute__((aligned(16))) float stash[];   // [NRT*16][chunk + pad]
     __shared__ float2 wml[kWaves][NRT * 16];
-    __shared__ float2 row_ml[kRowCap];
     __shared__ float row_lse[kRowCap];
     __shared__ float2 lse_part[kWaves][kRowCap];
     __shared__ int wait_failed;
@@ -256,16 +228,16 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         L[rt] += shfl_xor_f(L[rt], 32);
         if (G == 0) wml[wave][rt * 16 + m16] = make_float2(M[rt], L[rt]);
     }
+    if (tid == 0) wait_failed = 0;
     __syncthreads();
-    // the workgroup's row statistics, merged over its waves
+    // the workgroup's row statistics, merged over its waves (published below,
+    // once the partial output has landed)
+    float own_m = -INFINITY, own_l = 0.f;
     if (tid < R) {
-        float Mw = -INFINITY, Lw = 0.f;
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) Mw = fmaxf(Mw, wml[w][tid].x);
+        for (int w = 0; w < kWaves; ++w) own_m = fmaxf(own_m, wml[w][tid].x);
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) Lw += wml[w][tid].y * fast_exp2(wml[w][tid].x - safe_max(Mw));
-        st_dev64(reinterpret_cast<uint64_t*>(a.part_ml + (size_t)slot * kRowCap + tid),
-                 __builtin_bit_cast(uint64_t, make_float2(Mw, Lw)));
+        for (int w = 0; w < kWaves; ++w) own_l += wml[w][tid].y * fast_exp2(wml[w][tid].x - safe_max(own_m));
     }
     // the partial P.V relative to the workgroup's row maxima: per row tile,
     // waves 2 and 3 park theirs, waves 0 and 1 add them, park the sums, and
@@ -326,26 +298,78 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         }
     }
 
-    // ---- wait for every chunk of this (sequence, KV head) -------------------
+    // ---- publish the statistics; wait for every chunk of the head ----------
+    // Each (max, sum) word carries the low 32 bits of the exchange tag above
+    // the value, and is stored only once this workgroup's partial output has
+    // landed: a reader that finds every chunk's words tagged has the head's
+    // statistics from that one poll, and may then load the partial outputs.
     wait_stores_done();
     __syncthreads();
     const uint64_t epv = scalar_here(ep);
     const uint64_t want = exchange_tag(fa.call_tag, epv);
+    const uint64_t tag_hi = (want & 0xFFFFFFFFull) << 32;
+    uint64_t* ml64 = reinterpret_cast<uint64_t*>(a.part_ml);   // [slot][kRowCap][2]
     // a dirty epoch: an earlier captured call on this workspace gave up
     const bool clean = !epoch_is_dirty(epv);
-    if (clean && tid == 0) st_dev64(fa.tag + slot, want ^ fa.xc.tag_flip);
-    if (clean && wave == 0) {
-        const bool in = wait_unit(fa.tag + slot0, nchunk, want, fa.xc.spin_limit);
-        if (lane == 0) wait_failed = !in;
+    if (clean && tid < R) {
+        const uint64_t pub = ((want ^ fa.xc.tag_flip) & 0xFFFFFFFFull) << 32;
+        uint64_t* e = ml64 + ((size_t)slot * kRowCap + tid) * 2;
+        st_dev64(e, pub | __float_as_uint(own_m));
+        st_dev64(e + 1, pub | __float_as_uint(own_l));
+    }
+
+    // ---- 3a. exact row statistics over every chunk of the head -------------
+    // Wave w polls rows 0..63 of chunks w, w + 4, ... (eight chunks per
+    // round trip) until all their words carry the tag, then merges them.
+    // (One poll in flight per wave: two, issued half a round trip apart, load
+    // the memory system enough to cost more than the earlier sight gains.)
+    {
+        const int rr = tid & (kRowCap - 1), ph = tid >> 6;
+        float Mx = -INFINITY, Lx = 0.f;
+        bool in_all = clean;
+        for (int s0 = ph; in_all && s0 < nchunk; s0 += 8 * kWaves) {   // wave-uniform
+            uint64_t w0[8], w1[8];
+            // every lane loads (lanes past the rows or chunks re-read valid
+            // entries): no branch around the loads
+            const uint64_t* e[8];
+#pragma unroll
+            for (int uu = 0; uu < 8; ++uu)
+                e[uu] = ml64 + ((size_t)(slot0 + min(s0 + uu * kWaves, nchunk - 1)) * kRowCap + min(rr, R - 1)) * 2;
+            int spins = 0;
+            bool all_in;
+            do {
+                bool in = true;
+#pragma unroll
+                for (int uu = 0; uu < 8; ++uu) {
+                    w0[uu] = ld_dev64(e[uu]);
+                    w1[uu] = ld_dev64(e[uu] + 1);
+                }
+#pragma unroll
+                for (int uu = 0; uu < 8; ++uu)
+                    in &= ((w0[uu] & ~0xFFFFFFFFull) == tag_hi && (w1[uu] & ~0xFFFFFFFFull) == tag_hi);
+                all_in = __all(in);
+                if (!all_in) __builtin_amdgcn_s_sleep(1);
+            } while (!all_in && ++spins < fa.xc.spin_limit);
+            in_all = all_in;
+            if (all_in && rr < R) {
+#pragma unroll
+                for (int uu = 0; uu < 8; ++uu)
+                    if (s0 + uu * kWaves < nchunk)
+                        ml_merge(Mx, Lx, __uint_as_float((uint32_t)w0[uu]), __uint_as_float((uint32_t)w1[uu]));
+            }
+        }
+        if (!in_all && lane == 0) wait_failed = 1;
+        lse_part[ph][rr] = make_float2(Mx, Lx);
     }
     __syncthreads();
-    if (!clean || wait_failed) {
+    if (wait_failed) {
         if (tid == 0) exchange_gave_up(fa.xc, kStatusVerify, fa.epoch ? fa.epoch + unit : nullptr);
         return;
     }
 
     // The first chunks of this workgroup's first row in step 4 (all of them
-    // for up to 32 chunks), loaded now so that the round trip overlaps 3a, 3b.
+    // for up to 32 chunks), loaded now so that the round trip overlaps the
+    // normalizers and 3b.
     const int d4 = tid & 31, sg = tid >> 5;
     auto load_part = [&](int row, int s0, f32x4 (&v)[4], float (&m)[4]) {
 #pragma unroll
@@ -357,7 +381,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
                 const float2 lo = __builtin_bit_cast(float2, ld_dev64(s64));
                 const float2 hi = __builtin_bit_cast(float2, ld_dev64(s64 + 1));
                 v[uu] = f32x4{lo.x, lo.y, hi.x, hi.y};
-                m[uu] = __builtin_bit_cast(float2, ld_dev64(reinterpret_cast<const uint64_t*>(a.part_ml + rw))).x;
+                m[uu] = __uint_as_float((uint32_t)ld_dev64(ml64 + rw * 2));
             } else {
                 v[uu] = f32x4{0.f, 0.f, 0.f, 0.f};
                 m[uu] = -INFINITY;
@@ -368,33 +392,10 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     float pm[4];
     if (it.s < R) load_part(it.s, sg, pv, pm);
 
-    // ---- 3a. exact row statistics over every chunk of the head -------------
-    {
-        const int rr = tid & (kRowCap - 1), ph = tid >> 6;
-        float Mx = -INFINITY, Lx = 0.f;
-        if (rr < R) {
-            for (int s0 = ph; s0 < nchunk; s0 += 8 * kWaves) {
-                float2 v[8];
-#pragma unroll
-                for (int uu = 0; uu < 8; ++uu) {
-                    const int s2 = s0 + uu * kWaves;
-                    v[uu] = s2 < nchunk
-                                ? __builtin_bit_cast(float2, ld_dev64(reinterpret_cast<const uint64_t*>(
-                                                                 a.part_ml + (size_t)(slot0 + s2) * kRowCap + rr)))
-                                : make_float2(-INFINITY, 0.f);
-                }
-#pragma unroll
-                for (int uu = 0; uu < 8; ++uu) ml_merge(Mx, Lx, v[uu].x, v[uu].y);
-            }
-        }
-        lse_part[ph][rr] = make_float2(Mx, Lx);
-    }
-    __syncthreads();
     if (tid < kRowCap) {
         float Mx = -INFINITY, Lx = 0.f;
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) ml_merge(Mx, Lx, lse_part[w][tid].x, lse_part[w][tid].y);
-        row_ml[tid] = make_float2(Mx, Lx);
         row_lse[tid] = Lx > 0.f ? Mx + fast_log2(Lx) : INFINITY;
     }
     __syncthreads();
