@@ -45,11 +45,12 @@ def algorithmic_bytes(w, out_bytes: int):
 
 REPO = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(REPO, "profiles", "verify_traffic_llama8b_T32K.txt")
-OUR_KERNELS = ("verify_fused_kernel", "verify_stats_kernel", "verify_main_kernel",
+OUR_KERNELS = ("verify_fused_kernel", "verify_pipe_kernel", "verify_stats_kernel", "verify_main_kernel",
                "verify_combine_kernel", "select_hist_kernel", "select_mark_kernel",
                "select_finish_kernel", "select_fused_kernel", "draft_materialize_kernel",
-               "draft_kernel", "logit_stats_kernel", "greedy_accept_kernel")
-VERIFY_KERNELS = ("verify_fused_kernel", "verify_stats_kernel", "verify_main_kernel",
+               "draft_kernel", "logit_stats_kernel", "greedy_accept_kernel", "spec_stats_kernel",
+               "spec_rows_kernel", "spec_decide_kernel", "spec_mass_kernel", "spec_sample_kernel")
+VERIFY_KERNELS = ("verify_fused_kernel", "verify_pipe_kernel", "verify_stats_kernel", "verify_main_kernel",
                   "verify_combine_kernel")
 
 
@@ -83,7 +84,7 @@ def is_paged(short: str) -> bool:
     k = short.split("<")[0]
     if k == "verify_fused_kernel":   # <row tiles, stream, paged, whole step>
         return len(args) >= 3 and args[2] == "true"
-    if k in ("verify_stats_kernel", "verify_main_kernel"):
+    if k in ("verify_stats_kernel", "verify_main_kernel", "verify_pipe_kernel"):
         return len(args) == 2 and args[1] == "true"
     return k == "draft_kernel" and args[0] == "3"
 
@@ -609,7 +610,8 @@ def workload_entry(B, n: int, steps: int, warmup: int, torch, np, cpu: bool):
     entry = {"name": w.name, "batch": w.batch, "n_q_heads": w.n_q_heads,
              "n_kv_heads": w.n_kv_heads, "ctx_len": list(map(int, w.ctx_len)),
              "q_len": list(map(int, w.q_len)), "budget": w.budget,
-             "verify_schedule": "one-sweep" if schedule == B.VERIFY_ONE_SWEEP else "two-sweep",
+             "verify_schedule": {B.VERIFY_ONE_SWEEP: "one-sweep", B.VERIFY_TWO_SWEEP: "two-sweep",
+                                 B.VERIFY_ONE_SWEEP_PERSISTENT: "one-sweep persistent"}[schedule],
              "verify_items": vitems, "select_schedule": "one kernel" if sel_one else "three kernels",
              "select_partitions_per_unit": sel_parts,
              "step_call": "one kernel" if sts[0].one_kernel else "verify, then select_draft",
@@ -717,9 +719,11 @@ def main() -> int:
 
     vshape = B.Shape(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.max_ctx, w.max_q)
     schedule, vchunk, vitems = B.verify_plan(vshape, params, w.ctx_len, w.q_len)
-    sched_name = "one-sweep" if schedule == B.VERIFY_ONE_SWEEP else "two-sweep"
-    verify_kernels = ("verify_fused_kernel" if schedule == B.VERIFY_ONE_SWEEP
-                      else "verify_stats_kernel + verify_main_kernel + verify_combine_kernel")
+    sched_name = {B.VERIFY_ONE_SWEEP: "one-sweep", B.VERIFY_TWO_SWEEP: "two-sweep",
+                  B.VERIFY_ONE_SWEEP_PERSISTENT: "one-sweep persistent"}[schedule]
+    verify_kernels = {B.VERIFY_ONE_SWEEP: "verify_fused_kernel",
+                      B.VERIFY_ONE_SWEEP_PERSISTENT: "verify_pipe_kernel",
+                      B.VERIFY_TWO_SWEEP: "verify_stats_kernel + verify_main_kernel + verify_combine_kernel"}[schedule]
 
     stream = torch.cuda.current_stream()
     steps = [B.PreparedStep(q, k, v, qd, w.ctx_len, w.q_len, params, out, scores, idx, n_idx,

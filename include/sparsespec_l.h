@@ -136,15 +136,29 @@ typedef struct {
 } ssl_params;
 
 /* How ssl_verify_attn schedules its work (results agree to rounding):
- *  AUTO       the one-sweep schedule where it fits and a KV head has at most
- *             32 verify rows (its measured sweet spot), else the two-sweep one;
+ *  AUTO       a one-sweep schedule where one fits and a KV head has at most
+ *             32 verify rows, or 48 when the persistent form runs (their
+ *             measured sweet spots), else the two-sweep one;
  *  TWO_SWEEP  a K-only pass for the row statistics, then a K+V pass;
  *  ONE_SWEEP  a single K+V pass whose chunks of one (sequence, KV head)
- *             exchange row statistics while resident together;
- *             SSL_ERR_UNSUPPORTED when it does not fit: a (sequence, KV head)
- *             may span at most 128 chunks of at most 2048 / 1024 / 640 / 512
- *             keys for up to 16 / 32 / 48 / 64 verify rows per KV head. */
-enum { SSL_VERIFY_AUTO = 0, SSL_VERIFY_TWO_SWEEP = 1, SSL_VERIFY_ONE_SWEEP = 2 };
+ *             exchange row statistics while resident together: one
+ *             workgroup per chunk when every chunk of the call runs in one
+ *             round of workgroups (a (sequence, KV head) may then span at most
+ *             128 chunks of at most 2048 / 1024 / 640 / 512 keys for up to
+ *             16 / 32 / 48 / 64 verify rows per KV head), else, for up to 48
+ *             rows, a persistent grid of what the device holds at once (see
+ *             ssl_set_cu_budget), each workgroup taking every grid-th chunk
+ *             and keeping two chunks' probabilities in 16-bit form (relative
+ *             error 2^-11; probabilities below 2^-54 of the row's running
+ *             maximum count as 0); SSL_ERR_UNSUPPORTED when neither fits.
+ * ssl_verify_plan reports the persistent form as
+ * SSL_VERIFY_ONE_SWEEP_PERSISTENT (an output only, not a request). */
+enum {
+    SSL_VERIFY_AUTO = 0,
+    SSL_VERIFY_TWO_SWEEP = 1,
+    SSL_VERIFY_ONE_SWEEP = 2,
+    SSL_VERIFY_ONE_SWEEP_PERSISTENT = 3
+};
 
 /* Human-readable text of a status code (static storage). */
 const char *ssl_status_string(int status);
@@ -248,9 +262,10 @@ int ssl_verify_attn_static(const ssl_shape *shape, const ssl_params *params,
                            void *out, float *scores, hipStream_t stream);
 
 /* The schedule ssl_verify_attn would use for these arguments: *schedule_out
- * = SSL_VERIFY_ONE_SWEEP or SSL_VERIFY_TWO_SWEEP (one sweep still falls back
- * to two if the device refuses the co-resident launch), *chunk_out = keys per
- * work item, *items_out = work items (each one workgroup).  Host only. */
+ * = SSL_VERIFY_ONE_SWEEP, SSL_VERIFY_ONE_SWEEP_PERSISTENT or
+ * SSL_VERIFY_TWO_SWEEP, *chunk_out = keys per work item, *items_out = work
+ * items (each one workgroup, or, persistent, one chunk of a workgroup's
+ * sequence).  Host only. */
 int ssl_verify_plan(const ssl_shape *shape, const ssl_params *params,
                     const int32_t *ctx_len_host, const int32_t *q_len_host,
                     int32_t *schedule_out, int32_t *chunk_out, int32_t *items_out);

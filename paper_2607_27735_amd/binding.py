@@ -30,6 +30,7 @@ SSL_ERR_HIP = -7
 VERIFY_AUTO = 0
 VERIFY_TWO_SWEEP = 1
 VERIFY_ONE_SWEEP = 2
+VERIFY_ONE_SWEEP_PERSISTENT = 3   # a schedule verify_plan reports, not a request
 
 EXPORTED = [
     "ssl_status_string", "ssl_build_id", "ssl_exchange_status", "ssl_last_hip_error",

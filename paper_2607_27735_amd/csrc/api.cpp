@@ -170,6 +170,8 @@ struct VerifyPlan {
     int block_pos;   // verify positions per launch (row blocks); >= every q_len when one block
     bool fused_ok;
     int fused_chunk, fused_slots;
+    bool pipe;       // one sweep by the persistent kernel: fused_slots chunks over pipe_grid workgroups
+    int pipe_grid;
     size_t ml_off, o_off, bytes;
     SeqTable seq;
     SeqTable fseq;   // the one-sweep slots as items
@@ -261,6 +263,54 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
             plan->fused_slots = (int)slots;
         }
     }
+    // Persistent one sweep, where the chunks above would take more than one
+    // round of workgroups (or do not fit at all) and a KV head has at most 48
+    // rows: a grid of what the device holds at once (the whole grid must be
+    // resident), each workgroup taking every grid-th chunk of a 16-bit stash
+    // size, a unit's chunks within two consecutive rounds (at most one grid
+    // of them) and at most kPipeMaxChunksPerUnit of them (every chunk's finish
+    // loads each chunk's statistics and its rows' partials in passes of 32
+    // chunks, one round trip each: at 103 and 256 chunks per unit the call
+    // measured slower than two sweeps).  The chunk is the one that minimises
+    // rounds * (chunk + 96): a round costs about 96 keys' streaming besides
+    // its own keys.
+    constexpr int64_t kPipeMaxChunksPerUnit = 64;
+    plan->pipe = false;
+    plan->pipe_grid = 0;
+    const int64_t resident1 = n_cu * std::max(fused_blocks_per_cu(plan->row_tiles), 1);
+    const bool one_round = plan->fused_ok && plan->fused_slots <= resident1;
+    // (pipe_max_chunk is 0 where the persistent kernel is not built: > 48 rows)
+    if (!one_round && plan->block_pos >= s->max_q) {
+        const int64_t grid_cap = n_cu * std::max(pipe_blocks_per_cu(plan->row_tiles), 1);
+        int64_t best_cost = -1, best_chunk = 0, best_tasks = 0;
+        for (int64_t pc = pipe_max_chunk(plan->row_tiles); pc >= 128; pc -= 128) {
+            int64_t tasks = 0;
+            for (int b = 0; b < s->batch; ++b) tasks += (int64_t)s->n_kv_heads * ((ctx[b] + pc - 1) / pc);
+            const int64_t grid = std::min(tasks, grid_cap);
+            const int64_t per_unit = (max_ctx + pc - 1) / pc;
+            if (per_unit > grid || per_unit > kPipeMaxChunksPerUnit || tasks > (1 << 30)) continue;
+            const int64_t cost = (tasks + grid - 1) / grid * (pc + 96);
+            if (best_cost < 0 || cost < best_cost) {
+                best_cost = cost;
+                best_chunk = pc;
+                best_tasks = tasks;
+            }
+        }
+        if (best_cost >= 0) {
+            plan->fseq = plan->seq;
+            int64_t slots = 0;
+            for (int b = 0; b < s->batch; ++b) {
+                plan->fseq.item_start[b] = (int32_t)slots;
+                slots += (int64_t)s->n_kv_heads * ((ctx[b] + best_chunk - 1) / best_chunk);
+            }
+            plan->fseq.item_start[s->batch] = (int32_t)slots;
+            plan->fused_ok = true;
+            plan->fused_chunk = (int)best_chunk;
+            plan->fused_slots = (int)best_tasks;
+            plan->pipe = true;
+            plan->pipe_grid = (int)std::min(best_tasks, grid_cap);
+        }
+    }
     if (p->verify_mode == SSL_VERIFY_ONE_SWEEP && !plan->fused_ok) return SSL_ERR_UNSUPPORTED;
     const size_t slots_max = (size_t)std::max(plan->n_items, plan->fused_slots);
     // per item and row: (max, sum), each word tagged in the one-sweep schedule
@@ -275,7 +325,7 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
 // row in LDS) is bound by its per-tile latency and two sweeps are faster.
 bool use_one_sweep(const VerifyPlan& plan, const ssl_params* p) {
     if (!plan.fused_ok || p->verify_mode == SSL_VERIFY_TWO_SWEEP) return false;
-    return p->verify_mode == SSL_VERIFY_ONE_SWEEP || plan.row_tiles <= 2;
+    return p->verify_mode == SSL_VERIFY_ONE_SWEEP || plan.row_tiles <= 2 || plan.pipe;
 }
 
 struct DraftPlan {
@@ -480,7 +530,7 @@ int ssl_verify_plan(const ssl_shape* shape, const ssl_params* params, const int3
     const int rc = plan_verify(shape, params, ctx_len_host, q_len_host, &plan);
     if (rc) return rc;
     const bool one = use_one_sweep(plan, params);
-    *schedule_out = one ? SSL_VERIFY_ONE_SWEEP : SSL_VERIFY_TWO_SWEEP;
+    *schedule_out = !one ? SSL_VERIFY_TWO_SWEEP : plan.pipe ? SSL_VERIFY_ONE_SWEEP_PERSISTENT : SSL_VERIFY_ONE_SWEEP;
     *chunk_out = one ? plan.fused_chunk : plan.chunk;
     *items_out = one ? plan.fused_slots : plan.n_items;
     return SSL_OK;
@@ -576,7 +626,9 @@ int verify_call(const ssl_shape* shape, const ssl_params* params, const int32_t*
         // lifting the mark a captured call that gave up may have left there.
         fa.heal = scratch && !fa.epoch ? static_cast<uint64_t*>(workspace) : nullptr;
         fa.heal_value = mix64(fa.call_tag);
-        return hip_rc(launch_verify_fused(fa, plan.fused_slots, plan.row_tiles, stream));
+        fa.n_tasks = plan.pipe ? plan.fused_slots : 0;
+        return hip_rc(launch_verify_fused(fa, plan.pipe ? plan.pipe_grid : plan.fused_slots, plan.row_tiles,
+                                          stream));
     }
     if (plan.block_pos >= shape->max_q)
         return hip_rc(launch_verify(a, plan.n_items, plan.n_rows, plan.row_tiles, stream));
@@ -965,7 +1017,7 @@ int plan_decode(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
     constexpr int kStepMinChunk = 512;
     const int g = s->n_q_heads / s->n_kv_heads;
     const int64_t resident = (int64_t)device_cus() * std::max(fused_blocks_per_cu(plan->v.row_tiles), 1);
-    plan->one_kernel = use_one_sweep(plan->v, p) && !p->per_head && g <= 16 &&
+    plan->one_kernel = use_one_sweep(plan->v, p) && !plan->v.pipe && !p->per_head && g <= 16 &&
                        plan->v.fused_slots <= resident && plan->v.fused_chunk >= kStepMinChunk;
     if (!plan->one_kernel) {
         plan->parts = 0;

@@ -181,6 +181,10 @@ struct FusedArgs {
     // units to set to heal_value + unit at the end (null otherwise).
     uint64_t* heal;
     uint64_t heal_value;
+    // Persistent schedule: n_tasks chunks (work items) over a grid of at most
+    // n_tasks workgroups, all resident at once, each taking every grid-th
+    // chunk; 0: one workgroup per chunk.
+    int32_t n_tasks;
     // Whole decode step (step = 1): after its outputs and scores, each
     // workgroup runs the one-kernel select as partition s (the chunk) of its
     // unit over the scores it has just computed, and then the first draft
@@ -202,7 +206,8 @@ struct StaticScratch {
 hipError_t launch_verify(const VerifyArgs& a, int n_items, int n_rows_total, int row_tiles,
                          hipStream_t stream);
 // Launches the single-sweep kernel over n_slots workgroups (it adds the
-// chunks of each row itself; with a.step it also selects and drafts).
+// chunks of each row itself; with a.step it also selects and drafts), or,
+// with a.n_tasks > 0, the persistent one over a grid of n_slots workgroups.
 // Returns the launch error.
 hipError_t launch_verify_fused(const FusedArgs& a, int n_slots, int row_tiles, hipStream_t stream);
 // The combine kernel alone: out[row] = sum of the row's normalised partials.
@@ -214,6 +219,11 @@ int fused_max_chunk(int row_tiles);
 // current device holds at once; 0 if the device cannot be queried.
 int fused_blocks_per_cu(int row_tiles);
 int select_blocks_per_cu(int part);
+// The persistent single-sweep kernel (FusedArgs.n_tasks > 0): the largest key
+// chunk its two 16-bit stash buffers hold (0 for row_tiles it is not built
+// for), and its workgroups per CU.
+int pipe_max_chunk(int row_tiles);
+int pipe_blocks_per_cu(int row_tiles);
 // Partition length for the longest context max_t: the smallest multiple of
 // 1024 (in powers of two, at most kSelectMaxRounds * 1024) that keeps a unit at
 // <= kSelectTargetParts partitions.

@@ -71,14 +71,50 @@ constexpr int max_fused_chunk() {
 
 __device__ __forceinline__ float safe_max(float m) { return m == -INFINITY ? 0.f : m; }
 
+// The LDS stash holds each key's probability per verify row, relative to the
+// row's reference maximum (at most 2^kLazy).  Two element formats:
+//  - StashF32: the fp32 value (the kernel that runs one chunk per workgroup);
+//  - StashU16: a 16-bit code, half the LDS, so that the persistent kernel can
+//    keep two chunks' stashes: 6 exponent bits (2^-54 .. 2^9) above the top 10
+//    mantissa bits, rounded to nearest (relative error at most 2^-11, so a
+//    score, a sum of such terms times exact factors, keeps that bound); values
+//    below 2^-54 of the reference are coded 0.
+struct StashF32 {
+    using T = float;
+    static constexpr int kPad = 4;   // elements of padding per row
+    static __device__ __forceinline__ void put(T* p, float v) { *p = v; }
+    // keys k4 .. k4 + 3 of a row (k4 a multiple of 4)
+    static __device__ __forceinline__ f32x4 get4(const T* row, int k4) {
+        return *reinterpret_cast<const f32x4*>(row + k4);
+    }
+};
+
+struct StashU16 {
+    using T = uint16_t;
+    static constexpr int kPad = 8;
+    static constexpr uint32_t kBias = 72u << 10;   // exponent field 72 at code 0
+    static __device__ __forceinline__ uint32_t enc(float v) {
+        const uint32_t r = (__float_as_uint(v) + 0x1000u) >> 13;   // 10 mantissa bits, rounded
+        return r >= kBias + 1024u ? min(r - kBias, 0xFFFFu) : 0u;
+    }
+    static __device__ __forceinline__ float dec(uint32_t c) {
+        return c ? __uint_as_float((c + kBias) << 13) : 0.f;
+    }
+    static __device__ __forceinline__ void put(T* p, float v) { *p = (uint16_t)enc(v); }
+    static __device__ __forceinline__ f32x4 get4(const T* row, int k4) {
+        const uint2 w = *reinterpret_cast<const uint2*>(row + k4);
+        return f32x4{dec(w.x & 0xFFFFu), dec(w.x >> 16), dec(w.y & 0xFFFFu), dec(w.y >> 16)};
+    }
+};
+
 // One 32-key tile: online softmax and P.V; the tile's probabilities relative
 // to the rows' reference maxima go to the LDS stash, those maxima to mtile.
-template <int NRT>
+template <int NRT, typename Codec>
 __device__ __forceinline__ void fused_tile(const VerifyArgs& a, const Rows<NRT>& r,
-                                           const KVTile& tl, int key0, int kl0, float* stash,
-                                           int stride, float* mtile, int mts, int m16, int G,
-                                           float (&M)[NRT], float (&L)[NRT],
-                                           f32x4 (&oacc)[8][NRT]) {
+                                           const KVTile& tl, int key0, int kl0,
+                                           typename Codec::T* stash, int stride, float* mtile,
+                                           int mts, int m16, int G, float (&M)[NRT],
+                                           float (&L)[NRT], f32x4 (&oacc)[8][NRT]) {
     f32x4 acc[2][NRT];
     qk_tile<NRT>(tl.k, r, acc);
     float p[2][NRT][4];
@@ -86,7 +122,7 @@ __device__ __forceinline__ void fused_tile(const VerifyArgs& a, const Rows<NRT>&
     for (int rt = 0; rt < NRT; ++rt) {
         float y[8];
         float mt = -INFINITY;
-        float* srow = stash + (rt * 16 + m16) * stride + kl0;
+        typename Codec::T* srow = stash + (rt * 16 + m16) * stride + kl0;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
             const int t = e >> 2, i = e & 3;
@@ -114,7 +150,7 @@ __device__ __forceinline__ void fused_tile(const VerifyArgs& a, const Rows<NRT>&
         for (int e = 0; e < 8; ++e) {
             p[e >> 2][rt][e & 3] = fast_exp2(y[e] - Mr);
             sum += p[e >> 2][rt][e & 3];
-            srow[16 * (e >> 2) + G + 4 * (e & 3)] = p[e >> 2][rt][e & 3];
+            Codec::put(srow + 16 * (e >> 2) + G + 4 * (e & 3), p[e >> 2][rt][e & 3]);
         }
         if (G == 0) mtile[(rt * 16 + m16) * mts + kl0 / kTile] = Mr;
         L[rt] += sum;
@@ -164,38 +200,31 @@ __device__ __forceinline__ bool step_select(const SelectArgs& sa, const Geom& g,
     return select_partition<NR, true>(sa, g, p, u, keys, L, want);
 }
 
-template <int NRT, bool kStream, bool kPaged, bool kStep>
-__global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
-    const VerifyArgs& a = fa.v;
-    extern __shared__ __attribute__((aligned(16))) float stash[];   // [NRT*16][chunk + pad]
-    __shared__ float2 wml[kWaves][NRT * 16];
-    __shared__ float row_lse[kRowCap];
-    __shared__ float2 lse_part[kWaves][kRowCap];
-    __shared__ int wait_failed;
+// A chunk of one (sequence, KV head): work item `slot` of the launch.
+struct Chunk {
+    int slot, unit, b, c, s, slot0, nchunk, T, nq, R, key_begin, key_end;
+};
 
-    const int slot = blockIdx.x;
+__device__ __forceinline__ Chunk chunk_of(const VerifyArgs& a, int slot) {
     const Item it = decode_item<false>(a, a.seq, slot, a.chunk);
-    const int unit = it.unit, b = it.b, c = it.c;
-    const int slot0 = it.item0, nchunk = it.nchunk;
-    const int T = it.T, nq = it.nq;
-    const int R = nq * a.group;
-    const int chunk = a.chunk;
-    const int key_begin = it.key_begin, key_end = it.key_end;
-    const int stride = chunk + kStashPad;
-    const int mts = chunk / kTile;
-    float* mtile = stash + NRT * 16 * stride;   // [NRT*16][mts] running row maxima per tile
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int m16 = lane & 15, G = lane >> 4;
+    Chunk k;
+    k.slot = slot;
+    k.unit = it.unit;
+    k.b = it.b;
+    k.c = it.c;
+    k.s = it.s;
+    k.slot0 = it.item0;
+    k.nchunk = it.nchunk;
+    k.T = it.T;
+    k.nq = it.nq;
+    k.R = it.nq * a.group;
+    k.key_begin = it.key_begin;
+    k.key_end = it.key_end;
+    return k;
+}
 
-    Rows<NRT> r;
-    load_rows<NRT>(a, b, c, T, nq, it.qoff, it.qfull, m16, G, r);
-    const size_t cache_off = (size_t)unit * a.max_ctx * kHeadDim;
-    const uint16_t* kbase = a.k + cache_off;
-    const uint16_t* vbase = a.v + cache_off;
-
-    // ---- 1. the sweep ------------------------------------------------------
-    float M[NRT], L[NRT];
-    f32x4 oacc[8][NRT];
+template <int NRT>
+__device__ __forceinline__ void clear_state(float (&M)[NRT], float (&L)[NRT], f32x4 (&oacc)[8][NRT]) {
 #pragma unroll
     for (int rt = 0; rt < NRT; ++rt) {
         M[rt] = -INFINITY;
@@ -203,37 +232,65 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
 #pragma unroll
         for (int jd = 0; jd < 8; ++jd) oacc[jd][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    const int ntile = (key_end - key_begin + kTile - 1) / kTile;
-    const int pages = kPaged ? wave_pages(a, b, key_begin, ntile, wave, lane) : 0;
+}
+
+// ---- 1. the sweep: the chunk's K and V once, online softmax, P.V ----------
+// pre() runs once per wave with each wave's first tile already in flight.
+template <int NRT, bool kStream, bool kPaged, typename Codec, typename Pre>
+__device__ __forceinline__ void sweep_chunk(const VerifyArgs& a, const Chunk& k, const Rows<NRT>& r,
+                                            typename Codec::T* stash, int stride, float* mtile,
+                                            int mts, float (&M)[NRT], float (&L)[NRT],
+                                            f32x4 (&oacc)[8][NRT], Pre&& pre) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int m16 = lane & 15, G = lane >> 4;
+    const size_t cache_off = (size_t)k.unit * a.max_ctx * kHeadDim;
+    const uint16_t* kbase = a.k + cache_off;
+    const uint16_t* vbase = a.v + cache_off;
+    const int ntile = (k.key_end - k.key_begin + kTile - 1) / kTile;
+    const int pages = kPaged ? wave_pages(a, k.b, k.key_begin, ntile, wave, lane) : 0;
     tile_pipeline<2, KVTile>(
         wave, ntile, kWaves,
         [&](KVTile& bf, int t) {
             load_kv_tile<kPaged, kStream>(a, kbase, vbase, kPaged ? tile_page(pages, t, wave) : 0,
-                                          c, key_begin + t * kTile, T, m16, G, bf);
+                                          k.c, k.key_begin + t * kTile, k.T, m16, G, bf);
         },
         [&](const KVTile& bf, int t) {
-            fused_tile<NRT>(a, r, bf, key_begin + t * kTile, t * kTile, stash, stride, mtile, mts, m16,
-                            G, M, L, oacc);
-        });
+            fused_tile<NRT, Codec>(a, r, bf, k.key_begin + t * kTile, t * kTile, stash, stride, mtile,
+                                   mts, m16, G, M, L, oacc);
+        },
+        pre);
+}
 
-    // ---- 2. publish the chunk's row statistics and partial output ----------
+// ---- 2. publish the chunk's partial output, then its row statistics ------
+// Every thread calls this.  Returns the exchange tag; *clean is false when an
+// earlier captured call on this workspace gave up (the epoch is marked), and
+// then nothing is published.  Uses L (summed over the wave's lanes here).
+template <int NRT>
+__device__ __forceinline__ uint64_t publish_chunk(const FusedArgs& fa, const Chunk& k,
+                                                  const float (&M)[NRT], float (&L)[NRT],
+                                                  const f32x4 (&oacc)[8][NRT],
+                                                  float2 (*wml)[NRT * 16], float* park,
+                                                  int* wait_failed, bool* clean) {
+    const VerifyArgs& a = fa.v;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int m16 = lane & 15, G = lane >> 4;
     // The unit's exchange epoch (exchange_tag), loaded here so that its round
     // trip overlaps the stores below (the tag is formed only after the wait
-    // for them); chunk 0 advances it at its end, when every chunk has
-    // published, and so has read it.
-    const uint64_t ep = fa.epoch ? ld_dev64(fa.epoch + unit) : 0ull;
+    // for them); the unit's chunk 0 advances it once it has every chunk's
+    // statistics, i.e. once every chunk has read it.
+    const uint64_t ep = fa.epoch ? ld_dev64(fa.epoch + k.unit) : 0ull;
 #pragma unroll
     for (int rt = 0; rt < NRT; ++rt) {
         L[rt] += shfl_xor_f(L[rt], 16);
         L[rt] += shfl_xor_f(L[rt], 32);
         if (G == 0) wml[wave][rt * 16 + m16] = make_float2(M[rt], L[rt]);
     }
-    if (tid == 0) wait_failed = 0;
+    if (tid == 0) *wait_failed = 0;
     __syncthreads();
     // the workgroup's row statistics, merged over its waves (published below,
     // once the partial output has landed)
     float own_m = -INFINITY, own_l = 0.f;
-    if (tid < R) {
+    if (tid < k.R) {
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) own_m = fmaxf(own_m, wml[w][tid].x);
 #pragma unroll
@@ -243,8 +300,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     // waves 2 and 3 park theirs, waves 0 and 1 add them, park the sums, and
     // all threads add the two slices and store the rows device-coherently
     {
-        float* park = stash + NRT * 16 * stride + (chunk / kTile) * (NRT * 16);   // [2][16][kParkStride]
-        float* po = a.part_o + (size_t)slot * kRowCap * kHeadDim;
+        float* po = a.part_o + (size_t)k.slot * kRowCap * kHeadDim;
 #pragma unroll
         for (int rt = 0; rt < NRT; ++rt) {
             const int row = rt * 16 + m16;
@@ -277,7 +333,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
                 }
             }
             __syncthreads();
-            const int rows_here = min(16, R - rt * 16);
+            const int rows_here = min(16, k.R - rt * 16);
             f32x4 o[2];
 #pragma unroll
             for (int h = 0; h < 2; ++h) {   // both halves' reads in flight
@@ -294,11 +350,9 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
                     st_dev64(d64 + 1, __builtin_bit_cast(uint64_t, make_float2(o[h][2], o[h][3])));
                 }
             }
-            if (rt + 1 < NRT) __syncthreads();   // (the last one: the tag's barrier below)
+            if (rt + 1 < NRT) __syncthreads();   // (the last one: the barrier below)
         }
     }
-
-    // ---- publish the statistics; wait for every chunk of the head ----------
     // Each (max, sum) word carries the low 32 bits of the exchange tag above
     // the value, and is stored only once this workgroup's partial output has
     // landed: a reader that finds every chunk's words tagged has the head's
@@ -307,16 +361,34 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     __syncthreads();
     const uint64_t epv = scalar_here(ep);
     const uint64_t want = exchange_tag(fa.call_tag, epv);
-    const uint64_t tag_hi = (want & 0xFFFFFFFFull) << 32;
-    uint64_t* ml64 = reinterpret_cast<uint64_t*>(a.part_ml);   // [slot][kRowCap][2]
     // a dirty epoch: an earlier captured call on this workspace gave up
-    const bool clean = !epoch_is_dirty(epv);
-    if (clean && tid < R) {
+    *clean = !epoch_is_dirty(epv);
+    if (*clean && tid < k.R) {
+        uint64_t* ml64 = reinterpret_cast<uint64_t*>(a.part_ml);   // [slot][kRowCap][2]
         const uint64_t pub = ((want ^ fa.xc.tag_flip) & 0xFFFFFFFFull) << 32;
-        uint64_t* e = ml64 + ((size_t)slot * kRowCap + tid) * 2;
+        uint64_t* e = ml64 + ((size_t)k.slot * kRowCap + tid) * 2;
         st_dev64(e, pub | __float_as_uint(own_m));
         st_dev64(e + 1, pub | __float_as_uint(own_l));
     }
+    return want;
+}
+
+// ---- 3, 4. the chunk's scores and its rows' outputs ----------------------
+// Every thread calls this.  Waits for every chunk's statistics of the unit
+// (false: the wait gave up, reported on the status word; nothing written),
+// then writes the scores of the chunk's keys from its stash and the outputs
+// of rows s, s + nchunk, ... .  With kStep the score bits also go to skeys.
+template <int NRT, typename Codec, bool kStep>
+__device__ __forceinline__ bool finish_chunk(const FusedArgs& fa, const Chunk& k, uint64_t want,
+                                             bool clean, typename Codec::T* stash, int stride,
+                                             const float* mtile, int mts,
+                                             float2 (*lse_part)[kRowCap], float* row_lse,
+                                             int* wait_failed, uint32_t* skeys) {
+    const VerifyArgs& a = fa.v;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int R = k.R, nchunk = k.nchunk, slot0 = k.slot0;
+    const uint64_t tag_hi = (want & 0xFFFFFFFFull) << 32;
+    const uint64_t* ml64 = reinterpret_cast<const uint64_t*>(a.part_ml);   // [slot][kRowCap][2]
 
     // ---- 3a. exact row statistics over every chunk of the head -------------
     // Wave w polls rows 0..63 of chunks w, w + 4, ... (eight chunks per
@@ -358,13 +430,13 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
                         ml_merge(Mx, Lx, __uint_as_float((uint32_t)w0[uu]), __uint_as_float((uint32_t)w1[uu]));
             }
         }
-        if (!in_all && lane == 0) wait_failed = 1;
+        if (!in_all && lane == 0) *wait_failed = 1;
         lse_part[ph][rr] = make_float2(Mx, Lx);
     }
     __syncthreads();
-    if (wait_failed) {
-        if (tid == 0) exchange_gave_up(fa.xc, kStatusVerify, fa.epoch ? fa.epoch + unit : nullptr);
-        return;
+    if (*wait_failed) {
+        if (tid == 0) exchange_gave_up(fa.xc, kStatusVerify, fa.epoch ? fa.epoch + k.unit : nullptr);
+        return false;
     }
 
     // The first chunks of this workgroup's first row in step 4 (all of them
@@ -390,7 +462,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     };
     f32x4 pv[4];
     float pm[4];
-    if (it.s < R) load_part(it.s, sg, pv, pm);
+    if (k.s < R) load_part(k.s, sg, pv, pm);
 
     if (tid < kRowCap) {
         float Mx = -INFINITY, Lx = 0.f;
@@ -399,18 +471,16 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
         row_lse[tid] = Lx > 0.f ? Mx + fast_log2(Lx) : INFINITY;
     }
     __syncthreads();
-    const int nk = key_end - key_begin;
+    const int nk = k.key_end - k.key_begin;
 
     // ---- 3b. scores of this chunk's keys from the stashed probabilities ----
     {
-        const int wn = min(a.window, nq);
-        const int r0 = (nq - wn) * a.group;   // first window row
-        float* srow = a.scores + (size_t)unit * a.max_ctx;
-        // four consecutive keys per thread (one 16-byte LDS read per row, four
-        // rows in flight); the stash row stride and the chunk are multiples of
-        // 4 floats, and 4 consecutive keys share one tile
-        const f32x4* stash4 = reinterpret_cast<const f32x4*>(stash);
-        const int stride4 = stride / 4;
+        const int wn = min(a.window, k.nq);
+        const int r0 = (k.nq - wn) * a.group;   // first window row
+        float* srow = a.scores + (size_t)k.unit * a.max_ctx;
+        // four consecutive keys per thread (one LDS read per row, several rows
+        // in flight); the stash row stride and the chunk are multiples of 4
+        // elements, and 4 consecutive keys share one tile.
         // A stashed probability times its tile's factor 2^(m_tile - lse) is
         // exact; the tile maxima are [row][tile], so the lanes of a wave
         // (eight tiles, one row) read distinct banks.
@@ -421,16 +491,13 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
             for (int hh = 0; hh < a.group; ++hh) {
                 f32x4 sc = {0.f, 0.f, 0.f, 0.f};
                 for (int row = r0 + hh; row < R; row += a.group)
-                    sc += stash4[row * stride4 + k4 / 4] * fast_exp2(mt[row * mts] - row_lse[row]);
-                float* hrow = a.scores + ((size_t)b * a.n_q_heads + c * a.group + hh) * a.max_ctx;
+                    sc += Codec::get4(stash + row * stride, k4) * fast_exp2(mt[row * mts] - row_lse[row]);
+                float* hrow = a.scores + ((size_t)k.b * a.n_q_heads + k.c * a.group + hh) * a.max_ctx;
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    if (k4 + i < nk) hrow[key_begin + k4 + i] = sc[i];
+                    if (k4 + i < nk) hrow[k.key_begin + k4 + i] = sc[i];
             }
         }
-        // (decode step: the chunk's score bits also go to skeys, in the
-        // parking slices, free since step 2)
-        uint32_t* skeys = reinterpret_cast<uint32_t*>(stash + NRT * 16 * stride + mts * (NRT * 16));
         for (int k4 = 4 * tid; !a.per_head && k4 < nk; k4 += 4 * kThreads) {
             const float* mt = mtile + k4 / kTile;   // mt[row * mts]
             f32x4 sc = {0.f, 0.f, 0.f, 0.f};
@@ -440,7 +507,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
                 float cr[8];
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    pr[j] = stash4[(row + j) * stride4 + k4 / 4];
+                    pr[j] = Codec::get4(stash + (row + j) * stride, k4);
                     cr[j] = mt[(row + j) * mts] - row_lse[row + j];
                 }
 #pragma unroll
@@ -451,35 +518,35 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
                 float cr[4];
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    pr[j] = stash4[(row + j) * stride4 + k4 / 4];
+                    pr[j] = Codec::get4(stash + (row + j) * stride, k4);
                     cr[j] = fast_exp2(mt[(row + j) * mts] - row_lse[row + j]);
                 }
 #pragma unroll
                 for (int j = 0; j < 4; ++j) sc += pr[j] * cr[j];
             }
             for (; row < R; ++row)
-                sc += stash4[row * stride4 + k4 / 4] * fast_exp2(mt[row * mts] - row_lse[row]);
+                sc += Codec::get4(stash + row * stride, k4) * fast_exp2(mt[row * mts] - row_lse[row]);
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                if (k4 + i < nk) srow[key_begin + k4 + i] = sc[i];
+                if (k4 + i < nk) srow[k.key_begin + k4 + i] = sc[i];
             if constexpr (kStep) *reinterpret_cast<f32x4*>(skeys + k4) = sc;   // k4 + 3 < chunk
         }
     }
 
-    // ---- 4. rows it.s, it.s + nchunk, ... summed over the unit's chunks ------
+    // ---- 4. rows s, s + nchunk, ... summed over the unit's chunks ----------
     // A chunk's partial is relative to its maxima m: it enters with 2^(m - lse).
     // Chunks are added in index order within eight interleaved groups, then
     // the groups in order.
     __syncthreads();   // the stash is free once every thread's scores are out
     {
         f32x4* red = reinterpret_cast<f32x4*>(stash);   // [8][32]
-        for (int row = it.s; row < R; row += nchunk) {
+        for (int row = k.s; row < R; row += nchunk) {
             const float lse = row_lse[row];
             f32x4 acc = {0.f, 0.f, 0.f, 0.f};
             for (int s0 = sg; s0 < nchunk; s0 += 4 * 8) {
                 f32x4 v[4];
                 float m[4];
-                if (row == it.s && s0 == sg) {
+                if (row == k.s && s0 == sg) {
 #pragma unroll
                     for (int uu = 0; uu < 4; ++uu) {
                         v[uu] = pv[uu];
@@ -498,8 +565,8 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
 #pragma unroll
                 for (int gq = 1; gq < 8; ++gq) o += red[gq * 32 + d4];
                 const int j = row / a.group;
-                const int h = c * a.group + (row - j * a.group);
-                const size_t base = (((size_t)b * a.max_q + j) * a.n_q_heads + h) * kHeadDim + 4 * d4;
+                const int h = k.c * a.group + (row - j * a.group);
+                const size_t base = (((size_t)k.b * a.max_q + j) * a.n_q_heads + h) * kHeadDim + 4 * d4;
                 if (a.out_fp32) {
                     *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out) + base) = o;
                 } else {
@@ -510,28 +577,148 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
             __syncthreads();
         }
     }
+    return true;
+}
+
+// The unit's chunk 0, once it has every chunk's statistics: every chunk has
+// published, so has read the epoch; advanced after the workgroup's final wait
+// for loads.
+__device__ __forceinline__ void chunk0_done(const FusedArgs& fa, const Chunk& k) {
+    if (threadIdx.x != 0 || k.slot != k.slot0) return;
+    if (fa.epoch) epoch_advance(fa.epoch + k.unit);
+    if (fa.heal) st_dev64(fa.heal + k.unit, fa.heal_value + k.unit);
+}
+
+// One workgroup per chunk (fp32 stash): sweep, publish, then the scores and
+// outputs; with kStep it goes on as partition s of its unit's select and draft.
+template <int NRT, bool kStream, bool kPaged, bool kStep>
+__global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
+    const VerifyArgs& a = fa.v;
+    extern __shared__ __attribute__((aligned(16))) float stash[];   // [NRT*16][chunk + pad]
+    __shared__ float2 wml[kWaves][NRT * 16];
+    __shared__ float row_lse[kRowCap];
+    __shared__ float2 lse_part[kWaves][kRowCap];
+    __shared__ int wait_failed;
+
+    const Chunk k = chunk_of(a, blockIdx.x);
+    const int chunk = a.chunk;
+    const int stride = chunk + StashF32::kPad;
+    const int mts = chunk / kTile;
+    float* mtile = stash + NRT * 16 * stride;   // [NRT*16][mts] reference row maxima per tile
+    float* park = mtile + mts * (NRT * 16);     // [2][16][kParkStride]
+    const int lane = threadIdx.x & 63;
+    const int m16 = lane & 15, G = lane >> 4;
+
+    Rows<NRT> r;
+    load_rows<NRT>(a, k.b, k.c, k.T, k.nq, 0, k.nq, m16, G, r);
+    float M[NRT], L[NRT];
+    f32x4 oacc[8][NRT];
+    clear_state<NRT>(M, L, oacc);
+    sweep_chunk<NRT, kStream, kPaged, StashF32>(a, k, r, stash, stride, mtile, mts, M, L, oacc, [] {});
+    bool clean;
+    const uint64_t want = publish_chunk<NRT>(fa, k, M, L, oacc, wml, park, &wait_failed, &clean);
+    // (decode step: the chunk's score bits also go to skeys, in the parking
+    // slices, free once the partial output is out)
+    uint32_t* skeys = reinterpret_cast<uint32_t*>(park);
+    if (!finish_chunk<NRT, StashF32, kStep>(fa, k, want, clean, stash, stride, mtile, mts, lse_part, row_lse,
+                                            &wait_failed, skeys))
+        return;
     if constexpr (kStep) {
         // ---- 5. select (Eq. 4) and the first draft step (Eq. 5) ------------
         const SelectArgs& sa = fa.sel;
-        const Geom g = geom_of(sa, b);
-        SelLds& L = *reinterpret_cast<SelLds*>(stash);
-        const uint32_t* skeys = reinterpret_cast<const uint32_t*>(stash + NRT * 16 * stride + mts * (NRT * 16));
+        const Geom g = geom_of(sa, k.b);
+        SelLds& SL = *reinterpret_cast<SelLds*>(stash);
+        const int nk = k.key_end - k.key_begin;
         bool done;
         if (g.simple) {
             __syncthreads();   // the stash becomes the select's
-            done = select_simple<true>(sa, g, it.s, unit, L, want);
+            done = select_simple<true>(sa, g, k.s, k.unit, SL, want);
         } else if (NRT > 1 || chunk <= kRound) {
-            done = step_select<1>(sa, g, it.s, unit, skeys, nk, key_begin, L, want);
+            done = step_select<1>(sa, g, k.s, k.unit, skeys, nk, k.key_begin, SL, want);
         } else {
-            done = step_select<NRT == 1 ? 2 : 1>(sa, g, it.s, unit, skeys, nk, key_begin, L, want);
+            done = step_select<NRT == 1 ? 2 : 1>(sa, g, k.s, k.unit, skeys, nk, k.key_begin, SL, want);
         }
         // chunk 0 goes on only when every exchange of the step completed
         if (!done) return;
     }
-    // every chunk has published, so has read the epoch; advanced last, after
-    // the workgroup's final wait for loads
-    if (fa.epoch && tid == 0 && slot == slot0) epoch_advance(fa.epoch + unit);
-    if (fa.heal && tid == 0 && slot == slot0) st_dev64(fa.heal + unit, fa.heal_value + unit);
+    chunk0_done(fa, k);
+}
+
+// Persistent one-sweep kernel (16-bit stash, two chunk buffers): workgroup w
+// takes chunks w, w + G, w + 2G, ... (G = the grid, all resident at once).
+// Chunk j's partial output and statistics are published, and chunk j - 1's
+// scores and outputs written, at the start of chunk j + 1's sweep, while each
+// wave's first tile of it is in flight; so the exchange of one chunk runs
+// under the streaming of the next.  The wait in chunk j - 1's finish needs
+// only chunks of earlier rounds or of round j, all published before any
+// workgroup's round j + 1 finish: the host keeps a unit's chunks within two
+// consecutive rounds (at most G per unit), so no wait depends on a workgroup
+// that is itself waiting.
+template <int NRT, bool kPaged>
+__global__ __launch_bounds__(kThreads) void verify_pipe_kernel(FusedArgs fa) {
+    using Codec = StashU16;
+    const VerifyArgs& a = fa.v;
+    extern __shared__ __attribute__((aligned(16))) float lds[];
+    __shared__ float2 wml[kWaves][NRT * 16];
+    __shared__ float row_lse[kRowCap];
+    __shared__ float2 lse_part[kWaves][kRowCap];
+    __shared__ int wait_failed;
+
+    const int chunk = a.chunk;
+    const int stride = chunk + Codec::kPad;
+    const int mts = chunk / kTile;
+    const int code_bytes = NRT * 16 * stride * 2;                 // a multiple of 16
+    const int buf_bytes = code_bytes + NRT * 16 * mts * 4;
+    char* base = reinterpret_cast<char*>(lds);
+    float* park = reinterpret_cast<float*>(base + 2 * buf_bytes);   // [2][16][kParkStride]
+    auto codes = [&](int j) { return reinterpret_cast<uint16_t*>(base + (j & 1) * buf_bytes); };
+    auto tiles = [&](int j) { return reinterpret_cast<float*>(base + (j & 1) * buf_bytes + code_bytes); };
+    const int lane = threadIdx.x & 63;
+    const int m16 = lane & 15, G = lane >> 4;
+    const int grid = gridDim.x, w = blockIdx.x;
+    const int n = (fa.n_tasks - w + grid - 1) / grid;   // >= 1: the grid is at most the task count
+
+    float M[NRT], L[NRT];
+    f32x4 oacc[8][NRT];
+    clear_state<NRT>(M, L, oacc);
+    Chunk k1 = chunk_of(a, w), k2 = k1;   // chunks j - 1 and j - 2
+    uint64_t want1 = 0, want2 = 0;
+    bool clean1 = false, clean2 = false, failed = false;
+    for (int j = 0; j < n; ++j) {
+        const Chunk k = chunk_of(a, w + j * grid);
+        Rows<NRT> r;
+        load_rows<NRT>(a, k.b, k.c, k.T, k.nq, 0, k.nq, m16, G, r);
+        sweep_chunk<NRT, false, kPaged, Codec>(
+            a, k, r, codes(j), stride, tiles(j), mts, M, L, oacc, [&] {
+                if (j >= 1) {
+                    want1 = publish_chunk<NRT>(fa, k1, M, L, oacc, wml, park, &wait_failed, &clean1);
+                    clear_state<NRT>(M, L, oacc);
+                }
+                if (j >= 2) {
+                    if (finish_chunk<NRT, Codec, false>(fa, k2, want2, clean2, codes(j), stride, tiles(j), mts,
+                                                        lse_part, row_lse, &wait_failed, nullptr))
+                        chunk0_done(fa, k2);
+                    else
+                        failed = true;
+                }
+            });
+        if (failed) return;
+        k2 = k1;
+        want2 = want1;
+        clean2 = clean1;
+        k1 = k;
+    }
+    want1 = publish_chunk<NRT>(fa, k1, M, L, oacc, wml, park, &wait_failed, &clean1);
+    if (n >= 2) {
+        if (!finish_chunk<NRT, Codec, false>(fa, k2, want2, clean2, codes(n), stride, tiles(n), mts, lse_part,
+                                             row_lse, &wait_failed, nullptr))
+            return;
+        chunk0_done(fa, k2);
+    }
+    if (!finish_chunk<NRT, Codec, false>(fa, k1, want1, clean1, codes(n - 1), stride, tiles(n - 1), mts, lse_part,
+                                         row_lse, &wait_failed, nullptr))
+        return;
+    chunk0_done(fa, k1);
 }
 
 template <int NRT>
@@ -540,14 +727,37 @@ constexpr size_t fused_lds_bytes(int chunk) {
     return ((size_t)NRT * 16 * (chunk + kStashPad + chunk / kTile) + kParkFloats) * sizeof(float);
 }
 
-// Once per device and row-tile count: the kernels' dynamic LDS limit is raised
-// to the largest stash, and the CU count and the workgroups a CU holds at that
-// LDS use are read (doing this twice is harmless, so a race between threads is
-// too).  Packed as n_cu * 16 + blocks per CU.
+constexpr int kPipeMaxRowTiles = 3;   // 48 rows: more spill the persistent kernel's registers
+
 template <int NRT>
-hipError_t fused_setup(int* n_cu, int* per_cu) {
+constexpr size_t pipe_lds_bytes(int chunk) {
+    // two buffers of 16-bit codes and tile maxima, then the parking slices
+    const size_t codes = (size_t)NRT * 16 * (chunk + StashU16::kPad) * 2;
+    const size_t tiles = (size_t)NRT * 16 * (chunk / kTile) * sizeof(float);
+    return 2 * (codes + tiles) + kParkFloats * sizeof(float);
+}
+
+// The largest chunk (a multiple of 128 keys) whose two buffers fit in LDS.
+template <int NRT>
+constexpr int max_pipe_chunk() {
+    int c = 128;
+    while (pipe_lds_bytes<NRT>(c + 128) + static_lds_bytes<NRT>() + 1024 <= 160 * 1024) c += 128;
+    return c;
+}
+
+// Once per device and row-tile count: the kernels' dynamic LDS limits are
+// raised to the largest stashes, and the CU count and the workgroups a CU
+// holds at that LDS use are read (doing this twice is harmless, so a race
+// between threads is too).
+struct FusedDevice {
+    int n_cu, per_cu, pipe_per_cu;
+};
+
+template <int NRT>
+hipError_t fused_setup(FusedDevice* out) {
     constexpr int kMaxDevices = 64;
-    static std::atomic<int> state[kMaxDevices];   // packed + 1; 0: not set up yet
+    // packed (n_cu * 16 + per_cu) * 16 + pipe_per_cu, plus 1; 0: not set up yet
+    static std::atomic<int> state[kMaxDevices];
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
@@ -564,29 +774,54 @@ hipError_t fused_setup(int* n_cu, int* per_cu) {
             e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
             if (e != hipSuccess) return e;
         }
-        int cu = 0, blocks = 0;
+        int cu = 0, blocks = 0, pipe_blocks = 0;
+        if constexpr (NRT <= kPipeMaxRowTiles) {
+            const int pipe_lds = (int)pipe_lds_bytes<NRT>(max_pipe_chunk<NRT>());
+            const void* pfns[2] = {reinterpret_cast<const void*>(verify_pipe_kernel<NRT, false>),
+                                   reinterpret_cast<const void*>(verify_pipe_kernel<NRT, true>)};
+            for (const void* f : pfns) {
+                e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, pipe_lds);
+                if (e != hipSuccess) return e;
+            }
+            e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&pipe_blocks, verify_pipe_kernel<NRT, false>,
+                                                             kThreads, pipe_lds);
+            if (e != hipSuccess) return e;
+        }
         e = hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev);
         if (e != hipSuccess) return e;
         e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, verify_fused_kernel<NRT, true, false, false>,
                                                          kThreads, lds);
         if (e != hipSuccess) return e;
-        st = cu * 16 + std::min(blocks, 15) + 1;
+        st = (std::min(cu, (1 << 20) - 1) * 16 + std::min(blocks, 15)) * 16 + std::min(pipe_blocks, 15) + 1;
         if (dev >= 0 && dev < kMaxDevices) state[dev].store(st, std::memory_order_relaxed);
     }
-    *n_cu = (st - 1) / 16;
-    *per_cu = (st - 1) % 16;
+    out->n_cu = (st - 1) / 256;
+    out->per_cu = ((st - 1) / 16) % 16;
+    out->pipe_per_cu = (st - 1) % 16;
     return hipSuccess;
 }
 
 template <int NRT>
 hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, hipStream_t stream) {
-    int n_cu = 0, per_cu = 0;
-    const hipError_t e = fused_setup<NRT>(&n_cu, &per_cu);
+    FusedDevice fd;
+    const hipError_t e = fused_setup<NRT>(&fd);
     if (e != hipSuccess) return e;
-    // non-temporal K/V loads when every workgroup runs in the first round
     const bool paged = a.v.block_table != nullptr;
-    const bool stream1 = n_slots <= n_cu;
     const dim3 grid(n_slots), block(kThreads);
+    if (a.n_tasks > 0) {   // persistent: n_slots workgroups over n_tasks chunks
+        if constexpr (NRT <= kPipeMaxRowTiles) {
+            const size_t dyn = pipe_lds_bytes<NRT>(a.v.chunk);
+            if (paged)
+                hipLaunchKernelGGL((verify_pipe_kernel<NRT, true>), grid, block, dyn, stream, a);
+            else
+                hipLaunchKernelGGL((verify_pipe_kernel<NRT, false>), grid, block, dyn, stream, a);
+            return hipGetLastError();
+        } else {
+            return hipErrorInvalidValue;   // (the host plans it only up to kPipeMaxRowTiles)
+        }
+    }
+    // non-temporal K/V loads when every workgroup runs in the first round
+    const bool stream1 = n_slots <= fd.n_cu;
     if (a.step) {   // (dense caches only; the host checks)
         const size_t dyn = std::max(fused_lds_bytes<NRT>(a.v.chunk), sizeof(SelLds));
         if (stream1)
@@ -611,13 +846,13 @@ hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, hipStream_t stream)
 }
 
 template <int NRT>
-int blocks_per_cu_nrt() {
-    int n_cu = 0, per_cu = 0;
-    if (fused_setup<NRT>(&n_cu, &per_cu) != hipSuccess) {
+FusedDevice fused_device() {
+    FusedDevice fd = {0, 0, 0};
+    if (fused_setup<NRT>(&fd) != hipSuccess) {
         (void)hipGetLastError();
-        return 0;
+        return FusedDevice{0, 0, 0};
     }
-    return per_cu;
+    return fd;
 }
 
 }  // namespace
@@ -633,10 +868,29 @@ int fused_max_chunk(int row_tiles) {
 
 int fused_blocks_per_cu(int row_tiles) {
     switch (row_tiles) {
-        case 1: return blocks_per_cu_nrt<1>();
-        case 2: return blocks_per_cu_nrt<2>();
-        case 3: return blocks_per_cu_nrt<3>();
-        default: return blocks_per_cu_nrt<4>();
+        case 1: return fused_device<1>().per_cu;
+        case 2: return fused_device<2>().per_cu;
+        case 3: return fused_device<3>().per_cu;
+        default: return fused_device<4>().per_cu;
+    }
+}
+
+int pipe_max_chunk(int row_tiles) {
+    static_assert(kPipeMaxRowTiles == 3, "the cases below");
+    switch (row_tiles) {
+        case 1: return max_pipe_chunk<1>();
+        case 2: return max_pipe_chunk<2>();
+        case 3: return max_pipe_chunk<3>();
+        default: return 0;   // not built for more rows
+    }
+}
+
+int pipe_blocks_per_cu(int row_tiles) {
+    switch (row_tiles) {
+        case 1: return fused_device<1>().pipe_per_cu;
+        case 2: return fused_device<2>().pipe_per_cu;
+        case 3: return fused_device<3>().pipe_per_cu;
+        default: return fused_device<4>().pipe_per_cu;
     }
 }
 

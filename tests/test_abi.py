@@ -504,16 +504,22 @@ def _plan_32k(rows_q=7, group=4, T=32768, batch=1, hkv=8):
 
 
 def test_verify_plan_follows_the_cu_budget(lib, cu_budget):
-    """The one-sweep schedule needs every chunk of a (sequence, KV head) resident
+    """The one-workgroup-per-chunk one sweep needs the call's chunks to run in
+    one round of workgroups and every chunk of a (sequence, KV head) resident
     at once, within half of what the CUs hold (one workgroup per CU here): the
     32K workload's heads take 32 chunks of 1024 keys (the LDS stash's limit at
-    28 rows), which fit a 64-CU budget but not a 62-CU one."""
+    28 rows).  Below 256 CUs the persistent form takes over (a grid of the
+    budget, at most one grid of chunks per head, 1024 keys of 16-bit stash),
+    and below 32 CUs neither fits: two sweeps."""
     s, p, ctx, ql = _plan_32k()
     cu_budget(256)
     assert B.verify_plan(s, p, ctx, ql) == (B.VERIFY_ONE_SWEEP, 1024, 256)
-    cu_budget(64)
-    assert B.verify_plan(s, p, ctx, ql) == (B.VERIFY_ONE_SWEEP, 1024, 256)
-    cu_budget(62)
+    for n in (64, 32):
+        cu_budget(n)
+        assert B.verify_plan(s, p, ctx, ql) == (B.VERIFY_ONE_SWEEP_PERSISTENT, 1024, 256), n
+    cu_budget(62)   # 896 keys: 296 chunks in five rounds of 62, against 256 in five
+    assert B.verify_plan(s, p, ctx, ql) == (B.VERIFY_ONE_SWEEP_PERSISTENT, 896, 296)
+    cu_budget(31)
     assert B.verify_plan(s, p, ctx, ql)[0] == B.VERIFY_TWO_SWEEP
     cu_budget(16)
     assert B.verify_plan(s, p, ctx, ql)[0] == B.VERIFY_TWO_SWEEP
@@ -524,9 +530,29 @@ def test_verify_plan_follows_the_cu_budget(lib, cu_budget):
     q_a, q_p = _i32(*ql)
     assert lib.ssl_verify_workspace(ctypes.byref(s), ctypes.byref(one), ctx_p, q_p,
                                     ctypes.byref(n)) == B.SSL_ERR_UNSUPPORTED
-    # a short context still fits in a small budget
+    # a short context still takes one sweep in a small budget (persistent: its
+    # 32 chunks over 16 workgroups)
     s2, p2, ctx2, ql2 = _plan_32k(T=4096)
-    assert B.verify_plan(s2, p2, ctx2, ql2)[0] == B.VERIFY_ONE_SWEEP
+    assert B.verify_plan(s2, p2, ctx2, ql2)[0] == B.VERIFY_ONE_SWEEP_PERSISTENT
+
+
+def test_persistent_plan_limits(lib, cu_budget):
+    """The persistent form: at most 48 rows per KV head (its kernel is built for
+    three row tiles), at most 64 chunks per head, a grid of what the budget
+    holds and never more workgroups than chunks; its chunks a multiple of 128
+    keys within the two 16-bit stash buffers' limit."""
+    cu_budget(64)
+    for rows_q, group, ok in ((7, 4, True), (6, 8, True), (16, 4, False)):
+        s, p, ctx, ql = _plan_32k(rows_q=rows_q, group=group)
+        sch, chunk, items = B.verify_plan(s, p, ctx, ql)
+        if ok:
+            assert sch == B.VERIFY_ONE_SWEEP_PERSISTENT and chunk % 128 == 0, (rows_q, group)
+            assert -(-32768 // chunk) <= 64 and items == 8 * -(-32768 // chunk)
+        else:
+            assert sch == B.VERIFY_TWO_SWEEP, (rows_q, group)
+    # a head of 131K keys needs more than 64 chunks of what 48 rows allow
+    s, p, ctx, ql = _plan_32k(rows_q=6, group=8, T=131072)
+    assert B.verify_plan(s, p, ctx, ql)[0] == B.VERIFY_TWO_SWEEP
 
 
 def test_select_plan_follows_the_cu_budget(lib, cu_budget):

@@ -192,8 +192,9 @@ def test_a_captured_call_that_gave_up_fails_until_its_workspace_is_cleared():
 
 @pytest.mark.parametrize("budget", [8, 24])
 def test_small_cu_budget_keeps_results_right(budget):
-    """Planned for a few CUs, verify takes two sweeps and select three kernels
-    (or smaller groups); the results still match the oracle."""
+    """Planned for a few CUs, verify takes the persistent one sweep (a grid of
+    the budget) or two sweeps, and select three kernels (or smaller groups);
+    the results still match the oracle."""
     w = generate(211, name="budget", batch=2, n_q_heads=32, n_kv_heads=8, ctx_len=[6000, 2500],
                  q_len=[5, 3], budget=300)
     B.set_cu_budget(budget)

@@ -131,7 +131,8 @@ def test_graph_with_one_shared_workspace():
     cap.wait_stream(torch.cuda.current_stream())
     st = B.PreparedStep(q, k, v, qd, ctx, ql, params, out, scores, idx, n_idx, dout, stream=cap,
                         shared_workspace=True)
-    assert B.verify_plan(st.shape, params, ctx, ql)[0] == B.VERIFY_ONE_SWEEP
+    # (three sequences of 16K: 384 chunks, so the persistent one-sweep form)
+    assert B.verify_plan(st.shape, params, ctx, ql)[0] == B.VERIFY_ONE_SWEEP_PERSISTENT
     assert B.select_plan(st.shape, params, ctx)[0] is False
     with torch.cuda.stream(cap):
         st.step_separate()
