@@ -18,6 +18,7 @@ CPU oracle timed on the host's cores on the same workload.
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import math
 import os
@@ -585,6 +586,8 @@ def workload_entry(B, n: int, steps: int, warmup: int, torch, np, cpu: bool):
     sel_one, _, sel_parts = B.select_plan(vshape, params, w.ctx_len)
     for i in range(max(warmup, n_copies)):
         sts[i % n_copies].step()
+    gc.collect()
+    gc.disable()   # (as in the headline passes)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
@@ -606,6 +609,7 @@ def workload_entry(B, n: int, steps: int, warmup: int, torch, np, cpu: bool):
     b2b = {}
     for c in calls:
         b2b[c] = back_to_back_us(lambda i, c=c: getattr(sts[i % n_copies], c)(), steps, stream, torch)
+    gc.enable()
     nbytes, _ = algorithmic_bytes(w, out_bytes=2)
     entry = {"name": w.name, "batch": w.batch, "n_q_heads": w.n_q_heads,
              "n_kv_heads": w.n_kv_heads, "ctx_len": list(map(int, w.ctx_len)),
@@ -764,7 +768,11 @@ def main() -> int:
                 g.replay()
         torch.cuda.synchronize()
 
-    # Headline: exactly K steps back to back, nothing else on the stream.
+    # Headline: exactly K steps back to back, nothing else on the stream.  The
+    # timed passes run with Python's garbage collector paused, so that a
+    # collection cannot stall the host between two launches.
+    gc.collect()
+    gc.disable()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -808,6 +816,7 @@ def main() -> int:
     else:
         v_iso = back_to_back_us(lambda i: steps[i % n_copies].verify(), args.steps, stream, torch)
 
+    gc.enable()
     per = {c: [ev[i][j].elapsed_time(ev[i][j + 1]) * 1e3 for i in range(args.steps)]
            for j, c in enumerate(calls)}
     step_us = [ev[i][0].elapsed_time(ev[i][3]) * 1e3 for i in range(args.steps)]
