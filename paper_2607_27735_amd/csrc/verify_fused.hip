@@ -378,7 +378,7 @@ __device__ __forceinline__ uint64_t publish_chunk(const FusedArgs& fa, const Chu
 // (false: the wait gave up, reported on the status word; nothing written),
 // then writes the scores of the chunk's keys from its stash and the outputs
 // of rows s, s + nchunk, ... .  With kStep the score bits also go to skeys.
-template <int NRT, typename Codec, bool kStep>
+template <int NRT, typename Codec, bool kStep, int kPoll = 8, int kSum = 4>
 __device__ __forceinline__ bool finish_chunk(const FusedArgs& fa, const Chunk& k, uint64_t want,
                                              bool clean, typename Codec::T* stash, int stride,
                                              const float* mtile, int mts,
@@ -399,25 +399,25 @@ __device__ __forceinline__ bool finish_chunk(const FusedArgs& fa, const Chunk& k
         const int rr = tid & (kRowCap - 1), ph = tid >> 6;
         float Mx = -INFINITY, Lx = 0.f;
         bool in_all = clean;
-        for (int s0 = ph; in_all && s0 < nchunk; s0 += 8 * kWaves) {   // wave-uniform
-            uint64_t w0[8], w1[8];
+        for (int s0 = ph; in_all && s0 < nchunk; s0 += kPoll * kWaves) {   // wave-uniform
+            uint64_t w0[kPoll], w1[kPoll];
             // every lane loads (lanes past the rows or chunks re-read valid
             // entries): no branch around the loads
-            const uint64_t* e[8];
+            const uint64_t* e[kPoll];
 #pragma unroll
-            for (int uu = 0; uu < 8; ++uu)
+            for (int uu = 0; uu < kPoll; ++uu)
                 e[uu] = ml64 + ((size_t)(slot0 + min(s0 + uu * kWaves, nchunk - 1)) * kRowCap + min(rr, R - 1)) * 2;
             int spins = 0;
             bool all_in;
             do {
                 bool in = true;
 #pragma unroll
-                for (int uu = 0; uu < 8; ++uu) {
+                for (int uu = 0; uu < kPoll; ++uu) {
                     w0[uu] = ld_dev64(e[uu]);
                     w1[uu] = ld_dev64(e[uu] + 1);
                 }
 #pragma unroll
-                for (int uu = 0; uu < 8; ++uu)
+                for (int uu = 0; uu < kPoll; ++uu)
                     in &= ((w0[uu] & ~0xFFFFFFFFull) == tag_hi && (w1[uu] & ~0xFFFFFFFFull) == tag_hi);
                 all_in = __all(in);
                 if (!all_in) __builtin_amdgcn_s_sleep(1);
@@ -425,7 +425,7 @@ __device__ __forceinline__ bool finish_chunk(const FusedArgs& fa, const Chunk& k
             in_all = all_in;
             if (all_in && rr < R) {
 #pragma unroll
-                for (int uu = 0; uu < 8; ++uu)
+                for (int uu = 0; uu < kPoll; ++uu)
                     if (s0 + uu * kWaves < nchunk)
                         ml_merge(Mx, Lx, __uint_as_float((uint32_t)w0[uu]), __uint_as_float((uint32_t)w1[uu]));
             }
@@ -443,9 +443,9 @@ __device__ __forceinline__ bool finish_chunk(const FusedArgs& fa, const Chunk& k
     // for up to 32 chunks), loaded now so that the round trip overlaps the
     // normalizers and 3b.
     const int d4 = tid & 31, sg = tid >> 5;
-    auto load_part = [&](int row, int s0, f32x4 (&v)[4], float (&m)[4]) {
+    auto load_part = [&](int row, int s0, f32x4 (&v)[kSum], float (&m)[kSum]) {
 #pragma unroll
-        for (int uu = 0; uu < 4; ++uu) {
+        for (int uu = 0; uu < kSum; ++uu) {
             const int s2 = s0 + 8 * uu;
             if (s2 < nchunk) {
                 const size_t rw = (size_t)(slot0 + s2) * kRowCap + row;
@@ -460,8 +460,8 @@ __device__ __forceinline__ bool finish_chunk(const FusedArgs& fa, const Chunk& k
             }
         }
     };
-    f32x4 pv[4];
-    float pm[4];
+    f32x4 pv[kSum];
+    float pm[kSum];
     if (k.s < R) load_part(k.s, sg, pv, pm);
 
     if (tid < kRowCap) {
@@ -543,12 +543,12 @@ __device__ __forceinline__ bool finish_chunk(const FusedArgs& fa, const Chunk& k
         for (int row = k.s; row < R; row += nchunk) {
             const float lse = row_lse[row];
             f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-            for (int s0 = sg; s0 < nchunk; s0 += 4 * 8) {
-                f32x4 v[4];
-                float m[4];
+            for (int s0 = sg; s0 < nchunk; s0 += kSum * 8) {
+                f32x4 v[kSum];
+                float m[kSum];
                 if (row == k.s && s0 == sg) {
 #pragma unroll
-                    for (int uu = 0; uu < 4; ++uu) {
+                    for (int uu = 0; uu < kSum; ++uu) {
                         v[uu] = pv[uu];
                         m[uu] = pm[uu];
                     }
@@ -556,7 +556,7 @@ __device__ __forceinline__ bool finish_chunk(const FusedArgs& fa, const Chunk& k
                     load_part(row, s0, v, m);
                 }
 #pragma unroll
-                for (int uu = 0; uu < 4; ++uu) acc += v[uu] * fast_exp2(m[uu] - lse);
+                for (int uu = 0; uu < kSum; ++uu) acc += v[uu] * fast_exp2(m[uu] - lse);
             }
             red[sg * 32 + d4] = acc;
             __syncthreads();
@@ -644,6 +644,10 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     chunk0_done(fa, k);
 }
 
+// Chunks per lane per statistics poll, and per thread per row-sum pass, in
+// the persistent kernel's finish (its units may have more chunks).
+constexpr int kPipePoll = 16, kPipeSum = 8;
+
 // Persistent one-sweep kernel (16-bit stash, two chunk buffers): workgroup w
 // takes chunks w, w + G, w + 2G, ... (G = the grid, all resident at once).
 // Chunk j's partial output and statistics are published, and chunk j - 1's
@@ -695,7 +699,7 @@ __global__ __launch_bounds__(kThreads) void verify_pipe_kernel(FusedArgs fa) {
                     clear_state<NRT>(M, L, oacc);
                 }
                 if (j >= 2) {
-                    if (finish_chunk<NRT, Codec, false>(fa, k2, want2, clean2, codes(j), stride, tiles(j), mts,
+                    if (finish_chunk<NRT, Codec, false, kPipePoll, kPipeSum>(fa, k2, want2, clean2, codes(j), stride, tiles(j), mts,
                                                         lse_part, row_lse, &wait_failed, nullptr))
                         chunk0_done(fa, k2);
                     else
@@ -710,12 +714,12 @@ __global__ __launch_bounds__(kThreads) void verify_pipe_kernel(FusedArgs fa) {
     }
     want1 = publish_chunk<NRT>(fa, k1, M, L, oacc, wml, park, &wait_failed, &clean1);
     if (n >= 2) {
-        if (!finish_chunk<NRT, Codec, false>(fa, k2, want2, clean2, codes(n), stride, tiles(n), mts, lse_part,
+        if (!finish_chunk<NRT, Codec, false, kPipePoll, kPipeSum>(fa, k2, want2, clean2, codes(n), stride, tiles(n), mts, lse_part,
                                              row_lse, &wait_failed, nullptr))
             return;
         chunk0_done(fa, k2);
     }
-    if (!finish_chunk<NRT, Codec, false>(fa, k1, want1, clean1, codes(n - 1), stride, tiles(n - 1), mts, lse_part,
+    if (!finish_chunk<NRT, Codec, false, kPipePoll, kPipeSum>(fa, k1, want1, clean1, codes(n - 1), stride, tiles(n - 1), mts, lse_part,
                                          row_lse, &wait_failed, nullptr))
         return;
     chunk0_done(fa, k1);
