@@ -1,4 +1,5 @@
-// verify_fused.hip -- single-sweep verify attention with fused Eq. 3 scores.
+// verify_fused.hip -- single-sweep verify attention with fused Eq. 3 scores
+// (Sec. 3.1 verification, Sec. 3.2 Eq. 3).
 //
 // The Eq. 3 score of a key needs the final normalizer of every verify row,
 // which no split of the context knows while it streams.  When every chunk of
@@ -28,11 +29,17 @@
 // a clock-seeded start (consecutive calls differ in the low 32 bits for 2^32
 // calls), so a stale or uninitialised word matches only by a 2^-32 accident.
 //
-// The wait ends: workgroups are dispatched in index order and the chunks of
-// one head are consecutive, so when the lowest unfinished head waits, every
-// workgroup ahead of its chunks has finished and its chunks are resident (the
-// host plans at most half of what the device's CUs hold at once per head).
-// The wait is also bounded: a workgroup whose wait gives up reports it on the
+// Two kernels run these steps.  verify_fused_kernel gives each chunk its own
+// workgroup (fp32 stash; with kStep it then selects and drafts too).  Its wait
+// ends: workgroups are dispatched in index order and the chunks of one head
+// are consecutive, so when the lowest unfinished head waits, every workgroup
+// ahead of its chunks has finished and its chunks are resident (the host
+// plans at most half of what the device's CUs hold at once per head).
+// verify_pipe_kernel, for calls whose chunks would take several rounds of
+// workgroups, is a resident grid that takes every grid-th chunk with two
+// 16-bit stash buffers and runs steps 2-4 of one chunk while the next one
+// streams (its own comment gives the order and why its waits end).  Every
+// wait is also bounded: a workgroup whose wait gives up reports it on the
 // device's status word and leaves without writing scores or outputs.
 #include <algorithm>
 #include <atomic>
@@ -45,31 +52,9 @@ namespace {
 
 using namespace vc;
 
-constexpr int kStashPad = 4;          // floats of padding per stashed row
 constexpr int kParkStride = kHeadDim + 4;                 // floats per parked output row
 constexpr int kParkFloats = 2 * 16 * kParkStride;         // two waves' slices of a row tile
 constexpr float kLazy = 8.f;          // reference-maximum slack, log2 units
-
-template <int NRT>
-constexpr int static_lds_bytes() {
-    return kWaves * NRT * 16 * 8            // wml
-           + kRowCap * 4                    // row_lse
-           + kWaves * kRowCap * 8           // lse_part
-           + 64;
-}
-
-// The largest chunk whose stash (probabilities, padding, one running maximum
-// per tile and row) fits in LDS beside the static arrays and the parking
-// slices.
-template <int NRT>
-constexpr int max_fused_chunk() {
-    constexpr int kLds = 160 * 1024;
-    constexpr int floats_per_row =
-        (kLds - static_lds_bytes<NRT>() - kParkFloats * 4 - 1024) / 4 / (16 * NRT);
-    return (floats_per_row - kStashPad) * kTile / (kTile + 1) / 128 * 128;
-}
-
-__device__ __forceinline__ float safe_max(float m) { return m == -INFINITY ? 0.f : m; }
 
 // The LDS stash holds each key's probability per verify row, relative to the
 // row's reference maximum (at most 2^kLazy).  Two element formats:
@@ -106,6 +91,27 @@ struct StashU16 {
         return f32x4{dec(w.x & 0xFFFFu), dec(w.x >> 16), dec(w.y & 0xFFFFu), dec(w.y >> 16)};
     }
 };
+
+template <int NRT>
+constexpr int static_lds_bytes() {
+    return kWaves * NRT * 16 * 8            // wml
+           + kRowCap * 4                    // row_lse
+           + kWaves * kRowCap * 8           // lse_part
+           + 64;
+}
+
+// The largest chunk whose stash (probabilities, padding, one running maximum
+// per tile and row) fits in LDS beside the static arrays and the parking
+// slices.
+template <int NRT>
+constexpr int max_fused_chunk() {
+    constexpr int kLds = 160 * 1024;
+    constexpr int floats_per_row =
+        (kLds - static_lds_bytes<NRT>() - kParkFloats * 4 - 1024) / 4 / (16 * NRT);
+    return (floats_per_row - StashF32::kPad) * kTile / (kTile + 1) / 128 * 128;
+}
+
+__device__ __forceinline__ float safe_max(float m) { return m == -INFINITY ? 0.f : m; }
 
 // One 32-key tile: online softmax and P.V; the tile's probabilities relative
 // to the rows' reference maxima go to the LDS stash, those maxima to mtile.
@@ -649,15 +655,16 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
 constexpr int kPipePoll = 16, kPipeSum = 8;
 
 // Persistent one-sweep kernel (16-bit stash, two chunk buffers): workgroup w
-// takes chunks w, w + G, w + 2G, ... (G = the grid, all resident at once).
-// Chunk j's partial output and statistics are published, and chunk j - 1's
-// scores and outputs written, at the start of chunk j + 1's sweep, while each
-// wave's first tile of it is in flight; so the exchange of one chunk runs
-// under the streaming of the next.  The wait in chunk j - 1's finish needs
-// only chunks of earlier rounds or of round j, all published before any
-// workgroup's round j + 1 finish: the host keeps a unit's chunks within two
-// consecutive rounds (at most G per unit), so no wait depends on a workgroup
-// that is itself waiting.
+// takes chunks w, w + G, w + 2G, ... (round j: its chunk w + jG; G = the grid,
+// all resident at once).  At the start of round j + 1's sweep, with each
+// wave's first tile of it in flight, the workgroup publishes its round-j chunk
+// and finishes its round j - 1 chunk (whose stash buffer the new sweep then
+// fills), so each chunk's exchange runs a round behind its streaming.  The
+// host keeps a unit's chunks within two consecutive rounds (at most G per
+// unit), so that finish waits only for chunks of rounds j - 1 and j, which
+// every workgroup publishes at the start of rounds j and j + 1, before it
+// waits on anything there: no wait depends on a workgroup that is itself
+// waiting.
 template <int NRT, bool kPaged>
 __global__ __launch_bounds__(kThreads) void verify_pipe_kernel(FusedArgs fa) {
     using Codec = StashU16;
@@ -688,24 +695,26 @@ __global__ __launch_bounds__(kThreads) void verify_pipe_kernel(FusedArgs fa) {
     Chunk k1 = chunk_of(a, w), k2 = k1;   // chunks j - 1 and j - 2
     uint64_t want1 = 0, want2 = 0;
     bool clean1 = false, clean2 = false, failed = false;
+    // (the finish calls are written out: a lambda around them is not inlined
+    // and puts the kernel's locals on the scratch stack)
     for (int j = 0; j < n; ++j) {
         const Chunk k = chunk_of(a, w + j * grid);
         Rows<NRT> r;
         load_rows<NRT>(a, k.b, k.c, k.T, k.nq, 0, k.nq, m16, G, r);
-        sweep_chunk<NRT, false, kPaged, Codec>(
-            a, k, r, codes(j), stride, tiles(j), mts, M, L, oacc, [&] {
-                if (j >= 1) {
-                    want1 = publish_chunk<NRT>(fa, k1, M, L, oacc, wml, park, &wait_failed, &clean1);
-                    clear_state<NRT>(M, L, oacc);
-                }
-                if (j >= 2) {
-                    if (finish_chunk<NRT, Codec, false, kPipePoll, kPipeSum>(fa, k2, want2, clean2, codes(j), stride, tiles(j), mts,
-                                                        lse_part, row_lse, &wait_failed, nullptr))
-                        chunk0_done(fa, k2);
-                    else
-                        failed = true;
-                }
-            });
+        sweep_chunk<NRT, false, kPaged, Codec>(a, k, r, codes(j), stride, tiles(j), mts, M, L, oacc, [&] {
+            if (j >= 1) {
+                want1 = publish_chunk<NRT>(fa, k1, M, L, oacc, wml, park, &wait_failed, &clean1);
+                clear_state<NRT>(M, L, oacc);
+            }
+            if (j >= 2) {   // chunk j - 2's stash: buffer (j - 2) & 1 = j & 1
+                if (finish_chunk<NRT, Codec, false, kPipePoll, kPipeSum>(fa, k2, want2, clean2, codes(j), stride,
+                                                                         tiles(j), mts, lse_part, row_lse,
+                                                                         &wait_failed, nullptr))
+                    chunk0_done(fa, k2);
+                else
+                    failed = true;
+            }
+        });
         if (failed) return;
         k2 = k1;
         want2 = want1;
@@ -714,13 +723,14 @@ __global__ __launch_bounds__(kThreads) void verify_pipe_kernel(FusedArgs fa) {
     }
     want1 = publish_chunk<NRT>(fa, k1, M, L, oacc, wml, park, &wait_failed, &clean1);
     if (n >= 2) {
-        if (!finish_chunk<NRT, Codec, false, kPipePoll, kPipeSum>(fa, k2, want2, clean2, codes(n), stride, tiles(n), mts, lse_part,
-                                             row_lse, &wait_failed, nullptr))
+        if (!finish_chunk<NRT, Codec, false, kPipePoll, kPipeSum>(fa, k2, want2, clean2, codes(n), stride, tiles(n),
+                                                                  mts, lse_part, row_lse, &wait_failed, nullptr))
             return;
         chunk0_done(fa, k2);
     }
-    if (!finish_chunk<NRT, Codec, false, kPipePoll, kPipeSum>(fa, k1, want1, clean1, codes(n - 1), stride, tiles(n - 1), mts, lse_part,
-                                         row_lse, &wait_failed, nullptr))
+    if (!finish_chunk<NRT, Codec, false, kPipePoll, kPipeSum>(fa, k1, want1, clean1, codes(n - 1), stride,
+                                                              tiles(n - 1), mts, lse_part, row_lse, &wait_failed,
+                                                              nullptr))
         return;
     chunk0_done(fa, k1);
 }
@@ -728,7 +738,7 @@ __global__ __launch_bounds__(kThreads) void verify_pipe_kernel(FusedArgs fa) {
 template <int NRT>
 constexpr size_t fused_lds_bytes(int chunk) {
     // the probability stash with its tile maxima, then the parking slices
-    return ((size_t)NRT * 16 * (chunk + kStashPad + chunk / kTile) + kParkFloats) * sizeof(float);
+    return ((size_t)NRT * 16 * (chunk + StashF32::kPad + chunk / kTile) + kParkFloats) * sizeof(float);
 }
 
 constexpr int kPipeMaxRowTiles = 3;   // 48 rows: more spill the persistent kernel's registers
