@@ -221,10 +221,13 @@ constexpr int kTags = kSelectTagWords;   // tag words per partition: histogram e
 // merges the partials in partition order and writes the output.  Called by
 // every thread of the workgroup; returns whether partition 0 completed (the
 // caller then advances the exchange epoch).
-__device__ bool select_draft_tail(const SelectArgs& a, const Geom& g, int u, int p, int n_mid,
-                                  int mid_base, int s_len, int n_rec, const uint32_t* rows_l,
-                                  float* park, float2* wml, float2* gml, int* wait_failed,
-                                  uint64_t* tag, uint64_t want, uint64_t pub) {
+// (Inlined: a call would take the address of the launch arguments, which the
+// compiler then copies to scratch memory for the whole kernel.)
+__device__ __forceinline__ bool select_draft_tail(const SelectArgs& a, const Geom& g, int u, int p,
+                                                  int n_mid, int mid_base, int s_len, int n_rec,
+                                                  const uint32_t* rows_l, float* park, float2* wml,
+                                                  float2* gml, int* wait_failed, uint64_t* tag,
+                                                  uint64_t want, uint64_t pub) {
     using dc::kTile;
     const SelectDraft& d = a.d;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
