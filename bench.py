@@ -125,7 +125,8 @@ def summarize_trace(d: str, command: str, title: str = "") -> str:
                 else "draft round step (index list)" if k == "draft_kernel" and mode == "1"
                 else "draft round step (materialized rows)" if k == "draft_kernel" and mode == "2"
                 else "logit statistics" if k.startswith("logit")
-                else "greedy acceptance" if k.startswith("greedy") else "draft")
+                else "greedy acceptance" if k.startswith("greedy")
+                else "speculative sampling" if k.startswith("spec_") else "draft")
         per_call[call] = per_call.get(call, 0.0) + float(r["AverageNs"]) / 1e3
     out += ["", "sum of kernel averages per call: " +
             ", ".join(f"{c} {v:.2f} us" for c, v in per_call.items())]
