@@ -210,6 +210,69 @@ __device__ __forceinline__ void wait_counts(const uint64_t* tag, int n, int stri
 constexpr int kTags = kSelectTagWords;   // tag words per partition: histogram entries, candidates,
                                          // middle above d1, draft partial
 
+// Output columns 4 d4 .. 4 d4 + 3 of head row `row` (x = row * 32 + d4) of KV
+// head c of sequence b: the merged sum over its total.
+__device__ __forceinline__ void draft_out(const SelectDraft& d, int b, int c, int x, const f32x4& acc, float Lx) {
+    const int row = x >> 5, d4 = x & 31;
+    const f32x4 o = acc * (1.0f / Lx);
+    const size_t base = ((size_t)b * d.n_q_heads + c * d.group + row) * kHeadDim + 4 * d4;
+    if (d.out_fp32) {
+        *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(d.out) + base) = o;
+    } else {
+        const uint2 pk = make_uint2(pack_bf16(o[0], o[1]), pack_bf16(o[2], o[3]));
+        *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(d.out) + base) = pk;
+    }
+}
+
+constexpr int kSelectMergeBatch = 16;   // draft partials merged per round trip
+
+// Folds the draft partials of partitions p0 .. p0 + kSelectMergeBatch - 1
+// (those below P) into (Mx, Lx, acc) for head row `row`, columns 4 d4 ..
+// 4 d4 + 3: partition 0's own from the LDS park (its four waves), the others'
+// from their published slots (loaded together, one round trip).
+__device__ __forceinline__ void absorb_partials(int p0, int P, int row, int d4, const float* part0,
+                                                const float* park, const float2* gml, float& Mx,
+                                                float& Lx, f32x4& acc) {
+    constexpr int kStride = kSelectDraftStride;
+    float2 ml[kSelectMergeBatch];
+    f32x4 o[kSelectMergeBatch];
+#pragma unroll
+    for (int uu = 0; uu < kSelectMergeBatch; ++uu) {
+        const int pp = p0 + uu;
+        if (pp == 0) {
+            ml[uu] = gml[row];
+            f32x4 ov = *reinterpret_cast<const f32x4*>(park + row * kStride + 4 + 4 * d4);
+#pragma unroll
+            for (int w = 1; w < kSelWaves; ++w)
+                ov += *reinterpret_cast<const f32x4*>(park + (w * 16 + row) * kStride + 4 + 4 * d4);
+            o[uu] = ov;
+        } else if (pp < P) {
+            const float* dp = part0 + ((size_t)pp * 16 + row) * kStride;
+            ml[uu] = __builtin_bit_cast(float2, ld_dev64(reinterpret_cast<const uint64_t*>(dp)));
+            const uint64_t* po = reinterpret_cast<const uint64_t*>(dp + 4) + 2 * d4;
+            const float2 lo = __builtin_bit_cast(float2, ld_dev64(po));
+            const float2 hi = __builtin_bit_cast(float2, ld_dev64(po + 1));
+            o[uu] = f32x4{lo.x, lo.y, hi.x, hi.y};
+        } else {
+            ml[uu] = make_float2(-INFINITY, 0.f);
+            o[uu] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+    }
+    float Mn = Mx;
+#pragma unroll
+    for (int uu = 0; uu < kSelectMergeBatch; ++uu) Mn = fmaxf(Mn, ml[uu].x);
+    const float alpha = Mx == -INFINITY ? 0.f : fast_exp2(Mx - Mn);
+    Lx *= alpha;
+    acc *= alpha;
+#pragma unroll
+    for (int uu = 0; uu < kSelectMergeBatch; ++uu) {
+        const float wgt = ml[uu].x == -INFINITY ? 0.f : fast_exp2(ml[uu].x - Mn);
+        Lx += ml[uu].y * wgt;
+        acc += o[uu] * wgt;
+    }
+    Mx = Mn;
+}
+
 // The first draft step (Eq. 5) over the rows partition p selected, run by the
 // select kernel so that no second launch reads the index set back.  Entries
 // e < n_mid are the partition's selected middle positions (rows_l[e], or
@@ -226,8 +289,8 @@ constexpr int kTags = kSelectTagWords;   // tag words per partition: histogram e
 __device__ __forceinline__ bool select_draft_tail(const SelectArgs& a, const Geom& g, int u, int p,
                                                   int n_mid, int mid_base, int s_len, int n_rec,
                                                   const uint32_t* rows_l, float* park, float2* wml,
-                                                  float2* gml, int* wait_failed, uint64_t* tag,
-                                                  uint64_t want, uint64_t pub) {
+                                                  float2* gml, float2* xfer, int* wait_failed,
+                                                  uint64_t* tag, uint64_t want, uint64_t pub) {
     using dc::kTile;
     const SelectDraft& d = a.d;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -338,58 +401,40 @@ __device__ __forceinline__ bool select_draft_tail(const SelectArgs& a, const Geo
         if (tid == 0) exchange_gave_up(a.xc, kStatusSelect, a.epoch ? a.epoch + u : nullptr);
         return false;
     }
-    constexpr int kBatch = 16;
-    for (int x = tid; x < gq * (kHeadDim / 4); x += kSelThreads) {
-        const int row = x >> 5, d4 = x & 31;
+    // Every head row's output sums P partials; thread (row, d4) takes
+    // columns 4 d4 .. 4 d4 + 3, kSelectMergeBatch partitions per round trip.
+    // When there are more partitions than one batch and the rows fit in half
+    // the workgroup, the halves take alternate batches at once and half 1
+    // hands its sum to half 0 through LDS (xfer): one round trip fewer.
+    const int cols = gq * (kHeadDim / 4);
+    if (P > kSelectMergeBatch && 2 * cols <= kSelThreads) {
+        const int half = tid / (kSelThreads / 2), x = tid % (kSelThreads / 2);
         float Mx = -INFINITY, Lx = 0.f;
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        for (int p0 = 0; p0 < P; p0 += kBatch) {
-            float2 ml[kBatch];
-            f32x4 o[kBatch];
-#pragma unroll
-            for (int uu = 0; uu < kBatch; ++uu) {
-                const int pp = p0 + uu;
-                if (pp == 0) {
-                    ml[uu] = gml[row];
-                    f32x4 ov = *reinterpret_cast<const f32x4*>(park + row * kStride + 4 + 4 * d4);
-#pragma unroll
-                    for (int w = 1; w < kSelWaves; ++w)
-                        ov += *reinterpret_cast<const f32x4*>(park + (w * 16 + row) * kStride + 4 + 4 * d4);
-                    o[uu] = ov;
-                } else if (pp < P) {
-                    const float* dp = part0 + ((size_t)pp * 16 + row) * kStride;
-                    ml[uu] = __builtin_bit_cast(float2, ld_dev64(reinterpret_cast<const uint64_t*>(dp)));
-                    const uint64_t* po = reinterpret_cast<const uint64_t*>(dp + 4) + 2 * d4;
-                    const float2 lo = __builtin_bit_cast(float2, ld_dev64(po));
-                    const float2 hi = __builtin_bit_cast(float2, ld_dev64(po + 1));
-                    o[uu] = f32x4{lo.x, lo.y, hi.x, hi.y};
-                } else {
-                    ml[uu] = make_float2(-INFINITY, 0.f);
-                    o[uu] = f32x4{0.f, 0.f, 0.f, 0.f};
-                }
-            }
-            float Mn = Mx;
-#pragma unroll
-            for (int uu = 0; uu < kBatch; ++uu) Mn = fmaxf(Mn, ml[uu].x);
-            const float alpha = Mx == -INFINITY ? 0.f : fast_exp2(Mx - Mn);
-            Lx *= alpha;
-            acc *= alpha;
-#pragma unroll
-            for (int uu = 0; uu < kBatch; ++uu) {
-                const float wgt = ml[uu].x == -INFINITY ? 0.f : fast_exp2(ml[uu].x - Mn);
-                Lx += ml[uu].y * wgt;
-                acc += o[uu] * wgt;
-            }
-            Mx = Mn;
+        if (x < cols)
+            for (int p0 = half * kSelectMergeBatch; p0 < P; p0 += 2 * kSelectMergeBatch)
+                absorb_partials(p0, P, x >> 5, x & 31, part0, park, gml, Mx, Lx, acc);
+        if (half == 1 && x < cols) {
+            xfer[x] = make_float2(Mx, Lx);
+            reinterpret_cast<f32x4*>(xfer + kSelThreads / 2)[x] = acc;
         }
-        acc *= 1.0f / Lx;
-        const size_t base = ((size_t)b * d.n_q_heads + c * gq + row) * kHeadDim + 4 * d4;
-        if (d.out_fp32) {
-            *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(d.out) + base) = acc;
-        } else {
-            const uint2 pk = make_uint2(pack_bf16(acc[0], acc[1]), pack_bf16(acc[2], acc[3]));
-            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(d.out) + base) = pk;
+        __syncthreads();
+        if (half == 0 && x < cols) {
+            const float2 ml = xfer[x];
+            const f32x4 o = reinterpret_cast<const f32x4*>(xfer + kSelThreads / 2)[x];
+            const float Mn = fmaxf(Mx, ml.x);
+            const float w0 = Mx == -INFINITY ? 0.f : fast_exp2(Mx - Mn);
+            const float w1 = ml.x == -INFINITY ? 0.f : fast_exp2(ml.x - Mn);
+            draft_out(d, b, c, x, acc * w0 + o * w1, Lx * w0 + ml.y * w1);
         }
+        return true;
+    }
+    for (int x = tid; x < cols; x += kSelThreads) {
+        float Mx = -INFINITY, Lx = 0.f;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int p0 = 0; p0 < P; p0 += kSelectMergeBatch)
+            absorb_partials(p0, P, x >> 5, x & 31, part0, park, gml, Mx, Lx, acc);
+        draft_out(d, b, c, x, acc, Lx);
     }
     return true;
 }
@@ -413,6 +458,9 @@ struct __attribute__((aligned(16))) SelLds {
     int wait_failed;
     float2 d_wml[kSelWaves * 16], d_gml[16];
 };
+
+static_assert(sizeof(SelLds::h2) >= (kSelThreads / 2) * (sizeof(float2) + sizeof(f32x4)),
+              "the draft merge's half-to-half exchange fits h2 (free by then)");
 
 // Clears the partition's counters and histograms its keys (bins of the top 12
 // score bits).  Synchronises the workgroup before and after the adds.
@@ -457,7 +505,8 @@ __device__ __forceinline__ bool select_simple(const SelectArgs& a, const Geom& g
                                  !all && p == 0 ? g.s_end : 0, !all && p == 0 ? g.T - g.r_start : 0,
                                  reinterpret_cast<uint32_t*>(L.cand_p),
                                  reinterpret_cast<float*>(L.cand_lds), L.d_wml, L.d_gml,
-                                 &L.wait_failed, tag, want, want ^ a.xc.tag_flip);
+                                 reinterpret_cast<float2*>(L.h2), &L.wait_failed, tag, want,
+                                 want ^ a.xc.tag_flip);
     }
     return false;
 }
@@ -871,7 +920,7 @@ __device__ __forceinline__ bool select_partition(const SelectArgs& a, const Geom
         __syncthreads();   // the row list and the free candidate cache
         return select_draft_tail(a, g, u, p, n_mid, -1, p == 0 ? g.s_end : 0,
                                  p == 0 ? g.T - g.r_start : 0, d_rows, d_park, L.d_wml, L.d_gml,
-                                 &wait_failed, tag, want, pub);
+                                 reinterpret_cast<float2*>(L.h2), &wait_failed, tag, want, pub);
     }
     return p == 0;
 }
