@@ -585,10 +585,10 @@ def workload_entry(B, n: int, steps: int, warmup: int, torch, np, cpu: bool):
     vshape = B.verify_shape(q, k0)
     schedule, vchunk, vitems = B.verify_plan(vshape, params, w.ctx_len, w.q_len)
     sel_one, _, sel_parts = B.select_plan(vshape, params, w.ctx_len)
-    for i in range(max(warmup, n_copies)):
-        sts[i % n_copies].step()
     gc.collect()
     gc.disable()   # (as in the headline passes)
+    for i in range(max(warmup, n_copies)):
+        sts[i % n_copies].step()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
@@ -596,6 +596,12 @@ def workload_entry(B, n: int, steps: int, warmup: int, torch, np, cpu: bool):
     torch.cuda.synchronize()
     step_us = (time.perf_counter() - t0) * 1e6 / steps
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    for e in ev:   # (created at their first record: not inside the pass)
+        for x in e:
+            x.record(stream)
+    for c in ("verify", "select", "draft"):   # (first launches load kernels: not inside the pass)
+        getattr(sts[-1], c)()
+    torch.cuda.synchronize()
     for i in range(steps):
         st, e = sts[i % n_copies], ev[i]
         e[0].record(stream)
@@ -733,6 +739,11 @@ def main() -> int:
     stream = torch.cuda.current_stream()
     steps = [B.PreparedStep(q, k, v, qd, w.ctx_len, w.q_len, params, out, scores, idx, n_idx,
                             dout, stream=stream) for (k, v) in kvs]
+    # The timed passes run with Python's garbage collector paused, so that a
+    # collection cannot stall the host between two launches; the collection
+    # runs before the warm-up, not between it and the timed steps.
+    gc.collect()
+    gc.disable()
     for i in range(args.warmup):
         steps[i % n_copies].step()
     torch.cuda.synchronize()
@@ -769,11 +780,7 @@ def main() -> int:
                 g.replay()
         torch.cuda.synchronize()
 
-    # Headline: exactly K steps back to back, nothing else on the stream.  The
-    # timed passes run with Python's garbage collector paused, so that a
-    # collection cannot stall the host between two launches.
-    gc.collect()
-    gc.disable()
+    # Headline: exactly K steps back to back, nothing else on the stream.
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -787,6 +794,12 @@ def main() -> int:
     # Breakdown: K more steps with HIP events between the calls (on the stream
     # the kernels run on) for the per-call durations and the roofline.
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for e in ev:   # (torch creates an event's HIP event at its first record: not inside the pass)
+        for x in e:
+            x.record(stream)
+    if graphs is None:   # each call's first launch loads its kernels: not inside the pass
+        for c in calls:
+            getattr(steps[-1], c)()
     torch.cuda.synchronize()
     for i in range(args.steps):
         e = ev[i]
@@ -812,10 +825,16 @@ def main() -> int:
 
     # Roofline: K verify calls back to back (a different KV copy each) between
     # two events, i.e. the call's average launch duration in steady state.
-    if graphs is not None:
-        v_iso = back_to_back_us(lambda i: graphs[i % n_copies][0].replay(), args.steps, stream, torch)
-    else:
-        v_iso = back_to_back_us(lambda i: steps[i % n_copies].verify(), args.steps, stream, torch)
+    # The same for select and draft: each call's bandwidth figures below come
+    # from these back-to-back averages, which a host stall between two launches
+    # of the event-bracketed pass above cannot inflate.
+    b2b = {}
+    for j, c in enumerate(calls):
+        if graphs is not None:
+            b2b[c] = back_to_back_us(lambda i, j=j: graphs[i % n_copies][j].replay(), args.steps, stream, torch)
+        else:
+            b2b[c] = back_to_back_us(lambda i, c=c: getattr(steps[i % n_copies], c)(), args.steps, stream, torch)
+    v_iso = b2b["verify"]
 
     gc.enable()
     per = {c: [ev[i][j].elapsed_time(ev[i][j + 1]) * 1e3 for i in range(args.steps)]
@@ -826,12 +845,13 @@ def main() -> int:
     kernels = {}
     for c in calls:
         avg = statistics.fmean(per[c])
-        kernels[c] = {"avg_us": round(avg, 3), "median_us": round(statistics.median(per[c]), 3),
+        kernels[c] = {"back_to_back_us": round(b2b[c], 3),
+                      "avg_us": round(avg, 3), "median_us": round(statistics.median(per[c]), 3),
                       "p10_us": round(float(np.percentile(per[c], 10)), 3),
                       "p90_us": round(float(np.percentile(per[c], 90)), 3),
                       "alg_bytes": nbytes[c],
-                      "gbps": round(nbytes[c] / (avg * 1e-6) / 1e9, 1),
-                      "hbm_frac": round(nbytes[c] / (avg * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)}
+                      "gbps": round(nbytes[c] / (b2b[c] * 1e-6) / 1e9, 1),
+                      "hbm_frac": round(nbytes[c] / (b2b[c] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)}
     v_avg = round(v_iso, 3)
     step_total = sum(nbytes.values())
     result = {
@@ -874,6 +894,9 @@ def main() -> int:
                      "avg_launch_us": v_avg,
                      "timing": "K back-to-back verify calls between two HIP events on the launch stream, after one untimed call"},
         "kernels": kernels,
+        "kernels_timing": "back_to_back_us: K calls of one kind back to back between two HIP events "
+                          "(after one untimed call), which gbps and hbm_frac use; avg, median, p10, "
+                          "p90: each call bracketed by events inside K whole steps",
     }
     if args.workload == 2 and args.mode == "eager" and args.verify_mode == "auto":
         result["mfma"] = measured_mfma("verify_fused_kernel<2, true, false, false>", v_avg)
