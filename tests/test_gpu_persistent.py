@@ -48,6 +48,12 @@ CASES = {
     "kv8-rows48-g8": (lambda: _poison(generate(
         503, name="kv8-rows48-g8", batch=2, n_q_heads=64, n_kv_heads=8, ctx_len=[2600, 1300],
         q_len=[6, 4], max_ctx=2600, max_q=6, budget=200)), 8),
+    # sixteen sequences of 1-3000 keys and 1-8 positions: many short units,
+    # several per round, some of a single chunk
+    "b16-short": (lambda: _poison(generate(
+        505, name="b16-short", batch=16, n_q_heads=8, n_kv_heads=2,
+        ctx_len=[2433, 2551, 917, 2110, 2226, 53, 935, 2997, 601, 2338, 1248, 1530, 2013, 235, 658, 983],
+        q_len=[3, 7, 8, 6, 2, 7, 3, 8, 7, 5, 6, 2, 3, 3, 8, 7], max_ctx=3000, max_q=8, budget=128)), 8),
     # tiny contexts: chunks of a single key, sequences shorter than a tile
     "tiny-T": (lambda: _poison(generate(
         504, name="tiny-T", batch=4, n_q_heads=8, n_kv_heads=2, ctx_len=[1, 5, 130, 700],
