@@ -41,8 +41,13 @@ def _kernels(tmp_path):
             pytest.skip(f"{tool} not available")
     if not shutil.which("objcopy") or not shutil.which("c++filt"):
         pytest.skip("binutils not available")
+    # objcopy with no output file rewrites its input in place, which would
+    # change the pages of a library this process already has loaded: it works
+    # on a copy.
+    lib_copy = tmp_path / "lib.so"
+    shutil.copyfile(LIB, lib_copy)
     fatbin = tmp_path / "fatbin.bin"
-    subprocess.run(["objcopy", "--dump-section", f".hip_fatbin={fatbin}", LIB], check=True)
+    subprocess.run(["objcopy", "--dump-section", f".hip_fatbin={fatbin}", str(lib_copy)], check=True)
     data = fatbin.read_bytes()
     starts = [m.start() for m in re.finditer(re.escape(MAGIC), data)]
     assert starts, "no offload bundles in the library"
