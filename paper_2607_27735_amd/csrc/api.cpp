@@ -170,6 +170,7 @@ struct VerifyPlan {
     int block_pos;   // verify positions per launch (row blocks); >= every q_len when one block
     bool fused_ok;
     int fused_chunk, fused_slots;
+    bool one_round;  // the one-workgroup-per-chunk one sweep runs in one round of workgroups
     bool pipe;       // one sweep by the persistent kernel: fused_slots chunks over pipe_grid workgroups
     int pipe_grid;
     size_t ml_off, o_off, bytes;
@@ -294,6 +295,7 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
     plan->pipe_grid = 0;
     const int64_t resident1 = n_cu * std::max(fused_blocks_per_cu(plan->row_tiles), 1);
     const bool one_round = plan->fused_ok && plan->fused_slots <= resident1;
+    plan->one_round = one_round;
     // (pipe_max_chunk is 0 where the persistent kernel is not built: > 48 rows)
     if (!one_round && plan->block_pos >= s->max_q) {
         const int64_t grid_cap = n_cu * std::max(pipe_blocks_per_cu(plan->row_tiles), 1);
@@ -335,12 +337,16 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
     return SSL_OK;
 }
 
-// AUTO takes one sweep where it fits and a KV head has at most 32 verify rows;
-// with more rows the single-sweep kernel (one wave per SIMD, logits of every
-// row in LDS) is bound by its per-tile latency and two sweeps are faster.
+// AUTO takes one sweep where it fits and a KV head has at most 32 verify rows,
+// or 48 when it runs in one round of workgroups or in the persistent form;
+// over several rounds at 33-48 rows (one wave per SIMD, logits of every row
+// in LDS) the one-workgroup-per-chunk kernel waits across rounds and two
+// sweeps are faster (70B shape: 457 vs 336 us), while in one round it wins
+// (44 rows at 16K: 26.1 vs 36.5 us; 48 rows at 8K: 21.8 vs 29.6 us).
 bool use_one_sweep(const VerifyPlan& plan, const ssl_params* p) {
     if (!plan.fused_ok || p->verify_mode == SSL_VERIFY_TWO_SWEEP) return false;
-    return p->verify_mode == SSL_VERIFY_ONE_SWEEP || plan.row_tiles <= 2 || plan.pipe;
+    return p->verify_mode == SSL_VERIFY_ONE_SWEEP || plan.row_tiles <= 2 || plan.pipe ||
+           (plan.row_tiles == 3 && plan.one_round);
 }
 
 struct DraftPlan {

@@ -555,6 +555,26 @@ def test_persistent_plan_limits(lib, cu_budget):
     assert B.verify_plan(s, p, ctx, ql)[0] == B.VERIFY_TWO_SWEEP
 
 
+def test_auto_one_sweep_at_three_row_tiles_needs_one_round(lib, cu_budget):
+    """33-48 rows per KV head: AUTO takes the one-workgroup-per-chunk one sweep
+    when its chunks run in one round of workgroups (44 rows at 16K: 256 chunks
+    of 512 keys), the persistent form where that applies, and two sweeps where
+    neither does (48 rows over 64K keys per head: 103 chunks of 640 keys)."""
+    cu_budget(256)
+    s, p, ctx, ql = _plan_32k(rows_q=11, group=4, T=16384)
+    assert B.verify_plan(s, p, ctx, ql) == (B.VERIFY_ONE_SWEEP, 512, 256)
+    assert B.decode_step_plan(s, p, ctx, ql) is True
+    s, p, ctx, ql = _plan_32k(rows_q=6, group=8, T=8192)
+    assert B.verify_plan(s, p, ctx, ql)[0] == B.VERIFY_ONE_SWEEP
+    s, p, ctx, ql = _plan_32k(rows_q=9, group=4, T=32768)   # 416 chunks of 640: persistent
+    assert B.verify_plan(s, p, ctx, ql)[0] == B.VERIFY_ONE_SWEEP_PERSISTENT
+    s, p, ctx, ql = _plan_32k(rows_q=6, group=8, T=65536, batch=4)
+    assert B.verify_plan(s, p, ctx, ql)[0] == B.VERIFY_TWO_SWEEP
+    # 64 rows (four row tiles) keep two sweeps even in one round
+    s, p, ctx, ql = _plan_32k(rows_q=16, group=4, T=4096)
+    assert B.verify_plan(s, p, ctx, ql)[0] == B.VERIFY_TWO_SWEEP
+
+
 def test_select_plan_follows_the_cu_budget(lib, cu_budget):
     s, p, ctx, _ = _plan_32k()
     cu_budget(256)

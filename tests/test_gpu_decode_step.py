@@ -39,7 +39,8 @@ def test_decode_step_bf16_outputs(name):
 
 # Shapes whose step runs as one kernel on the full device (every chunk
 # workgroup resident at once, chunks of >= 512 keys): ragged contexts with
-# ragged last chunks, ragged verify lengths, groups of 4, 8 and 16.
+# ragged last chunks, ragged verify lengths, groups of 4, 8 and 16, two and
+# three row tiles.
 ONE_KERNEL = {
     "b2-kv8-ragged": lambda: generate(611, name="b2-kv8-ragged", batch=2, n_q_heads=32,
                                       n_kv_heads=8, ctx_len=[8192, 5000], q_len=[5, 3],
@@ -49,6 +50,9 @@ ONE_KERNEL = {
                                   max_ctx=20000),
     "b1-kv2-g16": lambda: generate(613, name="b1-kv2-g16", batch=1, n_q_heads=32, n_kv_heads=2,
                                    ctx_len=[60000], q_len=[2], budget=2048, window=1),
+    # 44 rows per KV head: three row tiles, chunks of 512 keys in one round
+    "b1-kv8-rows44": lambda: generate(615, name="b1-kv8-rows44", batch=1, n_q_heads=32, n_kv_heads=8,
+                                      ctx_len=[16384], q_len=[11], budget=2048, heavy_hitters=4),
 }
 
 
