@@ -517,12 +517,18 @@ __device__ __forceinline__ bool select_simple(const SelectArgs& a, const Geom& g
 // partition).  select_local_hist must have run on the same keys; `want` is
 // the unit's exchange tag of this call, whose epoch the caller has checked.
 // With kDraft the first draft step over the partition's selections follows.
-// Returns whether partition 0 completed (its caller then advances the unit's
-// epoch); a partition whose wait gave up has reported it and returns false.
-template <int NR, bool kDraft>
+// mid() runs, on every thread, once the partition's histogram bins are out
+// and before it waits for the others' (work off the exchange's path; it may
+// not touch the select's LDS).  Returns whether partition 0 completed (its
+// caller then advances the unit's epoch); a partition whose wait gave up has
+// reported it and returns false.
+struct NoMid {
+    __device__ void operator()() const {}
+};
+template <int NR, bool kDraft, typename Mid = NoMid>
 __device__ __forceinline__ bool select_partition(const SelectArgs& a, const Geom& g, int p, int u,
                                                  const uint32_t (&keys)[4 * NR], SelLds& L,
-                                                 uint64_t want) {
+                                                 uint64_t want, Mid&& mid = Mid{}) {
     static_assert(!kDraft || NR * kRound <= 4096, "the draft step's row list holds 4096 entries");
     const int b = u / a.n_kv_heads;
     const int c_head = u - b * a.n_kv_heads;
@@ -574,6 +580,7 @@ __device__ __forceinline__ bool select_partition(const SelectArgs& a, const Geom
         // (no wait for the entry stores: every entry carries the call tag)
         if (tid == 0) st_dev64(tag + (size_t)p * kTags + 0, tagged(pub, (uint32_t)n_entries));
     }
+    mid();
     __syncthreads();
     for (int x = tid; x < 2048; x += kSelThreads) hist[x] = 0u;   // now the unit's histogram
     __syncthreads();

@@ -55,6 +55,11 @@ using namespace vc;
 constexpr int kParkStride = kHeadDim + 4;                 // floats per parked output row
 constexpr int kParkFloats = 2 * 16 * kParkStride;         // two waves' slices of a row tile
 constexpr float kLazy = 8.f;          // reference-maximum slack, log2 units
+// The decode step's row-sum scratch (256 f32x4) in the dynamic LDS, past the
+// select's.
+constexpr size_t kStepRedOffset = (sizeof(SelLds) + 15) / 16 * 16;
+constexpr size_t kStepLdsMin = kStepRedOffset + 256 * sizeof(f32x4);
+static_assert(kStepLdsMin + 8 * 1024 <= 160 * 1024, "the step's LDS fits beside the static arrays");
 
 // The LDS stash holds each key's probability per verify row, relative to the
 // row's reference maximum (at most 2^kLazy).  Two element formats:
@@ -185,10 +190,10 @@ __device__ __forceinline__ void fused_tile(const VerifyArgs& a, const Rows<NRT>&
 // The decode step's select (partition p of unit u): the keys in the select
 // layout from the chunk's score bits in skeys (LDS), then the one-kernel
 // select and draft step (select_common.h) with the stash as their LDS.
-template <int NR>
+template <int NR, typename Mid>
 __device__ __forceinline__ bool step_select(const SelectArgs& sa, const Geom& g, int p, int u,
                                             const uint32_t* skeys, int nk, int key_begin,
-                                            SelLds& L, uint64_t want) {
+                                            SelLds& L, uint64_t want, Mid&& mid) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     uint32_t keys[4 * NR];
 #pragma unroll
@@ -203,7 +208,7 @@ __device__ __forceinline__ bool step_select(const SelectArgs& sa, const Geom& g,
         }
     __syncthreads();   // every key is read: the stash becomes the select's
     select_local_hist<NR>(keys, L);
-    return select_partition<NR, true>(sa, g, p, u, keys, L, want);
+    return select_partition<NR, true>(sa, g, p, u, keys, L, want, mid);
 }
 
 // A chunk of one (sequence, KV head): work item `slot` of the launch.
@@ -379,12 +384,86 @@ __device__ __forceinline__ uint64_t publish_chunk(const FusedArgs& fa, const Chu
     return want;
 }
 
+// Partial outputs and maxima of row `row` of chunks s0, s0 + 8, ... (kSum of
+// them; past the unit's chunks: zero and -inf), columns 4 d4 .. 4 d4 + 3.
+template <int kSum>
+__device__ __forceinline__ void load_part(const VerifyArgs& a, const Chunk& k, int row, int s0, int d4,
+                                          f32x4 (&v)[kSum], float (&m)[kSum]) {
+    const uint64_t* ml64 = reinterpret_cast<const uint64_t*>(a.part_ml);   // [slot][kRowCap][2]
+#pragma unroll
+    for (int uu = 0; uu < kSum; ++uu) {
+        const int s2 = s0 + 8 * uu;
+        if (s2 < k.nchunk) {
+            const size_t rw = (size_t)(k.slot0 + s2) * kRowCap + row;
+            const uint64_t* s64 = reinterpret_cast<const uint64_t*>(a.part_o + rw * kHeadDim + 4 * d4);
+            const float2 lo = __builtin_bit_cast(float2, ld_dev64(s64));
+            const float2 hi = __builtin_bit_cast(float2, ld_dev64(s64 + 1));
+            v[uu] = f32x4{lo.x, lo.y, hi.x, hi.y};
+            m[uu] = __uint_as_float((uint32_t)ld_dev64(ml64 + rw * 2));
+        } else {
+            v[uu] = f32x4{0.f, 0.f, 0.f, 0.f};
+            m[uu] = -INFINITY;
+        }
+    }
+}
+
+// ---- 4. rows s, s + nchunk, ... summed over the unit's chunks ----------
+// Every thread calls this, with the normalizers in row_lse; red: 256 f32x4
+// of free LDS.  A chunk's partial is relative to its maxima m: it enters with
+// 2^(m - lse).  Chunks are added in index order within eight interleaved
+// groups, then the groups in order.  pre_v / pre_m (or null): the first batch
+// of row s, already loaded.
+template <int kSum>
+__device__ __forceinline__ void row_sums(const VerifyArgs& a, const Chunk& k, const float* row_lse,
+                                         f32x4* red, const f32x4 (*pre_v)[kSum],
+                                         const float (*pre_m)[kSum]) {
+    const int tid = threadIdx.x, d4 = tid & 31, sg = tid >> 5;
+    const int R = k.R, nchunk = k.nchunk;
+    for (int row = k.s; row < R; row += nchunk) {
+        const float lse = row_lse[row];
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int s0 = sg; s0 < nchunk; s0 += kSum * 8) {
+            f32x4 v[kSum];
+            float m[kSum];
+            if (pre_v && row == k.s && s0 == sg) {
+#pragma unroll
+                for (int uu = 0; uu < kSum; ++uu) {
+                    v[uu] = (*pre_v)[uu];
+                    m[uu] = (*pre_m)[uu];
+                }
+            } else {
+                load_part<kSum>(a, k, row, s0, d4, v, m);
+            }
+#pragma unroll
+            for (int uu = 0; uu < kSum; ++uu) acc += v[uu] * fast_exp2(m[uu] - lse);
+        }
+        red[sg * 32 + d4] = acc;
+        __syncthreads();
+        if (sg == 0) {
+            f32x4 o = red[d4];
+#pragma unroll
+            for (int gq = 1; gq < 8; ++gq) o += red[gq * 32 + d4];
+            const int j = row / a.group;
+            const int h = k.c * a.group + (row - j * a.group);
+            const size_t base = (((size_t)k.b * a.max_q + j) * a.n_q_heads + h) * kHeadDim + 4 * d4;
+            if (a.out_fp32) {
+                *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out) + base) = o;
+            } else {
+                const uint2 pk = make_uint2(pack_bf16(o[0], o[1]), pack_bf16(o[2], o[3]));
+                *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + base) = pk;
+            }
+        }
+        __syncthreads();
+    }
+}
+
 // ---- 3, 4. the chunk's scores and its rows' outputs ----------------------
 // Every thread calls this.  Waits for every chunk's statistics of the unit
 // (false: the wait gave up, reported on the status word; nothing written),
 // then writes the scores of the chunk's keys from its stash and the outputs
-// of rows s, s + nchunk, ... .  With kStep the score bits also go to skeys.
-template <int NRT, typename Codec, bool kStep, int kPoll = 8, int kSum = 4>
+// of rows s, s + nchunk, ... (kDefer: the caller runs row_sums later).  With
+// kStep the score bits also go to skeys.
+template <int NRT, typename Codec, bool kStep, int kPoll = 8, int kSum = 4, bool kDefer = false>
 __device__ __forceinline__ bool finish_chunk(const FusedArgs& fa, const Chunk& k, uint64_t want,
                                              bool clean, typename Codec::T* stash, int stride,
                                              const float* mtile, int mts,
@@ -447,28 +526,11 @@ __device__ __forceinline__ bool finish_chunk(const FusedArgs& fa, const Chunk& k
 
     // The first chunks of this workgroup's first row in step 4 (all of them
     // for up to 32 chunks), loaded now so that the round trip overlaps the
-    // normalizers and 3b.
+    // normalizers and 3b (kDefer: step 4 is left to the caller).
     const int d4 = tid & 31, sg = tid >> 5;
-    auto load_part = [&](int row, int s0, f32x4 (&v)[kSum], float (&m)[kSum]) {
-#pragma unroll
-        for (int uu = 0; uu < kSum; ++uu) {
-            const int s2 = s0 + 8 * uu;
-            if (s2 < nchunk) {
-                const size_t rw = (size_t)(slot0 + s2) * kRowCap + row;
-                const uint64_t* s64 = reinterpret_cast<const uint64_t*>(a.part_o + rw * kHeadDim + 4 * d4);
-                const float2 lo = __builtin_bit_cast(float2, ld_dev64(s64));
-                const float2 hi = __builtin_bit_cast(float2, ld_dev64(s64 + 1));
-                v[uu] = f32x4{lo.x, lo.y, hi.x, hi.y};
-                m[uu] = __uint_as_float((uint32_t)ld_dev64(ml64 + rw * 2));
-            } else {
-                v[uu] = f32x4{0.f, 0.f, 0.f, 0.f};
-                m[uu] = -INFINITY;
-            }
-        }
-    };
     f32x4 pv[kSum];
     float pm[kSum];
-    if (k.s < R) load_part(k.s, sg, pv, pm);
+    if (!kDefer && k.s < R) load_part<kSum>(a, k, k.s, sg, d4, pv, pm);
 
     if (tid < kRowCap) {
         float Mx = -INFINITY, Lx = 0.f;
@@ -540,48 +602,9 @@ __device__ __forceinline__ bool finish_chunk(const FusedArgs& fa, const Chunk& k
     }
 
     // ---- 4. rows s, s + nchunk, ... summed over the unit's chunks ----------
-    // A chunk's partial is relative to its maxima m: it enters with 2^(m - lse).
-    // Chunks are added in index order within eight interleaved groups, then
-    // the groups in order.
-    __syncthreads();   // the stash is free once every thread's scores are out
-    {
-        f32x4* red = reinterpret_cast<f32x4*>(stash);   // [8][32]
-        for (int row = k.s; row < R; row += nchunk) {
-            const float lse = row_lse[row];
-            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-            for (int s0 = sg; s0 < nchunk; s0 += kSum * 8) {
-                f32x4 v[kSum];
-                float m[kSum];
-                if (row == k.s && s0 == sg) {
-#pragma unroll
-                    for (int uu = 0; uu < kSum; ++uu) {
-                        v[uu] = pv[uu];
-                        m[uu] = pm[uu];
-                    }
-                } else {
-                    load_part(row, s0, v, m);
-                }
-#pragma unroll
-                for (int uu = 0; uu < kSum; ++uu) acc += v[uu] * fast_exp2(m[uu] - lse);
-            }
-            red[sg * 32 + d4] = acc;
-            __syncthreads();
-            if (sg == 0) {
-                f32x4 o = red[d4];
-#pragma unroll
-                for (int gq = 1; gq < 8; ++gq) o += red[gq * 32 + d4];
-                const int j = row / a.group;
-                const int h = k.c * a.group + (row - j * a.group);
-                const size_t base = (((size_t)k.b * a.max_q + j) * a.n_q_heads + h) * kHeadDim + 4 * d4;
-                if (a.out_fp32) {
-                    *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out) + base) = o;
-                } else {
-                    const uint2 pk = make_uint2(pack_bf16(o[0], o[1]), pack_bf16(o[2], o[3]));
-                    *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + base) = pk;
-                }
-            }
-            __syncthreads();
-        }
+    if constexpr (!kDefer) {
+        __syncthreads();   // the stash is free once every thread's scores are out
+        row_sums<kSum>(a, k, row_lse, reinterpret_cast<f32x4*>(stash), &pv, &pm);
     }
     return true;
 }
@@ -626,23 +649,31 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     // (decode step: the chunk's score bits also go to skeys, in the parking
     // slices, free once the partial output is out)
     uint32_t* skeys = reinterpret_cast<uint32_t*>(park);
-    if (!finish_chunk<NRT, StashF32, kStep>(fa, k, want, clean, stash, stride, mtile, mts, lse_part, row_lse,
-                                            &wait_failed, skeys))
+    // (decode step: the output rows are summed later, see below)
+    if (!finish_chunk<NRT, StashF32, kStep, 8, 4, kStep>(fa, k, want, clean, stash, stride, mtile, mts, lse_part,
+                                                         row_lse, &wait_failed, skeys))
         return;
     if constexpr (kStep) {
         // ---- 5. select (Eq. 4) and the first draft step (Eq. 5) ------------
+        // The verify output rows of the chunk are summed once its select
+        // histogram is out, while that exchange is in flight (rows summed
+        // first would hold up the unit's exchange for the chunks that have
+        // one), in 4 KB of LDS past the select's.
         const SelectArgs& sa = fa.sel;
         const Geom g = geom_of(sa, k.b);
         SelLds& SL = *reinterpret_cast<SelLds*>(stash);
+        f32x4* red = reinterpret_cast<f32x4*>(reinterpret_cast<char*>(stash) + kStepRedOffset);
+        auto sums = [&]() __attribute__((always_inline)) { row_sums<4>(a, k, row_lse, red, nullptr, nullptr); };
         const int nk = k.key_end - k.key_begin;
         bool done;
         if (g.simple) {
             __syncthreads();   // the stash becomes the select's
+            sums();
             done = select_simple<true>(sa, g, k.s, k.unit, SL, want);
         } else if (NRT > 1 || chunk <= kRound) {
-            done = step_select<1>(sa, g, k.s, k.unit, skeys, nk, k.key_begin, SL, want);
+            done = step_select<1>(sa, g, k.s, k.unit, skeys, nk, k.key_begin, SL, want, sums);
         } else {
-            done = step_select<NRT == 1 ? 2 : 1>(sa, g, k.s, k.unit, skeys, nk, k.key_begin, SL, want);
+            done = step_select<NRT == 1 ? 2 : 1>(sa, g, k.s, k.unit, skeys, nk, k.key_begin, SL, want, sums);
         }
         // chunk 0 goes on only when every exchange of the step completed
         if (!done) return;
@@ -777,7 +808,7 @@ hipError_t fused_setup(FusedDevice* out) {
     if (e != hipSuccess) return e;
     int st = dev >= 0 && dev < kMaxDevices ? state[dev].load(std::memory_order_relaxed) : 0;
     if (st == 0) {
-        const int lds = (int)std::max(fused_lds_bytes<NRT>(max_fused_chunk<NRT>()), sizeof(SelLds));
+        const int lds = (int)std::max(fused_lds_bytes<NRT>(max_fused_chunk<NRT>()), kStepLdsMin);
         const void* fns[6] = {reinterpret_cast<const void*>(verify_fused_kernel<NRT, true, false, false>),
                               reinterpret_cast<const void*>(verify_fused_kernel<NRT, false, false, false>),
                               reinterpret_cast<const void*>(verify_fused_kernel<NRT, true, true, false>),
@@ -837,7 +868,7 @@ hipError_t launch_fused_nrt(const FusedArgs& a, int n_slots, hipStream_t stream)
     // non-temporal K/V loads when every workgroup runs in the first round
     const bool stream1 = n_slots <= fd.n_cu;
     if (a.step) {   // (dense caches only; the host checks)
-        const size_t dyn = std::max(fused_lds_bytes<NRT>(a.v.chunk), sizeof(SelLds));
+        const size_t dyn = std::max(fused_lds_bytes<NRT>(a.v.chunk), kStepLdsMin);
         if (stream1)
             hipLaunchKernelGGL((verify_fused_kernel<NRT, true, false, true>), grid, block, dyn, stream, a);
         else
