@@ -8,8 +8,10 @@ B = 2048, four planted heavy-hitter keys per KV head).  Inputs are seeded and
 synthetic and already resident in HBM when timing starts.
 
 Every step reads a different copy of the KV cache (enough copies that each
-step's cache was last touched more than 512 MiB earlier), so the 256 MB
-Infinity Cache cannot serve it and the numbers are HBM numbers.
+step's cache was last touched more than 512 MiB earlier, and that the rows a
+draft gathers from a copy were last gathered more than 512 MiB of such rows
+earlier, up to 256 copies), so the 256 MB Infinity Cache cannot serve it and
+the numbers are HBM numbers.
 
 Prints one JSON line: µs per step (lower is better), per-call times from HIP
 events on the launch stream, the verify call against the HBM roofline, and the
@@ -42,6 +44,15 @@ def algorithmic_bytes(w, out_bytes: int):
     select = sum(hkv * t * 4 + hkv * nb * 4 for t, nb in zip(T, n)) + 4 * w.batch
     draft = sum(hkv * nb * (d * 2 * 2 + 4) for nb in n) + w.batch * hq * d * (2 + out_bytes)
     return {"verify": verify, "select": select, "draft": draft}, n
+
+
+def kv_copies(w, kv_bytes: int) -> int:
+    """KV copies to rotate: each call's cache bytes, and each draft's gathered
+    rows, last touched more than 512 MiB (twice the Infinity Cache) earlier;
+    at least 2, at most 256."""
+    draft = algorithmic_bytes(w, out_bytes=2)[0]["draft"]
+    need = max(math.ceil((512 << 20) / kv_bytes), math.ceil((512 << 20) / max(draft, 1))) + 1
+    return int(min(256, max(2, need)))
 
 
 REPO = os.path.dirname(os.path.abspath(__file__))
@@ -570,7 +581,7 @@ def workload_entry(B, n: int, steps: int, warmup: int, torch, np, cpu: bool):
     q, qd = up(w.q), up(w.q_draft)
     k0, v0 = up(w.k), up(w.v)
     kv_bytes = k0.numel() * 2 * 2
-    n_copies = max(2, math.ceil((512 << 20) / kv_bytes) + 1)
+    n_copies = kv_copies(w, kv_bytes)
     kvs = [(k0, v0)] + [(k0.clone(), v0.clone()) for _ in range(n_copies - 1)]
     params = B.make_params(w.sm_scale, window=w.window, k_sink=w.k_sink, k_recent=w.k_recent,
                            budget=w.budget, out_fp32=False)
@@ -716,7 +727,7 @@ def main() -> int:
     q, qd = up(w.q), up(w.q_draft)
     k0, v0 = up(w.k), up(w.v)
     kv_bytes = k0.numel() * 2 * 2
-    n_copies = max(2, math.ceil((512 << 20) / kv_bytes) + 1)
+    n_copies = kv_copies(w, kv_bytes)
     kvs = [(k0, v0)] + [(k0.clone(), v0.clone()) for _ in range(n_copies - 1)]
     vmode = {"auto": B.VERIFY_AUTO, "two-sweep": B.VERIFY_TWO_SWEEP,
              "one-sweep": B.VERIFY_ONE_SWEEP}[args.verify_mode]
