@@ -96,7 +96,7 @@ enum {
     SSL_OK = 0,
     SSL_ERR_NULL = -1,        /* a required pointer is NULL */
     SSL_ERR_SHAPE = -2,       /* inconsistent sizes (see each call) */
-    SSL_ERR_UNSUPPORTED = -3, /* valid request outside this build's limits */
+    SSL_ERR_UNSUPPORTED = -3, /* valid request outside the limits the library is built for */
     SSL_ERR_BUDGET = -4,      /* budget < 1, k_sink/k_recent < 0 or k_sink + k_recent > budget */
     SSL_ERR_ALIGN = -5,       /* device pointer not 16-byte (tensors) / 4-byte (int, fp32) aligned */
     SSL_ERR_WORKSPACE = -6,   /* workspace NULL or smaller than required */

@@ -26,7 +26,7 @@ CXX_SOURCES = ["api.cpp", "controller.cpp"]
 
 def source_id() -> str:
     """Hash of every source the library is built from (kernels, ABI, headers and
-    this build script); the library reports it through ssl_build_id()."""
+    the build script itself); the library reports it through ssl_build_id()."""
     import hashlib
     files = [os.path.join(CSRC, f) for f in sorted(os.listdir(CSRC))
              if f.endswith((".hip", ".cpp", ".h"))]
