@@ -137,9 +137,9 @@ typedef struct {
 
 /* How ssl_verify_attn schedules its work (results agree to rounding):
  *  AUTO       a one-sweep schedule where one fits and a KV head has at most
- *             32 verify rows, or 48 when its chunks run in one round of
- *             workgroups or the persistent form runs (their measured sweet
- *             spots), else the two-sweep one;
+ *             32 verify rows, or more when its chunks run in one round of
+ *             workgroups, or up to 48 when the persistent form runs (their
+ *             measured sweet spots), else the two-sweep one;
  *  TWO_SWEEP  a K-only pass for the row statistics, then a K+V pass;
  *  ONE_SWEEP  a single K+V pass whose chunks of one (sequence, KV head)
  *             exchange row statistics while resident together: one

@@ -338,15 +338,15 @@ int plan_verify(const ssl_shape* s, const ssl_params* p, const int32_t* ctx, con
 }
 
 // AUTO takes one sweep where it fits and a KV head has at most 32 verify rows,
-// or 48 when it runs in one round of workgroups or in the persistent form;
-// over several rounds at 33-48 rows (one wave per SIMD, logits of every row
-// in LDS) the one-workgroup-per-chunk kernel waits across rounds and two
-// sweeps are faster (70B shape: 457 vs 336 us), while in one round it wins
-// (44 rows at 16K: 26.1 vs 36.5 us; 48 rows at 8K: 21.8 vs 29.6 us).
+// or more when it runs in one round of workgroups or (up to 48 rows) in the
+// persistent form; over several rounds at 33-64 rows (one wave per SIMD,
+// logits of every row in LDS) the one-workgroup-per-chunk kernel waits
+// across rounds and two sweeps are faster (70B shape: 457 vs 336 us), while
+// in one round it wins (44 rows at 16K: 26.1 vs 36.5 us; 48 rows at 8K: 21.8
+// vs 29.6 us; 64 rows at 8K: 25.2 vs 34.0 us).
 bool use_one_sweep(const VerifyPlan& plan, const ssl_params* p) {
     if (!plan.fused_ok || p->verify_mode == SSL_VERIFY_TWO_SWEEP) return false;
-    return p->verify_mode == SSL_VERIFY_ONE_SWEEP || plan.row_tiles <= 2 || plan.pipe ||
-           (plan.row_tiles == 3 && plan.one_round);
+    return p->verify_mode == SSL_VERIFY_ONE_SWEEP || plan.row_tiles <= 2 || plan.pipe || plan.one_round;
 }
 
 struct DraftPlan {

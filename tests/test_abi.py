@@ -556,7 +556,7 @@ def test_persistent_plan_limits(lib, cu_budget):
 
 
 def test_auto_one_sweep_at_three_row_tiles_needs_one_round(lib, cu_budget):
-    """33-48 rows per KV head: AUTO takes the one-workgroup-per-chunk one sweep
+    """33-64 rows per KV head: AUTO takes the one-workgroup-per-chunk one sweep
     when its chunks run in one round of workgroups (44 rows at 16K: 256 chunks
     of 512 keys), the persistent form where that applies, and two sweeps where
     neither does (48 rows over 64K keys per head: 103 chunks of 640 keys)."""
@@ -570,8 +570,11 @@ def test_auto_one_sweep_at_three_row_tiles_needs_one_round(lib, cu_budget):
     assert B.verify_plan(s, p, ctx, ql)[0] == B.VERIFY_ONE_SWEEP_PERSISTENT
     s, p, ctx, ql = _plan_32k(rows_q=6, group=8, T=65536, batch=4)
     assert B.verify_plan(s, p, ctx, ql)[0] == B.VERIFY_TWO_SWEEP
-    # 64 rows (four row tiles) keep two sweeps even in one round
+    # 64 rows (four row tiles): one sweep in one round, else two sweeps (the
+    # persistent form is built for up to three row tiles)
     s, p, ctx, ql = _plan_32k(rows_q=16, group=4, T=4096)
+    assert B.verify_plan(s, p, ctx, ql)[0] == B.VERIFY_ONE_SWEEP
+    s, p, ctx, ql = _plan_32k(rows_q=8, group=8, T=32768)
     assert B.verify_plan(s, p, ctx, ql)[0] == B.VERIFY_TWO_SWEEP
 
 

@@ -39,8 +39,8 @@ def test_decode_step_bf16_outputs(name):
 
 # Shapes whose step runs as one kernel on the full device (every chunk
 # workgroup resident at once, chunks of >= 512 keys): ragged contexts with
-# ragged last chunks, ragged verify lengths, groups of 4, 8 and 16, two and
-# three row tiles.
+# ragged last chunks, ragged verify lengths, groups of 4, 8 and 16, two to
+# four row tiles.
 ONE_KERNEL = {
     "b2-kv8-ragged": lambda: generate(611, name="b2-kv8-ragged", batch=2, n_q_heads=32,
                                       n_kv_heads=8, ctx_len=[8192, 5000], q_len=[5, 3],
@@ -53,6 +53,9 @@ ONE_KERNEL = {
     # 44 rows per KV head: three row tiles, chunks of 512 keys in one round
     "b1-kv8-rows44": lambda: generate(615, name="b1-kv8-rows44", batch=1, n_q_heads=32, n_kv_heads=8,
                                       ctx_len=[16384], q_len=[11], budget=2048, heavy_hitters=4),
+    # 64 rows per KV head (group 8): four row tiles, chunks of 512 keys
+    "b1-kv8-rows64": lambda: generate(616, name="b1-kv8-rows64", batch=1, n_q_heads=64, n_kv_heads=8,
+                                      ctx_len=[16384], q_len=[8], budget=2048),
 }
 
 
