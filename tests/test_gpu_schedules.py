@@ -104,3 +104,28 @@ def test_verify_agrees_across_chunkings():
         assert np.all(np.abs(o - outs[0])[mask] <= 2 * (4e-3 * oabs[mask] + 1e-6))
     assert len(plans) >= 3   # several chunkings (and both schedules) were exercised
     assert B.exchange_status() == 0
+
+
+@pytest.mark.parametrize("ctx,cus,chunk", [([16384, 16379], 16, 16384), ([32768, 30000], 8, 32768)])
+def test_two_sweep_large_chunks(ctx, cus, chunk):
+    """Two sweeps over chunks of 16384 and 32768 keys (the chunk the plan takes
+    when a call's units outnumber the CUs: fewer rounds of workgroups), with a
+    ragged last chunk and a sequence shorter than one chunk, against the
+    oracle."""
+    w = generate(702, name="big-chunks", batch=2, n_q_heads=32, n_kv_heads=8, ctx_len=ctx,
+                 q_len=[7, 4], budget=512, heavy_hitters=4)
+    d = Dev(w)
+    B.set_cu_budget(cus)
+    p = B.make_params(w.sm_scale, window=w.window, verify_mode=B.VERIFY_TWO_SWEEP)
+    assert B.verify_plan(B.verify_shape(d.q, d.k), p, w.ctx_len, w.q_len)[:2] == (B.VERIFY_TWO_SWEEP, chunk)
+    o, s = gpu_verify(d, mode=B.VERIFY_TWO_SWEEP)
+    out_ref, s_ref = oracle.verify(w)
+    oabs, _ = oracle.verify(w, v=abs_v(w))
+    mask = np.arange(w.max_q)[None, :, None] < w.q_len[:, None, None] * np.ones((1, 1, w.n_q_heads), bool)
+    check_outputs(o, out_ref, oabs, mask, what=f"two sweeps, chunk {chunk}")
+    for b in range(w.batch):
+        T = int(w.ctx_len[b])
+        rel = np.abs(s[b, :, :T] - s_ref[b, :, :T]) / np.maximum(s_ref[b, :, :T], 1e-30)
+        assert np.all(rel[s_ref[b, :, :T] > 0] <= 1e-3)
+        assert np.all(s[b, :, T:] == -1.0)
+    assert B.exchange_status() == 0
