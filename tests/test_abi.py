@@ -627,3 +627,28 @@ def test_static_verify_validates_before_any_hip_call(lib):
     assert n.value > 128 << 20
     assert f(ctypes.byref(big), ctypes.byref(p), cbp, qbp, FAKE, FAKE, FAKE, FAKE, FAKE,
              None) == B.SSL_ERR_WORKSPACE
+
+
+def test_two_sweep_chunk_minimises_rounds(lib, cu_budget):
+    """The two-sweep chunk is the power of two in [128, 65536] that minimises
+    (rounds of one item per CU) x (chunk + 256 keys), the smallest on ties:
+    checked by brute force over random ragged shapes and CU budgets."""
+    import numpy as np
+    rng = np.random.default_rng(11)
+    for _ in range(60):
+        batch = int(rng.integers(1, 9))
+        hkv = int(rng.choice([1, 2, 4, 8]))
+        ctx = [int(x) for x in rng.integers(1, 200000, size=batch)]
+        ql = [1] * batch
+        n_cu = int(rng.choice([1, 3, 8, 64, 256]))
+        cu_budget(n_cu)
+        s = _shape(batch=batch, n_q_heads=hkv * 4, n_kv_heads=hkv, max_ctx=max(ctx), max_q=1)
+        p = _params(budget=64, verify_mode=B.VERIFY_TWO_SWEEP)
+        sch, chunk, items = B.verify_plan(s, p, ctx, ql)
+        best = None
+        for c in (128 << j for j in range(10)):
+            n = sum(hkv * -(-t // c) for t in ctx)
+            cost = -(-n // n_cu) * (c + 256)
+            if best is None or cost < best[0]:
+                best = (cost, c, n)
+        assert (sch, chunk, items) == (B.VERIFY_TWO_SWEEP, best[1], best[2]), (batch, hkv, ctx, n_cu)
