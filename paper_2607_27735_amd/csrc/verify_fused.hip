@@ -101,7 +101,7 @@ template <int NRT>
 constexpr int static_lds_bytes() {
     return kWaves * NRT * 16 * 8            // wml
            + kRowCap * 4                    // row_lse
-           + kWaves * kRowCap * 8           // lse_part
+           + kWaves * kRowCap * 8           // slack kept: the chunk limits below were tuned with it
            + 64;
 }
 
@@ -466,8 +466,7 @@ __device__ __forceinline__ void row_sums(const VerifyArgs& a, const Chunk& k, co
 template <int NRT, typename Codec, bool kStep, int kPoll = 8, int kSum = 4, bool kDefer = false>
 __device__ __forceinline__ bool finish_chunk(const FusedArgs& fa, const Chunk& k, uint64_t want,
                                              bool clean, typename Codec::T* stash, int stride,
-                                             const float* mtile, int mts,
-                                             float2 (*lse_part)[kRowCap], float* row_lse,
+                                             const float* mtile, int mts, float* row_lse,
                                              int* wait_failed, uint32_t* skeys) {
     const VerifyArgs& a = fa.v;
     const int tid = threadIdx.x, lane = tid & 63;
@@ -476,47 +475,55 @@ __device__ __forceinline__ bool finish_chunk(const FusedArgs& fa, const Chunk& k
     const uint64_t* ml64 = reinterpret_cast<const uint64_t*>(a.part_ml);   // [slot][kRowCap][2]
 
     // ---- 3a. exact row statistics over every chunk of the head -------------
-    // Wave w polls rows 0..63 of chunks w, w + 4, ... (eight chunks per
-    // round trip) until all their words carry the tag, then merges them.
-    // (One poll in flight per wave: two, issued half a round trip apart, load
-    // the memory system enough to cost more than the earlier sight gains.)
+    // Wave w takes rows 16 w .. 16 w + 15 (those below R): lane (c4, r16)
+    // polls row 16 w + r16 of chunks c4, c4 + 4, ... (kPoll of them per round
+    // trip) until all their words carry the tag, merges them, and the four
+    // chunk groups are merged across lanes, so each row's normalizer is
+    // formed in the wave that polled it.  (One poll in flight per wave: two,
+    // issued half a round trip apart, load the memory system enough to cost
+    // more than the earlier sight gains.)
     {
-        const int rr = tid & (kRowCap - 1), ph = tid >> 6;
+        const int ph = tid >> 6, r16 = lane & 15, c4 = lane >> 4;
+        const int row = ph * 16 + r16;
         float Mx = -INFINITY, Lx = 0.f;
         bool in_all = clean;
-        for (int s0 = ph; in_all && s0 < nchunk; s0 += kPoll * kWaves) {   // wave-uniform
-            uint64_t w0[kPoll], w1[kPoll];
-            // every lane loads (lanes past the rows or chunks re-read valid
-            // entries): no branch around the loads
-            const uint64_t* e[kPoll];
+        if (ph * 16 < R) {   // wave-uniform
+            for (int b0 = 0; in_all && b0 < nchunk; b0 += kPoll * 4) {   // wave-uniform
+                uint64_t w0[kPoll], w1[kPoll];
+                // every lane loads (lanes past the rows or chunks re-read valid
+                // entries): no branch around the loads
+                const uint64_t* e[kPoll];
 #pragma unroll
-            for (int uu = 0; uu < kPoll; ++uu)
-                e[uu] = ml64 + ((size_t)(slot0 + min(s0 + uu * kWaves, nchunk - 1)) * kRowCap + min(rr, R - 1)) * 2;
-            int spins = 0;
-            bool all_in;
-            do {
-                bool in = true;
+                for (int uu = 0; uu < kPoll; ++uu)
+                    e[uu] = ml64 + ((size_t)(slot0 + min(b0 + c4 + 4 * uu, nchunk - 1)) * kRowCap + min(row, R - 1)) * 2;
+                int spins = 0;
+                bool all_in;
+                do {
+                    bool in = true;
 #pragma unroll
-                for (int uu = 0; uu < kPoll; ++uu) {
-                    w0[uu] = ld_dev64(e[uu]);
-                    w1[uu] = ld_dev64(e[uu] + 1);
+                    for (int uu = 0; uu < kPoll; ++uu) {
+                        w0[uu] = ld_dev64(e[uu]);
+                        w1[uu] = ld_dev64(e[uu] + 1);
+                    }
+#pragma unroll
+                    for (int uu = 0; uu < kPoll; ++uu)
+                        in &= ((w0[uu] & ~0xFFFFFFFFull) == tag_hi && (w1[uu] & ~0xFFFFFFFFull) == tag_hi);
+                    all_in = __all(in);
+                    if (!all_in) __builtin_amdgcn_s_sleep(1);
+                } while (!all_in && ++spins < fa.xc.spin_limit);
+                in_all = all_in;
+                if (all_in && row < R) {
+#pragma unroll
+                    for (int uu = 0; uu < kPoll; ++uu)
+                        if (b0 + c4 + 4 * uu < nchunk)
+                            ml_merge(Mx, Lx, __uint_as_float((uint32_t)w0[uu]), __uint_as_float((uint32_t)w1[uu]));
                 }
-#pragma unroll
-                for (int uu = 0; uu < kPoll; ++uu)
-                    in &= ((w0[uu] & ~0xFFFFFFFFull) == tag_hi && (w1[uu] & ~0xFFFFFFFFull) == tag_hi);
-                all_in = __all(in);
-                if (!all_in) __builtin_amdgcn_s_sleep(1);
-            } while (!all_in && ++spins < fa.xc.spin_limit);
-            in_all = all_in;
-            if (all_in && rr < R) {
-#pragma unroll
-                for (int uu = 0; uu < kPoll; ++uu)
-                    if (s0 + uu * kWaves < nchunk)
-                        ml_merge(Mx, Lx, __uint_as_float((uint32_t)w0[uu]), __uint_as_float((uint32_t)w1[uu]));
             }
+            ml_merge(Mx, Lx, shfl_xor_f(Mx, 16), shfl_xor_f(Lx, 16));
+            ml_merge(Mx, Lx, shfl_xor_f(Mx, 32), shfl_xor_f(Lx, 32));
+            if (c4 == 0 && row < R) row_lse[row] = Lx > 0.f ? Mx + fast_log2(Lx) : INFINITY;
         }
         if (!in_all && lane == 0) *wait_failed = 1;
-        lse_part[ph][rr] = make_float2(Mx, Lx);
     }
     __syncthreads();
     if (*wait_failed) {
@@ -525,20 +532,13 @@ __device__ __forceinline__ bool finish_chunk(const FusedArgs& fa, const Chunk& k
     }
 
     // The first chunks of this workgroup's first row in step 4 (all of them
-    // for up to 32 chunks), loaded now so that the round trip overlaps the
-    // normalizers and 3b (kDefer: step 4 is left to the caller).
+    // for up to 32 chunks), loaded now so that the round trip overlaps 3b
+    // (kDefer: step 4 is left to the caller).
     const int d4 = tid & 31, sg = tid >> 5;
     f32x4 pv[kSum];
     float pm[kSum];
     if (!kDefer && k.s < R) load_part<kSum>(a, k, k.s, sg, d4, pv, pm);
 
-    if (tid < kRowCap) {
-        float Mx = -INFINITY, Lx = 0.f;
-#pragma unroll
-        for (int w = 0; w < kWaves; ++w) ml_merge(Mx, Lx, lse_part[w][tid].x, lse_part[w][tid].y);
-        row_lse[tid] = Lx > 0.f ? Mx + fast_log2(Lx) : INFINITY;
-    }
-    __syncthreads();
     const int nk = k.key_end - k.key_begin;
 
     // ---- 3b. scores of this chunk's keys from the stashed probabilities ----
@@ -626,7 +626,6 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     extern __shared__ __attribute__((aligned(16))) float stash[];   // [NRT*16][chunk + pad]
     __shared__ float2 wml[kWaves][NRT * 16];
     __shared__ float row_lse[kRowCap];
-    __shared__ float2 lse_part[kWaves][kRowCap];
     __shared__ int wait_failed;
 
     const Chunk k = chunk_of(a, blockIdx.x);
@@ -650,7 +649,7 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(FusedArgs fa) {
     // slices, free once the partial output is out)
     uint32_t* skeys = reinterpret_cast<uint32_t*>(park);
     // (decode step: the output rows are summed later, see below)
-    if (!finish_chunk<NRT, StashF32, kStep, 8, 4, kStep>(fa, k, want, clean, stash, stride, mtile, mts, lse_part,
+    if (!finish_chunk<NRT, StashF32, kStep, 8, 4, kStep>(fa, k, want, clean, stash, stride, mtile, mts,
                                                          row_lse, &wait_failed, skeys))
         return;
     if constexpr (kStep) {
@@ -703,7 +702,6 @@ __global__ __launch_bounds__(kThreads) void verify_pipe_kernel(FusedArgs fa) {
     extern __shared__ __attribute__((aligned(16))) float lds[];
     __shared__ float2 wml[kWaves][NRT * 16];
     __shared__ float row_lse[kRowCap];
-    __shared__ float2 lse_part[kWaves][kRowCap];
     __shared__ int wait_failed;
 
     const int chunk = a.chunk;
@@ -739,7 +737,7 @@ __global__ __launch_bounds__(kThreads) void verify_pipe_kernel(FusedArgs fa) {
             }
             if (j >= 2) {   // chunk j - 2's stash: buffer (j - 2) & 1 = j & 1
                 if (finish_chunk<NRT, Codec, false, kPipePoll, kPipeSum>(fa, k2, want2, clean2, codes(j), stride,
-                                                                         tiles(j), mts, lse_part, row_lse,
+                                                                         tiles(j), mts, row_lse,
                                                                          &wait_failed, nullptr))
                     chunk0_done(fa, k2);
                 else
@@ -755,12 +753,12 @@ __global__ __launch_bounds__(kThreads) void verify_pipe_kernel(FusedArgs fa) {
     want1 = publish_chunk<NRT>(fa, k1, M, L, oacc, wml, park, &wait_failed, &clean1);
     if (n >= 2) {
         if (!finish_chunk<NRT, Codec, false, kPipePoll, kPipeSum>(fa, k2, want2, clean2, codes(n), stride, tiles(n),
-                                                                  mts, lse_part, row_lse, &wait_failed, nullptr))
+                                                                  mts, row_lse, &wait_failed, nullptr))
             return;
         chunk0_done(fa, k2);
     }
     if (!finish_chunk<NRT, Codec, false, kPipePoll, kPipeSum>(fa, k1, want1, clean1, codes(n - 1), stride,
-                                                              tiles(n - 1), mts, lse_part, row_lse, &wait_failed,
+                                                              tiles(n - 1), mts, row_lse, &wait_failed,
                                                               nullptr))
         return;
     chunk0_done(fa, k1);
